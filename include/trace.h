@@ -1,0 +1,170 @@
+/*
+ * trace.h -- C ABI of libtrace: the batched next-byte estimator of TRACE
+ * (Mao et al., "A Fast Transformer-based General-Purpose Lossless Compressor",
+ * arXiv 2203.16114) and its controller-gated online update, on one AMD
+ * Instinct MI355X (gfx950).
+ *
+ * The paper states the problem as three model calls inside its dynamic
+ * compression loop (Sec. 3.2, Algorithm 1): Model.initialize(), the forward
+ * estimate P(x_i | x_{i-c} .. x_{i-1}) and Model.backward on the byte just
+ * coded; and one controller call that turns the step's cross-entropy into a
+ * back-propagate / skip decision (Sec. 4.4, Algorithm 2, Eq. 7).  The entry
+ * points below are those calls for B independent byte streams at once.
+ *
+ * Conventions for every call:
+ *   - the return value is 0 (TRACE_OK) or a negative TRACE_E* code; nothing
+ *     throws across the ABI; trace_last_error() describes the last failure of
+ *     the calling thread;
+ *   - "device pointer" means memory on the HIP device the model was created
+ *     on; "host pointer" means ordinary CPU memory;
+ *   - buffers passed in are owned by the caller and are never freed or kept
+ *     by the library past the call, except where stated;
+ *   - GPU work is enqueued on the caller's stream (a hipStream_t passed as
+ *     void*; NULL is the legacy default stream) and is asynchronous unless the
+ *     call says it synchronises; argument errors are reported synchronously,
+ *     before anything is enqueued; launch failures come back as TRACE_EHIP;
+ *   - one model is used by one host thread at a time.
+ */
+#ifndef TRACE_H
+#define TRACE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  TRACE_OK = 0,
+  TRACE_EINVAL = -1,       /* bad argument or configuration                     */
+  TRACE_ENOMEM = -2,       /* device or host allocation failed                  */
+  TRACE_EHIP = -3,         /* a HIP runtime call or kernel launch failed        */
+  TRACE_ESTATE = -4,       /* call out of order (e.g. adapt with no kept batch) */
+  TRACE_ENONFINITE = -5,   /* a NaN/Inf cross-entropy reached the controller    */
+  TRACE_EUNSUPPORTED = -6  /* shape valid but no kernel is built for it         */
+};
+
+enum { TRACE_FP32 = 0, TRACE_BF16 = 1 };  /* BF16: fp32 master + bf16 operand copies */
+enum { TRACE_KEEP_ACTS = 1u };
+
+/* Model shape and optimiser settings.
+ *   W        window bytes, the c*g bytes before the target (Sec. 4.2; Alg. 1 line 8)
+ *   e        per-byte embedding width h/g (Sec. 4.2)
+ *   g        bytes per group; T = W/g tokens of width d = g*e (Sec. 4.2, Fig. 4b)
+ *   H        attention heads, head width d/H (Eqs. 1-2)
+ *   F        FFN width (Eq. 3)
+ *   k        shared-FFN repeats N (Sec. 4.3, Fig. 4c)
+ *   dtype    TRACE_FP32: every GEMM operand in fp32; TRACE_BF16: GEMM operands
+ *            (weights and activations) rounded to bf16 (RNE), fp32 accumulate,
+ *            fp32 residual stream, softmax, code lengths, master weights, Adam
+ *   use_pos  1: a learned positional table P[T][d] is added after grouping
+ *   max_windows  windows per internal forward chunk (workspace size); a
+ *            forward over more windows runs in chunks, with identical results
+ *   max_keep windows a KEEP_ACTS forward may hold for trace_adapt_step
+ *            (0: the model cannot adapt)
+ *   lr, beta1, beta2, eps  Adam (Sec. 6 uses lr 0.001)
+ * Supported shapes: W % g == 0, d % H == 0, T in {4, 8}, d/H in {32, 64},
+ * d in {64, 128, 256, 512} (a multiple of 64), e % 8 == 0, F % 256 == 0,
+ * 1 <= k <= 8.  Others return TRACE_EINVAL or TRACE_EUNSUPPORTED. */
+typedef struct {
+  int32_t W, e, g, H, F, k;
+  int32_t dtype;
+  int32_t use_pos;
+  int64_t max_windows;
+  int64_t max_keep;
+  double lr, beta1, beta2, eps; /* used as float, except beta^t in double for the bias corrections */
+} trace_config;
+
+typedef struct trace_model trace_model; /* opaque, library-owned */
+
+/* Allocates a model on the current HIP device: fp32 master parameters in the
+ * canonical flat order E[256][e], P[T][d], Wq, Wk, Wv, Wo [d][d], W1 [d][F],
+ * W2 [F][d], Wout [d][256], bout [256] (every matrix row-major [in][out]),
+ * Adam moments, operand copies and workspace.  Parameters start at zero until
+ * trace_init_weights.  EINVAL for an invalid config, EUNSUPPORTED for a shape
+ * with no kernel, ENOMEM if device memory runs out.  *out is NULL on error. */
+int trace_create(const trace_config* cfg, trace_model** out);
+void trace_destroy(trace_model* m); /* NULL is a no-op; synchronises the device */
+
+/* Number of parameters (flat master length) of a configuration; host only. */
+int trace_param_count(const trace_config* cfg, int64_t* n);
+
+/* Model.initialize() of Alg. 1: the dynamic setting starts from a random
+ * model (Sec. 3.2, Sec. 5 "Dynamic-Random").  With host_flat == NULL every
+ * entry of E, P, Wq .. Wout is std * N(0, 1), drawn in flat order by
+ * Box-Muller (cos, then sin) from splitmix64 uniforms ((x >> 11) + 0.5) * 2^-53
+ * seeded with `seed`, computed in double and rounded to float; bout = 0.
+ * With host_flat != NULL (a host array of trace_param_count floats) it is
+ * copied instead.  Resets Adam (m = v = 0, step count 0) and drops any kept
+ * batch.  Synchronises the device. */
+int trace_init_weights(trace_model* m, uint64_t seed, double std, const float* host_flat);
+
+/* The same generator into a host array of n = trace_param_count floats,
+ * without a model or a GPU. */
+int trace_init_flat_host(const trace_config* cfg, uint64_t seed, double std, float* host_out, int64_t n);
+
+/* Model.forward of Alg. 1 line 8 for many streams and steps at once, with the
+ * code length of Alg. 2 line 3.  Window (b, s), b < n_streams, s < n_steps,
+ * is d_streams[b*stride + pos0 + s - W .. b*stride + pos0 + s - 1] (oldest
+ * first) and its target is the byte d_streams[b*stride + pos0 + s]; requires
+ * pos0 >= W.  Writes
+ *   d_bits[b*n_steps + s]            = -log2 p(target)            (device, fp32)
+ *   d_logits[(b*n_steps + s)*256+v]  = head output z_v            (device, fp32; optional)
+ *   d_step_ce[s] = mean over b of d_bits[b*n_steps + s]           (device, fp64; optional)
+ * The byte-grouped single-layer transformer is: tokens by byte grouping
+ * (Sec. 4.2), causal multi-head attention (Eqs. 1-2), the layer of Eq. 4 with
+ * its FFN (Eq. 3) shared and applied k times (Sec. 4.3), and a 256-way softmax
+ * head reading the last token.  flags may hold TRACE_KEEP_ACTS: the call then
+ * also keeps the activations of these n_streams*n_steps <= max_keep windows
+ * for trace_adapt_step.  Results depend only on each window's bytes and the
+ * weights (not on n_streams, n_steps, chunking or position in the batch). */
+int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams,
+                       int64_t pos0, int32_t n_steps, float* d_bits, float* d_logits,
+                       double* d_step_ce, uint32_t flags, void* stream);
+
+/* Model.backward of Alg. 1 line 10 on the batch kept by the last
+ * KEEP_ACTS forward: the gradient of the batch-mean cross-entropy (nats)
+ * followed by one Adam step (Kingma & Ba, Alg. 1; bias-corrected; the step
+ * count advances once per call) on the fp32 master, then a refresh of the
+ * operand copies.  The kept batch is consumed.  ESTATE if none is kept. */
+int trace_adapt_step(trace_model* m, void* stream);
+
+/* The back-prop controller of Sec. 4.4 (Algorithm 2, uniform weights, Eq. 7):
+ * a FIFO loss cache of the last t step cross-entropies (bits) and their sum.
+ * decide(e) sets *update = 1 (back-propagate) iff fewer than t values are
+ * cached yet, or e > sum/t + delta in IEEE double; then the oldest value
+ * leaves a full cache and e enters it, whatever the decision.  Host only,
+ * O(1), no GPU.  A non-finite e returns ENONFINITE with *update = 0 and leaves
+ * the cache unchanged. */
+typedef struct {
+  int32_t t, count, head, pad_;
+  double delta, sum;
+  double ring[256];
+} trace_controller;
+int trace_controller_init(trace_controller* c, int32_t t, double delta); /* 1 <= t <= 256 */
+int trace_controller_decide(trace_controller* c, double batch_ce_bits, int32_t* update);
+
+/* Copies of the training state (host arrays of trace_param_count floats each;
+ * any pointer may be NULL to skip it).  get synchronises the device; set also
+ * refreshes the operand copies and drops any kept batch. */
+int trace_get_state(trace_model* m, float* theta, float* adam_m, float* adam_v, int64_t* step, int64_t n);
+int trace_set_state(trace_model* m, const float* theta, const float* adam_m, const float* adam_v, int64_t step,
+                    int64_t n);
+
+/* Gradient (flat, canonical order) computed by the last trace_adapt_step,
+ * copied to a host array of trace_param_count floats; synchronises. */
+int trace_get_grads(trace_model* m, float* host_out, int64_t n);
+
+/* Byte-group gather alone (Sec. 4.2): writes the operand values of the
+ * tokens, d_X[((b*n_steps + s)*T + t)*d + c] (device, fp32; in BF16 mode the
+ * bf16-rounded value), for the windows defined as in trace_forward_bits. */
+int trace_debug_gather(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams, int64_t pos0,
+                       int32_t n_steps, float* d_X, void* stream);
+
+const char* trace_strerror(int code);
+const char* trace_last_error(void); /* thread-local text of the last failure ("" if none) */
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* TRACE_H */

@@ -1,0 +1,223 @@
+"""Python binding of libtrace: TRACE's batched next-byte estimator and its
+controller-gated online update on one MI355X (gfx950).
+
+This module only marshals arguments for the C ABI declared in include/trace.h;
+every step of the estimator runs in the HIP kernels of libtrace.so.  PyTorch
+supplies device memory and the current stream.  There is no fallback: if the
+library is missing, loading it raises.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from ctypes import POINTER, byref, c_double, c_float, c_int32, c_int64, c_uint32, c_uint64, c_void_p
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libtrace.so")
+
+TRACE_OK, TRACE_EINVAL, TRACE_ENOMEM, TRACE_EHIP, TRACE_ESTATE, TRACE_ENONFINITE, TRACE_EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
+TRACE_FP32, TRACE_BF16 = 0, 1
+TRACE_KEEP_ACTS = 1
+
+EXPORTS = ("trace_create", "trace_destroy", "trace_param_count", "trace_init_weights", "trace_init_flat_host",
+           "trace_forward_bits", "trace_adapt_step", "trace_controller_init", "trace_controller_decide",
+           "trace_get_state", "trace_set_state", "trace_get_grads", "trace_debug_gather", "trace_strerror",
+           "trace_last_error")
+
+
+class TraceError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{msg} (code {code})")
+        self.code = code
+
+
+class TraceConfig(ctypes.Structure):
+    _fields_ = [("W", c_int32), ("e", c_int32), ("g", c_int32), ("H", c_int32), ("F", c_int32), ("k", c_int32),
+                ("dtype", c_int32), ("use_pos", c_int32), ("max_windows", c_int64), ("max_keep", c_int64),
+                ("lr", c_double), ("beta1", c_double), ("beta2", c_double), ("eps", c_double)]
+
+
+class TraceControllerState(ctypes.Structure):
+    _fields_ = [("t", c_int32), ("count", c_int32), ("head", c_int32), ("pad_", c_int32),
+                ("delta", c_double), ("sum", c_double), ("ring", c_double * 256)]
+
+
+_lib = None
+
+
+def lib():
+    """Loads libtrace.so (built by build.py); raises if it is missing."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
+                              "or python paper_2203_16114_amd/build.py")
+        L = ctypes.CDLL(LIB_PATH)
+        P = c_void_p
+        sig = {
+            "trace_create": (c_int32, [POINTER(TraceConfig), POINTER(c_void_p)]),
+            "trace_destroy": (None, [P]),
+            "trace_param_count": (c_int32, [POINTER(TraceConfig), POINTER(c_int64)]),
+            "trace_init_weights": (c_int32, [P, c_uint64, c_double, P]),
+            "trace_init_flat_host": (c_int32, [POINTER(TraceConfig), c_uint64, c_double, P, c_int64]),
+            "trace_forward_bits": (c_int32, [P, P, c_int64, c_int32, c_int64, c_int32, P, P, P, c_uint32, P]),
+            "trace_adapt_step": (c_int32, [P, P]),
+            "trace_controller_init": (c_int32, [POINTER(TraceControllerState), c_int32, c_double]),
+            "trace_controller_decide": (c_int32, [POINTER(TraceControllerState), c_double, POINTER(c_int32)]),
+            "trace_get_state": (c_int32, [P, P, P, P, POINTER(c_int64), c_int64]),
+            "trace_set_state": (c_int32, [P, P, P, P, c_int64, c_int64]),
+            "trace_get_grads": (c_int32, [P, P, c_int64]),
+            "trace_debug_gather": (c_int32, [P, P, c_int64, c_int32, c_int64, c_int32, P, P]),
+            "trace_strerror": (ctypes.c_char_p, [c_int32]),
+            "trace_last_error": (ctypes.c_char_p, []),
+        }
+        for name, (res, args) in sig.items():
+            f = getattr(L, name)
+            f.restype = res
+            f.argtypes = args
+        _lib = L
+    return _lib
+
+
+def check(rc: int):
+    if rc != TRACE_OK:
+        L = lib()
+        raise TraceError(rc, f"{L.trace_strerror(rc).decode()}: {L.trace_last_error().decode()}")
+
+
+def make_config(W, e, g, H, F, k, dtype="fp32", use_pos=True, max_windows=1 << 16, max_keep=0,
+                lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8) -> TraceConfig:
+    dt = {"fp32": TRACE_FP32, "bf16": TRACE_BF16}[dtype] if isinstance(dtype, str) else int(dtype)
+    return TraceConfig(W, e, g, H, F, k, dt, int(bool(use_pos)), int(max_windows), int(max_keep),
+                       float(lr), float(beta1), float(beta2), float(eps))
+
+
+def param_count(cfg: TraceConfig) -> int:
+    n = c_int64()
+    check(lib().trace_param_count(byref(cfg), byref(n)))
+    return n.value
+
+
+def init_flat_host(cfg: TraceConfig, seed: int, std: float = 0.02) -> np.ndarray:
+    out = np.empty(param_count(cfg), np.float32)
+    check(lib().trace_init_flat_host(byref(cfg), c_uint64(seed & ((1 << 64) - 1)), float(std),
+                                     out.ctypes.data, out.size))
+    return out
+
+
+class Controller:
+    """The back-prop controller (host only; see trace_controller_decide)."""
+
+    def __init__(self, t: int = 16, delta: float = 0.05):
+        self.state = TraceControllerState()
+        check(lib().trace_controller_init(byref(self.state), int(t), float(delta)))
+
+    def decide(self, e: float) -> int:
+        u = c_int32()
+        check(lib().trace_controller_decide(byref(self.state), float(e), byref(u)))
+        return u.value
+
+
+def _stream_ptr(stream=None):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return c_void_p(s.cuda_stream)
+
+
+def _dptr(t):
+    return c_void_p(t.data_ptr()) if t is not None else None
+
+
+class TraceModel:
+    """One model on the current HIP device (see include/trace.h)."""
+
+    def __init__(self, W, e, g, H, F, k, dtype="fp32", use_pos=True, max_windows=1 << 16, max_keep=0,
+                 lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8):
+        self.cfg = make_config(W, e, g, H, F, k, dtype, use_pos, max_windows, max_keep, lr, beta1, beta2, eps)
+        self.W, self.e, self.g, self.H, self.F, self.k = W, e, g, H, F, k
+        self.T, self.d = W // g, g * e
+        self.dtype = dtype
+        self.n_params = param_count(self.cfg)
+        h = c_void_p()
+        check(lib().trace_create(byref(self.cfg), byref(h)))
+        self._h = h
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib().trace_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def init_weights(self, seed: int, std: float = 0.02, flat: np.ndarray | None = None):
+        if flat is not None:
+            flat = np.ascontiguousarray(flat, np.float32)
+            if flat.size != self.n_params:
+                raise ValueError("flat has the wrong length")
+        check(lib().trace_init_weights(self._h, c_uint64(seed & ((1 << 64) - 1)), float(std),
+                                       None if flat is None else flat.ctypes.data))
+
+    def forward_bits(self, streams, pos0: int, n_steps: int, bits=None, logits=None, step_ce=None,
+                     keep: bool = False, n_streams: int | None = None, stride: int | None = None, stream=None):
+        """streams: uint8 CUDA tensor [B][L] (row stride = L) or flat with n_streams/stride given.
+        bits/logits/step_ce: preallocated CUDA tensors, or True to allocate (logits, step_ce)."""
+        import torch
+        if streams.dtype != torch.uint8 or not streams.is_cuda:
+            raise TypeError("streams must be a uint8 CUDA tensor")
+        if n_streams is None:
+            if streams.dim() != 2 or not streams.is_contiguous():
+                raise ValueError("streams must be a contiguous [B][L] tensor, or give n_streams and stride")
+            n_streams, stride = streams.shape[0], streams.shape[1]
+        dev = streams.device
+        N = n_streams * n_steps
+        if bits is None:
+            bits = torch.empty(N, dtype=torch.float32, device=dev)
+        if logits is True:
+            logits = torch.empty(N, 256, dtype=torch.float32, device=dev)
+        if step_ce is True:
+            step_ce = torch.empty(n_steps, dtype=torch.float64, device=dev)
+        for t, n in ((bits, N), (logits, N * 256), (step_ce, n_steps)):
+            if t is not None and (not t.is_cuda or not t.is_contiguous() or t.numel() < n):
+                raise ValueError("output buffers must be contiguous CUDA tensors of the right size")
+        check(lib().trace_forward_bits(self._h, _dptr(streams), int(stride), int(n_streams), int(pos0), int(n_steps),
+                                       _dptr(bits), _dptr(logits) if logits is not None else None,
+                                       _dptr(step_ce) if step_ce is not None else None,
+                                       TRACE_KEEP_ACTS if keep else 0, _stream_ptr(stream)))
+        return {"bits": bits, "logits": logits, "step_ce": step_ce}
+
+    def adapt_step(self, stream=None):
+        check(lib().trace_adapt_step(self._h, _stream_ptr(stream)))
+
+    def get_state(self):
+        n = self.n_params
+        th, m, v = (np.empty(n, np.float32) for _ in range(3))
+        step = c_int64()
+        check(lib().trace_get_state(self._h, th.ctypes.data, m.ctypes.data, v.ctypes.data, byref(step), n))
+        return th, m, v, step.value
+
+    def set_state(self, theta, adam_m=None, adam_v=None, step: int = 0):
+        n = self.n_params
+        arrs = [None if a is None else np.ascontiguousarray(a, np.float32) for a in (theta, adam_m, adam_v)]
+        for a in arrs:
+            if a is not None and a.size != n:
+                raise ValueError("state arrays must have trace_param_count entries")
+        check(lib().trace_set_state(self._h, *[None if a is None else a.ctypes.data for a in arrs], int(step), n))
+
+    def grads(self) -> np.ndarray:
+        out = np.empty(self.n_params, np.float32)
+        check(lib().trace_get_grads(self._h, out.ctypes.data, self.n_params))
+        return out
+
+    def debug_gather(self, streams, pos0: int, n_steps: int, stream=None):
+        import torch
+        B, L = streams.shape
+        X = torch.empty(B * n_steps, self.T, self.d, dtype=torch.float32, device=streams.device)
+        check(lib().trace_debug_gather(self._h, _dptr(streams), L, B, int(pos0), int(n_steps), _dptr(X),
+                                       _stream_ptr(stream)))
+        return X

@@ -1,0 +1,431 @@
+// C ABI of libtrace (include/trace.h): device memory, operand copies and the
+// launch sequence of the forward estimator and of the gated update.
+#include <hip/hip_runtime_api.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/trace.h"
+#include "host.h"
+#include "kernels.h"
+
+struct trace_model {
+  trace_config cfg;
+  Layout L;
+  bool bf;
+  int device;
+  attn_fn attn;
+  ffn_fn ffn;
+  int64_t max_windows, max_keep;
+  // fp32 master, Adam moments, gradient (canonical flat order)
+  float *theta, *am, *av, *grad;
+  int64_t step;
+  // operand copies
+  void *Ec, *Pc;
+  uint4 *Wq, *Wk, *Wv, *Wo, *W1, *W2, *Wout;
+  // forward workspace
+  float* h0;
+  // kept batch
+  bool kept;
+  int64_t keepN;
+  uint8_t* kwin;
+  int32_t* ktgt;
+  float *kq, *kK, *kV, *kA, *kO, *kY, *kU, *kZ;
+  // backward scratch
+  float *dz, *dY, *dG, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *gws, *cws;
+  int64_t gws_cap;
+  std::vector<void*> allocs;
+};
+
+namespace {
+
+int fail(int code, const std::string& msg) {
+  trace_set_error(msg);
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* where) {
+  return fail(TRACE_EHIP, std::string(where) + ": " + hipGetErrorString(e));
+}
+
+template <typename P>
+bool dalloc(trace_model* m, P** p, int64_t bytes) {
+  void* q = nullptr;
+  if (bytes <= 0) bytes = 16;
+  if (hipMalloc(&q, (size_t)bytes) != hipSuccess) {
+    *p = nullptr;
+    return false;
+  }
+  m->allocs.push_back(q);
+  *p = (P*)q;
+  return true;
+}
+
+void free_all(trace_model* m) {
+  for (void* p : m->allocs) (void)hipFree(p);
+  m->allocs.clear();
+}
+
+// Largest split-K workspace over the GEMMs of trace_adapt_step.
+int64_t adapt_gemm_ws(const trace_model* m, int64_t N) {
+  const int D = m->L.D, F = m->cfg.F, T = m->L.T;
+  const int n = (int)N;
+  const int shapes[][3] = {{D, 256, n}, {n, D, 256}, {F, D, n}, {n, F, D}, {D, F, n}, {n, D, F}, {D, D, n},
+                           {n, D, D},   {D, D, n * T}, {n * T, D, D}};
+  int64_t w = 0;
+  for (auto& s : shapes) w = std::max(w, gemm_ws_floats(s[0], s[1], s[2]));
+  return w;
+}
+
+hipStream_t S(void* s) { return (hipStream_t)s; }
+
+// Refresh the operand copies from the fp32 master.
+void refresh_operands(trace_model* m, hipStream_t s) {
+  const Layout& L = m->L;
+  const int D = L.D, F = m->cfg.F;
+  const float* th = m->theta;
+  launch_cvt(m->bf, th + L.off[P_E], m->Ec, L.size[P_E], s);
+  if (m->cfg.use_pos)
+    launch_cvt(m->bf, th + L.off[P_P], m->Pc, L.size[P_P], s);
+  else
+    launch_zero(m->Pc, (L.size[P_P] * (m->bf ? 2 : 4) + 3) / 4, s);
+  launch_pack(m->bf, th + L.off[P_WQ], D, D, m->Wq, s);
+  launch_pack(m->bf, th + L.off[P_WK], D, D, m->Wk, s);
+  launch_pack(m->bf, th + L.off[P_WV], D, D, m->Wv, s);
+  launch_pack(m->bf, th + L.off[P_WO], D, D, m->Wo, s);
+  launch_pack(m->bf, th + L.off[P_W1], D, F, m->W1, s);
+  launch_pack(m->bf, th + L.off[P_W2], F, D, m->W2, s);
+  launch_pack(m->bf, th + L.off[P_WOUT], D, 256, m->Wout, s);
+}
+
+GemmArgs gemm(int M, int N, int K, const float* A, int64_t sam, int64_t sak, int rA, const float* B, int64_t sbk,
+              int64_t sbn, int rB, float* C, int64_t ldc, float beta) {
+  GemmArgs g;
+  g.M = M;
+  g.N = N;
+  g.K = K;
+  g.A = A;
+  g.sam = sam;
+  g.sak = sak;
+  g.B = B;
+  g.sbk = sbk;
+  g.sbn = sbn;
+  g.C = C;
+  g.ldc = ldc;
+  g.roundA = rA;
+  g.roundB = rB;
+  g.beta = beta;
+  return g;
+}
+
+}  // namespace
+
+extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
+  if (!out) return fail(TRACE_EINVAL, "out is NULL");
+  *out = nullptr;
+  Layout L;
+  int rc = trace_check_config(cfg, &L);
+  if (rc) return rc;
+  const bool bf = cfg->dtype == TRACE_BF16;
+  if (cfg->e % 8 != 0 || cfg->e > 256) return fail(TRACE_EUNSUPPORTED, "e must be a multiple of 8, at most 256");
+  if (cfg->F % 256 != 0) return fail(TRACE_EUNSUPPORTED, "F must be a multiple of 256");
+  if (cfg->g > 64 || cfg->W > 64) return fail(TRACE_EUNSUPPORTED, "W must be at most 64 bytes");
+  attn_fn af = find_attn(bf, L.T, L.D, L.DH);
+  ffn_fn ff = find_ffn(bf, L.D);
+  if (!af || !ff)
+    return fail(TRACE_EUNSUPPORTED, "no kernel for T=" + std::to_string(L.T) + " d=" + std::to_string(L.D) +
+                                        " head width " + std::to_string(L.DH) + (bf ? " bf16" : " fp32"));
+  trace_model* m = new (std::nothrow) trace_model();
+  if (!m) return fail(TRACE_ENOMEM, "host allocation failed");
+  m->cfg = *cfg;
+  m->L = L;
+  m->bf = bf;
+  m->attn = af;
+  m->ffn = ff;
+  m->max_keep = cfg->max_keep;
+  m->max_windows = std::max<int64_t>(std::max<int64_t>(cfg->max_windows, cfg->max_keep), 1);
+  (void)hipGetDevice(&m->device);
+  const int64_t n = L.n, D = L.D, T = L.T, F = cfg->F, W = cfg->W;
+  const int es = bf ? 2 : 4;
+  bool ok = dalloc(m, &m->theta, n * 4) && dalloc(m, &m->am, n * 4) && dalloc(m, &m->av, n * 4) &&
+            dalloc(m, &m->grad, n * 4) && dalloc(m, &m->Ec, L.size[P_E] * es) && dalloc(m, &m->Pc, L.size[P_P] * es) &&
+            dalloc(m, &m->Wq, D * D * es) && dalloc(m, &m->Wk, D * D * es) && dalloc(m, &m->Wv, D * D * es) &&
+            dalloc(m, &m->Wo, D * D * es) && dalloc(m, &m->W1, D * F * es) && dalloc(m, &m->W2, F * D * es) &&
+            dalloc(m, &m->Wout, D * 256 * es) && dalloc(m, &m->h0, m->max_windows * D * 4);
+  const int64_t K = cfg->max_keep;
+  if (ok && K > 0) {
+    ok = dalloc(m, &m->kwin, K * W) && dalloc(m, &m->ktgt, K * 4) && dalloc(m, &m->kq, K * D * 4) &&
+         dalloc(m, &m->kK, K * T * D * 4) && dalloc(m, &m->kV, K * T * D * 4) &&
+         dalloc(m, &m->kA, K * cfg->H * T * 4) && dalloc(m, &m->kO, K * D * 4) &&
+         dalloc(m, &m->kY, (cfg->k + 1) * K * D * 4) && dalloc(m, &m->kU, cfg->k * K * F * 4) &&
+         dalloc(m, &m->kZ, K * 256 * 4) && dalloc(m, &m->dz, K * 256 * 4) && dalloc(m, &m->dY, K * D * 4) &&
+         dalloc(m, &m->dG, K * F * 4) && dalloc(m, &m->dU, K * F * 4) && dalloc(m, &m->G, K * F * 4) &&
+         dalloc(m, &m->dO, K * D * 4) && dalloc(m, &m->dQ, K * D * 4) && dalloc(m, &m->dK, K * T * D * 4) &&
+         dalloc(m, &m->dV, K * T * D * 4) && dalloc(m, &m->dX, K * T * D * 4) && dalloc(m, &m->Xk, K * T * D * 4) &&
+         dalloc(m, &m->gws, (m->gws_cap = adapt_gemm_ws(m, K)) * 4) &&
+         dalloc(m, &m->cws, colsum_ws_floats(std::max<int64_t>(T * D, 256)) * 4);
+  }
+  if (!ok) {
+    free_all(m);
+    delete m;
+    return fail(TRACE_ENOMEM, "device allocation failed");
+  }
+  hipError_t e = hipMemset(m->theta, 0, n * 4);
+  if (e == hipSuccess) e = hipMemset(m->am, 0, n * 4);
+  if (e == hipSuccess) e = hipMemset(m->av, 0, n * 4);
+  if (e == hipSuccess) e = hipMemset(m->grad, 0, n * 4);
+  if (e == hipSuccess) {
+    refresh_operands(m, nullptr);
+    e = hipDeviceSynchronize();
+  }
+  if (e != hipSuccess) {
+    rc = hip_fail(e, "trace_create");
+    free_all(m);
+    delete m;
+    return rc;
+  }
+  *out = m;
+  return TRACE_OK;
+}
+
+extern "C" void trace_destroy(trace_model* m) {
+  if (!m) return;
+  (void)hipDeviceSynchronize();
+  free_all(m);
+  delete m;
+}
+
+extern "C" int trace_init_weights(trace_model* m, uint64_t seed, double stdv, const float* host_flat) {
+  if (!m) return fail(TRACE_EINVAL, "model is NULL");
+  if (!std::isfinite(stdv)) return fail(TRACE_EINVAL, "std must be finite");
+  std::vector<float> h;
+  const float* src = host_flat;
+  if (!src) {
+    h.resize((size_t)m->L.n);
+    trace_fill_init(m->L, seed, stdv, h.data());
+    src = h.data();
+  }
+  hipError_t e = hipMemcpy(m->theta, src, (size_t)m->L.n * 4, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemset(m->am, 0, (size_t)m->L.n * 4);
+  if (e == hipSuccess) e = hipMemset(m->av, 0, (size_t)m->L.n * 4);
+  if (e != hipSuccess) return hip_fail(e, "trace_init_weights");
+  m->step = 0;
+  m->kept = false;
+  refresh_operands(m, nullptr);
+  e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "trace_init_weights");
+  return TRACE_OK;
+}
+
+static int check_windows(const trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams,
+                         int64_t pos0, int32_t n_steps) {
+  if (!m) return fail(TRACE_EINVAL, "model is NULL");
+  if (!d_streams) return fail(TRACE_EINVAL, "streams is NULL");
+  if (n_streams < 0 || n_steps < 0) return fail(TRACE_EINVAL, "n_streams and n_steps must be non-negative");
+  if (pos0 < m->cfg.W) return fail(TRACE_EINVAL, "pos0 must be at least W (the first W bytes have no window)");
+  if (n_streams > 1 && stride < pos0 + n_steps)
+    return fail(TRACE_EINVAL, "stride shorter than the bytes each stream must hold (pos0 + n_steps)");
+  return TRACE_OK;
+}
+
+extern "C" int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams,
+                                  int64_t pos0, int32_t n_steps, float* d_bits, float* d_logits, double* d_step_ce,
+                                  uint32_t flags, void* stream) {
+  int rc = check_windows(m, d_streams, stride, n_streams, pos0, n_steps);
+  if (rc) return rc;
+  if (flags & ~(uint32_t)TRACE_KEEP_ACTS) return fail(TRACE_EINVAL, "unknown flag");
+  const bool keep = (flags & TRACE_KEEP_ACTS) != 0;
+  const int64_t total = (int64_t)n_streams * n_steps;
+  if (keep && (m->max_keep <= 0 || total > m->max_keep))
+    return fail(TRACE_EINVAL, "KEEP_ACTS needs n_streams*n_steps <= max_keep");
+  if (total == 0) return TRACE_OK;  // nothing to write: output pointers may be NULL
+  if (!d_bits) return fail(TRACE_EINVAL, "bits is NULL");
+  const hipStream_t s = S(stream);
+  const Layout& L = m->L;
+  const int64_t chunk = keep ? total : m->max_windows;
+  for (int64_t n0 = 0; n0 < total; n0 += chunk) {
+    WinArgs w;
+    w.streams = d_streams;
+    w.stride = stride;
+    w.pos0 = pos0;
+    w.n_steps = n_steps;
+    w.n0 = n0;
+    w.N = std::min(chunk, total - n0);
+    AttnArgs a;
+    std::memset(&a, 0, sizeof(a));
+    a.w = w;
+    a.E = m->Ec;
+    a.P = m->Pc;
+    a.e = m->cfg.e;
+    a.g = m->cfg.g;
+    a.Wq = m->Wq;
+    a.Wk = m->Wk;
+    a.Wv = m->Wv;
+    a.Wo = m->Wo;
+    a.h0 = m->h0;
+    a.scale = (float)(1.0 / std::sqrt((double)L.DH));
+    FfnArgs f;
+    std::memset(&f, 0, sizeof(f));
+    f.w = w;
+    f.h0 = m->h0;
+    f.W1 = m->W1;
+    f.W2 = m->W2;
+    f.Wout = m->Wout;
+    f.bout = m->theta + L.off[P_BOUT];
+    f.F = m->cfg.F;
+    f.k = m->cfg.k;
+    f.bits = d_bits;
+    f.logits = d_logits;
+    if (keep) {
+      a.kwin = m->kwin;
+      a.kq = m->kq;
+      a.kK = m->kK;
+      a.kV = m->kV;
+      a.kA = m->kA;
+      a.kO = m->kO;
+      f.kY = m->kY;
+      f.kU = m->kU;
+      f.kZ = m->kZ;
+      f.ktgt = m->ktgt;
+    }
+    m->attn(a, s);
+    m->ffn(f, s);
+  }
+  if (d_step_ce && n_streams > 0) launch_step_ce(d_bits, n_streams, n_steps, d_step_ce, s);
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "trace_forward_bits");
+  if (keep) {
+    m->kept = true;
+    m->keepN = total;
+  }
+  return TRACE_OK;
+}
+
+extern "C" int trace_adapt_step(trace_model* m, void* stream) {
+  if (!m) return fail(TRACE_EINVAL, "model is NULL");
+  if (!m->kept) return fail(TRACE_ESTATE, "no batch kept: run trace_forward_bits with TRACE_KEEP_ACTS first");
+  const hipStream_t s = S(stream);
+  const Layout& L = m->L;
+  const int N = (int)m->keepN, D = L.D, T = L.T, F = m->cfg.F, H = m->cfg.H, k = m->cfg.k;
+  const int rb = m->bf ? 1 : 0;  // bf16 storage points round their operands
+  float* th = m->theta;
+  float* gr = m->grad;
+  float* ws = m->gws;
+  // head: dz = (softmax(z) - onehot) / N
+  launch_ce_grad(m->kZ, m->ktgt, N, m->dz, s);
+  // dWout = h_k^T . dz ; dbout = sum_n dz ; dY_k = dz . Wout^T
+  const float* Yk = m->kY + (int64_t)k * N * D;
+  launch_gemm(gemm(D, 256, N, Yk, 1, D, rb, m->dz, 256, 1, rb, gr + L.off[P_WOUT], 256, 0.f), ws, m->gws_cap, s);
+  launch_colsum(m->dz, N, 256, 256, gr + L.off[P_BOUT], 0.f, m->cws, s);
+  launch_gemm(gemm(N, D, 256, m->dz, 256, 1, rb, th + L.off[P_WOUT], 1, 256, rb, m->dY, D, 0.f), ws, m->gws_cap, s);
+  // shared FFN, repeats in reverse; W1 and W2 gradients accumulate over repeats
+  for (int r = k - 1; r >= 0; --r) {
+    const float* Ur = m->kU + (int64_t)r * N * F;
+    const float* Yr = m->kY + (int64_t)r * N * D;
+    const float beta = (r == k - 1) ? 0.f : 1.f;
+    launch_gelu_fwd_round(Ur, m->G, (int64_t)N * F, rb, s);
+    launch_gemm(gemm(F, D, N, m->G, 1, F, rb, m->dY, D, 1, rb, gr + L.off[P_W2], D, beta), ws, m->gws_cap, s);
+    launch_gemm(gemm(N, F, D, m->dY, D, 1, rb, th + L.off[P_W2], 1, D, rb, m->dG, F, 0.f), ws, m->gws_cap, s);
+    launch_gelu_bwd(m->dG, Ur, m->dU, (int64_t)N * F, s);
+    launch_gemm(gemm(D, F, N, Yr, 1, D, rb, m->dU, F, 1, rb, gr + L.off[P_W1], F, beta), ws, m->gws_cap, s);
+    launch_gemm(gemm(N, D, F, m->dU, F, 1, rb, th + L.off[P_W1], 1, F, rb, m->dY, D, 1.f), ws, m->gws_cap, s);
+  }
+  // attention output projection: dWo = O^T . dY0 ; dO = dY0 . Wo^T
+  launch_gemm(gemm(D, D, N, m->kO, 1, D, rb, m->dY, D, 1, rb, gr + L.off[P_WO], D, 0.f), ws, m->gws_cap, s);
+  launch_gemm(gemm(N, D, D, m->dY, D, 1, rb, th + L.off[P_WO], 1, D, rb, m->dO, D, 0.f), ws, m->gws_cap, s);
+  // attention (last query row) -> dQ, dK, dV
+  launch_attn_bwd(m->dO, m->kq, m->kK, m->kV, m->kA, N, T, D, H, (float)(1.0 / std::sqrt((double)L.DH)), rb, m->dQ,
+                  m->dK, m->dV, s);
+  // projections: dWq = X_last^T dQ, dWk = X^T dK, dWv = X^T dV  (dQ, dK, dV stay fp32)
+  launch_gather_kept(m->bf, m->kwin, N, m->Ec, m->Pc, T, D, m->cfg.e, m->cfg.g, m->Xk, s);
+  launch_gemm(gemm(D, D, N, m->Xk + (int64_t)(T - 1) * D, 1, (int64_t)T * D, rb, m->dQ, D, 1, 0, gr + L.off[P_WQ], D,
+                   0.f),
+              ws, m->gws_cap, s);
+  launch_gemm(gemm(D, D, N * T, m->Xk, 1, D, rb, m->dK, D, 1, 0, gr + L.off[P_WK], D, 0.f), ws, m->gws_cap, s);
+  launch_gemm(gemm(D, D, N * T, m->Xk, 1, D, rb, m->dV, D, 1, 0, gr + L.off[P_WV], D, 0.f), ws, m->gws_cap, s);
+  // dX = dK Wk^T + dV Wv^T (+ dQ Wq^T + dY0 on the last token)
+  launch_gemm(gemm(N * T, D, D, m->dK, D, 1, 0, th + L.off[P_WK], 1, D, rb, m->dX, D, 0.f), ws, m->gws_cap, s);
+  launch_gemm(gemm(N * T, D, D, m->dV, D, 1, 0, th + L.off[P_WV], 1, D, rb, m->dX, D, 1.f), ws, m->gws_cap, s);
+  launch_gemm(gemm(N, D, D, m->dQ, D, 1, 0, th + L.off[P_WQ], 1, D, rb, m->dX + (int64_t)(T - 1) * D, (int64_t)T * D,
+                   1.f),
+              ws, m->gws_cap, s);
+  launch_add(m->dX + (int64_t)(T - 1) * D, m->dY, N, D, (int64_t)T * D, D, s);
+  // positional table and byte embedding
+  if (m->cfg.use_pos)
+    launch_colsum(m->dX, N, (int64_t)T * D, (int64_t)T * D, gr + L.off[P_P], 0.f, m->cws, s);
+  else
+    launch_zero(gr + L.off[P_P], L.size[P_P], s);
+  launch_embed_bwd(m->kwin, m->dX, N, m->cfg.W, m->cfg.g, m->cfg.e, D, gr + L.off[P_E], s);
+  // Adam on the flat master, then new operand copies
+  m->step += 1;
+  const float bc1 = (float)(1.0 - std::pow(m->cfg.beta1, (double)m->step));
+  const float bc2 = (float)(1.0 - std::pow(m->cfg.beta2, (double)m->step));
+  launch_adam(th, gr, m->am, m->av, L.n, (float)m->cfg.lr, (float)m->cfg.beta1, (float)m->cfg.beta2,
+              (float)m->cfg.eps, bc1, bc2, s);
+  refresh_operands(m, s);
+  m->kept = false;
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "trace_adapt_step");
+  return TRACE_OK;
+}
+
+extern "C" int trace_get_state(trace_model* m, float* theta, float* adam_m, float* adam_v, int64_t* step, int64_t n) {
+  if (!m) return fail(TRACE_EINVAL, "model is NULL");
+  if (n != m->L.n) return fail(TRACE_EINVAL, "n must equal trace_param_count");
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess && theta) e = hipMemcpy(theta, m->theta, n * 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess && adam_m) e = hipMemcpy(adam_m, m->am, n * 4, hipMemcpyDeviceToHost);
+  if (e == hipSuccess && adam_v) e = hipMemcpy(adam_v, m->av, n * 4, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "trace_get_state");
+  if (step) *step = m->step;
+  return TRACE_OK;
+}
+
+extern "C" int trace_set_state(trace_model* m, const float* theta, const float* adam_m, const float* adam_v,
+                               int64_t step, int64_t n) {
+  if (!m) return fail(TRACE_EINVAL, "model is NULL");
+  if (n != m->L.n) return fail(TRACE_EINVAL, "n must equal trace_param_count");
+  if (step < 0) return fail(TRACE_EINVAL, "step must be non-negative");
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess && theta) e = hipMemcpy(m->theta, theta, n * 4, hipMemcpyHostToDevice);
+  if (e == hipSuccess && adam_m) e = hipMemcpy(m->am, adam_m, n * 4, hipMemcpyHostToDevice);
+  if (e == hipSuccess && adam_v) e = hipMemcpy(m->av, adam_v, n * 4, hipMemcpyHostToDevice);
+  if (e != hipSuccess) return hip_fail(e, "trace_set_state");
+  m->step = step;
+  m->kept = false;
+  refresh_operands(m, nullptr);
+  e = hipDeviceSynchronize();
+  if (e != hipSuccess) return hip_fail(e, "trace_set_state");
+  return TRACE_OK;
+}
+
+extern "C" int trace_get_grads(trace_model* m, float* host_out, int64_t n) {
+  if (!m || !host_out) return fail(TRACE_EINVAL, "model or output is NULL");
+  if (n != m->L.n) return fail(TRACE_EINVAL, "n must equal trace_param_count");
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess) e = hipMemcpy(host_out, m->grad, n * 4, hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_fail(e, "trace_get_grads");
+  return TRACE_OK;
+}
+
+extern "C" int trace_debug_gather(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams,
+                                  int64_t pos0, int32_t n_steps, float* d_X, void* stream) {
+  int rc = check_windows(m, d_streams, stride, n_streams, pos0, n_steps);
+  if (rc) return rc;
+  if (!d_X) return fail(TRACE_EINVAL, "X is NULL");
+  WinArgs w;
+  w.streams = d_streams;
+  w.stride = stride;
+  w.pos0 = pos0;
+  w.n_steps = n_steps;
+  w.n0 = 0;
+  w.N = (int64_t)n_streams * n_steps;
+  if (w.N == 0) return TRACE_OK;
+  launch_gather(m->bf, w, m->Ec, m->Pc, m->L.T, m->L.D, m->cfg.e, m->cfg.g, d_X, S(stream));
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "trace_debug_gather");
+  return TRACE_OK;
+}

@@ -1,0 +1,389 @@
+// Gated adaptation on gfx950: the gradient of the batch-mean cross-entropy
+// through the forward of fwd.hip (Model.backward of Alg. 1, line 10), and the
+// Adam update (Sec. 6: Adam, lr 0.001).  Every reduction runs in a fixed order,
+// so two runs on the same inputs give bitwise-identical gradients: split-K
+// partial products and column sums are combined by a second pass that adds
+// them in index order, and the embedding scatter is a per-byte-value gather.
+#include "kcommon.h"
+#include "kernels.h"
+
+// ------------------------------------------------------------ generic GEMM ----
+// C(m,n) [+]= sum_k A(m,k) B(k,n) for arbitrary element strides.  64x64 output
+// tile per workgroup, 4 waves in a 2x2 layout of 32x32 sub-tiles; the k range
+// is walked in steps of 32 staged through LDS as [row][k] (A) and [col][k] (B)
+// so that both fragments are 16-byte LDS reads.  Operands are rounded to bf16
+// on the way into LDS where the caller asks (the bf16 storage points).
+template <bool BF>
+__global__ __launch_bounds__(256) void k_gemm(GemmArgs g, float* __restrict__ part, int kchunk) {
+  typedef Mma<BF> M;
+  typedef typename M::T OT;
+  constexpr int BM = 64, BN = 64, BK = 32;
+  constexpr int STR = BK * (int)sizeof(OT) + 16;
+  __shared__ __align__(16) unsigned char As[BM * STR];
+  __shared__ __align__(16) unsigned char Bs[BN * STR];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lg = lane >> 4, lc = lane & 15;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int kbeg = blockIdx.z * kchunk;
+  const int kend = min(g.K, kbeg + kchunk);
+  f32x4 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const bool a_k_fast = (g.sak == 1);
+  const bool b_n_fast = (g.sbn == 1);
+  for (int k0 = kbeg; k0 < kend; k0 += BK) {
+#pragma unroll
+    for (int it = 0; it < (BM * BK) / 256; ++it) {
+      const int i = tid + it * 256;
+      int mm, kk;
+      if (a_k_fast) {
+        mm = i / BK;
+        kk = i % BK;
+      } else {
+        kk = i / BM;
+        mm = i % BM;
+      }
+      const int m = m0 + mm, k = k0 + kk;
+      float v = (m < g.M && k < kend) ? g.A[(int64_t)m * g.sam + (int64_t)k * g.sak] : 0.f;
+      if (g.roundA) v = round_bf(v);
+      ((OT*)(As + mm * STR))[kk] = M::cvt(v);
+    }
+#pragma unroll
+    for (int it = 0; it < (BN * BK) / 256; ++it) {
+      const int i = tid + it * 256;
+      int nn, kk;
+      if (b_n_fast) {
+        kk = i / BN;
+        nn = i % BN;
+      } else {
+        nn = i / BK;
+        kk = i % BK;
+      }
+      const int n = n0 + nn, k = k0 + kk;
+      float v = (n < g.N && k < kend) ? g.B[(int64_t)k * g.sbk + (int64_t)n * g.sbn] : 0.f;
+      if (g.roundB) v = round_bf(v);
+      ((OT*)(Bs + nn * STR))[kk] = M::cvt(v);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < BK / M::KS; ++ks) {
+      uint4 af[2], bfr[2];
+#pragma unroll
+      for (int rf = 0; rf < 2; ++rf) af[rf] = *(const uint4*)(As + (wm * 32 + rf * 16 + lc) * STR + ks * 64 + lg * 16);
+#pragma unroll
+      for (int nf = 0; nf < 2; ++nf) bfr[nf] = *(const uint4*)(Bs + (wn * 32 + nf * 16 + lc) * STR + ks * 64 + lg * 16);
+#pragma unroll
+      for (int rf = 0; rf < 2; ++rf)
+#pragma unroll
+        for (int nf = 0; nf < 2; ++nf) M::run(acc[rf][nf], af[rf], bfr[nf]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int rf = 0; rf < 2; ++rf)
+#pragma unroll
+    for (int nf = 0; nf < 2; ++nf)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + wm * 32 + rf * 16 + 4 * lg + r;
+        const int n = n0 + wn * 32 + nf * 16 + lc;
+        if (m < g.M && n < g.N) {
+          if (part) {
+            part[((int64_t)blockIdx.z * g.M + m) * g.N + n] = acc[rf][nf][r];
+          } else {
+            float* c = g.C + (int64_t)m * g.ldc + n;
+            *c = (g.beta != 0.f) ? (*c + acc[rf][nf][r]) : acc[rf][nf][r];
+          }
+        }
+      }
+}
+
+// C(m,n) = [C(m,n) +] sum_z part[z][m][n], z in increasing order.
+__global__ void k_splitk_reduce(const float* __restrict__ part, int splits, int M, int N, float* C, int64_t ldc,
+                                float beta) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)M * N) return;
+  const int m = (int)(i / N), n = (int)(i % N);
+  float s = 0.f;
+  for (int z = 0; z < splits; ++z) s += part[((int64_t)z * M + m) * N + n];
+  float* c = C + (int64_t)m * ldc + n;
+  *c = (beta != 0.f) ? (*c + s) : s;
+}
+
+static int gemm_splits(int M, int N, int K) {
+  const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
+  int splits = 1;
+  // enough workgroups to fill 256 CUs, each split still covering >= 256 k values
+  while (tiles * splits < 512 && (K + splits * 2 - 1) / (splits * 2) >= 256) splits *= 2;
+  return splits;
+}
+int64_t gemm_ws_floats(int M, int N, int K) {
+  const int s = gemm_splits(M, N, K);
+  return s > 1 ? (int64_t)s * M * N : 0;
+}
+void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return;
+  const bool bf = g.roundA && g.roundB;
+  int splits = gemm_splits(g.M, g.N, g.K);
+  while (splits > 1 && (int64_t)splits * g.M * g.N > ws_cap) splits /= 2;
+  int kchunk = (g.K + splits - 1) / splits;
+  kchunk = (kchunk + 31) / 32 * 32;
+  const dim3 grid((g.N + 63) / 64, (g.M + 63) / 64, splits);
+  float* part = splits > 1 ? ws : nullptr;
+  if (bf)
+    hipLaunchKernelGGL(k_gemm<true>, grid, dim3(256), 0, s, g, part, kchunk);
+  else
+    hipLaunchKernelGGL(k_gemm<false>, grid, dim3(256), 0, s, g, part, kchunk);
+  if (splits > 1) {
+    const int64_t tot = (int64_t)g.M * g.N;
+    hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, ws, splits, g.M, g.N,
+                       g.C, g.ldc, g.beta);
+  }
+}
+
+// ------------------------------------------------------------- column sums ----
+constexpr int COLSUM_SPLITS = 64;
+__global__ void k_colsum1(const float* __restrict__ in, int64_t rows, int64_t cols, int64_t ld, float* __restrict__ ws) {
+  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (c >= cols) return;
+  const int s = blockIdx.y;
+  const int64_t chunk = (rows + COLSUM_SPLITS - 1) / COLSUM_SPLITS;
+  const int64_t r0 = s * chunk, r1 = min(rows, r0 + chunk);
+  float acc = 0.f;
+  for (int64_t r = r0; r < r1; ++r) acc += in[r * ld + c];
+  ws[s * cols + c] = acc;
+}
+__global__ void k_colsum2(const float* __restrict__ ws, int64_t cols, float* out, float beta) {
+  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (c >= cols) return;
+  float acc = 0.f;
+  for (int s = 0; s < COLSUM_SPLITS; ++s) acc += ws[s * cols + c];
+  out[c] = (beta != 0.f) ? out[c] + acc : acc;
+}
+int64_t colsum_ws_floats(int64_t cols) { return COLSUM_SPLITS * cols; }
+void launch_colsum(const float* in, int64_t rows, int64_t cols, int64_t ld, float* out, float beta, float* ws,
+                   hipStream_t s) {
+  const unsigned gx = (unsigned)((cols + 255) / 256);
+  hipLaunchKernelGGL(k_colsum1, dim3(gx, COLSUM_SPLITS), dim3(256), 0, s, in, rows, cols, ld, ws);
+  hipLaunchKernelGGL(k_colsum2, dim3(gx), dim3(256), 0, s, ws, cols, out, beta);
+}
+
+// ------------------------------------------------------ head: dz of the CE ----
+// dz[n] = (softmax(z[n]) - onehot(y[n])) / N for the mean cross-entropy in nats.
+// One wave per window; each lane holds 4 of the 256 logits.
+__global__ __launch_bounds__(256) void k_ce_grad(const float* __restrict__ z, const int32_t* __restrict__ tgt, int64_t N,
+                                                 float* __restrict__ dz) {
+  const int lane = threadIdx.x & 63;
+  const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (n >= N) return;
+  float v[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) v[i] = z[n * 256 + lane + 64 * i];
+  float mx = fmaxf(fmaxf(v[0], v[1]), fmaxf(v[2], v[3]));
+  for (int o = 32; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+  float ex[4], sm = 0.f;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    ex[i] = expf(v[i] - mx);
+    sm += ex[i];
+  }
+  for (int o = 32; o > 0; o >>= 1) sm += __shfl_xor(sm, o, 64);
+  const int y = tgt[n];
+  const float fn = (float)N;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int c = lane + 64 * i;
+    const float p = ex[i] / sm;
+    dz[n * 256 + c] = (p - (c == y ? 1.f : 0.f)) / fn;
+  }
+}
+void launch_ce_grad(const float* z, const int32_t* tgt, int64_t N, float* dz, hipStream_t s) {
+  hipLaunchKernelGGL(k_ce_grad, dim3((unsigned)((N + 3) / 4)), dim3(256), 0, s, z, tgt, N, dz);
+}
+
+// -------------------------------------------------------------- elementwise ----
+__global__ void k_gelu_fwd_round(const float* __restrict__ U, float* __restrict__ G, int64_t n, int round) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const float g = gelu_f(U[i]);
+  G[i] = round ? round_bf(g) : g;
+}
+void launch_gelu_fwd_round(const float* U, float* G, int64_t n, int round, hipStream_t s) {
+  hipLaunchKernelGGL(k_gelu_fwd_round, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, U, G, n, round);
+}
+__global__ void k_gelu_bwd(const float* __restrict__ dG, const float* __restrict__ U, float* __restrict__ dU, int64_t n) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  dU[i] = dG[i] * gelu_grad_f(U[i]);
+}
+void launch_gelu_bwd(const float* dG, const float* U, float* dU, int64_t n, hipStream_t s) {
+  hipLaunchKernelGGL(k_gelu_bwd, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, dG, U, dU, n);
+}
+// y[r][c] += x[r][c]
+__global__ void k_add(float* __restrict__ y, const float* __restrict__ x, int64_t rows, int64_t cols, int64_t ldy,
+                      int64_t ldx) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= rows * cols) return;
+  const int64_t r = i / cols, c = i % cols;
+  y[r * ldy + c] += x[r * ldx + c];
+}
+void launch_add(float* y, const float* x, int64_t rows, int64_t cols, int64_t ldy, int64_t ldx, hipStream_t s) {
+  hipLaunchKernelGGL(k_add, dim3((unsigned)((rows * cols + 255) / 256)), dim3(256), 0, s, y, x, rows, cols, ldy, ldx);
+}
+
+// ------------------------------------------------------- attention backward ----
+// Last query row only (the only row with an upstream gradient).  For window n
+// and head h with weights a_u over the T keys:
+//   dA_u = dO . V_u,  dS_u = a_u (dA_u - sum_u' a_u' dA_u'),
+//   dq = scale sum_u dS_u K_u,  dK_u = scale dS_u q,  dV_u = a_u dO.
+// One thread per (window, head, column); the two reductions over the head's
+// columns go through LDS.
+template <int DH>
+__global__ __launch_bounds__(256) void k_attn_bwd(const float* __restrict__ dO, const float* __restrict__ q,
+                                                  const float* __restrict__ K, const float* __restrict__ V,
+                                                  const float* __restrict__ A, int64_t N, int T, int D, int H,
+                                                  float scale, int round_dO, float* __restrict__ dQ,
+                                                  float* __restrict__ dK, float* __restrict__ dV) {
+  constexpr int GROUPS = 256 / DH;  // (window, head) pairs per block
+  __shared__ float red[GROUPS][8][DH];
+  __shared__ float dS[GROUPS][8];
+  const int gi = threadIdx.x / DH, c = threadIdx.x % DH;
+  const int64_t pair = (int64_t)blockIdx.x * GROUPS + gi;
+  const bool live = pair < N * H;
+  const int64_t n = live ? pair / H : 0;
+  const int h = live ? (int)(pair % H) : 0;
+  const int col = h * DH + c;
+  float o = live ? dO[n * D + col] : 0.f;
+  if (round_dO) o = round_bf(o);
+  for (int u = 0; u < T; ++u) red[gi][u][c] = live ? o * V[(n * T + u) * D + col] : 0.f;
+  __syncthreads();
+  if (c < T) {
+    float s = 0.f;
+    for (int i = 0; i < DH; ++i) s += red[gi][c][i];
+    dS[gi][c] = s;  // dA_c for now
+  }
+  __syncthreads();
+  if (c == 0 && live) {
+    float a[8], dA[8], sum = 0.f;
+    for (int u = 0; u < T; ++u) {
+      a[u] = A[(n * H + h) * T + u];
+      dA[u] = dS[gi][u];
+      sum += a[u] * dA[u];
+    }
+    for (int u = 0; u < T; ++u) dS[gi][u] = a[u] * (dA[u] - sum);
+  }
+  __syncthreads();
+  if (!live) return;
+  const float qv = q[n * D + col];
+  float dq = 0.f;
+  for (int u = 0; u < T; ++u) {
+    const float ds = dS[gi][u];
+    dq += ds * K[(n * T + u) * D + col];
+    dK[(n * T + u) * D + col] = (ds * qv) * scale;
+    dV[(n * T + u) * D + col] = A[(n * H + h) * T + u] * o;
+  }
+  dQ[n * D + col] = dq * scale;
+}
+void launch_attn_bwd(const float* dO, const float* q, const float* K, const float* V, const float* A, int64_t N, int T,
+                     int D, int H, float scale, int round_dO, float* dQ, float* dK, float* dV, hipStream_t s) {
+  const int DH = D / H;
+  const int64_t pairs = N * H;
+  if (DH == 32) {
+    hipLaunchKernelGGL(k_attn_bwd<32>, dim3((unsigned)((pairs + 7) / 8)), dim3(256), 0, s, dO, q, K, V, A, N, T, D,
+                       H, scale, round_dO, dQ, dK, dV);
+  } else {
+    hipLaunchKernelGGL(k_attn_bwd<64>, dim3((unsigned)((pairs + 3) / 4)), dim3(256), 0, s, dO, q, K, V, A, N, T, D,
+                       H, scale, round_dO, dQ, dK, dV);
+  }
+}
+
+// ------------------------------------------------------ embedding backward ----
+// dE[v][c] = sum over (n, p) with win[n][p] == v of dX[n][p/g][(p%g)*e + c].
+// One block per byte value v: thread (r, c) walks the positions r, r+R, ... in
+// order, and the R partial sums are combined in a fixed order.
+__global__ __launch_bounds__(256) void k_embed_bwd(const uint8_t* __restrict__ win, const float* __restrict__ dX,
+                                                   int64_t N, int W, int g, int e, int D, float* __restrict__ dE) {
+  __shared__ float red[256];
+  const int v = blockIdx.x;
+  const int R = 256 / e;
+  const int r = threadIdx.x / e, c = threadIdx.x % e;
+  float acc = 0.f;
+  if (r < R) {
+    const int64_t total = N * W;
+    for (int64_t i = r; i < total; i += R) {
+      if (win[i] == v) {
+        const int64_t n = i / W;
+        const int p = (int)(i - n * W);
+        const int t = p / g, j = p - t * g;
+        acc += dX[(n * (W / g) + t) * D + j * e + c];
+      }
+    }
+  }
+  red[threadIdx.x] = acc;
+  __syncthreads();
+  if (threadIdx.x < e) {
+    float s = 0.f;
+    for (int i = 0; i < R; ++i) s += red[i * e + threadIdx.x];
+    dE[v * e + threadIdx.x] = s;
+  }
+}
+void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int g, int e, int D, float* dE,
+                      hipStream_t s) {
+  hipLaunchKernelGGL(k_embed_bwd, dim3(256), dim3(256), 0, s, win, dX, N, W, g, e, D, dE);
+}
+
+// token operand values of the kept windows: X[n][t][c] (fp32 value of the operand)
+template <bool BF>
+__global__ void k_gather_kept(const uint8_t* __restrict__ win, int64_t N, const typename Mma<BF>::T* __restrict__ E,
+                              const typename Mma<BF>::T* __restrict__ P, int T, int D, int e, int g,
+                              float* __restrict__ X) {
+  typedef Mma<BF> M;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= N * T * D) return;
+  const int c = (int)(i % D);
+  const int64_t rr = i / D;
+  const int t = (int)(rr % T);
+  const int64_t n = rr / T;
+  const int j = c / e, cc = c - j * e;
+  const int byte = win[n * (T * g) + t * g + j];
+  X[i] = M::val(M::cvt(M::val(E[byte * e + cc]) + M::val(P[t * D + c])));
+}
+void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, const void* P, int T, int D, int e,
+                        int g, float* X, hipStream_t s) {
+  const dim3 grid((unsigned)((N * T * D + 255) / 256));
+  if (bf)
+    hipLaunchKernelGGL(k_gather_kept<true>, grid, dim3(256), 0, s, win, N, (const uint16_t*)E, (const uint16_t*)P, T,
+                       D, e, g, X);
+  else
+    hipLaunchKernelGGL(k_gather_kept<false>, grid, dim3(256), 0, s, win, N, (const float*)E, (const float*)P, T, D, e,
+                       g, X);
+}
+
+// -------------------------------------------------------------------- Adam ----
+// Kingma & Ba, Alg. 1, with the bias corrections bc1 = 1 - beta1^t and
+// bc2 = 1 - beta2^t supplied by the host.  Each product and sum is rounded on
+// its own (no fused multiply-add), in the order m = b1*m + (1-b1)*g,
+// v = b2*v + ((1-b2)*g)*g, theta -= (lr * m/bc1) / (sqrt(v/bc2) + eps).
+__global__ void k_adam(float* __restrict__ theta, const float* __restrict__ grad, float* __restrict__ m,
+                       float* __restrict__ v, int64_t n, float lr, float b1, float b2, float eps, float bc1,
+                       float bc2) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  const float g = grad[i];
+  const float omb1 = __fsub_rn(1.f, b1), omb2 = __fsub_rn(1.f, b2);
+  const float mi = __fadd_rn(__fmul_rn(b1, m[i]), __fmul_rn(omb1, g));
+  const float vi = __fadd_rn(__fmul_rn(b2, v[i]), __fmul_rn(__fmul_rn(omb2, g), g));
+  m[i] = mi;
+  v[i] = vi;
+  const float mhat = __fdiv_rn(mi, bc1);
+  const float vhat = __fdiv_rn(vi, bc2);
+  const float step = __fdiv_rn(__fmul_rn(lr, mhat), __fadd_rn(__fsqrt_rn(vhat), eps));
+  theta[i] = __fsub_rn(theta[i], step);
+}
+void launch_adam(float* theta, const float* grad, float* m, float* v, int64_t n, float lr, float b1, float b2,
+                 float eps, float bc1, float bc2, hipStream_t s) {
+  hipLaunchKernelGGL(k_adam, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, theta, grad, m, v, n, lr, b1, b2, eps,
+                     bc1, bc2);
+}

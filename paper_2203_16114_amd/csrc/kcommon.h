@@ -1,0 +1,113 @@
+// Device helpers shared by the libtrace kernels (gfx950 / CDNA4).
+//
+// MFMA fragment conventions (the GPU parity tests in tests/ check every use of them):
+//   v_mfma_f32_16x16x32_bf16: lane l holds A[row l%16][k (l/16)*8 + j], j < 8, and
+//     B[k (l/16)*8 + j][col l%16]; the 16x16 fp32 result lands in lane l as
+//     rows 4*(l/16) + r (r < 4) of column l%16.
+//   v_mfma_f32_16x16x4_f32: lane l holds A[row l%16][k l/16] and B[k l/16][col l%16],
+//     same result layout.
+// Every fragment is 16 bytes per lane: 8 bf16, or 4 fp32 covering four chained
+// 16x16x4 steps.  A "k-step" is therefore 32 (bf16) or 16 (fp32) k values, and
+// lane l reads bytes [(l/16)*16, (l/16)*16 + 16) of the k-step's 64-byte slice of
+// its row.  The k order inside a step is the same for A and B, so the products
+// pair up exactly as in the plain sum over k.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+typedef __attribute__((ext_vector_type(4))) float f32x4;
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8;
+
+#define TRACE_LOG2E 1.4426950408889634f
+
+// fp32 -> bf16 bits, round to nearest even; NaN stays NaN.
+__device__ __forceinline__ uint16_t f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+__device__ __forceinline__ float bf2f(uint16_t h) { return __uint_as_float(((uint32_t)h) << 16); }
+__device__ __forceinline__ float round_bf(float f) { return bf2f(f2bf(f)); }
+
+template <bool BF> struct Mma;
+
+template <> struct Mma<true> {
+  typedef uint16_t T;            // storage of one operand element (bf16 bits)
+  static constexpr int KS = 32;  // k values per fragment step
+  static constexpr int EPF = 8;  // elements per lane per fragment
+  __device__ static __forceinline__ void run(f32x4& c, const uint4& a, const uint4& b) {
+    c = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b), c, 0,
+                                                0, 0);
+  }
+  __device__ static __forceinline__ T cvt(float x) { return f2bf(x); }
+  __device__ static __forceinline__ float val(T x) { return bf2f(x); }
+};
+
+template <> struct Mma<false> {
+  typedef float T;
+  static constexpr int KS = 16;
+  static constexpr int EPF = 4;
+  __device__ static __forceinline__ void run(f32x4& c, const uint4& a, const uint4& b) {
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), c, 0, 0, 0);
+  }
+  __device__ static __forceinline__ T cvt(float x) { return x; }
+  __device__ static __forceinline__ float val(T x) { return x; }
+};
+
+// Eight consecutive operand elements -> fp32.
+__device__ __forceinline__ void load8(const uint16_t* p, float* out) {
+  uint4 v = *reinterpret_cast<const uint4*>(p);
+  uint32_t w[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    out[2 * i] = __uint_as_float(w[i] << 16);
+    out[2 * i + 1] = __uint_as_float(w[i] & 0xffff0000u);
+  }
+}
+__device__ __forceinline__ void load8(const float* p, float* out) {
+  float4 a = *reinterpret_cast<const float4*>(p);
+  float4 b = *reinterpret_cast<const float4*>(p + 4);
+  out[0] = a.x; out[1] = a.y; out[2] = a.z; out[3] = a.w;
+  out[4] = b.x; out[5] = b.y; out[6] = b.z; out[7] = b.w;
+}
+// fp32 x8 -> eight operand elements at p (16 or 32 bytes, aligned).
+__device__ __forceinline__ void store8(uint16_t* p, const float* in) {
+  uint4 v;
+  v.x = (uint32_t)f2bf(in[0]) | ((uint32_t)f2bf(in[1]) << 16);
+  v.y = (uint32_t)f2bf(in[2]) | ((uint32_t)f2bf(in[3]) << 16);
+  v.z = (uint32_t)f2bf(in[4]) | ((uint32_t)f2bf(in[5]) << 16);
+  v.w = (uint32_t)f2bf(in[6]) | ((uint32_t)f2bf(in[7]) << 16);
+  *reinterpret_cast<uint4*>(p) = v;
+}
+__device__ __forceinline__ void store8(float* p, const float* in) {
+  *reinterpret_cast<float4*>(p) = make_float4(in[0], in[1], in[2], in[3]);
+  *reinterpret_cast<float4*>(p + 4) = make_float4(in[4], in[5], in[6], in[7]);
+}
+
+// Exact-erf GELU of Eq. 3: u * Phi(u), Phi(u) = erfc(-u / sqrt 2) / 2.
+__device__ __forceinline__ float gelu_f(float u) { return u * (0.5f * erfcf(-u * 0.70710678118654752f)); }
+// d/du [u Phi(u)] = Phi(u) + u phi(u).
+__device__ __forceinline__ float gelu_grad_f(float u) {
+  float Phi = 0.5f * erfcf(-u * 0.70710678118654752f);
+  float phi = expf(-0.5f * u * u) * 0.3989422804014327f;
+  return Phi + u * phi;
+}
+
+__device__ __forceinline__ float wave_sum16(float v) {  // over the 16 lanes sharing l/16
+  v += __shfl_xor(v, 1, 64);
+  v += __shfl_xor(v, 2, 64);
+  v += __shfl_xor(v, 4, 64);
+  v += __shfl_xor(v, 8, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max16(float v) {
+  v = fmaxf(v, __shfl_xor(v, 1, 64));
+  v = fmaxf(v, __shfl_xor(v, 2, 64));
+  v = fmaxf(v, __shfl_xor(v, 4, 64));
+  v = fmaxf(v, __shfl_xor(v, 8, 64));
+  return v;
+}

@@ -1,0 +1,93 @@
+// Launch interface between the C-ABI layer (api.cpp) and the HIP kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+// Windows are addressed by a flat index n = b * n_steps + s over (stream, step);
+// a launch covers n0 .. n0 + N - 1.  Window n reads bytes
+// streams[b*stride + pos0 + s - W .. + W - 1] and targets streams[b*stride + pos0 + s].
+struct WinArgs {
+  const uint8_t* streams;
+  int64_t stride, pos0;
+  int32_t n_steps;
+  int64_t n0, N;
+};
+
+struct AttnArgs {
+  WinArgs w;
+  const void* E;  // operand copy [256][e]
+  const void* P;  // operand copy [T][D] (zeros when the positional table is off)
+  int32_t e, g;
+  const uint4 *Wq, *Wk, *Wv, *Wo;  // packed operand copies
+  float* h0;                       // [N][D]: Attn + X, the residual stream entering the FFN
+  float scale;                     // 1/sqrt(head width)
+  // kept activations for the backward (all NULL unless kept), indexed by local window
+  uint8_t* kwin;  // [N][W]
+  float* kq;      // [N][D]     query of the last token
+  float* kK;      // [N][T][D]
+  float* kV;      // [N][T][D]
+  float* kA;      // [N][H][T]  attention weights of the last row
+  float* kO;      // [N][D]     attention output as the operand of Wo
+};
+
+struct FfnArgs {
+  WinArgs w;
+  const float* h0;                 // [N][D]
+  const uint4 *W1, *W2, *Wout;     // packed operand copies
+  const float* bout;               // [256]
+  int32_t F, k;
+  float* bits;                     // [n0 + N] global window index
+  float* logits;                   // nullable, [n0 + N][256]
+  float* kY;                       // nullable, [k+1][N][D]: Y_0 .. Y_k (fp32)
+  float* kU;                       // nullable, [k][N][F]
+  float* kZ;                       // nullable, [N][256]
+  int32_t* ktgt;                   // nullable, [N]
+};
+
+typedef void (*attn_fn)(const AttnArgs&, hipStream_t);
+typedef void (*ffn_fn)(const FfnArgs&, hipStream_t);
+
+// NULL when no kernel is built for the shape.
+attn_fn find_attn(bool bf, int T, int D, int DH);
+ffn_fn find_ffn(bool bf, int D);
+
+void launch_pack(bool bf, const float* W, int K, int N, void* out, hipStream_t s);
+void launch_zero(void* p, int64_t n32, hipStream_t s);
+void launch_cvt(bool bf, const float* src, void* dst, int64_t n, hipStream_t s);
+void launch_step_ce(const float* bits, int32_t n_streams, int32_t n_steps, double* out, hipStream_t s);
+void launch_gather(bool bf, const WinArgs& w, const void* E, const void* P, int T, int D, int e, int g, float* X,
+                   hipStream_t s);
+
+// ---- backward building blocks (bwd.hip) ----
+struct GemmArgs {
+  int M, N, K;
+  const float* A;
+  int64_t sam, sak;  // A(m,k) = A[m*sam + k*sak]
+  const float* B;
+  int64_t sbk, sbn;  // B(k,n) = B[k*sbk + n*sbn]
+  float* C;
+  int64_t ldc;       // C(m,n) = C[m*ldc + n]
+  int roundA, roundB;  // round that operand to bf16 (RNE) as it is read
+  float beta;          // C = beta*C + A.B  (beta 0 or 1)
+};
+// Deterministic: split-K partials are summed in a fixed order.  The split count
+// depends only on (M, N, K, ws_cap); gemm_ws_floats(M, N, K) floats let it
+// reach its preferred value.
+int64_t gemm_ws_floats(int M, int N, int K);
+void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s);
+
+void launch_colsum(const float* in, int64_t rows, int64_t cols, int64_t ld, float* out, float beta, float* ws,
+                   hipStream_t s);
+int64_t colsum_ws_floats(int64_t cols);
+void launch_ce_grad(const float* z, const int32_t* tgt, int64_t N, float* dz, hipStream_t s);
+void launch_gelu_fwd_round(const float* U, float* G, int64_t n, int round, hipStream_t s);
+void launch_gelu_bwd(const float* dG, const float* U, float* dU, int64_t n, hipStream_t s);
+void launch_attn_bwd(const float* dO, const float* q, const float* K, const float* V, const float* A, int64_t N, int T,
+                     int D, int H, float scale, int round_dO, float* dQ, float* dK, float* dV, hipStream_t s);
+void launch_add(float* y, const float* x, int64_t rows, int64_t cols, int64_t ldy, int64_t ldx, hipStream_t s);
+void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int g, int e, int D, float* dE,
+                      hipStream_t s);
+void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, const void* P, int T, int D, int e,
+                        int g, float* X, hipStream_t s);
+void launch_adam(float* theta, const float* grad, float* m, float* v, int64_t n, float lr, float b1, float b2,
+                 float eps, float bc1, float bc2, hipStream_t s);

@@ -1,0 +1,162 @@
+"""Forward parity of the HIP path (through the C ABI) against the CPU oracle.
+
+Inputs are the seeded synthetic streams of the five workloads (prefixes of
+them where the full size is not needed) and weights from the shared seeded
+initialiser.  fp32 models are compared with the oracle in fp64, bf16 models
+with the oracle emulating the bf16 storage points."""
+import numpy as np
+import pytest
+import torch
+
+import oracle as O
+import synth
+from gpu_helpers import check_parity, make_model, ocfg, oracle_mode, to_dev, workload_cfg
+
+pytestmark = pytest.mark.gpu
+
+
+def _oracle_at(shape, flat, streams, b, i, mode, use_pos=True):
+    cfg = ocfg(**shape, use_pos=use_pos)
+    w, y = O.windows_at(streams, b, i, cfg.W)
+    return O.forward(flat, cfg, w, y, mode=mode)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+@pytest.mark.parametrize("shape", [dict(W=16, e=16, g=4, H=1, F=256, k=2), dict(W=64, e=64, g=8, H=8, F=256, k=1),
+                                   dict(W=32, e=32, g=4, H=4, F=256, k=1)])
+def test_byte_group_gather_is_bit_exact(dtype, shape):
+    if dtype == "fp32" and shape["e"] * shape["g"] == 512:
+        pytest.skip("no fp32 kernel at d=512")
+    m = make_model(shape, dtype, seed=5)
+    streams = synth.random_streams(11, 7, 300)
+    n_steps = 300 - shape["W"] - 5
+    X = m.debug_gather(to_dev(streams), shape["W"], n_steps).cpu().numpy()
+    cfg = ocfg(**shape)
+    flat = O.init_flat(cfg, 5)
+    mode = "fp32" if dtype == "fp32" else "bf16"
+    p = O.compute_params(flat, cfg, mode)
+    w, _ = O.all_windows(streams, cfg.W, shape["W"], n_steps)
+    mo = O.trace_oracle._Mode(mode)
+    Xref = mo.R(O.embed_group(p, w, cfg, mo))
+    assert np.array_equal(X.reshape(Xref.shape).view(np.uint32), Xref.astype(np.float32).view(np.uint32))
+
+
+def test_workload1_every_window():
+    """Workload 1 (tiny fp32) in full: 16 streams x 4080 windows."""
+    shape, dtype = workload_cfg(1)
+    streams, _ = synth.workload_streams(1)
+    m = make_model(shape, dtype, seed=0x7ACE1001)
+    B, L = streams.shape
+    W = shape["W"]
+    out = m.forward_bits(to_dev(streams), W, L - W, logits=True, step_ce=True)
+    bits = out["bits"].cpu().numpy()
+    z = out["logits"].cpu().numpy()
+    flat = O.init_flat(ocfg(**shape), 0x7ACE1001)
+    cfg = ocfg(**shape)
+    w, y = O.all_windows(streams, W)
+    ref = O.forward(flat, cfg, w, y, mode="fp64")
+    check_parity(dtype, z, bits, ref)
+    ce = out["step_ce"].cpu().numpy()
+    np.testing.assert_allclose(ce, bits.reshape(B, L - W).astype(np.float64).mean(0), rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("wid,L,B", [(2, 4096, 512), (3, 2048, 4096), (4, 2048, 4096), (5, 1024, 8192)])
+def test_workload_sampled_windows(wid, L, B):
+    """Every window of a prefix of the workload's streams on the GPU; 2048 seeded
+    windows of the result compared with the oracle one by one."""
+    shape, dtype = workload_cfg(wid)
+    streams, _ = synth.workload_streams(wid, L=L, B=B)
+    seed = 0x7ACE1000 + wid
+    m = make_model(shape, dtype, seed=seed, max_windows=1 << 18)
+    W = shape["W"]
+    n_steps = L - W
+    out = m.forward_bits(to_dev(streams), W, n_steps, logits=True)
+    torch.cuda.synchronize()
+    b, i = synth.sample_positions(100 + wid, B, L, W, 2048)
+    idx = b * n_steps + (i - W)
+    bits = out["bits"][torch.from_numpy(idx).cuda()].cpu().numpy()
+    z = out["logits"][torch.from_numpy(idx).cuda()].cpu().numpy()
+    flat = O.init_flat(ocfg(**shape), seed)
+    ref = _oracle_at(shape, flat, streams, b, i, oracle_mode(dtype))
+    check_parity(dtype, z, bits, ref)
+    assert np.all(np.isfinite(out["bits"].cpu().numpy()))
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_ragged_tiles_and_chunking_are_bitwise_invariant(dtype):
+    """Window counts that leave partial tiles, and a forward split into small
+    chunks, give the same bits bit for bit as one launch over everything."""
+    shape = dict(W=32, e=32, g=4, H=4, F=512, k=2)
+    streams = synth.random_streams(3, 37, 200)
+    n_steps = 200 - 32 - 1
+    big = make_model(shape, dtype, seed=9, max_windows=1 << 16)
+    small = make_model(shape, dtype, seed=9, max_windows=999)
+    s = to_dev(streams)
+    a = big.forward_bits(s, 32, n_steps, logits=True)
+    c = small.forward_bits(s, 32, n_steps, logits=True)
+    assert torch.equal(a["bits"], c["bits"]) and torch.equal(a["logits"], c["logits"])
+    # one stream, one step: the smallest batch
+    d = big.forward_bits(s[5:6].contiguous(), 32 + 17, 1)
+    assert torch.equal(d["bits"][0], a["bits"][5 * n_steps + 17])
+    flat = O.init_flat(ocfg(**shape), 9)
+    bb, ii = np.meshgrid(np.arange(37), 32 + np.arange(n_steps), indexing="ij")
+    ref = _oracle_at(shape, flat, streams, bb.ravel(), ii.ravel(), oracle_mode(dtype))
+    check_parity(dtype, a["logits"].cpu().numpy(), a["bits"].cpu().numpy(), ref)
+
+
+def test_permuting_streams_permutes_outputs_bitwise():
+    shape, dtype = workload_cfg(3)
+    streams, _ = synth.workload_streams(3, L=400, B=96)
+    perm = np.random.default_rng(4).permutation(96)
+    m = make_model(shape, dtype, seed=77)
+    a = m.forward_bits(to_dev(streams), 64, 400 - 64)["bits"].view(96, -1)
+    b = m.forward_bits(to_dev(streams[perm]), 64, 400 - 64)["bits"].view(96, -1)
+    assert torch.equal(a[torch.from_numpy(perm).cuda()], b)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_zeroed_head_gives_exactly_8_bits(dtype):
+    shape = dict(W=16, e=16, g=4, H=1, F=256, k=2)
+    cfg = ocfg(**shape)
+    flat = O.init_flat(cfg, 21)
+    p = O.unflatten(flat, cfg)
+    p["Wout"][:] = 0
+    p["bout"][:] = 0
+    m = make_model(shape, dtype, seed=0, flat=flat)
+    streams = synth.random_streams(8, 5, 100)
+    bits = m.forward_bits(to_dev(streams), 16, 84)["bits"].cpu().numpy()
+    assert np.all(bits == 8.0)
+
+
+@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
+def test_without_positional_table(dtype):
+    shape = dict(W=32, e=32, g=4, H=4, F=512, k=2)
+    m = make_model(shape, dtype, seed=13, use_pos=False)
+    streams = synth.random_streams(6, 9, 300)
+    out = m.forward_bits(to_dev(streams), 32, 268, logits=True)
+    cfg = ocfg(**shape, use_pos=False)
+    flat = O.init_flat(cfg, 13)
+    w, y = O.all_windows(streams, 32, 32, 268)
+    ref = O.forward(flat, cfg, w, y, mode=oracle_mode(dtype))
+    check_parity(dtype, out["logits"].cpu().numpy(), out["bits"].cpu().numpy(), ref)
+
+
+def test_argument_errors_and_empty_batches():
+    import paper_2203_16114_amd as P
+    shape = dict(W=16, e=16, g=4, H=1, F=256, k=2)
+    m = make_model(shape, "fp32", seed=1)
+    s = to_dev(synth.random_streams(1, 2, 64))
+    with pytest.raises(P.TraceError) as ei:
+        m.forward_bits(s, 15, 4)           # pos0 < W
+    assert ei.value.code == P.TRACE_EINVAL
+    with pytest.raises(P.TraceError) as ei:
+        m.forward_bits(s, 16, 4, keep=True)  # model built without max_keep
+    assert ei.value.code == P.TRACE_EINVAL
+    with pytest.raises(P.TraceError) as ei:
+        m.adapt_step()
+    assert ei.value.code == P.TRACE_ESTATE
+    out = m.forward_bits(s, 16, 0)
+    assert out["bits"].numel() == 0
+    with pytest.raises(P.TraceError) as ei:
+        P.TraceModel(W=24, e=16, g=4, H=1, F=256, k=2)  # T = 6 has no kernel
+    assert ei.value.code == P.TRACE_EUNSUPPORTED
