@@ -1,0 +1,247 @@
+#!/usr/bin/env python3
+"""Throughput of TRACE's batched next-byte estimator on one MI355X.
+
+A step is one call of the forward estimator with code lengths over a batch of
+windows of the main workload (4096 streams, W = 64 bytes, e = 32, g = 8 -> 8
+tokens of d = 256, 8 heads, FFN 1024 shared x3, bf16 operands with fp32
+accumulation): `--steps-per-call` consecutive positions of every stream, i.e.
+4096 x S windows.  Successive steps walk along the streams.  The value is
+predicted bytes (= windows) per second over the timed steps, with the streams
+already in device memory.
+
+Besides the headline line this run measures, on the adaptation workload
+(the small model in bf16 with fp32 master weights, B = 4096 windows per step,
+sources switching every 2 KiB per stream), the controller-gated update loop
+against the always-update loop, and times the CPU oracle on a bounded sample
+of the main workload's windows on this machine's cores.
+
+Prints ONE JSON line (rank 0).  Only one GPU is supported.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_TFLOPS = {"bf16": 2500.0, "fp32": 157.3}   # MI355X dense MFMA peaks
+HBM_GBS = 8000.0
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def flops_per_window(w):
+    """Algorithmic flops of the last-token readout path, split by kernel:
+    attention block 4*T*d^2 (K, V of all T tokens) + 2*d^2 (q) + 2*d^2 (Wo)
+    + 4*T*d (scores, weighted values); FFN+head 4*k*d*F + 512*d."""
+    T, d, F, k = w.T, w.d, w.F, w.k
+    return {"attn": 4 * T * d * d + 4 * d * d + 4 * T * d, "ffn_head": 4 * k * d * F + 512 * d}
+
+
+def gated_loop(model, sdev, B, pos0, n_steps, t, delta, always, max_spec=64):
+    """Alg. 1 with the controller of Alg. 2 over B streams.  Forward passes run
+    speculatively over up to max_spec steps at unchanged weights; the controller
+    walks their step cross-entropies and at the first step it flags, that step
+    is re-run keeping its activations and updated; the walk resumes after it."""
+    import torch
+    import paper_2203_16114_amd as P
+    ctl = P.Controller(t, delta)
+    dev = sdev.device
+    bits = torch.empty(B * max_spec, dtype=torch.float32, device=dev)
+    ce = torch.empty(max_spec, dtype=torch.float64, device=dev)
+    kb = torch.empty(B, dtype=torch.float32, device=dev)
+    kce = torch.empty(1, dtype=torch.float64, device=dev)
+    i, updates, spec, ce_sum = 0, 0, 1, 0.0
+    ce_dev = []
+    while i < n_steps:
+        if always:
+            model.forward_bits(sdev, pos0 + i, 1, bits=kb, step_ce=kce, keep=True)
+            model.adapt_step()
+            ce_dev.append(kce.clone())
+            i += 1
+            updates += 1
+            continue
+        S = min(spec, n_steps - i)
+        model.forward_bits(sdev, pos0 + i, S, bits=bits, step_ce=ce)
+        ces = ce[:S].cpu().numpy()
+        j = None
+        for s in range(S):
+            if ctl.decide(float(ces[s])):
+                j = s
+                break
+        used = S if j is None else j + 1
+        ce_sum += float(ces[:used].sum())
+        if j is not None:
+            model.forward_bits(sdev, pos0 + i + j, 1, bits=kb, keep=True)
+            model.adapt_step()
+            updates += 1
+            spec = 1
+        else:
+            spec = min(max_spec, spec * 2)
+        i += used
+    if ce_dev:
+        ce_sum = float(torch.cat(ce_dev).sum())
+    return updates, ce_sum / n_steps
+
+
+def measure_gated(args):
+    import torch
+    import paper_2203_16114_amd as P
+    import synth
+    w = synth.WORKLOADS[4]
+    B = w.B
+    n = args.gated_steps
+    L = min(w.L, w.W + 1 + 2 * n + 2 * 64 + 64)
+    t0 = time.time()
+    streams, _ = synth.workload_streams(4, L=L)
+    log(f"[bench] adaptation workload streams {streams.shape} in {time.time() - t0:.1f}s")
+    sdev = torch.from_numpy(streams).cuda()
+    res = {}
+    for name, always in (("gated", False), ("always_update", True)):
+        m = P.TraceModel(w.W, w.e, w.g, w.H, w.F, w.k, dtype=w.dtype, max_windows=B * 64, max_keep=B)
+        m.init_weights(w.weight_seed)
+        gated_loop(m, sdev, B, w.W, 8, w.t, w.delta, always)      # warm-up, then a fresh start
+        m.init_weights(w.weight_seed)
+        torch.cuda.synchronize()
+        m.set_timing(True)
+        t0 = time.perf_counter()
+        upd, bpb = gated_loop(m, sdev, B, w.W + 8, n, w.t, w.delta, always)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        tm = m.read_timing()
+        m.set_timing(False)
+        res[name] = {"bytes_per_s": B * n / dt, "steps": n, "updates": upd, "update_fraction": upd / n,
+                     "bits_per_byte": bpb,
+                     "kernel_ms": {k: round(v[0], 3) for k, v in tm.items() if k != "overflow" and v[1]},
+                     "kernel_launches": {k: v[1] for k, v in tm.items() if k != "overflow" and v[1]}}
+        if tm.get("adam", (0, 0))[1]:
+            ms = tm["adam"][0] / tm["adam"][1]
+            res[name]["adam_hbm_frac"] = (28.0 * m.n_params / (ms * 1e-3)) / (HBM_GBS * 1e9)
+        log(f"[bench] {name}: {res[name]['bytes_per_s']:.4g} B/s, updates {upd}/{n}")
+        m.close()
+    res["speedup_gated_vs_always"] = res["gated"]["bytes_per_s"] / res["always_update"]["bytes_per_s"]
+    res["workload"] = f"{w.name}: B={B} windows/step, W={w.W} e={w.e} g={w.g} d={w.d} H={w.H} F={w.F} k={w.k}, " \
+                      f"t={w.t} delta={w.delta}"
+    return res
+
+
+def cpu_baseline(streams, w, n_windows):
+    import numpy as np
+    import oracle as O
+    import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([x.get("num_threads", 1) for x in threadpool_info()] or [1])
+    except Exception:
+        threads = None
+    cores = len(os.sched_getaffinity(0))
+    cfg = O.Config(W=w.W, e=w.e, g=w.g, H=w.H, F=w.F, k=w.k)
+    flat = O.init_flat(cfg, w.weight_seed)
+    b, i = synth.sample_positions(0xBA5E, streams.shape[0], streams.shape[1], w.W, n_windows)
+    win, y = O.windows_at(streams, b, i, w.W)
+    mode = "bf16" if w.dtype == "bf16" else "fp64"
+    t0 = time.perf_counter()
+    O.forward(flat, cfg, win, y, mode=mode)
+    dt = time.perf_counter() - t0
+    return {"value": n_windows / dt, "unit": "bytes/s", "cores": threads or cores, "kind": "oracle",
+            "sample": f"{n_windows} seeded windows of the {w.name} streams, oracle forward + code length in "
+                      f"{mode} mode (numpy, {threads} BLAS threads on {cores} host cores), {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=40)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--steps-per-call", type=int, default=256, help="positions per stream in one step")
+    ap.add_argument("--full", action="store_true", help="generate the full 256 KiB streams")
+    ap.add_argument("--gated-steps", type=int, default=256, help="steps of the gated-adaptation run (0: skip)")
+    ap.add_argument("--cpu-windows", type=int, default=2048, help="oracle sample (0: skip)")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU only: this build has no multi-GPU path "
+              "(--gpus must be 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import paper_2203_16114_amd as P
+    import synth
+
+    w = synth.WORKLOADS[3]
+    B, S, K = w.B, args.steps_per_call, args.steps
+    need = w.W + (args.warmup + K) * S + 1
+    if need > w.L:
+        raise SystemExit(f"steps x steps-per-call exceed the stream length {w.L}")
+    L = w.L if args.full else need
+    t0 = time.time()
+    streams, _ = synth.workload_streams(3, L=L)
+    log(f"[bench] main workload streams {streams.shape} in {time.time() - t0:.1f}s")
+    sdev = torch.from_numpy(streams).cuda()
+    model = P.TraceModel(w.W, w.e, w.g, w.H, w.F, w.k, dtype=w.dtype, max_windows=B * S)
+    model.init_weights(w.weight_seed)
+    bits = torch.empty(B * S, dtype=torch.float32, device="cuda")
+    ce = torch.empty(K + args.warmup, S, dtype=torch.float64, device="cuda")
+    pos = w.W
+    for i in range(args.warmup):
+        model.forward_bits(sdev, pos, S, bits=bits, step_ce=ce[i])
+        pos += S
+    torch.cuda.synchronize()
+    model.set_timing(True)
+    model.read_timing()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    ev0.record()
+    for i in range(K):
+        model.forward_bits(sdev, pos, S, bits=bits, step_ce=ce[args.warmup + i])
+        pos += S
+    ev1.record()
+    torch.cuda.synchronize()
+    ms = ev0.elapsed_time(ev1)
+    tm = model.read_timing()
+    model.set_timing(False)
+    windows = B * S * K
+    value = windows / (ms * 1e-3)
+    bpb = float(ce[args.warmup:].mean())
+    log(f"[bench] main: {K} steps x {B * S} windows in {ms:.1f} ms -> {value:.4g} bytes/s; {tm}")
+
+    fpw = flops_per_window(w)
+    per = {k: tm[k][0] / max(tm[k][1], 1) for k in ("attn", "ffn_head")}
+    dom = max(per, key=lambda k: tm[k][0])
+    wpl = B * S
+    achieved = fpw[dom] * wpl / (per[dom] * 1e-3) / 1e12
+    peak = PEAK_TFLOPS[w.dtype]
+    total_tflops = (fpw["attn"] + fpw["ffn_head"]) * value / 1e12
+    roofline = {"bound": "mfma", "kernel": "k_ffn_head" if dom == "ffn_head" else "k_attn",
+                "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                "traffic": None,
+                "flops_per_window": fpw[dom], "windows_per_launch": wpl, "avg_launch_ms": round(per[dom], 4),
+                "kernels": {k: {"avg_launch_ms": round(per[k], 4),
+                                "tflops": round(fpw[k] * wpl / (per[k] * 1e-3) / 1e12, 2)} for k in per},
+                "path_tflops": round(total_tflops, 2), "path_frac": round(total_tflops / peak, 4)}
+
+    out = {"metric": "bytes/sec estimated (fwd+bits) and with gated adapt; MFMA util; bits/byte",
+           "value": value, "unit": "bytes/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
+           "ms_per_step": ms / K, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
+           "dtype": "bf16", "data": "synthetic",
+           "config": {"workload": f"{w.name}: B={B} streams x {w.L} bytes (order-3 Markov Dirichlet(0.02) / "
+                                  f"Zipf(1.2) / uniform thirds), W={w.W} e={w.e} g={w.g} -> T={w.T} d={w.d}, "
+                                  f"H={w.H}, F={w.F} shared x{w.k}, bf16 operands fp32 accumulate",
+                      "windows_per_step": B * S, "steps_per_call": S, "stream_prefix_bytes": L},
+           "bits_per_byte": bpb, "mfma_util": roofline["path_frac"], "roofline": roofline}
+    if args.gated_steps > 0:
+        out["gated_adapt"] = measure_gated(args)
+    if args.cpu_windows > 0:
+        out["cpu_baseline"] = cpu_baseline(streams, w, args.cpu_windows)
+        log(f"[bench] cpu oracle: {out['cpu_baseline']['value']:.4g} bytes/s")
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -161,6 +161,24 @@ int trace_get_grads(trace_model* m, float* host_out, int64_t n);
 int trace_debug_gather(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams, int64_t pos0,
                        int32_t n_steps, float* d_X, void* stream);
 
+/* Per-kernel timing with HIP events recorded on the caller's stream around each
+ * launch (measurement support; off by default).  While enabled, every kernel
+ * launch of the calls above is bracketed by two events; trace_read_timing waits
+ * for them, returns per-kind totals (milliseconds) and launch counts in arrays
+ * of TRACE_NKINDS entries, and starts a new measurement.  At most 65536 launches
+ * are recorded between reads; later ones are counted in overflow. */
+enum {
+  TRACE_KIND_ATTN = 0,      /* fused gather + attention block                 */
+  TRACE_KIND_FFN_HEAD = 1,  /* fused shared FFN x k + softmax head            */
+  TRACE_KIND_STEP_CE = 2,   /* per-step mean code length                      */
+  TRACE_KIND_BACKWARD = 3,  /* gradient of one gated update (all its kernels) */
+  TRACE_KIND_ADAM = 4,      /* the Adam update                                */
+  TRACE_KIND_REFRESH = 5,   /* operand copies refreshed from the master       */
+  TRACE_NKINDS = 6
+};
+int trace_set_timing(trace_model* m, int enable);
+int trace_read_timing(trace_model* m, double* ms_total, int64_t* launches, int64_t* overflow);
+
 const char* trace_strerror(int code);
 const char* trace_last_error(void); /* thread-local text of the last failure ("" if none) */
 

@@ -23,8 +23,9 @@ TRACE_KEEP_ACTS = 1
 
 EXPORTS = ("trace_create", "trace_destroy", "trace_param_count", "trace_init_weights", "trace_init_flat_host",
            "trace_forward_bits", "trace_adapt_step", "trace_controller_init", "trace_controller_decide",
-           "trace_get_state", "trace_set_state", "trace_get_grads", "trace_debug_gather", "trace_strerror",
-           "trace_last_error")
+           "trace_get_state", "trace_set_state", "trace_get_grads", "trace_debug_gather", "trace_set_timing",
+           "trace_read_timing", "trace_strerror", "trace_last_error")
+KINDS = ("attn", "ffn_head", "step_ce", "backward", "adam", "refresh")
 
 
 class TraceError(RuntimeError):
@@ -70,6 +71,8 @@ def lib():
             "trace_set_state": (c_int32, [P, P, P, P, c_int64, c_int64]),
             "trace_get_grads": (c_int32, [P, P, c_int64]),
             "trace_debug_gather": (c_int32, [P, P, c_int64, c_int32, c_int64, c_int32, P, P]),
+            "trace_set_timing": (c_int32, [P, c_int32]),
+            "trace_read_timing": (c_int32, [P, P, P, POINTER(c_int64)]),
             "trace_strerror": (ctypes.c_char_p, [c_int32]),
             "trace_last_error": (ctypes.c_char_p, []),
         }
@@ -212,6 +215,19 @@ class TraceModel:
     def grads(self) -> np.ndarray:
         out = np.empty(self.n_params, np.float32)
         check(lib().trace_get_grads(self._h, out.ctypes.data, self.n_params))
+        return out
+
+    def set_timing(self, enable: bool):
+        check(lib().trace_set_timing(self._h, int(bool(enable))))
+
+    def read_timing(self):
+        """{kind: (total ms, launches)} since the last read (synchronises)."""
+        ms = np.zeros(len(KINDS), np.float64)
+        n = np.zeros(len(KINDS), np.int64)
+        ov = c_int64()
+        check(lib().trace_read_timing(self._h, ms.ctypes.data, n.ctypes.data, byref(ov)))
+        out = {k: (float(ms[i]), int(n[i])) for i, k in enumerate(KINDS)}
+        out["overflow"] = ov.value
         return out
 
     def debug_gather(self, streams, pos0: int, n_steps: int, stream=None):

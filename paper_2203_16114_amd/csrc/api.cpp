@@ -38,6 +38,12 @@ struct trace_model {
   float *dz, *dY, *dG, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *gws, *cws;
   int64_t gws_cap;
   std::vector<void*> allocs;
+  // event timing (trace_set_timing)
+  bool timing;
+  std::vector<hipEvent_t> events;
+  size_t ev_used;
+  std::vector<int> ev_kind;  // kind of the launch bracketed by events 2i, 2i+1
+  int64_t overflow;
 };
 
 namespace {
@@ -67,6 +73,8 @@ bool dalloc(trace_model* m, P** p, int64_t bytes) {
 void free_all(trace_model* m) {
   for (void* p : m->allocs) (void)hipFree(p);
   m->allocs.clear();
+  for (hipEvent_t e : m->events) (void)hipEventDestroy(e);
+  m->events.clear();
 }
 
 // Largest split-K workspace over the GEMMs of trace_adapt_step.
@@ -82,8 +90,35 @@ int64_t adapt_gemm_ws(const trace_model* m, int64_t N) {
 
 hipStream_t S(void* s) { return (hipStream_t)s; }
 
+constexpr size_t MAX_TIMED = 65536;
+
+// Starts a timed region of `kind` on stream s; returns its index or -1.
+long tbegin(trace_model* m, hipStream_t s) {
+  if (!m->timing) return -1;
+  if (m->ev_kind.size() >= MAX_TIMED) {
+    m->overflow += 1;
+    return -1;
+  }
+  while (m->events.size() < m->ev_used + 2) {
+    hipEvent_t e;
+    if (hipEventCreate(&e) != hipSuccess) return -1;
+    m->events.push_back(e);
+  }
+  const long i = (long)m->ev_kind.size();
+  (void)hipEventRecord(m->events[m->ev_used], s);
+  m->ev_used += 2;
+  m->ev_kind.push_back(-1);
+  return i;
+}
+void tend(trace_model* m, long i, int kind, hipStream_t s) {
+  if (i < 0) return;
+  (void)hipEventRecord(m->events[2 * i + 1], s);
+  m->ev_kind[i] = kind;
+}
+
 // Refresh the operand copies from the fp32 master.
 void refresh_operands(trace_model* m, hipStream_t s) {
+  const long tk = tbegin(m, s);
   const Layout& L = m->L;
   const int D = L.D, F = m->cfg.F;
   const float* th = m->theta;
@@ -99,6 +134,7 @@ void refresh_operands(trace_model* m, hipStream_t s) {
   launch_pack(m->bf, th + L.off[P_W1], D, F, m->W1, s);
   launch_pack(m->bf, th + L.off[P_W2], F, D, m->W2, s);
   launch_pack(m->bf, th + L.off[P_WOUT], D, 256, m->Wout, s);
+  tend(m, tk, TRACE_KIND_REFRESH, s);
 }
 
 GemmArgs gemm(int M, int N, int K, const float* A, int64_t sam, int64_t sak, int rA, const float* B, int64_t sbk,
@@ -291,10 +327,18 @@ extern "C" int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int6
       f.kZ = m->kZ;
       f.ktgt = m->ktgt;
     }
+    long tk = tbegin(m, s);
     m->attn(a, s);
+    tend(m, tk, TRACE_KIND_ATTN, s);
+    tk = tbegin(m, s);
     m->ffn(f, s);
+    tend(m, tk, TRACE_KIND_FFN_HEAD, s);
   }
-  if (d_step_ce && n_streams > 0) launch_step_ce(d_bits, n_streams, n_steps, d_step_ce, s);
+  if (d_step_ce && n_streams > 0) {
+    const long tk = tbegin(m, s);
+    launch_step_ce(d_bits, n_streams, n_steps, d_step_ce, s);
+    tend(m, tk, TRACE_KIND_STEP_CE, s);
+  }
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "trace_forward_bits");
   if (keep) {
@@ -314,6 +358,7 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   float* th = m->theta;
   float* gr = m->grad;
   float* ws = m->gws;
+  const long tk = tbegin(m, s);
   // head: dz = (softmax(z) - onehot) / N
   launch_ce_grad(m->kZ, m->ktgt, N, m->dz, s);
   // dWout = h_k^T . dz ; dbout = sum_n dz ; dY_k = dz . Wout^T
@@ -359,12 +404,15 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   else
     launch_zero(gr + L.off[P_P], L.size[P_P], s);
   launch_embed_bwd(m->kwin, m->dX, N, m->cfg.W, m->cfg.g, m->cfg.e, D, gr + L.off[P_E], s);
+  tend(m, tk, TRACE_KIND_BACKWARD, s);
   // Adam on the flat master, then new operand copies
   m->step += 1;
   const float bc1 = (float)(1.0 - std::pow(m->cfg.beta1, (double)m->step));
   const float bc2 = (float)(1.0 - std::pow(m->cfg.beta2, (double)m->step));
+  const long ta = tbegin(m, s);
   launch_adam(th, gr, m->am, m->av, L.n, (float)m->cfg.lr, (float)m->cfg.beta1, (float)m->cfg.beta2,
               (float)m->cfg.eps, bc1, bc2, s);
+  tend(m, ta, TRACE_KIND_ADAM, s);
   refresh_operands(m, s);
   m->kept = false;
   const hipError_t e = hipGetLastError();
@@ -428,4 +476,37 @@ extern "C" int trace_debug_gather(trace_model* m, const uint8_t* d_streams, int6
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "trace_debug_gather");
   return TRACE_OK;
+}
+
+extern "C" int trace_set_timing(trace_model* m, int enable) {
+  if (!m) return fail(TRACE_EINVAL, "model is NULL");
+  m->timing = enable != 0;
+  return TRACE_OK;
+}
+
+extern "C" int trace_read_timing(trace_model* m, double* ms_total, int64_t* launches, int64_t* overflow) {
+  if (!m || !ms_total || !launches) return fail(TRACE_EINVAL, "model or output is NULL");
+  for (int k = 0; k < TRACE_NKINDS; ++k) {
+    ms_total[k] = 0.0;
+    launches[k] = 0;
+  }
+  int rc = TRACE_OK;
+  for (size_t i = 0; i < m->ev_kind.size(); ++i) {
+    const int kind = m->ev_kind[i];
+    if (kind < 0) continue;
+    hipError_t e = hipEventSynchronize(m->events[2 * i + 1]);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, m->events[2 * i], m->events[2 * i + 1]);
+    if (e != hipSuccess) {
+      rc = hip_fail(e, "trace_read_timing");
+      break;
+    }
+    ms_total[kind] += ms;
+    launches[kind] += 1;
+  }
+  if (overflow) *overflow = m->overflow;
+  m->ev_kind.clear();
+  m->ev_used = 0;
+  m->overflow = 0;
+  return rc;
 }

@@ -364,11 +364,12 @@ void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, c
 // -------------------------------------------------------------------- Adam ----
 // Kingma & Ba, Alg. 1, with the bias corrections bc1 = 1 - beta1^t and
 // bc2 = 1 - beta2^t supplied by the host.  Each product and sum is rounded on
-// its own (no fused multiply-add), in the order m = b1*m + (1-b1)*g,
+// its own (contraction into fused multiply-adds is off), in the order m = b1*m + (1-b1)*g,
 // v = b2*v + ((1-b2)*g)*g, theta -= (lr * m/bc1) / (sqrt(v/bc2) + eps).
 __global__ void k_adam(float* __restrict__ theta, const float* __restrict__ grad, float* __restrict__ m,
                        float* __restrict__ v, int64_t n, float lr, float b1, float b2, float eps, float bc1,
                        float bc2) {
+#pragma clang fp contract(off)
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= n) return;
   const float g = grad[i];
@@ -379,7 +380,10 @@ __global__ void k_adam(float* __restrict__ theta, const float* __restrict__ grad
   v[i] = vi;
   const float mhat = __fdiv_rn(mi, bc1);
   const float vhat = __fdiv_rn(vi, bc2);
-  const float step = __fdiv_rn(__fmul_rn(lr, mhat), __fadd_rn(__fsqrt_rn(vhat), eps));
+  // correctly rounded sqrt: the fp64 root rounded once to fp32 (53 >= 2*24 + 2
+  // bits, so the two roundings give the singly rounded result)
+  const float root = (float)__dsqrt_rn((double)vhat);
+  const float step = __fdiv_rn(__fmul_rn(lr, mhat), __fadd_rn(root, eps));
   theta[i] = __fsub_rn(theta[i], step);
 }
 void launch_adam(float* theta, const float* grad, float* m, float* v, int64_t n, float lr, float b1, float b2,
