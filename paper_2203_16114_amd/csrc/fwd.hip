@@ -4,10 +4,11 @@
 // softmax head giving the code length -log2 p(next byte) (Alg. 2, line 3).
 //
 // Two fused kernels per chunk of windows:
-//   k_attn      bytes -> tokens X (LDS) -> q (last token), K/V per head (MFMA)
-//               -> softmax over the T keys -> O (LDS) -> O.Wo + X_last = h0 (HBM)
-//   k_ffn_head  h0 -> k x [h += GELU(h.W1).W2] with F streamed in chunks, h kept
-//               in accumulator registers -> z = h.Wout + bout -> bits (HBM)
+//   k_attn      (this file) bytes -> tokens X (LDS) -> q (last token), K/V per
+//               head (MFMA) -> softmax over the T keys -> O (LDS) -> O.Wo + X_last
+//               = h0 (HBM)
+//   k_ffn_head  (ffn.hip) h0 -> k x [h += GELU(h.W1).W2] with F streamed in
+//               chunks, h kept in accumulator registers -> z = h.Wout + bout -> bits
 // Weights are read from L2 in a fragment-packed layout (see k_pack), one 16-byte
 // load per lane per 16x16 fragment; activations stay in LDS or registers.  The
 // only per-window HBM traffic is the window bytes, h0 (d floats written and read
@@ -15,12 +16,7 @@
 #include "kcommon.h"
 #include "kernels.h"
 
-__device__ __forceinline__ int64_t target_offset(const WinArgs& w, int64_t n_local) {
-  int64_t gn = w.n0 + n_local;
-  int64_t b = gn / w.n_steps;
-  int64_t s = gn - b * w.n_steps;
-  return b * w.stride + w.pos0 + s;
-}
+#include "win.h"
 
 // ------------------------------------------------------------------ packing ----
 // W [K][N] row-major fp32 -> fragment-packed operand copy: fragment (ks, nb) is
@@ -341,196 +337,6 @@ __global__ __launch_bounds__(256) void k_attn(AttnArgs a) {
   }
 }
 
-// --------------------------------------------------- shared FFN + softmax head ----
-// One workgroup (4 waves) per tile of MB windows.  Wave w owns columns
-// [w*D/4, (w+1)*D/4) of the residual stream h, held in MFMA accumulators for the
-// whole kernel, so the residual adds of Eq. 4 / Sec. 4.3 are the accumulator's
-// initial value.  For each of the k repeats, F is streamed in chunks of FC:
-// U = bf(h).W1[:, chunk] (waves split the chunk columns), GELU into LDS, then
-// h += GELU(U).W2[chunk, :].  The head z = bf(h).Wout + bout is split over the
-// waves by column; the row max and the sum of exponentials are combined
-// through LDS in a fixed order.
-template <bool BF, int D, int MB, int FC>
-__global__ __launch_bounds__(256) void k_ffn_head(FfnArgs a) {
-  typedef Mma<BF> M;
-  typedef typename M::T OT;
-  constexpr int YSTR = D * (int)sizeof(OT) + 16;
-  constexpr int GSTR = FC * (int)sizeof(OT) + 16;
-  constexpr int RFM = MB / 16;
-  constexpr int NFY = D / 64;
-  constexpr int NFU = FC / 64;
-  constexpr int KD = D / M::KS;
-  constexpr int KC = FC / M::KS;
-  constexpr int NB2 = D / 16;
-  static_assert(MB % 16 == 0 && D % 64 == 0 && FC % 64 == 0, "shape");
-  __shared__ __align__(16) unsigned char Ys[MB * YSTR];
-  __shared__ __align__(16) unsigned char Gs[MB * GSTR];
-  __shared__ float red[2][4][MB];
-  __shared__ float zy[MB];
-  __shared__ int tg[MB];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lg = lane >> 4, lc = lane & 15;
-  const int64_t tile0 = (int64_t)blockIdx.x * MB;
-  const int64_t N = a.w.N;
-  const int F = a.F;
-  const int NB1 = F / 16;
-
-  f32x4 y[RFM][NFY];
-#pragma unroll
-  for (int rf = 0; rf < RFM; ++rf)
-#pragma unroll
-    for (int nf = 0; nf < NFY; ++nf)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const int64_t n = tile0 + rf * 16 + 4 * lg + r;
-        const int col = wave * (D / 4) + nf * 16 + lc;
-        y[rf][nf][r] = (n < N) ? a.h0[n * D + col] : 0.f;
-      }
-  if (tid < MB) {
-    const int64_t n = tile0 + tid;
-    int v = 0;
-    if (n < N) {
-      v = a.w.streams[target_offset(a.w, n)];
-      if (a.ktgt) a.ktgt[n] = v;
-    }
-    tg[tid] = v;
-  }
-
-  for (int rep = 0; rep <= a.k; ++rep) {
-    // keep Y_rep and stage its operand copy
-#pragma unroll
-    for (int rf = 0; rf < RFM; ++rf)
-#pragma unroll
-      for (int nf = 0; nf < NFY; ++nf)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int m = rf * 16 + 4 * lg + r;
-          const int col = wave * (D / 4) + nf * 16 + lc;
-          const int64_t n = tile0 + m;
-          if (a.kY && n < N) a.kY[((int64_t)rep * N + n) * D + col] = y[rf][nf][r];
-          ((OT*)(Ys + m * YSTR))[col] = M::cvt(y[rf][nf][r]);
-        }
-    __syncthreads();
-    if (rep == a.k) break;
-    for (int c0 = 0; c0 < F; c0 += FC) {
-      f32x4 u[RFM][NFU];
-#pragma unroll
-      for (int rf = 0; rf < RFM; ++rf)
-#pragma unroll
-        for (int nf = 0; nf < NFU; ++nf) u[rf][nf] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int nb0 = c0 / 16 + wave * NFU;
-      for (int ks = 0; ks < KD; ++ks) {
-        uint4 bw[NFU];
-#pragma unroll
-        for (int nf = 0; nf < NFU; ++nf) bw[nf] = a.W1[(ks * NB1 + nb0 + nf) * 64 + lane];
-#pragma unroll
-        for (int rf = 0; rf < RFM; ++rf) {
-          const uint4 af = *(const uint4*)(Ys + (rf * 16 + lc) * YSTR + ks * 64 + lg * 16);
-#pragma unroll
-          for (int nf = 0; nf < NFU; ++nf) M::run(u[rf][nf], af, bw[nf]);
-        }
-      }
-#pragma unroll
-      for (int rf = 0; rf < RFM; ++rf)
-#pragma unroll
-        for (int nf = 0; nf < NFU; ++nf)
-#pragma unroll
-          for (int r = 0; r < 4; ++r) {
-            const int m = rf * 16 + 4 * lg + r;
-            const int cl = wave * (FC / 4) + nf * 16 + lc;
-            const float uv = u[rf][nf][r];
-            const int64_t n = tile0 + m;
-            if (a.kU && n < N) a.kU[((int64_t)rep * N + n) * F + c0 + cl] = uv;
-            ((OT*)(Gs + m * GSTR))[cl] = M::cvt(gelu_f(uv));
-          }
-      __syncthreads();
-      const int kc0 = c0 / M::KS;
-      for (int ks = 0; ks < KC; ++ks) {
-        uint4 bw[NFY];
-#pragma unroll
-        for (int nf = 0; nf < NFY; ++nf) bw[nf] = a.W2[((kc0 + ks) * NB2 + wave * NFY + nf) * 64 + lane];
-#pragma unroll
-        for (int rf = 0; rf < RFM; ++rf) {
-          const uint4 af = *(const uint4*)(Gs + (rf * 16 + lc) * GSTR + ks * 64 + lg * 16);
-#pragma unroll
-          for (int nf = 0; nf < NFY; ++nf) M::run(y[rf][nf], af, bw[nf]);
-        }
-      }
-      __syncthreads();
-    }
-  }
-
-  // head: z = bf(h_k) . Wout + bout, then the code length of the target
-  f32x4 z[RFM][4];
-#pragma unroll
-  for (int rf = 0; rf < RFM; ++rf)
-#pragma unroll
-    for (int nf = 0; nf < 4; ++nf) z[rf][nf] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int ks = 0; ks < KD; ++ks) {
-    uint4 bw[4];
-#pragma unroll
-    for (int nf = 0; nf < 4; ++nf) bw[nf] = a.Wout[(ks * 16 + wave * 4 + nf) * 64 + lane];
-#pragma unroll
-    for (int rf = 0; rf < RFM; ++rf) {
-      const uint4 af = *(const uint4*)(Ys + (rf * 16 + lc) * YSTR + ks * 64 + lg * 16);
-#pragma unroll
-      for (int nf = 0; nf < 4; ++nf) M::run(z[rf][nf], af, bw[nf]);
-    }
-  }
-#pragma unroll
-  for (int nf = 0; nf < 4; ++nf) {
-    const float bo = a.bout[wave * 64 + nf * 16 + lc];
-#pragma unroll
-    for (int rf = 0; rf < RFM; ++rf)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) z[rf][nf][r] += bo;
-  }
-#pragma unroll
-  for (int rf = 0; rf < RFM; ++rf)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = rf * 16 + 4 * lg + r;
-      float mx = fmaxf(fmaxf(z[rf][0][r], z[rf][1][r]), fmaxf(z[rf][2][r], z[rf][3][r]));
-      mx = wave_max16(mx);
-      if (lc == 0) red[0][wave][m] = mx;
-#pragma unroll
-      for (int nf = 0; nf < 4; ++nf)
-        if (wave * 64 + nf * 16 + lc == tg[m]) zy[m] = z[rf][nf][r];
-    }
-  __syncthreads();
-#pragma unroll
-  for (int rf = 0; rf < RFM; ++rf)
-#pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = rf * 16 + 4 * lg + r;
-      const float mx = fmaxf(fmaxf(red[0][0][m], red[0][1][m]), fmaxf(red[0][2][m], red[0][3][m]));
-      float se = 0.f;
-#pragma unroll
-      for (int nf = 0; nf < 4; ++nf) se += expf(z[rf][nf][r] - mx);
-      se = wave_sum16(se);
-      if (lc == 0) red[1][wave][m] = se;
-      const int64_t n = tile0 + m;
-      if (n < N) {
-#pragma unroll
-        for (int nf = 0; nf < 4; ++nf) {
-          const int col = wave * 64 + nf * 16 + lc;
-          if (a.logits) a.logits[(a.w.n0 + n) * 256 + col] = z[rf][nf][r];
-          if (a.kZ) a.kZ[n * 256 + col] = z[rf][nf][r];
-        }
-      }
-    }
-  __syncthreads();
-  if (tid < MB) {
-    const int m = tid;
-    const int64_t n = tile0 + m;
-    if (n < N) {
-      const float mx = fmaxf(fmaxf(red[0][0][m], red[0][1][m]), fmaxf(red[0][2][m], red[0][3][m]));
-      const float tot = ((red[1][0][m] + red[1][1][m]) + red[1][2][m]) + red[1][3][m];
-      a.bits[a.w.n0 + n] = log2f(tot) - (zy[m] - mx) * TRACE_LOG2E;
-    }
-  }
-}
-
 // ------------------------------------------------------------- step means ----
 // step_ce[s] = (1/B) sum_b bits[b][s] in double, in a fixed order.
 __global__ __launch_bounds__(256) void k_step_ce(const float* __restrict__ bits, int32_t n_streams, int32_t n_steps,
@@ -561,15 +367,6 @@ constexpr int pick_ma(bool bf, int T, int D, int DH) {
   while (ma > 2 && attn_lds_bytes(bf, T, D, ma) > 160 * 1024) ma /= 2;
   return ma;
 }
-constexpr int ffn_lds_bytes(bool bf, int D, int mb, int fc) {
-  return mb * (D * (bf ? 2 : 4) + 16) + mb * (fc * (bf ? 2 : 4) + 16) + mb * 4 * 10;
-}
-constexpr int pick_mb(bool bf, int D) {
-  int mb = 64;
-  while (mb > 16 && ffn_lds_bytes(bf, D, mb, 256) > 160 * 1024) mb /= 2;
-  return mb;
-}
-
 template <bool BF, int T, int D, int DH>
 static void run_attn(const AttnArgs& a, hipStream_t s) {
   constexpr int MA = pick_ma(BF, T, D, DH);
@@ -577,14 +374,6 @@ static void run_attn(const AttnArgs& a, hipStream_t s) {
   const dim3 grid((unsigned)((a.w.N + MA - 1) / MA));
   hipLaunchKernelGGL((k_attn<BF, T, D, DH, MA>), grid, dim3(256), 0, s, a);
 }
-template <bool BF, int D>
-static void run_ffn(const FfnArgs& a, hipStream_t s) {
-  constexpr int MB = pick_mb(BF, D);
-  static_assert(ffn_lds_bytes(BF, D, MB, 256) <= 160 * 1024, "LDS");
-  const dim3 grid((unsigned)((a.w.N + MB - 1) / MB));
-  hipLaunchKernelGGL((k_ffn_head<BF, D, MB, 256>), grid, dim3(256), 0, s, a);
-}
-
 attn_fn find_attn(bool bf, int T, int D, int DH) {
 #define TRACE_ATTN(BF_, T_, D_, DH_) \
   if (bf == BF_ && T == T_ && D == D_ && DH == DH_) return &run_attn<BF_, T_, D_, DH_>;
@@ -598,11 +387,3 @@ attn_fn find_attn(bool bf, int T, int D, int DH) {
   return nullptr;
 }
 
-ffn_fn find_ffn(bool bf, int D) {
-#define TRACE_FFN(BF_, D_) \
-  if (bf == BF_ && D == D_) return &run_ffn<BF_, D_>;
-  TRACE_FFN(true, 64) TRACE_FFN(true, 128) TRACE_FFN(true, 256) TRACE_FFN(true, 512)
-  TRACE_FFN(false, 64) TRACE_FFN(false, 128) TRACE_FFN(false, 256) TRACE_FFN(false, 512)
-#undef TRACE_FFN
-  return nullptr;
-}

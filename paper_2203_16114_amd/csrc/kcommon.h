@@ -97,6 +97,34 @@ __device__ __forceinline__ float gelu_grad_f(float u) {
   return Phi + u * phi;
 }
 
+// GELU with erf by Abramowitz & Stegun, Handbook of Mathematical Functions,
+// 7.1.28: erf(x) = 1 - (1 + a1 x + ... + a6 x^6)^-16 for x >= 0, |error| <= 3e-7.
+// GELU(u) = u (1 + erf(u/sqrt2)) / 2 = (u + |u| - |u| / p(|u|/sqrt2)^16) / 2.
+// Absolute error <= 1.5e-7 |u|; used where the exact form is not required.
+__device__ __forceinline__ float gelu_as(float u) {
+  const float au = fabsf(u);
+  const float x = au * 0.70710678118654752f;
+  float p = fmaf(4.30638e-5f, x, 2.765672e-4f);
+  p = fmaf(p, x, 1.520143e-4f);
+  p = fmaf(p, x, 9.2705272e-3f);
+  p = fmaf(p, x, 4.22820123e-2f);
+  p = fmaf(p, x, 7.05230784e-2f);
+  p = fmaf(p, x, 1.0f);
+  p = p * p;
+  p = p * p;
+  p = p * p;
+  p = p * p;
+  const float r = __builtin_amdgcn_rcpf(p);
+  return 0.5f * fmaf(-au, r, u + au);
+}
+
+// two fp32 -> packed bf16 pair (round to nearest even, v_cvt_pk_bf16_f32)
+__device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
+  typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+  bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
 __device__ __forceinline__ float wave_sum16(float v) {  // over the 16 lanes sharing l/16
   v += __shfl_xor(v, 1, 64);
   v += __shfl_xor(v, 2, 64);
