@@ -1,0 +1,351 @@
+// Byte-grouping gather (Sec. 4.2) and the causal multi-head attention of the
+// last token (Eqs. 1-2) with its output projection and the first residual of
+// Eq. 4, fused: window bytes -> h0 = O.Wo + X_last.
+//
+// One workgroup of 8 waves per tile of MA windows.  Wave w owns RFW*16
+// consecutive token rows (whole windows).  Its tokens X, built from the
+// embedding table and the positional table, stay in registers for the whole
+// kernel as MFMA B-operand fragments (8 consecutive features per lane).
+// Every product is formed transposed (weights as the A operand), so a lane's
+// four results are four consecutive features of one token:
+//   q^T   = Wq^T . X_last^T                 (waves split the features)   -> LDS
+//   per head h:  K_h^T = Wk_h^T . X^T, then V_h^T = Wv_h^T . X^T; the head's
+//                weight fragments are staged through LDS in double-buffered
+//                chunks shared by all 8 waves;
+//                score of row u = q . K_u / sqrt(dh): 4-lane-group reduction;
+//                softmax over the T rows of a window (lanes of one window);
+//                O_h = sum_u a_u V_u: reduction over the same lanes      -> LDS
+//   h0^T  = Wo^T . O^T + X_last (fp32)    (waves split the features)   -> HBM
+// Only the last query row is formed: the head reads the last token, and under
+// the causal mask that row attends to every key of the window.
+#include "kcommon.h"
+#include "kernels.h"
+#include "win.h"
+
+namespace {
+
+// Token fragment: features [d, d + EPF) of token t of a window whose bytes are
+// at wb: E[byte] + P[t] in fp32, rounded to the operand type.
+template <bool BF>
+__device__ __forceinline__ uint4 x_frag(const typename Mma<BF>::T* __restrict__ E,
+                                        const typename Mma<BF>::T* __restrict__ P, const uint8_t* wb, int t, int d,
+                                        int e, int g, int D) {
+  const int j = d / e, cc = d - j * e;
+  const int byte = wb[t * g + j];
+  if constexpr (BF) {
+    float ev[8], pv[8];
+    load8(E + byte * e + cc, ev);
+    load8(P + t * D + d, pv);
+    uint4 r;
+    r.x = pack_bf16x2(ev[0] + pv[0], ev[1] + pv[1]);
+    r.y = pack_bf16x2(ev[2] + pv[2], ev[3] + pv[3]);
+    r.z = pack_bf16x2(ev[4] + pv[4], ev[5] + pv[5]);
+    r.w = pack_bf16x2(ev[6] + pv[6], ev[7] + pv[7]);
+    return r;
+  } else {
+    const float4 ev = *reinterpret_cast<const float4*>(E + byte * e + cc);
+    const float4 pv = *reinterpret_cast<const float4*>(P + t * D + d);
+    return make_uint4(__float_as_uint(ev.x + pv.x), __float_as_uint(ev.y + pv.y), __float_as_uint(ev.z + pv.z),
+                      __float_as_uint(ev.w + pv.w));
+  }
+}
+
+__device__ __forceinline__ void put4o(uint16_t* p, const f32x4& v) {
+  *reinterpret_cast<uint2*>(p) = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
+}
+__device__ __forceinline__ void put4o(float* p, const f32x4& v) {
+  *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+}
+__device__ __forceinline__ f32x4 rounded4(const f32x4& v, bool bf) {
+  if (!bf) return v;
+  return f32x4{round_bf(v[0]), round_bf(v[1]), round_bf(v[2]), round_bf(v[3])};
+}
+
+template <bool BF, int T, int D, int DH>
+struct AttnShape {
+  typedef typename Mma<BF>::T OT;
+  static constexpr int NW = 8;
+  static constexpr int KSTEPS = D / Mma<BF>::KS;
+  static constexpr int NFH = DH / 16;
+  static constexpr int KSC = (KSTEPS * NFH <= 16) ? KSTEPS : 16 / NFH;  // k-steps per staged chunk
+  static constexpr int CHUNK = KSC * NFH * 64;                            // uint4 per chunk
+  static constexpr int XLSTR = D * (int)sizeof(OT) + 16;
+  static constexpr int lds(int rfw) {
+    return 2 * CHUNK * 16 + (NW * rfw * 16 / T) * (D * 4 + XLSTR + 64);
+  }
+  // row fragments per wave: the largest of 4, 2, 1 whose register-held tokens,
+  // accumulators and fragments stay within the register budget of two waves per
+  // SIMD and whose tile fits the LDS
+  static constexpr int vgprs(int rfw) { return rfw * KSTEPS * 4 + rfw * NFH * 4 + NFH * 4 + 8; }
+  static constexpr bool fits(int rfw) { return vgprs(rfw) <= 184 && lds(rfw) <= 160 * 1024; }
+  static constexpr int RFW = (KSTEPS <= 8 && fits(4)) ? 4 : (fits(2) ? 2 : 1);
+  static constexpr int RW = RFW * 16;
+  static constexpr int MA = NW * RW / T;
+  static constexpr int LDS = lds(RFW);
+};
+
+}  // namespace
+
+template <bool BF, int T, int D, int DH, bool KEEP>
+__global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
+  typedef Mma<BF> M;
+  typedef typename M::T OT;
+  typedef AttnShape<BF, T, D, DH> S;
+  constexpr int H = D / DH;
+  constexpr int NW = S::NW, KSTEPS = S::KSTEPS, NFH = S::NFH, KSC = S::KSC, CPP = KSTEPS / KSC, CHUNK = S::CHUNK;
+  constexpr int RFW = S::RFW, RW = S::RW, MA = S::MA, XLSTR = S::XLSTR;
+  constexpr int NQF = D / 16, QFW = (NQF + NW - 1) / NW, NMF = (MA + 15) / 16;
+  constexpr int NB = D / 16;
+  static_assert(KSTEPS % KSC == 0 && (T == 4 || T == 8) && MA % 16 == 0, "shape");
+  __shared__ uint4 Wst[2][CHUNK];
+  __shared__ __align__(16) float Qs[MA * D];
+  __shared__ __align__(16) unsigned char Xl[MA * XLSTR];  // X_last rows, then O rows
+  __shared__ uint8_t Wb[MA * 64];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lg = lane >> 4, lc = lane & 15;
+  const int64_t tile0 = (int64_t)blockIdx.x * MA;
+  const int64_t N = a.w.N;
+  const int W = T * a.g;
+  const OT* __restrict__ E = (const OT*)a.E;
+  const OT* __restrict__ P = (const OT*)a.P;
+
+  for (int i = tid; i < MA * W; i += 512) {
+    const int m = i / W, j = i - m * W;
+    const int64_t n = tile0 + m;
+    uint8_t v = 0;
+    if (n < N) {
+      v = a.w.streams[target_offset(a.w, n) - W + j];
+      if (KEEP) a.kwin[n * W + j] = v;
+    }
+    Wb[m * 64 + j] = v;
+  }
+  __syncthreads();
+
+  // this wave's tokens as B fragments; the last token of each window also to LDS
+  uint4 xb[RFW][KSTEPS];
+#pragma unroll
+  for (int rf = 0; rf < RFW; ++rf) {
+    const int row = wave * RW + rf * 16 + lc;
+    const int m = row / T, t = row - m * T;
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      const int d = ks * M::KS + lg * M::EPF;
+      xb[rf][ks] = x_frag<BF>(E, P, Wb + m * 64, t, d, a.e, a.g, D);
+      if (t == T - 1) *(uint4*)(Xl + m * XLSTR + ks * 64 + lg * 16) = xb[rf][ks];
+    }
+  }
+  __syncthreads();
+
+  // q^T = Wq^T . X_last^T ; lane holds q[m = nf*16 + lc][c = qf*16 + 4*lg + r]
+#pragma unroll
+  for (int qi = 0; qi < QFW; ++qi) {
+    const int qf = wave * QFW + qi;
+    if (qf < NQF) {
+      f32x4 acc[NMF];
+#pragma unroll
+      for (int nf = 0; nf < NMF; ++nf) acc[nf] = f32x4{0.f, 0.f, 0.f, 0.f};
+      uint4 wq[2];
+      wq[0] = a.Wq[qf * 64 + lane];
+#pragma unroll
+      for (int ks = 0; ks < KSTEPS; ++ks) {
+        if (ks + 1 < KSTEPS) wq[(ks + 1) & 1] = a.Wq[((ks + 1) * NB + qf) * 64 + lane];
+#pragma unroll
+        for (int nf = 0; nf < NMF; ++nf) {
+          const uint4 bx = *(const uint4*)(Xl + (nf * 16 + lc) * XLSTR + ks * 64 + lg * 16);
+          M::run(acc[nf], wq[ks & 1], bx);
+        }
+      }
+#pragma unroll
+      for (int nf = 0; nf < NMF; ++nf) {
+        const int m = nf * 16 + lc;
+        const int c = qf * 16 + 4 * lg;
+        *reinterpret_cast<float4*>(Qs + m * D + c) = make_float4(acc[nf][0], acc[nf][1], acc[nf][2], acc[nf][3]);
+        if (KEEP && tile0 + m < N)
+          *reinterpret_cast<float4*>(a.kq + (tile0 + m) * D + c) =
+              make_float4(acc[nf][0], acc[nf][1], acc[nf][2], acc[nf][3]);
+      }
+    }
+  }
+
+  // staged weight chunks: chunk c = ((h * 2 + pass) * CPP + ck); element i of a
+  // chunk is fragment (k-step ck*KSC + i/(NFH*64), feature frag h*NFH + (i/64)%NFH)
+  auto chunk_src = [&](int c, int i) -> const uint4* {
+    const int ck = c % CPP, pass = (c / CPP) & 1, h = c / (2 * CPP);
+    const int kk = i / (NFH * 64), f = (i / 64) % NFH, ln = i & 63;
+    const uint4* Wp = pass ? a.Wv : a.Wk;
+    return Wp + ((ck * KSC + kk) * NB + h * NFH + f) * 64 + ln;
+  };
+  constexpr int PT = (CHUNK + 511) / 512;
+  constexpr int NCH = H * 2 * CPP;
+  uint4 pre[PT];
+#pragma unroll
+  for (int p = 0; p < PT; ++p) {
+    const int i = tid + p * 512;
+    if (i < CHUNK) Wst[0][i] = *chunk_src(0, i);
+  }
+  __syncthreads();  // chunk 0 staged; Qs complete; X_last rows no longer needed
+
+  const float scale = a.scale;
+  float prob[RFW];
+  for (int h = 0; h < H; ++h) {
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+      f32x4 acc[RFW][NFH];
+#pragma unroll
+      for (int rf = 0; rf < RFW; ++rf)
+#pragma unroll
+        for (int f = 0; f < NFH; ++f) acc[rf][f] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ck = 0; ck < CPP; ++ck) {
+        const int c = (h * 2 + pass) * CPP + ck;
+        if (c + 1 < NCH) {
+#pragma unroll
+          for (int p = 0; p < PT; ++p) {
+            const int i = tid + p * 512;
+            if (i < CHUNK) pre[p] = *chunk_src(c + 1, i);
+          }
+        }
+        const uint4* buf = Wst[c & 1];
+#pragma unroll
+        for (int kk = 0; kk < KSC; ++kk) {
+          uint4 af[NFH];
+#pragma unroll
+          for (int f = 0; f < NFH; ++f) af[f] = buf[(kk * NFH + f) * 64 + lane];
+#pragma unroll
+          for (int rf = 0; rf < RFW; ++rf)
+#pragma unroll
+            for (int f = 0; f < NFH; ++f) M::run(acc[rf][f], af[f], xb[rf][ck * KSC + kk]);
+        }
+        if (c + 1 < NCH) {
+#pragma unroll
+          for (int p = 0; p < PT; ++p) {
+            const int i = tid + p * 512;
+            if (i < CHUNK) Wst[(c + 1) & 1][i] = pre[p];
+          }
+        }
+        __syncthreads();
+      }
+      // lane holds K_h or V_h [row = wave*RW + rf*16 + lc][c = f*16 + 4*lg + r]
+#pragma unroll
+      for (int rf = 0; rf < RFW; ++rf) {
+        const int row = wave * RW + rf * 16 + lc;
+        const int m = row / T, t = row - m * T;
+        const int64_t n = tile0 + m;
+        const bool live = n < N;
+        if (pass == 0) {
+          float s = 0.f;
+#pragma unroll
+          for (int f = 0; f < NFH; ++f) {
+            const float4 q4 = *reinterpret_cast<const float4*>(Qs + m * D + h * DH + f * 16 + 4 * lg);
+            s += q4.x * acc[rf][f][0] + q4.y * acc[rf][f][1] + q4.z * acc[rf][f][2] + q4.w * acc[rf][f][3];
+          }
+          s += __shfl_xor(s, 16, 64);
+          s += __shfl_xor(s, 32, 64);
+          s *= scale;
+          float mx = s;
+#pragma unroll
+          for (int o = 1; o < T; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+          const float p = expf(s - mx);
+          float sm = p;
+#pragma unroll
+          for (int o = 1; o < T; o <<= 1) sm += __shfl_xor(sm, o, 64);
+          prob[rf] = p / sm;
+          if (KEEP && live) {
+            if (lg == 0) a.kA[(n * H + h) * T + t] = prob[rf];
+#pragma unroll
+            for (int f = 0; f < NFH; ++f)
+              *reinterpret_cast<float4*>(a.kK + (n * T + t) * D + h * DH + f * 16 + 4 * lg) =
+                  make_float4(acc[rf][f][0], acc[rf][f][1], acc[rf][f][2], acc[rf][f][3]);
+          }
+        } else {
+#pragma unroll
+          for (int f = 0; f < NFH; ++f) {
+            if (KEEP && live)
+              *reinterpret_cast<float4*>(a.kV + (n * T + t) * D + h * DH + f * 16 + 4 * lg) =
+                  make_float4(acc[rf][f][0], acc[rf][f][1], acc[rf][f][2], acc[rf][f][3]);
+            f32x4 ov;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+              float o = prob[rf] * acc[rf][f][r];
+#pragma unroll
+              for (int sh = 1; sh < T; sh <<= 1) o += __shfl_xor(o, sh, 64);
+              ov[r] = o;
+            }
+            if (t == 0) {
+              const int cc = h * DH + f * 16 + 4 * lg;
+              put4o((OT*)(Xl + m * XLSTR) + cc, ov);
+              if (KEEP && live) {
+                const f32x4 rv = rounded4(ov, BF);
+                *reinterpret_cast<float4*>(a.kO + n * D + cc) = make_float4(rv[0], rv[1], rv[2], rv[3]);
+              }
+            }
+          }
+        }
+      }
+    }
+  }
+  __syncthreads();  // O complete
+
+  // h0^T = Wo^T . O^T + X_last
+#pragma unroll
+  for (int qi = 0; qi < QFW; ++qi) {
+    const int qf = wave * QFW + qi;
+    if (qf < NQF) {
+      f32x4 acc[NMF];
+#pragma unroll
+      for (int nf = 0; nf < NMF; ++nf) acc[nf] = f32x4{0.f, 0.f, 0.f, 0.f};
+      uint4 wo[2];
+      wo[0] = a.Wo[qf * 64 + lane];
+#pragma unroll
+      for (int ks = 0; ks < KSTEPS; ++ks) {
+        if (ks + 1 < KSTEPS) wo[(ks + 1) & 1] = a.Wo[((ks + 1) * NB + qf) * 64 + lane];
+#pragma unroll
+        for (int nf = 0; nf < NMF; ++nf) {
+          const uint4 bo = *(const uint4*)(Xl + (nf * 16 + lc) * XLSTR + ks * 64 + lg * 16);
+          M::run(acc[nf], wo[ks & 1], bo);
+        }
+      }
+#pragma unroll
+      for (int nf = 0; nf < NMF; ++nf) {
+        const int m = nf * 16 + lc;
+        const int64_t n = tile0 + m;
+        if (n < N) {
+          const int d = qf * 16 + 4 * lg;
+          const int j = d / a.e, cc = d - j * a.e;
+          const int byte = Wb[m * 64 + (T - 1) * a.g + j];
+          float4 r;
+          r.x = acc[nf][0] + (M::val(E[byte * a.e + cc]) + M::val(P[(T - 1) * D + d]));
+          r.y = acc[nf][1] + (M::val(E[byte * a.e + cc + 1]) + M::val(P[(T - 1) * D + d + 1]));
+          r.z = acc[nf][2] + (M::val(E[byte * a.e + cc + 2]) + M::val(P[(T - 1) * D + d + 2]));
+          r.w = acc[nf][3] + (M::val(E[byte * a.e + cc + 3]) + M::val(P[(T - 1) * D + d + 3]));
+          *reinterpret_cast<float4*>(a.h0 + n * D + d) = r;
+        }
+      }
+    }
+  }
+}
+
+// ------------------------------------------------------------ dispatch ----
+template <bool BF, int T, int D, int DH>
+static void run_attn(const AttnArgs& a, hipStream_t s) {
+  typedef AttnShape<BF, T, D, DH> S;
+  static_assert(S::LDS <= 160 * 1024, "LDS");
+  const dim3 grid((unsigned)((a.w.N + S::MA - 1) / S::MA));
+  if (a.kK)
+    hipLaunchKernelGGL((k_attn<BF, T, D, DH, true>), grid, dim3(512), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_attn<BF, T, D, DH, false>), grid, dim3(512), 0, s, a);
+}
+
+attn_fn find_attn(bool bf, int T, int D, int DH) {
+#define TRACE_ATTN(BF_, T_, D_, DH_) \
+  if (bf == BF_ && T == T_ && D == D_ && DH == DH_) return &run_attn<BF_, T_, D_, DH_>;
+#define TRACE_ATTN_T(BF_, D_, DH_) TRACE_ATTN(BF_, 4, D_, DH_) TRACE_ATTN(BF_, 8, D_, DH_)
+  TRACE_ATTN_T(true, 64, 32) TRACE_ATTN_T(true, 64, 64) TRACE_ATTN_T(true, 128, 32) TRACE_ATTN_T(true, 128, 64)
+  TRACE_ATTN_T(true, 256, 32) TRACE_ATTN_T(true, 256, 64) TRACE_ATTN_T(true, 512, 64)
+  TRACE_ATTN_T(false, 64, 32) TRACE_ATTN_T(false, 64, 64) TRACE_ATTN_T(false, 128, 32) TRACE_ATTN_T(false, 128, 64)
+  TRACE_ATTN_T(false, 256, 32) TRACE_ATTN_T(false, 256, 64)
+#undef TRACE_ATTN_T
+#undef TRACE_ATTN
+  return nullptr;
+}
