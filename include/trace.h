@@ -64,7 +64,7 @@ enum { TRACE_KEEP_ACTS = 1u };
  *            (0: the model cannot adapt)
  *   lr, beta1, beta2, eps  Adam (Sec. 6 uses lr 0.001)
  * Supported shapes: W % g == 0, d % H == 0, T in {4, 8}, d/H in {32, 64},
- * d in {64, 128, 256, 512} (a multiple of 64), e % 8 == 0, F % 256 == 0,
+ * d in {64, 128, 256, 512} (a multiple of 64), e % 8 == 0, e <= 128, F % 256 == 0,
  * 1 <= k <= 8.  Others return TRACE_EINVAL or TRACE_EUNSUPPORTED. */
 typedef struct {
   int32_t W, e, g, H, F, k;

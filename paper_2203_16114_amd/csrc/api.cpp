@@ -35,7 +35,7 @@ struct trace_model {
   int32_t* ktgt;
   float *kq, *kK, *kV, *kA, *kO, *kY, *kU, *kZ;
   // backward scratch
-  float *dz, *dY, *dG, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *gws, *cws;
+  float *dz, *dY, *dG, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *gws, *cws, *ews;
   int64_t gws_cap;
   std::vector<void*> allocs;
   // event timing (trace_set_timing)
@@ -166,7 +166,7 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
   int rc = trace_check_config(cfg, &L);
   if (rc) return rc;
   const bool bf = cfg->dtype == TRACE_BF16;
-  if (cfg->e % 8 != 0 || cfg->e > 256) return fail(TRACE_EUNSUPPORTED, "e must be a multiple of 8, at most 256");
+  if (cfg->e % 8 != 0 || cfg->e > 128) return fail(TRACE_EUNSUPPORTED, "e must be a multiple of 8, at most 128");
   if (cfg->F % 256 != 0) return fail(TRACE_EUNSUPPORTED, "F must be a multiple of 256");
   if (cfg->g > 64 || cfg->W > 64) return fail(TRACE_EUNSUPPORTED, "W must be at most 64 bytes");
   attn_fn af = find_attn(bf, L.T, L.D, L.DH);
@@ -202,7 +202,8 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
          dalloc(m, &m->dO, K * D * 4) && dalloc(m, &m->dQ, K * D * 4) && dalloc(m, &m->dK, K * T * D * 4) &&
          dalloc(m, &m->dV, K * T * D * 4) && dalloc(m, &m->dX, K * T * D * 4) && dalloc(m, &m->Xk, K * T * D * 4) &&
          dalloc(m, &m->gws, (m->gws_cap = adapt_gemm_ws(m, K)) * 4) &&
-         dalloc(m, &m->cws, colsum_ws_floats(std::max<int64_t>(T * D, 256)) * 4);
+         dalloc(m, &m->ews, embed_bwd_ws_floats(K * W, cfg->e) * 4) &&
+         dalloc(m, &m->cws, colsum_ws_floats(std::max<int64_t>(std::max<int64_t>(T * D, 256), 256 * cfg->e)) * 4);
   }
   if (!ok) {
     free_all(m);
@@ -403,7 +404,7 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
     launch_colsum(m->dX, N, (int64_t)T * D, (int64_t)T * D, gr + L.off[P_P], 0.f, m->cws, s);
   else
     launch_zero(gr + L.off[P_P], L.size[P_P], s);
-  launch_embed_bwd(m->kwin, m->dX, N, m->cfg.W, m->cfg.g, m->cfg.e, D, gr + L.off[P_E], s);
+  launch_embed_bwd(m->kwin, m->dX, N, m->cfg.W, m->cfg.g, m->cfg.e, D, gr + L.off[P_E], m->ews, m->cws, s);
   tend(m, tk, TRACE_KIND_BACKWARD, s);
   // Adam on the flat master, then new operand copies
   m->step += 1;

@@ -2,8 +2,8 @@
 // through the forward of fwd.hip (Model.backward of Alg. 1, line 10), and the
 // Adam update (Sec. 6: Adam, lr 0.001).  Every reduction runs in a fixed order,
 // so two runs on the same inputs give bitwise-identical gradients: split-K
-// partial products and column sums are combined by a second pass that adds
-// them in index order, and the embedding scatter is a per-byte-value gather.
+// partial products, column sums and embedding-gradient partial tables are
+// combined by a second pass that adds them in index order.
 #include "kcommon.h"
 #include "kernels.h"
 
@@ -112,10 +112,193 @@ __global__ void k_splitk_reduce(const float* __restrict__ part, int splits, int 
   *c = (beta != 0.f) ? (*c + s) : s;
 }
 
+// 128x128-tile GEMM for the two operand layouts of the update: operands whose
+// contiguous dimension is k (activation gradients, dY . W^T) and operands
+// whose contiguous dimension is m or n (weight gradients, act^T . dY).  Global
+// reads are float4 along the contiguous dimension; the next k-tile is held in
+// registers while the current one is multiplied from LDS (two LDS buffers,
+// one barrier per k-tile).  Modes:
+//   GM_F32      both operands fp32 (fp32 models): 16x16x4 fp32 MFMA;
+//   GM_BF16     both operands at a bf16 storage point: 16x16x32 bf16 MFMA;
+//   GM_SPLIT_A  A is an fp32 value, B a bf16 storage point: A = hi + lo with
+//   GM_SPLIT_B  hi = bf16(A), lo = bf16(A - hi), two bf16 MFMAs per product
+//               (the fp32 operand keeps ~16 significant bits; 2^-17 relative).
+enum { GM_F32 = 0, GM_BF16 = 1, GM_SPLIT_A = 2, GM_SPLIT_B = 3 };
+
+template <int MODE>
+__device__ __forceinline__ void st_lds(unsigned char* row_hi, unsigned char* row_lo, int k, float v, bool split,
+                                       bool rnd) {
+  if constexpr (MODE == GM_F32) {
+    ((float*)row_hi)[k] = v;
+  } else {
+    const uint16_t h = f2bf(v);
+    ((uint16_t*)row_hi)[k] = h;
+    if (split) ((uint16_t*)row_lo)[k] = f2bf(v - bf2f(h));
+    (void)rnd;
+  }
+}
+
+template <int MODE, bool AK, bool BKF>
+__global__ __launch_bounds__(256) void k_gemm128(GemmArgs g, float* __restrict__ part, int kchunk) {
+  constexpr bool BFOP = MODE != GM_F32;
+  typedef Mma<BFOP> M;
+  typedef typename M::T OT;
+  constexpr int BM = 128, BN = 128, BK = 32;
+  constexpr int STR = BK * (int)sizeof(OT) + 16;
+  constexpr bool SPA = MODE == GM_SPLIT_A, SPB = MODE == GM_SPLIT_B;
+  constexpr int AT = BM * STR, BT = BN * STR;
+  __shared__ __align__(16) unsigned char As[2][(SPA ? 2 : 1) * AT];
+  __shared__ __align__(16) unsigned char Bs[2][(SPB ? 2 : 1) * BT];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lg = lane >> 4, lc = lane & 15;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
+  const int kbeg = blockIdx.z * kchunk;
+  const int kend = min(g.K, kbeg + kchunk);
+  f32x4 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float4 ra[4], rb[4];
+  // element (row, k) of the tile loaded by float4 q: see the index maps below
+  auto load = [&](int k0) {
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int q = tid + it * 256;
+      if (AK) {
+        const int mm = q >> 3, kk = (q & 7) * 4;
+        const int m = m0 + mm, k = k0 + kk;
+        if (m < g.M && k + 3 < kend) {
+          ra[it] = *reinterpret_cast<const float4*>(g.A + (int64_t)m * g.sam + k);
+        } else {
+          float t[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) t[u] = (m < g.M && k + u < kend) ? g.A[(int64_t)m * g.sam + k + u] : 0.f;
+          ra[it] = make_float4(t[0], t[1], t[2], t[3]);
+        }
+      } else {
+        const int kk = q >> 5, mm = (q & 31) * 4;
+        const int m = m0 + mm, k = k0 + kk;
+        ra[it] = (k < kend && m < g.M) ? *reinterpret_cast<const float4*>(g.A + m + (int64_t)k * g.sak)
+                                       : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      if (BKF) {
+        const int nn = q >> 3, kk = (q & 7) * 4;
+        const int n = n0 + nn, k = k0 + kk;
+        if (n < g.N && k + 3 < kend) {
+          rb[it] = *reinterpret_cast<const float4*>(g.B + k + (int64_t)n * g.sbn);
+        } else {
+          float t[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) t[u] = (n < g.N && k + u < kend) ? g.B[k + u + (int64_t)n * g.sbn] : 0.f;
+          rb[it] = make_float4(t[0], t[1], t[2], t[3]);
+        }
+      } else {
+        const int kk = q >> 5, nn = (q & 31) * 4;
+        const int n = n0 + nn, k = k0 + kk;
+        rb[it] = (k < kend && n < g.N) ? *reinterpret_cast<const float4*>(g.B + (int64_t)k * g.sbk + n)
+                                       : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+    }
+  };
+  auto store = [&](int buf) {
+    unsigned char* Ah = As[buf];
+    unsigned char* Al = As[buf] + (SPA ? AT : 0);
+    unsigned char* Bh = Bs[buf];
+    unsigned char* Bl = Bs[buf] + (SPB ? BT : 0);
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int q = tid + it * 256;
+      const float va[4] = {ra[it].x, ra[it].y, ra[it].z, ra[it].w};
+      const float vb[4] = {rb[it].x, rb[it].y, rb[it].z, rb[it].w};
+      if (AK) {
+        const int mm = q >> 3, kk = (q & 7) * 4;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) st_lds<MODE>(Ah + mm * STR, Al + mm * STR, kk + u, va[u], SPA, true);
+      } else {
+        const int kk = q >> 5, mm = (q & 31) * 4;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) st_lds<MODE>(Ah + (mm + u) * STR, Al + (mm + u) * STR, kk, va[u], SPA, true);
+      }
+      if (BKF) {
+        const int nn = q >> 3, kk = (q & 7) * 4;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) st_lds<MODE>(Bh + nn * STR, Bl + nn * STR, kk + u, vb[u], SPB, true);
+      } else {
+        const int kk = q >> 5, nn = (q & 31) * 4;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) st_lds<MODE>(Bh + (nn + u) * STR, Bl + (nn + u) * STR, kk, vb[u], SPB, true);
+      }
+    }
+  };
+  if (kbeg < kend) {
+    load(kbeg);
+    store(0);
+  }
+  __syncthreads();
+  int it = 0;
+  for (int k0 = kbeg; k0 < kend; k0 += BK, ++it) {
+    const int cur = it & 1;
+    const bool more = k0 + BK < kend;
+    if (more) load(k0 + BK);
+    const unsigned char* Ah = As[cur];
+    const unsigned char* Bh = Bs[cur];
+#pragma unroll
+    for (int ks = 0; ks < BK / M::KS; ++ks) {
+      uint4 af[4], bfr[4];
+#pragma unroll
+      for (int rf = 0; rf < 4; ++rf) af[rf] = *(const uint4*)(Ah + (wm * 64 + rf * 16 + lc) * STR + ks * 64 + lg * 16);
+#pragma unroll
+      for (int nf = 0; nf < 4; ++nf) bfr[nf] = *(const uint4*)(Bh + (wn * 64 + nf * 16 + lc) * STR + ks * 64 + lg * 16);
+#pragma unroll
+      for (int rf = 0; rf < 4; ++rf)
+#pragma unroll
+        for (int nf = 0; nf < 4; ++nf) M::run(acc[rf][nf], af[rf], bfr[nf]);
+      if constexpr (SPA) {
+#pragma unroll
+        for (int rf = 0; rf < 4; ++rf)
+          af[rf] = *(const uint4*)(Ah + AT + (wm * 64 + rf * 16 + lc) * STR + ks * 64 + lg * 16);
+#pragma unroll
+        for (int rf = 0; rf < 4; ++rf)
+#pragma unroll
+          for (int nf = 0; nf < 4; ++nf) M::run(acc[rf][nf], af[rf], bfr[nf]);
+      }
+      if constexpr (SPB) {
+#pragma unroll
+        for (int nf = 0; nf < 4; ++nf)
+          bfr[nf] = *(const uint4*)(Bh + BT + (wn * 64 + nf * 16 + lc) * STR + ks * 64 + lg * 16);
+#pragma unroll
+        for (int rf = 0; rf < 4; ++rf)
+#pragma unroll
+          for (int nf = 0; nf < 4; ++nf) M::run(acc[rf][nf], af[rf], bfr[nf]);
+      }
+    }
+    if (more) store(cur ^ 1);
+    __syncthreads();
+  }
+#pragma unroll
+  for (int rf = 0; rf < 4; ++rf)
+#pragma unroll
+    for (int nf = 0; nf < 4; ++nf)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = m0 + wm * 64 + rf * 16 + 4 * lg + r;
+        const int n = n0 + wn * 64 + nf * 16 + lc;
+        if (m < g.M && n < g.N) {
+          if (part) {
+            part[((int64_t)blockIdx.z * g.M + m) * g.N + n] = acc[rf][nf][r];
+          } else {
+            float* c = g.C + (int64_t)m * g.ldc + n;
+            *c = (g.beta != 0.f) ? (*c + acc[rf][nf][r]) : acc[rf][nf][r];
+          }
+        }
+      }
+}
+
 static int gemm_splits(int M, int N, int K) {
-  const int tiles = ((M + 63) / 64) * ((N + 63) / 64);
+  const int tiles = ((M + 127) / 128) * ((N + 127) / 128);
   int splits = 1;
-  // enough workgroups to fill 256 CUs, each split still covering >= 256 k values
+  // enough workgroups to fill 256 CUs twice, each split still covering >= 256 k values
   while (tiles * splits < 512 && (K + splits * 2 - 1) / (splits * 2) >= 256) splits *= 2;
   return splits;
 }
@@ -123,19 +306,48 @@ int64_t gemm_ws_floats(int M, int N, int K) {
   const int s = gemm_splits(M, N, K);
   return s > 1 ? (int64_t)s * M * N : 0;
 }
+static bool aligned16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+template <int MODE>
+static void launch128(const GemmArgs& g, float* part, int kchunk, dim3 grid, hipStream_t s) {
+  const bool ak = g.sak == 1, bk = g.sbk == 1;
+  if (ak && bk)
+    hipLaunchKernelGGL((k_gemm128<MODE, true, true>), grid, dim3(256), 0, s, g, part, kchunk);
+  else if (ak)
+    hipLaunchKernelGGL((k_gemm128<MODE, true, false>), grid, dim3(256), 0, s, g, part, kchunk);
+  else if (bk)
+    hipLaunchKernelGGL((k_gemm128<MODE, false, true>), grid, dim3(256), 0, s, g, part, kchunk);
+  else
+    hipLaunchKernelGGL((k_gemm128<MODE, false, false>), grid, dim3(256), 0, s, g, part, kchunk);
+}
+
 void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return;
-  const bool bf = g.roundA && g.roundB;
   int splits = gemm_splits(g.M, g.N, g.K);
   while (splits > 1 && (int64_t)splits * g.M * g.N > ws_cap) splits /= 2;
   int kchunk = (g.K + splits - 1) / splits;
   kchunk = (kchunk + 31) / 32 * 32;
-  const dim3 grid((g.N + 63) / 64, (g.M + 63) / 64, splits);
   float* part = splits > 1 ? ws : nullptr;
-  if (bf)
-    hipLaunchKernelGGL(k_gemm<true>, grid, dim3(256), 0, s, g, part, kchunk);
-  else
-    hipLaunchKernelGGL(k_gemm<false>, grid, dim3(256), 0, s, g, part, kchunk);
+  // the 128-tile kernel needs float4 access along each operand's contiguous dimension
+  const bool a_ok = aligned16(g.A) && ((g.sak == 1 && g.sam % 4 == 0) || (g.sam == 1 && g.sak % 4 == 0 && g.M % 4 == 0));
+  const bool b_ok = aligned16(g.B) && ((g.sbk == 1 && g.sbn % 4 == 0) || (g.sbn == 1 && g.sbk % 4 == 0 && g.N % 4 == 0));
+  if (a_ok && b_ok) {
+    const dim3 grid((g.N + 127) / 128, (g.M + 127) / 128, splits);
+    if (g.roundA && g.roundB)
+      launch128<GM_BF16>(g, part, kchunk, grid, s);
+    else if (!g.roundA && !g.roundB)
+      launch128<GM_F32>(g, part, kchunk, grid, s);
+    else if (g.roundB)
+      launch128<GM_SPLIT_A>(g, part, kchunk, grid, s);
+    else
+      launch128<GM_SPLIT_B>(g, part, kchunk, grid, s);
+  } else {
+    const dim3 grid((g.N + 63) / 64, (g.M + 63) / 64, splits);
+    if (g.roundA && g.roundB)
+      hipLaunchKernelGGL(k_gemm<true>, grid, dim3(256), 0, s, g, part, kchunk);
+    else
+      hipLaunchKernelGGL(k_gemm<false>, grid, dim3(256), 0, s, g, part, kchunk);
+  }
   if (splits > 1) {
     const int64_t tot = (int64_t)g.M * g.N;
     hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, ws, splits, g.M, g.N,
@@ -300,38 +512,71 @@ void launch_attn_bwd(const float* dO, const float* q, const float* K, const floa
 }
 
 // ------------------------------------------------------ embedding backward ----
-// dE[v][c] = sum over (n, p) with win[n][p] == v of dX[n][p/g][(p%g)*e + c].
-// One block per byte value v: thread (r, c) walks the positions r, r+R, ... in
-// order, and the R partial sums are combined in a fixed order.
-__global__ __launch_bounds__(256) void k_embed_bwd(const uint8_t* __restrict__ win, const float* __restrict__ dX,
-                                                   int64_t N, int W, int g, int e, int D, float* __restrict__ dE) {
-  __shared__ float red[256];
-  const int v = blockIdx.x;
-  const int R = 256 / e;
-  const int r = threadIdx.x / e, c = threadIdx.x % e;
-  float acc = 0.f;
-  if (r < R) {
-    const int64_t total = N * W;
-    for (int64_t i = r; i < total; i += R) {
-      if (win[i] == v) {
-        const int64_t n = i / W;
-        const int p = (int)(i - n * W);
-        const int t = p / g, j = p - t * g;
-        acc += dX[(n * (W / g) + t) * D + j * e + c];
+// dE[v][c] = sum over positions (n, p) with win[n][p] == v of
+// dX[n][p/g][(p%g)*e + c], in two deterministic passes.
+// Pass 1: block b takes a contiguous range of positions; its NG groups of e
+// threads take every NG-th position of the range in increasing order and add
+// the position's e-vector into the group's own LDS table [256][e]; the group
+// tables are then added in group order into part[b][256][e].
+// Pass 2: dE = sum over b of part[b], in block order (column sums).
+constexpr int EMB_LDS_FLOATS = 32768;  // 128 KiB of group tables
+__global__ __launch_bounds__(256) void k_embed_bwd_part(const uint8_t* __restrict__ win, const float* __restrict__ dX,
+                                                        int64_t total, int64_t chunk, int W, int g, int e, int D,
+                                                        float* __restrict__ part) {
+  __shared__ float tab[EMB_LDS_FLOATS];
+  const int NG = min(256 / e, EMB_LDS_FLOATS / (256 * e));
+  const int tid = threadIdx.x;
+  const int grp = tid / e, c = tid - grp * e;
+  for (int i = tid; i < NG * 256 * e; i += 256) tab[i] = 0.f;
+  __syncthreads();
+  const int64_t p0 = (int64_t)blockIdx.x * chunk;
+  const int64_t p1 = min(total, p0 + chunk);
+  const int T = W / g;
+  if (grp < NG) {
+    float* my = tab + grp * 256 * e;
+    int64_t i = p0 + grp;
+    // eight positions at a time: loads first, then the table updates in order
+    for (; i + 7 * NG < p1; i += 8 * NG) {
+      int v[8];
+      float x[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int64_t q = i + u * NG;
+        const int64_t n = q / W;
+        const int pp = (int)(q - n * W);
+        const int t = pp / g, j = pp - t * g;
+        v[u] = win[q];
+        x[u] = dX[(n * T + t) * D + j * e + c];
       }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) my[v[u] * e + c] += x[u];
+    }
+    for (; i < p1; i += NG) {
+      const int64_t n = i / W;
+      const int pp = (int)(i - n * W);
+      const int t = pp / g, j = pp - t * g;
+      my[win[i] * e + c] += dX[(n * T + t) * D + j * e + c];
     }
   }
-  red[threadIdx.x] = acc;
   __syncthreads();
-  if (threadIdx.x < e) {
+  for (int k = tid; k < 256 * e; k += 256) {
     float s = 0.f;
-    for (int i = 0; i < R; ++i) s += red[i * e + threadIdx.x];
-    dE[v * e + threadIdx.x] = s;
+    for (int q = 0; q < NG; ++q) s += tab[q * 256 * e + k];
+    part[(int64_t)blockIdx.x * 256 * e + k] = s;
   }
 }
+int embed_bwd_blocks(int64_t total) {
+  int64_t b = total / 512;
+  return (int)(b < 64 ? 64 : (b > 1024 ? 1024 : b));
+}
+int64_t embed_bwd_ws_floats(int64_t total, int e) { return (int64_t)embed_bwd_blocks(total) * 256 * e; }
 void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int g, int e, int D, float* dE,
-                      hipStream_t s) {
-  hipLaunchKernelGGL(k_embed_bwd, dim3(256), dim3(256), 0, s, win, dX, N, W, g, e, D, dE);
+                      float* ws, float* cws, hipStream_t s) {
+  const int64_t total = N * W;
+  const int G = embed_bwd_blocks(total);
+  const int64_t chunk = (total + G - 1) / G;
+  hipLaunchKernelGGL(k_embed_bwd_part, dim3(G), dim3(256), 0, s, win, dX, total, chunk, W, g, e, D, ws);
+  launch_colsum(ws, G, 256 * e, 256 * e, dE, 0.f, cws, s);
 }
 
 // token operand values of the kept windows: X[n][t][c] (fp32 value of the operand)

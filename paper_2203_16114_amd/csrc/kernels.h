@@ -85,8 +85,9 @@ void launch_gelu_bwd(const float* dG, const float* U, float* dU, int64_t n, hipS
 void launch_attn_bwd(const float* dO, const float* q, const float* K, const float* V, const float* A, int64_t N, int T,
                      int D, int H, float scale, int round_dO, float* dQ, float* dK, float* dV, hipStream_t s);
 void launch_add(float* y, const float* x, int64_t rows, int64_t cols, int64_t ldy, int64_t ldx, hipStream_t s);
+int64_t embed_bwd_ws_floats(int64_t total, int e);  // total = N * W positions
 void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int g, int e, int D, float* dE,
-                      hipStream_t s);
+                      float* ws, float* cws, hipStream_t s);
 void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, const void* P, int T, int D, int e,
                         int g, float* X, hipStream_t s);
 void launch_adam(float* theta, const float* grad, float* m, float* v, int64_t n, float lr, float b1, float b2,
