@@ -163,6 +163,9 @@ def main():
     ap.add_argument("--full", action="store_true", help="generate the full 256 KiB streams")
     ap.add_argument("--gated-steps", type=int, default=256, help="steps of the gated-adaptation run (0: skip)")
     ap.add_argument("--cpu-windows", type=int, default=2048, help="oracle sample (0: skip)")
+    ap.add_argument("--copy-probe-mib", type=int, default=0,
+                    help="only run 5 device-to-device copies of this many MiB (calibrates the HBM "
+                         "byte counters FETCH_SIZE / WRITE_SIZE against a copy of known size)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU only: this build has no multi-GPU path "
@@ -173,6 +176,16 @@ def main():
     import torch
     import paper_2203_16114_amd as P
     import synth
+
+    if args.copy_probe_mib > 0:
+        n = args.copy_probe_mib << 20
+        src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_probe_bytes": n, "copies": 5}), flush=True)
+        return
 
     w = synth.WORKLOADS[3]
     B, S, K = w.B, args.steps_per_call, args.steps

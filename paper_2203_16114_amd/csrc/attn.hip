@@ -13,8 +13,8 @@
 //                weight fragments are staged through LDS in double-buffered
 //                chunks shared by all 8 waves;
 //                score of row u = q . K_u / sqrt(dh): 4-lane-group reduction;
-//                softmax over the T rows of a window (lanes of one window);
-//                O_h = sum_u a_u V_u: reduction over the same lanes      -> LDS
+//                softmax over the T rows of a window and O_h = sum_u a_u V_u:
+//                DPP reductions over the T lanes that hold one window  -> LDS
 //   h0^T  = Wo^T . O^T + X_last (fp32)    (waves split the features)   -> HBM
 // Only the last query row is formed: the head reads the last token, and under
 // the causal mask that row attends to every key of the window.
@@ -242,13 +242,9 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
           s += __shfl_xor(s, 16, 64);
           s += __shfl_xor(s, 32, 64);
           s *= scale;
-          float mx = s;
-#pragma unroll
-          for (int o = 1; o < T; o <<= 1) mx = fmaxf(mx, __shfl_xor(mx, o, 64));
+          const float mx = group_max<T>(s);
           const float p = expf(s - mx);
-          float sm = p;
-#pragma unroll
-          for (int o = 1; o < T; o <<= 1) sm += __shfl_xor(sm, o, 64);
+          const float sm = group_sum<T>(p);
           prob[rf] = p / sm;
           if (KEEP && live) {
             if (lg == 0) a.kA[(n * H + h) * T + t] = prob[rf];
@@ -265,12 +261,7 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
                   make_float4(acc[rf][f][0], acc[rf][f][1], acc[rf][f][2], acc[rf][f][3]);
             f32x4 ov;
 #pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              float o = prob[rf] * acc[rf][f][r];
-#pragma unroll
-              for (int sh = 1; sh < T; sh <<= 1) o += __shfl_xor(o, sh, 64);
-              ov[r] = o;
-            }
+            for (int r = 0; r < 4; ++r) ov[r] = group_sum<T>(prob[rf] * acc[rf][f][r]);
             if (t == 0) {
               const int cc = h * DH + f * 16 + 4 * lg;
               put4o((OT*)(Xl + m * XLSTR) + cc, ov);

@@ -261,6 +261,12 @@ __global__ __launch_bounds__(512) void k_ffn_head(FfnArgs a) {
 }
 
 // ------------------------------------------------------------ dispatch ----
+// Measured alternatives, both slower on the main workload (2^20 windows):
+// two 4-wave workgroups of 64 windows per CU (barriers desynchronised, but each
+// window carries twice the weight traffic from L2): 4.5 ms against 3.8 ms; a
+// software pipeline with G double-buffered in LDS (GEMM2 of chunk c, GELU of
+// chunk c+1 and GEMM1 of chunk c+2 in one interval), which needs 128-feature
+// chunks to fit the LDS: 4.5 ms.
 constexpr int ffn_lds_bytes(bool bf, int D, int mb, int fc) {
   return mb * (D * (bf ? 2 : 4) + 16) + mb * (fc * (bf ? 2 : 4) + 16) + mb * (2 * 4 * 4 + 8);
 }

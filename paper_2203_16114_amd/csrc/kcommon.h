@@ -125,6 +125,31 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
   return __builtin_bit_cast(uint32_t, v);
 }
 
+// Cross-lane reductions on the DPP path (no LDS traffic).  Within aligned
+// groups of 4 lanes: quad permutations xor 1 and xor 2; groups of 8 add the
+// mirrored half-row (lane i <-> 7 - i), which pairs each quad with the other.
+template <int CTRL>
+__device__ __forceinline__ float dpp_f(float v) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+}
+constexpr int DPP_XOR1 = 0xB1;          // quad_perm [1,0,3,2]
+constexpr int DPP_XOR2 = 0x4E;          // quad_perm [2,3,0,1]
+constexpr int DPP_HALF_MIRROR = 0x141;  // row_half_mirror
+template <int G>  // G = 4 or 8 lanes
+__device__ __forceinline__ float group_sum(float v) {
+  v += dpp_f<DPP_XOR1>(v);
+  v += dpp_f<DPP_XOR2>(v);
+  if constexpr (G == 8) v += dpp_f<DPP_HALF_MIRROR>(v);
+  return v;
+}
+template <int G>
+__device__ __forceinline__ float group_max(float v) {
+  v = fmaxf(v, dpp_f<DPP_XOR1>(v));
+  v = fmaxf(v, dpp_f<DPP_XOR2>(v));
+  if constexpr (G == 8) v = fmaxf(v, dpp_f<DPP_HALF_MIRROR>(v));
+  return v;
+}
+
 __device__ __forceinline__ float wave_sum16(float v) {  // over the 16 lanes sharing l/16
   v += __shfl_xor(v, 1, 64);
   v += __shfl_xor(v, 2, 64);
