@@ -11,7 +11,8 @@
 //   q^T   = Wq^T . X_last^T                 (waves split the features)   -> LDS
 //   per head h:  K_h^T = Wk_h^T . X^T, then V_h^T = Wv_h^T . X^T; the head's
 //                weight fragments are staged through LDS in double-buffered
-//                chunks shared by all 8 waves;
+//                chunks shared by all 8 waves, moved by direct global-to-LDS
+//                loads issued one chunk ahead;
 //                score of row u = q . K_u / sqrt(dh): 4-lane-group reduction;
 //                softmax over the T rows of a window and O_h = sum_u a_u V_u:
 //                DPP reductions over the T lanes that hold one window  -> LDS
@@ -175,14 +176,18 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
     const uint4* Wp = pass ? a.Wv : a.Wk;
     return Wp + ((ck * KSC + kk) * NB + h * NFH + f) * 64 + ln;
   };
-  constexpr int PT = (CHUNK + 511) / 512;
-  constexpr int NCH = H * 2 * CPP;
-  uint4 pre[PT];
+  constexpr int NFRAG = KSC * NFH;  // fragments per chunk, 1 KiB each
+  // chunk c -> LDS buffer: wave w moves fragments w, w + 8, ... with direct
+  // global-to-LDS loads (16 bytes per lane, lane order), no register staging
+  auto stage = [&](int c, int buf) {
 #pragma unroll
-  for (int p = 0; p < PT; ++p) {
-    const int i = tid + p * 512;
-    if (i < CHUNK) Wst[0][i] = *chunk_src(0, i);
-  }
+    for (int q = wave; q < NFRAG; q += NW)
+      __builtin_amdgcn_global_load_lds((const void*)chunk_src(c, q * 64 + lane),
+                                       (__attribute__((address_space(3))) void*)(Wst[buf] + q * 64), 16, 0, 0);
+  };
+  constexpr int NCH = H * 2 * CPP;
+  stage(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();  // chunk 0 staged; Qs complete; X_last rows no longer needed
 
   const float scale = a.scale;
@@ -198,13 +203,7 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
 #pragma unroll
       for (int ck = 0; ck < CPP; ++ck) {
         const int c = (h * 2 + pass) * CPP + ck;
-        if (c + 1 < NCH) {
-#pragma unroll
-          for (int p = 0; p < PT; ++p) {
-            const int i = tid + p * 512;
-            if (i < CHUNK) pre[p] = *chunk_src(c + 1, i);
-          }
-        }
+        if (c + 1 < NCH) stage(c + 1, (c + 1) & 1);
         const uint4* buf = Wst[c & 1];
 #pragma unroll
         for (int kk = 0; kk < KSC; ++kk) {
@@ -216,13 +215,7 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
 #pragma unroll
             for (int f = 0; f < NFH; ++f) M::run(acc[rf][f], af[f], xb[rf][ck * KSC + kk]);
         }
-        if (c + 1 < NCH) {
-#pragma unroll
-          for (int p = 0; p < PT; ++p) {
-            const int i = tid + p * 512;
-            if (i < CHUNK) Wst[(c + 1) & 1][i] = pre[p];
-          }
-        }
+        __builtin_amdgcn_s_waitcnt(0);  // this wave's part of chunk c + 1 has landed
         __syncthreads();
       }
       // lane holds K_h or V_h [row = wave*RW + rf*16 + lc][c = f*16 + 4*lg + r]
