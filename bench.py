@@ -9,11 +9,12 @@ accumulation): `--steps-per-call` consecutive positions of every stream, i.e.
 predicted bytes (= windows) per second over the timed steps, with the streams
 already in device memory.
 
-Besides the headline line this run measures, on the adaptation workload
-(the small model in bf16 with fp32 master weights, B = 4096 windows per step,
-sources switching every 2 KiB per stream), the controller-gated update loop
-against the always-update loop, and times the CPU oracle on a bounded sample
-of the main workload's windows on this machine's cores.
+Besides the headline line this run measures the controller-gated update loop
+against the always-update loop on the adaptation workload (the small model in
+bf16 with fp32 master weights, B = 4096 windows per step, sources switching
+every 2 KiB per stream) and on the large mixed workload (d = 512, B = 8192),
+and times the CPU oracle on a bounded sample of the main workload's windows on
+this machine's cores.
 
 Prints ONE JSON line (rank 0).  Only one GPU is supported.
 """
@@ -90,17 +91,17 @@ def gated_loop(model, sdev, B, pos0, n_steps, t, delta, always, max_spec=64):
     return updates, ce_sum / n_steps
 
 
-def measure_gated(args):
+def measure_gated(wid, n):
+    """Gated (controller) vs always-update loop over n steps of workload wid."""
     import torch
     import paper_2203_16114_amd as P
     import synth
-    w = synth.WORKLOADS[4]
+    w = synth.WORKLOADS[wid]
     B = w.B
-    n = args.gated_steps
     L = min(w.L, w.W + 1 + 2 * n + 2 * 64 + 64)
     t0 = time.time()
-    streams, _ = synth.workload_streams(4, L=L)
-    log(f"[bench] adaptation workload streams {streams.shape} in {time.time() - t0:.1f}s")
+    streams, _ = synth.workload_streams(wid, L=L)
+    log(f"[bench] {w.name} streams {streams.shape} in {time.time() - t0:.1f}s")
     sdev = torch.from_numpy(streams).cuda()
     res = {}
     for name, always in (("gated", False), ("always_update", True)):
@@ -122,13 +123,33 @@ def measure_gated(args):
                      "kernel_launches": {k: v[1] for k, v in tm.items() if k != "overflow" and v[1]}}
         if tm.get("adam", (0, 0))[1]:
             ms = tm["adam"][0] / tm["adam"][1]
-            res[name]["adam_hbm_frac"] = (28.0 * m.n_params / (ms * 1e-3)) / (HBM_GBS * 1e9)
-        log(f"[bench] {name}: {res[name]['bytes_per_s']:.4g} B/s, updates {upd}/{n}")
+            # Adam moves 28 bytes per parameter: reads theta, g, m, v; writes theta, m, v
+            res[name]["adam"] = {"avg_launch_ms": round(ms, 5), "bytes_per_launch": 28 * m.n_params,
+                                 "hbm_frac": round((28.0 * m.n_params / (ms * 1e-3)) / (HBM_GBS * 1e9), 4)}
+        log(f"[bench] {w.name} {name}: {res[name]['bytes_per_s']:.4g} B/s, updates {upd}/{n}")
         m.close()
     res["speedup_gated_vs_always"] = res["gated"]["bytes_per_s"] / res["always_update"]["bytes_per_s"]
     res["workload"] = f"{w.name}: B={B} windows/step, W={w.W} e={w.e} g={w.g} d={w.d} H={w.H} F={w.F} k={w.k}, " \
                       f"t={w.t} delta={w.delta}"
     return res
+
+
+def traffic_for(kernel, windows_per_launch):
+    """HBM bytes per launch of `kernel` from the committed counter summary
+    (profiles/hbm_traffic.json: FETCH_SIZE and WRITE_SIZE per dispatch, scaled by
+    the factors a 1 GiB device copy gives), or None when the summary is missing
+    or was taken on a different version of the kernel's source."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    try:
+        rec = json.load(open(path))["kernels"][kernel]
+        src = os.path.join(ROOT, "paper_2203_16114_amd", "csrc", rec["source"])
+        if hashlib.sha256(open(src, "rb").read()).hexdigest() != rec["source_sha256"]:
+            return None
+        per_window = rec["hbm_bytes_per_launch"] / rec["windows_per_launch"]
+        return per_window * windows_per_launch
+    except (OSError, KeyError, ValueError):
+        return None
 
 
 def cpu_baseline(streams, w, n_windows):
@@ -161,8 +182,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--steps-per-call", type=int, default=256, help="positions per stream in one step")
     ap.add_argument("--full", action="store_true", help="generate the full 256 KiB streams")
-    ap.add_argument("--gated-steps", type=int, default=256, help="steps of the gated-adaptation run (0: skip)")
-    ap.add_argument("--cpu-windows", type=int, default=2048, help="oracle sample (0: skip)")
+    ap.add_argument("--gated-steps", type=int, default=256, help="steps of each gated-adaptation run (0: skip)")
+    ap.add_argument("--cpu-windows", type=int, default=16384, help="oracle sample (0: skip)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run 5 device-to-device copies of this many MiB (calibrates the HBM "
                          "byte counters FETCH_SIZE / WRITE_SIZE against a copy of known size)")
@@ -231,9 +252,11 @@ def main():
     achieved = fpw[dom] * wpl / (per[dom] * 1e-3) / 1e12
     peak = PEAK_TFLOPS[w.dtype]
     total_tflops = (fpw["attn"] + fpw["ffn_head"]) * value / 1e12
-    roofline = {"bound": "mfma", "kernel": "k_ffn_head" if dom == "ffn_head" else "k_attn",
+    kname = "k_ffn_head" if dom == "ffn_head" else "k_attn"
+    traffic = traffic_for(kname, wpl)
+    roofline = {"bound": "mfma", "kernel": kname,
                 "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
-                "traffic": None,
+                "traffic": None if traffic is None else round(traffic),
                 "flops_per_window": fpw[dom], "windows_per_launch": wpl, "avg_launch_ms": round(per[dom], 4),
                 "kernels": {k: {"avg_launch_ms": round(per[k], 4),
                                 "tflops": round(fpw[k] * wpl / (per[k] * 1e-3) / 1e12, 2)} for k in per},
@@ -249,7 +272,8 @@ def main():
                       "windows_per_step": B * S, "steps_per_call": S, "stream_prefix_bytes": L},
            "bits_per_byte": bpb, "mfma_util": roofline["path_frac"], "roofline": roofline}
     if args.gated_steps > 0:
-        out["gated_adapt"] = measure_gated(args)
+        out["gated_adapt"] = {"adapt-bf16": measure_gated(4, args.gated_steps),
+                              "large-mixed-bf16": measure_gated(5, max(16, args.gated_steps // 2))}
     if args.cpu_windows > 0:
         out["cpu_baseline"] = cpu_baseline(streams, w, args.cpu_windows)
         log(f"[bench] cpu oracle: {out['cpu_baseline']['value']:.4g} bytes/s")

@@ -611,28 +611,49 @@ void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, c
 // bc2 = 1 - beta2^t supplied by the host.  Each product and sum is rounded on
 // its own (contraction into fused multiply-adds is off), in the order m = b1*m + (1-b1)*g,
 // v = b2*v + ((1-b2)*g)*g, theta -= (lr * m/bc1) / (sqrt(v/bc2) + eps).
-__global__ void k_adam(float* __restrict__ theta, const float* __restrict__ grad, float* __restrict__ m,
-                       float* __restrict__ v, int64_t n, float lr, float b1, float b2, float eps, float bc1,
-                       float bc2) {
+__device__ __forceinline__ void adam1(float& th, float g, float& m, float& v, float lr, float b1, float b2, float eps,
+                                      float bc1, float bc2) {
 #pragma clang fp contract(off)
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= n) return;
-  const float g = grad[i];
   const float omb1 = __fsub_rn(1.f, b1), omb2 = __fsub_rn(1.f, b2);
-  const float mi = __fadd_rn(__fmul_rn(b1, m[i]), __fmul_rn(omb1, g));
-  const float vi = __fadd_rn(__fmul_rn(b2, v[i]), __fmul_rn(__fmul_rn(omb2, g), g));
-  m[i] = mi;
-  v[i] = vi;
+  const float mi = __fadd_rn(__fmul_rn(b1, m), __fmul_rn(omb1, g));
+  const float vi = __fadd_rn(__fmul_rn(b2, v), __fmul_rn(__fmul_rn(omb2, g), g));
+  m = mi;
+  v = vi;
   const float mhat = __fdiv_rn(mi, bc1);
   const float vhat = __fdiv_rn(vi, bc2);
   // correctly rounded sqrt: the fp64 root rounded once to fp32 (53 >= 2*24 + 2
   // bits, so the two roundings give the singly rounded result)
   const float root = (float)__dsqrt_rn((double)vhat);
   const float step = __fdiv_rn(__fmul_rn(lr, mhat), __fadd_rn(root, eps));
-  theta[i] = __fsub_rn(theta[i], step);
+  th = __fsub_rn(th, step);
+}
+// four parameters per thread with 16-byte loads and stores (n % 4 elements at
+// the end one per thread)
+__global__ void k_adam(float* __restrict__ theta, const float* __restrict__ grad, float* __restrict__ m,
+                       float* __restrict__ v, int64_t n, float lr, float b1, float b2, float eps, float bc1,
+                       float bc2) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t n4 = n / 4;
+  if (i < n4) {
+    float4 t = reinterpret_cast<float4*>(theta)[i];
+    const float4 g = reinterpret_cast<const float4*>(grad)[i];
+    float4 mm = reinterpret_cast<float4*>(m)[i];
+    float4 vv = reinterpret_cast<float4*>(v)[i];
+    adam1(t.x, g.x, mm.x, vv.x, lr, b1, b2, eps, bc1, bc2);
+    adam1(t.y, g.y, mm.y, vv.y, lr, b1, b2, eps, bc1, bc2);
+    adam1(t.z, g.z, mm.z, vv.z, lr, b1, b2, eps, bc1, bc2);
+    adam1(t.w, g.w, mm.w, vv.w, lr, b1, b2, eps, bc1, bc2);
+    reinterpret_cast<float4*>(theta)[i] = t;
+    reinterpret_cast<float4*>(m)[i] = mm;
+    reinterpret_cast<float4*>(v)[i] = vv;
+  } else {
+    const int64_t j = 4 * n4 + (i - n4);
+    if (j < n) adam1(theta[j], grad[j], m[j], v[j], lr, b1, b2, eps, bc1, bc2);
+  }
 }
 void launch_adam(float* theta, const float* grad, float* m, float* v, int64_t n, float lr, float b1, float b2,
                  float eps, float bc1, float bc2, hipStream_t s) {
-  hipLaunchKernelGGL(k_adam, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, theta, grad, m, v, n, lr, b1, b2, eps,
-                     bc1, bc2);
+  const int64_t threads = n / 4 + n % 4;
+  hipLaunchKernelGGL(k_adam, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, theta, grad, m, v, n, lr, b1,
+                     b2, eps, bc1, bc2);
 }
