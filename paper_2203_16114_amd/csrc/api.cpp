@@ -132,7 +132,8 @@ void refresh_operands(trace_model* m, hipStream_t s) {
   launch_pack(m->bf, th + L.off[P_WV], D, D, m->Wv, s);
   launch_pack(m->bf, th + L.off[P_WO], D, D, m->Wo, s);
   launch_pack(m->bf, th + L.off[P_W1], D, F, m->W1, s);
-  launch_pack(m->bf, th + L.off[P_W2], F, D, m->W2, s);
+  // bf16: W2/2 (exact), since the bf16 FFN kernel forms 2 GELU(U) (exact in bf16 too)
+  launch_pack(m->bf, th + L.off[P_W2], F, D, m->W2, s, m->bf ? 0.5f : 1.f);
   launch_pack(m->bf, th + L.off[P_WOUT], D, 256, m->Wout, s);
   tend(m, tk, TRACE_KIND_REFRESH, s);
 }

@@ -11,7 +11,11 @@
 // Waves form a 4 x 2 grid: 4 groups of output features x 2 groups of windows.
 // The residual stream Y stays in accumulator registers for all k repeats; the
 // weights stream from L2 in the fragment-packed layout, one k-step ahead of the
-// MFMAs that use them; the activations are read from LDS.
+// MFMAs that use them; the activations are read from LDS.  k_ffn_head is the
+// plain form (fp32 operands); k_ffn_pipe, further down, is the bf16 form, which
+// overlaps the GELU with the MFMAs of neighbouring chunks.
+#include <type_traits>
+
 #include "kcommon.h"
 #include "kernels.h"
 #include "win.h"
@@ -22,6 +26,114 @@ __device__ __forceinline__ void put4(uint16_t* p, const f32x4& v) {
 }
 __device__ __forceinline__ void put4(float* p, const f32x4& v) {
   *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
+}
+
+// Head on bf(Y_k) staged in Ys, then the code length (shared by both FFN
+// kernels): z^T = Wout^T . Y^T + bout, log-sum-exp across the 4 feature waves
+// through LDS in a fixed order, bits = log2 sum exp(z - max) - (z_y - max) log2 e.
+template <bool BF, int D, int MB, bool KEEP, int YSTR>
+__device__ __forceinline__ void ffn_head_out(const FfnArgs& a, const unsigned char* Ys, float (&red)[2][4][MB],
+                                             float* zy, const int* tg) {
+  typedef Mma<BF> M;
+  typedef typename M::T OT;
+  constexpr int WR = 4, WC = 2;
+  constexpr int CW = MB / WC, NFC = CW / 16;
+  constexpr int RFH = 256 / (WR * 16);
+  constexpr int KD = D / M::KS;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lg = lane >> 4, lc = lane & 15;
+  const int wr = wave % WR, wc = wave / WR;
+  const int64_t tile0 = (int64_t)blockIdx.x * MB;
+  const int64_t N = a.w.N;
+  const int m0 = wc * CW;
+  const unsigned char* yrow[NFC];
+#pragma unroll
+  for (int nf = 0; nf < NFC; ++nf) yrow[nf] = Ys + (m0 + nf * 16 + lc) * YSTR + lg * 16;
+  f32x4 z[RFH][NFC];
+#pragma unroll
+  for (int rf = 0; rf < RFH; ++rf)
+#pragma unroll
+    for (int nf = 0; nf < NFC; ++nf) z[rf][nf] = f32x4{0.f, 0.f, 0.f, 0.f};
+  uint4 wz[2][RFH];
+#pragma unroll
+  for (int rf = 0; rf < RFH; ++rf) wz[0][rf] = a.Wout[(wr * RFH + rf) * 64 + lane];
+#pragma unroll
+  for (int ks = 0; ks < KD; ++ks) {
+    if (ks + 1 < KD) {
+#pragma unroll
+      for (int rf = 0; rf < RFH; ++rf) wz[(ks + 1) & 1][rf] = a.Wout[((ks + 1) * 16 + wr * RFH + rf) * 64 + lane];
+    }
+    uint4 bb[NFC];
+#pragma unroll
+    for (int nf = 0; nf < NFC; ++nf) bb[nf] = *(const uint4*)(yrow[nf] + ks * 64);
+#pragma unroll
+    for (int rf = 0; rf < RFH; ++rf)
+#pragma unroll
+      for (int nf = 0; nf < NFC; ++nf) M::run(z[rf][nf], wz[ks & 1][rf], bb[nf]);
+  }
+  // lane holds z[v = wr*64 + rf*16 + 4*lg + r] of window m0 + nf*16 + lc
+#pragma unroll
+  for (int rf = 0; rf < RFH; ++rf) {
+    const float4 bo = *reinterpret_cast<const float4*>(a.bout + wr * 64 + rf * 16 + 4 * lg);
+#pragma unroll
+    for (int nf = 0; nf < NFC; ++nf) {
+      z[rf][nf][0] += bo.x;
+      z[rf][nf][1] += bo.y;
+      z[rf][nf][2] += bo.z;
+      z[rf][nf][3] += bo.w;
+    }
+  }
+#pragma unroll
+  for (int nf = 0; nf < NFC; ++nf) {
+    const int m = m0 + nf * 16 + lc;
+    float mx = z[0][nf][0];
+#pragma unroll
+    for (int rf = 0; rf < RFH; ++rf)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) mx = fmaxf(mx, z[rf][nf][r]);
+    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    if (lg == 0) red[0][wr][m] = mx;
+    const int t = tg[m];
+#pragma unroll
+    for (int rf = 0; rf < RFH; ++rf)
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (wr * 64 + rf * 16 + 4 * lg + r == t) zy[m] = z[rf][nf][r];
+  }
+  __syncthreads();
+#pragma unroll
+  for (int nf = 0; nf < NFC; ++nf) {
+    const int m = m0 + nf * 16 + lc;
+    const int64_t n = tile0 + m;
+    const float mx = fmaxf(fmaxf(red[0][0][m], red[0][1][m]), fmaxf(red[0][2][m], red[0][3][m]));
+    float se = 0.f;
+#pragma unroll
+    for (int rf = 0; rf < RFH; ++rf)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) se += expf(z[rf][nf][r] - mx);
+    se += __shfl_xor(se, 16, 64);
+    se += __shfl_xor(se, 32, 64);
+    if (lg == 0) red[1][wr][m] = se;
+    if (n < N) {
+#pragma unroll
+      for (int rf = 0; rf < RFH; ++rf) {
+        const int v = wr * 64 + rf * 16 + 4 * lg;
+        const float4 zz = make_float4(z[rf][nf][0], z[rf][nf][1], z[rf][nf][2], z[rf][nf][3]);
+        if (a.logits) *reinterpret_cast<float4*>(a.logits + (a.w.n0 + n) * 256 + v) = zz;
+        if (KEEP) *reinterpret_cast<float4*>(a.kZ + n * 256 + v) = zz;
+      }
+    }
+  }
+  __syncthreads();
+  if (tid < MB) {
+    const int m = tid;
+    const int64_t n = tile0 + m;
+    if (n < N) {
+      const float mx = fmaxf(fmaxf(red[0][0][m], red[0][1][m]), fmaxf(red[0][2][m], red[0][3][m]));
+      const float tot = ((red[1][0][m] + red[1][1][m]) + red[1][2][m]) + red[1][3][m];
+      a.bits[a.w.n0 + n] = log2f(tot) - (zy[m] - mx) * TRACE_LOG2E;
+    }
+  }
 }
 
 template <bool BF, int D, int MB, int FC, bool KEEP>
@@ -171,102 +283,277 @@ __global__ __launch_bounds__(512) void k_ffn_head(FfnArgs a) {
     }
   }
 
-  // head on bf(Y_k) (staged in Ys by the last pass above)
-  f32x4 z[RFH][NFC];
-#pragma unroll
-  for (int rf = 0; rf < RFH; ++rf)
-#pragma unroll
-    for (int nf = 0; nf < NFC; ++nf) z[rf][nf] = f32x4{0.f, 0.f, 0.f, 0.f};
-  uint4 wz[2][RFH];
-#pragma unroll
-  for (int rf = 0; rf < RFH; ++rf) wz[0][rf] = a.Wout[(wr * RFH + rf) * 64 + lane];
-#pragma unroll
-  for (int ks = 0; ks < KD; ++ks) {
-    if (ks + 1 < KD) {
-#pragma unroll
-      for (int rf = 0; rf < RFH; ++rf) wz[(ks + 1) & 1][rf] = a.Wout[((ks + 1) * 16 + wr * RFH + rf) * 64 + lane];
-    }
-    uint4 bb[NFC];
-#pragma unroll
-    for (int nf = 0; nf < NFC; ++nf) bb[nf] = *(const uint4*)(yrow[nf] + ks * 64);
-#pragma unroll
-    for (int rf = 0; rf < RFH; ++rf)
-#pragma unroll
-      for (int nf = 0; nf < NFC; ++nf) M::run(z[rf][nf], wz[ks & 1][rf], bb[nf]);
-  }
-  // lane holds z[v = wr*64 + rf*16 + 4*lg + r] of window m0 + nf*16 + lc
-#pragma unroll
-  for (int rf = 0; rf < RFH; ++rf) {
-    const float4 bo = *reinterpret_cast<const float4*>(a.bout + wr * 64 + rf * 16 + 4 * lg);
-#pragma unroll
-    for (int nf = 0; nf < NFC; ++nf) {
-      z[rf][nf][0] += bo.x;
-      z[rf][nf][1] += bo.y;
-      z[rf][nf][2] += bo.z;
-      z[rf][nf][3] += bo.w;
-    }
-  }
-#pragma unroll
-  for (int nf = 0; nf < NFC; ++nf) {
-    const int m = m0 + nf * 16 + lc;
-    float mx = z[0][nf][0];
-#pragma unroll
-    for (int rf = 0; rf < RFH; ++rf)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) mx = fmaxf(mx, z[rf][nf][r]);
-    mx = fmaxf(mx, __shfl_xor(mx, 16, 64));
-    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    if (lg == 0) red[0][wr][m] = mx;
-    const int t = tg[m];
-#pragma unroll
-    for (int rf = 0; rf < RFH; ++rf)
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (wr * 64 + rf * 16 + 4 * lg + r == t) zy[m] = z[rf][nf][r];
-  }
-  __syncthreads();
-#pragma unroll
-  for (int nf = 0; nf < NFC; ++nf) {
-    const int m = m0 + nf * 16 + lc;
-    const int64_t n = tile0 + m;
-    const float mx = fmaxf(fmaxf(red[0][0][m], red[0][1][m]), fmaxf(red[0][2][m], red[0][3][m]));
-    float se = 0.f;
-#pragma unroll
-    for (int rf = 0; rf < RFH; ++rf)
-#pragma unroll
-      for (int r = 0; r < 4; ++r) se += expf(z[rf][nf][r] - mx);
-    se += __shfl_xor(se, 16, 64);
-    se += __shfl_xor(se, 32, 64);
-    if (lg == 0) red[1][wr][m] = se;
-    if (n < N) {
-#pragma unroll
-      for (int rf = 0; rf < RFH; ++rf) {
-        const int v = wr * 64 + rf * 16 + 4 * lg;
-        const float4 zz = make_float4(z[rf][nf][0], z[rf][nf][1], z[rf][nf][2], z[rf][nf][3]);
-        if (a.logits) *reinterpret_cast<float4*>(a.logits + (a.w.n0 + n) * 256 + v) = zz;
-        if (KEEP) *reinterpret_cast<float4*>(a.kZ + n * 256 + v) = zz;
-      }
-    }
-  }
-  __syncthreads();
-  if (tid < MB) {
-    const int m = tid;
-    const int64_t n = tile0 + m;
-    if (n < N) {
-      const float mx = fmaxf(fmaxf(red[0][0][m], red[0][1][m]), fmaxf(red[0][2][m], red[0][3][m]));
-      const float tot = ((red[1][0][m] + red[1][1][m]) + red[1][2][m]) + red[1][3][m];
-      a.bits[a.w.n0 + n] = log2f(tot) - (zy[m] - mx) * TRACE_LOG2E;
-    }
+  ffn_head_out<BF, D, MB, KEEP, YSTR>(a, Ys, red, zy, tg);
+}
+
+// ------------------------------------------------- pipelined bf16 variant ----
+// Same arithmetic as k_ffn_head (bf16 operands, fp32 accumulation, U rounded
+// to bf16 after GELU), restructured so that the GELU's vector ALU work runs in
+// the same wave as independent MFMAs.  F is cut into chunks of 128 features
+// and each interval between two barriers does, per wave:
+//   GEMM2 of chunk j-1 (reads G from LDS buffer (j-1)&1, accumulates Y),
+//   GEMM1 of chunk j+1 (reads bf(Y) from LDS, accumulates U into one register set),
+//   GELU of chunk j    (the other register set, in place, written to buffer j&1),
+// with one GELU value issued after every few MFMAs.  The two U register sets
+// alternate roles from one interval to the next; the loop takes two intervals
+// per trip so that the roles stay compile-time.  G holds bf(2 GELU(U)) and the
+// packed W2 copy holds bf(W2)/2: both scalings are exact, so every product is
+// the one of bf(GELU(U)) and bf(W2), with one vector operation less per value.
+template <int D, int MB>
+struct FfnPipe {
+  static constexpr int FC = 128, WR = 4, WC = 2;
+  static constexpr int CW = MB / WC, NFC = CW / 16;
+  static constexpr int RF1 = FC / (WR * 16), RF2 = D / (WR * 16);
+  static constexpr int RFA = RF2 > RF1 ? RF2 : RF1;
+#ifndef TRACE_FFN_YPAD
+#define TRACE_FFN_YPAD 16
+#endif
+#ifndef TRACE_FFN_GPAD
+#define TRACE_FFN_GPAD 16
+#endif
+  static constexpr int YSTR = D * 2 + TRACE_FFN_YPAD, GSTR = FC * 2 + TRACE_FFN_GPAD;
+  static constexpr int KD = D / 32, KC = FC / 32;
+  static constexpr int NB2 = D / 16;
+  static constexpr int NGV = RF1 * NFC * 4;  // GELU values per lane per chunk
+  static constexpr int LDS = MB * YSTR + 2 * MB * GSTR + MB * (2 * 4 * 4 + 8);
+#ifdef TRACE_FFN_PDA
+  static constexpr int PDA = TRACE_FFN_PDA;
+#else
+  static constexpr int PDA = 1;
+#endif
+};
+
+struct PipeLane {
+  __amdgpu_buffer_rsrc_t W1r, W2r;  // buffer descriptors of the packed W1 / W2 copies
+  int w1o, w2o;                     // byte offset of this wave's first fragment column (wave-uniform)
+  int NB1, lg, f0;
+  int voff;                         // lane * 16 bytes
+  const unsigned char* ybase;       // Ys row (m0 + lc), byte lg*16
+};
+
+// Buffer descriptor over n bytes at p (raw, untyped; reads past n return 0).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* p, int64_t n) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(p), (short)0, (int)n, 0x00020000);
+}
+// The lane's 16-byte fragment at a wave-uniform byte offset: one buffer load
+// with the lane offset in a vector register and the rest in a scalar one.
+__device__ __forceinline__ uint4 frag_at(__amdgpu_buffer_rsrc_t r, int voff, int soff) {
+  return __builtin_bit_cast(uint4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+
+// Calls f(integral_constant<I>) for I = B .. E-1: every index is a constant.
+template <int B, int E, class Fn>
+__device__ __forceinline__ void static_for(Fn&& f) {
+  if constexpr (B < E) {
+    f(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(f);
   }
 }
 
+// One interval.  G2ON: GEMM2 of the chunk at feature c2 from buffer gr;
+// G1ON: GEMM1 of the chunk at feature c1 into un; GELUON: GELU of ug into gw.
+template <int D, int MB, bool G2ON, bool G1ON, bool GELUON>
+__device__ __forceinline__ void ffn_interval(const PipeLane& L, f32x4 (&y)[FfnPipe<D, MB>::RF2][FfnPipe<D, MB>::NFC],
+                                             f32x4 (&ug)[FfnPipe<D, MB>::RF1][FfnPipe<D, MB>::NFC],
+                                             f32x4 (&un)[FfnPipe<D, MB>::RF1][FfnPipe<D, MB>::NFC], int c1, int c2,
+                                             const unsigned char* gr, unsigned char* gw) {
+  typedef FfnPipe<D, MB> P;
+  constexpr int NFC = P::NFC, RF1 = P::RF1, RF2 = P::RF2, RFA = P::RFA;
+  constexpr int S2 = G2ON ? P::KC : 0, S1 = G1ON ? P::KD : 0, NS = S2 + S1;
+  constexpr int NM = S2 * RF2 * NFC + S1 * RF1 * NFC;
+  constexpr int NGV = GELUON ? P::NGV : 0;
+  static_assert(NS > 0, "empty interval");
+  if constexpr (G1ON) {
+#pragma unroll
+    for (int rf = 0; rf < RF1; ++rf)
+#pragma unroll
+      for (int nf = 0; nf < NFC; ++nf) un[rf][nf] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const int kc2 = c2 / 32, nb1 = c1 / 16;
+  // weight fragments (L2) are requested PDA steps ahead, activations (LDS) one
+  constexpr int PDA = P::PDA, NA = PDA + 1;
+  uint4 A[NA][RFA], B[2][NFC];
+  auto loadA = [&](auto sc) {
+    constexpr int s = decltype(sc)::value, buf = s % NA;
+    if constexpr (s < S2) {
+#pragma unroll
+      for (int rf = 0; rf < RF2; ++rf) A[buf][rf] = frag_at(L.W2r, L.voff, L.w2o + ((kc2 + s) * P::NB2 + rf) * 1024);
+    } else {
+      constexpr int ks = s - S2;
+#pragma unroll
+      for (int rf = 0; rf < RF1; ++rf) A[buf][rf] = frag_at(L.W1r, L.voff, L.w1o + (ks * L.NB1 + nb1 + rf) * 1024);
+    }
+  };
+  auto loadB = [&](auto sc) {
+    constexpr int s = decltype(sc)::value, buf = s & 1;
+    if constexpr (s < S2) {
+#pragma unroll
+      for (int nf = 0; nf < NFC; ++nf) B[buf][nf] = *(const uint4*)(gr + nf * 16 * P::GSTR + s * 64);
+    } else {
+      constexpr int ks = s - S2;
+#pragma unroll
+      for (int nf = 0; nf < NFC; ++nf) B[buf][nf] = *(const uint4*)(L.ybase + nf * 16 * P::YSTR + ks * 64);
+    }
+  };
+  static_for<0, (PDA < NS ? PDA : NS)>(loadA);
+  loadB(std::integral_constant<int, 0>{});
+  static_for<0, NS>([&](auto sc) {
+    constexpr int s = decltype(sc)::value, abuf = s % NA, bbuf = s & 1;
+    if constexpr (s + PDA < NS) loadA(std::integral_constant<int, s + PDA>{});
+    if constexpr (s + 1 < NS) loadB(std::integral_constant<int, s + 1>{});
+    constexpr bool g2 = s < S2;
+    constexpr int RFN = g2 ? RF2 : RF1;
+    constexpr int MB0 = g2 ? s * RF2 * NFC : S2 * RF2 * NFC + (s - S2) * RF1 * NFC;
+    static_for<0, RFN * NFC>([&](auto ic) {
+      constexpr int i = decltype(ic)::value, rf = i / NFC, nf = i % NFC, m = MB0 + i;
+      if constexpr (g2)
+        Mma<true>::run(y[rf][nf], A[abuf][rf], B[bbuf][nf]);
+      else
+        Mma<true>::run(un[rf][nf], A[abuf][rf], B[bbuf][nf]);
+      if constexpr (NGV > 0) {
+        static_for<(m * NGV) / NM, ((m + 1) * NGV) / NM>([&](auto gc) {
+          constexpr int g = decltype(gc)::value;
+          f32x4& v = ug[g / (NFC * 4)][(g / 4) % NFC];
+          v[g % 4] = gelu2_as(v[g % 4]);
+        });
+      }
+    });
+    // keep each step's loads one step ahead, not hoisted further
+    __builtin_amdgcn_sched_barrier(0);
+  });
+  if constexpr (GELUON) {
+#pragma unroll
+    for (int nf = 0; nf < NFC; ++nf)
+#pragma unroll
+      for (int rf = 0; rf < RF1; ++rf)
+        put4((uint16_t*)(gw + nf * 16 * P::GSTR) + L.f0 + rf * 16 + 4 * L.lg, ug[rf][nf]);
+  }
+}
+
+template <int D, int MB, bool KEEP>
+__global__ __launch_bounds__(512) void k_ffn_pipe(FfnArgs a) {
+  typedef FfnPipe<D, MB> P;
+  constexpr int NFC = P::NFC, RF1 = P::RF1, RF2 = P::RF2, FC = P::FC;
+  static_assert(RF1 >= 1 && RF2 >= 1 && NFC >= 1 && MB % (16 * P::WC) == 0, "shape");
+  static_assert(P::LDS <= 160 * 1024, "LDS");
+  __shared__ __align__(16) unsigned char Ys[MB * P::YSTR];
+  __shared__ __align__(16) unsigned char Gs[2][MB * P::GSTR];
+  __shared__ float red[2][4][MB];
+  __shared__ float zy[MB];
+  __shared__ int tg[MB];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lg = lane >> 4, lc = lane & 15;
+  const int wr = wave % P::WR, wc = wave / P::WR;
+  const int64_t tile0 = (int64_t)blockIdx.x * MB;
+  const int64_t N = a.w.N;
+  const int F = a.F;
+  const int NC = F / FC;  // even: F is a multiple of 256
+  const int m0 = wc * P::CW;
+  const int d0 = wr * (D / P::WR);
+  PipeLane L;
+  L.f0 = __builtin_amdgcn_readfirstlane(wr * (FC / P::WR));
+  L.W1r = make_rsrc(a.W1, (int64_t)D * F * 2);
+  L.W2r = make_rsrc(a.W2, (int64_t)D * F * 2);
+  L.w1o = (L.f0 / 16) * 1024;
+  L.w2o = __builtin_amdgcn_readfirstlane(d0 / 16) * 1024;
+  L.NB1 = F / 16;
+  L.voff = lane * 16;
+  L.lg = lg;
+  L.ybase = Ys + (m0 + lc) * P::YSTR + lg * 16;
+  const unsigned char* gr0 = Gs[0] + (m0 + lc) * P::GSTR + lg * 16;
+  const unsigned char* gr1 = Gs[1] + (m0 + lc) * P::GSTR + lg * 16;
+  unsigned char* gw0 = Gs[0] + (m0 + lc) * P::GSTR;
+  unsigned char* gw1 = Gs[1] + (m0 + lc) * P::GSTR;
+
+  f32x4 y[RF2][NFC];
+#pragma unroll
+  for (int nf = 0; nf < NFC; ++nf) {
+    const int64_t n = tile0 + m0 + nf * 16 + lc;
+#pragma unroll
+    for (int rf = 0; rf < RF2; ++rf) {
+      if (n < N) {
+        const float4 v = *reinterpret_cast<const float4*>(a.h0 + n * D + d0 + rf * 16 + 4 * lg);
+        y[rf][nf] = f32x4{v.x, v.y, v.z, v.w};
+      } else {
+        y[rf][nf] = f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+  }
+  if (tid < MB) {
+    const int64_t n = tile0 + tid;
+    int v = 0;
+    if (n < N) {
+      v = a.w.streams[target_offset(a.w, n)];
+      if (KEEP) a.ktgt[n] = v;
+    }
+    tg[tid] = v;
+  }
+
+  f32x4 ua[RF1][NFC], ub[RF1][NFC];
+  // pre-GELU U of the chunk at feature c, kept for the backward pass
+  auto keep_u = [&](const f32x4 (&u)[RF1][NFC], int rep, int c) {
+#pragma unroll
+    for (int nf = 0; nf < NFC; ++nf) {
+      const int64_t n = tile0 + m0 + nf * 16 + lc;
+      if (n < N) {
+#pragma unroll
+        for (int rf = 0; rf < RF1; ++rf)
+          *reinterpret_cast<float4*>(a.kU + ((int64_t)rep * N + n) * F + c + L.f0 + rf * 16 + 4 * lg) =
+              make_float4(u[rf][nf][0], u[rf][nf][1], u[rf][nf][2], u[rf][nf][3]);
+      }
+    }
+  };
+
+  for (int rep = 0; rep <= a.k; ++rep) {
+#pragma unroll
+    for (int nf = 0; nf < NFC; ++nf) {
+      const int m = m0 + nf * 16 + lc;
+      const int64_t n = tile0 + m;
+#pragma unroll
+      for (int rf = 0; rf < RF2; ++rf) {
+        const int dd = d0 + rf * 16 + 4 * lg;
+        if (KEEP && n < N)
+          *reinterpret_cast<float4*>(a.kY + ((int64_t)rep * N + n) * D + dd) =
+              make_float4(y[rf][nf][0], y[rf][nf][1], y[rf][nf][2], y[rf][nf][3]);
+        put4((uint16_t*)(Ys + m * P::YSTR) + dd, y[rf][nf]);
+      }
+    }
+    __syncthreads();
+    if (rep == a.k) break;
+    // prologue: GEMM1 of chunk 0 into ua
+    ffn_interval<D, MB, false, true, false>(L, y, ub, ua, 0, 0, gr0, gw0);
+    if (KEEP) keep_u(ua, rep, 0);
+    // j = 0: GELU(0) -> buffer 0, GEMM1(1) -> ub
+    ffn_interval<D, MB, false, true, true>(L, y, ua, ub, FC, 0, gr0, gw0);
+    __syncthreads();
+    for (int j = 1; j < NC - 1; j += 2) {
+      if (KEEP) keep_u(ub, rep, j * FC);
+      // j (odd): GELU(j) -> buffer 1, GEMM1(j+1) -> ua, GEMM2(j-1) from buffer 0
+      ffn_interval<D, MB, true, true, true>(L, y, ub, ua, (j + 1) * FC, (j - 1) * FC, gr0, gw1);
+      __syncthreads();
+      if (KEEP) keep_u(ua, rep, (j + 1) * FC);
+      // j+1 (even): GELU(j+1) -> buffer 0, GEMM1(j+2) -> ub, GEMM2(j) from buffer 1
+      ffn_interval<D, MB, true, true, true>(L, y, ua, ub, (j + 2) * FC, j * FC, gr1, gw0);
+      __syncthreads();
+    }
+    if (KEEP) keep_u(ub, rep, (NC - 1) * FC);
+    // j = NC-1 (odd): GELU(NC-1) -> buffer 1, GEMM2(NC-2) from buffer 0
+    ffn_interval<D, MB, true, false, true>(L, y, ub, ua, 0, (NC - 2) * FC, gr0, gw1);
+    __syncthreads();
+    // epilogue: GEMM2(NC-1) from buffer 1
+    ffn_interval<D, MB, true, false, false>(L, y, ua, ub, 0, (NC - 1) * FC, gr1, gw0);
+  }
+  ffn_head_out<true, D, MB, KEEP, P::YSTR>(a, Ys, red, zy, tg);
+}
+
 // ------------------------------------------------------------ dispatch ----
-// Measured alternatives, both slower on the main workload (2^20 windows):
-// two 4-wave workgroups of 64 windows per CU (barriers desynchronised, but each
-// window carries twice the weight traffic from L2): 4.5 ms against 3.8 ms; a
-// software pipeline with G double-buffered in LDS (GEMM2 of chunk c, GELU of
-// chunk c+1 and GEMM1 of chunk c+2 in one interval), which needs 128-feature
-// chunks to fit the LDS: 4.5 ms.
+// bf16 runs the pipelined kernel (k_ffn_pipe); fp32 runs k_ffn_head.
+// Measured on the main workload (2^20 windows, d = 256), k_ffn_head in bf16
+// took 3.67 ms and k_ffn_pipe 3.55 ms.  Slower alternatives measured: two 4-wave
+// workgroups of 64 windows per CU (each window carries twice the weight traffic
+// from L2), 4.5 ms; the pipeline with weights requested 2 or 3 steps ahead
+// instead of 1, 3.65 / 3.69 ms; LDS row padding of 32 or 64 bytes instead of 16,
+// 3.60 / 3.84 ms (none: 6.25 ms).
 constexpr int ffn_lds_bytes(bool bf, int D, int mb, int fc) {
   return mb * (D * (bf ? 2 : 4) + 16) + mb * (fc * (bf ? 2 : 4) + 16) + mb * (2 * 4 * 4 + 8);
 }
@@ -276,15 +563,28 @@ constexpr int pick_mb(bool bf, int D) {
 }
 constexpr int pick_fc(bool bf, int D) { return ffn_lds_bytes(bf, D, pick_mb(bf, D), 256) <= 160 * 1024 ? 256 : 128; }
 
+template <int D>
+constexpr int pick_mb_pipe() { return FfnPipe<D, 128>::LDS <= 160 * 1024 ? 128 : 64; }
+
 template <bool BF, int D>
 static void run_ffn(const FfnArgs& a, hipStream_t s) {
-  constexpr int MB = pick_mb(BF, D), FC = pick_fc(BF, D);
-  static_assert(ffn_lds_bytes(BF, D, MB, FC) <= 160 * 1024, "LDS");
-  const dim3 grid((unsigned)((a.w.N + MB - 1) / MB));
-  if (a.kY)
-    hipLaunchKernelGGL((k_ffn_head<BF, D, MB, FC, true>), grid, dim3(512), 0, s, a);
-  else
-    hipLaunchKernelGGL((k_ffn_head<BF, D, MB, FC, false>), grid, dim3(512), 0, s, a);
+  if constexpr (BF) {
+    constexpr int MB = pick_mb_pipe<D>();
+    static_assert(FfnPipe<D, MB>::LDS <= 160 * 1024, "LDS");
+    const dim3 grid((unsigned)((a.w.N + MB - 1) / MB));
+    if (a.kY)
+      hipLaunchKernelGGL((k_ffn_pipe<D, MB, true>), grid, dim3(512), 0, s, a);
+    else
+      hipLaunchKernelGGL((k_ffn_pipe<D, MB, false>), grid, dim3(512), 0, s, a);
+  } else {
+    constexpr int MB = pick_mb(BF, D), FC = pick_fc(BF, D);
+    static_assert(ffn_lds_bytes(BF, D, MB, FC) <= 160 * 1024, "LDS");
+    const dim3 grid((unsigned)((a.w.N + MB - 1) / MB));
+    if (a.kY)
+      hipLaunchKernelGGL((k_ffn_head<BF, D, MB, FC, true>), grid, dim3(512), 0, s, a);
+    else
+      hipLaunchKernelGGL((k_ffn_head<BF, D, MB, FC, false>), grid, dim3(512), 0, s, a);
+  }
 }
 
 ffn_fn find_ffn(bool bf, int D) {

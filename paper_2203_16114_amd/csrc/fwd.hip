@@ -22,9 +22,10 @@
 // ------------------------------------------------------------------ packing ----
 // W [K][N] row-major fp32 -> fragment-packed operand copy: fragment (ks, nb) is
 // 64 lanes x 16 bytes at offset ((ks * N/16 + nb) * 64 + lane) * 16; lane l holds
-// column nb*16 + l%16 and k = ks*KS + (l/16)*EPF + j, j < EPF.
+// column nb*16 + l%16 and k = ks*KS + (l/16)*EPF + j, j < EPF.  Each value is
+// multiplied by scale (a power of two, so the operand is the scaled rounded value).
 template <bool BF>
-__global__ void k_pack(const float* __restrict__ W, int K, int N, uint4* __restrict__ out) {
+__global__ void k_pack(const float* __restrict__ W, int K, int N, uint4* __restrict__ out, float scale) {
   typedef Mma<BF> M;
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   const int NB = N / 16, KSN = K / M::KS;
@@ -36,21 +37,21 @@ __global__ void k_pack(const float* __restrict__ W, int K, int N, uint4* __restr
   const int kb = ks * M::KS + (lane >> 4) * M::EPF;
   float v[8];
 #pragma unroll
-  for (int j = 0; j < M::EPF; ++j) v[j] = W[(int64_t)(kb + j) * N + n];
+  for (int j = 0; j < M::EPF; ++j) v[j] = W[(int64_t)(kb + j) * N + n] * scale;
   union { uint4 u; typename M::T t[M::EPF]; } r;
 #pragma unroll
   for (int j = 0; j < M::EPF; ++j) r.t[j] = M::cvt(v[j]);
   out[i] = r.u;
 }
 
-void launch_pack(bool bf, const float* W, int K, int N, void* out, hipStream_t s) {
+void launch_pack(bool bf, const float* W, int K, int N, void* out, hipStream_t s, float scale) {
   const int KS = bf ? 32 : 16;
   const int64_t total = (int64_t)(K / KS) * (N / 16) * 64;
   const dim3 grid((unsigned)((total + 255) / 256));
   if (bf)
-    hipLaunchKernelGGL(k_pack<true>, grid, dim3(256), 0, s, W, K, N, (uint4*)out);
+    hipLaunchKernelGGL(k_pack<true>, grid, dim3(256), 0, s, W, K, N, (uint4*)out, scale);
   else
-    hipLaunchKernelGGL(k_pack<false>, grid, dim3(256), 0, s, W, K, N, (uint4*)out);
+    hipLaunchKernelGGL(k_pack<false>, grid, dim3(256), 0, s, W, K, N, (uint4*)out, scale);
 }
 
 template <bool BF>

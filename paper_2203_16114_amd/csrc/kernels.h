@@ -51,7 +51,7 @@ typedef void (*ffn_fn)(const FfnArgs&, hipStream_t);
 attn_fn find_attn(bool bf, int T, int D, int DH);
 ffn_fn find_ffn(bool bf, int D);
 
-void launch_pack(bool bf, const float* W, int K, int N, void* out, hipStream_t s);
+void launch_pack(bool bf, const float* W, int K, int N, void* out, hipStream_t s, float scale = 1.f);
 void launch_zero(void* p, int64_t n32, hipStream_t s);
 void launch_cvt(bool bf, const float* src, void* dst, int64_t n, hipStream_t s);
 void launch_step_ce(const float* bits, int32_t n_streams, int32_t n_steps, double* out, hipStream_t s);
