@@ -305,22 +305,12 @@ struct FfnPipe {
   static constexpr int CW = MB / WC, NFC = CW / 16;
   static constexpr int RF1 = FC / (WR * 16), RF2 = D / (WR * 16);
   static constexpr int RFA = RF2 > RF1 ? RF2 : RF1;
-#ifndef TRACE_FFN_YPAD
-#define TRACE_FFN_YPAD 16
-#endif
-#ifndef TRACE_FFN_GPAD
-#define TRACE_FFN_GPAD 16
-#endif
-  static constexpr int YSTR = D * 2 + TRACE_FFN_YPAD, GSTR = FC * 2 + TRACE_FFN_GPAD;
+  static constexpr int YSTR = D * 2 + 16, GSTR = FC * 2 + 16;
   static constexpr int KD = D / 32, KC = FC / 32;
   static constexpr int NB2 = D / 16;
   static constexpr int NGV = RF1 * NFC * 4;  // GELU values per lane per chunk
   static constexpr int LDS = MB * YSTR + 2 * MB * GSTR + MB * (2 * 4 * 4 + 8);
-#ifdef TRACE_FFN_PDA
-  static constexpr int PDA = TRACE_FFN_PDA;
-#else
-  static constexpr int PDA = 1;
-#endif
+  static constexpr int PDA = 1;  // weight fragments requested one step ahead
 };
 
 struct PipeLane {
@@ -553,7 +543,11 @@ __global__ __launch_bounds__(512) void k_ffn_pipe(FfnArgs a) {
 // workgroups of 64 windows per CU (each window carries twice the weight traffic
 // from L2), 4.5 ms; the pipeline with weights requested 2 or 3 steps ahead
 // instead of 1, 3.65 / 3.69 ms; LDS row padding of 32 or 64 bytes instead of 16,
-// 3.60 / 3.84 ms (none: 6.25 ms).
+// 3.60 / 3.84 ms (none: 6.25 ms); the same pipeline on v_mfma_f32_32x32x16_bf16
+// tiles, 3.71-3.79 ms against 3.62-3.65 ms: it takes 8.5% fewer cycles, but the
+// clock under load falls from 1.98 to 1.84 GHz.  This kernel runs at the power
+// limit: a loop of MFMAs alone on random bf16 operands sustains 1.94-2.04 PF/s
+// with 16x16x32 and 1.53 PF/s with 32x32x16 (2.41 / 2.44 PF/s on constant ones).
 constexpr int ffn_lds_bytes(bool bf, int D, int mb, int fc) {
   return mb * (D * (bf ? 2 : 4) + 16) + mb * (fc * (bf ? 2 : 4) + 16) + mb * (2 * 4 * 4 + 8);
 }
