@@ -24,7 +24,7 @@ struct trace_model {
   float *theta, *am, *av, *grad;
   int64_t step;
   // operand copies
-  void *Ec, *Pc;
+  void *Ec, *Pc, *XT;
   uint4 *Wq, *Wk, *Wv, *Wo, *W1, *W2, *Wout;
   // forward workspace
   float* h0;
@@ -127,6 +127,7 @@ void refresh_operands(trace_model* m, hipStream_t s) {
     launch_cvt(m->bf, th + L.off[P_P], m->Pc, L.size[P_P], s);
   else
     launch_zero(m->Pc, (L.size[P_P] * (m->bf ? 2 : 4) + 3) / 4, s);
+  launch_xtab(m->bf, m->Ec, m->Pc, L.T, m->cfg.g, m->cfg.e, m->XT, s);
   launch_pack(m->bf, th + L.off[P_WQ], D, D, m->Wq, s);
   launch_pack(m->bf, th + L.off[P_WK], D, D, m->Wk, s);
   launch_pack(m->bf, th + L.off[P_WV], D, D, m->Wv, s);
@@ -189,6 +190,7 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
   const int es = bf ? 2 : 4;
   bool ok = dalloc(m, &m->theta, n * 4) && dalloc(m, &m->am, n * 4) && dalloc(m, &m->av, n * 4) &&
             dalloc(m, &m->grad, n * 4) && dalloc(m, &m->Ec, L.size[P_E] * es) && dalloc(m, &m->Pc, L.size[P_P] * es) &&
+            dalloc(m, &m->XT, T * cfg->g * 256 * cfg->e * es) &&
             dalloc(m, &m->Wq, D * D * es) && dalloc(m, &m->Wk, D * D * es) && dalloc(m, &m->Wv, D * D * es) &&
             dalloc(m, &m->Wo, D * D * es) && dalloc(m, &m->W1, D * F * es) && dalloc(m, &m->W2, F * D * es) &&
             dalloc(m, &m->Wout, D * 256 * es) && dalloc(m, &m->h0, m->max_windows * D * 4);
@@ -297,6 +299,7 @@ extern "C" int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int6
     a.w = w;
     a.E = m->Ec;
     a.P = m->Pc;
+    a.XT = m->XT;
     a.e = m->cfg.e;
     a.g = m->cfg.g;
     a.Wq = m->Wq;

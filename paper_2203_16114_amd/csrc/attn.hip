@@ -26,29 +26,13 @@
 namespace {
 
 // Token fragment: features [d, d + EPF) of token t of a window whose bytes are
-// at wb: E[byte] + P[t] in fp32, rounded to the operand type.
+// at wb, one 16-byte load from the token-slot table (E[byte] + P[t], rounded).
 template <bool BF>
-__device__ __forceinline__ uint4 x_frag(const typename Mma<BF>::T* __restrict__ E,
-                                        const typename Mma<BF>::T* __restrict__ P, const uint8_t* wb, int t, int d,
-                                        int e, int g, int D) {
-  const int j = d / e, cc = d - j * e;
+__device__ __forceinline__ uint4 x_frag(const typename Mma<BF>::T* __restrict__ XT, const uint8_t* wb, int t, int d,
+                                        int e, int g, uint32_t einv) {
+  const int j = (int)(((uint32_t)d * einv) >> 20), cc = d - j * e;
   const int byte = wb[t * g + j];
-  if constexpr (BF) {
-    float ev[8], pv[8];
-    load8(E + byte * e + cc, ev);
-    load8(P + t * D + d, pv);
-    uint4 r;
-    r.x = pack_bf16x2(ev[0] + pv[0], ev[1] + pv[1]);
-    r.y = pack_bf16x2(ev[2] + pv[2], ev[3] + pv[3]);
-    r.z = pack_bf16x2(ev[4] + pv[4], ev[5] + pv[5]);
-    r.w = pack_bf16x2(ev[6] + pv[6], ev[7] + pv[7]);
-    return r;
-  } else {
-    const float4 ev = *reinterpret_cast<const float4*>(E + byte * e + cc);
-    const float4 pv = *reinterpret_cast<const float4*>(P + t * D + d);
-    return make_uint4(__float_as_uint(ev.x + pv.x), __float_as_uint(ev.y + pv.y), __float_as_uint(ev.z + pv.z),
-                      __float_as_uint(ev.w + pv.w));
-  }
+  return *reinterpret_cast<const uint4*>(XT + ((int64_t)(t * g + j) * 256 + byte) * e + cc);
 }
 
 __device__ __forceinline__ void put4o(uint16_t* p, const f32x4& v) {
@@ -109,17 +93,23 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
   const int W = T * a.g;
   const OT* __restrict__ E = (const OT*)a.E;
   const OT* __restrict__ P = (const OT*)a.P;
+  const OT* __restrict__ XT = (const OT*)a.XT;
 
-  for (int i = tid; i < MA * W; i += 512) {
-    const int m = i / W, j = i - m * W;
+  // window bytes to LDS: wave w takes windows w, w + 8, ... (one offset per
+  // window, on the scalar unit), lane j < W takes byte j
+  for (int m = __builtin_amdgcn_readfirstlane(wave); m < MA; m += NW) {
     const int64_t n = tile0 + m;
-    uint8_t v = 0;
-    if (n < N) {
-      v = a.w.streams[target_offset(a.w, n) - W + j];
-      if (KEEP) a.kwin[n * W + j] = v;
+    if (lane < W) {
+      uint8_t v = 0;
+      if (n < N) {
+        v = a.w.streams[target_offset(a.w, n) - W + lane];
+        if (KEEP) a.kwin[n * W + lane] = v;
+      }
+      Wb[m * 64 + lane] = v;
     }
-    Wb[m * 64 + j] = v;
   }
+  // d / e as (d * einv) >> 20: exact for d < 1024 and e < 2048
+  const uint32_t einv = ((1u << 20) + (uint32_t)a.e - 1u) / (uint32_t)a.e;
   __syncthreads();
 
   // this wave's tokens as B fragments; the last token of each window also to LDS
@@ -131,7 +121,7 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks) {
       const int d = ks * M::KS + lg * M::EPF;
-      xb[rf][ks] = x_frag<BF>(E, P, Wb + m * 64, t, d, a.e, a.g, D);
+      xb[rf][ks] = x_frag<BF>(XT, Wb + m * 64, t, d, a.e, a.g, einv);
       if (t == T - 1) *(uint4*)(Xl + m * XLSTR + ks * 64 + lg * 16) = xb[rf][ks];
     }
   }
@@ -238,7 +228,7 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
           const float mx = group_max<T>(s);
           const float p = expf(s - mx);
           const float sm = group_sum<T>(p);
-          prob[rf] = p / sm;
+          prob[rf] = p * __builtin_amdgcn_rcpf(sm);
           if (KEEP && live) {
             if (lg == 0) a.kA[(n * H + h) * T + t] = prob[rf];
 #pragma unroll
@@ -295,7 +285,7 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
         const int64_t n = tile0 + m;
         if (n < N) {
           const int d = qf * 16 + 4 * lg;
-          const int j = d / a.e, cc = d - j * a.e;
+          const int j = (int)(((uint32_t)d * einv) >> 20), cc = d - j * a.e;
           const int byte = Wb[m * 64 + (T - 1) * a.g + j];
           float4 r;
           r.x = acc[nf][0] + (M::val(E[byte * a.e + cc]) + M::val(P[(T - 1) * D + d]));

@@ -54,6 +54,33 @@ void launch_pack(bool bf, const float* W, int K, int N, void* out, hipStream_t s
     hipLaunchKernelGGL(k_pack<false>, grid, dim3(256), 0, s, W, K, N, (uint4*)out, scale);
 }
 
+// Token-slot table: every value a token feature can take, E[b] + P[t] summed in
+// fp32 from the operand copies and rounded once to the operand type, so the
+// attention block builds a token fragment with one 16-byte load.
+template <bool BF>
+__global__ void k_xtab(const typename Mma<BF>::T* __restrict__ E, const typename Mma<BF>::T* __restrict__ P, int T,
+                       int g, int e, typename Mma<BF>::T* __restrict__ XT) {
+  typedef Mma<BF> M;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int64_t total = (int64_t)T * g * 256 * e;
+  if (i >= total) return;
+  const int c = (int)(i % e);
+  const int b = (int)((i / e) % 256);
+  const int tj = (int)(i / ((int64_t)e * 256));
+  const int t = tj / g, j = tj - t * g;
+  XT[i] = M::cvt(M::val(E[b * e + c]) + M::val(P[t * (g * e) + j * e + c]));
+}
+
+void launch_xtab(bool bf, const void* E, const void* P, int T, int g, int e, void* XT, hipStream_t s) {
+  const int64_t total = (int64_t)T * g * 256 * e;
+  const dim3 grid((unsigned)((total + 255) / 256));
+  if (bf)
+    hipLaunchKernelGGL(k_xtab<true>, grid, dim3(256), 0, s, (const uint16_t*)E, (const uint16_t*)P, T, g, e,
+                       (uint16_t*)XT);
+  else
+    hipLaunchKernelGGL(k_xtab<false>, grid, dim3(256), 0, s, (const float*)E, (const float*)P, T, g, e, (float*)XT);
+}
+
 template <bool BF>
 __global__ void k_cvt(const float* __restrict__ src, typename Mma<BF>::T* __restrict__ dst, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;

@@ -148,25 +148,33 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float lo, float hi) {
 // Cross-lane reductions on the DPP path (no LDS traffic).  Within aligned
 // groups of 4 lanes: quad permutations xor 1 and xor 2; groups of 8 add the
 // mirrored half-row (lane i <-> 7 - i), which pairs each quad with the other.
-template <int CTRL>
-__device__ __forceinline__ float dpp_f(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
-}
-constexpr int DPP_XOR1 = 0xB1;          // quad_perm [1,0,3,2]
-constexpr int DPP_XOR2 = 0x4E;          // quad_perm [2,3,0,1]
-constexpr int DPP_HALF_MIRROR = 0x141;  // row_half_mirror
+// Each step is one VALU instruction with the DPP operand (v op v[perm]); the
+// s_nop gives the two wait states a DPP read needs after a VALU write of its
+// source.  (The builtin form leaves a separate DPP move and, for the maximum,
+// two canonicalising operations per step.)
+#define TRACE_DPP_STEP(NAME, OP, CTRL)                                                                   \
+  __device__ __forceinline__ float NAME(float v) {                                                     \
+    float r;                                                                                           \
+    asm("s_nop 1\n\t" OP " %0, %1, %1 " CTRL " row_mask:0xf bank_mask:0xf" : "=v"(r) : "v"(v));        \
+    return r;                                                                                          \
+  }
+TRACE_DPP_STEP(dpp_add_x1, "v_add_f32_dpp", "quad_perm:[1,0,3,2]")
+TRACE_DPP_STEP(dpp_add_x2, "v_add_f32_dpp", "quad_perm:[2,3,0,1]")
+TRACE_DPP_STEP(dpp_add_hm, "v_add_f32_dpp", "row_half_mirror")
+TRACE_DPP_STEP(dpp_max_x1, "v_max_f32_dpp", "quad_perm:[1,0,3,2]")
+TRACE_DPP_STEP(dpp_max_x2, "v_max_f32_dpp", "quad_perm:[2,3,0,1]")
+TRACE_DPP_STEP(dpp_max_hm, "v_max_f32_dpp", "row_half_mirror")
+#undef TRACE_DPP_STEP
 template <int G>  // G = 4 or 8 lanes
 __device__ __forceinline__ float group_sum(float v) {
-  v += dpp_f<DPP_XOR1>(v);
-  v += dpp_f<DPP_XOR2>(v);
-  if constexpr (G == 8) v += dpp_f<DPP_HALF_MIRROR>(v);
+  v = dpp_add_x2(dpp_add_x1(v));
+  if constexpr (G == 8) v = dpp_add_hm(v);
   return v;
 }
 template <int G>
 __device__ __forceinline__ float group_max(float v) {
-  v = fmaxf(v, dpp_f<DPP_XOR1>(v));
-  v = fmaxf(v, dpp_f<DPP_XOR2>(v));
-  if constexpr (G == 8) v = fmaxf(v, dpp_f<DPP_HALF_MIRROR>(v));
+  v = dpp_max_x2(dpp_max_x1(v));
+  if constexpr (G == 8) v = dpp_max_hm(v);
   return v;
 }
 

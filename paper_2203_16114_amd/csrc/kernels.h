@@ -17,6 +17,7 @@ struct AttnArgs {
   WinArgs w;
   const void* E;  // operand copy [256][e]
   const void* P;  // operand copy [T][D] (zeros when the positional table is off)
+  const void* XT; // operand copy [T][g][256][e]: token slot (t, j) of byte b = E[b] + P[t][j*e ..], rounded
   int32_t e, g;
   const uint4 *Wq, *Wk, *Wv, *Wo;  // packed operand copies
   float* h0;                       // [N][D]: Attn + X, the residual stream entering the FFN
@@ -55,6 +56,8 @@ void launch_pack(bool bf, const float* W, int K, int N, void* out, hipStream_t s
 void launch_zero(void* p, int64_t n32, hipStream_t s);
 void launch_cvt(bool bf, const float* src, void* dst, int64_t n, hipStream_t s);
 void launch_step_ce(const float* bits, int32_t n_streams, int32_t n_steps, double* out, hipStream_t s);
+// XT[t][j][b][c] = operand(E[b][c] + P[t][j*e + c]) for the T x g token slots
+void launch_xtab(bool bf, const void* E, const void* P, int T, int g, int e, void* XT, hipStream_t s);
 void launch_gather(bool bf, const WinArgs& w, const void* E, const void* P, int T, int D, int e, int g, float* X,
                    hipStream_t s);
 
