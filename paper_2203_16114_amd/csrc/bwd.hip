@@ -321,8 +321,16 @@ static void launch128(const GemmArgs& g, float* part, int kchunk, dim3 grid, hip
     hipLaunchKernelGGL((k_gemm128<MODE, false, false>), grid, dim3(256), 0, s, g, part, kchunk);
 }
 
-void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s) {
+void launch_splitk_reduce(const float* ws, int splits, int M, int N, float* C, int64_t ldc, float beta, hipStream_t s) {
+  const int64_t tot = (int64_t)M * N;
+  hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, ws, splits, M, N, C, ldc,
+                     beta);
+}
+
+void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, void* prep, int64_t prep_cap, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return;
+  // bf16 storage points on at least one side: prepared-operand bf16 GEMM
+  if (launch_bgemm(g, ws, ws_cap, prep, prep_cap, s)) return;
   int splits = gemm_splits(g.M, g.N, g.K);
   while (splits > 1 && (int64_t)splits * g.M * g.N > ws_cap) splits /= 2;
   int kchunk = (g.K + splits - 1) / splits;
@@ -348,11 +356,7 @@ void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s) {
     else
       hipLaunchKernelGGL(k_gemm<false>, grid, dim3(256), 0, s, g, part, kchunk);
   }
-  if (splits > 1) {
-    const int64_t tot = (int64_t)g.M * g.N;
-    hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, ws, splits, g.M, g.N,
-                       g.C, g.ldc, g.beta);
-  }
+  if (splits > 1) launch_splitk_reduce(ws, splits, g.M, g.N, g.C, g.ldc, g.beta, s);
 }
 
 // ------------------------------------------------------------- column sums ----
