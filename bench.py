@@ -252,7 +252,8 @@ def main():
     achieved = fpw[dom] * wpl / (per[dom] * 1e-3) / 1e12
     peak = PEAK_TFLOPS[w.dtype]
     total_tflops = (fpw["attn"] + fpw["ffn_head"]) * value / 1e12
-    kname = "k_ffn_head" if dom == "ffn_head" else "k_attn"
+    # the FFN + head kernel is k_ffn_pipe in bf16, k_ffn_head in fp32
+    kname = ("k_ffn_pipe" if w.dtype == "bf16" else "k_ffn_head") if dom == "ffn_head" else "k_attn"
     traffic = traffic_for(kname, wpl)
     roofline = {"bound": "mfma", "kernel": kname,
                 "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),

@@ -535,7 +535,8 @@ __global__ __launch_bounds__(256) void k_embed_bwd_part(const uint8_t* __restric
   __syncthreads();
   const int64_t p0 = (int64_t)blockIdx.x * chunk;
   const int64_t p1 = min(total, p0 + chunk);
-  const int T = W / g;
+  // the W token slots of a window are W consecutive e-vectors of dX (D = g*e),
+  // so position q = n*W + t*g + j reads row q of dX viewed as [N*W][e]
   if (grp < NG) {
     float* my = tab + grp * 256 * e;
     int64_t i = p0 + grp;
@@ -546,21 +547,13 @@ __global__ __launch_bounds__(256) void k_embed_bwd_part(const uint8_t* __restric
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
         const int64_t q = i + u * NG;
-        const int64_t n = q / W;
-        const int pp = (int)(q - n * W);
-        const int t = pp / g, j = pp - t * g;
         v[u] = win[q];
-        x[u] = dX[(n * T + t) * D + j * e + c];
+        x[u] = dX[q * e + c];
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) my[v[u] * e + c] += x[u];
     }
-    for (; i < p1; i += NG) {
-      const int64_t n = i / W;
-      const int pp = (int)(i - n * W);
-      const int t = pp / g, j = pp - t * g;
-      my[win[i] * e + c] += dX[(n * T + t) * D + j * e + c];
-    }
+    for (; i < p1; i += NG) my[win[i] * e + c] += dX[i * e + c];
   }
   __syncthreads();
   for (int k = tid; k < 256 * e; k += 256) {
