@@ -155,9 +155,10 @@ int trace_set_state(trace_model* m, const float* theta, const float* adam_m, con
  * copied to a host array of trace_param_count floats; synchronises. */
 int trace_get_grads(trace_model* m, float* host_out, int64_t n);
 
-/* Byte-group gather alone (Sec. 4.2): writes the operand values of the
- * tokens, d_X[((b*n_steps + s)*T + t)*d + c] (device, fp32; in BF16 mode the
- * bf16-rounded value), for the windows defined as in trace_forward_bits. */
+/* Byte-group gather alone (Sec. 4.2): writes the tokens X = E[byte] + P[t],
+ * d_X[((b*n_steps + s)*T + t)*d + c] (device, fp32: the sum of the operand
+ * copies of E and P, not rounded), for the windows defined as in
+ * trace_forward_bits. */
 int trace_debug_gather(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams, int64_t pos0,
                        int32_t n_steps, float* d_X, void* stream);
 

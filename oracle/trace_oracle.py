@@ -182,8 +182,11 @@ class _Mode:
 
 
 # bf16 storage points (all else fp32): the weight copies E,P,Wq,Wk,Wv,Wo,W1,W2,
-# Wout; the GEMM operands X, O, Y_{r-1} (into W1), GELU(U_r) (into W2), Y_k
-# (into the head); in the backward dz, dY, dU, dO.
+# Wout; the GEMM operands O, Y_{r-1} (into W1), GELU(U_r) (into W2), Y_k (into
+# the head); in the backward dz, dY, dU, dO.  The token X = E[byte] + P[t] is
+# not one: it is the fp32 sum of two rounded copies, and the projections take it
+# as it is (X.W = E.W + P.W exactly, which lets the projection of a byte group be
+# shared by every window that holds it).
 _WEIGHTS_ROUNDED = ("E", "P", "Wq", "Wk", "Wv", "Wo", "W1", "W2", "Wout")
 
 
@@ -272,7 +275,7 @@ def forward(flat: np.ndarray, cfg: Config, windows: np.ndarray, targets: np.ndar
     N, T, d, H, dh = windows.shape[0], cfg.T, cfg.d, cfg.H, cfg.dh
 
     X = embed_group(p, windows, cfg, m)                 # residual copy
-    Xo = m.R(X)                                         # GEMM operand
+    Xo = X                                              # GEMM operand (fp32, not rounded)
     Q = Xo @ p["Wq"]
     K = Xo @ p["Wk"]
     V = Xo @ p["Wv"]

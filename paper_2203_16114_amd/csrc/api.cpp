@@ -25,7 +25,8 @@ struct trace_model {
   float *theta, *am, *av, *grad;
   int64_t step;
   // operand copies
-  void *Ec, *Pc, *XT;
+  void *Ec, *Pc;
+  float* PW;  // [3][T][D] positional parts of the q, k, v projections
   uint4 *Wq, *Wk, *Wv, *Wo, *W1, *W2, *Wout;
   // forward workspace
   float* h0;
@@ -36,7 +37,7 @@ struct trace_model {
   int32_t* ktgt;
   float *kq, *kK, *kV, *kA, *kO, *kY, *kU, *kZ;
   // backward scratch
-  float *dz, *dY, *dG, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *gws, *cws, *ews;
+  float *dz, *dY, *dG, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *sP, *gws, *cws, *ews;
   int64_t gws_cap;
   void* pws;  // bf16 operand copies of the update GEMMs
   int64_t pws_cap;
@@ -140,7 +141,7 @@ void refresh_operands(trace_model* m, hipStream_t s) {
     launch_cvt(m->bf, th + L.off[P_P], m->Pc, L.size[P_P], s);
   else
     launch_zero(m->Pc, (L.size[P_P] * (m->bf ? 2 : 4) + 3) / 4, s);
-  launch_xtab(m->bf, m->Ec, m->Pc, L.T, m->cfg.g, m->cfg.e, m->XT, s);
+  launch_ptab(m->bf, m->Pc, th + L.off[P_WQ], th + L.off[P_WK], th + L.off[P_WV], L.T, D, m->PW, s);
   launch_pack(m->bf, th + L.off[P_WQ], D, D, m->Wq, s);
   launch_pack(m->bf, th + L.off[P_WK], D, D, m->Wk, s);
   launch_pack(m->bf, th + L.off[P_WV], D, D, m->Wv, s);
@@ -203,7 +204,7 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
   const int es = bf ? 2 : 4;
   bool ok = dalloc(m, &m->theta, n * 4) && dalloc(m, &m->am, n * 4) && dalloc(m, &m->av, n * 4) &&
             dalloc(m, &m->grad, n * 4) && dalloc(m, &m->Ec, L.size[P_E] * es) && dalloc(m, &m->Pc, L.size[P_P] * es) &&
-            dalloc(m, &m->XT, T * cfg->g * 256 * cfg->e * es) &&
+            dalloc(m, &m->PW, 3 * T * D * 4) &&
             dalloc(m, &m->Wq, D * D * es) && dalloc(m, &m->Wk, D * D * es) && dalloc(m, &m->Wv, D * D * es) &&
             dalloc(m, &m->Wo, D * D * es) && dalloc(m, &m->W1, D * F * es) && dalloc(m, &m->W2, F * D * es) &&
             dalloc(m, &m->Wout, D * 256 * es) && dalloc(m, &m->h0, m->max_windows * D * 4);
@@ -217,6 +218,7 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
          dalloc(m, &m->dG, K * F * 4) && dalloc(m, &m->dU, K * F * 4) && dalloc(m, &m->G, K * F * 4) &&
          dalloc(m, &m->dO, K * D * 4) && dalloc(m, &m->dQ, K * D * 4) && dalloc(m, &m->dK, K * T * D * 4) &&
          dalloc(m, &m->dV, K * T * D * 4) && dalloc(m, &m->dX, K * T * D * 4) && dalloc(m, &m->Xk, K * T * D * 4) &&
+         dalloc(m, &m->sP, T * D * 4) &&
          dalloc(m, &m->gws, (m->gws_cap = adapt_gemm_ws(m, K)) * 4) &&
          (!bf || dalloc(m, &m->pws, (m->pws_cap = adapt_prep_bytes(m, K)))) &&
          dalloc(m, &m->ews, embed_bwd_ws_floats(K * W, cfg->e) * 4) &&
@@ -313,7 +315,7 @@ extern "C" int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int6
     a.w = w;
     a.E = m->Ec;
     a.P = m->Pc;
-    a.XT = m->XT;
+    a.PW = m->PW;
     a.e = m->cfg.e;
     a.g = m->cfg.g;
     a.Wq = m->Wq;
@@ -403,13 +405,23 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // attention (last query row) -> dQ, dK, dV
   launch_attn_bwd(m->dO, m->kq, m->kK, m->kV, m->kA, N, T, D, H, (float)(1.0 / std::sqrt((double)L.DH)), rb, m->dQ,
                   m->dK, m->dV, s);
-  // projections: dWq = X_last^T dQ, dWk = X^T dK, dWv = X^T dV  (dQ, dK, dV stay fp32)
-  launch_gather_kept(m->bf, m->kwin, N, m->Ec, m->Pc, T, D, m->cfg.e, m->cfg.g, m->Xk, s);
+  // projections: dWq = X_last^T dQ, dWk = X^T dK, dWv = X^T dV  (dQ, dK, dV stay fp32),
+  // with X = G + P[t]: G^T dZ as GEMMs on the byte-embedding part G, then
+  // P^T (sum over windows of dZ) for the positional part
+  launch_gather_kept(m->bf, m->kwin, N, m->Ec, T, D, m->cfg.e, m->cfg.g, m->Xk, s);
   launch_gemm(gemm(D, D, N, m->Xk + (int64_t)(T - 1) * D, 1, (int64_t)T * D, rb, m->dQ, D, 1, 0, gr + L.off[P_WQ], D,
                    0.f),
               ws, m->gws_cap, m->pws, m->pws_cap, s);
   launch_gemm(gemm(D, D, N * T, m->Xk, 1, D, rb, m->dK, D, 1, 0, gr + L.off[P_WK], D, 0.f), ws, m->gws_cap, m->pws, m->pws_cap, s);
   launch_gemm(gemm(D, D, N * T, m->Xk, 1, D, rb, m->dV, D, 1, 0, gr + L.off[P_WV], D, 0.f), ws, m->gws_cap, m->pws, m->pws_cap, s);
+  if (m->cfg.use_pos) {
+    launch_colsum(m->dQ, N, D, D, m->sP, 0.f, m->cws, s);
+    launch_pos_grad(m->bf, m->Pc, m->sP, T - 1, 1, D, gr + L.off[P_WQ], s);
+    launch_colsum(m->dK, N, (int64_t)T * D, (int64_t)T * D, m->sP, 0.f, m->cws, s);
+    launch_pos_grad(m->bf, m->Pc, m->sP, 0, T, D, gr + L.off[P_WK], s);
+    launch_colsum(m->dV, N, (int64_t)T * D, (int64_t)T * D, m->sP, 0.f, m->cws, s);
+    launch_pos_grad(m->bf, m->Pc, m->sP, 0, T, D, gr + L.off[P_WV], s);
+  }
   // dX = dK Wk^T + dV Wv^T (+ dQ Wq^T + dY0 on the last token)
   launch_gemm(gemm(N * T, D, D, m->dK, D, 1, 0, th + L.off[P_WK], 1, D, rb, m->dX, D, 0.f), ws, m->gws_cap, m->pws, m->pws_cap, s);
   launch_gemm(gemm(N * T, D, D, m->dV, D, 1, 0, th + L.off[P_WV], 1, D, rb, m->dX, D, 1.f), ws, m->gws_cap, m->pws, m->pws_cap, s);

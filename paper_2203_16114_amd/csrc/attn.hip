@@ -3,12 +3,13 @@
 // Eq. 4, fused: window bytes -> h0 = O.Wo + X_last.
 //
 // One workgroup of 8 waves per tile of MA windows.  Wave w owns RFW*16
-// consecutive token rows (whole windows).  Its tokens X, built from the
-// embedding table and the positional table, stay in registers for the whole
-// kernel as MFMA B-operand fragments (8 consecutive features per lane).
+// consecutive token rows (whole windows).  The byte-embedding part of its
+// tokens stays in registers for the whole kernel as MFMA B-operand fragments
+// (8 consecutive features per lane); the positional part enters every
+// projection as a precomputed row of P.W (X.W = E.W + P.W, X = E + P in fp32).
 // Every product is formed transposed (weights as the A operand), so a lane's
 // four results are four consecutive features of one token:
-//   q^T   = Wq^T . X_last^T                 (waves split the features)   -> LDS
+//   q^T   = Wq^T . E_last^T + (P.Wq)[T-1]   (waves split the features)   -> LDS
 //   per head h:  K_h^T = Wk_h^T . X^T, then V_h^T = Wv_h^T . X^T; the head's
 //                weight fragments are staged through LDS in double-buffered
 //                chunks shared by all 8 waves, moved by direct global-to-LDS
@@ -25,14 +26,15 @@
 
 namespace {
 
-// Token fragment: features [d, d + EPF) of token t of a window whose bytes are
-// at wb, one 16-byte load from the token-slot table (E[byte] + P[t], rounded).
+// E-part of a token fragment: features [d, d + EPF) of token t of a window
+// whose bytes are at wb, one 16-byte load from the byte embedding (the
+// positional part enters the projections through the table P.W).
 template <bool BF>
-__device__ __forceinline__ uint4 x_frag(const typename Mma<BF>::T* __restrict__ XT, const uint8_t* wb, int t, int d,
+__device__ __forceinline__ uint4 x_frag(const typename Mma<BF>::T* __restrict__ E, const uint8_t* wb, int t, int d,
                                         int e, int g, uint32_t einv) {
   const int j = (int)(((uint32_t)d * einv) >> 20), cc = d - j * e;
   const int byte = wb[t * g + j];
-  return *reinterpret_cast<const uint4*>(XT + ((int64_t)(t * g + j) * 256 + byte) * e + cc);
+  return *reinterpret_cast<const uint4*>(E + byte * e + cc);
 }
 
 __device__ __forceinline__ void put4o(uint16_t* p, const f32x4& v) {
@@ -46,7 +48,7 @@ __device__ __forceinline__ f32x4 rounded4(const f32x4& v, bool bf) {
   return f32x4{round_bf(v[0]), round_bf(v[1]), round_bf(v[2]), round_bf(v[3])};
 }
 
-template <bool BF, int T, int D, int DH>
+template <bool BF, int T, int D, int DH, bool SMALL = false>
 struct AttnShape {
   typedef typename Mma<BF>::T OT;
   static constexpr int NW = 8;
@@ -63,7 +65,7 @@ struct AttnShape {
   // SIMD and whose tile fits the LDS
   static constexpr int vgprs(int rfw) { return rfw * KSTEPS * 4 + rfw * NFH * 4 + NFH * 4 + 8; }
   static constexpr bool fits(int rfw) { return vgprs(rfw) <= 184 && lds(rfw) <= 160 * 1024; }
-  static constexpr int RFW = (KSTEPS <= 8 && fits(4)) ? 4 : (fits(2) ? 2 : 1);
+  static constexpr int RFW = SMALL ? 1 : (KSTEPS <= 8 && fits(4)) ? 4 : (fits(2) ? 2 : 1);
   static constexpr int RW = RFW * 16;
   static constexpr int MA = NW * RW / T;
   static constexpr int LDS = lds(RFW);
@@ -71,11 +73,11 @@ struct AttnShape {
 
 }  // namespace
 
-template <bool BF, int T, int D, int DH, bool KEEP>
+template <bool BF, int T, int D, int DH, bool KEEP, bool SMALL>
 __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
   typedef Mma<BF> M;
   typedef typename M::T OT;
-  typedef AttnShape<BF, T, D, DH> S;
+  typedef AttnShape<BF, T, D, DH, SMALL> S;
   constexpr int H = D / DH;
   constexpr int NW = S::NW, KSTEPS = S::KSTEPS, NFH = S::NFH, KSC = S::KSC, CPP = KSTEPS / KSC, CHUNK = S::CHUNK;
   constexpr int RFW = S::RFW, RW = S::RW, MA = S::MA, XLSTR = S::XLSTR;
@@ -93,7 +95,9 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
   const int W = T * a.g;
   const OT* __restrict__ E = (const OT*)a.E;
   const OT* __restrict__ P = (const OT*)a.P;
-  const OT* __restrict__ XT = (const OT*)a.XT;
+  const float* __restrict__ PQ = a.PW;  // [T][D] each: P.Wq, P.Wk, P.Wv
+  const float* __restrict__ PK = a.PW + (int64_t)T * D;
+  const float* __restrict__ PV = a.PW + (int64_t)2 * T * D;
 
   // window bytes to LDS: wave w takes windows w, w + 8, ... (one offset per
   // window, on the scalar unit), lane j < W takes byte j
@@ -121,7 +125,7 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks) {
       const int d = ks * M::KS + lg * M::EPF;
-      xb[rf][ks] = x_frag<BF>(XT, Wb + m * 64, t, d, a.e, a.g, einv);
+      xb[rf][ks] = x_frag<BF>(E, Wb + m * 64, t, d, a.e, a.g, einv);
       if (t == T - 1) *(uint4*)(Xl + m * XLSTR + ks * 64 + lg * 16) = xb[rf][ks];
     }
   }
@@ -146,10 +150,15 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
           M::run(acc[nf], wq[ks & 1], bx);
         }
       }
+      const float4 pq = *reinterpret_cast<const float4*>(PQ + (T - 1) * D + qf * 16 + 4 * lg);
 #pragma unroll
       for (int nf = 0; nf < NMF; ++nf) {
         const int m = nf * 16 + lc;
         const int c = qf * 16 + 4 * lg;
+        acc[nf][0] += pq.x;
+        acc[nf][1] += pq.y;
+        acc[nf][2] += pq.z;
+        acc[nf][3] += pq.w;
         *reinterpret_cast<float4*>(Qs + m * D + c) = make_float4(acc[nf][0], acc[nf][1], acc[nf][2], acc[nf][3]);
         if (KEEP && tile0 + m < N)
           *reinterpret_cast<float4*>(a.kq + (tile0 + m) * D + c) =
@@ -215,6 +224,16 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
         const int m = row / T, t = row - m * T;
         const int64_t n = tile0 + m;
         const bool live = n < N;
+        // positional part of the token's projection
+        const float* pp = (pass == 0 ? PK : PV) + t * D + h * DH + 4 * lg;
+#pragma unroll
+        for (int f = 0; f < NFH; ++f) {
+          const float4 p4 = *reinterpret_cast<const float4*>(pp + f * 16);
+          acc[rf][f][0] += p4.x;
+          acc[rf][f][1] += p4.y;
+          acc[rf][f][2] += p4.z;
+          acc[rf][f][3] += p4.w;
+        }
         if (pass == 0) {
           float s = 0.f;
 #pragma unroll
@@ -303,15 +322,25 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
 // Measured alternative, slower on the main workload (2^20 windows): two
 // accumulator sets so that the scores of head h run under the MFMAs of its V
 // pass and its weighted sum under those of the next K pass: 3.4 ms against 3.2.
-template <bool BF, int T, int D, int DH>
-static void run_attn(const AttnArgs& a, hipStream_t s) {
-  typedef AttnShape<BF, T, D, DH> S;
+template <bool BF, int T, int D, int DH, bool SMALL>
+static void launch_attn(const AttnArgs& a, hipStream_t s) {
+  typedef AttnShape<BF, T, D, DH, SMALL> S;
   static_assert(S::LDS <= 160 * 1024, "LDS");
   const dim3 grid((unsigned)((a.w.N + S::MA - 1) / S::MA));
   if (a.kK)
-    hipLaunchKernelGGL((k_attn<BF, T, D, DH, true>), grid, dim3(512), 0, s, a);
+    hipLaunchKernelGGL((k_attn<BF, T, D, DH, true, SMALL>), grid, dim3(512), 0, s, a);
   else
-    hipLaunchKernelGGL((k_attn<BF, T, D, DH, false>), grid, dim3(512), 0, s, a);
+    hipLaunchKernelGGL((k_attn<BF, T, D, DH, false, SMALL>), grid, dim3(512), 0, s, a);
+}
+
+// Launches too small to give every CU a workgroup at the widest tile (one step
+// of the update path) take one 16-row fragment per wave.
+template <bool BF, int T, int D, int DH>
+static void run_attn(const AttnArgs& a, hipStream_t s) {
+  if (a.w.N >= (int64_t)256 * AttnShape<BF, T, D, DH>::MA || AttnShape<BF, T, D, DH>::RFW == 1)
+    launch_attn<BF, T, D, DH, false>(a, s);
+  else
+    launch_attn<BF, T, D, DH, true>(a, s);
 }
 
 attn_fn find_attn(bool bf, int T, int D, int DH) {

@@ -197,6 +197,7 @@ int bgemm_splits(int M, int N, int Kp) {
   const int tiles = (int)(rup(M, BM) / BM * (rup(N, BN) / BN));
   int splits = 1;
   // fill the 256 CUs about twice, each split keeping at least 512 k values
+  // (shorter splits measured slower: the partial sums cost more than they fill)
   while (tiles * splits < 512 && Kp / (splits * 2) >= 512) splits *= 2;
   return splits;
 }

@@ -576,11 +576,12 @@ void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int
   launch_colsum(ws, G, 256 * e, 256 * e, dE, 0.f, cws, s);
 }
 
-// token operand values of the kept windows: X[n][t][c] (fp32 value of the operand)
+// byte-embedding part of the kept tokens: G[n][t][c] = E[byte][c % e] (the
+// operand value).  The token is X = G + P[t]; the weight gradients X^T.dZ are
+// formed as G^T.dZ (a GEMM) plus P^T.(sum over windows of dZ) (k_pos_grad).
 template <bool BF>
 __global__ void k_gather_kept(const uint8_t* __restrict__ win, int64_t N, const typename Mma<BF>::T* __restrict__ E,
-                              const typename Mma<BF>::T* __restrict__ P, int T, int D, int e, int g,
-                              float* __restrict__ X) {
+                              int T, int D, int e, int g, float* __restrict__ X) {
   typedef Mma<BF> M;
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= N * T * D) return;
@@ -590,17 +591,38 @@ __global__ void k_gather_kept(const uint8_t* __restrict__ win, int64_t N, const 
   const int64_t n = rr / T;
   const int j = c / e, cc = c - j * e;
   const int byte = win[n * (T * g) + t * g + j];
-  X[i] = M::val(M::cvt(M::val(E[byte * e + cc]) + M::val(P[t * D + c])));
+  X[i] = M::val(E[byte * e + cc]);
 }
-void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, const void* P, int T, int D, int e,
-                        int g, float* X, hipStream_t s) {
+void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, int T, int D, int e, int g, float* X,
+                        hipStream_t s) {
   const dim3 grid((unsigned)((N * T * D + 255) / 256));
   if (bf)
-    hipLaunchKernelGGL(k_gather_kept<true>, grid, dim3(256), 0, s, win, N, (const uint16_t*)E, (const uint16_t*)P, T,
-                       D, e, g, X);
+    hipLaunchKernelGGL(k_gather_kept<true>, grid, dim3(256), 0, s, win, N, (const uint16_t*)E, T, D, e, g, X);
   else
-    hipLaunchKernelGGL(k_gather_kept<false>, grid, dim3(256), 0, s, win, N, (const float*)E, (const float*)P, T, D, e,
-                       g, X);
+    hipLaunchKernelGGL(k_gather_kept<false>, grid, dim3(256), 0, s, win, N, (const float*)E, T, D, e, g, X);
+}
+
+// Positional part of a projection's weight gradient:
+// dW[i][j] += sum_{u < nt} P[t0 + u][i] * S[u][j], with S[u] = sum over windows
+// of dZ at token t0 + u (column sums, formed beforehand in a fixed order); the
+// sum over u runs in increasing order.
+template <bool BF>
+__global__ void k_pos_grad(const typename Mma<BF>::T* __restrict__ P, const float* __restrict__ S, int t0, int nt,
+                           int D, float* __restrict__ dW) {
+  typedef Mma<BF> M;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)D * D) return;
+  const int r = (int)(i / D), c = (int)(i % D);
+  float acc = 0.f;
+  for (int u = 0; u < nt; ++u) acc += M::val(P[(t0 + u) * D + r]) * S[u * D + c];
+  dW[i] += acc;
+}
+void launch_pos_grad(bool bf, const void* P, const float* S, int t0, int nt, int D, float* dW, hipStream_t s) {
+  const dim3 grid((unsigned)(((int64_t)D * D + 255) / 256));
+  if (bf)
+    hipLaunchKernelGGL(k_pos_grad<true>, grid, dim3(256), 0, s, (const uint16_t*)P, S, t0, nt, D, dW);
+  else
+    hipLaunchKernelGGL(k_pos_grad<false>, grid, dim3(256), 0, s, (const float*)P, S, t0, nt, D, dW);
 }
 
 // -------------------------------------------------------------------- Adam ----

@@ -560,16 +560,26 @@ constexpr int pick_fc(bool bf, int D) { return ffn_lds_bytes(bf, D, pick_mb(bf, 
 template <int D>
 constexpr int pick_mb_pipe() { return FfnPipe<D, 128>::LDS <= 160 * 1024 ? 128 : 64; }
 
+template <int D, int MB>
+static void launch_pipe(const FfnArgs& a, hipStream_t s) {
+  static_assert(FfnPipe<D, MB>::LDS <= 160 * 1024, "LDS");
+  const dim3 grid((unsigned)((a.w.N + MB - 1) / MB));
+  if (a.kY)
+    hipLaunchKernelGGL((k_ffn_pipe<D, MB, true>), grid, dim3(512), 0, s, a);
+  else
+    hipLaunchKernelGGL((k_ffn_pipe<D, MB, false>), grid, dim3(512), 0, s, a);
+}
+
 template <bool BF, int D>
 static void run_ffn(const FfnArgs& a, hipStream_t s) {
   if constexpr (BF) {
+    // the widest window tile that still gives every CU a workgroup; launches of
+    // a few thousand windows (one step of the update path) take 32-window tiles
     constexpr int MB = pick_mb_pipe<D>();
-    static_assert(FfnPipe<D, MB>::LDS <= 160 * 1024, "LDS");
-    const dim3 grid((unsigned)((a.w.N + MB - 1) / MB));
-    if (a.kY)
-      hipLaunchKernelGGL((k_ffn_pipe<D, MB, true>), grid, dim3(512), 0, s, a);
+    if (a.w.N >= (int64_t)256 * MB)
+      launch_pipe<D, MB>(a, s);
     else
-      hipLaunchKernelGGL((k_ffn_pipe<D, MB, false>), grid, dim3(512), 0, s, a);
+      launch_pipe<D, 32>(a, s);
   } else {
     constexpr int MB = pick_mb(BF, D), FC = pick_fc(BF, D);
     static_assert(ffn_lds_bytes(BF, D, MB, FC) <= 160 * 1024, "LDS");

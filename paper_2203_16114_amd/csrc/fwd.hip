@@ -54,31 +54,32 @@ void launch_pack(bool bf, const float* W, int K, int N, void* out, hipStream_t s
     hipLaunchKernelGGL(k_pack<false>, grid, dim3(256), 0, s, W, K, N, (uint4*)out, scale);
 }
 
-// Token-slot table: every value a token feature can take, E[b] + P[t] summed in
-// fp32 from the operand copies and rounded once to the operand type, so the
-// attention block builds a token fragment with one 16-byte load.
+// Positional parts of the projections: PW[w][t][j] = sum_i P[t][i] W_w[i][j] for
+// w = q, k, v, in fp32 over i in increasing order, from the operand values of P
+// and of the weights (bf16-rounded in BF16 mode).  A token's projection is then
+// E-part (an MFMA on the rounded byte embeddings) + PW[w][t]: X.W = E.W + P.W.
 template <bool BF>
-__global__ void k_xtab(const typename Mma<BF>::T* __restrict__ E, const typename Mma<BF>::T* __restrict__ P, int T,
-                       int g, int e, typename Mma<BF>::T* __restrict__ XT) {
+__global__ void k_ptab(const typename Mma<BF>::T* __restrict__ P, const float* __restrict__ Wq,
+                       const float* __restrict__ Wk, const float* __restrict__ Wv, int T, int D,
+                       float* __restrict__ PW) {
   typedef Mma<BF> M;
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t total = (int64_t)T * g * 256 * e;
-  if (i >= total) return;
-  const int c = (int)(i % e);
-  const int b = (int)((i / e) % 256);
-  const int tj = (int)(i / ((int64_t)e * 256));
-  const int t = tj / g, j = tj - t * g;
-  XT[i] = M::cvt(M::val(E[b * e + c]) + M::val(P[t * (g * e) + j * e + c]));
+  if (i >= (int64_t)3 * T * D) return;
+  const int j = (int)(i % D), t = (int)((i / D) % T), w = (int)(i / ((int64_t)T * D));
+  const float* Wm = w == 0 ? Wq : (w == 1 ? Wk : Wv);
+  float s = 0.f;
+  for (int k = 0; k < D; ++k) s = fmaf(M::val(P[t * D + k]), M::val(M::cvt(Wm[(int64_t)k * D + j])), s);
+  PW[i] = s;
 }
 
-void launch_xtab(bool bf, const void* E, const void* P, int T, int g, int e, void* XT, hipStream_t s) {
-  const int64_t total = (int64_t)T * g * 256 * e;
+void launch_ptab(bool bf, const void* P, const float* Wq, const float* Wk, const float* Wv, int T, int D, float* PW,
+                 hipStream_t s) {
+  const int64_t total = (int64_t)3 * T * D;
   const dim3 grid((unsigned)((total + 255) / 256));
   if (bf)
-    hipLaunchKernelGGL(k_xtab<true>, grid, dim3(256), 0, s, (const uint16_t*)E, (const uint16_t*)P, T, g, e,
-                       (uint16_t*)XT);
+    hipLaunchKernelGGL(k_ptab<true>, grid, dim3(256), 0, s, (const uint16_t*)P, Wq, Wk, Wv, T, D, PW);
   else
-    hipLaunchKernelGGL(k_xtab<false>, grid, dim3(256), 0, s, (const float*)E, (const float*)P, T, g, e, (float*)XT);
+    hipLaunchKernelGGL(k_ptab<false>, grid, dim3(256), 0, s, (const float*)P, Wq, Wk, Wv, T, D, PW);
 }
 
 template <bool BF>
@@ -122,8 +123,7 @@ __global__ void k_gather(WinArgs w, const typename Mma<BF>::T* __restrict__ E, c
   const int j = c / e, cc = c - j * e;
   const int W = T * g;
   const int byte = w.streams[target_offset(w, n) - W + t * g + j];
-  const float x = M::val(E[byte * e + cc]) + M::val(P[t * D + c]);
-  X[i] = M::val(M::cvt(x));
+  X[i] = M::val(E[byte * e + cc]) + M::val(P[t * D + c]);
 }
 void launch_gather(bool bf, const WinArgs& w, const void* E, const void* P, int T, int D, int e, int g, float* X,
                    hipStream_t s) {

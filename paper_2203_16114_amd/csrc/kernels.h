@@ -17,7 +17,7 @@ struct AttnArgs {
   WinArgs w;
   const void* E;  // operand copy [256][e]
   const void* P;  // operand copy [T][D] (zeros when the positional table is off)
-  const void* XT; // operand copy [T][g][256][e]: token slot (t, j) of byte b = E[b] + P[t][j*e ..], rounded
+  const float* PW; // [3][T][D]: P.Wq, P.Wk, P.Wv (fp32), the positional parts of the projections
   int32_t e, g;
   const uint4 *Wq, *Wk, *Wv, *Wo;  // packed operand copies
   float* h0;                       // [N][D]: Attn + X, the residual stream entering the FFN
@@ -56,8 +56,9 @@ void launch_pack(bool bf, const float* W, int K, int N, void* out, hipStream_t s
 void launch_zero(void* p, int64_t n32, hipStream_t s);
 void launch_cvt(bool bf, const float* src, void* dst, int64_t n, hipStream_t s);
 void launch_step_ce(const float* bits, int32_t n_streams, int32_t n_steps, double* out, hipStream_t s);
-// XT[t][j][b][c] = operand(E[b][c] + P[t][j*e + c]) for the T x g token slots
-void launch_xtab(bool bf, const void* E, const void* P, int T, int g, int e, void* XT, hipStream_t s);
+// PW[w][t][:] = P[t] . W_w for w = q, k, v (W_* the fp32 master, rounded as operands)
+void launch_ptab(bool bf, const void* P, const float* Wq, const float* Wk, const float* Wv, int T, int D, float* PW,
+                 hipStream_t s);
 void launch_gather(bool bf, const WinArgs& w, const void* E, const void* P, int T, int D, int e, int g, float* X,
                    hipStream_t s);
 
@@ -98,7 +99,9 @@ void launch_add(float* y, const float* x, int64_t rows, int64_t cols, int64_t ld
 int64_t embed_bwd_ws_floats(int64_t total, int e);  // total = N * W positions
 void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int g, int e, int D, float* dE,
                       float* ws, float* cws, hipStream_t s);
-void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, const void* P, int T, int D, int e,
-                        int g, float* X, hipStream_t s);
+void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, int T, int D, int e, int g, float* X,
+                        hipStream_t s);
+// dW[i][j] += sum_{u < nt} P[t0 + u][i] * S[u][j]  (P: operand copy [T][D])
+void launch_pos_grad(bool bf, const void* P, const float* S, int t0, int nt, int D, float* dW, hipStream_t s);
 void launch_adam(float* theta, const float* grad, float* m, float* v, int64_t n, float lr, float b1, float b2,
                  float eps, float bc1, float bc2, hipStream_t s);

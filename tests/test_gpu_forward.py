@@ -37,7 +37,7 @@ def test_byte_group_gather_is_bit_exact(dtype, shape):
     p = O.compute_params(flat, cfg, mode)
     w, _ = O.all_windows(streams, cfg.W, shape["W"], n_steps)
     mo = O.trace_oracle._Mode(mode)
-    Xref = mo.R(O.embed_group(p, w, cfg, mo))
+    Xref = O.embed_group(p, w, cfg, mo)  # the fp32 token, E + P of the rounded copies
     assert np.array_equal(X.reshape(Xref.shape).view(np.uint32), Xref.astype(np.float32).view(np.uint32))
 
 
