@@ -318,6 +318,278 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
   }
 }
 
+// ------------------------------------------------- shared byte groups ----
+// k_attn_grp: the same block for bf16 tiles of MA consecutive windows of one
+// stream.  Windows at positions i and i + g share T-1 of their tokens (their
+// bytes are grouped from the same alignment), and a token's projection is
+// E.W + P.W with the positional part a table row, so the E-part of a byte
+// group's q, K and V is computed once for all the windows that hold it.
+// Wave w takes the NPW = MA/8 windows i = c + g*(b*NPW + i') of alignment class
+// c = w % g (b = w / g): their NPW*T tokens are the NPW + T - 1 groups
+// r = i' + t, one 16-row MFMA fragment.  Per head the wave writes its groups'
+// K_h (then V_h) to its own LDS rows; lanes (i', t) form the scores
+// q . (K_E[i'+t] + (P.Wk)[t]) and the softmax over t (aligned groups of T
+// lanes), and lanes (i', 4 features) form sum_t a_t (V_E[i'+t] + (P.Wv)[t]).
+template <int T, int G, int D, int DH>
+struct GrpShape {
+  static constexpr int NW = 8, MA = 64, NPW = MA / NW, W = T * G;
+  static constexpr int KSTEPS = D / 32, NFH = DH / 16;
+  static constexpr int KSC = (KSTEPS * NFH <= 16) ? KSTEPS : 16 / NFH;  // k-steps per staged 16 KiB chunk
+  static constexpr int CHUNK = KSC * NFH * 64;
+  static constexpr int XLSTR = D * 2 + 16;
+  static constexpr int KVSTR = DH + 4;  // floats per group row in the exchange
+  static constexpr int WB = MA + W + 64;
+  // q and attention weights are stored class-major (a wave's windows in
+  // consecutive rows) with padded rows, so a wave's reads hit distinct banks
+  static constexpr int QSTR = D + 4, PSTR = T + 1;
+  static constexpr int LDS = 2 * CHUNK * 16 + MA * QSTR * 4 + MA * XLSTR + WB + NW * 16 * KVSTR * 4 + MA * PSTR * 4 +
+                             2 * 2 * T * DH * 4;
+  static constexpr bool ok = (8 % G == 0) && NPW + T - 1 <= 16 && LDS <= 160 * 1024;
+};
+
+template <int T, int G, int D, int DH>
+__global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
+  typedef Mma<true> M;
+  typedef GrpShape<T, G, D, DH> S;
+  constexpr int H = D / DH, NW = S::NW, MA = S::MA, NPW = S::NPW, W = S::W;
+  constexpr int KSTEPS = S::KSTEPS, NFH = S::NFH, KSC = S::KSC, CPP = KSTEPS / KSC, CHUNK = S::CHUNK;
+  constexpr int XLSTR = S::XLSTR, KVSTR = S::KVSTR;
+  constexpr int NQF = D / 16, QFW = (NQF + NW - 1) / NW, NMF = MA / 16, NB = D / 16;
+  constexpr int CQ = DH / 4;  // 4-feature chunks of a head
+  static_assert(S::ok && KSTEPS % KSC == 0 && (T == 4 || T == 8), "shape");
+  __shared__ uint4 Wst[2][CHUNK];
+  constexpr int QSTR = S::QSTR, PSTR = S::PSTR;
+  __shared__ __align__(16) float Qs[MA * QSTR];            // q, row cm(i) of window i
+  __shared__ __align__(16) unsigned char Xl[MA * XLSTR];  // E_last rows, then O rows
+  __shared__ __align__(16) float KV[NW][16 * KVSTR];       // this wave's group rows of K_h, then V_h
+  __shared__ float Ps[MA * PSTR];                          // attention weights, row cm(i)
+  __shared__ __align__(16) float PKV[2][2][T * DH];       // head slices of P.Wk and P.Wv, double-buffered
+  __shared__ uint8_t Wb[S::WB];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lg = lane >> 4, lc = lane & 15;
+  const int64_t tile0 = (int64_t)blockIdx.x * MA;
+  const int64_t N = a.w.N;
+  const uint16_t* __restrict__ E = (const uint16_t*)a.E;
+  const uint16_t* __restrict__ P = (const uint16_t*)a.P;
+  const float* __restrict__ PQ = a.PW;
+  const float* __restrict__ PK = a.PW + (int64_t)T * D;
+  const float* __restrict__ PV = a.PW + (int64_t)2 * T * D;
+
+  // the tile's bytes: Wb[k] = stream byte at (target of window 0) - W + k,
+  // k < MA + W (all windows of the tile lie in one stream)
+  {
+    const int64_t base = target_offset(a.w, tile0) - W;
+    for (int k = tid; k < S::WB; k += 512) Wb[k] = k < MA + W ? a.w.streams[base + k] : 0;
+  }
+  const uint32_t einv = ((1u << 20) + (uint32_t)a.e - 1u) / (uint32_t)a.e;
+  const int cls = wave % G, blk = wave / G;
+  // window (tile index) of this wave's i'-th window
+  auto win_of = [&](int ip) { return cls + G * (blk * NPW + ip); };
+  // class-major row of window i (the windows of a wave are consecutive rows)
+  auto cm = [&](int i) { return ((i % G) + G * ((i / G) / NPW)) * NPW + (i / G) % NPW; };
+  __syncthreads();
+
+  // this wave's groups r = 0..15 as B fragments (E-part); the last group of each
+  // window (r = i' + T - 1) also to LDS as that window's E_last row
+  uint4 xb[KSTEPS];
+  {
+    const int r = lc;
+    const int off = cls + G * (blk * NPW + r);  // first byte of group r in Wb
+    const int ip = r - (T - 1);
+    int byte[KSTEPS];
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      const int d = ks * 32 + lg * 8;
+      const int j = (int)(((uint32_t)d * einv) >> 20);
+      byte[ks] = Wb[off + j];
+    }
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      const int d = ks * 32 + lg * 8;
+      const int j = (int)(((uint32_t)d * einv) >> 20), cc = d - j * a.e;
+      xb[ks] = *reinterpret_cast<const uint4*>(E + byte[ks] * a.e + cc);
+    }
+    if (ip >= 0 && ip < NPW) {
+#pragma unroll
+      for (int ks = 0; ks < KSTEPS; ++ks) *(uint4*)(Xl + win_of(ip) * XLSTR + ks * 64 + lg * 16) = xb[ks];
+    }
+  }
+  __syncthreads();
+
+  // q^T = Wq^T . E_last^T + (P.Wq)[T-1] ; lane holds q[m = nf*16 + lc][c = qf*16 + 4*lg + r]
+#pragma unroll
+  for (int qi = 0; qi < QFW; ++qi) {
+    const int qf = wave * QFW + qi;
+    if (qf < NQF) {
+      f32x4 acc[NMF];
+#pragma unroll
+      for (int nf = 0; nf < NMF; ++nf) acc[nf] = f32x4{0.f, 0.f, 0.f, 0.f};
+      uint4 wq[2];
+      wq[0] = a.Wq[qf * 64 + lane];
+#pragma unroll
+      for (int ks = 0; ks < KSTEPS; ++ks) {
+        if (ks + 1 < KSTEPS) wq[(ks + 1) & 1] = a.Wq[((ks + 1) * NB + qf) * 64 + lane];
+#pragma unroll
+        for (int nf = 0; nf < NMF; ++nf) {
+          const uint4 bx = *(const uint4*)(Xl + (nf * 16 + lc) * XLSTR + ks * 64 + lg * 16);
+          M::run(acc[nf], wq[ks & 1], bx);
+        }
+      }
+      const float4 pq = *reinterpret_cast<const float4*>(PQ + (T - 1) * D + qf * 16 + 4 * lg);
+#pragma unroll
+      for (int nf = 0; nf < NMF; ++nf) {
+        const int m = nf * 16 + lc;
+        *reinterpret_cast<float4*>(Qs + cm(m) * QSTR + qf * 16 + 4 * lg) =
+            make_float4(acc[nf][0] + pq.x, acc[nf][1] + pq.y, acc[nf][2] + pq.z, acc[nf][3] + pq.w);
+      }
+    }
+  }
+
+  auto chunk_src = [&](int c, int i) -> const uint4* {
+    const int ck = c % CPP, pass = (c / CPP) & 1, h = c / (2 * CPP);
+    const int kk = i / (NFH * 64), f = (i / 64) % NFH, ln = i & 63;
+    const uint4* Wp = pass ? a.Wv : a.Wk;
+    return Wp + ((ck * KSC + kk) * NB + h * NFH + f) * 64 + ln;
+  };
+  constexpr int NFRAG = KSC * NFH;
+  auto stage = [&](int c, int buf) {
+#pragma unroll
+    for (int q = wave; q < NFRAG; q += NW)
+      __builtin_amdgcn_global_load_lds((const void*)chunk_src(c, q * 64 + lane),
+                                       (__attribute__((address_space(3))) void*)(Wst[buf] + q * 64), 16, 0, 0);
+  };
+  constexpr int NCH = H * 2 * CPP;
+  stage(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();  // chunk 0 staged; Qs complete; E_last rows no longer needed
+
+  const float scale = a.scale;
+  float* kv = KV[wave];
+  const int row0 = wave * NPW;  // this wave's first class-major row (cm(win_of(0)))
+  // lanes as (window i', token t) pairs for the scores
+  const int sp_i = lane / T, sp_t = lane - (lane / T) * T;
+  const bool sp_live = sp_i < NPW;
+  for (int h = 0; h < H; ++h) {
+    // this head's rows of P.Wk and P.Wv to LDS (read after the K pass's barrier;
+    // the buffer was last read two heads ago)
+    {
+      float* dst = &PKV[h & 1][0][0];
+      for (int k = tid; k < 2 * T * DH; k += 512) {
+        const int which = k / (T * DH), t = (k / DH) % T, c = k % DH;
+        dst[k] = (which ? PV : PK)[t * D + h * DH + c];
+      }
+    }
+    const float* pkh = PKV[h & 1][0];
+    const float* pvh = PKV[h & 1][1];
+#pragma unroll
+    for (int pass = 0; pass < 2; ++pass) {
+      f32x4 acc[NFH];
+#pragma unroll
+      for (int f = 0; f < NFH; ++f) acc[f] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ck = 0; ck < CPP; ++ck) {
+        const int c = (h * 2 + pass) * CPP + ck;
+        if (c + 1 < NCH) stage(c + 1, (c + 1) & 1);
+        const uint4* buf = Wst[c & 1];
+#pragma unroll
+        for (int kk = 0; kk < KSC; ++kk) {
+#pragma unroll
+          for (int f = 0; f < NFH; ++f) M::run(acc[f], buf[(kk * NFH + f) * 64 + lane], xb[ck * KSC + kk]);
+        }
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+      }
+      // group rows of K_h (E-part) or V_h to this wave's exchange rows
+#pragma unroll
+      for (int f = 0; f < NFH; ++f)
+        *reinterpret_cast<float4*>(kv + lc * KVSTR + f * 16 + 4 * lg) =
+            make_float4(acc[f][0], acc[f][1], acc[f][2], acc[f][3]);
+      __builtin_amdgcn_wave_barrier();
+      if (pass == 0) {
+        float s = 0.f;
+        if (sp_live) {
+          const float* qv = Qs + (row0 + sp_i) * QSTR + h * DH;
+          const float* kr = kv + (sp_i + sp_t) * KVSTR;
+          const float* pk = pkh + sp_t * DH;
+#pragma unroll
+          for (int c4 = 0; c4 < CQ; ++c4) {
+            const float4 q4 = *reinterpret_cast<const float4*>(qv + 4 * c4);
+            const float4 k4 = *reinterpret_cast<const float4*>(kr + 4 * c4);
+            const float4 p4 = *reinterpret_cast<const float4*>(pk + 4 * c4);
+            s += q4.x * (k4.x + p4.x) + q4.y * (k4.y + p4.y) + q4.z * (k4.z + p4.z) + q4.w * (k4.w + p4.w);
+          }
+        }
+        s *= scale;
+        const float mx = group_max<T>(s);
+        const float pe = expf(s - mx);
+        const float sm = group_sum<T>(pe);
+        if (sp_live) Ps[(row0 + sp_i) * PSTR + sp_t] = pe * __builtin_amdgcn_rcpf(sm);
+      } else {
+        // O_h[i'][4 cq .. 4 cq + 3] = sum_t a_t (V_E[i'+t] + (P.Wv)[t]) -> O rows (bf16)
+#pragma unroll
+        for (int pr0 = 0; pr0 < NPW * CQ; pr0 += 64) {
+          const int pr = pr0 + lane;
+          if (pr < NPW * CQ) {
+            const int ip = pr / CQ, cq = pr - (pr / CQ) * CQ;
+            float4 o = make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int t = 0; t < T; ++t) {
+              const float at = Ps[(row0 + ip) * PSTR + t];
+              const float4 v4 = *reinterpret_cast<const float4*>(kv + (ip + t) * KVSTR + 4 * cq);
+              const float4 p4 = *reinterpret_cast<const float4*>(pvh + t * DH + 4 * cq);
+              o.x += at * (v4.x + p4.x);
+              o.y += at * (v4.y + p4.y);
+              o.z += at * (v4.z + p4.z);
+              o.w += at * (v4.w + p4.w);
+            }
+            put4o((uint16_t*)(Xl + win_of(ip) * XLSTR) + h * DH + 4 * cq, f32x4{o.x, o.y, o.z, o.w});
+          }
+        }
+      }
+      __builtin_amdgcn_wave_barrier();
+    }
+  }
+  __syncthreads();  // O complete
+
+  // h0^T = Wo^T . O^T + X_last (fp32: E + P of the last token)
+#pragma unroll
+  for (int qi = 0; qi < QFW; ++qi) {
+    const int qf = wave * QFW + qi;
+    if (qf < NQF) {
+      f32x4 acc[NMF];
+#pragma unroll
+      for (int nf = 0; nf < NMF; ++nf) acc[nf] = f32x4{0.f, 0.f, 0.f, 0.f};
+      uint4 wo[2];
+      wo[0] = a.Wo[qf * 64 + lane];
+#pragma unroll
+      for (int ks = 0; ks < KSTEPS; ++ks) {
+        if (ks + 1 < KSTEPS) wo[(ks + 1) & 1] = a.Wo[((ks + 1) * NB + qf) * 64 + lane];
+#pragma unroll
+        for (int nf = 0; nf < NMF; ++nf) {
+          const uint4 bo = *(const uint4*)(Xl + (nf * 16 + lc) * XLSTR + ks * 64 + lg * 16);
+          M::run(acc[nf], wo[ks & 1], bo);
+        }
+      }
+#pragma unroll
+      for (int nf = 0; nf < NMF; ++nf) {
+        const int m = nf * 16 + lc;
+        const int64_t n = tile0 + m;
+        if (n < N) {
+          const int d = qf * 16 + 4 * lg;
+          const int j = (int)(((uint32_t)d * einv) >> 20), cc = d - j * a.e;
+          const int byte = Wb[m + (T - 1) * G + j];
+          float4 r;
+          r.x = acc[nf][0] + (M::val(E[byte * a.e + cc]) + M::val(P[(T - 1) * D + d]));
+          r.y = acc[nf][1] + (M::val(E[byte * a.e + cc + 1]) + M::val(P[(T - 1) * D + d + 1]));
+          r.z = acc[nf][2] + (M::val(E[byte * a.e + cc + 2]) + M::val(P[(T - 1) * D + d + 2]));
+          r.w = acc[nf][3] + (M::val(E[byte * a.e + cc + 3]) + M::val(P[(T - 1) * D + d + 3]));
+          *reinterpret_cast<float4*>(a.h0 + n * D + d) = r;
+        }
+      }
+    }
+  }
+}
+
 // ------------------------------------------------------------ dispatch ----
 // Measured alternative, slower on the main workload (2^20 windows): two
 // accumulator sets so that the scores of head h run under the MFMAs of its V
@@ -333,10 +605,27 @@ static void launch_attn(const AttnArgs& a, hipStream_t s) {
     hipLaunchKernelGGL((k_attn<BF, T, D, DH, false, SMALL>), grid, dim3(512), 0, s, a);
 }
 
-// Launches too small to give every CU a workgroup at the widest tile (one step
-// of the update path) take one 16-row fragment per wave.
+template <int T, int G, int D, int DH>
+static bool launch_grp(const AttnArgs& a, hipStream_t s) {
+  if constexpr (GrpShape<T, G, D, DH>::ok) {
+    hipLaunchKernelGGL((k_attn_grp<T, G, D, DH>), dim3((unsigned)((a.w.N + 63) / 64)), dim3(512), 0, s, a);
+    return true;
+  }
+  return false;
+}
+
+// bf16 launches whose 64-window tiles each lie in one stream (steps per stream
+// and the launch's first window multiples of 64) share the byte groups
+// (k_attn_grp); launches too small to give every CU a workgroup at the widest
+// token tile (one step of the update path) take one 16-row fragment per wave.
 template <bool BF, int T, int D, int DH>
 static void run_attn(const AttnArgs& a, hipStream_t s) {
+  if constexpr (BF) {
+    if (!a.kK && a.w.n_steps % 64 == 0 && a.w.n0 % 64 == 0) {
+      if (a.g == 8 && launch_grp<T, 8, D, DH>(a, s)) return;
+      if (a.g == 4 && launch_grp<T, 4, D, DH>(a, s)) return;
+    }
+  }
   if (a.w.N >= (int64_t)256 * AttnShape<BF, T, D, DH>::MA || AttnShape<BF, T, D, DH>::RFW == 1)
     launch_attn<BF, T, D, DH, false>(a, s);
   else

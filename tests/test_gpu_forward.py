@@ -104,6 +104,30 @@ def test_ragged_tiles_and_chunking_are_bitwise_invariant(dtype):
     check_parity(dtype, a["logits"].cpu().numpy(), a["bits"].cpu().numpy(), ref)
 
 
+@pytest.mark.parametrize("shape", [dict(W=32, e=32, g=4, H=4, F=512, k=2), dict(W=64, e=32, g=8, H=8, F=256, k=1)])
+def test_shared_group_and_token_paths_agree(shape):
+    """bf16 launches whose 64-window tiles lie in one stream share the byte groups
+    between windows (k_attn_grp).  A model whose chunks do not start on 64-window
+    boundaries runs the token kernel (k_attn) on its later chunks; both match the
+    oracle on every window and each other within the bf16 parity bar."""
+    W = shape["W"]
+    n_steps = 128
+    streams = synth.random_streams(21, 9, W + n_steps + 1)
+    s = to_dev(streams)
+    grp = make_model(shape, "bf16", seed=13, max_windows=1 << 16)
+    tok = make_model(shape, "bf16", seed=13, max_windows=65)
+    a = grp.forward_bits(s, W, n_steps, logits=True)
+    b = tok.forward_bits(s, W, n_steps, logits=True)
+    flat = O.init_flat(ocfg(**shape), 13)
+    bb, ii = np.meshgrid(np.arange(9), W + np.arange(n_steps), indexing="ij")
+    ref = _oracle_at(shape, flat, streams, bb.ravel(), ii.ravel(), oracle_mode("bf16"))
+    check_parity("bf16", a["logits"].cpu().numpy(), a["bits"].cpu().numpy(), ref)
+    check_parity("bf16", b["logits"].cpu().numpy(), b["bits"].cpu().numpy(), ref)
+    za, zb = a["logits"].cpu().numpy(), b["logits"].cpu().numpy()
+    rel = np.abs(za - zb).max(axis=1) / np.maximum(np.abs(zb).max(axis=1), 1e-6)
+    assert rel.max() < 2e-2
+
+
 def test_permuting_streams_permutes_outputs_bitwise():
     shape, dtype = workload_cfg(3)
     streams, _ = synth.workload_streams(3, L=400, B=96)
