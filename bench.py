@@ -45,6 +45,17 @@ def flops_per_window(w):
     return {"attn": 4 * T * d * d + 4 * d * d + 4 * T * d, "ffn_head": 4 * k * d * F + 512 * d}
 
 
+def mfma_flops_per_window(w):
+    """Flops the matrix cores execute per window on the main workload's launches
+    (bf16, 64-window tiles within one stream): the attention block projects each
+    wave's 16 byte-group rows (15 distinct groups of its 8 windows) to K and V
+    once, 16 * 4d^2 / 8 = 8d^2 per window, plus q and Wo (2d^2 each); the
+    scores and weighted sums run on the vector ALUs.  The FFN executes its
+    algorithmic work."""
+    d = w.d
+    return {"attn": 12 * d * d, "ffn_head": flops_per_window(w)["ffn_head"]}
+
+
 def gated_loop(model, sdev, B, pos0, n_steps, t, delta, always, max_spec=64):
     """Alg. 1 with the controller of Alg. 2 over B streams.  Forward passes run
     speculatively over up to max_spec steps at unchanged weights; the controller
@@ -246,6 +257,7 @@ def main():
     log(f"[bench] main: {K} steps x {B * S} windows in {ms:.1f} ms -> {value:.4g} bytes/s; {tm}")
 
     fpw = flops_per_window(w)
+    xpw = mfma_flops_per_window(w)
     per = {k: tm[k][0] / max(tm[k][1], 1) for k in ("attn", "ffn_head")}
     dom = max(per, key=lambda k: tm[k][0])
     wpl = B * S
@@ -253,15 +265,19 @@ def main():
     peak = PEAK_TFLOPS[w.dtype]
     total_tflops = (fpw["attn"] + fpw["ffn_head"]) * value / 1e12
     # the FFN + head kernel is k_ffn_pipe in bf16, k_ffn_head in fp32
-    kname = ("k_ffn_pipe" if w.dtype == "bf16" else "k_ffn_head") if dom == "ffn_head" else "k_attn"
+    # bf16 launches of whole 64-window tiles per stream take the shared-group attention kernel
+    attn_k = "k_attn_grp" if (w.dtype == "bf16" and S % 64 == 0) else "k_attn"
+    kname = ("k_ffn_pipe" if w.dtype == "bf16" else "k_ffn_head") if dom == "ffn_head" else attn_k
     traffic = traffic_for(kname, wpl)
     roofline = {"bound": "mfma", "kernel": kname,
                 "achieved": round(achieved, 2), "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
                 "traffic": None if traffic is None else round(traffic),
                 "flops_per_window": fpw[dom], "windows_per_launch": wpl, "avg_launch_ms": round(per[dom], 4),
                 "kernels": {k: {"avg_launch_ms": round(per[k], 4),
-                                "tflops": round(fpw[k] * wpl / (per[k] * 1e-3) / 1e12, 2)} for k in per},
-                "path_tflops": round(total_tflops, 2), "path_frac": round(total_tflops / peak, 4)}
+                                "tflops": round(fpw[k] * wpl / (per[k] * 1e-3) / 1e12, 2),
+                                "mfma_tflops": round(xpw[k] * wpl / (per[k] * 1e-3) / 1e12, 2)} for k in per},
+                "path_tflops": round(total_tflops, 2), "path_frac": round(total_tflops / peak, 4),
+                "path_mfma_frac": round((xpw["attn"] + xpw["ffn_head"]) * value / 1e12 / peak, 4)}
 
     out = {"metric": "bytes/sec estimated (fwd+bits) and with gated adapt; MFMA util; bits/byte",
            "value": value, "unit": "bytes/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
@@ -271,7 +287,7 @@ def main():
                                   f"Zipf(1.2) / uniform thirds), W={w.W} e={w.e} g={w.g} -> T={w.T} d={w.d}, "
                                   f"H={w.H}, F={w.F} shared x{w.k}, bf16 operands fp32 accumulate",
                       "windows_per_step": B * S, "steps_per_call": S, "stream_prefix_bytes": L},
-           "bits_per_byte": bpb, "mfma_util": roofline["path_frac"], "roofline": roofline}
+           "bits_per_byte": bpb, "mfma_util": roofline["path_mfma_frac"], "roofline": roofline}
     if args.gated_steps > 0:
         out["gated_adapt"] = {"adapt-bf16": measure_gated(4, args.gated_steps),
                               "large-mixed-bf16": measure_gated(5, max(16, args.gated_steps // 2))}

@@ -68,6 +68,7 @@ __global__ void k_ptab(const typename Mma<BF>::T* __restrict__ P, const float* _
   const int j = (int)(i % D), t = (int)((i / D) % T), w = (int)(i / ((int64_t)T * D));
   const float* Wm = w == 0 ? Wq : (w == 1 ? Wk : Wv);
   float s = 0.f;
+#pragma unroll 8
   for (int k = 0; k < D; ++k) s = fmaf(M::val(P[t * D + k]), M::val(M::cvt(Wm[(int64_t)k * D + j])), s);
   PW[i] = s;
 }
