@@ -39,8 +39,6 @@ struct trace_model {
   // backward scratch
   float *dz, *dY, *dG, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *sP, *gws, *cws, *ews;
   int64_t gws_cap;
-  void* pws;  // bf16 operand copies of the update GEMMs
-  int64_t pws_cap;
   std::vector<void*> allocs;
   // event timing (trace_set_timing)
   bool timing;
@@ -86,7 +84,7 @@ std::vector<std::array<int, 3>> adapt_gemm_shapes(const trace_model* m, int64_t 
   const int D = m->L.D, F = m->cfg.F, T = m->L.T;
   const int n = (int)N;
   return {{D, 256, n}, {n, D, 256}, {F, D, n}, {n, F, D}, {D, F, n},
-          {n, D, F},   {D, D, n},   {n, D, D}, {D, D, n * T}, {n * T, D, D}};
+          {n, D, F},   {D, D, n},   {n, D, D}, {D, D, n * T}, {n * T, D, D}, {n * T, D, 2 * D}};
 }
 // Largest split-K workspace (floats) over those GEMMs, for either GEMM path.
 int64_t adapt_gemm_ws(const trace_model* m, int64_t N) {
@@ -94,12 +92,6 @@ int64_t adapt_gemm_ws(const trace_model* m, int64_t N) {
   for (auto& s : adapt_gemm_shapes(m, N))
     w = std::max(w, std::max(gemm_ws_floats(s[0], s[1], s[2]), bgemm_ws_floats(s[0], s[1], s[2])));
   return w;
-}
-// Largest bf16 operand-copy space (bytes) of the prepared-operand GEMM.
-int64_t adapt_prep_bytes(const trace_model* m, int64_t N) {
-  int64_t b = 0;
-  for (auto& s : adapt_gemm_shapes(m, N)) b = std::max(b, bgemm_prep_bytes(s[0], s[1], s[2]));
-  return b;
 }
 
 hipStream_t S(void* s) { return (hipStream_t)s; }
@@ -220,7 +212,6 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
          dalloc(m, &m->dV, K * T * D * 4) && dalloc(m, &m->dX, K * T * D * 4) && dalloc(m, &m->Xk, K * T * D * 4) &&
          dalloc(m, &m->sP, T * D * 4) &&
          dalloc(m, &m->gws, (m->gws_cap = adapt_gemm_ws(m, K)) * 4) &&
-         (!bf || dalloc(m, &m->pws, (m->pws_cap = adapt_prep_bytes(m, K)))) &&
          dalloc(m, &m->ews, embed_bwd_ws_floats(K * W, cfg->e) * 4) &&
          dalloc(m, &m->cws, colsum_ws_floats(std::max<int64_t>(std::max<int64_t>(T * D, 256), 256 * cfg->e)) * 4);
   }
@@ -384,24 +375,24 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   launch_ce_grad(m->kZ, m->ktgt, N, m->dz, s);
   // dWout = h_k^T . dz ; dbout = sum_n dz ; dY_k = dz . Wout^T
   const float* Yk = m->kY + (int64_t)k * N * D;
-  launch_gemm(gemm(D, 256, N, Yk, 1, D, rb, m->dz, 256, 1, rb, gr + L.off[P_WOUT], 256, 0.f), ws, m->gws_cap, m->pws, m->pws_cap, s);
+  launch_gemm(gemm(D, 256, N, Yk, 1, D, rb, m->dz, 256, 1, rb, gr + L.off[P_WOUT], 256, 0.f), ws, m->gws_cap, s);
   launch_colsum(m->dz, N, 256, 256, gr + L.off[P_BOUT], 0.f, m->cws, s);
-  launch_gemm(gemm(N, D, 256, m->dz, 256, 1, rb, th + L.off[P_WOUT], 1, 256, rb, m->dY, D, 0.f), ws, m->gws_cap, m->pws, m->pws_cap, s);
+  launch_gemm(gemm(N, D, 256, m->dz, 256, 1, rb, th + L.off[P_WOUT], 1, 256, rb, m->dY, D, 0.f), ws, m->gws_cap, s);
   // shared FFN, repeats in reverse; W1 and W2 gradients accumulate over repeats
   for (int r = k - 1; r >= 0; --r) {
     const float* Ur = m->kU + (int64_t)r * N * F;
     const float* Yr = m->kY + (int64_t)r * N * D;
     const float beta = (r == k - 1) ? 0.f : 1.f;
     launch_gelu_fwd_round(Ur, m->G, (int64_t)N * F, rb, s);
-    launch_gemm(gemm(F, D, N, m->G, 1, F, rb, m->dY, D, 1, rb, gr + L.off[P_W2], D, beta), ws, m->gws_cap, m->pws, m->pws_cap, s);
-    launch_gemm(gemm(N, F, D, m->dY, D, 1, rb, th + L.off[P_W2], 1, D, rb, m->dG, F, 0.f), ws, m->gws_cap, m->pws, m->pws_cap, s);
+    launch_gemm(gemm(F, D, N, m->G, 1, F, rb, m->dY, D, 1, rb, gr + L.off[P_W2], D, beta), ws, m->gws_cap, s);
+    launch_gemm(gemm(N, F, D, m->dY, D, 1, rb, th + L.off[P_W2], 1, D, rb, m->dG, F, 0.f), ws, m->gws_cap, s);
     launch_gelu_bwd(m->dG, Ur, m->dU, (int64_t)N * F, s);
-    launch_gemm(gemm(D, F, N, Yr, 1, D, rb, m->dU, F, 1, rb, gr + L.off[P_W1], F, beta), ws, m->gws_cap, m->pws, m->pws_cap, s);
-    launch_gemm(gemm(N, D, F, m->dU, F, 1, rb, th + L.off[P_W1], 1, F, rb, m->dY, D, 1.f), ws, m->gws_cap, m->pws, m->pws_cap, s);
+    launch_gemm(gemm(D, F, N, Yr, 1, D, rb, m->dU, F, 1, rb, gr + L.off[P_W1], F, beta), ws, m->gws_cap, s);
+    launch_gemm(gemm(N, D, F, m->dU, F, 1, rb, th + L.off[P_W1], 1, F, rb, m->dY, D, 1.f), ws, m->gws_cap, s);
   }
   // attention output projection: dWo = O^T . dY0 ; dO = dY0 . Wo^T
-  launch_gemm(gemm(D, D, N, m->kO, 1, D, rb, m->dY, D, 1, rb, gr + L.off[P_WO], D, 0.f), ws, m->gws_cap, m->pws, m->pws_cap, s);
-  launch_gemm(gemm(N, D, D, m->dY, D, 1, rb, th + L.off[P_WO], 1, D, rb, m->dO, D, 0.f), ws, m->gws_cap, m->pws, m->pws_cap, s);
+  launch_gemm(gemm(D, D, N, m->kO, 1, D, rb, m->dY, D, 1, rb, gr + L.off[P_WO], D, 0.f), ws, m->gws_cap, s);
+  launch_gemm(gemm(N, D, D, m->dY, D, 1, rb, th + L.off[P_WO], 1, D, rb, m->dO, D, 0.f), ws, m->gws_cap, s);
   // attention (last query row) -> dQ, dK, dV
   launch_attn_bwd(m->dO, m->kq, m->kK, m->kV, m->kA, N, T, D, H, (float)(1.0 / std::sqrt((double)L.DH)), rb, m->dQ,
                   m->dK, m->dV, s);
@@ -411,9 +402,9 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   launch_gather_kept(m->bf, m->kwin, N, m->Ec, T, D, m->cfg.e, m->cfg.g, m->Xk, s);
   launch_gemm(gemm(D, D, N, m->Xk + (int64_t)(T - 1) * D, 1, (int64_t)T * D, rb, m->dQ, D, 1, 0, gr + L.off[P_WQ], D,
                    0.f),
-              ws, m->gws_cap, m->pws, m->pws_cap, s);
-  launch_gemm(gemm(D, D, N * T, m->Xk, 1, D, rb, m->dK, D, 1, 0, gr + L.off[P_WK], D, 0.f), ws, m->gws_cap, m->pws, m->pws_cap, s);
-  launch_gemm(gemm(D, D, N * T, m->Xk, 1, D, rb, m->dV, D, 1, 0, gr + L.off[P_WV], D, 0.f), ws, m->gws_cap, m->pws, m->pws_cap, s);
+              ws, m->gws_cap, s);
+  launch_gemm(gemm(D, D, N * T, m->Xk, 1, D, rb, m->dK, D, 1, 0, gr + L.off[P_WK], D, 0.f), ws, m->gws_cap, s);
+  launch_gemm(gemm(D, D, N * T, m->Xk, 1, D, rb, m->dV, D, 1, 0, gr + L.off[P_WV], D, 0.f), ws, m->gws_cap, s);
   if (m->cfg.use_pos) {
     launch_colsum(m->dQ, N, D, D, m->sP, 0.f, m->cws, s);
     launch_pos_grad(m->bf, m->Pc, m->sP, T - 1, 1, D, gr + L.off[P_WQ], s);
@@ -423,11 +414,11 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
     launch_pos_grad(m->bf, m->Pc, m->sP, 0, T, D, gr + L.off[P_WV], s);
   }
   // dX = dK Wk^T + dV Wv^T (+ dQ Wq^T + dY0 on the last token)
-  launch_gemm(gemm(N * T, D, D, m->dK, D, 1, 0, th + L.off[P_WK], 1, D, rb, m->dX, D, 0.f), ws, m->gws_cap, m->pws, m->pws_cap, s);
-  launch_gemm(gemm(N * T, D, D, m->dV, D, 1, 0, th + L.off[P_WV], 1, D, rb, m->dX, D, 1.f), ws, m->gws_cap, m->pws, m->pws_cap, s);
+  launch_gemm2(gemm(N * T, D, D, m->dK, D, 1, 0, th + L.off[P_WK], 1, D, rb, m->dX, D, 0.f),
+               gemm(N * T, D, D, m->dV, D, 1, 0, th + L.off[P_WV], 1, D, rb, m->dX, D, 0.f), ws, m->gws_cap, s);
   launch_gemm(gemm(N, D, D, m->dQ, D, 1, 0, th + L.off[P_WQ], 1, D, rb, m->dX + (int64_t)(T - 1) * D, (int64_t)T * D,
                    1.f),
-              ws, m->gws_cap, m->pws, m->pws_cap, s);
+              ws, m->gws_cap, s);
   launch_add(m->dX + (int64_t)(T - 1) * D, m->dY, N, D, (int64_t)T * D, D, s);
   // positional table and byte embedding
   if (m->cfg.use_pos)

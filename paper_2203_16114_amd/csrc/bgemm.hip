@@ -1,17 +1,22 @@
-// GEMM of the update step on bf16 operands (Alg. 1: the backward of the
+// GEMM of the update step on bf16 MFMAs (Alg. 1: the backward of the
 // estimator's loss, every product of which is a plain matrix product).
 //
-// Each operand is first written by a memory-bound prep kernel as a bf16 copy
-// whose contiguous dimension is k (rows = m for A, n for B), zero-padded to
-// whole tiles; operands that are fp32 values rather than bf16 storage points
-// are split into hi = bf16(v) and lo = bf16(v - hi), and their products take
-// two MFMAs (hi.B + lo.B), which keeps about 16 significant bits of v.
-// The GEMM then moves 128 x 64 operand tiles straight from global memory to
-// LDS (16-byte direct loads, no register staging), double-buffered, in an
-// XOR-swizzled layout that makes the 16-byte fragment reads conflict-free,
-// and runs 16x16x32 bf16 MFMAs on 64x64 blocks per wave.  Split-K partial
-// sums go to a workspace and are added in a fixed order, so results do not
-// depend on scheduling.
+// Operands are read as fp32 straight from where the update step keeps them,
+// in either orientation: k contiguous (activation gradients times weights,
+// dY . W^T) or m / n contiguous (weight gradients, act^T . dY).  Each thread
+// reads its share of the next 128 x 64 k-tile with float4 loads while the
+// current tile is multiplied, converts it in registers (one v_cvt_pk_bf16_f32
+// per pair, round to nearest even) and writes whole 16-byte units of 8 k
+// values to LDS, in an XOR-swizzled layout whose fragment reads are free of
+// bank conflicts.  Operands that are fp32 values rather than bf16 storage
+// points are split into hi = bf16(v) and lo = bf16(v - hi) (v - hi is exact in
+// fp32), and their products take two MFMAs (hi.B + lo.B), which keeps about
+// 16 significant bits of v.  A product may have two K segments summed into
+// one result (C = A1.B1 + A2.B2, as the two halves of the input gradient of
+// the key and value projections), so that C is written once.
+// Split-K partial sums go to a workspace and are added in a fixed order, so
+// results do not depend on scheduling.  Blocks are ordered so that the tiles
+// that share operand rows run on one XCD (one L2).
 #include "kcommon.h"
 #include "kernels.h"
 
@@ -22,108 +27,165 @@ constexpr int UNITS = BM * BK * 2 / 16;  // 16-byte units per 128 x 64 bf16 tile
 
 inline int64_t rup(int64_t x, int64_t a) { return (x + a - 1) / a * a; }
 
-__device__ __forceinline__ void split_bf(float v, uint16_t& h, uint16_t& l) {
-  h = f2bf(v);
-  l = f2bf(v - bf2f(h));
+typedef float f32x2v __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+
+// (a, b) -> bf16 pair, a in the low half, each rounded to nearest even
+__device__ __forceinline__ uint32_t pk_bf(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2v{a, b}, bf16x2v));
+}
+// bf16 pair of the residuals (a - hi_a, b - hi_b), h = pk_bf(a, b)
+__device__ __forceinline__ uint32_t pk_lo(float a, float b, uint32_t h) {
+  return pk_bf(a - __uint_as_float(h << 16), b - __uint_as_float(h & 0xffff0000u));
+}
+__device__ __forceinline__ float comp(const float4& v, int i) {
+  return i == 0 ? v.x : (i == 1 ? v.y : (i == 2 ? v.z : v.w));
 }
 
-// out[c][r] = bf16(src[r*ld + c]) for r < R, c < C, zero elsewhere: rows
-// [0, rows_p) of length Kp (k = r).  64 x 64 source tiles through LDS, so that
-// both the reads (along c) and the writes (along r) are coalesced.
-__global__ __launch_bounds__(256) void k_prep_t(const float* __restrict__ src, int R, int C, int64_t ld,
-                                                uint16_t* __restrict__ hi, uint16_t* __restrict__ lo, int Kp) {
-  __shared__ float t[64][65];
-  const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64, tid = threadIdx.x;
-#pragma unroll
-  for (int q = 0; q < 16; ++q) {
-    const int idx = tid + q * 256, rr = idx >> 6, cc = idx & 63;
-    const int r = r0 + rr, c = c0 + cc;
-    t[rr][cc] = (r < R && c < C) ? src[(int64_t)r * ld + c] : 0.f;
-  }
-  __syncthreads();
-#pragma unroll
-  for (int q = 0; q < 2; ++q) {
-    const int u = tid + q * 256, i = u >> 3, kc = u & 7;
-    uint16_t h[8], l[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) split_bf(t[kc * 8 + j][i], h[j], l[j]);
-    const int64_t o = (int64_t)(c0 + i) * Kp + r0 + kc * 8;
-    *reinterpret_cast<uint4*>(hi + o) = make_uint4(h[0] | (uint32_t)h[1] << 16, h[2] | (uint32_t)h[3] << 16,
-                                                   h[4] | (uint32_t)h[5] << 16, h[6] | (uint32_t)h[7] << 16);
-    if (lo)
-      *reinterpret_cast<uint4*>(lo + o) = make_uint4(l[0] | (uint32_t)l[1] << 16, l[2] | (uint32_t)l[3] << 16,
-                                                     l[4] | (uint32_t)l[5] << 16, l[6] | (uint32_t)l[7] << 16);
-  }
-}
-
-// out[r][c] = bf16(src[r*ld + c]) for r < R, c < C, zero elsewhere: rows
-// [0, rows_p) of length Kp (k = c); eight elements per thread.
-__global__ __launch_bounds__(256) void k_prep_n(const float* __restrict__ src, int R, int C, int64_t ld,
-                                                uint16_t* __restrict__ hi, uint16_t* __restrict__ lo, int rows_p,
-                                                int Kp) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int kcn = Kp / 8;
-  if (i >= (int64_t)rows_p * kcn) return;
-  const int r = (int)(i / kcn), c0 = (int)(i % kcn) * 8;
-  uint16_t h[8], l[8];
-#pragma unroll
-  for (int j = 0; j < 8; ++j) split_bf((r < R && c0 + j < C) ? src[(int64_t)r * ld + c0 + j] : 0.f, h[j], l[j]);
-  const int64_t o = (int64_t)r * Kp + c0;
-  *reinterpret_cast<uint4*>(hi + o) = make_uint4(h[0] | (uint32_t)h[1] << 16, h[2] | (uint32_t)h[3] << 16,
-                                                 h[4] | (uint32_t)h[5] << 16, h[6] | (uint32_t)h[7] << 16);
-  if (lo)
-    *reinterpret_cast<uint4*>(lo + o) = make_uint4(l[0] | (uint32_t)l[1] << 16, l[2] | (uint32_t)l[3] << 16,
-                                                   l[4] | (uint32_t)l[5] << 16, l[6] | (uint32_t)l[7] << 16);
-}
+// One operand: up to two K segments, element (row, k) of segment s at
+// p_s[row * ld_s + k] (k contiguous) or p_s[k * ld_s + row].  Segment 1 starts
+// at k = k1p of the product (segment 0's extent rounded up to BK).  (Named
+// fields, not arrays: an array indexed at run time would live in scratch.)
+struct Src {
+  const float* p0;
+  const float* p1;
+  int64_t ld0, ld1;
+  int kext0, kext1;
+  int k1p;
+  int rows;
+};
 
 // LDS unit (16 bytes) of (row, k-chunk c) in a swizzled 128 x 64 tile.
 __device__ __forceinline__ int unit_of(int row, int c) { return row * 8 + (c ^ (row & 7)); }
 
-// 128 x 64 tile of a prepared operand (rows row0.., k k0..) -> LDS tile, by
-// 16 direct 1 KiB loads; this wave issues loads q = wave*4 .. wave*4 + 3.
-__device__ __forceinline__ void tile_to_lds(const uint16_t* __restrict__ op, int64_t Kp, int row0, int k0,
-                                            uint4* dst, int wave, int lane) {
+// This thread's 32 values of the 128 x 64 tile (rows row0.., k k0..).  k
+// contiguous: units u = tid + 256 q (row u / 8, chunk u % 8), two float4 each.
+// Rows contiguous: rows 4 (tid % 32) .. +3 of chunk tid / 32, one float4 per k.
+// Every load is made, from an address clamped into the operand; bit j of the
+// returned mask says whether float4 j lies inside, and store_tile zeroes the
+// others.  (A load under a condition is compiled into a load from a select of
+// the address and a zero in scratch memory, and a select right after the load
+// would wait for it before the multiply.)
+template <bool KC>
+__device__ __forceinline__ uint32_t load_tile(const Src& s, int row0, int k0, int tid, float4 (&v)[8]) {
+  const bool seg1 = k0 >= s.k1p;
+  const float* __restrict__ p = seg1 ? s.p1 : s.p0;
+  const int ld = (int)(seg1 ? s.ld1 : s.ld0);
+  const int kk0 = seg1 ? k0 - s.k1p : k0, kr = (seg1 ? s.kext1 : s.kext0) - kk0;  // k values left
+  uint32_t mask = 0;
+  // per-tile base in scalar registers, 32-bit offsets within the tile
+  auto ld4 = [](const float* base, int off) {
+    return *reinterpret_cast<const float4*>(reinterpret_cast<const char*>(base) + (uint32_t)off * 4u);
+  };
+  if constexpr (KC) {
+    const float* base = p + (int64_t)row0 * ld + kk0;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int q = wave * 4 + i;
-    const int u = q * 64 + lane, row = u >> 3, c = (u & 7) ^ (row & 7);
-    __builtin_amdgcn_global_load_lds((const void*)(op + (int64_t)(row0 + row) * Kp + k0 + c * 8),
-                                     (__attribute__((address_space(3))) void*)(dst + q * 64), 16, 0, 0);
+    for (int q = 0; q < 4; ++q) {
+      const int u = tid + 256 * q, rr = u >> 3, c8 = (u & 7) * 8;
+      const int ro = min(rr, s.rows - 1 - row0) * ld;
+      v[2 * q] = ld4(base, ro + min(c8, kr - 4));
+      v[2 * q + 1] = ld4(base, ro + min(c8 + 4, kr - 4));
+      const bool rin = row0 + rr < s.rows;
+      mask |= (uint32_t)(rin && c8 < kr) << (2 * q);
+      mask |= (uint32_t)(rin && c8 + 4 < kr) << (2 * q + 1);
+    }
+  } else {
+    const float* base = p + (int64_t)kk0 * ld + row0;
+    const int rr = 4 * (tid & 31), kc = (tid >> 5) * 8;
+    const bool rin = row0 + rr < s.rows;
+    const int ro = min(rr, s.rows - 4 - row0);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      v[j] = ld4(base, min(kc + j, kr - 1) * ld + ro);
+      mask |= (uint32_t)(rin && kc + j < kr) << j;
+    }
+  }
+  return mask;
+}
+
+// The values of load_tile (float4 j zero unless bit j of mask) -> bf16 units
+// of the LDS tile hi (and lo when split).
+template <bool KC, bool SPLIT>
+__device__ __forceinline__ void store_tile(const float4 (&vin)[8], uint32_t mask, uint4* hi, uint4* lo, int tid) {
+  float4 v[8];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t m = 0u - ((mask >> j) & 1u);
+    v[j] = make_float4(__uint_as_float(__float_as_uint(vin[j].x) & m), __uint_as_float(__float_as_uint(vin[j].y) & m),
+                       __uint_as_float(__float_as_uint(vin[j].z) & m), __uint_as_float(__float_as_uint(vin[j].w) & m));
+  }
+  if constexpr (KC) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int u = tid + 256 * q, at = unit_of(u >> 3, u & 7);
+      const float4 a = v[2 * q], b = v[2 * q + 1];
+      const uint4 h = make_uint4(pk_bf(a.x, a.y), pk_bf(a.z, a.w), pk_bf(b.x, b.y), pk_bf(b.z, b.w));
+      hi[at] = h;
+      if constexpr (SPLIT)
+        lo[at] = make_uint4(pk_lo(a.x, a.y, h.x), pk_lo(a.z, a.w, h.y), pk_lo(b.x, b.y, h.z), pk_lo(b.z, b.w, h.w));
+    }
+  } else {
+    const int rr = 4 * (tid & 31), c = tid >> 5;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int at = unit_of(rr + i, c);
+      float x[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] = comp(v[j], i);
+      const uint4 h = make_uint4(pk_bf(x[0], x[1]), pk_bf(x[2], x[3]), pk_bf(x[4], x[5]), pk_bf(x[6], x[7]));
+      hi[at] = h;
+      if constexpr (SPLIT)
+        lo[at] = make_uint4(pk_lo(x[0], x[1], h.x), pk_lo(x[2], x[3], h.y), pk_lo(x[4], x[5], h.z),
+                            pk_lo(x[6], x[7], h.w));
+    }
   }
 }
 
-// C[m][n] (+)= sum_k A[m][k] B[n][k] over this split's k range, operands
-// prepared (bf16, k contiguous, padded); SA / SB: that operand has a lo part.
-template <bool SA, bool SB>
-__global__ __launch_bounds__(256) void k_bgemm(const uint16_t* __restrict__ Ah, const uint16_t* __restrict__ Al,
-                                               const uint16_t* __restrict__ Bh, const uint16_t* __restrict__ Bl,
-                                               int Kp, int M, int N, float* C, int64_t ldc, float beta,
-                                               float* __restrict__ part, int kchunk) {
+// C[m][n] (+)= sum_k A(m, k) B(k, n) over this split's k range.  AKC / BKC:
+// that operand's contiguous dimension is k; SA / SB: that operand is split.
+// 1-D grid of tn * tm * splits blocks.
+template <bool AKC, bool BKC, bool SA, bool SB>
+__global__ __launch_bounds__(256) void k_bgemm(Src A, Src B, int Kp, int M, int N, float* __restrict__ C, int64_t ldc,
+                                               float beta, float* __restrict__ part, int kchunk, int tn, int tm) {
   static_assert(!(SA && SB), "at most one operand is split");
   constexpr int NT = 2 + (SA ? 1 : 0) + (SB ? 1 : 0);  // tiles per stage: A hi, B hi, [A lo | B lo]
   __shared__ uint4 lds[2][NT][UNITS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lg = lane >> 4, lc = lane & 15;
   const int wm = wave >> 1, wn = wave & 1;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const int kb = blockIdx.z * kchunk;
-  const int ke = min(Kp, kb + kchunk);
+  // workgroups go to the 8 XCDs in turn: give each XCD a run of consecutive
+  // tiles (n fastest), which share rows of A and k ranges of B
+  const int nb = (int)gridDim.x, b = (int)blockIdx.x, per = nb / 8;
+  const int L = b < per * 8 ? (b & 7) * per + (b >> 3) : b;
+  const int bx = L % tn, by = (L / tn) % tm, bz = L / (tn * tm);
+  const int m0 = by * BM, n0 = bx * BN;
+  const int kb = bz * kchunk, ke = min(Kp, kb + kchunk);
   f32x4 acc[4][4];
 #pragma unroll
   for (int i = 0; i < 4; ++i)
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  auto stage = [&](int buf, int k0) {
-    tile_to_lds(Ah, Kp, m0, k0, lds[buf][0], wave, lane);
-    tile_to_lds(Bh, Kp, n0, k0, lds[buf][1], wave, lane);
-    if constexpr (SA) tile_to_lds(Al, Kp, m0, k0, lds[buf][2], wave, lane);
-    if constexpr (SB) tile_to_lds(Bl, Kp, n0, k0, lds[buf][NT - 1], wave, lane);
+  float4 va[8], vb[8];
+  uint32_t ma = 0, mb_ = 0;
+  auto put = [&](int buf) {
+    store_tile<AKC, SA>(va, ma, lds[buf][0], lds[buf][SA ? 2 : 0], tid);
+    store_tile<BKC, SB>(vb, mb_, lds[buf][1], lds[buf][NT - 1], tid);
   };
-  if (kb < ke) stage(0, kb);
-  __builtin_amdgcn_s_waitcnt(0);
+  if (kb < ke) {
+    ma = load_tile<AKC>(A, m0, kb, tid, va);
+    mb_ = load_tile<BKC>(B, n0, kb, tid, vb);
+    put(0);
+  }
   __syncthreads();
   int buf = 0;
   for (int k0 = kb; k0 < ke; k0 += BK, buf ^= 1) {
-    if (k0 + BK < ke) stage(buf ^ 1, k0 + BK);
+    const bool more = k0 + BK < ke;
+    if (more) {  // next tile into registers while this one is multiplied
+      ma = load_tile<AKC>(A, m0, k0 + BK, tid, va);
+      mb_ = load_tile<BKC>(B, n0, k0 + BK, tid, vb);
+    }
+    // keep the order loads / multiply / LDS writes: otherwise the writes to the
+    // other buffer are hoisted above the multiply and wait on the loads at once
+    asm volatile("" ::: "memory");
 #pragma unroll
     for (int ks = 0; ks < BK / 32; ++ks) {
       const int c = ks * 4 + lg;
@@ -153,92 +215,394 @@ __global__ __launch_bounds__(256) void k_bgemm(const uint16_t* __restrict__ Ah, 
           for (int nf = 0; nf < 4; ++nf) Mma<true>::run(acc[rf][nf], af[rf], bf[nf]);
       }
     }
-    __builtin_amdgcn_s_waitcnt(0);  // this wave's part of the next stage has landed
+    asm volatile("" ::: "memory");
+    // the other buffer was last read before the previous barrier
+    if (more) put(buf ^ 1);
     __syncthreads();
   }
   // lane holds C[m0 + wm*64 + rf*16 + 4*lg + r][n0 + wn*64 + nf*16 + lc]
+  const int mb = m0 + wm * 64 + 4 * lg, nbase = n0 + wn * 64 + lc;
+  if (part) {
+    float* pz = part + (int64_t)bz * M * N;
 #pragma unroll
-  for (int rf = 0; rf < 4; ++rf)
+    for (int rf = 0; rf < 4; ++rf)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int m = m0 + wm * 64 + rf * 16 + 4 * lg + r;
-      if (m >= M) continue;
+      for (int r = 0; r < 4; ++r) {
+        const int m = mb + rf * 16 + r;
+        if (m >= M) continue;
 #pragma unroll
-      for (int nf = 0; nf < 4; ++nf) {
-        const int n = n0 + wn * 64 + nf * 16 + lc;
-        if (n >= N) continue;
-        if (part) {
-          part[((int64_t)blockIdx.z * M + m) * N + n] = acc[rf][nf][r];
-        } else {
-          float* cp = C + (int64_t)m * ldc + n;
-          *cp = (beta != 0.f) ? (*cp + acc[rf][nf][r]) : acc[rf][nf][r];
+        for (int nf = 0; nf < 4; ++nf) {
+          const int n = nbase + nf * 16;
+          if (n < N) pz[(int64_t)m * N + n] = acc[rf][nf][r];
         }
       }
-    }
-}
-
-// One operand (rows x K, element (row, k) at src[row*srow + k*sk], one of the
-// strides 1) -> prepared copy at hi (and lo when split).
-void prep(const float* src, int rows, int K, int64_t srow, int64_t sk, bool split, uint16_t* hi, uint16_t* lo,
-          hipStream_t s) {
-  const int rows_p = (int)rup(rows, 128), Kp = (int)rup(K, BK);
-  if (sk == 1) {
-    const int64_t n = (int64_t)rows_p * (Kp / 8);
-    hipLaunchKernelGGL(k_prep_n, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src, rows, K, srow, hi,
-                       split ? lo : nullptr, rows_p, Kp);
   } else {
-    // src is [K][rows] with row stride sk: transpose into [rows][K]
-    hipLaunchKernelGGL(k_prep_t, dim3((unsigned)(Kp / 64), (unsigned)(rows_p / 64)), dim3(256), 0, s, src, K, rows,
-                       sk, hi, split ? lo : nullptr, Kp);
+    // with beta = 1, all the old values of C are read before any is written
+    if (beta != 0.f) {
+#pragma unroll
+      for (int rf = 0; rf < 4; ++rf)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = mb + rf * 16 + r;
+#pragma unroll
+          for (int nf = 0; nf < 4; ++nf) {
+            const int n = nbase + nf * 16;
+            if (m < M && n < N) acc[rf][nf][r] += C[(int64_t)m * ldc + n];
+          }
+        }
+    }
+#pragma unroll
+    for (int rf = 0; rf < 4; ++rf)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = mb + rf * 16 + r;
+        if (m >= M) continue;
+#pragma unroll
+        for (int nf = 0; nf < 4; ++nf) {
+          const int n = nbase + nf * 16;
+          if (n < N) C[(int64_t)m * ldc + n] = acc[rf][nf][r];
+        }
+      }
   }
 }
+
+// ---- 256 x 256 tiles, 512 threads (8 waves, two per SIMD), 32 k per stage ----
+// Twice the MFMA work per operand byte read of the 128 x 128 kernel, for the
+// large products.  Each wave owns a 64 x 128 block of C when A is split (its
+// rows are read twice from LDS, hi and lo) and a 128 x 64 block otherwise.
+namespace big {
+constexpr int TM = 256, TN = 256, TK = 32;
+constexpr int UNITS = TM * TK * 2 / 16;  // 16-byte units per 256 x 32 bf16 tile (1024)
+
+// LDS unit of (row, k-chunk c): 4 units per row, the chunk swizzled by bits
+// 2..3 of the row, so that 16 consecutive rows of one chunk hit distinct banks.
+__device__ __forceinline__ int unit_of(int row, int c) { return row * 4 + (c ^ ((row >> 2) & 3)); }
+
+// This thread's 16 values of the 256 x 32 tile (rows row0.., k k0..).  k
+// contiguous: units u = tid + 512 q (row u / 4, chunk u % 4), two float4
+// each.  Rows contiguous: rows 2 (tid % 128), +1 of chunk tid / 128, a float2
+// per k (v[j / 2] holds k = 2 (j / 2), +1).  Same clamping and mask as
+// load_tile.
+template <bool KC>
+__device__ __forceinline__ uint32_t load(const Src& s, int row0, int k0, int tid, float4 (&v)[4]) {
+  const bool seg1 = k0 >= s.k1p;
+  const float* __restrict__ p = seg1 ? s.p1 : s.p0;
+  const int ld = (int)(seg1 ? s.ld1 : s.ld0);
+  const int kk0 = seg1 ? k0 - s.k1p : k0, kr = (seg1 ? s.kext1 : s.kext0) - kk0;
+  uint32_t mask = 0;
+  auto at = [](const float* base, int off) { return reinterpret_cast<const char*>(base) + (uint32_t)off * 4u; };
+  if constexpr (KC) {
+    const float* base = p + (int64_t)row0 * ld + kk0;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int u = tid + 512 * q, rr = u >> 2, c8 = (u & 3) * 8;
+      const int ro = min(rr, s.rows - 1 - row0) * ld;
+      v[2 * q] = *reinterpret_cast<const float4*>(at(base, ro + min(c8, kr - 4)));
+      v[2 * q + 1] = *reinterpret_cast<const float4*>(at(base, ro + min(c8 + 4, kr - 4)));
+      const bool rin = row0 + rr < s.rows;
+      mask |= (uint32_t)(rin && c8 < kr) << (2 * q);
+      mask |= (uint32_t)(rin && c8 + 4 < kr) << (2 * q + 1);
+    }
+  } else {
+    const float* base = p + (int64_t)kk0 * ld + row0;
+    const int rr = 2 * (tid & 127), kc = (tid >> 7) * 8;
+    const bool rin = row0 + rr < s.rows;
+    const int ro = min(rr, s.rows - 2 - row0);
+#pragma unroll
+    for (int j = 0; j < 8; j += 2) {
+      const float2 a = *reinterpret_cast<const float2*>(at(base, min(kc + j, kr - 1) * ld + ro));
+      const float2 b = *reinterpret_cast<const float2*>(at(base, min(kc + j + 1, kr - 1) * ld + ro));
+      v[j >> 1] = make_float4(a.x, a.y, b.x, b.y);
+      mask |= (uint32_t)(rin && kc + j < kr) << j;
+      mask |= (uint32_t)(rin && kc + j + 1 < kr) << (j + 1);
+    }
+  }
+  return mask;
+}
+
+template <bool KC, bool SPLIT>
+__device__ __forceinline__ void store(const float4 (&v)[4], uint32_t mask, uint4* hi, uint4* lo, int tid) {
+  if constexpr (KC) {
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int u = tid + 512 * q, at = unit_of(u >> 2, u & 3);
+      const uint32_t m0 = 0u - ((mask >> (2 * q)) & 1u), m1 = 0u - ((mask >> (2 * q + 1)) & 1u);
+      float x[8] = {v[2 * q].x, v[2 * q].y, v[2 * q].z, v[2 * q].w,
+                    v[2 * q + 1].x, v[2 * q + 1].y, v[2 * q + 1].z, v[2 * q + 1].w};
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] = __uint_as_float(__float_as_uint(x[j]) & (j < 4 ? m0 : m1));
+      const uint4 h = make_uint4(pk_bf(x[0], x[1]), pk_bf(x[2], x[3]), pk_bf(x[4], x[5]), pk_bf(x[6], x[7]));
+      hi[at] = h;
+      if constexpr (SPLIT)
+        lo[at] = make_uint4(pk_lo(x[0], x[1], h.x), pk_lo(x[2], x[3], h.y), pk_lo(x[4], x[5], h.z),
+                            pk_lo(x[6], x[7], h.w));
+    }
+  } else {
+    const int rr = 2 * (tid & 127), c = tid >> 7;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int at = unit_of(rr + i, c);
+      float x[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float4& w = v[j >> 1];
+        const float val = (j & 1) ? (i ? w.w : w.z) : (i ? w.y : w.x);
+        x[j] = __uint_as_float(__float_as_uint(val) & (0u - ((mask >> j) & 1u)));
+      }
+      const uint4 h = make_uint4(pk_bf(x[0], x[1]), pk_bf(x[2], x[3]), pk_bf(x[4], x[5]), pk_bf(x[6], x[7]));
+      hi[at] = h;
+      if constexpr (SPLIT)
+        lo[at] = make_uint4(pk_lo(x[0], x[1], h.x), pk_lo(x[2], x[3], h.y), pk_lo(x[4], x[5], h.z),
+                            pk_lo(x[6], x[7], h.w));
+    }
+  }
+}
+
+template <bool AKC, bool BKC, bool SA, bool SB>
+__global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, int N, float* __restrict__ C,
+                                                   int64_t ldc, float beta, float* __restrict__ part, int kchunk, int tn,
+                                                   int tm) {
+  static_assert(!(SA && SB), "at most one operand is split");
+  constexpr int NT = 2 + (SA ? 1 : 0) + (SB ? 1 : 0);
+  constexpr int FM = SA ? 4 : 8, FN = SA ? 8 : 4;  // 16 x 16 fragments per wave along m, n
+  constexpr int WN = TN / (16 * FN);                // waves along n
+  __shared__ uint4 lds[2][NT][UNITS];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lg = lane >> 4, lc = lane & 15;
+  const int wm = wave / WN, wn = wave % WN;
+  const int nb = (int)gridDim.x, b = (int)blockIdx.x, per = nb / 8;
+  const int L = b < per * 8 ? (b & 7) * per + (b >> 3) : b;
+  const int bx = L % tn, by = (L / tn) % tm, bz = L / (tn * tm);
+  const int m0 = by * TM, n0 = bx * TN;
+  const int kb = bz * kchunk, ke = min(Kp, kb + kchunk);
+  f32x4 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float4 va[4], vb[4];
+  uint32_t ma = 0, mbk = 0;
+  auto put = [&](int buf) {
+    store<AKC, SA>(va, ma, lds[buf][0], lds[buf][SA ? 2 : 0], tid);
+    store<BKC, SB>(vb, mbk, lds[buf][1], lds[buf][NT - 1], tid);
+  };
+  if (kb < ke) {
+    ma = load<AKC>(A, m0, kb, tid, va);
+    mbk = load<BKC>(B, n0, kb, tid, vb);
+    put(0);
+  }
+  __syncthreads();
+  int buf = 0;
+  for (int k0 = kb; k0 < ke; k0 += TK, buf ^= 1) {
+    const bool more = k0 + TK < ke;
+    if (more) {
+      ma = load<AKC>(A, m0, k0 + TK, tid, va);
+      mbk = load<BKC>(B, n0, k0 + TK, tid, vb);
+    }
+    asm volatile("" ::: "memory");
+    uint4 af[FM], bf[FN];
+#pragma unroll
+    for (int rf = 0; rf < FM; ++rf) af[rf] = lds[buf][0][unit_of(wm * 16 * FM + rf * 16 + lc, lg)];
+#pragma unroll
+    for (int nf = 0; nf < FN; ++nf) bf[nf] = lds[buf][1][unit_of(wn * 16 * FN + nf * 16 + lc, lg)];
+#pragma unroll
+    for (int rf = 0; rf < FM; ++rf)
+#pragma unroll
+      for (int nf = 0; nf < FN; ++nf) Mma<true>::run(acc[rf][nf], af[rf], bf[nf]);
+    if constexpr (SA) {
+#pragma unroll
+      for (int rf = 0; rf < FM; ++rf) af[rf] = lds[buf][2][unit_of(wm * 16 * FM + rf * 16 + lc, lg)];
+#pragma unroll
+      for (int rf = 0; rf < FM; ++rf)
+#pragma unroll
+        for (int nf = 0; nf < FN; ++nf) Mma<true>::run(acc[rf][nf], af[rf], bf[nf]);
+    }
+    if constexpr (SB) {
+#pragma unroll
+      for (int nf = 0; nf < FN; ++nf) bf[nf] = lds[buf][NT - 1][unit_of(wn * 16 * FN + nf * 16 + lc, lg)];
+#pragma unroll
+      for (int rf = 0; rf < FM; ++rf)
+#pragma unroll
+        for (int nf = 0; nf < FN; ++nf) Mma<true>::run(acc[rf][nf], af[rf], bf[nf]);
+    }
+    asm volatile("" ::: "memory");
+    if (more) put(buf ^ 1);
+    __syncthreads();
+  }
+  const int mb = m0 + wm * 16 * FM + 4 * lg, nbase = n0 + wn * 16 * FN + lc;
+  if (part) {
+    float* pz = part + (int64_t)bz * M * N;
+#pragma unroll
+    for (int rf = 0; rf < FM; ++rf)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = mb + rf * 16 + r;
+        if (m >= M) continue;
+#pragma unroll
+        for (int nf = 0; nf < FN; ++nf) {
+          const int n = nbase + nf * 16;
+          if (n < N) pz[(int64_t)m * N + n] = acc[rf][nf][r];
+        }
+      }
+  } else {
+    if (beta != 0.f) {
+#pragma unroll
+      for (int rf = 0; rf < FM; ++rf)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int m = mb + rf * 16 + r;
+#pragma unroll
+          for (int nf = 0; nf < FN; ++nf) {
+            const int n = nbase + nf * 16;
+            if (m < M && n < N) acc[rf][nf][r] += C[(int64_t)m * ldc + n];
+          }
+        }
+    }
+#pragma unroll
+    for (int rf = 0; rf < FM; ++rf)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int m = mb + rf * 16 + r;
+        if (m >= M) continue;
+#pragma unroll
+        for (int nf = 0; nf < FN; ++nf) {
+          const int n = nbase + nf * 16;
+          if (n < N) C[(int64_t)m * ldc + n] = acc[rf][nf][r];
+        }
+      }
+  }
+}
+
+// split count of the 256-tile kernel (one block per CU): about 256 blocks,
+// each split keeping at least 1024 k values; 0 when the product cannot fill
+// the chip that way (shorter splits measured slower than the 128-tile kernel)
+int splits(int M, int N, int Kp) {
+  const int tiles = (int)(rup(M, TM) / TM * (rup(N, TN) / TN));
+  int s = 1;
+  while (tiles * s < 256 && Kp / (s * 2) >= 1024) s *= 2;
+  return tiles * s >= 256 ? s : 0;
+}
+
+template <bool AKC, bool BKC>
+void launch_orient(bool sa, bool sb, dim3 grid, const Src& A, const Src& B, int Kp, const GemmArgs& g, float* part,
+                   int kchunk, int tn, int tm, hipStream_t s) {
+  if (sa)
+    hipLaunchKernelGGL((k_bgemm_big<AKC, BKC, true, false>), grid, dim3(512), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
+                       g.beta, part, kchunk, tn, tm);
+  else if (sb)
+    hipLaunchKernelGGL((k_bgemm_big<AKC, BKC, false, true>), grid, dim3(512), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
+                       g.beta, part, kchunk, tn, tm);
+  else
+    hipLaunchKernelGGL((k_bgemm_big<AKC, BKC, false, false>), grid, dim3(512), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
+                       g.beta, part, kchunk, tn, tm);
+}
+}  // namespace big
 
 int bgemm_splits(int M, int N, int Kp) {
   const int tiles = (int)(rup(M, BM) / BM * (rup(N, BN) / BN));
   int splits = 1;
   // fill the 256 CUs about twice, each split keeping at least 512 k values
-  // (shorter splits measured slower: the partial sums cost more than they fill)
+  // (shorter splits cost more in partial sums than they gain in parallelism)
   while (tiles * splits < 512 && Kp / (splits * 2) >= 512) splits *= 2;
+  // products with few output tiles (weight gradients of narrow layers): fill
+  // the CUs once with splits down to 256 k values
+  while (tiles * splits < 256 && Kp / (splits * 2) >= 256) splits *= 2;
   return splits;
+}
+
+bool al16(const void* p) { return ((uintptr_t)p & 15) == 0; }
+
+// Operand (rows x K, element (row, k) at p[row*srow + k*sk]) as segment seg of
+// src; false when the kernel's float4 reads do not fit it.
+bool add_segment(Src& src, int seg, const float* p, int64_t srow, int64_t sk, int rows, int K, bool& kc) {
+  const bool this_kc = sk == 1;
+  if (!(this_kc || srow == 1)) return false;
+  const int64_t ld = this_kc ? srow : sk;
+  if (!al16(p) || ld % 4 != 0 || (this_kc ? K % 4 : rows % 4) != 0) return false;
+  if (ld > (1 << 20)) return false;  // byte offsets within a 128 x 64 tile stay below 2^31
+  if (seg == 1 && this_kc != kc) return false;
+  kc = this_kc;
+  (seg ? src.p1 : src.p0) = p;
+  (seg ? src.ld1 : src.ld0) = ld;
+  (seg ? src.kext1 : src.kext0) = K;
+  src.rows = rows;
+  return true;
+}
+
+template <bool AKC, bool BKC>
+void launch_orient(bool sa, bool sb, dim3 grid, const Src& A, const Src& B, int Kp, const GemmArgs& g, float* part,
+                   int kchunk, int tn, int tm, hipStream_t s) {
+  if (sa)
+    hipLaunchKernelGGL((k_bgemm<AKC, BKC, true, false>), grid, dim3(256), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
+                       g.beta, part, kchunk, tn, tm);
+  else if (sb)
+    hipLaunchKernelGGL((k_bgemm<AKC, BKC, false, true>), grid, dim3(256), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
+                       g.beta, part, kchunk, tn, tm);
+  else
+    hipLaunchKernelGGL((k_bgemm<AKC, BKC, false, false>), grid, dim3(256), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
+                       g.beta, part, kchunk, tn, tm);
 }
 
 }  // namespace
 
-int64_t bgemm_prep_bytes(int M, int N, int K) {
-  const int64_t Kp = rup(K, BK);
-  return 2 * (rup(M, BM) * Kp * 2) + 2 * (rup(N, BN) * Kp * 2) + 256;
-}
 int64_t bgemm_ws_floats(int M, int N, int K) {
-  const int s = bgemm_splits(M, N, (int)rup(K, BK));
+  const int s = std::max(bgemm_splits(M, N, (int)rup(K, BK)), big::splits(M, N, (int)rup(K, big::TK)));
   return s > 1 ? (int64_t)s * M * N : 0;
 }
 
-bool launch_bgemm(const GemmArgs& g, float* ws, int64_t ws_cap, void* prep_buf, int64_t prep_cap, hipStream_t s) {
+bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_cap, hipStream_t s) {
   if (!g.roundA && !g.roundB) return false;  // fp32 operands on both sides: not this kernel
-  if (!((g.sak == 1 || g.sam == 1) && (g.sbk == 1 || g.sbn == 1))) return false;
-  if (!prep_buf || bgemm_prep_bytes(g.M, g.N, g.K) > prep_cap) return false;
+  if (g2 && (g2->M != g.M || g2->N != g.N || g2->roundA != g.roundA || g2->roundB != g.roundB)) return false;
+  Src A{}, B{};
+  bool akc = false, bkc = false;
+  if (!add_segment(A, 0, g.A, g.sam, g.sak, g.M, g.K, akc)) return false;
+  if (!add_segment(B, 0, g.B, g.sbn, g.sbk, g.N, g.K, bkc)) return false;
+  if (g2) {
+    if (!add_segment(A, 1, g2->A, g2->sam, g2->sak, g.M, g2->K, akc)) return false;
+    if (!add_segment(B, 1, g2->B, g2->sbn, g2->sbk, g.N, g2->K, bkc)) return false;
+  } else {
+    A.p1 = A.p0;
+    A.ld1 = A.ld0;
+    B.p1 = B.p0;
+    B.ld1 = B.ld0;
+  }
+  const int K0 = g.K, K1 = g2 ? g2->K : 0;
+  if (K0 + K1 == 0) return false;
   const bool sa = !g.roundA, sb = !g.roundB;
-  const int Kp = (int)rup(g.K, BK);
-  const int64_t asz = rup(g.M, BM) * Kp, bsz = rup(g.N, BN) * Kp;  // elements per part
-  uint16_t* p = (uint16_t*)prep_buf;
-  uint16_t *Ah = p, *Al = p + asz, *Bh = p + 2 * asz, *Bl = p + 2 * asz + bsz;
-  // A(m, k) = A[m*sam + k*sak]; B(k, n) = B[k*sbk + n*sbn] is row n of B^T
-  prep(g.A, g.M, g.K, g.sak == 1 ? g.sam : 1, g.sak == 1 ? 1 : g.sak, sa, Ah, Al, s);
-  prep(g.B, g.N, g.K, g.sbk == 1 ? g.sbn : 1, g.sbk == 1 ? 1 : g.sbk, sb, Bh, Bl, s);
-  int splits = bgemm_splits(g.M, g.N, Kp);
+  // the 256-tile kernel when it fills the chip, else the 128-tile one; stages
+  // are aligned to each kernel's k step, and so is the start of segment 1
+  const int kpb = (int)(rup(K0, big::TK) + rup(K1, big::TK));
+  int splits = big::splits(g.M, g.N, kpb);
+  const bool use_big = splits > 0;
+  const int step = use_big ? big::TK : BK;
+  A.k1p = B.k1p = (int)rup(K0, step);
+  const int Kp = (int)(rup(K0, step) + rup(K1, step));
+  if (!use_big) splits = bgemm_splits(g.M, g.N, Kp);
   while (splits > 1 && (int64_t)splits * g.M * g.N > ws_cap) splits /= 2;
-  const int kchunk = (int)rup((Kp + splits - 1) / splits, BK);
+  const int kchunk = (int)rup((Kp + splits - 1) / splits, step);
+  splits = (Kp + kchunk - 1) / kchunk;
   float* part = splits > 1 ? ws : nullptr;
-  const dim3 grid((unsigned)(rup(g.N, BN) / BN), (unsigned)(rup(g.M, BM) / BM), (unsigned)splits);
-  if (sa)
-    hipLaunchKernelGGL((k_bgemm<true, false>), grid, dim3(256), 0, s, Ah, Al, Bh, Bl, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk);
-  else if (sb)
-    hipLaunchKernelGGL((k_bgemm<false, true>), grid, dim3(256), 0, s, Ah, Al, Bh, Bl, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk);
-  else
-    hipLaunchKernelGGL((k_bgemm<false, false>), grid, dim3(256), 0, s, Ah, Al, Bh, Bl, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk);
+  const int TMk = use_big ? big::TM : BM, TNk = use_big ? big::TN : BN;
+  const int tn = (int)(rup(g.N, TNk) / TNk), tm = (int)(rup(g.M, TMk) / TMk);
+  const dim3 grid((unsigned)(tn * tm * splits));
+  if (use_big) {
+    if (akc && bkc)
+      big::launch_orient<true, true>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+    else if (akc)
+      big::launch_orient<true, false>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+    else if (bkc)
+      big::launch_orient<false, true>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+    else
+      big::launch_orient<false, false>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+  } else {
+    if (akc && bkc)
+      launch_orient<true, true>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+    else if (akc)
+      launch_orient<true, false>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+    else if (bkc)
+      launch_orient<false, true>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+    else
+      launch_orient<false, false>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+  }
   if (splits > 1) launch_splitk_reduce(ws, splits, g.M, g.N, g.C, g.ldc, g.beta, s);
   return true;
 }

@@ -321,16 +321,58 @@ static void launch128(const GemmArgs& g, float* part, int kchunk, dim3 grid, hip
     hipLaunchKernelGGL((k_gemm128<MODE, false, false>), grid, dim3(256), 0, s, g, part, kchunk);
 }
 
-void launch_splitk_reduce(const float* ws, int splits, int M, int N, float* C, int64_t ldc, float beta, hipStream_t s) {
-  const int64_t tot = (int64_t)M * N;
-  hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, ws, splits, M, N, C, ldc,
-                     beta);
+// Four consecutive n per thread, eight partials in flight; the same sum order
+// (z increasing) as k_splitk_reduce.
+__global__ __launch_bounds__(256) void k_splitk_reduce4(const float* __restrict__ part, int splits, int M, int N,
+                                                        float* C, int64_t ldc, float beta) {
+  const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+  const int64_t MN = (int64_t)M * N;
+  if (i >= MN) return;
+  const int m = (int)(i / N), n = (int)(i % N);
+  const float* p = part + i;
+  float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
+  auto add = [&](const float4& v) {
+    s.x += v.x;
+    s.y += v.y;
+    s.z += v.z;
+    s.w += v.w;
+  };
+  int z = 0;
+  for (; z + 8 <= splits; z += 8) {
+    float4 v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = *reinterpret_cast<const float4*>(p + (int64_t)(z + j) * MN);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) add(v[j]);
+  }
+  for (; z < splits; ++z) add(*reinterpret_cast<const float4*>(p + (int64_t)z * MN));
+  float* c = C + (int64_t)m * ldc + n;
+  if (beta != 0.f) {
+    s.x += c[0];
+    s.y += c[1];
+    s.z += c[2];
+    s.w += c[3];
+  }
+  c[0] = s.x;
+  c[1] = s.y;
+  c[2] = s.z;
+  c[3] = s.w;
 }
 
-void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, void* prep, int64_t prep_cap, hipStream_t s) {
+void launch_splitk_reduce(const float* ws, int splits, int M, int N, float* C, int64_t ldc, float beta, hipStream_t s) {
+  const int64_t tot = (int64_t)M * N;
+  if (N % 4 == 0 && ((uintptr_t)ws & 15) == 0)
+    hipLaunchKernelGGL(k_splitk_reduce4, dim3((unsigned)((tot / 4 + 255) / 256)), dim3(256), 0, s, ws, splits, M, N, C,
+                       ldc, beta);
+  else
+    hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, ws, splits, M, N, C, ldc,
+                       beta);
+}
+
+void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return;
-  // bf16 storage points on at least one side: prepared-operand bf16 GEMM
-  if (launch_bgemm(g, ws, ws_cap, prep, prep_cap, s)) return;
+  // bf16 storage points on at least one side: register-staged bf16 GEMM
+  if (launch_bgemm(g, nullptr, ws, ws_cap, s)) return;
   int splits = gemm_splits(g.M, g.N, g.K);
   while (splits > 1 && (int64_t)splits * g.M * g.N > ws_cap) splits /= 2;
   int kchunk = (g.K + splits - 1) / splits;
@@ -359,6 +401,17 @@ void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, void* prep, int64
   if (splits > 1) launch_splitk_reduce(ws, splits, g.M, g.N, g.C, g.ldc, g.beta, s);
 }
 
+void launch_gemm2(const GemmArgs& g, const GemmArgs& g2, float* ws, int64_t ws_cap, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return;
+  if (launch_bgemm(g, &g2, ws, ws_cap, s)) return;
+  launch_gemm(g, ws, ws_cap, s);
+  GemmArgs h = g2;
+  h.C = g.C;
+  h.ldc = g.ldc;
+  h.beta = 1.f;
+  launch_gemm(h, ws, ws_cap, s);
+}
+
 // ------------------------------------------------------------- column sums ----
 constexpr int COLSUM_SPLITS = 64;
 __global__ void k_colsum1(const float* __restrict__ in, int64_t rows, int64_t cols, int64_t ld, float* __restrict__ ws) {
@@ -378,11 +431,40 @@ __global__ void k_colsum2(const float* __restrict__ ws, int64_t cols, float* out
   for (int s = 0; s < COLSUM_SPLITS; ++s) acc += ws[s * cols + c];
   out[c] = (beta != 0.f) ? out[c] + acc : acc;
 }
+// four columns per thread, eight rows in flight; the same sum order as k_colsum1
+__global__ __launch_bounds__(64) void k_colsum1v(const float* __restrict__ in, int64_t rows, int64_t cols, int64_t ld,
+                                                 float* __restrict__ ws) {
+  const int64_t c = ((int64_t)blockIdx.x * 64 + threadIdx.x) * 4;
+  if (c >= cols) return;
+  const int s = blockIdx.y;
+  const int64_t chunk = (rows + COLSUM_SPLITS - 1) / COLSUM_SPLITS;
+  const int64_t r0 = s * chunk, r1 = min(rows, r0 + chunk);
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  auto add = [&](const float4& v) {
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  };
+  int64_t r = r0;
+  for (; r + 8 <= r1; r += 8) {
+    float4 v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = *reinterpret_cast<const float4*>(in + (r + j) * ld + c);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) add(v[j]);
+  }
+  for (; r < r1; ++r) add(*reinterpret_cast<const float4*>(in + r * ld + c));
+  *reinterpret_cast<float4*>(ws + s * cols + c) = acc;
+}
 int64_t colsum_ws_floats(int64_t cols) { return COLSUM_SPLITS * cols; }
 void launch_colsum(const float* in, int64_t rows, int64_t cols, int64_t ld, float* out, float beta, float* ws,
                    hipStream_t s) {
   const unsigned gx = (unsigned)((cols + 255) / 256);
-  hipLaunchKernelGGL(k_colsum1, dim3(gx, COLSUM_SPLITS), dim3(256), 0, s, in, rows, cols, ld, ws);
+  if (cols % 4 == 0 && ld % 4 == 0 && ((uintptr_t)in & 15) == 0)
+    hipLaunchKernelGGL(k_colsum1v, dim3(gx, COLSUM_SPLITS), dim3(64), 0, s, in, rows, cols, ld, ws);
+  else
+    hipLaunchKernelGGL(k_colsum1, dim3(gx, COLSUM_SPLITS), dim3(256), 0, s, in, rows, cols, ld, ws);
   hipLaunchKernelGGL(k_colsum2, dim3(gx), dim3(256), 0, s, ws, cols, out, beta);
 }
 

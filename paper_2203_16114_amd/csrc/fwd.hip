@@ -55,32 +55,44 @@ void launch_pack(bool bf, const float* W, int K, int N, void* out, hipStream_t s
 }
 
 // Positional parts of the projections: PW[w][t][j] = sum_i P[t][i] W_w[i][j] for
-// w = q, k, v, in fp32 over i in increasing order, from the operand values of P
+// w = q, k, v, in fp32 (eight partial sums over consecutive eighths of i, added in
+// order), from the operand values of P
 // and of the weights (bf16-rounded in BF16 mode).  A token's projection is then
 // E-part (an MFMA on the rounded byte embeddings) + PW[w][t]: X.W = E.W + P.W.
 template <bool BF>
-__global__ void k_ptab(const typename Mma<BF>::T* __restrict__ P, const float* __restrict__ Wq,
-                       const float* __restrict__ Wk, const float* __restrict__ Wv, int T, int D,
-                       float* __restrict__ PW) {
+__global__ __launch_bounds__(512) void k_ptab(const typename Mma<BF>::T* __restrict__ P, const float* __restrict__ Wq,
+                                              const float* __restrict__ Wk, const float* __restrict__ Wv, int T, int D,
+                                              float* __restrict__ PW) {
+  // block (w*T + t, j-block): 64 columns j; its 8 waves sum over the 8 eighths of
+  // k, and the 8 partial sums are added in k order
   typedef Mma<BF> M;
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= (int64_t)3 * T * D) return;
-  const int j = (int)(i % D), t = (int)((i / D) % T), w = (int)(i / ((int64_t)T * D));
+  __shared__ float part[8][64];
+  const int wt = blockIdx.x, w = wt / T, t = wt - w * T;
+  const int j = blockIdx.y * 64 + (threadIdx.x & 63), kg = threadIdx.x >> 6;
   const float* Wm = w == 0 ? Wq : (w == 1 ? Wk : Wv);
+  const int kl = D / 8, k0 = kg * kl;
   float s = 0.f;
-#pragma unroll 8
-  for (int k = 0; k < D; ++k) s = fmaf(M::val(P[t * D + k]), M::val(M::cvt(Wm[(int64_t)k * D + j])), s);
-  PW[i] = s;
+  if (j < D) {
+#pragma unroll 4
+    for (int k = k0; k < k0 + kl; ++k) s = fmaf(M::val(P[t * D + k]), M::val(M::cvt(Wm[(int64_t)k * D + j])), s);
+  }
+  part[kg][threadIdx.x & 63] = s;
+  __syncthreads();
+  if (kg == 0 && j < D) {
+    float r = part[0][threadIdx.x];
+#pragma unroll
+    for (int q = 1; q < 8; ++q) r += part[q][threadIdx.x];
+    PW[(int64_t)wt * D + j] = r;
+  }
 }
 
 void launch_ptab(bool bf, const void* P, const float* Wq, const float* Wk, const float* Wv, int T, int D, float* PW,
                  hipStream_t s) {
-  const int64_t total = (int64_t)3 * T * D;
-  const dim3 grid((unsigned)((total + 255) / 256));
+  const dim3 grid((unsigned)(3 * T), (unsigned)((D + 63) / 64));
   if (bf)
-    hipLaunchKernelGGL(k_ptab<true>, grid, dim3(256), 0, s, (const uint16_t*)P, Wq, Wk, Wv, T, D, PW);
+    hipLaunchKernelGGL(k_ptab<true>, grid, dim3(512), 0, s, (const uint16_t*)P, Wq, Wk, Wv, T, D, PW);
   else
-    hipLaunchKernelGGL(k_ptab<false>, grid, dim3(256), 0, s, (const float*)P, Wq, Wk, Wv, T, D, PW);
+    hipLaunchKernelGGL(k_ptab<false>, grid, dim3(512), 0, s, (const float*)P, Wq, Wk, Wv, T, D, PW);
 }
 
 template <bool BF>

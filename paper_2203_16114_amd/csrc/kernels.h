@@ -78,13 +78,14 @@ struct GemmArgs {
 // depends only on (M, N, K, ws_cap); gemm_ws_floats(M, N, K) floats let it
 // reach its preferred value.
 int64_t gemm_ws_floats(int M, int N, int K);
-// prep (nullable, prep_cap bytes): room for the bf16 operand copies of the
-// prepared-operand GEMM (bgemm.hip), used when it holds bgemm_prep_bytes(M, N, K)
-void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, void* prep, int64_t prep_cap, hipStream_t s);
+void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s);
+// C = beta*C + A1.B1 + A2.B2: g and g2 share M, N, C, ldc, beta and rounding
+// flags; one launch when the bf16 kernel takes both, else two
+void launch_gemm2(const GemmArgs& g, const GemmArgs& g2, float* ws, int64_t ws_cap, hipStream_t s);
 void launch_splitk_reduce(const float* ws, int splits, int M, int N, float* C, int64_t ldc, float beta, hipStream_t s);
-// bgemm.hip: false (nothing launched) when the product is not one it takes
-bool launch_bgemm(const GemmArgs& g, float* ws, int64_t ws_cap, void* prep, int64_t prep_cap, hipStream_t s);
-int64_t bgemm_prep_bytes(int M, int N, int K);
+// bgemm.hip: false (nothing launched) when the product is not one it takes;
+// g2 (nullable) is a second K segment summed into the same result
+bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_cap, hipStream_t s);
 int64_t bgemm_ws_floats(int M, int N, int K);
 
 void launch_colsum(const float* in, int64_t rows, int64_t cols, int64_t ld, float* out, float beta, float* ws,
