@@ -35,9 +35,9 @@ struct trace_model {
   int64_t keepN;
   uint8_t* kwin;
   int32_t* ktgt;
-  float *kq, *kK, *kV, *kA, *kO, *kY, *kU, *kZ;
+  float *kq, *kK, *kV, *kA, *kO, *kY, *kU, *kG, *kZ;
   // backward scratch
-  float *dz, *dY, *dG, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *sP, *gws, *cws, *ews;
+  float *dz, *dY, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *sP, *gws, *cws, *ews;
   int64_t gws_cap;
   std::vector<void*> allocs;
   // event timing (trace_set_timing)
@@ -162,6 +162,7 @@ GemmArgs gemm(int M, int N, int K, const float* A, int64_t sam, int64_t sak, int
   g.roundA = rA;
   g.roundB = rB;
   g.beta = beta;
+  g.gelu_u = nullptr;
   return g;
 }
 
@@ -206,8 +207,9 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
          dalloc(m, &m->kK, K * T * D * 4) && dalloc(m, &m->kV, K * T * D * 4) &&
          dalloc(m, &m->kA, K * cfg->H * T * 4) && dalloc(m, &m->kO, K * D * 4) &&
          dalloc(m, &m->kY, (cfg->k + 1) * K * D * 4) && dalloc(m, &m->kU, cfg->k * K * F * 4) &&
+         (!bf || dalloc(m, &m->kG, cfg->k * K * F * 4)) &&
          dalloc(m, &m->kZ, K * 256 * 4) && dalloc(m, &m->dz, K * 256 * 4) && dalloc(m, &m->dY, K * D * 4) &&
-         dalloc(m, &m->dG, K * F * 4) && dalloc(m, &m->dU, K * F * 4) && dalloc(m, &m->G, K * F * 4) &&
+         dalloc(m, &m->dU, K * F * 4) && (bf || dalloc(m, &m->G, K * F * 4)) &&
          dalloc(m, &m->dO, K * D * 4) && dalloc(m, &m->dQ, K * D * 4) && dalloc(m, &m->dK, K * T * D * 4) &&
          dalloc(m, &m->dV, K * T * D * 4) && dalloc(m, &m->dX, K * T * D * 4) && dalloc(m, &m->Xk, K * T * D * 4) &&
          dalloc(m, &m->sP, T * D * 4) &&
@@ -336,6 +338,7 @@ extern "C" int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int6
       a.kO = m->kO;
       f.kY = m->kY;
       f.kU = m->kU;
+      f.kG = m->kG;
       f.kZ = m->kZ;
       f.ktgt = m->ktgt;
     }
@@ -381,12 +384,16 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // shared FFN, repeats in reverse; W1 and W2 gradients accumulate over repeats
   for (int r = k - 1; r >= 0; --r) {
     const float* Ur = m->kU + (int64_t)r * N * F;
+    // G = GELU(U) at its storage point: kept by the bf16 forward, formed here otherwise
+    const float* Gr = m->kG ? m->kG + (int64_t)r * N * F : m->G;
     const float* Yr = m->kY + (int64_t)r * N * D;
     const float beta = (r == k - 1) ? 0.f : 1.f;
-    launch_gelu_fwd_round(Ur, m->G, (int64_t)N * F, rb, s);
-    launch_gemm(gemm(F, D, N, m->G, 1, F, rb, m->dY, D, 1, rb, gr + L.off[P_W2], D, beta), ws, m->gws_cap, s);
-    launch_gemm(gemm(N, F, D, m->dY, D, 1, rb, th + L.off[P_W2], 1, D, rb, m->dG, F, 0.f), ws, m->gws_cap, s);
-    launch_gelu_bwd(m->dG, Ur, m->dU, (int64_t)N * F, s);
+    if (!m->kG) launch_gelu_fwd_round(Ur, m->G, (int64_t)N * F, rb, s);
+    launch_gemm(gemm(F, D, N, Gr, 1, F, rb, m->dY, D, 1, rb, gr + L.off[P_W2], D, beta), ws, m->gws_cap, s);
+    // dU = (dY . W2^T) * GELU'(U)
+    GemmArgs gd = gemm(N, F, D, m->dY, D, 1, rb, th + L.off[P_W2], 1, D, rb, m->dU, F, 0.f);
+    gd.gelu_u = Ur;
+    launch_gemm(gd, ws, m->gws_cap, s);
     launch_gemm(gemm(D, F, N, Yr, 1, D, rb, m->dU, F, 1, rb, gr + L.off[P_W1], F, beta), ws, m->gws_cap, s);
     launch_gemm(gemm(N, D, F, m->dU, F, 1, rb, th + L.off[P_W1], 1, F, rb, m->dY, D, 1.f), ws, m->gws_cap, s);
   }

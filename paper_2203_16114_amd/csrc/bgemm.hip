@@ -146,7 +146,8 @@ __device__ __forceinline__ void store_tile(const float4 (&vin)[8], uint32_t mask
 // 1-D grid of tn * tm * splits blocks.
 template <bool AKC, bool BKC, bool SA, bool SB>
 __global__ __launch_bounds__(256) void k_bgemm(Src A, Src B, int Kp, int M, int N, float* __restrict__ C, int64_t ldc,
-                                               float beta, float* __restrict__ part, int kchunk, int tn, int tm) {
+                                               float beta, float* __restrict__ part, int kchunk, int tn, int tm,
+                                               const float* __restrict__ gu) {
   static_assert(!(SA && SB), "at most one operand is split");
   constexpr int NT = 2 + (SA ? 1 : 0) + (SB ? 1 : 0);  // tiles per stage: A hi, B hi, [A lo | B lo]
   __shared__ uint4 lds[2][NT][UNITS];
@@ -238,18 +239,39 @@ __global__ __launch_bounds__(256) void k_bgemm(Src A, Src B, int Kp, int M, int 
       }
   } else {
     // with beta = 1, all the old values of C are read before any is written
-    if (beta != 0.f) {
+    if (beta != 0.f) {  // clamped addresses, as for gu below
 #pragma unroll
-      for (int rf = 0; rf < 4; ++rf)
+      for (int rf = 0; rf < 4; ++rf) {
+        float c[4][4];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int m = mb + rf * 16 + r;
+          const int64_t mo = (int64_t)min(mb + rf * 16 + r, M - 1) * ldc;
 #pragma unroll
-          for (int nf = 0; nf < 4; ++nf) {
-            const int n = nbase + nf * 16;
-            if (m < M && n < N) acc[rf][nf][r] += C[(int64_t)m * ldc + n];
-          }
+          for (int nf = 0; nf < 4; ++nf) c[r][nf] = C[mo + min(nbase + nf * 16, N - 1)];
         }
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int nf = 0; nf < 4; ++nf) acc[rf][nf][r] += c[r][nf];
+      }
+    }
+    if (gu) {  // C = (A.B) * GELU'(U), U laid out as C
+      // loads from clamped addresses, all of a fragment row before any use
+      // (elements outside C are computed but not stored)
+#pragma unroll
+      for (int rf = 0; rf < 4; ++rf) {
+        float u[4][4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t mo = (int64_t)min(mb + rf * 16 + r, M - 1) * ldc;
+#pragma unroll
+          for (int nf = 0; nf < 4; ++nf) u[r][nf] = gu[mo + min(nbase + nf * 16, N - 1)];
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int nf = 0; nf < 4; ++nf) acc[rf][nf][r] *= gelu_grad_as(u[r][nf]);
+      }
     }
 #pragma unroll
     for (int rf = 0; rf < 4; ++rf)
@@ -361,7 +383,7 @@ __device__ __forceinline__ void store(const float4 (&v)[4], uint32_t mask, uint4
 template <bool AKC, bool BKC, bool SA, bool SB>
 __global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, int N, float* __restrict__ C,
                                                    int64_t ldc, float beta, float* __restrict__ part, int kchunk, int tn,
-                                                   int tm) {
+                                                   int tm, const float* __restrict__ gu) {
   static_assert(!(SA && SB), "at most one operand is split");
   constexpr int NT = 2 + (SA ? 1 : 0) + (SB ? 1 : 0);
   constexpr int FM = SA ? 4 : 8, FN = SA ? 8 : 4;  // 16 x 16 fragments per wave along m, n
@@ -444,18 +466,39 @@ __global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, 
         }
       }
   } else {
-    if (beta != 0.f) {
+    if (beta != 0.f) {  // clamped addresses, as for gu below
 #pragma unroll
-      for (int rf = 0; rf < FM; ++rf)
+      for (int rf = 0; rf < FM; ++rf) {
+        float c[4][FN];
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          const int m = mb + rf * 16 + r;
+          const int64_t mo = (int64_t)min(mb + rf * 16 + r, M - 1) * ldc;
 #pragma unroll
-          for (int nf = 0; nf < FN; ++nf) {
-            const int n = nbase + nf * 16;
-            if (m < M && n < N) acc[rf][nf][r] += C[(int64_t)m * ldc + n];
-          }
+          for (int nf = 0; nf < FN; ++nf) c[r][nf] = C[mo + min(nbase + nf * 16, N - 1)];
         }
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int nf = 0; nf < FN; ++nf) acc[rf][nf][r] += c[r][nf];
+      }
+    }
+    if (gu) {  // C = (A.B) * GELU'(U), U laid out as C
+      // loads from clamped addresses, all of a fragment row before any use
+      // (elements outside C are computed but not stored)
+#pragma unroll
+      for (int rf = 0; rf < FM; ++rf) {
+        float u[4][FN];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t mo = (int64_t)min(mb + rf * 16 + r, M - 1) * ldc;
+#pragma unroll
+          for (int nf = 0; nf < FN; ++nf) u[r][nf] = gu[mo + min(nbase + nf * 16, N - 1)];
+        }
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int nf = 0; nf < FN; ++nf) acc[rf][nf][r] *= gelu_grad_as(u[r][nf]);
+      }
     }
 #pragma unroll
     for (int rf = 0; rf < FM; ++rf)
@@ -487,13 +530,13 @@ void launch_orient(bool sa, bool sb, dim3 grid, const Src& A, const Src& B, int 
                    int kchunk, int tn, int tm, hipStream_t s) {
   if (sa)
     hipLaunchKernelGGL((k_bgemm_big<AKC, BKC, true, false>), grid, dim3(512), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk, tn, tm);
+                       g.beta, part, kchunk, tn, tm, g.gelu_u);
   else if (sb)
     hipLaunchKernelGGL((k_bgemm_big<AKC, BKC, false, true>), grid, dim3(512), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk, tn, tm);
+                       g.beta, part, kchunk, tn, tm, g.gelu_u);
   else
     hipLaunchKernelGGL((k_bgemm_big<AKC, BKC, false, false>), grid, dim3(512), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk, tn, tm);
+                       g.beta, part, kchunk, tn, tm, g.gelu_u);
 }
 }  // namespace big
 
@@ -533,13 +576,13 @@ void launch_orient(bool sa, bool sb, dim3 grid, const Src& A, const Src& B, int 
                    int kchunk, int tn, int tm, hipStream_t s) {
   if (sa)
     hipLaunchKernelGGL((k_bgemm<AKC, BKC, true, false>), grid, dim3(256), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk, tn, tm);
+                       g.beta, part, kchunk, tn, tm, g.gelu_u);
   else if (sb)
     hipLaunchKernelGGL((k_bgemm<AKC, BKC, false, true>), grid, dim3(256), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk, tn, tm);
+                       g.beta, part, kchunk, tn, tm, g.gelu_u);
   else
     hipLaunchKernelGGL((k_bgemm<AKC, BKC, false, false>), grid, dim3(256), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk, tn, tm);
+                       g.beta, part, kchunk, tn, tm, g.gelu_u);
 }
 
 }  // namespace
@@ -567,6 +610,7 @@ bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_c
   }
   const int K0 = g.K, K1 = g2 ? g2->K : 0;
   if (K0 + K1 == 0) return false;
+  if (g.gelu_u && (g.beta != 0.f || g2)) return false;
   const bool sa = !g.roundA, sb = !g.roundB;
   // the 256-tile kernel when it fills the chip, else the 128-tile one; stages
   // are aligned to each kernel's k step, and so is the start of segment 1
@@ -578,6 +622,7 @@ bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_c
   const int Kp = (int)(rup(K0, step) + rup(K1, step));
   if (!use_big) splits = bgemm_splits(g.M, g.N, Kp);
   while (splits > 1 && (int64_t)splits * g.M * g.N > ws_cap) splits /= 2;
+  if (g.gelu_u) splits = 1;  // the epilogue needs the whole sum
   const int kchunk = (int)rup((Kp + splits - 1) / splits, step);
   splits = (Kp + kchunk - 1) / kchunk;
   float* part = splits > 1 ? ws : nullptr;

@@ -373,6 +373,13 @@ void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return;
   // bf16 storage points on at least one side: register-staged bf16 GEMM
   if (launch_bgemm(g, nullptr, ws, ws_cap, s)) return;
+  if (g.gelu_u) {  // the product, then the GELU derivative in place (C laid out densely, as gelu_u)
+    GemmArgs h = g;
+    h.gelu_u = nullptr;
+    launch_gemm(h, ws, ws_cap, s);
+    launch_gelu_bwd(g.C, g.gelu_u, g.C, (int64_t)g.M * g.N, s);
+    return;
+  }
   int splits = gemm_splits(g.M, g.N, g.K);
   while (splits > 1 && (int64_t)splits * g.M * g.N > ws_cap) splits /= 2;
   int kchunk = (g.K + splits - 1) / splits;
@@ -413,7 +420,7 @@ void launch_gemm2(const GemmArgs& g, const GemmArgs& g2, float* ws, int64_t ws_c
 }
 
 // ------------------------------------------------------------- column sums ----
-constexpr int COLSUM_SPLITS = 64;
+constexpr int COLSUM_SPLITS = 128;
 __global__ void k_colsum1(const float* __restrict__ in, int64_t rows, int64_t cols, int64_t ld, float* __restrict__ ws) {
   const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (c >= cols) return;
@@ -428,6 +435,7 @@ __global__ void k_colsum2(const float* __restrict__ ws, int64_t cols, float* out
   const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (c >= cols) return;
   float acc = 0.f;
+#pragma unroll 16
   for (int s = 0; s < COLSUM_SPLITS; ++s) acc += ws[s * cols + c];
   out[c] = (beta != 0.f) ? out[c] + acc : acc;
 }
@@ -511,7 +519,8 @@ __global__ void k_gelu_fwd_round(const float* __restrict__ U, float* __restrict_
 void launch_gelu_fwd_round(const float* U, float* G, int64_t n, int round, hipStream_t s) {
   hipLaunchKernelGGL(k_gelu_fwd_round, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, U, G, n, round);
 }
-__global__ void k_gelu_bwd(const float* __restrict__ dG, const float* __restrict__ U, float* __restrict__ dU, int64_t n) {
+// (dU may be dG: each element is read before it is written, by one thread)
+__global__ void k_gelu_bwd(const float* dG, const float* __restrict__ U, float* dU, int64_t n) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= n) return;
   dU[i] = dG[i] * gelu_grad_f(U[i]);

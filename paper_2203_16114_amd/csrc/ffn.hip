@@ -494,6 +494,22 @@ __global__ __launch_bounds__(512) void k_ffn_pipe(FfnArgs a) {
     }
   };
 
+  // GELU of the chunk at feature c (held doubled after its interval), kept as
+  // the bf16 operand values the second product used
+  auto keep_g = [&](const f32x4 (&g)[RF1][NFC], int rep, int c) {
+#pragma unroll
+    for (int nf = 0; nf < NFC; ++nf) {
+      const int64_t n = tile0 + m0 + nf * 16 + lc;
+      if (n < N) {
+#pragma unroll
+        for (int rf = 0; rf < RF1; ++rf)
+          *reinterpret_cast<float4*>(a.kG + ((int64_t)rep * N + n) * F + c + L.f0 + rf * 16 + 4 * lg) =
+              make_float4(0.5f * round_bf(g[rf][nf][0]), 0.5f * round_bf(g[rf][nf][1]),
+                          0.5f * round_bf(g[rf][nf][2]), 0.5f * round_bf(g[rf][nf][3]));
+      }
+    }
+  };
+
   for (int rep = 0; rep <= a.k; ++rep) {
 #pragma unroll
     for (int nf = 0; nf < NFC; ++nf) {
@@ -515,20 +531,24 @@ __global__ __launch_bounds__(512) void k_ffn_pipe(FfnArgs a) {
     if (KEEP) keep_u(ua, rep, 0);
     // j = 0: GELU(0) -> buffer 0, GEMM1(1) -> ub
     ffn_interval<D, MB, false, true, true>(L, y, ua, ub, FC, 0, gr0, gw0);
+    if (KEEP) keep_g(ua, rep, 0);
     __syncthreads();
     for (int j = 1; j < NC - 1; j += 2) {
       if (KEEP) keep_u(ub, rep, j * FC);
       // j (odd): GELU(j) -> buffer 1, GEMM1(j+1) -> ua, GEMM2(j-1) from buffer 0
       ffn_interval<D, MB, true, true, true>(L, y, ub, ua, (j + 1) * FC, (j - 1) * FC, gr0, gw1);
+      if (KEEP) keep_g(ub, rep, j * FC);
       __syncthreads();
       if (KEEP) keep_u(ua, rep, (j + 1) * FC);
       // j+1 (even): GELU(j+1) -> buffer 0, GEMM1(j+2) -> ub, GEMM2(j) from buffer 1
       ffn_interval<D, MB, true, true, true>(L, y, ua, ub, (j + 2) * FC, j * FC, gr1, gw0);
+      if (KEEP) keep_g(ua, rep, (j + 1) * FC);
       __syncthreads();
     }
     if (KEEP) keep_u(ub, rep, (NC - 1) * FC);
     // j = NC-1 (odd): GELU(NC-1) -> buffer 1, GEMM2(NC-2) from buffer 0
     ffn_interval<D, MB, true, false, true>(L, y, ub, ua, 0, (NC - 2) * FC, gr0, gw1);
+    if (KEEP) keep_g(ub, rep, (NC - 1) * FC);
     __syncthreads();
     // epilogue: GEMM2(NC-1) from buffer 1
     ffn_interval<D, MB, true, false, false>(L, y, ua, ub, 0, (NC - 1) * FC, gr1, gw0);

@@ -41,6 +41,7 @@ struct FfnArgs {
   float* logits;                   // nullable, [n0 + N][256]
   float* kY;                       // nullable, [k+1][N][D]: Y_0 .. Y_k (fp32)
   float* kU;                       // nullable, [k][N][F]
+  float* kG;                       // nullable, [k][N][F]: GELU(U) as the bf16 operand values (bf16 path)
   float* kZ;                       // nullable, [N][256]
   int32_t* ktgt;                   // nullable, [N]
 };
@@ -73,6 +74,9 @@ struct GemmArgs {
   int64_t ldc;       // C(m,n) = C[m*ldc + n]
   int roundA, roundB;  // round that operand to bf16 (RNE) as it is read
   float beta;          // C = beta*C + A.B  (beta 0 or 1)
+  // nullable: C = (A.B) * GELU'(gelu_u) elementwise, gelu_u laid out as C
+  // (the backward of the FFN activation fused into its product); needs beta 0
+  const float* gelu_u;
 };
 // Deterministic: split-K partials are summed in a fixed order.  The split count
 // depends only on (M, N, K, ws_cap); gemm_ws_floats(M, N, K) floats let it
