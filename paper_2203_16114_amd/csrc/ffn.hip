@@ -299,9 +299,10 @@ __global__ __launch_bounds__(512) void k_ffn_head(FfnArgs a) {
 // per trip so that the roles stay compile-time.  G holds bf(2 GELU(U)) and the
 // packed W2 copy holds bf(W2)/2: both scalings are exact, so every product is
 // the one of bf(GELU(U)) and bf(W2), with one vector operation less per value.
-template <int D, int MB>
+template <int D, int MB, int WC_ = 2>
 struct FfnPipe {
-  static constexpr int FC = 128, WR = 4, WC = 2;
+  // 8 waves: WR along features (GEMM1) / model dims (GEMM2), WC along windows
+  static constexpr int FC = 128, WC = WC_, WR = 8 / WC_;
   static constexpr int CW = MB / WC, NFC = CW / 16;
   static constexpr int RF1 = FC / (WR * 16), RF2 = D / (WR * 16);
   static constexpr int RFA = RF2 > RF1 ? RF2 : RF1;
@@ -310,7 +311,11 @@ struct FfnPipe {
   static constexpr int NB2 = D / 16;
   static constexpr int NGV = RF1 * NFC * 4;  // GELU values per lane per chunk
   static constexpr int LDS = MB * YSTR + 2 * MB * GSTR + MB * (2 * 4 * 4 + 8);
-  static constexpr int PDA = 1;  // weight fragments requested one step ahead
+  // weight fragments (L2) requested PDA steps ahead, activation fragments
+  // (LDS) PDB steps ahead: one each for wide window tiles; the 32-window
+  // tiles of the update path have only two MFMAs per GEMM1 step and need more
+  static constexpr bool SHORT = MB / WC_ <= 32;
+  static constexpr int PDA = SHORT ? 4 : 1, PDB = SHORT ? 2 : 1;
 };
 
 struct PipeLane {
@@ -342,12 +347,13 @@ __device__ __forceinline__ void static_for(Fn&& f) {
 
 // One interval.  G2ON: GEMM2 of the chunk at feature c2 from buffer gr;
 // G1ON: GEMM1 of the chunk at feature c1 into un; GELUON: GELU of ug into gw.
-template <int D, int MB, bool G2ON, bool G1ON, bool GELUON>
-__device__ __forceinline__ void ffn_interval(const PipeLane& L, f32x4 (&y)[FfnPipe<D, MB>::RF2][FfnPipe<D, MB>::NFC],
-                                             f32x4 (&ug)[FfnPipe<D, MB>::RF1][FfnPipe<D, MB>::NFC],
-                                             f32x4 (&un)[FfnPipe<D, MB>::RF1][FfnPipe<D, MB>::NFC], int c1, int c2,
+template <int D, int MB, int WC, bool G2ON, bool G1ON, bool GELUON>
+__device__ __forceinline__ void ffn_interval(const PipeLane& L,
+                                             f32x4 (&y)[FfnPipe<D, MB, WC>::RF2][FfnPipe<D, MB, WC>::NFC],
+                                             f32x4 (&ug)[FfnPipe<D, MB, WC>::RF1][FfnPipe<D, MB, WC>::NFC],
+                                             f32x4 (&un)[FfnPipe<D, MB, WC>::RF1][FfnPipe<D, MB, WC>::NFC], int c1, int c2,
                                              const unsigned char* gr, unsigned char* gw) {
-  typedef FfnPipe<D, MB> P;
+  typedef FfnPipe<D, MB, WC> P;
   constexpr int NFC = P::NFC, RF1 = P::RF1, RF2 = P::RF2, RFA = P::RFA;
   constexpr int S2 = G2ON ? P::KC : 0, S1 = G1ON ? P::KD : 0, NS = S2 + S1;
   constexpr int NM = S2 * RF2 * NFC + S1 * RF1 * NFC;
@@ -360,9 +366,8 @@ __device__ __forceinline__ void ffn_interval(const PipeLane& L, f32x4 (&y)[FfnPi
       for (int nf = 0; nf < NFC; ++nf) un[rf][nf] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
   const int kc2 = c2 / 32, nb1 = c1 / 16;
-  // weight fragments (L2) are requested PDA steps ahead, activations (LDS) one
-  constexpr int PDA = P::PDA, NA = PDA + 1;
-  uint4 A[NA][RFA], B[2][NFC];
+  constexpr int PDA = P::PDA, NA = PDA + 1, PDB = P::PDB, NB = PDB + 1;
+  uint4 A[NA][RFA], B[NB][NFC];
   auto loadA = [&](auto sc) {
     constexpr int s = decltype(sc)::value, buf = s % NA;
     if constexpr (s < S2) {
@@ -375,7 +380,7 @@ __device__ __forceinline__ void ffn_interval(const PipeLane& L, f32x4 (&y)[FfnPi
     }
   };
   auto loadB = [&](auto sc) {
-    constexpr int s = decltype(sc)::value, buf = s & 1;
+    constexpr int s = decltype(sc)::value, buf = s % NB;
     if constexpr (s < S2) {
 #pragma unroll
       for (int nf = 0; nf < NFC; ++nf) B[buf][nf] = *(const uint4*)(gr + nf * 16 * P::GSTR + s * 64);
@@ -386,11 +391,11 @@ __device__ __forceinline__ void ffn_interval(const PipeLane& L, f32x4 (&y)[FfnPi
     }
   };
   static_for<0, (PDA < NS ? PDA : NS)>(loadA);
-  loadB(std::integral_constant<int, 0>{});
+  static_for<0, (PDB < NS ? PDB : NS)>(loadB);
   static_for<0, NS>([&](auto sc) {
-    constexpr int s = decltype(sc)::value, abuf = s % NA, bbuf = s & 1;
+    constexpr int s = decltype(sc)::value, abuf = s % NA, bbuf = s % NB;
     if constexpr (s + PDA < NS) loadA(std::integral_constant<int, s + PDA>{});
-    if constexpr (s + 1 < NS) loadB(std::integral_constant<int, s + 1>{});
+    if constexpr (s + PDB < NS) loadB(std::integral_constant<int, s + PDB>{});
     constexpr bool g2 = s < S2;
     constexpr int RFN = g2 ? RF2 : RF1;
     constexpr int MB0 = g2 ? s * RF2 * NFC : S2 * RF2 * NFC + (s - S2) * RF1 * NFC;
@@ -420,9 +425,9 @@ __device__ __forceinline__ void ffn_interval(const PipeLane& L, f32x4 (&y)[FfnPi
   }
 }
 
-template <int D, int MB, bool KEEP>
+template <int D, int MB, bool KEEP, int WC>
 __global__ __launch_bounds__(512) void k_ffn_pipe(FfnArgs a) {
-  typedef FfnPipe<D, MB> P;
+  typedef FfnPipe<D, MB, WC> P;
   constexpr int NFC = P::NFC, RF1 = P::RF1, RF2 = P::RF2, FC = P::FC;
   static_assert(RF1 >= 1 && RF2 >= 1 && NFC >= 1 && MB % (16 * P::WC) == 0, "shape");
   static_assert(P::LDS <= 160 * 1024, "LDS");
@@ -527,31 +532,31 @@ __global__ __launch_bounds__(512) void k_ffn_pipe(FfnArgs a) {
     __syncthreads();
     if (rep == a.k) break;
     // prologue: GEMM1 of chunk 0 into ua
-    ffn_interval<D, MB, false, true, false>(L, y, ub, ua, 0, 0, gr0, gw0);
+    ffn_interval<D, MB, WC, false, true, false>(L, y, ub, ua, 0, 0, gr0, gw0);
     if (KEEP) keep_u(ua, rep, 0);
     // j = 0: GELU(0) -> buffer 0, GEMM1(1) -> ub
-    ffn_interval<D, MB, false, true, true>(L, y, ua, ub, FC, 0, gr0, gw0);
+    ffn_interval<D, MB, WC, false, true, true>(L, y, ua, ub, FC, 0, gr0, gw0);
     if (KEEP) keep_g(ua, rep, 0);
     __syncthreads();
     for (int j = 1; j < NC - 1; j += 2) {
       if (KEEP) keep_u(ub, rep, j * FC);
       // j (odd): GELU(j) -> buffer 1, GEMM1(j+1) -> ua, GEMM2(j-1) from buffer 0
-      ffn_interval<D, MB, true, true, true>(L, y, ub, ua, (j + 1) * FC, (j - 1) * FC, gr0, gw1);
+      ffn_interval<D, MB, WC, true, true, true>(L, y, ub, ua, (j + 1) * FC, (j - 1) * FC, gr0, gw1);
       if (KEEP) keep_g(ub, rep, j * FC);
       __syncthreads();
       if (KEEP) keep_u(ua, rep, (j + 1) * FC);
       // j+1 (even): GELU(j+1) -> buffer 0, GEMM1(j+2) -> ub, GEMM2(j) from buffer 1
-      ffn_interval<D, MB, true, true, true>(L, y, ua, ub, (j + 2) * FC, j * FC, gr1, gw0);
+      ffn_interval<D, MB, WC, true, true, true>(L, y, ua, ub, (j + 2) * FC, j * FC, gr1, gw0);
       if (KEEP) keep_g(ua, rep, (j + 1) * FC);
       __syncthreads();
     }
     if (KEEP) keep_u(ub, rep, (NC - 1) * FC);
     // j = NC-1 (odd): GELU(NC-1) -> buffer 1, GEMM2(NC-2) from buffer 0
-    ffn_interval<D, MB, true, false, true>(L, y, ub, ua, 0, (NC - 2) * FC, gr0, gw1);
+    ffn_interval<D, MB, WC, true, false, true>(L, y, ub, ua, 0, (NC - 2) * FC, gr0, gw1);
     if (KEEP) keep_g(ub, rep, (NC - 1) * FC);
     __syncthreads();
     // epilogue: GEMM2(NC-1) from buffer 1
-    ffn_interval<D, MB, true, false, false>(L, y, ua, ub, 0, (NC - 1) * FC, gr1, gw0);
+    ffn_interval<D, MB, WC, true, false, false>(L, y, ua, ub, 0, (NC - 1) * FC, gr1, gw0);
   }
   ffn_head_out<true, D, MB, KEEP, P::YSTR>(a, Ys, red, zy, tg);
 }
@@ -580,14 +585,14 @@ constexpr int pick_fc(bool bf, int D) { return ffn_lds_bytes(bf, D, pick_mb(bf, 
 template <int D>
 constexpr int pick_mb_pipe() { return FfnPipe<D, 128>::LDS <= 160 * 1024 ? 128 : 64; }
 
-template <int D, int MB>
+template <int D, int MB, int WC = 2>
 static void launch_pipe(const FfnArgs& a, hipStream_t s) {
-  static_assert(FfnPipe<D, MB>::LDS <= 160 * 1024, "LDS");
+  static_assert(FfnPipe<D, MB, WC>::LDS <= 160 * 1024, "LDS");
   const dim3 grid((unsigned)((a.w.N + MB - 1) / MB));
   if (a.kY)
-    hipLaunchKernelGGL((k_ffn_pipe<D, MB, true>), grid, dim3(512), 0, s, a);
+    hipLaunchKernelGGL((k_ffn_pipe<D, MB, true, WC>), grid, dim3(512), 0, s, a);
   else
-    hipLaunchKernelGGL((k_ffn_pipe<D, MB, false>), grid, dim3(512), 0, s, a);
+    hipLaunchKernelGGL((k_ffn_pipe<D, MB, false, WC>), grid, dim3(512), 0, s, a);
 }
 
 template <bool BF, int D>
@@ -598,6 +603,8 @@ static void run_ffn(const FfnArgs& a, hipStream_t s) {
     constexpr int MB = pick_mb_pipe<D>();
     if (a.w.N >= (int64_t)256 * MB)
       launch_pipe<D, MB>(a, s);
+    else if constexpr (D >= 128)
+      launch_pipe<D, 32, 1>(a, s);  // all 8 waves across the features: each weight fragment read once per block
     else
       launch_pipe<D, 32>(a, s);
   } else {
