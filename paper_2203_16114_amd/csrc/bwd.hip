@@ -431,13 +431,24 @@ __global__ void k_colsum1(const float* __restrict__ in, int64_t rows, int64_t co
   for (int64_t r = r0; r < r1; ++r) acc += in[r * ld + c];
   ws[s * cols + c] = acc;
 }
-__global__ void k_colsum2(const float* __restrict__ ws, int64_t cols, float* out, float beta) {
-  const int64_t c = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (c >= cols) return;
+// 64 columns per block; thread group q of four adds the partials q*S/4 ..
+// (q+1)*S/4 - 1 in order, and the four group sums are added in group order.
+__global__ __launch_bounds__(256) void k_colsum2(const float* __restrict__ ws, int64_t cols, float* out, float beta) {
+  __shared__ float red[4][64];
+  constexpr int PER = COLSUM_SPLITS / 4;
+  const int q = threadIdx.x >> 6, cl = threadIdx.x & 63;
+  const int64_t c = (int64_t)blockIdx.x * 64 + cl;
   float acc = 0.f;
+  if (c < cols) {
 #pragma unroll 16
-  for (int s = 0; s < COLSUM_SPLITS; ++s) acc += ws[s * cols + c];
-  out[c] = (beta != 0.f) ? out[c] + acc : acc;
+    for (int s = q * PER; s < (q + 1) * PER; ++s) acc += ws[s * cols + c];
+  }
+  red[q][cl] = acc;
+  __syncthreads();
+  if (q == 0 && c < cols) {
+    const float tot = ((red[0][cl] + red[1][cl]) + red[2][cl]) + red[3][cl];
+    out[c] = (beta != 0.f) ? out[c] + tot : tot;
+  }
 }
 // four columns per thread, eight rows in flight; the same sum order as k_colsum1
 __global__ __launch_bounds__(64) void k_colsum1v(const float* __restrict__ in, int64_t rows, int64_t cols, int64_t ld,
@@ -473,7 +484,7 @@ void launch_colsum(const float* in, int64_t rows, int64_t cols, int64_t ld, floa
     hipLaunchKernelGGL(k_colsum1v, dim3(gx, COLSUM_SPLITS), dim3(64), 0, s, in, rows, cols, ld, ws);
   else
     hipLaunchKernelGGL(k_colsum1, dim3(gx, COLSUM_SPLITS), dim3(256), 0, s, in, rows, cols, ld, ws);
-  hipLaunchKernelGGL(k_colsum2, dim3(gx), dim3(256), 0, s, ws, cols, out, beta);
+  hipLaunchKernelGGL(k_colsum2, dim3((unsigned)((cols + 63) / 64)), dim3(256), 0, s, ws, cols, out, beta);
 }
 
 // ------------------------------------------------------ head: dz of the CE ----
@@ -671,26 +682,32 @@ void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int
 // operand value).  The token is X = G + P[t]; the weight gradients X^T.dZ are
 // formed as G^T.dZ (a GEMM) plus P^T.(sum over windows of dZ) (k_pos_grad).
 template <bool BF>
-__global__ void k_gather_kept(const uint8_t* __restrict__ win, int64_t N, const typename Mma<BF>::T* __restrict__ E,
-                              int T, int D, int e, int g, float* __restrict__ X) {
+__global__ __launch_bounds__(256) void k_gather_kept(const uint8_t* __restrict__ win, int64_t rows,
+                                                     const typename Mma<BF>::T* __restrict__ E, int T, int D, int e,
+                                                     int g, float* __restrict__ X) {
+  // thread: four consecutive columns of one token row (row = n*T + t); e is a
+  // multiple of 4, so the four share one byte
   typedef Mma<BF> M;
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= N * T * D) return;
-  const int c = (int)(i % D);
-  const int64_t rr = i / D;
-  const int t = (int)(rr % T);
-  const int64_t n = rr / T;
+  const uint32_t q4 = (uint32_t)D / 4;
+  const uint32_t i = blockIdx.x * 256u + threadIdx.x;  // the grid has fewer than 2^32 threads
+  if ((int64_t)i >= rows * q4) return;
+  const uint32_t row32 = i / q4;
+  const int64_t row = row32;
+  const int c = (int)(i - row32 * q4) * 4;
   const int j = c / e, cc = c - j * e;
-  const int byte = win[n * (T * g) + t * g + j];
-  X[i] = M::val(E[byte * e + cc]);
+  // the byte of token t, group slot j of window n sits at win[n*T*g + t*g + j] = win[row*g + j]
+  const int byte = win[row * g + j];
+  const typename M::T* src = E + byte * e + cc;
+  *reinterpret_cast<float4*>(X + row * D + c) = make_float4(M::val(src[0]), M::val(src[1]), M::val(src[2]), M::val(src[3]));
 }
 void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, int T, int D, int e, int g, float* X,
                         hipStream_t s) {
-  const dim3 grid((unsigned)((N * T * D + 255) / 256));
+  const int64_t rows = N * T;
+  const dim3 grid((unsigned)((rows * (D / 4) + 255) / 256));
   if (bf)
-    hipLaunchKernelGGL(k_gather_kept<true>, grid, dim3(256), 0, s, win, N, (const uint16_t*)E, T, D, e, g, X);
+    hipLaunchKernelGGL(k_gather_kept<true>, grid, dim3(256), 0, s, win, rows, (const uint16_t*)E, T, D, e, g, X);
   else
-    hipLaunchKernelGGL(k_gather_kept<false>, grid, dim3(256), 0, s, win, N, (const float*)E, T, D, e, g, X);
+    hipLaunchKernelGGL(k_gather_kept<false>, grid, dim3(256), 0, s, win, rows, (const float*)E, T, D, e, g, X);
 }
 
 // Positional part of a projection's weight gradient:
