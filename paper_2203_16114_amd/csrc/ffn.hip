@@ -28,10 +28,26 @@ __device__ __forceinline__ void put4(float* p, const f32x4& v) {
   *reinterpret_cast<float4*>(p) = make_float4(v[0], v[1], v[2], v[3]);
 }
 
+// Swizzled rows (a power of two of 16-byte units, no padding): unit u of row
+// m is stored at unit u ^ (m & mask), mask = min(units, 16) - 1, which makes
+// the 16-row fragment reads of the MFMA loops free of LDS bank conflicts.  A
+// lane reads row m0 + lc (m0 a multiple of 16, so m & mask = lc & mask) at
+// units 4 ks + lg, i.e. at byte 64 (ks & ~3) + off[ks & 3] of the row:
+__device__ __forceinline__ void swz_off(int lg, int lc, int mask, int (&off)[4]) {
+  const int q = (lc & mask) >> 2, p = lg ^ (lc & 3);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) off[j] = 16 * (((j ^ q) << 2) | p);
+}
+// byte offset in a swizzled row of the 8-byte group holding elements e .. e+3
+// (bf16, e a multiple of 4) of row m
+__device__ __forceinline__ int swz_elem(int m, int e, int mask) { return 16 * ((e >> 3) ^ (m & mask)) + 8 * ((e >> 2) & 1); }
+
 // Head on bf(Y_k) staged in Ys, then the code length (shared by both FFN
 // kernels): z^T = Wout^T . Y^T + bout, log-sum-exp across the 4 feature waves
 // through LDS in a fixed order, bits = log2 sum exp(z - max) - (z_y - max) log2 e.
-template <bool BF, int D, int MB, bool KEEP, int YSTR>
+// YM >= 0: Ys rows are unpadded and swizzled (unit u of row m at u ^ (m & YM),
+// see swz_off); YM < 0: padded rows, unit u at u.
+template <bool BF, int D, int MB, bool KEEP, int YSTR, int YM = -1>
 __device__ __forceinline__ void ffn_head_out(const FfnArgs& a, const unsigned char* Ys, float (&red)[2][4][MB],
                                              float* zy, const int* tg) {
   typedef Mma<BF> M;
@@ -47,7 +63,9 @@ __device__ __forceinline__ void ffn_head_out(const FfnArgs& a, const unsigned ch
   const int m0 = wc * CW;
   const unsigned char* yrow[NFC];
 #pragma unroll
-  for (int nf = 0; nf < NFC; ++nf) yrow[nf] = Ys + (m0 + nf * 16 + lc) * YSTR + lg * 16;
+  for (int nf = 0; nf < NFC; ++nf) yrow[nf] = Ys + (m0 + nf * 16 + lc) * YSTR + (YM < 0 ? lg * 16 : 0);
+  int yo[4];
+  if constexpr (YM >= 0) swz_off(lg, lc, YM, yo);
   f32x4 z[RFH][NFC];
 #pragma unroll
   for (int rf = 0; rf < RFH; ++rf)
@@ -64,7 +82,12 @@ __device__ __forceinline__ void ffn_head_out(const FfnArgs& a, const unsigned ch
     }
     uint4 bb[NFC];
 #pragma unroll
-    for (int nf = 0; nf < NFC; ++nf) bb[nf] = *(const uint4*)(yrow[nf] + ks * 64);
+    for (int nf = 0; nf < NFC; ++nf) {
+      if constexpr (YM >= 0)
+        bb[nf] = *(const uint4*)(yrow[nf] + (ks & ~3) * 64 + yo[ks & 3]);
+      else
+        bb[nf] = *(const uint4*)(yrow[nf] + ks * 64);
+    }
 #pragma unroll
     for (int rf = 0; rf < RFH; ++rf)
 #pragma unroll
@@ -306,7 +329,9 @@ struct FfnPipe {
   static constexpr int CW = MB / WC, NFC = CW / 16;
   static constexpr int RF1 = FC / (WR * 16), RF2 = D / (WR * 16);
   static constexpr int RFA = RF2 > RF1 ? RF2 : RF1;
-  static constexpr int YSTR = D * 2 + 16, GSTR = FC * 2 + 16;
+  // unpadded rows, swizzled (swz_off): D / 8 and FC / 8 units
+  static constexpr int YSTR = D * 2, GSTR = FC * 2;
+  static constexpr int YM = (D / 8 >= 16 ? 16 : D / 8) - 1, GM = (FC / 8 >= 16 ? 16 : FC / 8) - 1;
   static constexpr int KD = D / 32, KC = FC / 32;
   static constexpr int NB2 = D / 16;
   static constexpr int NGV = RF1 * NFC * 4;  // GELU values per lane per chunk
@@ -323,7 +348,9 @@ struct PipeLane {
   int w1o, w2o;                     // byte offset of this wave's first fragment column (wave-uniform)
   int NB1, lg, f0;
   int voff;                         // lane * 16 bytes
-  const unsigned char* ybase;       // Ys row (m0 + lc), byte lg*16
+  const unsigned char* ybase;       // Ys row (m0 + lc)
+  int yo[4], go[4];                 // swizzled fragment offsets in Ys / Gs rows (swz_off)
+  int gwo[2];                       // swizzled offset of this lane's GELU values rf = 0, 1 in a Gs row
 };
 
 // Buffer descriptor over n bytes at p (raw, untyped; reads past n return 0).
@@ -383,11 +410,12 @@ __device__ __forceinline__ void ffn_interval(const PipeLane& L,
     constexpr int s = decltype(sc)::value, buf = s % NB;
     if constexpr (s < S2) {
 #pragma unroll
-      for (int nf = 0; nf < NFC; ++nf) B[buf][nf] = *(const uint4*)(gr + nf * 16 * P::GSTR + s * 64);
+      for (int nf = 0; nf < NFC; ++nf) B[buf][nf] = *(const uint4*)(gr + nf * 16 * P::GSTR + L.go[s & 3]);
     } else {
       constexpr int ks = s - S2;
 #pragma unroll
-      for (int nf = 0; nf < NFC; ++nf) B[buf][nf] = *(const uint4*)(L.ybase + nf * 16 * P::YSTR + ks * 64);
+      for (int nf = 0; nf < NFC; ++nf)
+        B[buf][nf] = *(const uint4*)(L.ybase + nf * 16 * P::YSTR + (ks & ~3) * 64 + L.yo[ks & 3]);
     }
   };
   static_for<0, (PDA < NS ? PDA : NS)>(loadA);
@@ -421,7 +449,7 @@ __device__ __forceinline__ void ffn_interval(const PipeLane& L,
     for (int nf = 0; nf < NFC; ++nf)
 #pragma unroll
       for (int rf = 0; rf < RF1; ++rf)
-        put4((uint16_t*)(gw + nf * 16 * P::GSTR) + L.f0 + rf * 16 + 4 * L.lg, ug[rf][nf]);
+        put4((uint16_t*)(gw + nf * 16 * P::GSTR + L.gwo[rf]), ug[rf][nf]);
   }
 }
 
@@ -454,9 +482,13 @@ __global__ __launch_bounds__(512) void k_ffn_pipe(FfnArgs a) {
   L.NB1 = F / 16;
   L.voff = lane * 16;
   L.lg = lg;
-  L.ybase = Ys + (m0 + lc) * P::YSTR + lg * 16;
-  const unsigned char* gr0 = Gs[0] + (m0 + lc) * P::GSTR + lg * 16;
-  const unsigned char* gr1 = Gs[1] + (m0 + lc) * P::GSTR + lg * 16;
+  L.ybase = Ys + (m0 + lc) * P::YSTR;
+  swz_off(lg, lc, P::YM, L.yo);
+  swz_off(lg, lc, P::GM, L.go);
+#pragma unroll
+  for (int rf = 0; rf < 2; ++rf) L.gwo[rf] = swz_elem(lc, L.f0 + rf * 16 + 4 * lg, P::GM);
+  const unsigned char* gr0 = Gs[0] + (m0 + lc) * P::GSTR;
+  const unsigned char* gr1 = Gs[1] + (m0 + lc) * P::GSTR;
   unsigned char* gw0 = Gs[0] + (m0 + lc) * P::GSTR;
   unsigned char* gw1 = Gs[1] + (m0 + lc) * P::GSTR;
 
@@ -526,7 +558,7 @@ __global__ __launch_bounds__(512) void k_ffn_pipe(FfnArgs a) {
         if (KEEP && n < N)
           *reinterpret_cast<float4*>(a.kY + ((int64_t)rep * N + n) * D + dd) =
               make_float4(y[rf][nf][0], y[rf][nf][1], y[rf][nf][2], y[rf][nf][3]);
-        put4((uint16_t*)(Ys + m * P::YSTR) + dd, y[rf][nf]);
+        put4((uint16_t*)(Ys + m * P::YSTR + swz_elem(m, dd, P::YM)), y[rf][nf]);
       }
     }
     __syncthreads();
@@ -558,7 +590,7 @@ __global__ __launch_bounds__(512) void k_ffn_pipe(FfnArgs a) {
     // epilogue: GEMM2(NC-1) from buffer 1
     ffn_interval<D, MB, WC, true, false, false>(L, y, ua, ub, 0, (NC - 1) * FC, gr1, gw0);
   }
-  ffn_head_out<true, D, MB, KEEP, P::YSTR>(a, Ys, red, zy, tg);
+  ffn_head_out<true, D, MB, KEEP, P::YSTR, P::YM>(a, Ys, red, zy, tg);
 }
 
 // ------------------------------------------------------------ dispatch ----
