@@ -355,6 +355,7 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
   constexpr int KSTEPS = S::KSTEPS, NFH = S::NFH, KSC = S::KSC, CPP = KSTEPS / KSC, CHUNK = S::CHUNK;
   constexpr int XLSTR = S::XLSTR, KVSTR = S::KVSTR;
   constexpr int NQF = D / 16, QFW = (NQF + NW - 1) / NW, NMF = MA / 16, NB = D / 16;
+  constexpr int WPD = 1;  // k-steps ahead that the q and output-projection weight fragments are fetched (3: no gain)
   constexpr int CQ = DH / 4;  // 4-feature chunks of a head
   static_assert(S::ok && KSTEPS % KSC == 0 && (T == 4 || T == 8), "shape");
   __shared__ uint4 Wst[2][CHUNK];
@@ -424,15 +425,17 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
       f32x4 acc[NMF];
 #pragma unroll
       for (int nf = 0; nf < NMF; ++nf) acc[nf] = f32x4{0.f, 0.f, 0.f, 0.f};
-      uint4 wq[2];
-      wq[0] = a.Wq[qf * 64 + lane];
+      // weight fragments (L2) fetched WPD k-steps ahead
+      uint4 wq[WPD + 1];
+#pragma unroll
+      for (int ks = 0; ks < WPD && ks < KSTEPS; ++ks) wq[ks] = a.Wq[(ks * NB + qf) * 64 + lane];
 #pragma unroll
       for (int ks = 0; ks < KSTEPS; ++ks) {
-        if (ks + 1 < KSTEPS) wq[(ks + 1) & 1] = a.Wq[((ks + 1) * NB + qf) * 64 + lane];
+        if (ks + WPD < KSTEPS) wq[(ks + WPD) % (WPD + 1)] = a.Wq[((ks + WPD) * NB + qf) * 64 + lane];
 #pragma unroll
         for (int nf = 0; nf < NMF; ++nf) {
           const uint4 bx = *(const uint4*)(Xl + (nf * 16 + lc) * XLSTR + ks * 64 + lg * 16);
-          M::run(acc[nf], wq[ks & 1], bx);
+          M::run(acc[nf], wq[ks % (WPD + 1)], bx);
         }
       }
       const float4 pq = *reinterpret_cast<const float4*>(PQ + (T - 1) * D + qf * 16 + 4 * lg);
@@ -459,9 +462,24 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
                                        (__attribute__((address_space(3))) void*)(Wst[buf] + q * 64), 16, 0, 0);
   };
   constexpr int NCH = H * 2 * CPP;
+  // rows t of P.Wk and P.Wv of head hh -> PKV[hh & 1] by direct 16-byte loads:
+  // slot l = (which * T + t) * DH / 4 + c4 holds features 4 c4 .. 4 c4 + 3
+  constexpr int PKV_SLOTS = 2 * T * DH / 4;
+  auto stage_pkv = [&](int hh) {
+    if (wave * 64 < PKV_SLOTS) {
+      const int l = wave * 64 + lane;
+      const int which = l / (T * DH / 4), t = (l / (DH / 4)) % T, c4 = l % (DH / 4);
+      const float* src = (which ? PV : PK) + t * D + hh * DH + 4 * c4;
+      __builtin_amdgcn_global_load_lds((const void*)src,
+                                       (__attribute__((address_space(3))) void*)(&PKV[hh & 1][0][0] + wave * 256), 16,
+                                       0, 0);
+    }
+  };
+  static_assert(PKV_SLOTS % 64 == 0, "PKV staging by whole waves");
   stage(0, 0);
+  stage_pkv(0);
   __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();  // chunk 0 staged; Qs complete; E_last rows no longer needed
+  __syncthreads();  // chunk 0 and head 0's P rows staged; Qs complete; E_last rows no longer needed
 
   const float scale = a.scale;
   float* kv = KV[wave];
@@ -470,15 +488,8 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
   const int sp_i = lane / T, sp_t = lane - (lane / T) * T;
   const bool sp_live = sp_i < NPW;
   for (int h = 0; h < H; ++h) {
-    // this head's rows of P.Wk and P.Wv to LDS (read after the K pass's barrier;
-    // the buffer was last read two heads ago)
-    {
-      float* dst = &PKV[h & 1][0][0];
-      for (int k = tid; k < 2 * T * DH; k += 512) {
-        const int which = k / (T * DH), t = (k / DH) % T, c = k % DH;
-        dst[k] = (which ? PV : PK)[t * D + h * DH + c];
-      }
-    }
+    // this head's rows of P.Wk and P.Wv are in PKV[h & 1]: staged during the
+    // previous head (head 0 with the first weight chunk)
     const float* pkh = PKV[h & 1][0];
     const float* pvh = PKV[h & 1][1];
 #pragma unroll
@@ -498,6 +509,9 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
         }
         __builtin_amdgcn_s_waitcnt(0);
         __syncthreads();
+        // every wave is past head h - 1, the last reader of PKV[(h + 1) & 1]:
+        // stage head h + 1's P rows there (waited for at the next chunk barrier)
+        if (pass == 0 && ck == 0 && h + 1 < H) stage_pkv(h + 1);
       }
       // group rows of K_h (E-part) or V_h to this wave's exchange rows
 #pragma unroll
@@ -559,15 +573,16 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
       f32x4 acc[NMF];
 #pragma unroll
       for (int nf = 0; nf < NMF; ++nf) acc[nf] = f32x4{0.f, 0.f, 0.f, 0.f};
-      uint4 wo[2];
-      wo[0] = a.Wo[qf * 64 + lane];
+      uint4 wo[WPD + 1];
+#pragma unroll
+      for (int ks = 0; ks < WPD && ks < KSTEPS; ++ks) wo[ks] = a.Wo[(ks * NB + qf) * 64 + lane];
 #pragma unroll
       for (int ks = 0; ks < KSTEPS; ++ks) {
-        if (ks + 1 < KSTEPS) wo[(ks + 1) & 1] = a.Wo[((ks + 1) * NB + qf) * 64 + lane];
+        if (ks + WPD < KSTEPS) wo[(ks + WPD) % (WPD + 1)] = a.Wo[((ks + WPD) * NB + qf) * 64 + lane];
 #pragma unroll
         for (int nf = 0; nf < NMF; ++nf) {
           const uint4 bo = *(const uint4*)(Xl + (nf * 16 + lc) * XLSTR + ks * 64 + lg * 16);
-          M::run(acc[nf], wo[ks & 1], bo);
+          M::run(acc[nf], wo[ks % (WPD + 1)], bo);
         }
       }
 #pragma unroll
