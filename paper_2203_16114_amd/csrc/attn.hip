@@ -337,7 +337,7 @@ struct GrpShape {
   static constexpr int KSC = (KSTEPS * NFH <= 16) ? KSTEPS : 16 / NFH;  // k-steps per staged 16 KiB chunk
   static constexpr int CHUNK = KSC * NFH * 64;
   static constexpr int XLSTR = D * 2 + 16;
-  static constexpr int KVSTR = DH + 4;  // floats per group row in the exchange
+  static constexpr int KVSTR = DH + 4;  // floats per group row in the exchange (unpadded swizzled rows: slower)
   static constexpr int WB = MA + W + 64;
   // q and attention weights are stored class-major (a wave's windows in
   // consecutive rows) with padded rows, so a wave's reads hit distinct banks
@@ -462,20 +462,22 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
                                        (__attribute__((address_space(3))) void*)(Wst[buf] + q * 64), 16, 0, 0);
   };
   constexpr int NCH = H * 2 * CPP;
-  // rows t of P.Wk and P.Wv of head hh -> PKV[hh & 1] by direct 16-byte loads:
-  // slot l = (which * T + t) * DH / 4 + c4 holds features 4 c4 .. 4 c4 + 3
+  // rows t of P.Wk and P.Wv of head hh -> PKV[hh & 1] by direct 16-byte loads,
+  // slot l = (which * T + t) * DH / 4 + c4 (T <= 8 <= DH / 4)
   constexpr int PKV_SLOTS = 2 * T * DH / 4;
   auto stage_pkv = [&](int hh) {
     if (wave * 64 < PKV_SLOTS) {
       const int l = wave * 64 + lane;
       const int which = l / (T * DH / 4), t = (l / (DH / 4)) % T, c4 = l % (DH / 4);
-      const float* src = (which ? PV : PK) + t * D + hh * DH + 4 * c4;
+      // unit c4 of row t holds features 4 (c4 ^ t) .. + 3 (rows of different t read
+      // at one unit hit different banks)
+      const float* src = (which ? PV : PK) + t * D + hh * DH + 4 * (c4 ^ t);
       __builtin_amdgcn_global_load_lds((const void*)src,
                                        (__attribute__((address_space(3))) void*)(&PKV[hh & 1][0][0] + wave * 256), 16,
                                        0, 0);
     }
   };
-  static_assert(PKV_SLOTS % 64 == 0, "PKV staging by whole waves");
+  static_assert(PKV_SLOTS % 64 == 0 && T <= DH / 4, "PKV staging by whole waves; swizzle within a row");
   stage(0, 0);
   stage_pkv(0);
   __builtin_amdgcn_s_waitcnt(0);
@@ -529,7 +531,7 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
           for (int c4 = 0; c4 < CQ; ++c4) {
             const float4 q4 = *reinterpret_cast<const float4*>(qv + 4 * c4);
             const float4 k4 = *reinterpret_cast<const float4*>(kr + 4 * c4);
-            const float4 p4 = *reinterpret_cast<const float4*>(pk + 4 * c4);
+            const float4 p4 = *reinterpret_cast<const float4*>(pk + 4 * (c4 ^ sp_t));
             s += q4.x * (k4.x + p4.x) + q4.y * (k4.y + p4.y) + q4.z * (k4.z + p4.z) + q4.w * (k4.w + p4.w);
           }
         }
@@ -550,7 +552,7 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
             for (int t = 0; t < T; ++t) {
               const float at = Ps[(row0 + ip) * PSTR + t];
               const float4 v4 = *reinterpret_cast<const float4*>(kv + (ip + t) * KVSTR + 4 * cq);
-              const float4 p4 = *reinterpret_cast<const float4*>(pvh + t * DH + 4 * cq);
+              const float4 p4 = *reinterpret_cast<const float4*>(pvh + t * DH + 4 * (cq ^ t));
               o.x += at * (v4.x + p4.x);
               o.y += at * (v4.y + p4.y);
               o.z += at * (v4.z + p4.z);
