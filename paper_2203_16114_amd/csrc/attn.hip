@@ -336,7 +336,8 @@ struct GrpShape {
   static constexpr int KSTEPS = D / 32, NFH = DH / 16;
   static constexpr int KSC = (KSTEPS * NFH <= 16) ? KSTEPS : 16 / NFH;  // k-steps per staged 16 KiB chunk
   static constexpr int CHUNK = KSC * NFH * 64;
-  static constexpr int XLSTR = D * 2 + 16;
+  // E_last / O rows: unpadded, 16-byte unit u of row m stored at u ^ (m & XXM)
+  static constexpr int XLSTR = D * 2, XXM = (D / 8 >= 16 ? 16 : D / 8) - 1;
   static constexpr int KVSTR = DH + 4;  // floats per group row in the exchange (unpadded swizzled rows: slower)
   static constexpr int WB = MA + W + 64;
   // q and attention weights are stored class-major (a wave's windows in
@@ -412,11 +413,19 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
     }
     if (ip >= 0 && ip < NPW) {
 #pragma unroll
-      for (int ks = 0; ks < KSTEPS; ++ks) *(uint4*)(Xl + win_of(ip) * XLSTR + ks * 64 + lg * 16) = xb[ks];
+      for (int ks = 0; ks < KSTEPS; ++ks)
+        *(uint4*)(Xl + win_of(ip) * XLSTR + 16 * ((ks * 4 + lg) ^ (win_of(ip) & S::XXM))) = xb[ks];
     }
   }
   __syncthreads();
 
+  // fragment reads of Xl rows nf*16 + lc at units 4 ks + lg: byte 64 (ks & ~3) + xo[ks & 3]
+  int xo[4];
+  {
+    const int q = (lc & S::XXM) >> 2, p = lg ^ (lc & 3);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) xo[j] = 16 * (((j ^ q) << 2) | p);
+  }
   // q^T = Wq^T . E_last^T + (P.Wq)[T-1] ; lane holds q[m = nf*16 + lc][c = qf*16 + 4*lg + r]
 #pragma unroll
   for (int qi = 0; qi < QFW; ++qi) {
@@ -434,7 +443,7 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
         if (ks + WPD < KSTEPS) wq[(ks + WPD) % (WPD + 1)] = a.Wq[((ks + WPD) * NB + qf) * 64 + lane];
 #pragma unroll
         for (int nf = 0; nf < NMF; ++nf) {
-          const uint4 bx = *(const uint4*)(Xl + (nf * 16 + lc) * XLSTR + ks * 64 + lg * 16);
+          const uint4 bx = *(const uint4*)(Xl + (nf * 16 + lc) * XLSTR + (ks & ~3) * 64 + xo[ks & 3]);
           M::run(acc[nf], wq[ks % (WPD + 1)], bx);
         }
       }
@@ -558,7 +567,9 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
               o.z += at * (v4.z + p4.z);
               o.w += at * (v4.w + p4.w);
             }
-            put4o((uint16_t*)(Xl + win_of(ip) * XLSTR) + h * DH + 4 * cq, f32x4{o.x, o.y, o.z, o.w});
+            const int orow = win_of(ip), oe = h * DH + 4 * cq;
+            put4o((uint16_t*)(Xl + orow * XLSTR + 16 * ((oe >> 3) ^ (orow & S::XXM)) + 8 * ((oe >> 2) & 1)),
+                  f32x4{o.x, o.y, o.z, o.w});
           }
         }
       }
@@ -583,7 +594,7 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
         if (ks + WPD < KSTEPS) wo[(ks + WPD) % (WPD + 1)] = a.Wo[((ks + WPD) * NB + qf) * 64 + lane];
 #pragma unroll
         for (int nf = 0; nf < NMF; ++nf) {
-          const uint4 bo = *(const uint4*)(Xl + (nf * 16 + lc) * XLSTR + ks * 64 + lg * 16);
+          const uint4 bo = *(const uint4*)(Xl + (nf * 16 + lc) * XLSTR + (ks & ~3) * 64 + xo[ks & 3]);
           M::run(acc[nf], wo[ks % (WPD + 1)], bo);
         }
       }
