@@ -58,7 +58,7 @@ struct AttnShape {
   static constexpr int CHUNK = KSC * NFH * 64;                            // uint4 per chunk
   static constexpr int XLSTR = D * (int)sizeof(OT) + 16;
   static constexpr int lds(int rfw) {
-    return 2 * CHUNK * 16 + (NW * rfw * 16 / T) * (D * 4 + XLSTR + 64);
+    return 2 * CHUNK * 16 + (NW * rfw * 16 / T) * (D * 4 + XLSTR + 64) + 2 * 2 * T * DH * 4;
   }
   // row fragments per wave: the largest of 4, 2, 1 whose register-held tokens,
   // accumulators and fragments stay within the register budget of two waves per
@@ -88,6 +88,7 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
   __shared__ __align__(16) float Qs[MA * D];
   __shared__ __align__(16) unsigned char Xl[MA * XLSTR];  // X_last rows, then O rows
   __shared__ uint8_t Wb[MA * 64];
+  __shared__ __align__(16) float PKV[2][2][T * DH];  // head slices of P.Wk and P.Wv, double-buffered
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lg = lane >> 4, lc = lane & 15;
   const int64_t tile0 = (int64_t)blockIdx.x * MA;
@@ -185,9 +186,24 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
                                        (__attribute__((address_space(3))) void*)(Wst[buf] + q * 64), 16, 0, 0);
   };
   constexpr int NCH = H * 2 * CPP;
+  // rows t of P.Wk and P.Wv of head hh -> PKV[hh & 1] by direct 16-byte loads,
+  // slot l = (which * T + t) * DH / 4 + c4
+  constexpr int PKV_SLOTS = 2 * T * DH / 4;
+  static_assert(PKV_SLOTS % 64 == 0, "PKV staging by whole waves");
+  auto stage_pkv = [&](int hh) {
+    if (wave * 64 < PKV_SLOTS) {
+      const int l = wave * 64 + lane;
+      const int which = l / (T * DH / 4), t = (l / (DH / 4)) % T, c4 = l % (DH / 4);
+      const float* src = (which ? PV : PK) + t * D + hh * DH + 4 * c4;
+      __builtin_amdgcn_global_load_lds((const void*)src,
+                                       (__attribute__((address_space(3))) void*)(&PKV[hh & 1][0][0] + wave * 256), 16,
+                                       0, 0);
+    }
+  };
   stage(0, 0);
+  stage_pkv(0);
   __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();  // chunk 0 staged; Qs complete; X_last rows no longer needed
+  __syncthreads();  // chunk 0 and head 0's P rows staged; Qs complete; X_last rows no longer needed
 
   const float scale = a.scale;
   float prob[RFW];
@@ -216,6 +232,9 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
         }
         __builtin_amdgcn_s_waitcnt(0);  // this wave's part of chunk c + 1 has landed
         __syncthreads();
+        // every wave is past head h - 1, the last reader of PKV[(h + 1) & 1]:
+        // stage head h + 1's P rows there (waited for at the next chunk barrier)
+        if (pass == 0 && ck == 0 && h + 1 < H) stage_pkv(h + 1);
       }
       // lane holds K_h or V_h [row = wave*RW + rf*16 + lc][c = f*16 + 4*lg + r]
 #pragma unroll
@@ -224,8 +243,8 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
         const int m = row / T, t = row - m * T;
         const int64_t n = tile0 + m;
         const bool live = n < N;
-        // positional part of the token's projection
-        const float* pp = (pass == 0 ? PK : PV) + t * D + h * DH + 4 * lg;
+        // positional part of the token's projection (this head's rows, staged in LDS)
+        const float* pp = &PKV[h & 1][pass][0] + t * DH + 4 * lg;
 #pragma unroll
         for (int f = 0; f < NFH; ++f) {
           const float4 p4 = *reinterpret_cast<const float4*>(pp + f * 16);
