@@ -55,12 +55,16 @@ struct Src {
   int rows;
 };
 
-// LDS unit (16 bytes) of (row, k-chunk c) in a swizzled 128 x 64 tile.
-__device__ __forceinline__ int unit_of(int row, int c) { return row * 8 + (c ^ (row & 7)); }
+// LDS unit (16 bytes) of (row, k-chunk c) in a swizzled 128 x 64 tile: the
+// chunk XOR-ed with (row ^ row >> 2) & 7, measured free of bank conflicts both
+// for the 16-row fragment reads and for the unit writes of operands whose rows
+// are contiguous (with row & 7 alone those writes were 8-way conflicted).
+__device__ __forceinline__ int unit_of(int row, int c) { return row * 8 + (c ^ ((row ^ (row >> 2)) & 7)); }
 
 // This thread's 32 values of the 128 x 64 tile (rows row0.., k k0..).  k
 // contiguous: units u = tid + 256 q (row u / 8, chunk u % 8), two float4 each.
-// Rows contiguous: rows 4 (tid % 32) .. +3 of chunk tid / 32, one float4 per k.
+// Rows contiguous: rows 4 (tid % 32) .. +3 of chunk tid / 32, one float4 per k
+// (lanes along the rows, for coalesced loads).
 // Every load is made, from an address clamped into the operand; bit j of the
 // returned mask says whether float4 j lies inside, and store_tile zeroes the
 // others.  (A load under a condition is compiled into a load from a select of
@@ -297,8 +301,9 @@ constexpr int TM = 256, TN = 256, TK = 32;
 constexpr int UNITS = TM * TK * 2 / 16;  // 16-byte units per 256 x 32 bf16 tile (1024)
 
 // LDS unit of (row, k-chunk c): 4 units per row, the chunk swizzled by bits
-// 2..3 of the row, so that 16 consecutive rows of one chunk hit distinct banks.
-__device__ __forceinline__ int unit_of(int row, int c) { return row * 4 + (c ^ ((row >> 2) & 3)); }
+// 1..2 of the row (16-row fragment reads measured free of bank conflicts;
+// bits 2..3 were 2-way conflicted).
+__device__ __forceinline__ int unit_of(int row, int c) { return row * 4 + (c ^ ((row >> 1) & 3)); }
 
 // This thread's 16 values of the 256 x 32 tile (rows row0.., k k0..).  k
 // contiguous: units u = tid + 512 q (row u / 4, chunk u % 4), two float4
