@@ -164,7 +164,10 @@ int trace_debug_gather(trace_model* m, const uint8_t* d_streams, int64_t stride,
 
 /* Per-kernel timing with HIP events recorded on the caller's stream around each
  * launch (measurement support; off by default).  While enabled, every kernel
- * launch of the calls above is bracketed by two events; trace_read_timing waits
+ * launch of the calls above is bracketed by two events (the Adam kernel's
+ * dispatch records its two itself, so that region is the kernel's own start to
+ * end, without the gap an event pair around one short launch adds; the other
+ * kinds span all their kernels' launches); trace_read_timing waits
  * for them, returns per-kind totals (milliseconds) and launch counts in arrays
  * of TRACE_NKINDS entries, and starts a new measurement.  At most 65536 launches
  * are recorded between reads; later ones are counted in overflow. */

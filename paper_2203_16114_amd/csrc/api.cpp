@@ -98,8 +98,8 @@ hipStream_t S(void* s) { return (hipStream_t)s; }
 
 constexpr size_t MAX_TIMED = 65536;
 
-// Starts a timed region of `kind` on stream s; returns its index or -1.
-long tbegin(trace_model* m, hipStream_t s) {
+// Reserves a timed region (two events); returns its index or -1.
+long treserve(trace_model* m) {
   if (!m->timing) return -1;
   if (m->ev_kind.size() >= MAX_TIMED) {
     m->overflow += 1;
@@ -111,9 +111,14 @@ long tbegin(trace_model* m, hipStream_t s) {
     m->events.push_back(e);
   }
   const long i = (long)m->ev_kind.size();
-  (void)hipEventRecord(m->events[m->ev_used], s);
   m->ev_used += 2;
   m->ev_kind.push_back(-1);
+  return i;
+}
+// Starts a timed region of `kind` on stream s; returns its index or -1.
+long tbegin(trace_model* m, hipStream_t s) {
+  const long i = treserve(m);
+  if (i >= 0) (void)hipEventRecord(m->events[2 * i], s);
   return i;
 }
 void tend(trace_model* m, long i, int kind, hipStream_t s) {
@@ -122,27 +127,46 @@ void tend(trace_model* m, long i, int kind, hipStream_t s) {
   m->ev_kind[i] = kind;
 }
 
-// Refresh the operand copies from the fp32 master.
-void refresh_operands(trace_model* m, hipStream_t s) {
+// Refresh the operand copies from the fp32 master (one launch).
+bool refresh_operands(trace_model* m, hipStream_t s) {
   const long tk = tbegin(m, s);
   const Layout& L = m->L;
   const int D = L.D, F = m->cfg.F;
   const float* th = m->theta;
-  launch_cvt(m->bf, th + L.off[P_E], m->Ec, L.size[P_E], s);
-  if (m->cfg.use_pos)
-    launch_cvt(m->bf, th + L.off[P_P], m->Pc, L.size[P_P], s);
-  else
-    launch_zero(m->Pc, (L.size[P_P] * (m->bf ? 2 : 4) + 3) / 4, s);
-  launch_ptab(m->bf, m->Pc, th + L.off[P_WQ], th + L.off[P_WK], th + L.off[P_WV], L.T, D, m->PW, s);
-  launch_pack(m->bf, th + L.off[P_WQ], D, D, m->Wq, s);
-  launch_pack(m->bf, th + L.off[P_WK], D, D, m->Wk, s);
-  launch_pack(m->bf, th + L.off[P_WV], D, D, m->Wv, s);
-  launch_pack(m->bf, th + L.off[P_WO], D, D, m->Wo, s);
-  launch_pack(m->bf, th + L.off[P_W1], D, F, m->W1, s);
-  // bf16: W2/2 (exact), since the bf16 FFN kernel forms 2 GELU(U) (exact in bf16 too)
-  launch_pack(m->bf, th + L.off[P_W2], F, D, m->W2, s, m->bf ? 0.5f : 1.f);
-  launch_pack(m->bf, th + L.off[P_WOUT], D, 256, m->Wout, s);
+  const bool pos = m->cfg.use_pos != 0;
+  auto job = [](int kind, const float* src, void* dst, int64_t K, int N, float scale = 1.f) {
+    RefreshJob j;
+    j.src = src;
+    j.src2 = nullptr;
+    j.dst = dst;
+    j.kind = kind;
+    j.K = (int)K;
+    j.N = N;
+    j.use_pos = 0;
+    j.scale = scale;
+    return j;
+  };
+  RefreshJob pt = job(RJ_PTAB, th + L.off[P_P], m->PW, L.T, D);
+  pt.src2 = th + L.off[P_WQ];  // W_q, W_k, W_v are consecutive D x D blocks of the master
+  pt.use_pos = pos;
+  // the positional table's blocks run longest: they are dispatched first
+  const RefreshJob jobs[] = {
+      pt,
+      job(RJ_PACK, th + L.off[P_W1], m->W1, D, F),
+      // bf16: W2/2 (exact), since the bf16 FFN kernel forms 2 GELU(U) (exact in bf16 too)
+      job(RJ_PACK, th + L.off[P_W2], m->W2, F, D, m->bf ? 0.5f : 1.f),
+      job(RJ_PACK, th + L.off[P_WQ], m->Wq, D, D),
+      job(RJ_PACK, th + L.off[P_WK], m->Wk, D, D),
+      job(RJ_PACK, th + L.off[P_WV], m->Wv, D, D),
+      job(RJ_PACK, th + L.off[P_WO], m->Wo, D, D),
+      job(RJ_PACK, th + L.off[P_WOUT], m->Wout, D, 256),
+      job(RJ_CVT, th + L.off[P_E], m->Ec, L.size[P_E], 0),
+      pos ? job(RJ_CVT, th + L.off[P_P], m->Pc, L.size[P_P], 0)
+          : job(RJ_ZERO, nullptr, m->Pc, (L.size[P_P] * (m->bf ? 2 : 4) + 3) / 4, 0),
+  };
+  const bool ok = launch_refresh(m->bf, jobs, (int)(sizeof(jobs) / sizeof(jobs[0])), s);
   tend(m, tk, TRACE_KIND_REFRESH, s);
+  return ok;
 }
 
 GemmArgs gemm(int M, int N, int K, const float* A, int64_t sam, int64_t sak, int rA, const float* B, int64_t sbk,
@@ -226,10 +250,12 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
   if (e == hipSuccess) e = hipMemset(m->am, 0, n * 4);
   if (e == hipSuccess) e = hipMemset(m->av, 0, n * 4);
   if (e == hipSuccess) e = hipMemset(m->grad, 0, n * 4);
-  if (e == hipSuccess) {
-    refresh_operands(m, nullptr);
-    e = hipDeviceSynchronize();
+  if (e == hipSuccess && !refresh_operands(m, nullptr)) {
+    free_all(m);
+    delete m;
+    return fail(TRACE_EUNSUPPORTED, "no operand refresh for this shape");
   }
+  if (e == hipSuccess) e = hipDeviceSynchronize();
   if (e != hipSuccess) {
     rc = hip_fail(e, "trace_create");
     free_all(m);
@@ -438,10 +464,12 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   m->step += 1;
   const float bc1 = (float)(1.0 - std::pow(m->cfg.beta1, (double)m->step));
   const float bc2 = (float)(1.0 - std::pow(m->cfg.beta2, (double)m->step));
-  const long ta = tbegin(m, s);
+  // one kernel: its dispatch records the two events itself, so the region is the kernel's own duration
+  const long ta = treserve(m);
   launch_adam(th, gr, m->am, m->av, L.n, (float)m->cfg.lr, (float)m->cfg.beta1, (float)m->cfg.beta2,
-              (float)m->cfg.eps, bc1, bc2, s);
-  tend(m, ta, TRACE_KIND_ADAM, s);
+              (float)m->cfg.eps, bc1, bc2, s, ta >= 0 ? m->events[2 * ta] : nullptr,
+              ta >= 0 ? m->events[2 * ta + 1] : nullptr);
+  if (ta >= 0) m->ev_kind[ta] = TRACE_KIND_ADAM;
   refresh_operands(m, s);
   m->kept = false;
   const hipError_t e = hipGetLastError();

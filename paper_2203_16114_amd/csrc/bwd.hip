@@ -7,6 +7,8 @@
 #include "kcommon.h"
 #include "kernels.h"
 
+#include <hip/hip_ext.h>
+
 // ------------------------------------------------------------ generic GEMM ----
 // C(m,n) [+]= sum_k A(m,k) B(k,n) for arbitrary element strides.  64x64 output
 // tile per workgroup, 4 waves in a 2x2 layout of 32x32 sub-tiles; the k range
@@ -779,8 +781,9 @@ __global__ void k_adam(float* __restrict__ theta, const float* __restrict__ grad
   }
 }
 void launch_adam(float* theta, const float* grad, float* m, float* v, int64_t n, float lr, float b1, float b2,
-                 float eps, float bc1, float bc2, hipStream_t s) {
+                 float eps, float bc1, float bc2, hipStream_t s, hipEvent_t t0, hipEvent_t t1) {
   const int64_t threads = n / 4 + n % 4;
-  hipLaunchKernelGGL(k_adam, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, theta, grad, m, v, n, lr, b1,
-                     b2, eps, bc1, bc2);
+  // t0 / t1 (may be null) take the dispatch's own start and end time stamps
+  hipExtLaunchKernelGGL(k_adam, dim3((unsigned)((threads + 255) / 256)), dim3(256), 0, s, t0, t1, 0, theta, grad, m,
+                        v, n, lr, b1, b2, eps, bc1, bc2);
 }

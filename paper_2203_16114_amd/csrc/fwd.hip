@@ -10,7 +10,7 @@
 //               chunks, h kept in accumulator registers -> z = h.Wout + bout -> bits
 // This file holds the small kernels around them: operand packing, the gather
 // used by tests, and the per-step mean code length.
-// Weights are read from L2 in a fragment-packed layout (see k_pack), one 16-byte
+// Weights are read from L2 in a fragment-packed layout (see refresh_pack), one 16-byte
 // load per lane per 16x16 fragment; activations stay in LDS or registers.  The
 // only per-window HBM traffic is the window bytes, h0 (d floats written and read
 // once) and the code length.
@@ -19,16 +19,24 @@
 
 #include "win.h"
 
-// ------------------------------------------------------------------ packing ----
-// W [K][N] row-major fp32 -> fragment-packed operand copy: fragment (ks, nb) is
-// 64 lanes x 16 bytes at offset ((ks * N/16 + nb) * 64 + lane) * 16; lane l holds
-// column nb*16 + l%16 and k = ks*KS + (l/16)*EPF + j, j < EPF.  Each value is
-// multiplied by scale (a power of two, so the operand is the scaled rounded value).
+// ------------------------------------------------------------------ refresh ----
+// Every operand copy of the model is derived from the fp32 master in one launch:
+// each job (kernels.h) owns a consecutive range of blocks, and a block finds its
+// job by comparing its index with the ranges' starts.
+struct RefreshArgs {
+  RefreshJob job[REFRESH_MAX_JOBS];
+  int b0[REFRESH_MAX_JOBS + 1];  // first block of each job; b0[n] = grid size
+  int n;
+};
+
+// Fragment-packed operand copy: fragment (ks, nb) of W [K][N] is 64 lanes x 16
+// bytes at offset ((ks * N/16 + nb) * 64 + lane) * 16; lane l holds column
+// nb*16 + l%16 and k = ks*KS + (l/16)*EPF + j, j < EPF.  Each value is multiplied
+// by scale (a power of two, so the operand is the scaled rounded value).
 template <bool BF>
-__global__ void k_pack(const float* __restrict__ W, int K, int N, uint4* __restrict__ out, float scale) {
+__device__ __forceinline__ void refresh_pack(const RefreshJob& jb, int64_t i) {
   typedef Mma<BF> M;
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int NB = N / 16, KSN = K / M::KS;
+  const int NB = jb.N / 16, KSN = jb.K / M::KS;
   if (i >= (int64_t)KSN * NB * 64) return;
   const int lane = (int)(i & 63);
   const int64_t f = i >> 6;
@@ -37,75 +45,130 @@ __global__ void k_pack(const float* __restrict__ W, int K, int N, uint4* __restr
   const int kb = ks * M::KS + (lane >> 4) * M::EPF;
   float v[8];
 #pragma unroll
-  for (int j = 0; j < M::EPF; ++j) v[j] = W[(int64_t)(kb + j) * N + n] * scale;
+  for (int j = 0; j < M::EPF; ++j) v[j] = jb.src[(int64_t)(kb + j) * jb.N + n] * jb.scale;
   union { uint4 u; typename M::T t[M::EPF]; } r;
 #pragma unroll
   for (int j = 0; j < M::EPF; ++j) r.t[j] = M::cvt(v[j]);
-  out[i] = r.u;
+  reinterpret_cast<uint4*>(jb.dst)[i] = r.u;
 }
 
-void launch_pack(bool bf, const float* W, int K, int N, void* out, hipStream_t s, float scale) {
-  const int KS = bf ? 32 : 16;
-  const int64_t total = (int64_t)(K / KS) * (N / 16) * 64;
-  const dim3 grid((unsigned)((total + 255) / 256));
-  if (bf)
-    hipLaunchKernelGGL(k_pack<true>, grid, dim3(256), 0, s, W, K, N, (uint4*)out, scale);
-  else
-    hipLaunchKernelGGL(k_pack<false>, grid, dim3(256), 0, s, W, K, N, (uint4*)out, scale);
-}
-
-// Positional parts of the projections: PW[w][t][j] = sum_i P[t][i] W_w[i][j] for
-// w = q, k, v, in fp32 (eight partial sums over consecutive eighths of i, added in
-// order), from the operand values of P
-// and of the weights (bf16-rounded in BF16 mode).  A token's projection is then
-// E-part (an MFMA on the rounded byte embeddings) + PW[w][t]: X.W = E.W + P.W.
-template <bool BF>
-__global__ __launch_bounds__(512) void k_ptab(const typename Mma<BF>::T* __restrict__ P, const float* __restrict__ Wq,
-                                              const float* __restrict__ Wk, const float* __restrict__ Wv, int T, int D,
-                                              float* __restrict__ PW) {
-  // block (w*T + t, j-block): 64 columns j; its 8 waves sum over the 8 eighths of
-  // k, and the 8 partial sums are added in k order
+// Positional parts of the projections, PW[w][t][j] = sum_i P[t][i] W_w[i][j]
+// (w = q, k, v), in fp32 from the operand values of P and of the weights, so that
+// a token's projection is an MFMA on the rounded byte embeddings plus PW[w][t]:
+// X.W = E.W + P.W.  A block takes 16 columns j of one W_w for every token t; its
+// 16 thread groups of 16 take consecutive sixteenths of i, read each weight value
+// once for all tokens, and their 16 partial sums are added in i order.
+constexpr int PTAB_TMAX = 8, PTAB_DMAX = 512;
+template <bool BF, int T>
+__device__ __forceinline__ void refresh_ptab(const RefreshJob& jb, int lb, float* Pv, float* part) {
   typedef Mma<BF> M;
-  __shared__ float part[8][64];
-  const int wt = blockIdx.x, w = wt / T, t = wt - w * T;
-  const int j = blockIdx.y * 64 + (threadIdx.x & 63), kg = threadIdx.x >> 6;
-  const float* Wm = w == 0 ? Wq : (w == 1 ? Wk : Wv);
-  const int kl = D / 8, k0 = kg * kl;
-  float s = 0.f;
-  if (j < D) {
-#pragma unroll 4
-    for (int k = k0; k < k0 + kl; ++k) s = fmaf(M::val(P[t * D + k]), M::val(M::cvt(Wm[(int64_t)k * D + j])), s);
-  }
-  part[kg][threadIdx.x & 63] = s;
+  const int D = jb.N, nbw = D / 16;
+  const int w = lb / nbw, j = (lb - w * nbw) * 16 + (threadIdx.x & 15), kg = threadIdx.x >> 4;
+  for (int i = threadIdx.x; i < T * D; i += 256) Pv[i] = jb.use_pos ? M::val(M::cvt(jb.src[i])) : 0.f;
   __syncthreads();
-  if (kg == 0 && j < D) {
-    float r = part[0][threadIdx.x];
+  const float* Wm = jb.src2 + (int64_t)w * D * D + j;
+  const int kl = D / 16, k0 = kg * kl;  // kl is a multiple of 4 (D a multiple of 64)
+  float acc[T];
 #pragma unroll
-    for (int q = 1; q < 8; ++q) r += part[q][threadIdx.x];
-    PW[(int64_t)wt * D + j] = r;
+  for (int t = 0; t < T; ++t) acc[t] = 0.f;
+#pragma unroll 4
+  for (int k = k0; k < k0 + kl; k += 4) {
+    float wv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) wv[u] = Wm[(int64_t)(k + u) * D];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) wv[u] = M::val(M::cvt(wv[u]));
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const float4 p = *reinterpret_cast<const float4*>(Pv + t * D + k);
+      acc[t] = fmaf(p.x, wv[0], acc[t]);
+      acc[t] = fmaf(p.y, wv[1], acc[t]);
+      acc[t] = fmaf(p.z, wv[2], acc[t]);
+      acc[t] = fmaf(p.w, wv[3], acc[t]);
+    }
   }
-}
-
-void launch_ptab(bool bf, const void* P, const float* Wq, const float* Wk, const float* Wv, int T, int D, float* PW,
-                 hipStream_t s) {
-  const dim3 grid((unsigned)(3 * T), (unsigned)((D + 63) / 64));
-  if (bf)
-    hipLaunchKernelGGL(k_ptab<true>, grid, dim3(512), 0, s, (const uint16_t*)P, Wq, Wk, Wv, T, D, PW);
-  else
-    hipLaunchKernelGGL(k_ptab<false>, grid, dim3(512), 0, s, (const float*)P, Wq, Wk, Wv, T, D, PW);
+#pragma unroll
+  for (int t = 0; t < T; ++t) part[(kg * T + t) * 16 + (threadIdx.x & 15)] = acc[t];
+  __syncthreads();
+  if ((int)threadIdx.x < T * 16) {
+    const int t = threadIdx.x >> 4, c = threadIdx.x & 15;
+    float r = part[t * 16 + c];
+#pragma unroll
+    for (int q = 1; q < 16; ++q) r += part[(q * T + t) * 16 + c];
+    reinterpret_cast<float*>(jb.dst)[(int64_t)(w * T + t) * D + (lb - w * nbw) * 16 + c] = r;
+  }
 }
 
 template <bool BF>
-__global__ void k_cvt(const float* __restrict__ src, typename Mma<BF>::T* __restrict__ dst, int64_t n) {
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i < n) dst[i] = Mma<BF>::cvt(src[i]);
+__global__ __launch_bounds__(256) void k_refresh(RefreshArgs a) {
+  __shared__ float Pv[PTAB_TMAX * PTAB_DMAX];
+  __shared__ float part[16 * PTAB_TMAX * 16];
+  const int b = (int)blockIdx.x;
+  int q = 0;
+#pragma unroll
+  for (int u = 1; u < REFRESH_MAX_JOBS; ++u) q += (u < a.n && b >= a.b0[u]) ? 1 : 0;
+  // the job's fields, selected with constant indexes (the block index is uniform)
+  RefreshJob jb = a.job[0];
+  int b0 = a.b0[0];
+#pragma unroll
+  for (int u = 1; u < REFRESH_MAX_JOBS; ++u)
+    if (q == u) {
+      jb = a.job[u];
+      b0 = a.b0[u];
+    }
+  const int lb = b - b0;
+  const int64_t i = (int64_t)lb * 256 + threadIdx.x;
+  typedef Mma<BF> M;
+  if (jb.kind == RJ_CVT) {
+    if (i < jb.K) reinterpret_cast<typename M::T*>(jb.dst)[i] = M::cvt(jb.src[i]);
+  } else if (jb.kind == RJ_PACK) {
+    refresh_pack<BF>(jb, i);
+  } else if (jb.kind == RJ_PTAB) {
+    if (jb.K == 8)
+      refresh_ptab<BF, 8>(jb, lb, Pv, part);
+    else
+      refresh_ptab<BF, 4>(jb, lb, Pv, part);
+  } else {
+    if (i < jb.K) reinterpret_cast<uint32_t*>(jb.dst)[i] = 0u;
+  }
 }
-void launch_cvt(bool bf, const float* src, void* dst, int64_t n, hipStream_t s) {
-  const dim3 grid((unsigned)((n + 255) / 256));
+
+bool launch_refresh(bool bf, const RefreshJob* jobs, int n, hipStream_t s) {
+  if (n < 1 || n > REFRESH_MAX_JOBS) return false;
+  RefreshArgs a;
+  int b = 0;
+  for (int u = 0; u < n; ++u) {
+    const RefreshJob& jb = jobs[u];
+    int64_t nb = 0;
+    if (jb.kind == RJ_CVT || jb.kind == RJ_ZERO) {
+      nb = ((int64_t)jb.K + 255) / 256;
+    } else if (jb.kind == RJ_PACK) {
+      const int KS = bf ? 32 : 16;
+      if (jb.K % KS != 0 || jb.N % 16 != 0) return false;
+      nb = ((int64_t)(jb.K / KS) * (jb.N / 16) * 64 + 255) / 256;
+    } else if (jb.kind == RJ_PTAB) {
+      if ((jb.K != 4 && jb.K != 8) || jb.N > PTAB_DMAX || jb.N % 64 != 0) return false;
+      nb = 3 * (int64_t)(jb.N / 16);
+    } else {
+      return false;
+    }
+    if (jb.K < 0 || b + nb > (1 << 30)) return false;
+    a.job[u] = jb;
+    a.b0[u] = b;
+    b += (int)nb;
+  }
+  for (int u = n; u < REFRESH_MAX_JOBS; ++u) {
+    a.job[u] = jobs[0];
+    a.b0[u] = b;
+  }
+  a.b0[REFRESH_MAX_JOBS] = b;
+  a.n = n;
+  if (b == 0) return true;
   if (bf)
-    hipLaunchKernelGGL(k_cvt<true>, grid, dim3(256), 0, s, src, (uint16_t*)dst, n);
+    hipLaunchKernelGGL(k_refresh<true>, dim3((unsigned)b), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(k_cvt<false>, grid, dim3(256), 0, s, src, (float*)dst, n);
+    hipLaunchKernelGGL(k_refresh<false>, dim3((unsigned)b), dim3(256), 0, s, a);
+  return true;
 }
 
 __global__ void k_zero(uint32_t* __restrict__ p, int64_t n) {

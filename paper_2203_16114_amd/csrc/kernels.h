@@ -53,13 +53,26 @@ typedef void (*ffn_fn)(const FfnArgs&, hipStream_t);
 attn_fn find_attn(bool bf, int T, int D, int DH);
 ffn_fn find_ffn(bool bf, int D);
 
-void launch_pack(bool bf, const float* W, int K, int N, void* out, hipStream_t s, float scale = 1.f);
 void launch_zero(void* p, int64_t n32, hipStream_t s);
-void launch_cvt(bool bf, const float* src, void* dst, int64_t n, hipStream_t s);
 void launch_step_ce(const float* bits, int32_t n_streams, int32_t n_steps, double* out, hipStream_t s);
-// PW[w][t][:] = P[t] . W_w for w = q, k, v (W_* the fp32 master, rounded as operands)
-void launch_ptab(bool bf, const void* P, const float* Wq, const float* Wk, const float* Wv, int T, int D, float* PW,
-                 hipStream_t s);
+// One part of the operand refresh (all parts run in one launch):
+//   RJ_CVT   dst[i] = operand(src[i]), i < K
+//   RJ_PACK  fragment-packed operand copy of the [K][N] row-major src, each value times scale
+//   RJ_PTAB  PW[w][t][j] = sum_i P[t][i] W_w[i][j] for w = q, k, v, t < K (= T: 4 or 8), j < N (= D: a multiple
+//            of 64, at most 512), with the operand
+//            values of P (src; zero if use_pos is 0) and of W_q (src2, W_k and W_v following it in the master)
+//   RJ_ZERO  K 32-bit words of dst cleared
+enum { RJ_CVT = 0, RJ_PACK = 1, RJ_PTAB = 2, RJ_ZERO = 3 };
+struct RefreshJob {
+  const float* src;
+  const float* src2;
+  void* dst;
+  int kind, K, N, use_pos;
+  float scale;
+};
+constexpr int REFRESH_MAX_JOBS = 12;
+// Runs jobs[0..n) on stream s; false (nothing launched) for an unsupported job.
+bool launch_refresh(bool bf, const RefreshJob* jobs, int n, hipStream_t s);
 void launch_gather(bool bf, const WinArgs& w, const void* E, const void* P, int T, int D, int e, int g, float* X,
                    hipStream_t s);
 
@@ -109,4 +122,4 @@ void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, i
 // dW[i][j] += sum_{u < nt} P[t0 + u][i] * S[u][j]  (P: operand copy [T][D])
 void launch_pos_grad(bool bf, const void* P, const float* S, int t0, int nt, int D, float* dW, hipStream_t s);
 void launch_adam(float* theta, const float* grad, float* m, float* v, int64_t n, float lr, float b1, float b2,
-                 float eps, float bc1, float bc2, hipStream_t s);
+                 float eps, float bc1, float bc2, hipStream_t s, hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
