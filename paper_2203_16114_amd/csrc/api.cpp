@@ -37,8 +37,16 @@ struct trace_model {
   int32_t* ktgt;
   float *kq, *kK, *kV, *kA, *kO, *kY, *kU, *kG, *kZ;
   // backward scratch
+  // dY: gradients w.r.t. the k+1 residual states, dU: w.r.t. the k pre-GELU
+  // activations (one buffer per repeat, read by the weight gradients later)
   float *dz, *dY, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *sP, *gws, *cws, *ews;
   int64_t gws_cap;
+  // second stream of the update step (the weight-gradient branch), its own
+  // split-K and column-sum workspaces, and the events that order the two streams
+  hipStream_t side;
+  float *gws2, *cws2;
+  std::vector<hipEvent_t> sev;
+  size_t sev_next;
   std::vector<void*> allocs;
   // event timing (trace_set_timing)
   bool timing;
@@ -77,7 +85,24 @@ void free_all(trace_model* m) {
   m->allocs.clear();
   for (hipEvent_t e : m->events) (void)hipEventDestroy(e);
   m->events.clear();
+  for (hipEvent_t e : m->sev) (void)hipEventDestroy(e);
+  m->sev.clear();
+  if (m->side) (void)hipStreamDestroy(m->side);
+  m->side = nullptr;
 }
+
+// An event marking everything issued so far on stream `from`.  A wait applies
+// to the record made before it, so the events are reused round-robin; every
+// mark is waited for within a few marks of being made.
+hipEvent_t mark(trace_model* m, hipStream_t from) {
+  hipEvent_t e = m->sev[m->sev_next];
+  m->sev_next = (m->sev_next + 1) % m->sev.size();
+  (void)hipEventRecord(e, from);
+  return e;
+}
+void after(hipStream_t to, hipEvent_t e) { (void)hipStreamWaitEvent(to, e, 0); }
+// Work on stream `to` after everything issued so far on stream `from`.
+void order(trace_model* m, hipStream_t from, hipStream_t to) { after(to, mark(m, from)); }
 
 // The GEMM shapes (M, N, K) of trace_adapt_step for N kept windows.
 std::vector<std::array<int, 3>> adapt_gemm_shapes(const trace_model* m, int64_t N) {
@@ -232,14 +257,22 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
          dalloc(m, &m->kA, K * cfg->H * T * 4) && dalloc(m, &m->kO, K * D * 4) &&
          dalloc(m, &m->kY, (cfg->k + 1) * K * D * 4) && dalloc(m, &m->kU, cfg->k * K * F * 4) &&
          (!bf || dalloc(m, &m->kG, cfg->k * K * F * 4)) &&
-         dalloc(m, &m->kZ, K * 256 * 4) && dalloc(m, &m->dz, K * 256 * 4) && dalloc(m, &m->dY, K * D * 4) &&
-         dalloc(m, &m->dU, K * F * 4) && (bf || dalloc(m, &m->G, K * F * 4)) &&
+         dalloc(m, &m->kZ, K * 256 * 4) && dalloc(m, &m->dz, K * 256 * 4) &&
+         dalloc(m, &m->dY, (cfg->k + 1) * K * D * 4) && dalloc(m, &m->dU, cfg->k * K * F * 4) &&
+         (bf || dalloc(m, &m->G, K * F * 4)) &&
          dalloc(m, &m->dO, K * D * 4) && dalloc(m, &m->dQ, K * D * 4) && dalloc(m, &m->dK, K * T * D * 4) &&
          dalloc(m, &m->dV, K * T * D * 4) && dalloc(m, &m->dX, K * T * D * 4) && dalloc(m, &m->Xk, K * T * D * 4) &&
-         dalloc(m, &m->sP, T * D * 4) &&
+         dalloc(m, &m->sP, (T + 1) * D * 4) &&
          dalloc(m, &m->gws, (m->gws_cap = adapt_gemm_ws(m, K)) * 4) &&
          dalloc(m, &m->ews, embed_bwd_ws_floats(K * W, cfg->e) * 4) &&
-         dalloc(m, &m->cws, colsum_ws_floats(std::max<int64_t>(std::max<int64_t>(T * D, 256), 256 * cfg->e)) * 4);
+         dalloc(m, &m->cws, colsum_ws_floats(std::max<int64_t>(std::max<int64_t>(T * D, 256), 256 * cfg->e)) * 4) &&
+         dalloc(m, &m->gws2, m->gws_cap * 4) && dalloc(m, &m->cws2, colsum_ws_floats(T * D) * 4);
+    if (ok) ok = hipStreamCreateWithFlags(&m->side, hipStreamNonBlocking) == hipSuccess;
+    for (int i = 0; ok && i < 16; ++i) {
+      hipEvent_t ev;
+      ok = hipEventCreateWithFlags(&ev, hipEventDisableTiming) == hipSuccess;
+      if (ok) m->sev.push_back(ev);
+    }
   }
   if (!ok) {
     free_all(m);
@@ -400,65 +433,87 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   float* gr = m->grad;
   float* ws = m->gws;
   const long tk = tbegin(m, s);
+  // Two streams: s carries the chain of input gradients (dY, dU, dO, dQ/dK/dV,
+  // dX, dE) without waiting; `side` computes most weight gradients from the
+  // per-repeat buffers that chain leaves behind.  They meet three times (after
+  // dz, after the attention backward, before Adam): a wait across streams costs
+  // several microseconds.  The side stream has its own split-K and column-sum
+  // workspaces of the same sizes, so every product is the same as on one stream.
+  const hipStream_t w = m->side;
+  float* ws2 = m->gws2;
+  auto dYr = [&](int r) { return m->dY + (int64_t)r * N * D; };  // w.r.t. the input of repeat r (r = k: Y_k)
+  auto dUr = [&](int r) { return m->dU + (int64_t)r * N * F; };
   // head: dz = (softmax(z) - onehot) / N
   launch_ce_grad(m->kZ, m->ktgt, N, m->dz, s);
-  // dWout = h_k^T . dz ; dbout = sum_n dz ; dY_k = dz . Wout^T
+  order(m, s, w);
+  // side: the byte-embedding part of the tokens (read by the projection
+  // gradients), dWout = h_k^T . dz and dbout = sum_n dz
+  launch_gather_kept(m->bf, m->kwin, N, m->Ec, T, D, m->cfg.e, m->cfg.g, m->Xk, w);
   const float* Yk = m->kY + (int64_t)k * N * D;
-  launch_gemm(gemm(D, 256, N, Yk, 1, D, rb, m->dz, 256, 1, rb, gr + L.off[P_WOUT], 256, 0.f), ws, m->gws_cap, s);
-  launch_colsum(m->dz, N, 256, 256, gr + L.off[P_BOUT], 0.f, m->cws, s);
-  launch_gemm(gemm(N, D, 256, m->dz, 256, 1, rb, th + L.off[P_WOUT], 1, 256, rb, m->dY, D, 0.f), ws, m->gws_cap, s);
-  // shared FFN, repeats in reverse; W1 and W2 gradients accumulate over repeats
+  launch_gemm(gemm(D, 256, N, Yk, 1, D, rb, m->dz, 256, 1, rb, gr + L.off[P_WOUT], 256, 0.f), ws2, m->gws_cap, w);
+  launch_colsum(m->dz, N, 256, 256, gr + L.off[P_BOUT], 0.f, m->cws2, w);
+  // dY_k = dz . Wout^T
+  launch_gemm(gemm(N, D, 256, m->dz, 256, 1, rb, th + L.off[P_WOUT], 1, 256, rb, dYr(k), D, 0.f), ws, m->gws_cap, s);
+  // shared FFN, repeats in reverse: dU_r = (dY_{r+1} . W2^T) * GELU'(U_r),
+  // dY_r = dY_{r+1} + dU_r . W1^T
   for (int r = k - 1; r >= 0; --r) {
-    const float* Ur = m->kU + (int64_t)r * N * F;
-    // G = GELU(U) at its storage point: kept by the bf16 forward, formed here otherwise
-    const float* Gr = m->kG ? m->kG + (int64_t)r * N * F : m->G;
-    const float* Yr = m->kY + (int64_t)r * N * D;
-    const float beta = (r == k - 1) ? 0.f : 1.f;
-    if (!m->kG) launch_gelu_fwd_round(Ur, m->G, (int64_t)N * F, rb, s);
-    launch_gemm(gemm(F, D, N, Gr, 1, F, rb, m->dY, D, 1, rb, gr + L.off[P_W2], D, beta), ws, m->gws_cap, s);
-    // dU = (dY . W2^T) * GELU'(U)
-    GemmArgs gd = gemm(N, F, D, m->dY, D, 1, rb, th + L.off[P_W2], 1, D, rb, m->dU, F, 0.f);
-    gd.gelu_u = Ur;
+    GemmArgs gd = gemm(N, F, D, dYr(r + 1), D, 1, rb, th + L.off[P_W2], 1, D, rb, dUr(r), F, 0.f);
+    gd.gelu_u = m->kU + (int64_t)r * N * F;
     launch_gemm(gd, ws, m->gws_cap, s);
-    launch_gemm(gemm(D, F, N, Yr, 1, D, rb, m->dU, F, 1, rb, gr + L.off[P_W1], F, beta), ws, m->gws_cap, s);
-    launch_gemm(gemm(N, D, F, m->dU, F, 1, rb, th + L.off[P_W1], 1, F, rb, m->dY, D, 1.f), ws, m->gws_cap, s);
+    (void)hipMemcpyAsync(dYr(r), dYr(r + 1), (size_t)N * D * 4, hipMemcpyDeviceToDevice, s);
+    launch_gemm(gemm(N, D, F, dUr(r), F, 1, rb, th + L.off[P_W1], 1, F, rb, dYr(r), D, 1.f), ws, m->gws_cap, s);
   }
-  // attention output projection: dWo = O^T . dY0 ; dO = dY0 . Wo^T
-  launch_gemm(gemm(D, D, N, m->kO, 1, D, rb, m->dY, D, 1, rb, gr + L.off[P_WO], D, 0.f), ws, m->gws_cap, s);
-  launch_gemm(gemm(N, D, D, m->dY, D, 1, rb, th + L.off[P_WO], 1, D, rb, m->dO, D, 0.f), ws, m->gws_cap, s);
-  // attention (last query row) -> dQ, dK, dV
+  // attention output projection: dO = dY_0 . Wo^T, then the attention (last
+  // query row) -> dQ, dK, dV
+  launch_gemm(gemm(N, D, D, dYr(0), D, 1, rb, th + L.off[P_WO], 1, D, rb, m->dO, D, 0.f), ws, m->gws_cap, s);
   launch_attn_bwd(m->dO, m->kq, m->kK, m->kV, m->kA, N, T, D, H, (float)(1.0 / std::sqrt((double)L.DH)), rb, m->dQ,
                   m->dK, m->dV, s);
-  // projections: dWq = X_last^T dQ, dWk = X^T dK, dWv = X^T dV  (dQ, dK, dV stay fp32),
-  // with X = G + P[t]: G^T dZ as GEMMs on the byte-embedding part G, then
-  // P^T (sum over windows of dZ) for the positional part
-  launch_gather_kept(m->bf, m->kwin, N, m->Ec, T, D, m->cfg.e, m->cfg.g, m->Xk, s);
-  launch_gemm(gemm(D, D, N, m->Xk + (int64_t)(T - 1) * D, 1, (int64_t)T * D, rb, m->dQ, D, 1, 0, gr + L.off[P_WQ], D,
-                   0.f),
-              ws, m->gws_cap, s);
-  launch_gemm(gemm(D, D, N * T, m->Xk, 1, D, rb, m->dK, D, 1, 0, gr + L.off[P_WK], D, 0.f), ws, m->gws_cap, s);
-  launch_gemm(gemm(D, D, N * T, m->Xk, 1, D, rb, m->dV, D, 1, 0, gr + L.off[P_WV], D, 0.f), ws, m->gws_cap, s);
-  if (m->cfg.use_pos) {
-    launch_colsum(m->dQ, N, D, D, m->sP, 0.f, m->cws, s);
-    launch_pos_grad(m->bf, m->Pc, m->sP, T - 1, 1, D, gr + L.off[P_WQ], s);
-    launch_colsum(m->dK, N, (int64_t)T * D, (int64_t)T * D, m->sP, 0.f, m->cws, s);
-    launch_pos_grad(m->bf, m->Pc, m->sP, 0, T, D, gr + L.off[P_WK], s);
-    launch_colsum(m->dV, N, (int64_t)T * D, (int64_t)T * D, m->sP, 0.f, m->cws, s);
-    launch_pos_grad(m->bf, m->Pc, m->sP, 0, T, D, gr + L.off[P_WV], s);
+  order(m, s, w);  // every dY_r, dU_r, dQ, dK, dV is complete
+  // side: W2 and W1 gradients, accumulated over the repeats in reverse
+  // (dW2 += G_r^T . dY_{r+1}, dW1 += Y_r^T . dU_r, with G = GELU(U) at its
+  // storage point: kept by the bf16 forward, formed here otherwise)
+  for (int r = k - 1; r >= 0; --r) {
+    const float beta = (r == k - 1) ? 0.f : 1.f;
+    const float* Gr = m->kG ? m->kG + (int64_t)r * N * F : m->G;
+    if (!m->kG) launch_gelu_fwd_round(m->kU + (int64_t)r * N * F, m->G, (int64_t)N * F, rb, w);
+    launch_gemm(gemm(F, D, N, Gr, 1, F, rb, dYr(r + 1), D, 1, rb, gr + L.off[P_W2], D, beta), ws2, m->gws_cap, w);
+    launch_gemm(gemm(D, F, N, m->kY + (int64_t)r * N * D, 1, D, rb, dUr(r), F, 1, rb, gr + L.off[P_W1], F, beta), ws2,
+                m->gws_cap, w);
   }
-  // dX = dK Wk^T + dV Wv^T (+ dQ Wq^T + dY0 on the last token)
+  // side: dWk = X^T dK, dWv = X^T dV (dK, dV stay fp32), with X = G + P[t]:
+  // G^T dZ as GEMMs on the byte-embedding part G, then P^T (sum over windows of
+  // dZ) for the positional part
+  launch_gemm(gemm(D, D, N * T, m->Xk, 1, D, rb, m->dK, D, 1, 0, gr + L.off[P_WK], D, 0.f), ws2, m->gws_cap, w);
+  launch_gemm(gemm(D, D, N * T, m->Xk, 1, D, rb, m->dV, D, 1, 0, gr + L.off[P_WV], D, 0.f), ws2, m->gws_cap, w);
+  if (m->cfg.use_pos) {
+    launch_colsum(m->dK, N, (int64_t)T * D, (int64_t)T * D, m->sP, 0.f, m->cws2, w);
+    launch_pos_grad(m->bf, m->Pc, m->sP, 0, T, D, gr + L.off[P_WK], w);
+    launch_colsum(m->dV, N, (int64_t)T * D, (int64_t)T * D, m->sP, 0.f, m->cws2, w);
+    launch_pos_grad(m->bf, m->Pc, m->sP, 0, T, D, gr + L.off[P_WV], w);
+  }
+  // dX = dK Wk^T + dV Wv^T (+ dQ Wq^T + dY_0 on the last token)
   launch_gemm2(gemm(N * T, D, D, m->dK, D, 1, 0, th + L.off[P_WK], 1, D, rb, m->dX, D, 0.f),
                gemm(N * T, D, D, m->dV, D, 1, 0, th + L.off[P_WV], 1, D, rb, m->dX, D, 0.f), ws, m->gws_cap, s);
   launch_gemm(gemm(N, D, D, m->dQ, D, 1, 0, th + L.off[P_WQ], 1, D, rb, m->dX + (int64_t)(T - 1) * D, (int64_t)T * D,
                    1.f),
               ws, m->gws_cap, s);
-  launch_add(m->dX + (int64_t)(T - 1) * D, m->dY, N, D, (int64_t)T * D, D, s);
+  launch_add(m->dX + (int64_t)(T - 1) * D, dYr(0), N, D, (int64_t)T * D, D, s);
   // positional table and byte embedding
   if (m->cfg.use_pos)
     launch_colsum(m->dX, N, (int64_t)T * D, (int64_t)T * D, gr + L.off[P_P], 0.f, m->cws, s);
   else
     launch_zero(gr + L.off[P_P], L.size[P_P], s);
   launch_embed_bwd(m->kwin, m->dX, N, m->cfg.W, m->cfg.g, m->cfg.e, D, gr + L.off[P_E], m->ews, m->cws, s);
+  // dWo = O^T . dY_0 ; dWq = X_last^T dQ (+ its positional part)
+  launch_gemm(gemm(D, D, N, m->kO, 1, D, rb, dYr(0), D, 1, rb, gr + L.off[P_WO], D, 0.f), ws, m->gws_cap, s);
+  launch_gemm(gemm(D, D, N, m->Xk + (int64_t)(T - 1) * D, 1, (int64_t)T * D, rb, m->dQ, D, 1, 0, gr + L.off[P_WQ], D,
+                   0.f),
+              ws, m->gws_cap, s);
+  if (m->cfg.use_pos) {
+    launch_colsum(m->dQ, N, D, D, m->sP + (int64_t)T * D, 0.f, m->cws, s);
+    launch_pos_grad(m->bf, m->Pc, m->sP + (int64_t)T * D, T - 1, 1, D, gr + L.off[P_WQ], s);
+  }
+  order(m, w, s);  // every gradient is complete
   tend(m, tk, TRACE_KIND_BACKWARD, s);
   // Adam on the flat master, then new operand copies
   m->step += 1;
