@@ -227,6 +227,8 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
   if (cfg->e % 8 != 0 || cfg->e > 128) return fail(TRACE_EUNSUPPORTED, "e must be a multiple of 8, at most 128");
   if (cfg->F % 256 != 0) return fail(TRACE_EUNSUPPORTED, "F must be a multiple of 256");
   if (cfg->g > 64 || cfg->W > 64) return fail(TRACE_EUNSUPPORTED, "W must be at most 64 bytes");
+  if (cfg->max_keep * (int64_t)cfg->W >= ((int64_t)1 << 31))
+    return fail(TRACE_EUNSUPPORTED, "max_keep * W must be below 2^31");
   attn_fn af = find_attn(bf, L.T, L.D, L.DH);
   ffn_fn ff = find_ffn(bf, L.D);
   if (!af || !ff)
@@ -265,7 +267,7 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
          dalloc(m, &m->sP, (T + 1) * D * 4) &&
          dalloc(m, &m->gws, (m->gws_cap = adapt_gemm_ws(m, K)) * 4) &&
          dalloc(m, &m->ews, embed_bwd_ws_floats(K * W, cfg->e) * 4) &&
-         dalloc(m, &m->cws, colsum_ws_floats(std::max<int64_t>(std::max<int64_t>(T * D, 256), 256 * cfg->e)) * 4) &&
+         dalloc(m, &m->cws, colsum_ws_floats(std::max<int64_t>(T * D, 256)) * 4) &&
          dalloc(m, &m->gws2, m->gws_cap * 4) && dalloc(m, &m->cws2, colsum_ws_floats(T * D) * 4);
     if (ok) ok = hipStreamCreateWithFlags(&m->side, hipStreamNonBlocking) == hipSuccess;
     for (int i = 0; ok && i < 16; ++i) {
@@ -503,7 +505,7 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
     launch_colsum(m->dX, N, (int64_t)T * D, (int64_t)T * D, gr + L.off[P_P], 0.f, m->cws, s);
   else
     launch_zero(gr + L.off[P_P], L.size[P_P], s);
-  launch_embed_bwd(m->kwin, m->dX, N, m->cfg.W, m->cfg.g, m->cfg.e, D, gr + L.off[P_E], m->ews, m->cws, s);
+  launch_embed_bwd(m->kwin, m->dX, N, m->cfg.W, m->cfg.e, gr + L.off[P_E], m->ews, s);
   // dWo = O^T . dY_0 ; dWq = X_last^T dQ (+ its positional part)
   launch_gemm(gemm(D, D, N, m->kO, 1, D, rb, dYr(0), D, 1, rb, gr + L.off[P_WO], D, 0.f), ws, m->gws_cap, s);
   launch_gemm(gemm(D, D, N, m->Xk + (int64_t)(T - 1) * D, 1, (int64_t)T * D, rb, m->dQ, D, 1, 0, gr + L.off[P_WQ], D,

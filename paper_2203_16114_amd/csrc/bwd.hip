@@ -620,64 +620,272 @@ void launch_attn_bwd(const float* dO, const float* q, const float* K, const floa
 }
 
 // ------------------------------------------------------ embedding backward ----
-// dE[v][c] = sum over positions (n, p) with win[n][p] == v of
-// dX[n][p/g][(p%g)*e + c], in two deterministic passes.
-// Pass 1: block b takes a contiguous range of positions; its NG groups of e
-// threads take every NG-th position of the range in increasing order and add
-// the position's e-vector into the group's own LDS table [256][e]; the group
-// tables are then added in group order into part[b][256][e].
-// Pass 2: dE = sum over b of part[b], in block order (column sums).
-constexpr int EMB_LDS_FLOATS = 32768;  // 128 KiB of group tables
-__global__ __launch_bounds__(256) void k_embed_bwd_part(const uint8_t* __restrict__ win, const float* __restrict__ dX,
-                                                        int64_t total, int64_t chunk, int W, int g, int e, int D,
-                                                        float* __restrict__ part) {
-  __shared__ float tab[EMB_LDS_FLOATS];
-  const int NG = min(256 / e, EMB_LDS_FLOATS / (256 * e));
-  const int tid = threadIdx.x;
-  const int grp = tid / e, c = tid - grp * e;
-  for (int i = tid; i < NG * 256 * e; i += 256) tab[i] = 0.f;
+// dE[v][c] = sum over positions q = n*W + p with win[q] == v of dX[q*e + c]
+// (the W token slots of a window are W consecutive e-vectors of dX, D = g*e,
+// so position q reads row q of dX viewed as [N*W][e]).
+// Deterministic, with dX read once: the positions are counting-sorted by byte
+// value, stably (k_emb_hist, k_emb_colscan, k_emb_pieces, k_emb_scatter); each
+// byte's sorted run is cut into pieces of EMB_PIECE positions, each summed in
+// order by one wave (k_emb_piece); the pieces of a byte are added in a fixed
+// order (k_emb_sum).
+// The order of every sum depends on the input bytes alone.
+constexpr int EMB_CS = 2048;    // positions per block of the counting sort
+constexpr int EMB_PIECE = 256;  // positions per piece
+
+struct EmbWs {
+  int *cnt, *off, *tot, *base, *pstart, *piece, *perm;
+  float* part;
+};
+static EmbWs emb_ws(float* ws, int64_t M, int e) {
+  const int64_t nb = (M + EMB_CS - 1) / EMB_CS, pmax = (M + EMB_PIECE - 1) / EMB_PIECE + 256;
+  EmbWs w;
+  w.cnt = (int*)ws;
+  w.off = w.cnt + nb * 256;
+  w.tot = w.off + nb * 256;
+  w.base = w.tot + 256;
+  w.pstart = w.base + 256;
+  w.piece = w.pstart + 260;
+  w.perm = w.piece + 3 * pmax;
+  w.part = (float*)(w.perm + M);
+  (void)e;
+  return w;
+}
+int64_t embed_bwd_ws_floats(int64_t M, int e) {
+  const int64_t nb = (M + EMB_CS - 1) / EMB_CS, pmax = (M + EMB_PIECE - 1) / EMB_PIECE + 256;
+  return 2 * nb * 256 + 512 + 260 + 3 * pmax + M + pmax * e;
+}
+
+// cnt[b][v] = number of positions of block b (EMB_CS positions) holding byte v
+// (integer counts: the order of the LDS atomic adds does not matter)
+__global__ __launch_bounds__(1024) void k_emb_hist(const uint8_t* __restrict__ win, int M, int* __restrict__ cnt) {
+  __shared__ int h[256];
+  if (threadIdx.x < 256) h[threadIdx.x] = 0;
   __syncthreads();
-  const int64_t p0 = (int64_t)blockIdx.x * chunk;
-  const int64_t p1 = min(total, p0 + chunk);
-  // the W token slots of a window are W consecutive e-vectors of dX (D = g*e),
-  // so position q = n*W + t*g + j reads row q of dX viewed as [N*W][e]
-  if (grp < NG) {
-    float* my = tab + grp * 256 * e;
-    int64_t i = p0 + grp;
-    // eight positions at a time: loads first, then the table updates in order
-    for (; i + 7 * NG < p1; i += 8 * NG) {
-      int v[8];
-      float x[8];
+  const int q0 = blockIdx.x * EMB_CS;
+  for (int u = threadIdx.x; u < EMB_CS; u += 1024) {
+    const int q = q0 + u;
+    if (q < M) atomicAdd(&h[win[q]], 1);
+  }
+  __syncthreads();
+  if (threadIdx.x < 256) cnt[blockIdx.x * 256 + threadIdx.x] = h[threadIdx.x];
+}
+
+// Workgroup v: off[b][v] = number of v in blocks before b, tot[v] = all of them
+// (thread t takes a contiguous range of blocks; exclusive scan over threads).
+__global__ __launch_bounds__(256) void k_emb_colscan(const int* __restrict__ cnt, int nb, int* __restrict__ off,
+                                                     int* __restrict__ tot) {
+  __shared__ int sc[256];
+  const int v = blockIdx.x, t = threadIdx.x;
+  const int per = (nb + 255) / 256, b0 = min(nb, t * per), b1 = min(nb, b0 + per);
+  int s = 0;
+  for (int b = b0; b < b1; ++b) s += cnt[b * 256 + v];
+  sc[t] = s;
+  __syncthreads();
+  for (int d = 1; d < 256; d <<= 1) {
+    const int a = t >= d ? sc[t - d] : 0;
+    __syncthreads();
+    sc[t] += a;
+    __syncthreads();
+  }
+  int run = sc[t] - s;
+  for (int b = b0; b < b1; ++b) {
+    off[b * 256 + v] = run;
+    run += cnt[b * 256 + v];
+  }
+  if (t == 255) tot[v] = sc[255];
+}
+
+// One workgroup: base[v] = sorted position of the first v (counts of smaller
+// bytes); byte v's run is cut into pieces (v, first sorted position, length),
+// numbered from pstart[v]; pstart[256] = number of pieces.
+__global__ __launch_bounds__(1024) void k_emb_pieces(const int* __restrict__ tot, int* __restrict__ base,
+                                                     int* __restrict__ pstart, int* __restrict__ piece) {
+  __shared__ int tb[256], np[256], ps[257];
+  const int t = threadIdx.x;
+  int total = 0, npv = 0;
+  if (t < 256) {
+    total = tot[t];
+    npv = (total + EMB_PIECE - 1) / EMB_PIECE;
+    tb[t] = total;
+    np[t] = npv;
+  }
+  __syncthreads();
+  for (int d = 1; d < 256; d <<= 1) {
+    int a = 0, c = 0;
+    if (t < 256 && t >= d) {
+      a = tb[t - d];
+      c = np[t - d];
+    }
+    __syncthreads();
+    if (t < 256) {
+      tb[t] += a;
+      np[t] += c;
+    }
+    __syncthreads();
+  }
+  if (t < 256) {
+    base[t] = tb[t] - total;
+    ps[t] = np[t] - npv;
+    pstart[t] = np[t] - npv;
+  }
+  if (t == 0) {
+    ps[256] = np[255];
+    pstart[256] = np[255];
+  }
+  __syncthreads();
+  // piece j: its byte by binary search over ps
+  for (int j = t; j < ps[256]; j += 1024) {
+    int lo = 0, hi = 256;  // ps[lo] <= j < ps[hi]
+    while (hi - lo > 1) {
+      const int mid = (lo + hi) >> 1;
+      if (ps[mid] <= j)
+        lo = mid;
+      else
+        hi = mid;
+    }
+    const int k = j - ps[lo], bv = tb[lo] - (lo > 0 ? tb[lo - 1] : 0);
+    piece[3 * j] = lo;
+    piece[3 * j + 1] = (tb[lo] - bv) + k * EMB_PIECE;
+    piece[3 * j + 2] = min(EMB_PIECE, bv - k * EMB_PIECE);
+  }
+}
+
+// perm[sorted position] = position, stable: block b places its positions in
+// increasing order, 1024 per round; within a wave the rank among lanes with the
+// same byte comes from ballots on the byte's 8 bits, across the round's waves
+// from their counts in wave order.
+__global__ __launch_bounds__(1024) void k_emb_scatter(const uint8_t* __restrict__ win, int M,
+                                                      const int* __restrict__ off, const int* __restrict__ base,
+                                                      int* __restrict__ perm) {
+  __shared__ int run[256];
+  __shared__ int wc[16][256];
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  if (tid < 256) run[tid] = base[tid] + off[blockIdx.x * 256 + tid];
+  const int q0 = blockIdx.x * EMB_CS;
+  const uint64_t below = lane == 0 ? 0ull : (~0ull >> (64 - lane));
+  constexpr int R = EMB_CS / 1024;
+  int vr[R];
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const int64_t q = i + u * NG;
-        v[u] = win[q];
-        x[u] = dX[q * e + c];
+  for (int r = 0; r < R; ++r) vr[r] = win[min(q0 + r * 1024 + tid, M - 1)];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    for (int i = tid; i < 16 * 256; i += 1024) (&wc[0][0])[i] = 0;
+    __syncthreads();
+    const int q = q0 + r * 1024 + tid;
+    const bool live = q < M;
+    const int v = live ? vr[r] : 0;
+    uint64_t same = __ballot(live);
+#pragma unroll
+    for (int bit = 0; bit < 8; ++bit) {
+      const uint64_t bb = __ballot((v >> bit) & 1);
+      same &= ((v >> bit) & 1) ? bb : ~bb;
+    }
+    const int rank = __popcll(same & below);
+    if (live && rank == 0) wc[wv][v] = __popcll(same);
+    __syncthreads();
+    if (live) {
+      int pos = run[v] + rank;
+      for (int w2 = 0; w2 < wv; ++w2) pos += wc[w2][v];
+      perm[pos] = q;
+    }
+    __syncthreads();
+    if (tid < 256) {
+      int t = 0;
+#pragma unroll
+      for (int w2 = 0; w2 < 16; ++w2) t += wc[w2][tid];
+      run[tid] += t;
+    }
+    __syncthreads();
+  }
+}
+
+// part[p][c] = sum of the dX rows of piece p's positions in sorted order, one
+// wave per piece.  e <= 64 dividing 64: lane l takes feature l % e of the
+// positions u with u % (64 / e) == l / e, and the 64 / e partial sums are added
+// at the end in a fixed tree; other e: lanes c and c + 64 take features c and
+// c + 64 of every position (e <= 128).
+__global__ __launch_bounds__(64) void k_emb_piece(const float* __restrict__ dX, int e, const int* __restrict__ perm,
+                                                  const int* __restrict__ piece, const int* __restrict__ pstart,
+                                                  float* __restrict__ part) {
+  constexpr int B = 16;  // loads in flight per lane
+  const int p = blockIdx.x;
+  if (p >= pstart[256]) return;
+  const int st = piece[3 * p + 1], len = piece[3 * p + 2];
+  const int lane = threadIdx.x;
+  const int ipl = (e <= 64 && 64 % e == 0) ? 64 / e : 1;  // positions per load instruction
+  const int sub = ipl > 1 ? lane / e : 0;
+  // every load is made, from a clamped feature; lanes past the features add nothing
+  const int f0 = ipl > 1 ? lane - sub * e : min(lane, e - 1), f1 = min(lane + 64, e - 1);
+  float a0 = 0.f, a1 = 0.f;
+  for (int i0 = 0; i0 < len; i0 += 64) {
+    const int n = min(64, len - i0);
+    const int my = perm[st + i0 + min(lane, n - 1)];
+    for (int u0 = 0; u0 < n; u0 += B * ipl) {
+      float x0[B], x1[B];
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        // this lane's position: u0 + u * ipl + sub (clamped; masked below)
+        const int j = u0 + u * ipl + sub;
+        const int q = ipl > 1 ? __builtin_amdgcn_ds_bpermute(4 * min(j, n - 1), my)
+                              : __builtin_amdgcn_readlane(my, min(u0 + u, n - 1));
+        x0[u] = dX[(int64_t)q * e + f0];
+        if (e > 64) x1[u] = dX[(int64_t)q * e + f1];
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) my[v[u] * e + c] += x[u];
+      for (int u = 0; u < B; ++u) {
+        if (u0 + u * ipl + sub < n) {
+          a0 += x0[u];
+          if (e > 64) a1 += x1[u];
+        }
+      }
     }
-    for (; i < p1; i += NG) my[win[i] * e + c] += dX[i * e + c];
   }
+  // partial sums of the position classes, added in a fixed tree
+  for (int d = 1; d < ipl; d <<= 1) a0 += __shfl_down(a0, d * e, 64);
+  if (lane < e) part[(int64_t)p * e + lane] = a0;
+  if (e > 64 && lane + 64 < e) part[(int64_t)p * e + lane + 64] = a1;
+}
+
+// dE[v][c] = sum of byte v's pieces: row group rg of 256 / e takes every
+// (256 / e)-th piece in order, then the groups are added in order
+__global__ __launch_bounds__(256) void k_emb_sum(const float* __restrict__ part, const int* __restrict__ pstart, int e,
+                                                 float* __restrict__ dE) {
+  __shared__ float red[256];
+  const int v = blockIdx.x, tid = threadIdx.x;
+  const int RG = 256 / e, rg = tid / e, c = tid - rg * e;
+  const int p0 = pstart[v], p1 = pstart[v + 1];
+  float s = 0.f;
+  if (rg < RG) {
+#pragma unroll 4
+    for (int p = p0 + rg; p < p1; p += RG) s += part[(int64_t)p * e + c];
+  }
+  red[tid] = s;
   __syncthreads();
-  for (int k = tid; k < 256 * e; k += 256) {
-    float s = 0.f;
-    for (int q = 0; q < NG; ++q) s += tab[q * 256 * e + k];
-    part[(int64_t)blockIdx.x * 256 * e + k] = s;
+  if (tid < e) {
+    float t = 0.f;
+    for (int q = 0; q < RG; ++q) t += red[q * e + tid];
+    dE[v * e + tid] = t;
   }
 }
-int embed_bwd_blocks(int64_t total) {
-  int64_t b = total / 512;
-  return (int)(b < 64 ? 64 : (b > 1024 ? 1024 : b));
-}
-int64_t embed_bwd_ws_floats(int64_t total, int e) { return (int64_t)embed_bwd_blocks(total) * 256 * e; }
-void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int g, int e, int D, float* dE,
-                      float* ws, float* cws, hipStream_t s) {
-  const int64_t total = N * W;
-  const int G = embed_bwd_blocks(total);
-  const int64_t chunk = (total + G - 1) / G;
-  hipLaunchKernelGGL(k_embed_bwd_part, dim3(G), dim3(256), 0, s, win, dX, total, chunk, W, g, e, D, ws);
-  launch_colsum(ws, G, 256 * e, 256 * e, dE, 0.f, cws, s);
+
+void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int e, float* dE, float* ws,
+                      hipStream_t s) {
+  const int64_t M = N * W;
+  if (M <= 0) {
+    launch_zero(dE, (int64_t)256 * e, s);
+    return;
+  }
+  const EmbWs w = emb_ws(ws, M, e);
+  const int nb = (int)((M + EMB_CS - 1) / EMB_CS);
+  const int pmax = (int)((M + EMB_PIECE - 1) / EMB_PIECE + 256);
+  hipLaunchKernelGGL(k_emb_hist, dim3(nb), dim3(1024), 0, s, win, (int)M, w.cnt);
+  hipLaunchKernelGGL(k_emb_colscan, dim3(256), dim3(256), 0, s, (const int*)w.cnt, nb, w.off, w.tot);
+  hipLaunchKernelGGL(k_emb_pieces, dim3(1), dim3(1024), 0, s, (const int*)w.tot, w.base, w.pstart, w.piece);
+  hipLaunchKernelGGL(k_emb_scatter, dim3(nb), dim3(1024), 0, s, win, (int)M, (const int*)w.off,
+                     (const int*)w.base, w.perm);
+  hipLaunchKernelGGL(k_emb_piece, dim3(pmax), dim3(64), 0, s, dX, e, (const int*)w.perm, (const int*)w.piece,
+                     (const int*)w.pstart, w.part);
+  hipLaunchKernelGGL(k_emb_sum, dim3(256), dim3(256), 0, s, (const float*)w.part, (const int*)w.pstart, e, dE);
 }
 
 // byte-embedding part of the kept tokens: G[n][t][c] = E[byte][c % e] (the

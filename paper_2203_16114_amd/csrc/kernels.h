@@ -114,9 +114,11 @@ void launch_gelu_bwd(const float* dG, const float* U, float* dU, int64_t n, hipS
 void launch_attn_bwd(const float* dO, const float* q, const float* K, const float* V, const float* A, int64_t N, int T,
                      int D, int H, float scale, int round_dO, float* dQ, float* dK, float* dV, hipStream_t s);
 void launch_add(float* y, const float* x, int64_t rows, int64_t cols, int64_t ldy, int64_t ldx, hipStream_t s);
-int64_t embed_bwd_ws_floats(int64_t total, int e);  // total = N * W positions
-void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int g, int e, int D, float* dE,
-                      float* ws, float* cws, hipStream_t s);
+// dE[v][:] = sum of the e-vectors of dX (viewed as [N*W][e]) at the positions
+// whose window byte is v; N*W < 2^31; deterministic
+int64_t embed_bwd_ws_floats(int64_t M, int e);  // M = N * W positions
+void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int e, float* dE, float* ws,
+                      hipStream_t s);
 void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, int T, int D, int e, int g, float* X,
                         hipStream_t s);
 // dW[i][j] += sum_{u < nt} P[t0 + u][i] * S[u][j]  (P: operand copy [T][D])

@@ -66,6 +66,32 @@ def test_bf16_gradient_matches_emulating_oracle():
         assert rel <= 1e-2, (name, rel)
 
 
+@pytest.mark.parametrize("kind", ["skewed", "one_byte"])
+def test_fp32_embedding_gradient_over_many_sort_blocks(kind):
+    """1100 kept windows of 32 bytes: 35200 positions, several blocks of the
+    counting sort with a ragged last one.  Skewed: most bytes are one value
+    (a byte run cut into many pieces); one_byte: every position holds the same
+    byte.  The E gradient matches the oracle's to the fp32 bar."""
+    B, L, pos = 1100, 40, 36
+    streams = synth.random_streams(77, B, L)
+    if kind == "skewed":
+        rng = np.random.default_rng(5)
+        streams = np.where(rng.random(streams.shape) < 0.8, np.uint8(32), streams).astype(np.uint8)
+    else:
+        streams = np.full_like(streams, 101)
+    m, cfg, flat, g, _, w, y = _grad_run(SMALL, "fp32", 0x5150, streams, pos)
+    _, ref = O.forward_backward(flat, cfg, w, y, mode="fp64")
+    a = O.unflatten(g, cfg)["E"].astype(np.float64)
+    b = np.asarray(ref["E"], np.float64)
+    scale = np.max(np.abs(b))
+    # sums over up to 35200 rows of fp32 values in a different order than the
+    # oracle's: 1e-4 relative with a floor of 1e-5 of the largest entry
+    assert np.all(np.abs(a - b) <= 1e-4 * np.abs(b) + 1e-5 * scale), np.max(np.abs(a - b))
+    used = np.zeros(256, bool)
+    used[np.unique(w)] = True
+    assert np.all(a[~used] == 0)
+
+
 def test_fp32_adam_step_matches_oracle():
     streams = synth.random_streams(32, 128, 90)
     m, cfg, flat, g, th, w, y = _grad_run(SMALL, "fp32", 77, streams, 40)
