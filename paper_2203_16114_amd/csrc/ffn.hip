@@ -311,13 +311,15 @@ __global__ __launch_bounds__(512) void k_ffn_head(FfnArgs a) {
 
 // ------------------------------------------------- pipelined bf16 variant ----
 // Same arithmetic as k_ffn_head (bf16 operands, fp32 accumulation, U rounded
-// to bf16 after GELU), restructured so that the GELU's vector ALU work runs in
-// the same wave as independent MFMAs.  F is cut into chunks of 128 features
+// to bf16 after GELU; the GELU by the exp2 form gelu2_ex), restructured so that
+// the GELU's vector ALU work runs in the same wave as independent MFMAs.  F is cut into chunks of 128 features
 // and each interval between two barriers does, per wave:
 //   GEMM2 of chunk j-1 (reads G from LDS buffer (j-1)&1, accumulates Y),
 //   GEMM1 of chunk j+1 (reads bf(Y) from LDS, accumulates U into one register set),
 //   GELU of chunk j    (the other register set, in place, written to buffer j&1),
-// with one GELU value issued after every few MFMAs.  The two U register sets
+// with one GELU value issued after every few MFMAs (scheduled as at most three
+// vector instructions after each MFMA: a 16-cycle MFMA hides up to about three,
+// more serialise).  The two U register sets
 // alternate roles from one interval to the next; the loop takes two intervals
 // per trip so that the roles stay compile-time.  G holds bf(2 GELU(U)) and the
 // packed W2 copy holds bf(W2)/2: both scalings are exact, so every product is
@@ -437,9 +439,16 @@ __device__ __forceinline__ void ffn_interval(const PipeLane& L,
         static_for<(m * NGV) / NM, ((m + 1) * NGV) / NM>([&](auto gc) {
           constexpr int g = decltype(gc)::value;
           f32x4& v = ug[g / (NFC * 4)][(g / 4) % NFC];
-          v[g % 4] = gelu2_as(v[g % 4]);
+          v[g % 4] = gelu2_ex(v[g % 4]);
         });
       }
+    });
+    // the step's loads first, then each MFMA followed by a share of the vector work
+    __builtin_amdgcn_sched_group_barrier(0x020, RFA, 0);
+    __builtin_amdgcn_sched_group_barrier(0x100, NFC, 0);
+    static_for<0, RFN * NFC>([&](auto) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);
     });
     // keep each step's loads one step ahead, not hoisted further
     __builtin_amdgcn_sched_barrier(0);
