@@ -139,19 +139,19 @@ __device__ __forceinline__ float gelu2_as(float u) {
 }
 
 // 2 GELU(u) = u + |u| - |u| erfc(|u|/sqrt2), with erfc(a/sqrt2) = 2^P(a) and P
-// of degree 6, P(0) = 0, fitted on a in [0, 4 sqrt2] minimax in |u| times the
-// error of erfc (a linear program over 4001 points); a is clamped there, where
-// erfc is below 1.6e-8.  |error| <= 3.7e-7 max(1, |u|) in fp32 (the 7.1.28
-// form: 7.2e-7).  Ten vector operations, the exp2 among them, against thirteen.
+// of degree 5, fitted on a in [0, 4 sqrt2] minimax in |u| times the error of
+// erfc (a linear program over 8001 points).  P decreases beyond that range (its
+// leading coefficient is negative), so 2^P falls to 0 with no clamp.  |error| <=
+// 6.8e-7 max(1, |u|) in fp32 (the 7.1.28 form: 7.2e-7).  Eight vector operations,
+// the exp2 among them, against thirteen.
 __device__ __forceinline__ float gelu2_ex(float u) {
-  const float a = fminf(fabsf(u), 5.656854249f);
-  float q = fmaf(1.7666612364e-05f, a, -6.4675855776e-04f);
-  q = fmaf(q, a, 7.7203886063e-03f);
-  q = fmaf(q, a, -5.2921410004e-02f);
-  q = fmaf(q, a, -4.5908602818e-01f);
-  q = fmaf(q, a, -1.1511162115e+00f);
-  const float e = __builtin_amdgcn_exp2f(q * a);
-  return fmaf(-fabsf(u), e, u + fabsf(u));
+  const float a = fabsf(u);
+  float q = fmaf(-5.1878412099e-04f, a, 7.3867838681e-03f);
+  q = fmaf(q, a, -5.2537328834e-02f);
+  q = fmaf(q, a, -4.5927711224e-01f);
+  q = fmaf(q, a, -1.1510829986e+00f);
+  q = fmaf(q, a, -8.5913516831e-07f);
+  return fmaf(-a, __builtin_amdgcn_exp2f(q), u + a);
 }
 
 // GELU'(u) = Phi(u) + u phi(u) with Phi from the same 7.1.28 formula,
