@@ -595,9 +595,10 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
       __builtin_amdgcn_wave_barrier();
     }
   }
-  __syncthreads();  // O complete
+  __syncthreads();  // O complete; q no longer needed
 
-  // h0^T = Wo^T . O^T + X_last (fp32: E + P of the last token)
+  // h0^T = Wo^T . O^T + X_last (fp32: E + P of the last token), rows staged in
+  // the q tile (padded rows: conflict-free), then written out whole
 #pragma unroll
   for (int qi = 0; qi < QFW; ++qi) {
     const int qf = wave * QFW + qi;
@@ -620,19 +621,27 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
 #pragma unroll
       for (int nf = 0; nf < NMF; ++nf) {
         const int m = nf * 16 + lc;
-        const int64_t n = tile0 + m;
-        if (n < N) {
-          const int d = qf * 16 + 4 * lg;
-          const int j = (int)(((uint32_t)d * einv) >> 20), cc = d - j * a.e;
-          const int byte = Wb[m + (T - 1) * G + j];
-          float4 r;
-          r.x = acc[nf][0] + (M::val(E[byte * a.e + cc]) + M::val(P[(T - 1) * D + d]));
-          r.y = acc[nf][1] + (M::val(E[byte * a.e + cc + 1]) + M::val(P[(T - 1) * D + d + 1]));
-          r.z = acc[nf][2] + (M::val(E[byte * a.e + cc + 2]) + M::val(P[(T - 1) * D + d + 2]));
-          r.w = acc[nf][3] + (M::val(E[byte * a.e + cc + 3]) + M::val(P[(T - 1) * D + d + 3]));
-          *reinterpret_cast<float4*>(a.h0 + n * D + d) = r;
-        }
+        const int d = qf * 16 + 4 * lg;
+        const int j = (int)(((uint32_t)d * einv) >> 20), cc = d - j * a.e;
+        const int byte = Wb[m + (T - 1) * G + j];
+        float4 r;
+        r.x = acc[nf][0] + (M::val(E[byte * a.e + cc]) + M::val(P[(T - 1) * D + d]));
+        r.y = acc[nf][1] + (M::val(E[byte * a.e + cc + 1]) + M::val(P[(T - 1) * D + d + 1]));
+        r.z = acc[nf][2] + (M::val(E[byte * a.e + cc + 2]) + M::val(P[(T - 1) * D + d + 2]));
+        r.w = acc[nf][3] + (M::val(E[byte * a.e + cc + 3]) + M::val(P[(T - 1) * D + d + 3]));
+        *reinterpret_cast<float4*>(Qs + m * QSTR + d) = r;
       }
+    }
+  }
+  __syncthreads();
+  // the tile's h0 rows are one contiguous block of MA * D floats: each wave
+  // writes whole rows, 16 bytes per lane
+  for (int m = wave; m < MA; m += NW) {
+    const int64_t n = tile0 + m;
+    if (n < N) {
+#pragma unroll
+      for (int c = 4 * lane; c < D; c += 256)
+        *reinterpret_cast<float4*>(a.h0 + n * D + c) = *reinterpret_cast<const float4*>(Qs + m * QSTR + c);
     }
   }
 }
