@@ -436,11 +436,12 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   float* ws = m->gws;
   const long tk = tbegin(m, s);
   // Two streams: s carries the chain of input gradients (dY, dU, dO, dQ/dK/dV,
-  // dX, dE) without waiting; `side` computes most weight gradients from the
-  // per-repeat buffers that chain leaves behind.  They meet three times (after
-  // dz, after the attention backward, before Adam): a wait across streams costs
-  // several microseconds.  The side stream has its own split-K and column-sum
-  // workspaces of the same sizes, so every product is the same as on one stream.
+  // dX, dE) and never waits for the other until the end; `side` computes most
+  // weight gradients from the per-repeat buffers that chain leaves behind, each
+  // as soon as its operands exist (a wait across streams costs several
+  // microseconds, so only the side stream waits).  The side stream has its own
+  // split-K and column-sum workspaces of the same sizes, so every product is the
+  // same as on one stream.
   const hipStream_t w = m->side;
   float* ws2 = m->gws2;
   auto dYr = [&](int r) { return m->dY + (int64_t)r * N * D; };  // w.r.t. the input of repeat r (r = k: Y_k)
@@ -457,31 +458,33 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // dY_k = dz . Wout^T
   launch_gemm(gemm(N, D, 256, m->dz, 256, 1, rb, th + L.off[P_WOUT], 1, 256, rb, dYr(k), D, 0.f), ws, m->gws_cap, s);
   // shared FFN, repeats in reverse: dU_r = (dY_{r+1} . W2^T) * GELU'(U_r),
-  // dY_r = dY_{r+1} + dU_r . W1^T
+  // dY_r = dY_{r+1} + dU_r . W1^T; once dU_r exists the side stream forms
+  // dW2 += G_r^T . dY_{r+1} and dW1 += Y_r^T . dU_r (accumulated over the repeats
+  // in reverse; G = GELU(U) at its storage point: kept by the bf16 forward,
+  // formed here otherwise)
   for (int r = k - 1; r >= 0; --r) {
     GemmArgs gd = gemm(N, F, D, dYr(r + 1), D, 1, rb, th + L.off[P_W2], 1, D, rb, dUr(r), F, 0.f);
     gd.gelu_u = m->kU + (int64_t)r * N * F;
     launch_gemm(gd, ws, m->gws_cap, s);
-    (void)hipMemcpyAsync(dYr(r), dYr(r + 1), (size_t)N * D * 4, hipMemcpyDeviceToDevice, s);
-    launch_gemm(gemm(N, D, F, dUr(r), F, 1, rb, th + L.off[P_W1], 1, F, rb, dYr(r), D, 1.f), ws, m->gws_cap, s);
-  }
-  // attention output projection: dO = dY_0 . Wo^T, then the attention (last
-  // query row) -> dQ, dK, dV
-  launch_gemm(gemm(N, D, D, dYr(0), D, 1, rb, th + L.off[P_WO], 1, D, rb, m->dO, D, 0.f), ws, m->gws_cap, s);
-  launch_attn_bwd(m->dO, m->kq, m->kK, m->kV, m->kA, N, T, D, H, (float)(1.0 / std::sqrt((double)L.DH)), rb, m->dQ,
-                  m->dK, m->dV, s);
-  order(m, s, w);  // every dY_r, dU_r, dQ, dK, dV is complete
-  // side: W2 and W1 gradients, accumulated over the repeats in reverse
-  // (dW2 += G_r^T . dY_{r+1}, dW1 += Y_r^T . dU_r, with G = GELU(U) at its
-  // storage point: kept by the bf16 forward, formed here otherwise)
-  for (int r = k - 1; r >= 0; --r) {
+    order(m, s, w);  // dY_{r+1} and dU_r are complete
     const float beta = (r == k - 1) ? 0.f : 1.f;
     const float* Gr = m->kG ? m->kG + (int64_t)r * N * F : m->G;
     if (!m->kG) launch_gelu_fwd_round(m->kU + (int64_t)r * N * F, m->G, (int64_t)N * F, rb, w);
     launch_gemm(gemm(F, D, N, Gr, 1, F, rb, dYr(r + 1), D, 1, rb, gr + L.off[P_W2], D, beta), ws2, m->gws_cap, w);
     launch_gemm(gemm(D, F, N, m->kY + (int64_t)r * N * D, 1, D, rb, dUr(r), F, 1, rb, gr + L.off[P_W1], F, beta), ws2,
                 m->gws_cap, w);
+    (void)hipMemcpyAsync(dYr(r), dYr(r + 1), (size_t)N * D * 4, hipMemcpyDeviceToDevice, s);
+    launch_gemm(gemm(N, D, F, dUr(r), F, 1, rb, th + L.off[P_W1], 1, F, rb, dYr(r), D, 1.f), ws, m->gws_cap, s);
   }
+  order(m, s, w);  // dY_0 is complete
+  // side: dWo = O^T . dY_0
+  launch_gemm(gemm(D, D, N, m->kO, 1, D, rb, dYr(0), D, 1, rb, gr + L.off[P_WO], D, 0.f), ws2, m->gws_cap, w);
+  // attention output projection: dO = dY_0 . Wo^T, then the attention (last
+  // query row) -> dQ, dK, dV
+  launch_gemm(gemm(N, D, D, dYr(0), D, 1, rb, th + L.off[P_WO], 1, D, rb, m->dO, D, 0.f), ws, m->gws_cap, s);
+  launch_attn_bwd(m->dO, m->kq, m->kK, m->kV, m->kA, N, T, D, H, (float)(1.0 / std::sqrt((double)L.DH)), rb, m->dQ,
+                  m->dK, m->dV, s);
+  order(m, s, w);  // dQ, dK, dV are complete
   // side: dWk = X^T dK, dWv = X^T dV (dK, dV stay fp32), with X = G + P[t]:
   // G^T dZ as GEMMs on the byte-embedding part G, then P^T (sum over windows of
   // dZ) for the positional part
@@ -506,8 +509,7 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   else
     launch_zero(gr + L.off[P_P], L.size[P_P], s);
   launch_embed_bwd(m->kwin, m->dX, N, m->cfg.W, m->cfg.e, gr + L.off[P_E], m->ews, s);
-  // dWo = O^T . dY_0 ; dWq = X_last^T dQ (+ its positional part)
-  launch_gemm(gemm(D, D, N, m->kO, 1, D, rb, dYr(0), D, 1, rb, gr + L.off[P_WO], D, 0.f), ws, m->gws_cap, s);
+  // dWq = X_last^T dQ (+ its positional part)
   launch_gemm(gemm(D, D, N, m->Xk + (int64_t)(T - 1) * D, 1, (int64_t)T * D, rb, m->dQ, D, 1, 0, gr + L.off[P_WQ], D,
                    0.f),
               ws, m->gws_cap, s);
