@@ -35,10 +35,13 @@ struct trace_model {
   int64_t keepN;
   uint8_t* kwin;
   int32_t* ktgt;
-  float *kq, *kK, *kV, *kA, *kO, *kY, *kU, *kG, *kZ;
+  float *kq, *kK, *kV, *kA, *kO, *kY, *kU, *kZ;
+  uint16_t* kG;  // bf16 models: GELU(U) of each repeat as bf16 operand values
   // backward scratch
   // dY: gradients w.r.t. the k+1 residual states, dU: w.r.t. the k pre-GELU
-  // activations (one buffer per repeat, read by the weight gradients later)
+  // activations (one buffer per repeat, read by the weight gradients later);
+  // in bf16 models dU and Xk (the byte-embedding part of the kept tokens) hold
+  // bf16 elements: both are only read as bf16 operands
   float *dz, *dY, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *sP, *gws, *cws, *ews;
   int64_t gws_cap;
   // second stream of the update step (the weight-gradient branch), its own
@@ -212,6 +215,7 @@ GemmArgs gemm(int M, int N, int K, const float* A, int64_t sam, int64_t sak, int
   g.roundB = rB;
   g.beta = beta;
   g.gelu_u = nullptr;
+  g.halfA = g.halfB = g.halfC = 0;
   return g;
 }
 
@@ -258,12 +262,12 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
          dalloc(m, &m->kK, K * T * D * 4) && dalloc(m, &m->kV, K * T * D * 4) &&
          dalloc(m, &m->kA, K * cfg->H * T * 4) && dalloc(m, &m->kO, K * D * 4) &&
          dalloc(m, &m->kY, (cfg->k + 1) * K * D * 4) && dalloc(m, &m->kU, cfg->k * K * F * 4) &&
-         (!bf || dalloc(m, &m->kG, cfg->k * K * F * 4)) &&
+         (!bf || dalloc(m, &m->kG, cfg->k * K * F * 2)) &&
          dalloc(m, &m->kZ, K * 256 * 4) && dalloc(m, &m->dz, K * 256 * 4) &&
-         dalloc(m, &m->dY, (cfg->k + 1) * K * D * 4) && dalloc(m, &m->dU, cfg->k * K * F * 4) &&
+         dalloc(m, &m->dY, (cfg->k + 1) * K * D * 4) && dalloc(m, &m->dU, cfg->k * K * F * es) &&
          (bf || dalloc(m, &m->G, K * F * 4)) &&
          dalloc(m, &m->dO, K * D * 4) && dalloc(m, &m->dQ, K * D * 4) && dalloc(m, &m->dK, K * T * D * 4) &&
-         dalloc(m, &m->dV, K * T * D * 4) && dalloc(m, &m->dX, K * T * D * 4) && dalloc(m, &m->Xk, K * T * D * 4) &&
+         dalloc(m, &m->dV, K * T * D * 4) && dalloc(m, &m->dX, K * T * D * 4) && dalloc(m, &m->Xk, K * T * D * es) &&
          dalloc(m, &m->sP, (T + 1) * D * 4) &&
          dalloc(m, &m->gws, (m->gws_cap = adapt_gemm_ws(m, K)) * 4) &&
          dalloc(m, &m->ews, embed_bwd_ws_floats(K * W, cfg->e) * 4) &&
@@ -435,6 +439,7 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   float* gr = m->grad;
   float* ws = m->gws;
   const long tk = tbegin(m, s);
+  bool ok = true;  // false if a product could not be launched
   // Two streams: s carries the chain of input gradients (dY, dU, dO, dQ/dK/dV,
   // dX, dE) and never waits for the other until the end; `side` computes most
   // weight gradients from the per-repeat buffers that chain leaves behind, each
@@ -445,7 +450,10 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   const hipStream_t w = m->side;
   float* ws2 = m->gws2;
   auto dYr = [&](int r) { return m->dY + (int64_t)r * N * D; };  // w.r.t. the input of repeat r (r = k: Y_k)
-  auto dUr = [&](int r) { return m->dU + (int64_t)r * N * F; };
+  const int hf = m->bf ? 1 : 0;  // dU and Xk stored as bf16
+  // bf16 element e of a buffer whose elements are bf16 (hf) or fp32
+  auto at = [&](float* p, int64_t e) { return hf ? (float*)((uint16_t*)p + e) : p + e; };
+  auto dUr = [&](int r) { return at(m->dU, (int64_t)r * N * F); };
   // head: dz = (softmax(z) - onehot) / N
   launch_ce_grad(m->kZ, m->ktgt, N, m->dz, s);
   order(m, s, w);
@@ -465,16 +473,27 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   for (int r = k - 1; r >= 0; --r) {
     GemmArgs gd = gemm(N, F, D, dYr(r + 1), D, 1, rb, th + L.off[P_W2], 1, D, rb, dUr(r), F, 0.f);
     gd.gelu_u = m->kU + (int64_t)r * N * F;
-    launch_gemm(gd, ws, m->gws_cap, s);
+    gd.halfC = hf;
+    ok = launch_gemm(gd, ws, m->gws_cap, s) && ok;
     order(m, s, w);  // dY_{r+1} and dU_r are complete
     const float beta = (r == k - 1) ? 0.f : 1.f;
-    const float* Gr = m->kG ? m->kG + (int64_t)r * N * F : m->G;
-    if (!m->kG) launch_gelu_fwd_round(m->kU + (int64_t)r * N * F, m->G, (int64_t)N * F, rb, w);
-    launch_gemm(gemm(F, D, N, Gr, 1, F, rb, dYr(r + 1), D, 1, rb, gr + L.off[P_W2], D, beta), ws2, m->gws_cap, w);
-    launch_gemm(gemm(D, F, N, m->kY + (int64_t)r * N * D, 1, D, rb, dUr(r), F, 1, rb, gr + L.off[P_W1], F, beta), ws2,
-                m->gws_cap, w);
+    GemmArgs g2w;
+    if (m->kG) {
+      g2w = gemm(F, D, N, (const float*)(m->kG + (int64_t)r * N * F), 1, F, rb, dYr(r + 1), D, 1, rb,
+                 gr + L.off[P_W2], D, beta);
+      g2w.halfA = 1;
+    } else {
+      launch_gelu_fwd_round(m->kU + (int64_t)r * N * F, m->G, (int64_t)N * F, rb, w);
+      g2w = gemm(F, D, N, m->G, 1, F, rb, dYr(r + 1), D, 1, rb, gr + L.off[P_W2], D, beta);
+    }
+    ok = launch_gemm(g2w, ws2, m->gws_cap, w) && ok;
+    GemmArgs g1w = gemm(D, F, N, m->kY + (int64_t)r * N * D, 1, D, rb, dUr(r), F, 1, rb, gr + L.off[P_W1], F, beta);
+    g1w.halfB = hf;
+    ok = launch_gemm(g1w, ws2, m->gws_cap, w) && ok;
     (void)hipMemcpyAsync(dYr(r), dYr(r + 1), (size_t)N * D * 4, hipMemcpyDeviceToDevice, s);
-    launch_gemm(gemm(N, D, F, dUr(r), F, 1, rb, th + L.off[P_W1], 1, F, rb, dYr(r), D, 1.f), ws, m->gws_cap, s);
+    GemmArgs gy = gemm(N, D, F, dUr(r), F, 1, rb, th + L.off[P_W1], 1, F, rb, dYr(r), D, 1.f);
+    gy.halfA = hf;
+    ok = launch_gemm(gy, ws, m->gws_cap, s) && ok;
   }
   order(m, s, w);  // dY_0 is complete
   // side: dWo = O^T . dY_0
@@ -488,8 +507,11 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // side: dWk = X^T dK, dWv = X^T dV (dK, dV stay fp32), with X = G + P[t]:
   // G^T dZ as GEMMs on the byte-embedding part G, then P^T (sum over windows of
   // dZ) for the positional part
-  launch_gemm(gemm(D, D, N * T, m->Xk, 1, D, rb, m->dK, D, 1, 0, gr + L.off[P_WK], D, 0.f), ws2, m->gws_cap, w);
-  launch_gemm(gemm(D, D, N * T, m->Xk, 1, D, rb, m->dV, D, 1, 0, gr + L.off[P_WV], D, 0.f), ws2, m->gws_cap, w);
+  GemmArgs gk = gemm(D, D, N * T, m->Xk, 1, D, rb, m->dK, D, 1, 0, gr + L.off[P_WK], D, 0.f);
+  GemmArgs gv = gemm(D, D, N * T, m->Xk, 1, D, rb, m->dV, D, 1, 0, gr + L.off[P_WV], D, 0.f);
+  gk.halfA = gv.halfA = hf;
+  ok = launch_gemm(gk, ws2, m->gws_cap, w) && ok;
+  ok = launch_gemm(gv, ws2, m->gws_cap, w) && ok;
   if (m->cfg.use_pos) {
     launch_colsum(m->dK, N, (int64_t)T * D, (int64_t)T * D, m->sP, 0.f, m->cws2, w);
     launch_pos_grad(m->bf, m->Pc, m->sP, 0, T, D, gr + L.off[P_WK], w);
@@ -510,14 +532,19 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
     launch_zero(gr + L.off[P_P], L.size[P_P], s);
   launch_embed_bwd(m->kwin, m->dX, N, m->cfg.W, m->cfg.e, gr + L.off[P_E], m->ews, s);
   // dWq = X_last^T dQ (+ its positional part)
-  launch_gemm(gemm(D, D, N, m->Xk + (int64_t)(T - 1) * D, 1, (int64_t)T * D, rb, m->dQ, D, 1, 0, gr + L.off[P_WQ], D,
-                   0.f),
-              ws, m->gws_cap, s);
+  GemmArgs gq = gemm(D, D, N, at(m->Xk, (int64_t)(T - 1) * D), 1, (int64_t)T * D, rb, m->dQ, D, 1, 0,
+                     gr + L.off[P_WQ], D, 0.f);
+  gq.halfA = hf;
+  ok = launch_gemm(gq, ws, m->gws_cap, s) && ok;
   if (m->cfg.use_pos) {
     launch_colsum(m->dQ, N, D, D, m->sP + (int64_t)T * D, 0.f, m->cws, s);
     launch_pos_grad(m->bf, m->Pc, m->sP + (int64_t)T * D, T - 1, 1, D, gr + L.off[P_WQ], s);
   }
   order(m, w, s);  // every gradient is complete
+  if (!ok) {
+    tend(m, tk, TRACE_KIND_BACKWARD, s);
+    return fail(TRACE_EUNSUPPORTED, "trace_adapt_step: an operand stored as bf16 does not fit the bf16 GEMM");
+  }
   tend(m, tk, TRACE_KIND_BACKWARD, s);
   // Adam on the flat master, then new operand copies
   m->step += 1;

@@ -70,8 +70,48 @@ __device__ __forceinline__ int unit_of(int row, int c) { return row * 8 + (c ^ (
 // others.  (A load under a condition is compiled into a load from a select of
 // the address and a zero in scratch memory, and a select right after the load
 // would wait for it before the multiply.)
-template <bool KC>
+// H: the operand is stored as bf16 (pointer and strides in bf16 elements).  k
+// contiguous: one 16-byte unit of 8 k values per (row, chunk), its bits in
+// v[2q] (the operand's K is a multiple of 8; bits 2q, 2q+1 of the mask both say
+// whether the unit lies inside).  Rows contiguous: per k, the 8 bytes of rows
+// 4 (tid % 32) .. +3 as the bits of v[j].x, v[j].y.
+template <bool KC, bool H>
+__device__ __forceinline__ uint32_t load_tile_h(const Src& s, int row0, int k0, int tid, float4 (&v)[8]) {
+  const bool seg1 = k0 >= s.k1p;
+  const uint16_t* __restrict__ p = (const uint16_t*)(seg1 ? s.p1 : s.p0);
+  const int ld = (int)(seg1 ? s.ld1 : s.ld0);
+  const int kk0 = seg1 ? k0 - s.k1p : k0, kr = (seg1 ? s.kext1 : s.kext0) - kk0;
+  uint32_t mask = 0;
+  auto at = [](const uint16_t* base, int off) { return reinterpret_cast<const char*>(base) + (uint32_t)off * 2u; };
+  if constexpr (KC) {
+    const uint16_t* base = p + (int64_t)row0 * ld + kk0;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int u = tid + 256 * q, rr = u >> 3, c8 = (u & 7) * 8;
+      const int ro = min(rr, s.rows - 1 - row0) * ld;
+      v[2 * q] = __builtin_bit_cast(float4, *reinterpret_cast<const uint4*>(at(base, ro + min(c8, kr - 8))));
+      v[2 * q + 1] = make_float4(0.f, 0.f, 0.f, 0.f);
+      const uint32_t in = (row0 + rr < s.rows && c8 < kr) ? 3u : 0u;
+      mask |= in << (2 * q);
+    }
+  } else {
+    const uint16_t* base = p + (int64_t)kk0 * ld + row0;
+    const int rr = 4 * (tid & 31), kc = (tid >> 5) * 8;
+    const bool rin = row0 + rr < s.rows;
+    const int ro = min(rr, s.rows - 4 - row0);
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const uint2 w = *reinterpret_cast<const uint2*>(at(base, min(kc + j, kr - 1) * ld + ro));
+      v[j] = make_float4(__uint_as_float(w.x), __uint_as_float(w.y), 0.f, 0.f);
+      mask |= (uint32_t)(rin && kc + j < kr) << j;
+    }
+  }
+  return mask;
+}
+
+template <bool KC, bool H = false>
 __device__ __forceinline__ uint32_t load_tile(const Src& s, int row0, int k0, int tid, float4 (&v)[8]) {
+  if constexpr (H) return load_tile_h<KC, true>(s, row0, k0, tid, v);
   const bool seg1 = k0 >= s.k1p;
   const float* __restrict__ p = seg1 ? s.p1 : s.p0;
   const int ld = (int)(seg1 ? s.ld1 : s.ld0);
@@ -109,8 +149,44 @@ __device__ __forceinline__ uint32_t load_tile(const Src& s, int row0, int k0, in
 
 // The values of load_tile (float4 j zero unless bit j of mask) -> bf16 units
 // of the LDS tile hi (and lo when split).
-template <bool KC, bool SPLIT>
+// bf16 pairs (k, k + 1) of one row from two words that each hold two rows:
+// the low halves (row 0 of the pair) or the high halves (row 1)
+__device__ __forceinline__ uint32_t pair_lo(uint32_t wa, uint32_t wb) { return __builtin_amdgcn_perm(wb, wa, 0x05040100u); }
+__device__ __forceinline__ uint32_t pair_hi(uint32_t wa, uint32_t wb) { return __builtin_amdgcn_perm(wb, wa, 0x07060302u); }
+
+template <bool KC, bool SPLIT, bool H = false>
 __device__ __forceinline__ void store_tile(const float4 (&vin)[8], uint32_t mask, uint4* hi, uint4* lo, int tid) {
+  if constexpr (H) {  // bf16 source: the units as loaded (k contiguous) or packed per row
+    static_assert(!SPLIT, "a bf16 operand is not split");
+    if constexpr (KC) {
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int u = tid + 256 * q;
+        const uint32_t m = 0u - ((mask >> (2 * q)) & 1u);
+        const uint4 w = __builtin_bit_cast(uint4, vin[2 * q]);
+        hi[unit_of(u >> 3, u & 7)] = make_uint4(w.x & m, w.y & m, w.z & m, w.w & m);
+      }
+    } else {
+      const int rr = 4 * (tid & 31), c = tid >> 5;
+      uint32_t w[8][2];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const uint32_t m = 0u - ((mask >> j) & 1u);
+        w[j][0] = __float_as_uint(vin[j].x) & m;
+        w[j][1] = __float_as_uint(vin[j].y) & m;
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        uint32_t x[4];
+#pragma unroll
+        for (int pp = 0; pp < 4; ++pp)
+          x[pp] = (i & 1) ? pair_hi(w[2 * pp][i >> 1], w[2 * pp + 1][i >> 1])
+                          : pair_lo(w[2 * pp][i >> 1], w[2 * pp + 1][i >> 1]);
+        hi[unit_of(rr + i, c)] = make_uint4(x[0], x[1], x[2], x[3]);
+      }
+    }
+    return;
+  }
   float4 v[8];
 #pragma unroll
   for (int j = 0; j < 8; ++j) {
@@ -148,10 +224,10 @@ __device__ __forceinline__ void store_tile(const float4 (&vin)[8], uint32_t mask
 // C[m][n] (+)= sum_k A(m, k) B(k, n) over this split's k range.  AKC / BKC:
 // that operand's contiguous dimension is k; SA / SB: that operand is split.
 // 1-D grid of tn * tm * splits blocks.
-template <bool AKC, bool BKC, bool SA, bool SB>
+template <bool AKC, bool BKC, bool SA, bool SB, bool HA, bool HB>
 __global__ __launch_bounds__(256) void k_bgemm(Src A, Src B, int Kp, int M, int N, float* __restrict__ C, int64_t ldc,
                                                float beta, float* __restrict__ part, int kchunk, int tn, int tm,
-                                               const float* __restrict__ gu) {
+                                               const float* __restrict__ gu, int hc) {
   static_assert(!(SA && SB), "at most one operand is split");
   constexpr int NT = 2 + (SA ? 1 : 0) + (SB ? 1 : 0);  // tiles per stage: A hi, B hi, [A lo | B lo]
   __shared__ uint4 lds[2][NT][UNITS];
@@ -172,12 +248,12 @@ __global__ __launch_bounds__(256) void k_bgemm(Src A, Src B, int Kp, int M, int 
   float4 va[8], vb[8];
   uint32_t ma = 0, mb_ = 0;
   auto put = [&](int buf) {
-    store_tile<AKC, SA>(va, ma, lds[buf][0], lds[buf][SA ? 2 : 0], tid);
-    store_tile<BKC, SB>(vb, mb_, lds[buf][1], lds[buf][NT - 1], tid);
+    store_tile<AKC, SA, HA>(va, ma, lds[buf][0], lds[buf][SA ? 2 : 0], tid);
+    store_tile<BKC, SB, HB>(vb, mb_, lds[buf][1], lds[buf][NT - 1], tid);
   };
   if (kb < ke) {
-    ma = load_tile<AKC>(A, m0, kb, tid, va);
-    mb_ = load_tile<BKC>(B, n0, kb, tid, vb);
+    ma = load_tile<AKC, HA>(A, m0, kb, tid, va);
+    mb_ = load_tile<BKC, HB>(B, n0, kb, tid, vb);
     put(0);
   }
   __syncthreads();
@@ -185,8 +261,8 @@ __global__ __launch_bounds__(256) void k_bgemm(Src A, Src B, int Kp, int M, int 
   for (int k0 = kb; k0 < ke; k0 += BK, buf ^= 1) {
     const bool more = k0 + BK < ke;
     if (more) {  // next tile into registers while this one is multiplied
-      ma = load_tile<AKC>(A, m0, k0 + BK, tid, va);
-      mb_ = load_tile<BKC>(B, n0, k0 + BK, tid, vb);
+      ma = load_tile<AKC, HA>(A, m0, k0 + BK, tid, va);
+      mb_ = load_tile<BKC, HB>(B, n0, k0 + BK, tid, vb);
     }
     // keep the order loads / multiply / LDS writes: otherwise the writes to the
     // other buffer are hoisted above the multiply and wait on the loads at once
@@ -286,7 +362,12 @@ __global__ __launch_bounds__(256) void k_bgemm(Src A, Src B, int Kp, int M, int 
 #pragma unroll
         for (int nf = 0; nf < 4; ++nf) {
           const int n = nbase + nf * 16;
-          if (n < N) C[(int64_t)m * ldc + n] = acc[rf][nf][r];
+          if (n < N) {
+            if (hc)
+              reinterpret_cast<uint16_t*>(C)[(int64_t)m * ldc + n] = f2bf(acc[rf][nf][r]);
+            else
+              C[(int64_t)m * ldc + n] = acc[rf][nf][r];
+          }
         }
       }
   }
@@ -310,8 +391,48 @@ __device__ __forceinline__ int unit_of(int row, int c) { return row * 4 + (c ^ (
 // each.  Rows contiguous: rows 2 (tid % 128), +1 of chunk tid / 128, a float2
 // per k (v[j / 2] holds k = 2 (j / 2), +1).  Same clamping and mask as
 // load_tile.
+// H: bf16 source.  k contiguous: unit q (8 k) bits in v[2q], mask bits 2q and
+// 2q + 1 both set when it lies inside.  Rows contiguous: per k the 4 bytes of
+// rows 2 (tid % 128), +1, k = 2i, 2i + 1 in v[i].x, v[i].y.
 template <bool KC>
+__device__ __forceinline__ uint32_t load_h(const Src& s, int row0, int k0, int tid, float4 (&v)[4]) {
+  const bool seg1 = k0 >= s.k1p;
+  const uint16_t* __restrict__ p = (const uint16_t*)(seg1 ? s.p1 : s.p0);
+  const int ld = (int)(seg1 ? s.ld1 : s.ld0);
+  const int kk0 = seg1 ? k0 - s.k1p : k0, kr = (seg1 ? s.kext1 : s.kext0) - kk0;
+  uint32_t mask = 0;
+  auto at = [](const uint16_t* base, int off) { return reinterpret_cast<const char*>(base) + (uint32_t)off * 2u; };
+  if constexpr (KC) {
+    const uint16_t* base = p + (int64_t)row0 * ld + kk0;
+#pragma unroll
+    for (int q = 0; q < 2; ++q) {
+      const int u = tid + 512 * q, rr = u >> 2, c8 = (u & 3) * 8;
+      const int ro = min(rr, s.rows - 1 - row0) * ld;
+      v[2 * q] = __builtin_bit_cast(float4, *reinterpret_cast<const uint4*>(at(base, ro + min(c8, kr - 8))));
+      v[2 * q + 1] = make_float4(0.f, 0.f, 0.f, 0.f);
+      const uint32_t in = (row0 + rr < s.rows && c8 < kr) ? 3u : 0u;
+      mask |= in << (2 * q);
+    }
+  } else {
+    const uint16_t* base = p + (int64_t)kk0 * ld + row0;
+    const int rr = 2 * (tid & 127), kc = (tid >> 7) * 8;
+    const bool rin = row0 + rr < s.rows;
+    const int ro = min(rr, s.rows - 2 - row0);
+#pragma unroll
+    for (int j = 0; j < 8; j += 2) {
+      const uint32_t a = *reinterpret_cast<const uint32_t*>(at(base, min(kc + j, kr - 1) * ld + ro));
+      const uint32_t b = *reinterpret_cast<const uint32_t*>(at(base, min(kc + j + 1, kr - 1) * ld + ro));
+      v[j >> 1] = make_float4(__uint_as_float(a), __uint_as_float(b), 0.f, 0.f);
+      mask |= (uint32_t)(rin && kc + j < kr) << j;
+      mask |= (uint32_t)(rin && kc + j + 1 < kr) << (j + 1);
+    }
+  }
+  return mask;
+}
+
+template <bool KC, bool H = false>
 __device__ __forceinline__ uint32_t load(const Src& s, int row0, int k0, int tid, float4 (&v)[4]) {
+  if constexpr (H) return load_h<KC>(s, row0, k0, tid, v);
   const bool seg1 = k0 >= s.k1p;
   const float* __restrict__ p = seg1 ? s.p1 : s.p0;
   const int ld = (int)(seg1 ? s.ld1 : s.ld0);
@@ -347,8 +468,33 @@ __device__ __forceinline__ uint32_t load(const Src& s, int row0, int k0, int tid
   return mask;
 }
 
-template <bool KC, bool SPLIT>
+template <bool KC, bool SPLIT, bool H = false>
 __device__ __forceinline__ void store(const float4 (&v)[4], uint32_t mask, uint4* hi, uint4* lo, int tid) {
+  if constexpr (H) {
+    static_assert(!SPLIT, "a bf16 operand is not split");
+    if constexpr (KC) {
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const int u = tid + 512 * q;
+        const uint32_t m = 0u - ((mask >> (2 * q)) & 1u);
+        const uint4 w = __builtin_bit_cast(uint4, v[2 * q]);
+        hi[unit_of(u >> 2, u & 3)] = make_uint4(w.x & m, w.y & m, w.z & m, w.w & m);
+      }
+    } else {
+      const int rr = 2 * (tid & 127), c = tid >> 7;
+      uint32_t w[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) w[j] = __float_as_uint((j & 1) ? v[j >> 1].y : v[j >> 1].x) & (0u - ((mask >> j) & 1u));
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        uint32_t x[4];
+#pragma unroll
+        for (int pp = 0; pp < 4; ++pp) x[pp] = i ? pair_hi(w[2 * pp], w[2 * pp + 1]) : pair_lo(w[2 * pp], w[2 * pp + 1]);
+        hi[unit_of(rr + i, c)] = make_uint4(x[0], x[1], x[2], x[3]);
+      }
+    }
+    return;
+  }
   if constexpr (KC) {
 #pragma unroll
     for (int q = 0; q < 2; ++q) {
@@ -385,10 +531,10 @@ __device__ __forceinline__ void store(const float4 (&v)[4], uint32_t mask, uint4
   }
 }
 
-template <bool AKC, bool BKC, bool SA, bool SB>
+template <bool AKC, bool BKC, bool SA, bool SB, bool HA, bool HB>
 __global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, int N, float* __restrict__ C,
                                                    int64_t ldc, float beta, float* __restrict__ part, int kchunk, int tn,
-                                                   int tm, const float* __restrict__ gu) {
+                                                   int tm, const float* __restrict__ gu, int hc) {
   static_assert(!(SA && SB), "at most one operand is split");
   constexpr int NT = 2 + (SA ? 1 : 0) + (SB ? 1 : 0);
   constexpr int FM = SA ? 4 : 8, FN = SA ? 8 : 4;  // 16 x 16 fragments per wave along m, n
@@ -409,12 +555,12 @@ __global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, 
   float4 va[4], vb[4];
   uint32_t ma = 0, mbk = 0;
   auto put = [&](int buf) {
-    store<AKC, SA>(va, ma, lds[buf][0], lds[buf][SA ? 2 : 0], tid);
-    store<BKC, SB>(vb, mbk, lds[buf][1], lds[buf][NT - 1], tid);
+    store<AKC, SA, HA>(va, ma, lds[buf][0], lds[buf][SA ? 2 : 0], tid);
+    store<BKC, SB, HB>(vb, mbk, lds[buf][1], lds[buf][NT - 1], tid);
   };
   if (kb < ke) {
-    ma = load<AKC>(A, m0, kb, tid, va);
-    mbk = load<BKC>(B, n0, kb, tid, vb);
+    ma = load<AKC, HA>(A, m0, kb, tid, va);
+    mbk = load<BKC, HB>(B, n0, kb, tid, vb);
     put(0);
   }
   __syncthreads();
@@ -422,8 +568,8 @@ __global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, 
   for (int k0 = kb; k0 < ke; k0 += TK, buf ^= 1) {
     const bool more = k0 + TK < ke;
     if (more) {
-      ma = load<AKC>(A, m0, k0 + TK, tid, va);
-      mbk = load<BKC>(B, n0, k0 + TK, tid, vb);
+      ma = load<AKC, HA>(A, m0, k0 + TK, tid, va);
+      mbk = load<BKC, HB>(B, n0, k0 + TK, tid, vb);
     }
     asm volatile("" ::: "memory");
     uint4 af[FM], bf[FN];
@@ -514,7 +660,12 @@ __global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, 
 #pragma unroll
         for (int nf = 0; nf < FN; ++nf) {
           const int n = nbase + nf * 16;
-          if (n < N) C[(int64_t)m * ldc + n] = acc[rf][nf][r];
+          if (n < N) {
+            if (hc)
+              reinterpret_cast<uint16_t*>(C)[(int64_t)m * ldc + n] = f2bf(acc[rf][nf][r]);
+            else
+              C[(int64_t)m * ldc + n] = acc[rf][nf][r];
+          }
         }
       }
   }
@@ -531,17 +682,31 @@ int splits(int M, int N, int Kp) {
 }
 
 template <bool AKC, bool BKC>
-void launch_orient(bool sa, bool sb, dim3 grid, const Src& A, const Src& B, int Kp, const GemmArgs& g, float* part,
-                   int kchunk, int tn, int tm, hipStream_t s) {
-  if (sa)
-    hipLaunchKernelGGL((k_bgemm_big<AKC, BKC, true, false>), grid, dim3(512), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk, tn, tm, g.gelu_u);
-  else if (sb)
-    hipLaunchKernelGGL((k_bgemm_big<AKC, BKC, false, true>), grid, dim3(512), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk, tn, tm, g.gelu_u);
-  else
-    hipLaunchKernelGGL((k_bgemm_big<AKC, BKC, false, false>), grid, dim3(512), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk, tn, tm, g.gelu_u);
+void launch_orient(bool sa, bool sb, bool ha, bool hb, dim3 grid, const Src& A, const Src& B, int Kp, const GemmArgs& g,
+                   float* part, int kchunk, int tn, int tm, hipStream_t s) {
+#define TRACE_BGEMM(SA_, SB_, HA_, HB_)                                                                       \
+  hipLaunchKernelGGL((k_bgemm_big<AKC, BKC, SA_, SB_, HA_, HB_>), grid, dim3(512), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc, \
+                     g.beta, part, kchunk, tn, tm, g.gelu_u, g.halfC)
+  if (sa) {
+    if (hb)
+      TRACE_BGEMM(true, false, false, true);
+    else
+      TRACE_BGEMM(true, false, false, false);
+  } else if (sb) {
+    if (ha)
+      TRACE_BGEMM(false, true, true, false);
+    else
+      TRACE_BGEMM(false, true, false, false);
+  } else if (ha && hb) {
+    TRACE_BGEMM(false, false, true, true);
+  } else if (ha) {
+    TRACE_BGEMM(false, false, true, false);
+  } else if (hb) {
+    TRACE_BGEMM(false, false, false, true);
+  } else {
+    TRACE_BGEMM(false, false, false, false);
+  }
+#undef TRACE_BGEMM
 }
 }  // namespace big
 
@@ -559,13 +724,20 @@ int bgemm_splits(int M, int N, int Kp) {
 
 bool al16(const void* p) { return ((uintptr_t)p & 15) == 0; }
 
-// Operand (rows x K, element (row, k) at p[row*srow + k*sk]) as segment seg of
-// src; false when the kernel's float4 reads do not fit it.
-bool add_segment(Src& src, int seg, const float* p, int64_t srow, int64_t sk, int rows, int K, bool& kc) {
+// Operand (rows x K, element (row, k) at p[row*srow + k*sk]; bf16 elements
+// when half) as segment seg of src; false when the kernel's vector reads do not
+// fit it (fp32: float4 along the contiguous dimension; bf16: 16-byte units of 8 k
+// when k is contiguous, 8 bytes of 4 rows per k otherwise).
+bool add_segment(Src& src, int seg, const float* p, int64_t srow, int64_t sk, int rows, int K, bool& kc, bool half) {
   const bool this_kc = sk == 1;
   if (!(this_kc || srow == 1)) return false;
   const int64_t ld = this_kc ? srow : sk;
-  if (!al16(p) || ld % 4 != 0 || (this_kc ? K % 4 : rows % 4) != 0) return false;
+  if (half) {
+    if (this_kc ? (!al16(p) || ld % 8 != 0 || K % 8 != 0) : (((uintptr_t)p & 7) != 0 || ld % 4 != 0 || rows % 4 != 0))
+      return false;
+  } else if (!al16(p) || ld % 4 != 0 || (this_kc ? K % 4 : rows % 4) != 0) {
+    return false;
+  }
   if (ld > (1 << 20)) return false;  // byte offsets within a 128 x 64 tile stay below 2^31
   if (seg == 1 && this_kc != kc) return false;
   kc = this_kc;
@@ -577,17 +749,31 @@ bool add_segment(Src& src, int seg, const float* p, int64_t srow, int64_t sk, in
 }
 
 template <bool AKC, bool BKC>
-void launch_orient(bool sa, bool sb, dim3 grid, const Src& A, const Src& B, int Kp, const GemmArgs& g, float* part,
-                   int kchunk, int tn, int tm, hipStream_t s) {
-  if (sa)
-    hipLaunchKernelGGL((k_bgemm<AKC, BKC, true, false>), grid, dim3(256), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk, tn, tm, g.gelu_u);
-  else if (sb)
-    hipLaunchKernelGGL((k_bgemm<AKC, BKC, false, true>), grid, dim3(256), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk, tn, tm, g.gelu_u);
-  else
-    hipLaunchKernelGGL((k_bgemm<AKC, BKC, false, false>), grid, dim3(256), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc,
-                       g.beta, part, kchunk, tn, tm, g.gelu_u);
+void launch_orient(bool sa, bool sb, bool ha, bool hb, dim3 grid, const Src& A, const Src& B, int Kp, const GemmArgs& g,
+                   float* part, int kchunk, int tn, int tm, hipStream_t s) {
+#define TRACE_BGEMM(SA_, SB_, HA_, HB_)                                                                       \
+  hipLaunchKernelGGL((k_bgemm<AKC, BKC, SA_, SB_, HA_, HB_>), grid, dim3(256), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc, \
+                     g.beta, part, kchunk, tn, tm, g.gelu_u, g.halfC)
+  if (sa) {
+    if (hb)
+      TRACE_BGEMM(true, false, false, true);
+    else
+      TRACE_BGEMM(true, false, false, false);
+  } else if (sb) {
+    if (ha)
+      TRACE_BGEMM(false, true, true, false);
+    else
+      TRACE_BGEMM(false, true, false, false);
+  } else if (ha && hb) {
+    TRACE_BGEMM(false, false, true, true);
+  } else if (ha) {
+    TRACE_BGEMM(false, false, true, false);
+  } else if (hb) {
+    TRACE_BGEMM(false, false, false, true);
+  } else {
+    TRACE_BGEMM(false, false, false, false);
+  }
+#undef TRACE_BGEMM
 }
 
 }  // namespace
@@ -599,14 +785,18 @@ int64_t bgemm_ws_floats(int M, int N, int K) {
 
 bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_cap, hipStream_t s) {
   if (!g.roundA && !g.roundB) return false;  // fp32 operands on both sides: not this kernel
-  if (g2 && (g2->M != g.M || g2->N != g.N || g2->roundA != g.roundA || g2->roundB != g.roundB)) return false;
+  if (g2 && (g2->M != g.M || g2->N != g.N || g2->roundA != g.roundA || g2->roundB != g.roundB ||
+             g2->halfA != g.halfA || g2->halfB != g.halfB))
+    return false;
+  // a bf16-stored operand is a storage point (rounded), never split
+  if ((g.halfA && !g.roundA) || (g.halfB && !g.roundB)) return false;
   Src A{}, B{};
   bool akc = false, bkc = false;
-  if (!add_segment(A, 0, g.A, g.sam, g.sak, g.M, g.K, akc)) return false;
-  if (!add_segment(B, 0, g.B, g.sbn, g.sbk, g.N, g.K, bkc)) return false;
+  if (!add_segment(A, 0, g.A, g.sam, g.sak, g.M, g.K, akc, g.halfA)) return false;
+  if (!add_segment(B, 0, g.B, g.sbn, g.sbk, g.N, g.K, bkc, g.halfB)) return false;
   if (g2) {
-    if (!add_segment(A, 1, g2->A, g2->sam, g2->sak, g.M, g2->K, akc)) return false;
-    if (!add_segment(B, 1, g2->B, g2->sbn, g2->sbk, g.N, g2->K, bkc)) return false;
+    if (!add_segment(A, 1, g2->A, g2->sam, g2->sak, g.M, g2->K, akc, g.halfA)) return false;
+    if (!add_segment(B, 1, g2->B, g2->sbn, g2->sbk, g.N, g2->K, bkc, g.halfB)) return false;
   } else {
     A.p1 = A.p0;
     A.ld1 = A.ld0;
@@ -616,7 +806,8 @@ bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_c
   const int K0 = g.K, K1 = g2 ? g2->K : 0;
   if (K0 + K1 == 0) return false;
   if (g.gelu_u && (g.beta != 0.f || g2)) return false;
-  const bool sa = !g.roundA, sb = !g.roundB;
+  if (g.halfC && (g.beta != 0.f || (g.ldc & 3) != 0)) return false;
+  const bool sa = !g.roundA, sb = !g.roundB, ha = g.halfA != 0, hb = g.halfB != 0;
   // the 256-tile kernel when it fills the chip, else the 128-tile one; stages
   // are aligned to each kernel's k step, and so is the start of segment 1
   const int kpb = (int)(rup(K0, big::TK) + rup(K1, big::TK));
@@ -627,7 +818,7 @@ bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_c
   const int Kp = (int)(rup(K0, step) + rup(K1, step));
   if (!use_big) splits = bgemm_splits(g.M, g.N, Kp);
   while (splits > 1 && (int64_t)splits * g.M * g.N > ws_cap) splits /= 2;
-  if (g.gelu_u) splits = 1;  // the epilogue needs the whole sum
+  if (g.gelu_u || g.halfC) splits = 1;  // the epilogue needs the whole sum
   const int kchunk = (int)rup((Kp + splits - 1) / splits, step);
   splits = (Kp + kchunk - 1) / kchunk;
   float* part = splits > 1 ? ws : nullptr;
@@ -636,22 +827,22 @@ bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_c
   const dim3 grid((unsigned)(tn * tm * splits));
   if (use_big) {
     if (akc && bkc)
-      big::launch_orient<true, true>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+      big::launch_orient<true, true>(sa, sb, ha, hb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
     else if (akc)
-      big::launch_orient<true, false>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+      big::launch_orient<true, false>(sa, sb, ha, hb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
     else if (bkc)
-      big::launch_orient<false, true>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+      big::launch_orient<false, true>(sa, sb, ha, hb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
     else
-      big::launch_orient<false, false>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+      big::launch_orient<false, false>(sa, sb, ha, hb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
   } else {
     if (akc && bkc)
-      launch_orient<true, true>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+      launch_orient<true, true>(sa, sb, ha, hb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
     else if (akc)
-      launch_orient<true, false>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+      launch_orient<true, false>(sa, sb, ha, hb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
     else if (bkc)
-      launch_orient<false, true>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+      launch_orient<false, true>(sa, sb, ha, hb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
     else
-      launch_orient<false, false>(sa, sb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
+      launch_orient<false, false>(sa, sb, ha, hb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
   }
   if (splits > 1) launch_splitk_reduce(ws, splits, g.M, g.N, g.C, g.ldc, g.beta, s);
   return true;

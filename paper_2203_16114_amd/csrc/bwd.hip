@@ -371,16 +371,17 @@ void launch_splitk_reduce(const float* ws, int splits, int M, int N, float* C, i
                        beta);
 }
 
-void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s) {
-  if (g.M <= 0 || g.N <= 0) return;
+bool launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s) {
+  if (g.M <= 0 || g.N <= 0) return true;
   // bf16 storage points on at least one side: register-staged bf16 GEMM
-  if (launch_bgemm(g, nullptr, ws, ws_cap, s)) return;
+  if (launch_bgemm(g, nullptr, ws, ws_cap, s)) return true;
+  if (g.halfA || g.halfB || g.halfC) return false;  // the kernels below use fp32 operands and results
   if (g.gelu_u) {  // the product, then the GELU derivative in place (C laid out densely, as gelu_u)
     GemmArgs h = g;
     h.gelu_u = nullptr;
     launch_gemm(h, ws, ws_cap, s);
     launch_gelu_bwd(g.C, g.gelu_u, g.C, (int64_t)g.M * g.N, s);
-    return;
+    return true;
   }
   int splits = gemm_splits(g.M, g.N, g.K);
   while (splits > 1 && (int64_t)splits * g.M * g.N > ws_cap) splits /= 2;
@@ -408,11 +409,12 @@ void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s) {
       hipLaunchKernelGGL(k_gemm<false>, grid, dim3(256), 0, s, g, part, kchunk);
   }
   if (splits > 1) launch_splitk_reduce(ws, splits, g.M, g.N, g.C, g.ldc, g.beta, s);
+  return true;
 }
 
 void launch_gemm2(const GemmArgs& g, const GemmArgs& g2, float* ws, int64_t ws_cap, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return;
-  if (launch_bgemm(g, &g2, ws, ws_cap, s)) return;
+  if (launch_bgemm(g, &g2, ws, ws_cap, s)) return;  // (no operand of these products is stored as bf16)
   launch_gemm(g, ws, ws_cap, s);
   GemmArgs h = g2;
   h.C = g.C;
@@ -894,9 +896,10 @@ void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int
 template <bool BF>
 __global__ __launch_bounds__(256) void k_gather_kept(const uint8_t* __restrict__ win, int64_t rows,
                                                      const typename Mma<BF>::T* __restrict__ E, int T, int D, int e,
-                                                     int g, float* __restrict__ X) {
+                                                     int g, void* __restrict__ X) {
   // thread: four consecutive columns of one token row (row = n*T + t); e is a
-  // multiple of 4, so the four share one byte
+  // multiple of 4, so the four share one byte.  BF: X holds the bf16 operand
+  // values themselves; otherwise fp32
   typedef Mma<BF> M;
   const uint32_t q4 = (uint32_t)D / 4;
   const uint32_t i = blockIdx.x * 256u + threadIdx.x;  // the grid has fewer than 2^32 threads
@@ -908,9 +911,14 @@ __global__ __launch_bounds__(256) void k_gather_kept(const uint8_t* __restrict__
   // the byte of token t, group slot j of window n sits at win[n*T*g + t*g + j] = win[row*g + j]
   const int byte = win[row * g + j];
   const typename M::T* src = E + byte * e + cc;
-  *reinterpret_cast<float4*>(X + row * D + c) = make_float4(M::val(src[0]), M::val(src[1]), M::val(src[2]), M::val(src[3]));
+  if constexpr (BF)
+    *reinterpret_cast<uint2*>((uint16_t*)X + row * D + c) =
+        make_uint2((uint32_t)src[0] | ((uint32_t)src[1] << 16), (uint32_t)src[2] | ((uint32_t)src[3] << 16));
+  else
+    *reinterpret_cast<float4*>((float*)X + row * D + c) =
+        make_float4(M::val(src[0]), M::val(src[1]), M::val(src[2]), M::val(src[3]));
 }
-void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, int T, int D, int e, int g, float* X,
+void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, int T, int D, int e, int g, void* X,
                         hipStream_t s) {
   const int64_t rows = N * T;
   const dim3 grid((unsigned)((rows * (D / 4) + 255) / 256));

@@ -549,9 +549,9 @@ __global__ __launch_bounds__(512) void k_ffn_pipe(FfnArgs a) {
       if (n < N) {
 #pragma unroll
         for (int rf = 0; rf < RF1; ++rf)
-          *reinterpret_cast<float4*>(a.kG + ((int64_t)rep * N + n) * F + c + L.f0 + rf * 16 + 4 * lg) =
-              make_float4(0.5f * round_bf(g[rf][nf][0]), 0.5f * round_bf(g[rf][nf][1]),
-                          0.5f * round_bf(g[rf][nf][2]), 0.5f * round_bf(g[rf][nf][3]));
+          *reinterpret_cast<uint2*>(a.kG + ((int64_t)rep * N + n) * F + c + L.f0 + rf * 16 + 4 * lg) =
+              make_uint2(pack_bf16x2(0.5f * round_bf(g[rf][nf][0]), 0.5f * round_bf(g[rf][nf][1])),
+                         pack_bf16x2(0.5f * round_bf(g[rf][nf][2]), 0.5f * round_bf(g[rf][nf][3])));
       }
     }
   };

@@ -41,7 +41,7 @@ struct FfnArgs {
   float* logits;                   // nullable, [n0 + N][256]
   float* kY;                       // nullable, [k+1][N][D]: Y_0 .. Y_k (fp32)
   float* kU;                       // nullable, [k][N][F]
-  float* kG;                       // nullable, [k][N][F]: GELU(U) as the bf16 operand values (bf16 path)
+  uint16_t* kG;                    // nullable, [k][N][F] bf16: GELU(U) as the operand values (bf16 path)
   float* kZ;                       // nullable, [N][256]
   int32_t* ktgt;                   // nullable, [N]
 };
@@ -90,12 +90,19 @@ struct GemmArgs {
   // nullable: C = (A.B) * GELU'(gelu_u) elementwise, gelu_u laid out as C
   // (the backward of the FFN activation fused into its product); needs beta 0
   const float* gelu_u;
+  // that operand is stored as bf16 (A / B then point at bf16 elements and the
+  // strides count them); only the bf16 kernel reads it, and it must be rounded
+  int halfA, halfB;
+  // C is written as bf16 (rounded to nearest even; C then points at bf16
+  // elements); needs beta 0, and the product is not split over k
+  int halfC;
 };
 // Deterministic: split-K partials are summed in a fixed order.  The split count
 // depends only on (M, N, K, ws_cap); gemm_ws_floats(M, N, K) floats let it
 // reach its preferred value.
 int64_t gemm_ws_floats(int M, int N, int K);
-void launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s);
+// false only when an operand or result stored as bf16 does not fit the bf16 kernel
+bool launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s);
 // C = beta*C + A1.B1 + A2.B2: g and g2 share M, N, C, ldc, beta and rounding
 // flags; one launch when the bf16 kernel takes both, else two
 void launch_gemm2(const GemmArgs& g, const GemmArgs& g2, float* ws, int64_t ws_cap, hipStream_t s);
@@ -119,7 +126,7 @@ void launch_add(float* y, const float* x, int64_t rows, int64_t cols, int64_t ld
 int64_t embed_bwd_ws_floats(int64_t M, int e);  // M = N * W positions
 void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int e, float* dE, float* ws,
                       hipStream_t s);
-void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, int T, int D, int e, int g, float* X,
+void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, int T, int D, int e, int g, void* X,
                         hipStream_t s);
 // dW[i][j] += sum_{u < nt} P[t0 + u][i] * S[u][j]  (P: operand copy [T][D])
 void launch_pos_grad(bool bf, const void* P, const float* S, int t0, int nt, int D, float* dW, hipStream_t s);

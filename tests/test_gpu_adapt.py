@@ -51,8 +51,11 @@ def test_fp32_gradient_matches_oracle(use_pos):
         assert np.all(gp["P"] == 0)
 
 
-def test_bf16_gradient_matches_emulating_oracle():
-    streams, _ = synth.workload_streams(4, L=600, B=512)
+@pytest.mark.parametrize("B", [512, 300])
+def test_bf16_gradient_matches_emulating_oracle(B):
+    """B = 300: the products over the kept windows end in a partial k tile
+    (their operands stored as bf16 included)."""
+    streams, _ = synth.workload_streams(4, L=600, B=B)
     m, cfg, flat, g, _, w, y = _grad_run(SMALL, "bf16", 0x4321, streams, 500)
     _, ref = O.forward_backward(flat, cfg, w, y, mode="bf16")
     gp = O.unflatten(g, cfg)
