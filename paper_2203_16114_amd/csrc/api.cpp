@@ -40,8 +40,8 @@ struct trace_model {
   // backward scratch
   // dY: gradients w.r.t. the k+1 residual states, dU: w.r.t. the k pre-GELU
   // activations (one buffer per repeat, read by the weight gradients later);
-  // in bf16 models dU and Xk (the byte-embedding part of the kept tokens) hold
-  // bf16 elements: both are only read as bf16 operands
+  // in bf16 models dU, Xk (the byte-embedding part of the kept tokens) and the
+  // kept Y hold bf16 elements: all are only read as bf16 operands
   float *dz, *dY, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *sP, *gws, *cws, *ews;
   int64_t gws_cap;
   // second stream of the update step (the weight-gradient branch), its own
@@ -261,7 +261,7 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
     ok = dalloc(m, &m->kwin, K * W) && dalloc(m, &m->ktgt, K * 4) && dalloc(m, &m->kq, K * D * 4) &&
          dalloc(m, &m->kK, K * T * D * 4) && dalloc(m, &m->kV, K * T * D * 4) &&
          dalloc(m, &m->kA, K * cfg->H * T * 4) && dalloc(m, &m->kO, K * D * 4) &&
-         dalloc(m, &m->kY, (cfg->k + 1) * K * D * 4) && dalloc(m, &m->kU, cfg->k * K * F * 4) &&
+         dalloc(m, &m->kY, (cfg->k + 1) * K * D * es) && dalloc(m, &m->kU, cfg->k * K * F * 4) &&
          (!bf || dalloc(m, &m->kG, cfg->k * K * F * 2)) &&
          dalloc(m, &m->kZ, K * 256 * 4) && dalloc(m, &m->dz, K * 256 * 4) &&
          dalloc(m, &m->dY, (cfg->k + 1) * K * D * 4) && dalloc(m, &m->dU, cfg->k * K * F * es) &&
@@ -450,7 +450,7 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   const hipStream_t w = m->side;
   float* ws2 = m->gws2;
   auto dYr = [&](int r) { return m->dY + (int64_t)r * N * D; };  // w.r.t. the input of repeat r (r = k: Y_k)
-  const int hf = m->bf ? 1 : 0;  // dU and Xk stored as bf16
+  const int hf = m->bf ? 1 : 0;  // dU, Xk, kY stored as bf16
   // bf16 element e of a buffer whose elements are bf16 (hf) or fp32
   auto at = [&](float* p, int64_t e) { return hf ? (float*)((uint16_t*)p + e) : p + e; };
   auto dUr = [&](int r) { return at(m->dU, (int64_t)r * N * F); };
@@ -460,8 +460,10 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // side: the byte-embedding part of the tokens (read by the projection
   // gradients), dWout = h_k^T . dz and dbout = sum_n dz
   launch_gather_kept(m->bf, m->kwin, N, m->Ec, T, D, m->cfg.e, m->cfg.g, m->Xk, w);
-  const float* Yk = m->kY + (int64_t)k * N * D;
-  launch_gemm(gemm(D, 256, N, Yk, 1, D, rb, m->dz, 256, 1, rb, gr + L.off[P_WOUT], 256, 0.f), ws2, m->gws_cap, w);
+  GemmArgs go =
+      gemm(D, 256, N, at(m->kY, (int64_t)k * N * D), 1, D, rb, m->dz, 256, 1, rb, gr + L.off[P_WOUT], 256, 0.f);
+  go.halfA = hf;
+  ok = launch_gemm(go, ws2, m->gws_cap, w) && ok;
   launch_colsum(m->dz, N, 256, 256, gr + L.off[P_BOUT], 0.f, m->cws2, w);
   // dY_k = dz . Wout^T
   launch_gemm(gemm(N, D, 256, m->dz, 256, 1, rb, th + L.off[P_WOUT], 1, 256, rb, dYr(k), D, 0.f), ws, m->gws_cap, s);
@@ -487,8 +489,8 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
       g2w = gemm(F, D, N, m->G, 1, F, rb, dYr(r + 1), D, 1, rb, gr + L.off[P_W2], D, beta);
     }
     ok = launch_gemm(g2w, ws2, m->gws_cap, w) && ok;
-    GemmArgs g1w = gemm(D, F, N, m->kY + (int64_t)r * N * D, 1, D, rb, dUr(r), F, 1, rb, gr + L.off[P_W1], F, beta);
-    g1w.halfB = hf;
+    GemmArgs g1w = gemm(D, F, N, at(m->kY, (int64_t)r * N * D), 1, D, rb, dUr(r), F, 1, rb, gr + L.off[P_W1], F, beta);
+    g1w.halfA = g1w.halfB = hf;
     ok = launch_gemm(g1w, ws2, m->gws_cap, w) && ok;
     (void)hipMemcpyAsync(dYr(r), dYr(r + 1), (size_t)N * D * 4, hipMemcpyDeviceToDevice, s);
     GemmArgs gy = gemm(N, D, F, dUr(r), F, 1, rb, th + L.off[P_W1], 1, F, rb, dYr(r), D, 1.f);

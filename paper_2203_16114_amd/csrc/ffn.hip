@@ -233,9 +233,7 @@ __global__ __launch_bounds__(512) void k_ffn_head(FfnArgs a) {
 #pragma unroll
       for (int rf = 0; rf < RF2; ++rf) {
         const int dd = d0 + rf * 16 + 4 * lg;
-        if (KEEP && n < N)
-          *reinterpret_cast<float4*>(a.kY + ((int64_t)rep * N + n) * D + dd) =
-              make_float4(y[rf][nf][0], y[rf][nf][1], y[rf][nf][2], y[rf][nf][3]);
+        if (KEEP && n < N) put4((OT*)a.kY + ((int64_t)rep * N + n) * D + dd, y[rf][nf]);
         put4((OT*)(Ys + m * YSTR) + dd, y[rf][nf]);
       }
     }
@@ -564,9 +562,7 @@ __global__ __launch_bounds__(512) void k_ffn_pipe(FfnArgs a) {
 #pragma unroll
       for (int rf = 0; rf < RF2; ++rf) {
         const int dd = d0 + rf * 16 + 4 * lg;
-        if (KEEP && n < N)
-          *reinterpret_cast<float4*>(a.kY + ((int64_t)rep * N + n) * D + dd) =
-              make_float4(y[rf][nf][0], y[rf][nf][1], y[rf][nf][2], y[rf][nf][3]);
+        if (KEEP && n < N) put4((uint16_t*)a.kY + ((int64_t)rep * N + n) * D + dd, y[rf][nf]);
         put4((uint16_t*)(Ys + m * P::YSTR + swz_elem(m, dd, P::YM)), y[rf][nf]);
       }
     }

@@ -39,7 +39,7 @@ struct FfnArgs {
   int32_t F, k;
   float* bits;                     // [n0 + N] global window index
   float* logits;                   // nullable, [n0 + N][256]
-  float* kY;                       // nullable, [k+1][N][D]: Y_0 .. Y_k (fp32)
+  void* kY;                        // nullable, [k+1][N][D]: Y_0 .. Y_k as operand values (bf16 or fp32)
   float* kU;                       // nullable, [k][N][F]
   uint16_t* kG;                    // nullable, [k][N][F] bf16: GELU(U) as the operand values (bf16 path)
   float* kZ;                       // nullable, [N][256]
