@@ -155,6 +155,20 @@ int trace_set_state(trace_model* m, const float* theta, const float* adam_m, con
  * copied to a host array of trace_param_count floats; synchronises. */
 int trace_get_grads(trace_model* m, float* host_out, int64_t n);
 
+/* One product of the update step on the bf16 GEMM kernels alone (test
+ * support): C[m][n] = sum_k A(m,k) B(k,n), all device memory, C row-major
+ * [M][N].  A(m,k) is d_A[m*K + k] when a_kc, else d_A[k*M + m]; B(k,n) is
+ * d_B[n*K + k] when b_kc, else d_B[k*N + n].  mode_a / mode_b: 0 fp32 rounded
+ * to bf16 as it is read, 1 fp32 split into bf16 hi + lo (two products; not both
+ * operands), 2 bf16 elements.  half_c: C written as bf16 (no split over k).
+ * kernel: 1 the 128-tile kernel, 2 the 256-tile kernel.  d_ws holds ws_floats
+ * floats of split-K partial sums (fewer splits when it is small).  EUNSUPPORTED
+ * when the operands do not fit the kernel's vector reads (fp32: a multiple of 4
+ * along the contiguous dimension; bf16: K a multiple of 8 when k is contiguous,
+ * a multiple of 4 rows otherwise; 16-byte aligned pointers). */
+int trace_debug_gemm(int M, int N, int K, const void* d_A, int a_kc, int mode_a, const void* d_B, int b_kc,
+                     int mode_b, void* d_C, int half_c, int kernel, float* d_ws, int64_t ws_floats, void* stream);
+
 /* Byte-group gather alone (Sec. 4.2): writes the tokens X = E[byte] + P[t],
  * d_X[((b*n_steps + s)*T + t)*d + c] (device, fp32: the sum of the operand
  * copies of E and P, not rounded), for the windows defined as in

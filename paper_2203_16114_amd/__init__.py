@@ -23,7 +23,8 @@ TRACE_KEEP_ACTS = 1
 
 EXPORTS = ("trace_create", "trace_destroy", "trace_param_count", "trace_init_weights", "trace_init_flat_host",
            "trace_forward_bits", "trace_adapt_step", "trace_controller_init", "trace_controller_decide",
-           "trace_get_state", "trace_set_state", "trace_get_grads", "trace_debug_gather", "trace_set_timing",
+           "trace_get_state", "trace_set_state", "trace_get_grads", "trace_debug_gemm", "trace_debug_gather",
+           "trace_set_timing",
            "trace_read_timing", "trace_strerror", "trace_last_error")
 KINDS = ("attn", "ffn_head", "step_ce", "backward", "adam", "refresh")
 
@@ -70,6 +71,8 @@ def lib():
             "trace_get_state": (c_int32, [P, P, P, P, POINTER(c_int64), c_int64]),
             "trace_set_state": (c_int32, [P, P, P, P, c_int64, c_int64]),
             "trace_get_grads": (c_int32, [P, P, c_int64]),
+            "trace_debug_gemm": (c_int32, [c_int32, c_int32, c_int32, P, c_int32, c_int32, P, c_int32, c_int32, P,
+                                           c_int32, c_int32, P, c_int64, P]),
             "trace_debug_gather": (c_int32, [P, P, c_int64, c_int32, c_int64, c_int32, P, P]),
             "trace_set_timing": (c_int32, [P, c_int32]),
             "trace_read_timing": (c_int32, [P, P, P, POINTER(c_int64)]),
@@ -131,6 +134,20 @@ def _stream_ptr(stream=None):
 
 def _dptr(t):
     return c_void_p(t.data_ptr()) if t is not None else None
+
+
+def debug_gemm(A, B, M: int, N: int, K: int, a_kc: bool, mode_a: int, b_kc: bool, mode_b: int,
+               half_c: bool = False, kernel: int = 1, ws_floats: int = 1 << 22, stream=None):
+    """One update-step product on the bf16 GEMM kernels (trace_debug_gemm).  A, B:
+    CUDA tensors (fp32, or int16 holding bf16 bits for mode 2), laid out as that
+    entry point describes; returns C [M][N] (fp32, or int16 bf16 bits)."""
+    import torch
+    C = torch.empty(M, N, dtype=torch.int16 if half_c else torch.float32, device=A.device)
+    ws = torch.empty(max(1, ws_floats), dtype=torch.float32, device=A.device)
+    check(lib().trace_debug_gemm(int(M), int(N), int(K), _dptr(A), int(bool(a_kc)), int(mode_a), _dptr(B),
+                                 int(bool(b_kc)), int(mode_b), _dptr(C), int(bool(half_c)), int(kernel), _dptr(ws),
+                                 int(ws_floats), _stream_ptr(stream)))
+    return C
 
 
 class TraceModel:

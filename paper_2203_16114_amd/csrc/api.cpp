@@ -623,6 +623,27 @@ extern "C" int trace_debug_gather(trace_model* m, const uint8_t* d_streams, int6
   return TRACE_OK;
 }
 
+extern "C" int trace_debug_gemm(int M, int N, int K, const void* d_A, int a_kc, int mode_a, const void* d_B, int b_kc,
+                                int mode_b, void* d_C, int half_c, int kernel, float* d_ws, int64_t ws_floats,
+                                void* stream) {
+  if (M <= 0 || N <= 0 || K <= 0) return fail(TRACE_EINVAL, "M, N, K must be positive");
+  if (!d_A || !d_B || !d_C) return fail(TRACE_EINVAL, "A, B or C is NULL");
+  if (mode_a < 0 || mode_a > 2 || mode_b < 0 || mode_b > 2 || (mode_a == 1 && mode_b == 1))
+    return fail(TRACE_EINVAL, "modes are 0, 1, 2, and at most one operand is split");
+  if (kernel != 1 && kernel != 2) return fail(TRACE_EINVAL, "kernel must be 1 or 2");
+  if (ws_floats < 0 || (ws_floats > 0 && !d_ws)) return fail(TRACE_EINVAL, "workspace");
+  GemmArgs g = gemm(M, N, K, (const float*)d_A, a_kc ? K : 1, a_kc ? 1 : M, mode_a != 1, (const float*)d_B,
+                    b_kc ? 1 : N, b_kc ? K : 1, mode_b != 1, (float*)d_C, N, 0.f);
+  g.halfA = mode_a == 2;
+  g.halfB = mode_b == 2;
+  g.halfC = half_c != 0;
+  if (!launch_bgemm(g, nullptr, d_ws, ws_floats, S(stream), kernel))
+    return fail(TRACE_EUNSUPPORTED, "trace_debug_gemm: the operands do not fit the bf16 kernel");
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "trace_debug_gemm");
+  return TRACE_OK;
+}
+
 extern "C" int trace_set_timing(trace_model* m, int enable) {
   if (!m) return fail(TRACE_EINVAL, "model is NULL");
   m->timing = enable != 0;

@@ -783,7 +783,7 @@ int64_t bgemm_ws_floats(int M, int N, int K) {
   return s > 1 ? (int64_t)s * M * N : 0;
 }
 
-bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_cap, hipStream_t s) {
+bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_cap, hipStream_t s, int force) {
   if (!g.roundA && !g.roundB) return false;  // fp32 operands on both sides: not this kernel
   if (g2 && (g2->M != g.M || g2->N != g.N || g2->roundA != g.roundA || g2->roundB != g.roundB ||
              g2->halfA != g.halfA || g2->halfB != g.halfB))
@@ -812,7 +812,12 @@ bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_c
   // are aligned to each kernel's k step, and so is the start of segment 1
   const int kpb = (int)(rup(K0, big::TK) + rup(K1, big::TK));
   int splits = big::splits(g.M, g.N, kpb);
-  const bool use_big = splits > 0;
+  bool use_big = splits > 0;
+  if (force == 1) use_big = false;
+  if (force == 2 && !use_big) {
+    use_big = true;
+    splits = 1;
+  }
   const int step = use_big ? big::TK : BK;
   A.k1p = B.k1p = (int)rup(K0, step);
   const int Kp = (int)(rup(K0, step) + rup(K1, step));

@@ -109,7 +109,8 @@ void launch_gemm2(const GemmArgs& g, const GemmArgs& g2, float* ws, int64_t ws_c
 void launch_splitk_reduce(const float* ws, int splits, int M, int N, float* C, int64_t ldc, float beta, hipStream_t s);
 // bgemm.hip: false (nothing launched) when the product is not one it takes;
 // g2 (nullable) is a second K segment summed into the same result
-bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_cap, hipStream_t s);
+// force: 0 the kernel the shape calls for, 1 the 128-tile kernel, 2 the 256-tile kernel
+bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_cap, hipStream_t s, int force = 0);
 int64_t bgemm_ws_floats(int M, int N, int K);
 
 void launch_colsum(const float* in, int64_t rows, int64_t cols, int64_t ld, float* out, float beta, float* ws,
