@@ -44,7 +44,9 @@ __device__ __forceinline__ int swz_elem(int m, int e, int mask) { return 16 * ((
 
 // Head on bf(Y_k) staged in Ys, then the code length (shared by both FFN
 // kernels): z^T = Wout^T . Y^T + bout, log-sum-exp across the 4 feature waves
-// through LDS in a fixed order, bits = log2 sum exp(z - max) - (z_y - max) log2 e.
+// through LDS in a fixed order, bits = log2 sum exp(z - max) - (z_y - max) log2 e
+// (each exp(z - max) as the hardware 2^x of (z - max) log2 e: relative error
+// about 1e-7 per term, against 1e-4 bits of parity tolerance).
 // YM >= 0: Ys rows are unpadded and swizzled (unit u of row m at u ^ (m & YM),
 // see swz_off); YM < 0: padded rows, unit u at u.
 template <bool BF, int D, int MB, bool KEEP, int YSTR, int YM = -1>
@@ -129,11 +131,12 @@ __device__ __forceinline__ void ffn_head_out(const FfnArgs& a, const unsigned ch
     const int m = m0 + nf * 16 + lc;
     const int64_t n = tile0 + m;
     const float mx = fmaxf(fmaxf(red[0][0][m], red[0][1][m]), fmaxf(red[0][2][m], red[0][3][m]));
+    const float mxl = -mx * TRACE_LOG2E;
     float se = 0.f;
 #pragma unroll
     for (int rf = 0; rf < RFH; ++rf)
 #pragma unroll
-      for (int r = 0; r < 4; ++r) se += expf(z[rf][nf][r] - mx);
+      for (int r = 0; r < 4; ++r) se += __builtin_amdgcn_exp2f(fmaf(z[rf][nf][r], TRACE_LOG2E, mxl));
     se += __shfl_xor(se, 16, 64);
     se += __shfl_xor(se, 32, 64);
     if (lg == 0) red[1][wr][m] = se;
