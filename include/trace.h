@@ -116,8 +116,12 @@ int trace_init_flat_host(const trace_config* cfg, uint64_t seed, double std, flo
  * its FFN (Eq. 3) shared and applied k times (Sec. 4.3), and a 256-way softmax
  * head reading the last token.  flags may hold TRACE_KEEP_ACTS: the call then
  * also keeps the activations of these n_streams*n_steps <= max_keep windows
- * for trace_adapt_step.  Results depend only on each window's bytes and the
- * weights (not on n_streams, n_steps, chunking or position in the batch). */
+ * for trace_adapt_step.  For a given attention kernel, results depend only on
+ * each window's bytes and the weights (not on n_streams, n_steps, chunking or
+ * position in the batch).  bf16 launches whose 64-window tiles each lie in one
+ * stream (n_steps and the first window a multiple of 64) share byte groups
+ * between windows in a kernel whose sums are ordered differently: their
+ * results agree with the other launches' within rounding, not bit for bit. */
 int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams,
                        int64_t pos0, int32_t n_steps, float* d_bits, float* d_logits,
                        double* d_step_ce, uint32_t flags, void* stream);
@@ -154,6 +158,66 @@ int trace_set_state(trace_model* m, const float* theta, const float* adam_m, con
 /* Gradient (flat, canonical order) computed by the last trace_adapt_step,
  * copied to a host array of trace_param_count floats; synchronises. */
 int trace_get_grads(trace_model* m, float* host_out, int64_t n);
+
+/* ---------------------------------------------------------------- coding ----
+ * Alg. 1, lines 3 and 9: the first W bytes of a stream are coded with
+ * probability 1/256, every later byte with the model's estimate.  The paper
+ * names arithmetic coding and does not fix how the estimate becomes integer
+ * intervals; this library uses:
+ *   frequencies (trace_quantize): for logits z[256] of a window, m = max z,
+ *     d_s = (m - z_s) * log2(e) in float32 (two IEEE operations), u_s =
+ *     trunc(256 d_s + 0.5) (float32) or 32*256-1 if d_s >= 32 (or NaN),
+ *     w_s = T[u_s % 256] >> (u_s / 256), freq_s = 1 + (65280 w_s) / sum w
+ *     (integer division); T as trace_quant_table.  Every freq_s >= 1 and the
+ *     total is at most 65536;
+ *   the coder: a 32-bit range coder (integer renormalisation by bytes, carry
+ *     into the byte held back); a code starts with byte 0, and its decoder
+ *     reads zeros past the end.
+ * Both directions of the compressor run the same launches in the same order,
+ * so the decoder sees bit for bit the encoder's frequencies. */
+
+/* T[j] = round(2^31 * 2^(-j/256)), j < 256, into out[256] (host). */
+int trace_quant_table(uint32_t* out);
+
+/* Frequencies of n windows: d_freq[w*256 + s] (device uint16, 8-byte
+ * aligned) from d_logits[w*256 + s] (device fp32, 16-byte aligned), on the
+ * stream; n = 0 is a no-op. */
+int trace_quantize(const float* d_logits, int64_t n, uint16_t* d_freq, void* stream);
+
+/* One code (host) for sym[i] under frequency row freq[i*freq_stride ..
+ * +256] (each >= 1, total <= 65536), or under 1/256 when freq_stride = 0.
+ * Writes at most cap bytes to out and the code length to *size; EINVAL if cap
+ * is too small (then *size is the length needed). */
+int trace_rc_encode(const uint16_t* freq, int64_t freq_stride, const uint8_t* sym, int64_t n, uint8_t* out,
+                    int64_t cap, int64_t* size);
+/* Inverse of trace_rc_encode: n symbols of the code in[0 .. size) (host). */
+int trace_rc_decode(const uint16_t* freq, int64_t freq_stride, const uint8_t* in, int64_t size, int64_t n,
+                    uint8_t* sym_out);
+
+/* The compressor of Alg. 1 over n_streams streams of `length` bytes each,
+ * stream b at d_streams[b*stride ..] (device).  One code per stream: stream
+ * b's goes to out[b*out_stride ..] (host) and its length to out_sizes[b].
+ * At each position i >= W: one forward over the n_streams windows ending
+ * before i (trace_forward_bits, one step), frequencies (trace_quantize), the
+ * byte at i coded; then, by mode, 0: no update, 1: the controller of Alg. 2
+ * (trace_controller_*, t = ctl_t, delta = ctl_delta) on the batch mean of the
+ * coded lengths log2(total) - log2(freq[x]) (double, streams in order),
+ * 2: always; an update re-runs that forward keeping activations and calls
+ * trace_adapt_step (Alg. 1, line 10).  The model's weights and Adam state
+ * advance as in the loop; *n_updates (may be NULL) counts updates.
+ * n_streams <= max_windows, and <= max_keep when mode != 0.  EINVAL if a code
+ * does not fit out_stride (out_sizes then hold the lengths needed); a code
+ * takes at most about 2 bytes per byte. */
+int trace_compress(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams, int64_t length,
+                   int32_t mode, int32_t ctl_t, double ctl_delta, uint8_t* out, int64_t out_stride,
+                   int64_t* out_sizes, int64_t* n_updates, void* stream);
+/* Inverse of trace_compress, for a model in the state the encoder's started
+ * from: codes at comp[b*comp_stride ..] of comp_sizes[b] bytes (host); the
+ * bytes go to d_out[b*stride ..] (device, stride >= length), byte by byte as
+ * they are decoded, with the same forwards, controller and updates. */
+int trace_decompress(trace_model* m, const uint8_t* comp, int64_t comp_stride, const int64_t* comp_sizes,
+                     int32_t n_streams, int64_t length, int32_t mode, int32_t ctl_t, double ctl_delta,
+                     uint8_t* d_out, int64_t stride, int64_t* n_updates, void* stream);
 
 /* One product of the update step on the bf16 GEMM kernels alone (test
  * support): C[m][n] = sum_k A(m,k) B(k,n), all device memory, C row-major

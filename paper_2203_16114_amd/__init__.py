@@ -23,7 +23,9 @@ TRACE_KEEP_ACTS = 1
 
 EXPORTS = ("trace_create", "trace_destroy", "trace_param_count", "trace_init_weights", "trace_init_flat_host",
            "trace_forward_bits", "trace_adapt_step", "trace_controller_init", "trace_controller_decide",
-           "trace_get_state", "trace_set_state", "trace_get_grads", "trace_debug_gemm", "trace_debug_gather",
+           "trace_get_state", "trace_set_state", "trace_get_grads", "trace_quant_table", "trace_quantize",
+           "trace_rc_encode", "trace_rc_decode", "trace_compress", "trace_decompress",
+           "trace_debug_gemm", "trace_debug_gather",
            "trace_set_timing",
            "trace_read_timing", "trace_strerror", "trace_last_error")
 KINDS = ("attn", "ffn_head", "step_ce", "backward", "adam", "refresh")
@@ -71,6 +73,14 @@ def lib():
             "trace_get_state": (c_int32, [P, P, P, P, POINTER(c_int64), c_int64]),
             "trace_set_state": (c_int32, [P, P, P, P, c_int64, c_int64]),
             "trace_get_grads": (c_int32, [P, P, c_int64]),
+            "trace_quant_table": (c_int32, [P]),
+            "trace_quantize": (c_int32, [P, c_int64, P, P]),
+            "trace_rc_encode": (c_int32, [P, c_int64, P, c_int64, P, c_int64, POINTER(c_int64)]),
+            "trace_rc_decode": (c_int32, [P, c_int64, P, c_int64, c_int64, P]),
+            "trace_compress": (c_int32, [P, P, c_int64, c_int32, c_int64, c_int32, c_int32, c_double, P, c_int64,
+                                         P, POINTER(c_int64), P]),
+            "trace_decompress": (c_int32, [P, P, c_int64, P, c_int32, c_int64, c_int32, c_int32, c_double, P,
+                                           c_int64, POINTER(c_int64), P]),
             "trace_debug_gemm": (c_int32, [c_int32, c_int32, c_int32, P, c_int32, c_int32, P, c_int32, c_int32, P,
                                            c_int32, c_int32, P, c_int64, P]),
             "trace_debug_gather": (c_int32, [P, P, c_int64, c_int32, c_int64, c_int32, P, P]),
@@ -150,6 +160,58 @@ def debug_gemm(A, B, M: int, N: int, K: int, a_kc: bool, mode_a: int, b_kc: bool
     return C
 
 
+MODE_NEVER, MODE_GATED, MODE_ALWAYS = 0, 1, 2
+
+
+def quant_table() -> np.ndarray:
+    """T[j] = round(2^31 2^(-j/256)) of trace_quantize, uint32[256]."""
+    t = np.empty(256, np.uint32)
+    check(lib().trace_quant_table(t.ctypes.data))
+    return t
+
+
+def quantize(logits, freq=None, stream=None):
+    """Integer frequencies (trace_quantize) of CUDA fp32 logits [n][256]:
+    a CUDA int16 tensor [n][256] holding the uint16 values."""
+    import torch
+    if logits.dtype != torch.float32 or not logits.is_cuda or not logits.is_contiguous():
+        raise TypeError("logits must be a contiguous float32 CUDA tensor")
+    n = logits.numel() // 256
+    if freq is None:
+        freq = torch.empty(n, 256, dtype=torch.int16, device=logits.device)
+    check(lib().trace_quantize(_dptr(logits), n, _dptr(freq), _stream_ptr(stream)))
+    return freq
+
+
+def _freq_arg(freq, n):
+    if freq is None:
+        return None, 0, None
+    f = np.ascontiguousarray(freq, np.uint16).reshape(-1, 256)
+    if f.shape[0] < n:
+        raise ValueError("one frequency row per symbol")
+    return f.ctypes.data, 256, f
+
+
+def rc_encode(freq, sym) -> bytes:
+    """One range code (trace_rc_encode) of uint8 symbols under frequency rows
+    [n][256] (uint16), or under 1/256 when freq is None."""
+    x = np.ascontiguousarray(sym, np.uint8)
+    fp, fs, keep = _freq_arg(freq, x.size)
+    cap = 2 * x.size + 16
+    out = np.empty(cap, np.uint8)
+    size = c_int64()
+    check(lib().trace_rc_encode(fp, fs, x.ctypes.data, x.size, out.ctypes.data, cap, byref(size)))
+    return out[:size.value].tobytes()
+
+
+def rc_decode(freq, data: bytes, n: int) -> np.ndarray:
+    fp, fs, keep = _freq_arg(freq, n)
+    buf = np.frombuffer(data, np.uint8) if len(data) else np.zeros(1, np.uint8)
+    out = np.empty(max(n, 1), np.uint8)
+    check(lib().trace_rc_decode(fp, fs, buf.ctypes.data, len(data), n, out.ctypes.data))
+    return out[:n]
+
+
 class TraceModel:
     """One model on the current HIP device (see include/trace.h)."""
 
@@ -210,6 +272,40 @@ class TraceModel:
                                        _dptr(step_ce) if step_ce is not None else None,
                                        TRACE_KEEP_ACTS if keep else 0, _stream_ptr(stream)))
         return {"bits": bits, "logits": logits, "step_ce": step_ce}
+
+    def compress(self, streams, mode: int = MODE_NEVER, t: int = 16, delta: float = 0.05, stream=None):
+        """The compressor of Alg. 1 (trace_compress) over a contiguous uint8
+        CUDA tensor [B][L]: (list of B codes, number of updates)."""
+        import torch
+        if streams.dtype != torch.uint8 or not streams.is_cuda or streams.dim() != 2 or not streams.is_contiguous():
+            raise TypeError("streams must be a contiguous uint8 CUDA tensor [B][L]")
+        B, L = streams.shape
+        cap = 2 * L + 16
+        out = np.empty((B, cap), np.uint8)
+        sizes = np.empty(B, np.int64)
+        nupd = c_int64()
+        check(lib().trace_compress(self._h, _dptr(streams), L, B, L, int(mode), int(t), float(delta),
+                                   out.ctypes.data, cap, sizes.ctypes.data, byref(nupd), _stream_ptr(stream)))
+        return [out[b, :sizes[b]].tobytes() for b in range(B)], nupd.value
+
+    def decompress(self, codes, length: int, mode: int = MODE_NEVER, t: int = 16, delta: float = 0.05,
+                   out=None, stream=None):
+        """Inverse of compress for a model in the encoder's starting state:
+        (uint8 CUDA tensor [B][length], number of updates)."""
+        import torch
+        B = len(codes)
+        cs = max([len(c) for c in codes] + [1])
+        buf = np.zeros((B, cs), np.uint8)
+        for b, c in enumerate(codes):
+            buf[b, :len(c)] = np.frombuffer(c, np.uint8)
+        sizes = np.array([len(c) for c in codes], np.int64)
+        if out is None:
+            out = torch.empty(B, max(int(length), 1), dtype=torch.uint8, device="cuda")
+        nupd = c_int64()
+        check(lib().trace_decompress(self._h, buf.ctypes.data, cs, sizes.ctypes.data, B, int(length), int(mode),
+                                     int(t), float(delta), _dptr(out), out.shape[1], byref(nupd),
+                                     _stream_ptr(stream)))
+        return out[:, :length], nupd.value
 
     def adapt_step(self, stream=None):
         check(lib().trace_adapt_step(self._h, _stream_ptr(stream)))

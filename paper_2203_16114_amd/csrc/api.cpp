@@ -676,3 +676,250 @@ extern "C" int trace_read_timing(trace_model* m, double* ms_total, int64_t* laun
   m->overflow = 0;
   return rc;
 }
+
+// ------------------------------------------------------------- coding ----
+#include "codec.h"
+
+extern "C" int trace_quant_table(uint32_t* out) {
+  if (!out) return fail(TRACE_EINVAL, "out is NULL");
+  std::memcpy(out, quant_table(), 256 * sizeof(uint32_t));
+  return TRACE_OK;
+}
+
+extern "C" int trace_quantize(const float* d_logits, int64_t n, uint16_t* d_freq, void* stream) {
+  if (n < 0) return fail(TRACE_EINVAL, "n must be non-negative");
+  if (n > 0 && (!d_logits || !d_freq)) return fail(TRACE_EINVAL, "NULL buffer");
+  if (((uintptr_t)d_logits & 15) || ((uintptr_t)d_freq & 7))
+    return fail(TRACE_EINVAL, "logits must be 16-byte and freq 8-byte aligned");
+  launch_quantize(d_logits, n, d_freq, (hipStream_t)stream);
+  const hipError_t e = hipGetLastError();
+  return e == hipSuccess ? TRACE_OK : hip_fail(e, "trace_quantize");
+}
+
+extern "C" int trace_rc_encode(const uint16_t* freq, int64_t freq_stride, const uint8_t* sym, int64_t n, uint8_t* out,
+                               int64_t cap, int64_t* size) {
+  if (n < 0 || cap < 0 || freq_stride < 0) return fail(TRACE_EINVAL, "negative size");
+  if ((n > 0 && (!sym || (freq_stride > 0 && !freq))) || !size || (cap > 0 && !out))
+    return fail(TRACE_EINVAL, "NULL buffer");
+  RcEnc enc;
+  enc.out = out;
+  enc.cap = cap;
+  for (int64_t i = 0; i < n; ++i) {
+    const int x = sym[i];
+    if (freq_stride == 0) {
+      enc.encode((uint32_t)x, 1, 256);
+      continue;
+    }
+    const uint16_t* f = freq + i * freq_stride;
+    uint32_t cum = 0, tot = 0;
+    for (int s = 0; s < 256; ++s) {
+      if (s < x) cum += f[s];
+      tot += f[s];
+    }
+    if (f[x] == 0 || tot > 65536) return fail(TRACE_EINVAL, "frequencies must be >= 1 with a total of at most 65536");
+    enc.encode(cum, f[x], tot);
+  }
+  enc.finish();
+  *size = enc.n;
+  return enc.over() ? fail(TRACE_EINVAL, "out is too small for the code (size holds the length needed)") : TRACE_OK;
+}
+
+extern "C" int trace_rc_decode(const uint16_t* freq, int64_t freq_stride, const uint8_t* in, int64_t size, int64_t n,
+                               uint8_t* sym_out) {
+  if (n < 0 || size < 0 || freq_stride < 0) return fail(TRACE_EINVAL, "negative size");
+  if ((n > 0 && (!sym_out || (freq_stride > 0 && !freq))) || (size > 0 && !in)) return fail(TRACE_EINVAL, "NULL buffer");
+  RcDec dec;
+  dec.in = in;
+  dec.size = size;
+  dec.start();
+  for (int64_t i = 0; i < n; ++i) {
+    if (freq_stride == 0) {
+      sym_out[i] = (uint8_t)dec.decode_uniform();
+      continue;
+    }
+    const uint16_t* f = freq + i * freq_stride;
+    uint32_t tot = 0;
+    for (int s = 0; s < 256; ++s) {
+      if (f[s] == 0) return fail(TRACE_EINVAL, "frequencies must be >= 1");
+      tot += f[s];
+    }
+    if (tot > 65536) return fail(TRACE_EINVAL, "frequency total above 65536");
+    sym_out[i] = (uint8_t)dec.decode(f, 256, tot);
+  }
+  return TRACE_OK;
+}
+
+namespace {
+// The loop of Alg. 1 shared by both directions over n_streams streams of
+// `length` bytes: bytes [0, W) at 1/256 (lines 1-5); at each i >= W one
+// forward over the windows ending before i (line 8) -> frequencies -> the
+// coding step code(i, freq) (line 9, which leaves the bytes at i in h) -> the
+// controller on the batch-mean coded length (Alg. 2) -> if it says so, the
+// forward again keeping activations and the backward + Adam (line 10).
+// d_src holds the bytes the forwards read; after code(i) its column i holds
+// the bytes at i (the targets of the keeping forward).
+template <class First, class Code>
+int coding_loop(trace_model* m, const uint8_t* d_src, int64_t stride, int32_t B, int64_t length, int32_t mode,
+                int32_t ctl_t, double ctl_delta, int64_t* n_updates, void* stream, First first, Code code) {
+  const int W = m->cfg.W;
+  hipStream_t s = (hipStream_t)stream;
+  trace_controller ctl;
+  if (mode == 1) {
+    const int rc = trace_controller_init(&ctl, ctl_t, ctl_delta);
+    if (rc) return rc;
+  }
+  int rc = first((int64_t)std::min<int64_t>(W, length));
+  if (rc) return rc;
+  if (length <= W) {
+    if (n_updates) *n_updates = 0;
+    return TRACE_OK;
+  }
+  float *d_logits = nullptr, *d_bits = nullptr;
+  uint16_t* d_freq = nullptr;
+  hipError_t e = hipMalloc(&d_logits, (size_t)B * 256 * 4);
+  if (e == hipSuccess) e = hipMalloc(&d_bits, (size_t)B * 4);
+  if (e == hipSuccess) e = hipMalloc(&d_freq, (size_t)B * 256 * 2);
+  std::vector<uint16_t> hf((size_t)B * 256);
+  int64_t updates = 0;
+  rc = e == hipSuccess ? TRACE_OK : hip_fail(e, "coding buffers");
+  for (int64_t i = W; i < length && rc == TRACE_OK; ++i) {
+    rc = trace_forward_bits(m, d_src, stride, B, i, 1, d_bits, d_logits, nullptr, 0, stream);
+    if (rc) break;
+    launch_quantize(d_logits, B, d_freq, s);
+    e = hipMemcpyAsync(hf.data(), d_freq, hf.size() * 2, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+      rc = hip_fail(e, "coding step");
+      break;
+    }
+    double ce = 0.0;
+    rc = code(i, hf.data(), &ce);
+    if (rc) break;
+    ce /= B;
+    int32_t upd = mode == 2 ? 1 : 0;
+    if (mode == 1) {
+      rc = trace_controller_decide(&ctl, ce, &upd);
+      if (rc) break;
+    }
+    if (upd) {
+      rc = trace_forward_bits(m, d_src, stride, B, i, 1, d_bits, nullptr, nullptr, TRACE_KEEP_ACTS, stream);
+      if (!rc) rc = trace_adapt_step(m, stream);
+      ++updates;
+    }
+  }
+  hipFree(d_logits);
+  hipFree(d_bits);
+  hipFree(d_freq);
+  if (n_updates) *n_updates = updates;
+  return rc;
+}
+
+int coding_args(trace_model* m, int32_t B, int64_t length, int64_t stride, int32_t mode) {
+  if (!m) return fail(TRACE_EINVAL, "model is NULL");
+  if (B < 1 || length < 0 || stride < length) return fail(TRACE_EINVAL, "bad stream count, length or stride");
+  if (mode < 0 || mode > 2) return fail(TRACE_EINVAL, "mode must be 0 (never), 1 (gated) or 2 (always)");
+  if (B > m->max_windows || (mode != 0 && B > m->max_keep))
+    return fail(TRACE_EINVAL, "n_streams above max_windows (or above max_keep when updates are on)");
+  return TRACE_OK;
+}
+
+// coded length of byte x under one frequency row, log2(total) - log2(freq[x])
+double coded_bits(const uint16_t* f, int x, uint32_t* cum_out, uint32_t* tot_out) {
+  uint32_t cum = 0, tot = 0;
+  for (int v = 0; v < 256; ++v) {
+    if (v < x) cum += f[v];
+    tot += f[v];
+  }
+  *cum_out = cum;
+  *tot_out = tot;
+  return std::log2((double)tot) - std::log2((double)f[x]);
+}
+}  // namespace
+
+extern "C" int trace_compress(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams,
+                              int64_t length, int32_t mode, int32_t ctl_t, double ctl_delta, uint8_t* out,
+                              int64_t out_stride, int64_t* out_sizes, int64_t* n_updates, void* stream) {
+  int rc = coding_args(m, n_streams, length, stride, mode);
+  if (rc) return rc;
+  if (!d_streams || !out || !out_sizes || out_stride < 1) return fail(TRACE_EINVAL, "NULL buffer or out_stride < 1");
+  const int32_t B = n_streams;
+  std::vector<uint8_t> h((size_t)B * length);
+  hipStream_t s = (hipStream_t)stream;
+  if (length > 0) {
+    hipError_t e = hipMemcpy2DAsync(h.data(), length, d_streams, stride, length, B, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) return hip_fail(e, "trace_compress");
+  }
+  std::vector<RcEnc> enc(B);
+  for (int32_t b = 0; b < B; ++b) {
+    enc[b].out = out + (int64_t)b * out_stride;
+    enc[b].cap = out_stride;
+  }
+  auto first = [&](int64_t n0) {
+    for (int64_t i = 0; i < n0; ++i)
+      for (int32_t b = 0; b < B; ++b) enc[b].encode(h[(size_t)b * length + i], 1, 256);
+    return TRACE_OK;
+  };
+  auto code = [&](int64_t i, const uint16_t* hf, double* ce) {
+    for (int32_t b = 0; b < B; ++b) {
+      const int x = h[(size_t)b * length + i];
+      uint32_t cum, tot;
+      *ce += coded_bits(hf + (size_t)b * 256, x, &cum, &tot);
+      enc[b].encode(cum, hf[(size_t)b * 256 + x], tot);
+    }
+    return TRACE_OK;
+  };
+  rc = coding_loop(m, d_streams, stride, B, length, mode, ctl_t, ctl_delta, n_updates, stream, first, code);
+  if (rc) return rc;
+  bool over = false;
+  for (int32_t b = 0; b < B; ++b) {
+    enc[b].finish();
+    out_sizes[b] = enc[b].n;
+    over = over || enc[b].over();
+  }
+  return over ? fail(TRACE_EINVAL, "out_stride is too small for a code (out_sizes hold the lengths needed)")
+              : TRACE_OK;
+}
+
+extern "C" int trace_decompress(trace_model* m, const uint8_t* comp, int64_t comp_stride, const int64_t* comp_sizes,
+                                int32_t n_streams, int64_t length, int32_t mode, int32_t ctl_t, double ctl_delta,
+                                uint8_t* d_out, int64_t stride, int64_t* n_updates, void* stream) {
+  int rc = coding_args(m, n_streams, length, stride, mode);
+  if (rc) return rc;
+  if (!comp || !comp_sizes || !d_out) return fail(TRACE_EINVAL, "NULL buffer");
+  const int32_t B = n_streams;
+  for (int32_t b = 0; b < B; ++b)
+    if (comp_sizes[b] < 0 || comp_sizes[b] > comp_stride) return fail(TRACE_EINVAL, "comp_sizes out of range");
+  std::vector<uint8_t> h((size_t)B * std::max<int64_t>(length, 1));
+  std::vector<RcDec> dec(B);
+  for (int32_t b = 0; b < B; ++b) {
+    dec[b].in = comp + (int64_t)b * comp_stride;
+    dec[b].size = comp_sizes[b];
+    dec[b].start();
+  }
+  hipStream_t s = (hipStream_t)stream;
+  // bytes at column i of the host copy -> column i of d_out
+  auto put_cols = [&](int64_t i0, int64_t n) {
+    hipError_t e = hipMemcpy2DAsync(d_out + i0, stride, h.data() + i0, length, n, B, hipMemcpyHostToDevice, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    return e == hipSuccess ? TRACE_OK : hip_fail(e, "trace_decompress");
+  };
+  auto first = [&](int64_t n0) {
+    for (int64_t i = 0; i < n0; ++i)
+      for (int32_t b = 0; b < B; ++b) h[(size_t)b * length + i] = (uint8_t)dec[b].decode_uniform();
+    return n0 > 0 ? put_cols(0, n0) : TRACE_OK;
+  };
+  auto code = [&](int64_t i, const uint16_t* hf, double* ce) {
+    for (int32_t b = 0; b < B; ++b) {
+      const uint16_t* f = hf + (size_t)b * 256;
+      uint32_t tot = 0;
+      for (int v = 0; v < 256; ++v) tot += f[v];
+      const int x = dec[b].decode(f, 256, tot);
+      h[(size_t)b * length + i] = (uint8_t)x;
+      uint32_t cum;
+      *ce += coded_bits(f, x, &cum, &tot);
+    }
+    return put_cols(i, 1);
+  };
+  return coding_loop(m, d_out, stride, B, length, mode, ctl_t, ctl_delta, n_updates, stream, first, code);
+}
