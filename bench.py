@@ -186,6 +186,43 @@ def cpu_baseline(streams, w, n_windows):
                       f"{mode} mode (numpy, {threads} BLAS threads on {cores} host cores), {dt:.1f} s"}
 
 
+def measure_codec(wid, n):
+    """The compressor of Alg. 1 (trace_compress, then trace_decompress on a
+    fresh model in the same starting state) over n positions past the window of
+    every stream of workload wid, with the controller gating updates: real code
+    bytes against the model's estimated bits, both directions timed, and the
+    decoded streams compared with the input."""
+    import torch
+    import paper_2203_16114_amd as P
+    import synth
+    w = synth.WORKLOADS[wid]
+    L = w.W + n
+    streams, _ = synth.workload_streams(wid, L=L)
+    sdev = torch.from_numpy(streams).cuda()
+    mk = lambda: P.TraceModel(w.W, w.e, w.g, w.H, w.F, w.k, dtype=w.dtype, max_windows=w.B, max_keep=w.B)
+    warm = mk()                                  # first launches and allocations, untimed
+    warm.init_weights(w.weight_seed)
+    warm.decompress(warm.compress(sdev[:8, :w.W + 4].contiguous())[0], w.W + 4)
+    enc, dec = mk(), mk()
+    enc.init_weights(w.weight_seed)
+    dec.init_weights(w.weight_seed)
+    torch.cuda.synchronize()
+    t0 = time.time()
+    codes, nu = enc.compress(sdev, mode=P.MODE_GATED, t=16, delta=0.05)
+    t1 = time.time()
+    out, nu2 = dec.decompress(codes, L, mode=P.MODE_GATED, t=16, delta=0.05)
+    torch.cuda.synchronize()
+    t2 = time.time()
+    nbytes = w.B * L
+    code_bytes = sum(len(c) for c in codes)
+    res = {"workload": w.name, "streams": w.B, "bytes_per_stream": L, "updates": nu,
+           "round_trip_exact": bool(torch.equal(out, sdev)) and nu == nu2,
+           "code_bits_per_byte": round(8.0 * code_bytes / nbytes, 4),
+           "compress_bytes_per_s": nbytes / (t1 - t0), "decompress_bytes_per_s": nbytes / (t2 - t1)}
+    log(f"[bench] codec {w.name}: {res}")
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -195,6 +232,7 @@ def main():
     ap.add_argument("--full", action="store_true", help="generate the full 256 KiB streams")
     ap.add_argument("--gated-steps", type=int, default=256, help="steps of each gated-adaptation run (0: skip)")
     ap.add_argument("--cpu-windows", type=int, default=16384, help="oracle sample (0: skip)")
+    ap.add_argument("--codec-steps", type=int, default=64, help="positions of the compress / decompress run (0: skip)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run 5 device-to-device copies of this many MiB (calibrates the HBM "
                          "byte counters FETCH_SIZE / WRITE_SIZE against a copy of known size)")
@@ -291,6 +329,8 @@ def main():
     if args.gated_steps > 0:
         out["gated_adapt"] = {"adapt-bf16": measure_gated(4, args.gated_steps),
                               "large-mixed-bf16": measure_gated(5, max(16, args.gated_steps // 2))}
+    if args.codec_steps > 0:
+        out["codec"] = measure_codec(4, args.codec_steps)
     if args.cpu_windows > 0:
         out["cpu_baseline"] = cpu_baseline(streams, w, args.cpu_windows)
         log(f"[bench] cpu oracle: {out['cpu_baseline']['value']:.4g} bytes/s")

@@ -898,10 +898,24 @@ extern "C" int trace_decompress(trace_model* m, const uint8_t* comp, int64_t com
     dec[b].start();
   }
   hipStream_t s = (hipStream_t)stream;
-  // bytes at column i of the host copy -> column i of d_out
+  // columns [i0, i0 + n) of the host copy -> d_out: each column as one
+  // contiguous copy and a scatter into the rows (strided copies of single
+  // bytes are slow)
+  uint8_t* d_col = nullptr;
+  std::vector<uint8_t> col(B);
+  hipError_t e0 = hipMalloc(&d_col, (size_t)B);
+  if (e0 != hipSuccess) return hip_fail(e0, "trace_decompress");
   auto put_cols = [&](int64_t i0, int64_t n) {
-    hipError_t e = hipMemcpy2DAsync(d_out + i0, stride, h.data() + i0, length, n, B, hipMemcpyHostToDevice, s);
-    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    hipError_t e = hipSuccess;
+    for (int64_t i = i0; i < i0 + n && e == hipSuccess; ++i) {
+      for (int32_t b = 0; b < B; ++b) col[b] = h[(size_t)b * length + i];
+      e = hipMemcpyAsync(d_col, col.data(), (size_t)B, hipMemcpyHostToDevice, s);
+      if (e == hipSuccess) {
+        launch_put_column(d_col, B, d_out, stride, i, s);
+        e = hipGetLastError();
+      }
+      if (e == hipSuccess) e = hipStreamSynchronize(s);
+    }
     return e == hipSuccess ? TRACE_OK : hip_fail(e, "trace_decompress");
   };
   auto first = [&](int64_t n0) {
@@ -921,5 +935,7 @@ extern "C" int trace_decompress(trace_model* m, const uint8_t* comp, int64_t com
     }
     return put_cols(i, 1);
   };
-  return coding_loop(m, d_out, stride, B, length, mode, ctl_t, ctl_delta, n_updates, stream, first, code);
+  rc = coding_loop(m, d_out, stride, B, length, mode, ctl_t, ctl_delta, n_updates, stream, first, code);
+  hipFree(d_col);
+  return rc;
 }

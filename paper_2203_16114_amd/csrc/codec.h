@@ -14,6 +14,8 @@ constexpr int QMAX = 32 * 256 - 1;        // largest fixed-point distance from t
 const uint32_t* quant_table();
 // freq[w][s] for logits z[w][256] of n windows (device), on stream s
 void launch_quantize(const float* z, int64_t n, uint16_t* freq, hipStream_t s);
+// dst[b*stride + col] = src[b], b < n (device)
+void launch_put_column(const uint8_t* src, int64_t n, uint8_t* dst, int64_t stride, int64_t col, hipStream_t s);
 
 // Encoder: low carries into the byte held back in cache (and the run of 0xFF
 // bytes behind it); the first byte written is 0.  Bytes past cap are counted

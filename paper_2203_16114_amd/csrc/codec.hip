@@ -43,7 +43,18 @@ __global__ __launch_bounds__(256) void k_quantize(const float* __restrict__ z, i
   *reinterpret_cast<uint2*>(freq + w * 256 + 4 * lane) =
       make_uint2((uint32_t)f[0] | ((uint32_t)f[1] << 16), (uint32_t)f[2] | ((uint32_t)f[3] << 16));
 }
+// column col of n rows of stride bytes from n contiguous bytes
+__global__ __launch_bounds__(256) void k_put_column(const uint8_t* __restrict__ src, int64_t n,
+                                                    uint8_t* __restrict__ dst, int64_t stride, int64_t col) {
+  const int64_t b = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (b < n) dst[b * stride + col] = src[b];
+}
 }  // namespace
+
+void launch_put_column(const uint8_t* src, int64_t n, uint8_t* dst, int64_t stride, int64_t col, hipStream_t s) {
+  if (n <= 0) return;
+  hipLaunchKernelGGL(k_put_column, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, src, n, dst, stride, col);
+}
 
 const uint32_t* quant_table() {
   static const QuantTab tab = [] {
