@@ -678,7 +678,27 @@ extern "C" int trace_read_timing(trace_model* m, double* ms_total, int64_t* laun
 }
 
 // ------------------------------------------------------------- coding ----
+#include <thread>
+
 #include "codec.h"
+
+namespace {
+// fn(b0, b1) over [0, n) in contiguous pieces on up to 16 host threads (one
+// below 512 items); each item is written by one thread only
+template <class Fn>
+void parallel_for(int64_t n, Fn fn) {
+  const int64_t hw = std::max<int64_t>(1, std::min<int64_t>(16, (int64_t)std::thread::hardware_concurrency()));
+  const int64_t nt = n < 512 ? 1 : std::min<int64_t>(hw, n / 256);
+  if (nt <= 1) {
+    fn((int64_t)0, n);
+    return;
+  }
+  std::vector<std::thread> th;
+  for (int64_t t = 1; t < nt; ++t) th.emplace_back(fn, n * t / nt, n * (t + 1) / nt);
+  fn((int64_t)0, n / nt);
+  for (auto& x : th) x.join();
+}
+}  // namespace
 
 extern "C" int trace_quant_table(uint32_t* out) {
   if (!out) return fail(TRACE_EINVAL, "out is NULL");
@@ -779,21 +799,23 @@ int coding_loop(trace_model* m, const uint8_t* d_src, int64_t stride, int32_t B,
   hipError_t e = hipMalloc(&d_logits, (size_t)B * 256 * 4);
   if (e == hipSuccess) e = hipMalloc(&d_bits, (size_t)B * 4);
   if (e == hipSuccess) e = hipMalloc(&d_freq, (size_t)B * 256 * 2);
-  std::vector<uint16_t> hf((size_t)B * 256);
+  // frequencies land in pinned host memory (one direct copy per position)
+  uint16_t* hf = nullptr;
+  if (e == hipSuccess) e = hipHostMalloc((void**)&hf, (size_t)B * 256 * 2, hipHostMallocDefault);
   int64_t updates = 0;
   rc = e == hipSuccess ? TRACE_OK : hip_fail(e, "coding buffers");
   for (int64_t i = W; i < length && rc == TRACE_OK; ++i) {
     rc = trace_forward_bits(m, d_src, stride, B, i, 1, d_bits, d_logits, nullptr, 0, stream);
     if (rc) break;
     launch_quantize(d_logits, B, d_freq, s);
-    e = hipMemcpyAsync(hf.data(), d_freq, hf.size() * 2, hipMemcpyDeviceToHost, s);
+    e = hipMemcpyAsync(hf, d_freq, (size_t)B * 256 * 2, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
     if (e != hipSuccess) {
       rc = hip_fail(e, "coding step");
       break;
     }
     double ce = 0.0;
-    rc = code(i, hf.data(), &ce);
+    rc = code(i, hf, &ce);
     if (rc) break;
     ce /= B;
     int32_t upd = mode == 2 ? 1 : 0;
@@ -810,6 +832,7 @@ int coding_loop(trace_model* m, const uint8_t* d_src, int64_t stride, int32_t B,
   hipFree(d_logits);
   hipFree(d_bits);
   hipFree(d_freq);
+  if (hf) hipHostFree(hf);
   if (n_updates) *n_updates = updates;
   return rc;
 }
@@ -846,8 +869,16 @@ extern "C" int trace_compress(trace_model* m, const uint8_t* d_streams, int64_t 
   std::vector<uint8_t> h((size_t)B * length);
   hipStream_t s = (hipStream_t)stream;
   if (length > 0) {
-    hipError_t e = hipMemcpy2DAsync(h.data(), length, d_streams, stride, length, B, hipMemcpyDeviceToHost, s);
+    // rows packed on the device, then one copy (a strided copy to the host
+    // moves row by row)
+    uint8_t* d_pack = nullptr;
+    hipError_t e = stride == length ? hipSuccess : hipMalloc(&d_pack, (size_t)B * length);
+    if (e == hipSuccess && d_pack)
+      e = hipMemcpy2DAsync(d_pack, length, d_streams, stride, length, B, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(h.data(), d_pack ? d_pack : d_streams, (size_t)B * length, hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (d_pack) hipFree(d_pack);
     if (e != hipSuccess) return hip_fail(e, "trace_compress");
   }
   std::vector<RcEnc> enc(B);
@@ -860,13 +891,17 @@ extern "C" int trace_compress(trace_model* m, const uint8_t* d_streams, int64_t 
       for (int32_t b = 0; b < B; ++b) enc[b].encode(h[(size_t)b * length + i], 1, 256);
     return TRACE_OK;
   };
+  std::vector<double> cb(B);
   auto code = [&](int64_t i, const uint16_t* hf, double* ce) {
-    for (int32_t b = 0; b < B; ++b) {
-      const int x = h[(size_t)b * length + i];
-      uint32_t cum, tot;
-      *ce += coded_bits(hf + (size_t)b * 256, x, &cum, &tot);
-      enc[b].encode(cum, hf[(size_t)b * 256 + x], tot);
-    }
+    parallel_for(B, [&](int64_t b0, int64_t b1) {
+      for (int64_t b = b0; b < b1; ++b) {
+        const int x = h[(size_t)b * length + i];
+        uint32_t cum, tot;
+        cb[b] = coded_bits(hf + (size_t)b * 256, x, &cum, &tot);
+        enc[b].encode(cum, hf[(size_t)b * 256 + x], tot);
+      }
+    });
+    for (int32_t b = 0; b < B; ++b) *ce += cb[b];  // streams in order
     return TRACE_OK;
   };
   rc = coding_loop(m, d_streams, stride, B, length, mode, ctl_t, ctl_delta, n_updates, stream, first, code);
@@ -923,16 +958,20 @@ extern "C" int trace_decompress(trace_model* m, const uint8_t* comp, int64_t com
       for (int32_t b = 0; b < B; ++b) h[(size_t)b * length + i] = (uint8_t)dec[b].decode_uniform();
     return n0 > 0 ? put_cols(0, n0) : TRACE_OK;
   };
+  std::vector<double> cb(B);
   auto code = [&](int64_t i, const uint16_t* hf, double* ce) {
-    for (int32_t b = 0; b < B; ++b) {
-      const uint16_t* f = hf + (size_t)b * 256;
-      uint32_t tot = 0;
-      for (int v = 0; v < 256; ++v) tot += f[v];
-      const int x = dec[b].decode(f, 256, tot);
-      h[(size_t)b * length + i] = (uint8_t)x;
-      uint32_t cum;
-      *ce += coded_bits(f, x, &cum, &tot);
-    }
+    parallel_for(B, [&](int64_t b0, int64_t b1) {
+      for (int64_t b = b0; b < b1; ++b) {
+        const uint16_t* f = hf + (size_t)b * 256;
+        uint32_t tot = 0;
+        for (int v = 0; v < 256; ++v) tot += f[v];
+        const int x = dec[b].decode(f, 256, tot);
+        h[(size_t)b * length + i] = (uint8_t)x;
+        uint32_t cum;
+        cb[b] = coded_bits(f, x, &cum, &tot);
+      }
+    });
+    for (int32_t b = 0; b < B; ++b) *ce += cb[b];  // streams in order
     return put_cols(i, 1);
   };
   rc = coding_loop(m, d_out, stride, B, length, mode, ctl_t, ctl_delta, n_updates, stream, first, code);
