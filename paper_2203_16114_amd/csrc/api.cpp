@@ -678,26 +678,77 @@ extern "C" int trace_read_timing(trace_model* m, double* ms_total, int64_t* laun
 }
 
 // ------------------------------------------------------------- coding ----
+#include <condition_variable>
+#include <functional>
+#include <mutex>
 #include <thread>
 
 #include "codec.h"
 
 namespace {
-// fn(b0, b1) over [0, n) in contiguous pieces on up to 16 host threads (one
-// below 512 items); each item is written by one thread only
-template <class Fn>
-void parallel_for(int64_t n, Fn fn) {
-  const int64_t hw = std::max<int64_t>(1, std::min<int64_t>(16, (int64_t)std::thread::hardware_concurrency()));
-  const int64_t nt = n < 512 ? 1 : std::min<int64_t>(hw, n / 256);
-  if (nt <= 1) {
-    fn((int64_t)0, n);
-    return;
+// Host threads kept for one compress or decompress call: run(n, fn) calls
+// fn(b0, b1) over [0, n) in contiguous pieces, one per thread (one thread
+// below 512 items, up to 16), and returns when all pieces are done.  Each item
+// is written by one thread only.
+class WorkPool {
+ public:
+  explicit WorkPool(int64_t n_items) {
+    const int64_t hw = std::max<int64_t>(1, std::min<int64_t>(16, (int64_t)std::thread::hardware_concurrency()));
+    nt_ = n_items < 512 ? 1 : std::min<int64_t>(hw, n_items / 256);
+    for (int64_t t = 1; t < nt_; ++t) th_.emplace_back([this, t] { worker(t); });
   }
-  std::vector<std::thread> th;
-  for (int64_t t = 1; t < nt; ++t) th.emplace_back(fn, n * t / nt, n * (t + 1) / nt);
-  fn((int64_t)0, n / nt);
-  for (auto& x : th) x.join();
-}
+  ~WorkPool() {
+    {
+      std::lock_guard<std::mutex> lk(mu_);
+      stop_ = true;
+    }
+    cv_.notify_all();
+    for (auto& x : th_) x.join();
+  }
+  void run(int64_t n, const std::function<void(int64_t, int64_t)>& fn) {
+    if (nt_ <= 1) {
+      fn(0, n);
+      return;
+    }
+    {
+      std::lock_guard<std::mutex> lk(mu_);
+      fn_ = &fn;
+      n_ = n;
+      left_ = nt_ - 1;
+      ++gen_;
+    }
+    cv_.notify_all();
+    fn(0, n / nt_);
+    std::unique_lock<std::mutex> lk(mu_);
+    done_.wait(lk, [&] { return left_ == 0; });
+  }
+
+ private:
+  void worker(int64_t t) {
+    int64_t seen = 0;
+    for (;;) {
+      const std::function<void(int64_t, int64_t)>* f;
+      int64_t n;
+      {
+        std::unique_lock<std::mutex> lk(mu_);
+        cv_.wait(lk, [&] { return stop_ || gen_ != seen; });
+        if (stop_) return;
+        seen = gen_;
+        f = fn_;
+        n = n_;
+      }
+      (*f)(n * t / nt_, n * (t + 1) / nt_);
+      std::lock_guard<std::mutex> lk(mu_);
+      if (--left_ == 0) done_.notify_one();
+    }
+  }
+  int64_t nt_ = 1, n_ = 0, left_ = 0, gen_ = 0;
+  bool stop_ = false;
+  const std::function<void(int64_t, int64_t)>* fn_ = nullptr;
+  std::vector<std::thread> th_;
+  std::mutex mu_;
+  std::condition_variable cv_, done_;
+};
 }  // namespace
 
 extern "C" int trace_quant_table(uint32_t* out) {
@@ -892,8 +943,9 @@ extern "C" int trace_compress(trace_model* m, const uint8_t* d_streams, int64_t 
     return TRACE_OK;
   };
   std::vector<double> cb(B);
+  WorkPool pool(B);
   auto code = [&](int64_t i, const uint16_t* hf, double* ce) {
-    parallel_for(B, [&](int64_t b0, int64_t b1) {
+    pool.run(B, [&](int64_t b0, int64_t b1) {
       for (int64_t b = b0; b < b1; ++b) {
         const int x = h[(size_t)b * length + i];
         uint32_t cum, tot;
@@ -959,8 +1011,9 @@ extern "C" int trace_decompress(trace_model* m, const uint8_t* comp, int64_t com
     return n0 > 0 ? put_cols(0, n0) : TRACE_OK;
   };
   std::vector<double> cb(B);
+  WorkPool pool(B);
   auto code = [&](int64_t i, const uint16_t* hf, double* ce) {
-    parallel_for(B, [&](int64_t b0, int64_t b1) {
+    pool.run(B, [&](int64_t b0, int64_t b1) {
       for (int64_t b = b0; b < b1; ++b) {
         const uint16_t* f = hf + (size_t)b * 256;
         uint32_t tot = 0;

@@ -108,3 +108,18 @@ def test_short_streams_and_errors():
     assert np.array_equal(out.cpu().numpy(), s)
     with pytest.raises(P.TraceError):                    # updates need max_keep >= streams
         m.compress(to_dev(synth.random_streams(4, 3, 40)), mode=C.MODE_GATED)
+
+
+def test_round_trip_large_shape_gated():
+    """The large mixed workload's shape (d=512, e=64, W=64, F=2048, k=3, bf16),
+    64 streams, controller-gated: every byte back, the same updates and the
+    same final weights."""
+    shape, dtype = workload_cfg(5)
+    L = 64 + 40
+    streams, _ = synth.workload_streams(5, L=L, B=64)
+    enc = make_model(shape, dtype, seed=2, max_windows=64, max_keep=64)
+    dec = make_model(shape, dtype, seed=2, max_windows=64, max_keep=64)
+    codes, nu = enc.compress(to_dev(streams), mode=C.MODE_GATED, t=4, delta=0.0)
+    out, nu2 = dec.decompress(codes, L, mode=C.MODE_GATED, t=4, delta=0.0)
+    assert np.array_equal(out.cpu().numpy(), streams) and nu == nu2 and nu >= 4
+    assert np.array_equal(enc.get_state()[0], dec.get_state()[0])
