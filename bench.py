@@ -223,6 +223,77 @@ def measure_codec(wid, n):
     return res
 
 
+def measure_sweep():
+    """Synthetic analogues of the paper's Eq. 5 study (Fig. 3) and of its
+    batch-size table: (1) for attention width d in {128, 256} and FFN width F in
+    {512, ..., 4096} (W=32, g=4, T=8, k=2, bf16), the model adapts on the small
+    workload's stream mix (order-2 Markov and Zipf bytes), 512 streams (the
+    paper's batch), with an update every step for 4096 steps; then its
+    compression ratio CR = 8 / (bits per byte of the next 64 positions, no
+    update) and its latency t (one forward step over the 512 windows) give
+    LCR = (t - t0) / (CR - CR0) against (d, F) = (128, 512); (2) forward
+    throughput and the model's device memory of the main workload's model at
+    128 to 8192 streams of 256 positions."""
+    import numpy as np
+    import torch
+    import paper_2203_16114_amd as P
+    import synth
+    B, S_ad, S_ev = 512, 4096, 64
+    streams, _ = synth.workload_streams(2, L=32 + S_ad + S_ev + 1, B=B)
+    assert streams.shape[0] == B
+    sdev = torch.from_numpy(streams).cuda()
+    rows = []
+    for d in (128, 256):
+        for F in (512, 1024, 2048, 4096):
+            m = P.TraceModel(32, d // 4, 4, d // 32, F, 2, dtype="bf16", max_windows=B * S_ev, max_keep=B)
+            m.init_weights(7)
+            for i in range(S_ad):
+                m.forward_bits(sdev, 32 + i, 1, keep=True)
+                m.adapt_step()
+            ce = torch.empty(S_ev, dtype=torch.float64, device="cuda")
+            bits = torch.empty(B * S_ev, dtype=torch.float32, device="cuda")
+            m.forward_bits(sdev, 32 + S_ad, S_ev, bits=bits, step_ce=ce)       # warm
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            m.forward_bits(sdev, 32 + S_ad, S_ev, bits=bits, step_ce=ce)
+            e1.record()
+            torch.cuda.synchronize()
+            bpb = float(ce.mean())
+            rows.append({"d": d, "F": F, "bits_per_byte": round(bpb, 4), "cr": round(8.0 / bpb, 4),
+                         "ms_per_step": round(e0.elapsed_time(e1) / S_ev, 4)})
+            del m
+            log(f"[bench] sweep {rows[-1]}")
+    r0 = rows[0]
+    for r in rows[1:]:
+        dcr = r["cr"] - r0["cr"]
+        r["lcr_ms"] = round((r["ms_per_step"] - r0["ms_per_step"]) / dcr, 4) if abs(dcr) > 1e-6 else None
+    w = synth.WORKLOADS[3]
+    st, _ = synth.workload_streams(3, L=w.W + 256 * 4 + 1)
+    st = np.concatenate([st, st[::-1]])[:8192]       # the workload holds 4096 streams
+    batch = []
+    for nb in (128, 512, 2048, 8192):
+        sd = torch.from_numpy(np.ascontiguousarray(st[:nb])).cuda()
+        torch.cuda.synchronize()
+        free0 = torch.cuda.mem_get_info()[0]
+        m = P.TraceModel(w.W, w.e, w.g, w.H, w.F, w.k, dtype=w.dtype, max_windows=nb * 256)
+        m.init_weights(w.weight_seed)
+        out = torch.empty(nb * 256, dtype=torch.float32, device="cuda")
+        torch.cuda.synchronize()
+        held = free0 - torch.cuda.mem_get_info()[0]
+        m.forward_bits(sd, w.W, 256, bits=out)
+        torch.cuda.synchronize()
+        t0 = time.time()
+        for i in range(3):
+            m.forward_bits(sd, w.W + 256 * (i + 1), 256, bits=out)
+        torch.cuda.synchronize()
+        batch.append({"streams": nb, "bytes_per_s": round(nb * 256 * 3 / (time.time() - t0), 1),
+                      "device_mib": round(held / 2**20, 1)})
+        del m, out, sd
+        log(f"[bench] batch {batch[-1]}")
+    return {"lcr": rows, "batch": batch}
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -233,6 +304,7 @@ def main():
     ap.add_argument("--gated-steps", type=int, default=256, help="steps of each gated-adaptation run (0: skip)")
     ap.add_argument("--cpu-windows", type=int, default=16384, help="oracle sample (0: skip)")
     ap.add_argument("--codec-steps", type=int, default=64, help="positions of the compress / decompress run (0: skip)")
+    ap.add_argument("--sweep", action="store_true", help="only the LCR and batch-size sweeps (one JSON line)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run 5 device-to-device copies of this many MiB (calibrates the HBM "
                          "byte counters FETCH_SIZE / WRITE_SIZE against a copy of known size)")
@@ -247,6 +319,9 @@ def main():
     import paper_2203_16114_amd as P
     import synth
 
+    if args.sweep:
+        print(json.dumps({"sweep": measure_sweep()}), flush=True)
+        return
     if args.copy_probe_mib > 0:
         n = args.copy_probe_mib << 20
         src = torch.empty(n, dtype=torch.uint8, device="cuda").fill_(1)
