@@ -273,18 +273,21 @@ class TraceModel:
                                        TRACE_KEEP_ACTS if keep else 0, _stream_ptr(stream)))
         return {"bits": bits, "logits": logits, "step_ce": step_ce}
 
-    def compress(self, streams, mode: int = MODE_NEVER, t: int = 16, delta: float = 0.05, stream=None):
+    def compress(self, streams, mode: int = MODE_NEVER, t: int = 16, delta: float = 0.05, length=None,
+                 stream=None):
         """The compressor of Alg. 1 (trace_compress) over a contiguous uint8
-        CUDA tensor [B][L]: (list of B codes, number of updates)."""
+        CUDA tensor [B][stride], coding the first `length` bytes of each row
+        (all by default): (list of B codes, number of updates)."""
         import torch
         if streams.dtype != torch.uint8 or not streams.is_cuda or streams.dim() != 2 or not streams.is_contiguous():
             raise TypeError("streams must be a contiguous uint8 CUDA tensor [B][L]")
-        B, L = streams.shape
+        B, stride = streams.shape
+        L = stride if length is None else int(length)
         cap = 2 * L + 16
         out = np.empty((B, cap), np.uint8)
         sizes = np.empty(B, np.int64)
         nupd = c_int64()
-        check(lib().trace_compress(self._h, _dptr(streams), L, B, L, int(mode), int(t), float(delta),
+        check(lib().trace_compress(self._h, _dptr(streams), stride, B, L, int(mode), int(t), float(delta),
                                    out.ctypes.data, cap, sizes.ctypes.data, byref(nupd), _stream_ptr(stream)))
         return [out[b, :sizes[b]].tobytes() for b in range(B)], nupd.value
 

@@ -123,3 +123,22 @@ def test_round_trip_large_shape_gated():
     out, nu2 = dec.decompress(codes, L, mode=C.MODE_GATED, t=4, delta=0.0)
     assert np.array_equal(out.cpu().numpy(), streams) and nu == nu2 and nu >= 4
     assert np.array_equal(enc.get_state()[0], dec.get_state()[0])
+
+
+def test_strided_streams():
+    """Rows longer than the coded length (the encoder packs them on the device;
+    the decoder writes into wider rows): the same codes as the packed layout."""
+    import torch
+    shape = dict(W=16, e=16, g=4, H=1, F=256, k=2)
+    s = synth.random_streams(8, 700, 90)                 # 700 streams: the threaded coding path
+    wide = np.concatenate([s, np.full((700, 13), 0xAB, np.uint8)], axis=1)
+    a, _ = make_model(shape, "fp32", seed=3, max_windows=1024, max_keep=1024).compress(
+        to_dev(wide), mode=C.MODE_ALWAYS, length=90)
+    b, _ = make_model(shape, "fp32", seed=3, max_windows=1024, max_keep=1024).compress(
+        to_dev(s), mode=C.MODE_ALWAYS)
+    assert a == b
+    out = torch.full((700, 103), 7, dtype=torch.uint8, device="cuda")
+    got, nu = make_model(shape, "fp32", seed=3, max_windows=1024, max_keep=1024).decompress(
+        a, 90, mode=C.MODE_ALWAYS, out=out)
+    o = out.cpu().numpy()
+    assert np.array_equal(o[:, :90], s) and np.all(o[:, 90:] == 7) and nu == 90 - 16
