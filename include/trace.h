@@ -73,6 +73,11 @@ typedef struct {
   int64_t max_windows;
   int64_t max_keep;
   double lr, beta1, beta2, eps; /* used as float, except beta^t in double for the bias corrections */
+  /* 0: the k repeats of Eq. 3 share W1, W2 (Sec. 4.3); 1: each repeat has its
+   * own (the deep-FFN variant of Sec. 6.3): W1 and W2 in the flat order become
+   * k consecutive blocks, repeat r's at r * D * F. */
+  int32_t untied_ffn;
+  int32_t reserved_; /* 0 */
 } trace_config;
 
 typedef struct trace_model trace_model; /* opaque, library-owned */

@@ -61,6 +61,9 @@ class Config:
     beta1: float = 0.9
     beta2: float = 0.999
     eps: float = 1e-8
+    # False: the k repeats share W1, W2 (Sec. 4.3); True: one W1, W2 per repeat
+    # (the deep-FFN variant of Sec. 6.3), stored as k consecutive blocks
+    untied: bool = False
 
     @property
     def T(self) -> int:  # tokens per window (Sec. 4.2: c groups)
@@ -85,8 +88,8 @@ def param_layout(cfg: Config):
         ("Wk", (d, d)),
         ("Wv", (d, d)),
         ("Wo", (d, d)),
-        ("W1", (d, F)),
-        ("W2", (F, d)),
+        ("W1", (cfg.k, d, F) if cfg.untied else (d, F)),
+        ("W2", (cfg.k, F, d) if cfg.untied else (F, d)),
         ("Wout", (d, 256)),
         ("bout", (256,)),
     ]
@@ -294,11 +297,13 @@ def forward(flat: np.ndarray, cfg: Config, windows: np.ndarray, targets: np.ndar
     Attn = Oo @ p["Wo"]                                 # Eq. 2 projection W
     Y = [Attn + X]                                      # Eq. 4 inner residual
     U, Yop, Gop = [], [], []
-    for _ in range(cfg.k):                              # Sec. 4.3, shared W1, W2
+    for r in range(cfg.k):                              # Sec. 4.3, shared W1, W2 (Sec. 6.3: untied)
+        W1r = p["W1"][r] if cfg.untied else p["W1"]
+        W2r = p["W2"][r] if cfg.untied else p["W2"]
         yo = m.R(Y[-1])
-        u = yo @ p["W1"]
+        u = yo @ W1r
         go = m.R(gelu(u))
-        Y.append(Y[-1] + go @ p["W2"])
+        Y.append(Y[-1] + go @ W2r)
         U.append(u); Yop.append(yo); Gop.append(go)
     hk = m.R(Y[-1][:, T - 1, :])
     z = hk @ p["Wout"] + p["bout"]
@@ -357,13 +362,16 @@ def backward(cache: dict, cfg: Config) -> dict:
     g["W1"] = np.zeros_like(p["W1"])
     g["W2"] = np.zeros_like(p["W2"])
     for r in reversed(range(cfg.k)):
+        # untied: repeat r's own blocks (views, so += lands in g)
+        gW1, gW2 = (g["W1"][r], g["W2"][r]) if cfg.untied else (g["W1"], g["W2"])
+        W1r, W2r = (p["W1"][r], p["W2"][r]) if cfg.untied else (p["W1"], p["W2"])
         dYo = m.R(dY)
-        g["W2"] += np.einsum("ntf,ntc->fc", cache["Gop"][r], dYo)
-        dG = dYo @ p["W2"].T
+        gW2 += np.einsum("ntf,ntc->fc", cache["Gop"][r], dYo)
+        dG = dYo @ W2r.T
         dU = dG * gelu_grad(cache["U"][r])
         dUo = m.R(dU)
-        g["W1"] += np.einsum("ntc,ntf->cf", cache["Yop"][r], dUo)
-        dY = dY + dUo @ p["W1"].T
+        gW1 += np.einsum("ntc,ntf->cf", cache["Yop"][r], dUo)
+        dY = dY + dUo @ W1r.T
     dY0 = dY
     dY0o = m.R(dY0)
     g["Wo"] = np.einsum("ntc,nto->co", cache["Oo"], dY0o)

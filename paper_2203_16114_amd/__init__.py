@@ -40,7 +40,8 @@ class TraceError(RuntimeError):
 class TraceConfig(ctypes.Structure):
     _fields_ = [("W", c_int32), ("e", c_int32), ("g", c_int32), ("H", c_int32), ("F", c_int32), ("k", c_int32),
                 ("dtype", c_int32), ("use_pos", c_int32), ("max_windows", c_int64), ("max_keep", c_int64),
-                ("lr", c_double), ("beta1", c_double), ("beta2", c_double), ("eps", c_double)]
+                ("lr", c_double), ("beta1", c_double), ("beta2", c_double), ("eps", c_double),
+                ("untied_ffn", c_int32), ("reserved_", c_int32)]
 
 
 class TraceControllerState(ctypes.Structure):
@@ -58,6 +59,12 @@ def lib():
         if not os.path.exists(LIB_PATH):
             raise ImportError(f"{LIB_PATH} is missing: build it with __graft_entry__.build() "
                               "or python paper_2203_16114_amd/build.py")
+        # PyTorch's HIP runtime first: loaded after the library's, it finds no
+        # GPU; loaded first, the library and PyTorch share it
+        try:
+            import torch  # noqa: F401
+        except ImportError:
+            pass
         L = ctypes.CDLL(LIB_PATH)
         P = c_void_p
         sig = {
@@ -104,10 +111,10 @@ def check(rc: int):
 
 
 def make_config(W, e, g, H, F, k, dtype="fp32", use_pos=True, max_windows=1 << 16, max_keep=0,
-                lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8) -> TraceConfig:
+                lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, untied_ffn=False) -> TraceConfig:
     dt = {"fp32": TRACE_FP32, "bf16": TRACE_BF16}[dtype] if isinstance(dtype, str) else int(dtype)
     return TraceConfig(W, e, g, H, F, k, dt, int(bool(use_pos)), int(max_windows), int(max_keep),
-                       float(lr), float(beta1), float(beta2), float(eps))
+                       float(lr), float(beta1), float(beta2), float(eps), int(bool(untied_ffn)), 0)
 
 
 def param_count(cfg: TraceConfig) -> int:
@@ -216,8 +223,9 @@ class TraceModel:
     """One model on the current HIP device (see include/trace.h)."""
 
     def __init__(self, W, e, g, H, F, k, dtype="fp32", use_pos=True, max_windows=1 << 16, max_keep=0,
-                 lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8):
-        self.cfg = make_config(W, e, g, H, F, k, dtype, use_pos, max_windows, max_keep, lr, beta1, beta2, eps)
+                 lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, untied_ffn=False):
+        self.cfg = make_config(W, e, g, H, F, k, dtype, use_pos, max_windows, max_keep, lr, beta1, beta2, eps,
+                               untied_ffn)
         self.W, self.e, self.g, self.H, self.F, self.k = W, e, g, H, F, k
         self.T, self.d = W // g, g * e
         self.dtype = dtype

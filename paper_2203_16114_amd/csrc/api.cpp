@@ -192,7 +192,16 @@ bool refresh_operands(trace_model* m, hipStream_t s) {
       pos ? job(RJ_CVT, th + L.off[P_P], m->Pc, L.size[P_P], 0)
           : job(RJ_ZERO, nullptr, m->Pc, (L.size[P_P] * (m->bf ? 2 : 4) + 3) / 4, 0),
   };
-  const bool ok = launch_refresh(m->bf, jobs, (int)(sizeof(jobs) / sizeof(jobs[0])), s);
+  bool ok = launch_refresh(m->bf, jobs, (int)(sizeof(jobs) / sizeof(jobs[0])), s);
+  // untied FFN: the packed copies of repeats 1 .. k-1
+  const int64_t es_ = m->bf ? 2 : 4;
+  for (int r = 1; ok && m->cfg.untied_ffn && r < m->cfg.k; ++r) {
+    const RefreshJob more[] = {
+        job(RJ_PACK, th + L.off[P_W1] + (int64_t)r * D * F, (char*)m->W1 + (int64_t)r * D * F * es_, D, F),
+        job(RJ_PACK, th + L.off[P_W2] + (int64_t)r * F * D, (char*)m->W2 + (int64_t)r * F * D * es_, F, D,
+            m->bf ? 0.5f : 1.f)};
+    ok = launch_refresh(m->bf, more, 2, s);
+  }
   tend(m, tk, TRACE_KIND_REFRESH, s);
   return ok;
 }
@@ -254,7 +263,8 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
             dalloc(m, &m->grad, n * 4) && dalloc(m, &m->Ec, L.size[P_E] * es) && dalloc(m, &m->Pc, L.size[P_P] * es) &&
             dalloc(m, &m->PW, 3 * T * D * 4) &&
             dalloc(m, &m->Wq, D * D * es) && dalloc(m, &m->Wk, D * D * es) && dalloc(m, &m->Wv, D * D * es) &&
-            dalloc(m, &m->Wo, D * D * es) && dalloc(m, &m->W1, D * F * es) && dalloc(m, &m->W2, F * D * es) &&
+            dalloc(m, &m->Wo, D * D * es) && dalloc(m, &m->W1, D * F * es * (cfg->untied_ffn ? cfg->k : 1)) &&
+            dalloc(m, &m->W2, F * D * es * (cfg->untied_ffn ? cfg->k : 1)) &&
             dalloc(m, &m->Wout, D * 256 * es) && dalloc(m, &m->h0, m->max_windows * D * 4);
   const int64_t K = cfg->max_keep;
   if (ok && K > 0) {
@@ -388,6 +398,7 @@ extern "C" int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int6
     f.h0 = m->h0;
     f.W1 = m->W1;
     f.W2 = m->W2;
+    f.wstride = m->cfg.untied_ffn ? (int64_t)m->L.D * m->cfg.F * (m->bf ? 2 : 4) / 16 : 0;
     f.Wout = m->Wout;
     f.bout = m->theta + L.off[P_BOUT];
     f.F = m->cfg.F;
@@ -473,27 +484,29 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // in reverse; G = GELU(U) at its storage point: kept by the bf16 forward,
   // formed here otherwise)
   for (int r = k - 1; r >= 0; --r) {
-    GemmArgs gd = gemm(N, F, D, dYr(r + 1), D, 1, rb, th + L.off[P_W2], 1, D, rb, dUr(r), F, 0.f);
+    // untied FFN: repeat r's own W1, W2 and gradient blocks (each written once)
+    const int64_t wr = m->cfg.untied_ffn ? (int64_t)r * D * F : 0;
+    GemmArgs gd = gemm(N, F, D, dYr(r + 1), D, 1, rb, th + L.off[P_W2] + wr, 1, D, rb, dUr(r), F, 0.f);
     gd.gelu_u = m->kU + (int64_t)r * N * F;
     gd.halfC = hf;
     ok = launch_gemm(gd, ws, m->gws_cap, s) && ok;
     order(m, s, w);  // dY_{r+1} and dU_r are complete
-    const float beta = (r == k - 1) ? 0.f : 1.f;
+    const float beta = (r == k - 1 || m->cfg.untied_ffn) ? 0.f : 1.f;
     GemmArgs g2w;
     if (m->kG) {
       g2w = gemm(F, D, N, (const float*)(m->kG + (int64_t)r * N * F), 1, F, rb, dYr(r + 1), D, 1, rb,
-                 gr + L.off[P_W2], D, beta);
+                 gr + L.off[P_W2] + wr, D, beta);
       g2w.halfA = 1;
     } else {
       launch_gelu_fwd_round(m->kU + (int64_t)r * N * F, m->G, (int64_t)N * F, rb, w);
-      g2w = gemm(F, D, N, m->G, 1, F, rb, dYr(r + 1), D, 1, rb, gr + L.off[P_W2], D, beta);
+      g2w = gemm(F, D, N, m->G, 1, F, rb, dYr(r + 1), D, 1, rb, gr + L.off[P_W2] + wr, D, beta);
     }
     ok = launch_gemm(g2w, ws2, m->gws_cap, w) && ok;
-    GemmArgs g1w = gemm(D, F, N, at(m->kY, (int64_t)r * N * D), 1, D, rb, dUr(r), F, 1, rb, gr + L.off[P_W1], F, beta);
+    GemmArgs g1w = gemm(D, F, N, at(m->kY, (int64_t)r * N * D), 1, D, rb, dUr(r), F, 1, rb, gr + L.off[P_W1] + wr, F, beta);
     g1w.halfA = g1w.halfB = hf;
     ok = launch_gemm(g1w, ws2, m->gws_cap, w) && ok;
     (void)hipMemcpyAsync(dYr(r), dYr(r + 1), (size_t)N * D * 4, hipMemcpyDeviceToDevice, s);
-    GemmArgs gy = gemm(N, D, F, dUr(r), F, 1, rb, th + L.off[P_W1], 1, F, rb, dYr(r), D, 1.f);
+    GemmArgs gy = gemm(N, D, F, dUr(r), F, 1, rb, th + L.off[P_W1] + wr, 1, F, rb, dYr(r), D, 1.f);
     gy.halfA = hf;
     ok = launch_gemm(gy, ws, m->gws_cap, s) && ok;
   }

@@ -188,8 +188,8 @@ __global__ __launch_bounds__(512) void k_ffn_head(FfnArgs a) {
   const int d0 = wr * (D / WR);  // first feature row of this wave in Y / GEMM2
   const int f0 = wr * (FC / WR); // first feature row of this wave within a chunk
   const int m0 = wc * CW;        // first window (column) of this wave
-  const uint4* __restrict__ W1p = a.W1;
-  const uint4* __restrict__ W2p = a.W2;
+  const uint4* W1p = a.W1;  // this repeat's W1, W2 (untied: advanced by wstride per repeat)
+  const uint4* W2p = a.W2;
 
   // Y^T: lane holds Y[m0 + nf*16 + lc][d0 + rf*16 + 4*lg + r]
   f32x4 y[RF2][NFC];
@@ -229,6 +229,10 @@ __global__ __launch_bounds__(512) void k_ffn_head(FfnArgs a) {
   for (int rf = 0; rf < RF1; ++rf) wa[0][rf] = W1p[(f0 / 16 + rf) * 64 + lane];
 
   for (int rep = 0; rep <= a.k; ++rep) {
+    if (rep > 0 && rep < a.k) {
+      W1p += a.wstride;
+      W2p += a.wstride;
+    }
 #pragma unroll
     for (int nf = 0; nf < NFC; ++nf) {
       const int m = m0 + nf * 16 + lc;
@@ -293,7 +297,8 @@ __global__ __launch_bounds__(512) void k_ffn_head(FfnArgs a) {
           for (int rf = 0; rf < RF2; ++rf) wb[(ks + 1) & 1][rf] = W2p[((kc0 + ks + 1) * NB2 + d0 / 16 + rf) * 64 + lane];
         } else {
 #pragma unroll
-          for (int rf = 0; rf < RF1; ++rf) wa[0][rf] = W1p[(nb1n + rf) * 64 + lane];
+          for (int rf = 0; rf < RF1; ++rf)
+            wa[0][rf] = (c0 + FC >= F && rep + 1 < a.k ? W1p + a.wstride : W1p)[(nb1n + rf) * 64 + lane];
         }
         uint4 bb[NFC];
 #pragma unroll
@@ -485,8 +490,8 @@ __global__ __launch_bounds__(512) void k_ffn_pipe(FfnArgs a) {
   const int d0 = wr * (D / P::WR);
   PipeLane L;
   L.f0 = __builtin_amdgcn_readfirstlane(wr * (FC / P::WR));
-  L.W1r = make_rsrc(a.W1, (int64_t)D * F * 2);
-  L.W2r = make_rsrc(a.W2, (int64_t)D * F * 2);
+  L.W1r = make_rsrc(a.W1, (int64_t)D * F * 2 * (a.wstride ? a.k : 1));
+  L.W2r = make_rsrc(a.W2, (int64_t)D * F * 2 * (a.wstride ? a.k : 1));
   L.w1o = (L.f0 / 16) * 1024;
   L.w2o = __builtin_amdgcn_readfirstlane(d0 / 16) * 1024;
   L.NB1 = F / 16;
@@ -557,7 +562,11 @@ __global__ __launch_bounds__(512) void k_ffn_pipe(FfnArgs a) {
     }
   };
 
+  const int w1o0 = L.w1o, w2o0 = L.w2o;  // repeat 0's fragment offsets
   for (int rep = 0; rep <= a.k; ++rep) {
+    // untied FFN: repeat rep's copies (wstride uint4 further per repeat)
+    L.w1o = w1o0 + (rep < a.k ? rep : 0) * (int)(a.wstride * 16);
+    L.w2o = w2o0 + (rep < a.k ? rep : 0) * (int)(a.wstride * 16);
 #pragma unroll
     for (int nf = 0; nf < NFC; ++nf) {
       const int m = m0 + nf * 16 + lc;

@@ -63,6 +63,10 @@ int trace_check_config(const trace_config* c, Layout* L) {
     trace_set_error("max_windows and max_keep must be non-negative");
     return TRACE_EINVAL;
   }
+  if (c->untied_ffn != 0 && c->untied_ffn != 1) {
+    trace_set_error("untied_ffn must be 0 or 1");
+    return TRACE_EINVAL;
+  }
   if (!(c->lr >= 0.0) || !(c->beta1 >= 0.0 && c->beta1 < 1.0) || !(c->beta2 >= 0.0 && c->beta2 < 1.0) ||
       !(c->eps > 0.0)) {
     trace_set_error("Adam settings out of range (lr >= 0, 0 <= beta < 1, eps > 0)");
@@ -73,7 +77,8 @@ int trace_check_config(const trace_config* c, Layout* L) {
     L->D = (int)d;
     L->DH = (int)(d / c->H);
     const int64_t T = L->T, D = d, e = c->e, F = c->F;
-    const int64_t sizes[NPARAM] = {256 * e, T * D, D * D, D * D, D * D, D * D, D * F, F * D, D * 256, 256};
+    const int64_t nr = c->untied_ffn ? c->k : 1;  // FFN weight blocks: one, or one per repeat
+    const int64_t sizes[NPARAM] = {256 * e, T * D, D * D, D * D, D * D, D * D, nr * D * F, nr * F * D, D * 256, 256};
     int64_t off = 0;
     for (int i = 0; i < NPARAM; ++i) {
       L->off[i] = off;

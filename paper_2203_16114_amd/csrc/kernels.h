@@ -37,6 +37,7 @@ struct FfnArgs {
   const uint4 *W1, *W2, *Wout;     // packed operand copies
   const float* bout;               // [256]
   int32_t F, k;
+  int64_t wstride;                 // uint4 between the packed W1 (W2) copies of two repeats; 0: shared
   float* bits;                     // [n0 + N] global window index
   float* logits;                   // nullable, [n0 + N][256]
   void* kY;                        // nullable, [k+1][N][D]: Y_0 .. Y_k as operand values (bf16 or fp32)

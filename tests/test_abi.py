@@ -95,3 +95,14 @@ def test_strerror_names_every_code():
     for code in (0, -1, -2, -3, -4, -5, -6):
         assert L.trace_strerror(code).decode() not in ("", "unknown error")
     assert L.trace_strerror(-99).decode() == "unknown error"
+
+
+@pytest.mark.parametrize("wid,seed", [(2, 3), (4, 77)])
+def test_untied_layout_and_initialiser_match_oracle(wid, seed):
+    w = WORKLOADS[wid]
+    cfg = P.make_config(w.W, w.e, w.g, w.H, w.F, w.k, w.dtype, untied_ffn=True)
+    ocf = O.Config(W=w.W, e=w.e, g=w.g, H=w.H, F=w.F, k=w.k, untied=True)
+    assert P.param_count(cfg) == O.param_count(ocf)
+    a = P.init_flat_host(cfg, seed, 0.02)
+    b = O.init_flat(ocf, seed, 0.02)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))

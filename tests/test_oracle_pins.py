@@ -363,3 +363,30 @@ def test_init_is_seeded_normal_with_zero_bias():
     assert abs(body.std() - 0.02) < 2e-4
     assert scipy.stats.kstest(body / 0.02, "norm").pvalue > 1e-3
     assert O.param_count(cfg) == 238848
+
+
+def test_untied_ffn_with_equal_copies_is_the_shared_ffn():
+    """Sec. 6.3's untied FFN with every repeat's W1, W2 equal to the shared
+    ones computes the shared FFN of Sec. 4.3; its per-repeat gradients sum to
+    the shared gradient."""
+    tied = O.Config(W=16, e=16, g=4, H=2, F=64, k=3)
+    unt = O.Config(W=16, e=16, g=4, H=2, F=64, k=3, untied=True)
+    ft = O.init_flat(tied, 5)
+    pt = O.unflatten(ft, tied)
+    pu = dict(pt)
+    pu["W1"] = np.stack([pt["W1"]] * 3)
+    pu["W2"] = np.stack([pt["W2"]] * 3)
+    fu = O.flatten(pu, unt, np.float64)
+    assert fu.size == O.param_count(tied) + 2 * 2 * 64 * 64      # two more copies of W1 and W2 (d = 64)
+    rng = np.random.default_rng(2)
+    streams = rng.integers(0, 256, (3, 40)).astype(np.uint8)
+    w, y = O.windows_at(streams, np.array([0, 1, 2, 0]), np.array([16, 20, 39, 30]), 16)
+    rt, gt = O.forward_backward(ft, tied, w, y)
+    ru, gu = O.forward_backward(fu, unt, w, y)
+    assert np.allclose(rt["bits"], ru["bits"], rtol=0, atol=1e-12)
+    assert np.allclose(gu["W1"].sum(0), gt["W1"], atol=1e-12) and np.allclose(gu["W2"].sum(0), gt["W2"], atol=1e-12)
+    assert np.allclose(gu["Wq"], gt["Wq"], atol=1e-12)
+    # different copies: the repeats are no longer interchangeable
+    pu["W1"][1] *= 1.5
+    r2 = O.forward(O.flatten(pu, unt, np.float64), unt, w, y)
+    assert np.max(np.abs(r2["bits"] - ru["bits"])) > 1e-7
