@@ -294,6 +294,37 @@ def measure_sweep():
     return {"lcr": rows, "batch": batch}
 
 
+def measure_deep_ffn(steps=3):
+    """The deep-FFN variant of Sec. 6.3 (untied W1, W2 per repeat) against the
+    shared FFN on the main workload's shape and streams: forward bytes/s of
+    4096 streams x 256 positions per step, both models in the same process."""
+    import torch
+    import paper_2203_16114_amd as P
+    import synth
+    w = synth.WORKLOADS[3]
+    S = 256
+    st, _ = synth.workload_streams(3, L=w.W + S * (steps + 1) + 1)
+    sd = torch.from_numpy(st).cuda()
+    B = st.shape[0]
+    res = {"workload": w.name, "streams": B, "positions_per_step": S}
+    for name, untied in (("shared", False), ("untied", True)):
+        m = P.TraceModel(w.W, w.e, w.g, w.H, w.F, w.k, dtype=w.dtype, max_windows=B * S, untied_ffn=untied)
+        m.init_weights(w.weight_seed)
+        bits = torch.empty(B * S, dtype=torch.float32, device="cuda")
+        m.forward_bits(sd, w.W, S, bits=bits)
+        torch.cuda.synchronize()
+        t0 = time.time()
+        for i in range(steps):
+            m.forward_bits(sd, w.W + S * (i + 1), S, bits=bits)
+        torch.cuda.synchronize()
+        res[name + "_bytes_per_s"] = B * S * steps / (time.time() - t0)
+        res[name + "_params"] = m.n_params
+        del m
+    res["untied_over_shared"] = round(res["untied_bytes_per_s"] / res["shared_bytes_per_s"], 4)
+    log(f"[bench] deep ffn {res}")
+    return res
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawDescriptionHelpFormatter)
     ap.add_argument("--gpus", type=int, default=1)
@@ -406,6 +437,7 @@ def main():
                               "large-mixed-bf16": measure_gated(5, max(16, args.gated_steps // 2))}
     if args.codec_steps > 0:
         out["codec"] = measure_codec(4, args.codec_steps)
+        out["deep_ffn"] = measure_deep_ffn()
     if args.cpu_windows > 0:
         out["cpu_baseline"] = cpu_baseline(streams, w, args.cpu_windows)
         log(f"[bench] cpu oracle: {out['cpu_baseline']['value']:.4g} bytes/s")
