@@ -1001,27 +1001,33 @@ extern "C" int trace_decompress(trace_model* m, const uint8_t* comp, int64_t com
   // columns [i0, i0 + n) of the host copy -> d_out: each column as one
   // contiguous copy and a scatter into the rows (strided copies of single
   // bytes are slow)
+  // (pinned, so the copy reads it directly; it is rewritten only after the
+  // next position's synchronisation, which follows this copy on the stream)
   uint8_t* d_col = nullptr;
-  std::vector<uint8_t> col(B);
+  uint8_t* col = nullptr;
   hipError_t e0 = hipMalloc(&d_col, (size_t)B);
-  if (e0 != hipSuccess) return hip_fail(e0, "trace_decompress");
-  auto put_cols = [&](int64_t i0, int64_t n) {
+  if (e0 == hipSuccess) e0 = hipHostMalloc((void**)&col, (size_t)B, hipHostMallocDefault);
+  if (e0 != hipSuccess) {
+    if (d_col) hipFree(d_col);
+    return hip_fail(e0, "trace_decompress");
+  }
+  auto put_cols = [&](int64_t i0, int64_t n, bool wait) {
     hipError_t e = hipSuccess;
     for (int64_t i = i0; i < i0 + n && e == hipSuccess; ++i) {
       for (int32_t b = 0; b < B; ++b) col[b] = h[(size_t)b * length + i];
-      e = hipMemcpyAsync(d_col, col.data(), (size_t)B, hipMemcpyHostToDevice, s);
+      e = hipMemcpyAsync(d_col, col, (size_t)B, hipMemcpyHostToDevice, s);
       if (e == hipSuccess) {
         launch_put_column(d_col, B, d_out, stride, i, s);
         e = hipGetLastError();
       }
-      if (e == hipSuccess) e = hipStreamSynchronize(s);
+      if (e == hipSuccess && (wait || i + 1 < i0 + n)) e = hipStreamSynchronize(s);
     }
     return e == hipSuccess ? TRACE_OK : hip_fail(e, "trace_decompress");
   };
   auto first = [&](int64_t n0) {
     for (int64_t i = 0; i < n0; ++i)
       for (int32_t b = 0; b < B; ++b) h[(size_t)b * length + i] = (uint8_t)dec[b].decode_uniform();
-    return n0 > 0 ? put_cols(0, n0) : TRACE_OK;
+    return n0 > 0 ? put_cols(0, n0, true) : TRACE_OK;
   };
   std::vector<double> cb(B);
   WorkPool pool(B);
@@ -1038,9 +1044,12 @@ extern "C" int trace_decompress(trace_model* m, const uint8_t* comp, int64_t com
       }
     });
     for (int32_t b = 0; b < B; ++b) *ce += cb[b];  // streams in order
-    return put_cols(i, 1);
+    return put_cols(i, 1, false);
   };
   rc = coding_loop(m, d_out, stride, B, length, mode, ctl_t, ctl_delta, n_updates, stream, first, code);
+  const hipError_t e1 = hipStreamSynchronize(s);  // the last column's copy reads col
   hipFree(d_col);
+  hipHostFree(col);
+  if (rc == TRACE_OK && e1 != hipSuccess) rc = hip_fail(e1, "trace_decompress");
   return rc;
 }
