@@ -481,14 +481,15 @@ class Controller:
 
 # ----------------------------------------------------- gated adaptation loop ----
 def run_gated(flat0, cfg, streams, pos0, n_steps, t, delta, mode="fp64",
-              forced_decisions=None):
+              forced_decisions=None, logits_out=None):
     """Alg. 1 with the controller of Alg. 2 over a batch of B streams: at each
     step every stream predicts its next byte (one window per stream), the
     batch-mean code length e goes to the controller, and if it says so one
     backward + Adam step runs on that same batch.  forced_decisions replays a
     given decision sequence (teacher forcing) instead of the controller's.
     Returns (bits [B][n_steps], step_ce [n_steps], decisions, own decisions,
-    final flat fp32 master)."""
+    final flat fp32 master); if logits_out is a list, each step's logits
+    [B][256] are appended to it."""
     B = streams.shape[0]
     theta = np.asarray(flat0, np.float32).copy()
     opt = Adam(theta.size, cfg)
@@ -502,6 +503,8 @@ def run_gated(flat0, cfg, streams, pos0, n_steps, t, delta, mode="fp64",
         out = forward(theta, cfg, w, y, mode=mode, keep=True)
         out["windows"] = w
         bits[:, s] = out["bits"]
+        if logits_out is not None:
+            logits_out.append(np.array(out["z"], copy=True))
         e = float(np.mean(np.asarray(out["bits"], np.float64)))
         step_ce[s] = e
         o = ctl.decide(e)

@@ -452,12 +452,19 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   const long tk = tbegin(m, s);
   bool ok = true;  // false if a product could not be launched
   // Two streams: s carries the chain of input gradients (dY, dU, dO, dQ/dK/dV,
-  // dX, dE) and never waits for the other until the end; `side` computes most
+  // dX, dE) and never waits for the other until the end; `side` computes the
   // weight gradients from the per-repeat buffers that chain leaves behind, each
   // as soon as its operands exist (a wait across streams costs several
   // microseconds, so only the side stream waits).  The side stream has its own
   // split-K and column-sum workspaces of the same sizes, so every product is the
   // same as on one stream.
+  // Buffers by writer -> readers (every cross-stream read follows a mark of the
+  // writer's stream, or, for the side stream's results, the final wait of s):
+  //   s: dz -> s, side; dY_r, dU_r -> s, side (one buffer per repeat); dO, dX,
+  //      grad P, grad E -> s; dQ, dK, dV -> s, side
+  //   side: Xk, sP, grad Wout, bout, W1, W2, Wo, Wq, Wk, Wv -> side only
+  //   kept activations (forward, on s) -> both; s waits for side before Adam,
+  //   so the next forward cannot overwrite them while side still reads
   const hipStream_t w = m->side;
   float* ws2 = m->gws2;
   auto dYr = [&](int r) { return m->dY + (int64_t)r * N * D; };  // w.r.t. the input of repeat r (r = k: Y_k)
@@ -533,6 +540,16 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
     launch_colsum(m->dV, N, (int64_t)T * D, (int64_t)T * D, m->sP, 0.f, m->cws2, w);
     launch_pos_grad(m->bf, m->Pc, m->sP, 0, T, D, gr + L.off[P_WV], w);
   }
+  // side: dWq = X_last^T dQ (+ its positional part); Xk was written on this
+  // stream, dQ before the last mark
+  GemmArgs gq = gemm(D, D, N, at(m->Xk, (int64_t)(T - 1) * D), 1, (int64_t)T * D, rb, m->dQ, D, 1, 0,
+                     gr + L.off[P_WQ], D, 0.f);
+  gq.halfA = hf;
+  ok = launch_gemm(gq, ws2, m->gws_cap, w) && ok;
+  if (m->cfg.use_pos) {
+    launch_colsum(m->dQ, N, D, D, m->sP + (int64_t)T * D, 0.f, m->cws2, w);
+    launch_pos_grad(m->bf, m->Pc, m->sP + (int64_t)T * D, T - 1, 1, D, gr + L.off[P_WQ], w);
+  }
   // dX = dK Wk^T + dV Wv^T (+ dQ Wq^T + dY_0 on the last token)
   launch_gemm2(gemm(N * T, D, D, m->dK, D, 1, 0, th + L.off[P_WK], 1, D, rb, m->dX, D, 0.f),
                gemm(N * T, D, D, m->dV, D, 1, 0, th + L.off[P_WV], 1, D, rb, m->dX, D, 0.f), ws, m->gws_cap, s);
@@ -546,15 +563,6 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   else
     launch_zero(gr + L.off[P_P], L.size[P_P], s);
   launch_embed_bwd(m->kwin, m->dX, N, m->cfg.W, m->cfg.e, gr + L.off[P_E], m->ews, s);
-  // dWq = X_last^T dQ (+ its positional part)
-  GemmArgs gq = gemm(D, D, N, at(m->Xk, (int64_t)(T - 1) * D), 1, (int64_t)T * D, rb, m->dQ, D, 1, 0,
-                     gr + L.off[P_WQ], D, 0.f);
-  gq.halfA = hf;
-  ok = launch_gemm(gq, ws, m->gws_cap, s) && ok;
-  if (m->cfg.use_pos) {
-    launch_colsum(m->dQ, N, D, D, m->sP + (int64_t)T * D, 0.f, m->cws, s);
-    launch_pos_grad(m->bf, m->Pc, m->sP + (int64_t)T * D, T - 1, 1, D, gr + L.off[P_WQ], s);
-  }
   order(m, w, s);  // every gradient is complete
   if (!ok) {
     tend(m, tk, TRACE_KIND_BACKWARD, s);
