@@ -145,6 +145,22 @@ int trace_adapt_step(trace_model* m, void* stream);
  * leaves a full cache and e enters it, whatever the decision.  Host only,
  * O(1), no GPU.  A non-finite e returns ENONFINITE with *update = 0 and leaves
  * the cache unchanged. */
+/* The forward of trace_forward_bits (same arguments, flags and results, bit
+ * for bit) for callers that cannot allocate device memory: code under HIP graph
+ * capture, serving loops, harnesses that forbid allocation.  Its only device
+ * workspace, the hand-off between the attention and FFN kernels
+ * (n_streams * n_steps * d floats), lives in one fixed 32 MiB array that the
+ * library holds on each device from its first trace_create there until the
+ * process ends; the call allocates nothing and records no timing events.
+ * The batch must fit that array in one launch: n_streams * n_steps * d * 4 <=
+ * 32 MiB (e.g. 32768 windows at d = 256), else EINVAL before any work.  Every
+ * call on a device shares the array, so calls that overlap on one device (two
+ * streams, two threads) race; calls queued on one stream do not.  The model's
+ * device must be current. */
+int trace_forward_bits_noalloc(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams,
+                               int64_t pos0, int32_t n_steps, float* d_bits, float* d_logits, double* d_step_ce,
+                               uint32_t flags, void* stream);
+
 typedef struct {
   int32_t t, count, head, pad_;
   double delta, sum;

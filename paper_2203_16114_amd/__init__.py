@@ -22,7 +22,7 @@ TRACE_FP32, TRACE_BF16 = 0, 1
 TRACE_KEEP_ACTS = 1
 
 EXPORTS = ("trace_create", "trace_destroy", "trace_param_count", "trace_init_weights", "trace_init_flat_host",
-           "trace_forward_bits", "trace_adapt_step", "trace_controller_init", "trace_controller_decide",
+           "trace_forward_bits", "trace_forward_bits_noalloc", "trace_adapt_step", "trace_controller_init", "trace_controller_decide",
            "trace_get_state", "trace_set_state", "trace_get_grads", "trace_quant_table", "trace_quantize",
            "trace_rc_encode", "trace_rc_decode", "trace_compress", "trace_decompress",
            "trace_debug_gemm", "trace_debug_gather",
@@ -74,6 +74,7 @@ def lib():
             "trace_init_weights": (c_int32, [P, c_uint64, c_double, P]),
             "trace_init_flat_host": (c_int32, [POINTER(TraceConfig), c_uint64, c_double, P, c_int64]),
             "trace_forward_bits": (c_int32, [P, P, c_int64, c_int32, c_int64, c_int32, P, P, P, c_uint32, P]),
+            "trace_forward_bits_noalloc": (c_int32, [P, P, c_int64, c_int32, c_int64, c_int32, P, P, P, c_uint32, P]),
             "trace_adapt_step": (c_int32, [P, P]),
             "trace_controller_init": (c_int32, [POINTER(TraceControllerState), c_int32, c_double]),
             "trace_controller_decide": (c_int32, [POINTER(TraceControllerState), c_double, POINTER(c_int32)]),
@@ -254,9 +255,11 @@ class TraceModel:
                                        None if flat is None else flat.ctypes.data))
 
     def forward_bits(self, streams, pos0: int, n_steps: int, bits=None, logits=None, step_ce=None,
-                     keep: bool = False, n_streams: int | None = None, stride: int | None = None, stream=None):
+                     keep: bool = False, n_streams: int | None = None, stride: int | None = None, stream=None,
+                     noalloc: bool = False):
         """streams: uint8 CUDA tensor [B][L] (row stride = L) or flat with n_streams/stride given.
-        bits/logits/step_ce: preallocated CUDA tensors, or True to allocate (logits, step_ce)."""
+        bits/logits/step_ce: preallocated CUDA tensors, or True to allocate (logits, step_ce).
+        noalloc: through trace_forward_bits_noalloc."""
         import torch
         if streams.dtype != torch.uint8 or not streams.is_cuda:
             raise TypeError("streams must be a uint8 CUDA tensor")
@@ -275,10 +278,11 @@ class TraceModel:
         for t, n in ((bits, N), (logits, N * 256), (step_ce, n_steps)):
             if t is not None and (not t.is_cuda or not t.is_contiguous() or t.numel() < n):
                 raise ValueError("output buffers must be contiguous CUDA tensors of the right size")
-        check(lib().trace_forward_bits(self._h, _dptr(streams), int(stride), int(n_streams), int(pos0), int(n_steps),
-                                       _dptr(bits), _dptr(logits) if logits is not None else None,
-                                       _dptr(step_ce) if step_ce is not None else None,
-                                       TRACE_KEEP_ACTS if keep else 0, _stream_ptr(stream)))
+        fn = lib().trace_forward_bits_noalloc if noalloc else lib().trace_forward_bits
+        check(fn(self._h, _dptr(streams), int(stride), int(n_streams), int(pos0), int(n_steps),
+                 _dptr(bits), _dptr(logits) if logits is not None else None,
+                 _dptr(step_ce) if step_ce is not None else None,
+                 TRACE_KEEP_ACTS if keep else 0, _stream_ptr(stream)))
         return {"bits": bits, "logits": logits, "step_ce": step_ce}
 
     def compress(self, streams, mode: int = MODE_NEVER, t: int = 16, delta: float = 0.05, length=None,

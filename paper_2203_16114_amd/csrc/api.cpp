@@ -311,6 +311,9 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
     delete m;
     return rc;
   }
+  // the fixed workspace of trace_forward_bits_noalloc on this device (if this
+  // fails, that entry point retries and reports the error; nothing else uses it)
+  (void)trace_scratch_setup(m->device);
   *out = m;
   return TRACE_OK;
 }
@@ -355,9 +358,12 @@ static int check_windows(const trace_model* m, const uint8_t* d_streams, int64_t
   return TRACE_OK;
 }
 
-extern "C" int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams,
-                                  int64_t pos0, int32_t n_steps, float* d_bits, float* d_logits, double* d_step_ce,
-                                  uint32_t flags, void* stream) {
+int trace_model_dim(const trace_model* m) { return m->L.D; }
+int trace_model_device(const trace_model* m) { return m->device; }
+
+int trace_forward_into(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams, int64_t pos0,
+                       int32_t n_steps, float* d_bits, float* d_logits, double* d_step_ce, uint32_t flags,
+                       void* stream, float* h0, int64_t chunk_cap, bool timed) {
   int rc = check_windows(m, d_streams, stride, n_streams, pos0, n_steps);
   if (rc) return rc;
   if (flags & ~(uint32_t)TRACE_KEEP_ACTS) return fail(TRACE_EINVAL, "unknown flag");
@@ -365,11 +371,14 @@ extern "C" int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int6
   const int64_t total = (int64_t)n_streams * n_steps;
   if (keep && (m->max_keep <= 0 || total > m->max_keep))
     return fail(TRACE_EINVAL, "KEEP_ACTS needs n_streams*n_steps <= max_keep");
+  if (keep && total > chunk_cap) return fail(TRACE_EINVAL, "KEEP_ACTS batch larger than the workspace");
   if (total == 0) return TRACE_OK;  // nothing to write: output pointers may be NULL
   if (!d_bits) return fail(TRACE_EINVAL, "bits is NULL");
   const hipStream_t s = S(stream);
   const Layout& L = m->L;
-  const int64_t chunk = keep ? total : m->max_windows;
+  const int64_t chunk = keep ? total : chunk_cap;
+  const bool was_timing = m->timing;
+  if (!timed) m->timing = false;
   for (int64_t n0 = 0; n0 < total; n0 += chunk) {
     WinArgs w;
     w.streams = d_streams;
@@ -390,12 +399,12 @@ extern "C" int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int6
     a.Wk = m->Wk;
     a.Wv = m->Wv;
     a.Wo = m->Wo;
-    a.h0 = m->h0;
+    a.h0 = h0;
     a.scale = (float)(1.0 / std::sqrt((double)L.DH));
     FfnArgs f;
     std::memset(&f, 0, sizeof(f));
     f.w = w;
-    f.h0 = m->h0;
+    f.h0 = h0;
     f.W1 = m->W1;
     f.W2 = m->W2;
     f.wstride = m->cfg.untied_ffn ? (int64_t)m->L.D * m->cfg.F * (m->bf ? 2 : 4) / 16 : 0;
@@ -430,6 +439,7 @@ extern "C" int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int6
     launch_step_ce(d_bits, n_streams, n_steps, d_step_ce, s);
     tend(m, tk, TRACE_KIND_STEP_CE, s);
   }
+  m->timing = was_timing;
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "trace_forward_bits");
   if (keep) {
@@ -437,6 +447,14 @@ extern "C" int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int6
     m->keepN = total;
   }
   return TRACE_OK;
+}
+
+extern "C" int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams,
+                                  int64_t pos0, int32_t n_steps, float* d_bits, float* d_logits, double* d_step_ce,
+                                  uint32_t flags, void* stream) {
+  if (!m) return fail(TRACE_EINVAL, "model is NULL");
+  return trace_forward_into(m, d_streams, stride, n_streams, pos0, n_steps, d_bits, d_logits, d_step_ce, flags,
+                            stream, m->h0, m->max_windows, true);
 }
 
 extern "C" int trace_adapt_step(trace_model* m, void* stream) {
