@@ -155,14 +155,18 @@ def init_flat(cfg: Config, seed: int, std: float = 0.02) -> np.ndarray:
 
 # --------------------------------------------------------------- rounding ----
 def bf16_round(x) -> np.ndarray:
-    """fp32 -> bfloat16 -> fp32 with round-to-nearest-even (NaN preserved)."""
+    """fp32 -> bfloat16 -> fp32 with round-to-nearest-even (NaN preserved).
+
+    Adds 0x7FFF plus the lowest kept bit, then clears the 16 low bits.  In
+    32-bit unsigned arithmetic only NaN patterns (0xFFFF7FFF and above) wrap;
+    NaNs are restored from the input afterwards."""
     x = np.ascontiguousarray(x, dtype=np.float32)
-    u = x.view(np.uint32).astype(np.uint64)
-    lsb = (u >> 16) & 1
-    r = ((u + 0x7FFF + lsb) >> 16) << 16
-    out = (r & 0xFFFFFFFF).astype(np.uint32).view(np.float32).copy()
+    u = x.view(np.uint32)
+    r = ((u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)) << np.uint32(16)
+    out = r.view(np.float32)
     nan = np.isnan(x)
-    out[nan] = x[nan]
+    if nan.any():
+        out[nan] = x[nan]
     return out
 
 
