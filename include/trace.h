@@ -45,7 +45,15 @@ enum {
 };
 
 enum { TRACE_FP32 = 0, TRACE_BF16 = 1 };  /* BF16: fp32 master + bf16 operand copies */
-enum { TRACE_KEEP_ACTS = 1u };
+/* Flags of trace_forward_bits.
+ *   TRACE_KEEP_ACTS   keep the batch's activations for trace_adapt_step
+ *   TRACE_TOKEN_ATTN  run every window through the per-token attention kernel,
+ *                     whose result for a window is the same bit for bit in
+ *                     every launch (any n_streams, n_steps, pos0, chunking):
+ *                     the step cross-entropies of a launch over many steps then
+ *                     equal those of one-step launches, which a loop that may
+ *                     update between steps needs for exact decisions */
+enum { TRACE_KEEP_ACTS = 1u, TRACE_TOKEN_ATTN = 2u };
 
 /* Model shape and optimiser settings.
  *   W        window bytes, the c*g bytes before the target (Sec. 4.2; Alg. 1 line 8)
@@ -121,12 +129,13 @@ int trace_init_flat_host(const trace_config* cfg, uint64_t seed, double std, flo
  * its FFN (Eq. 3) shared and applied k times (Sec. 4.3), and a 256-way softmax
  * head reading the last token.  flags may hold TRACE_KEEP_ACTS: the call then
  * also keeps the activations of these n_streams*n_steps <= max_keep windows
- * for trace_adapt_step.  For a given attention kernel, results depend only on
- * each window's bytes and the weights (not on n_streams, n_steps, chunking or
- * position in the batch).  bf16 launches whose 64-window tiles each lie in one
- * stream (n_steps and the first window a multiple of 64) share byte groups
- * between windows in a kernel whose sums are ordered differently: their
- * results agree with the other launches' within rounding, not bit for bit. */
+ * for trace_adapt_step; TRACE_TOKEN_ATTN as above.  For a given attention
+ * kernel, results depend only on each window's bytes and the weights (not on
+ * n_streams, n_steps, chunking or position in the batch).  bf16 launches whose
+ * 64-window tiles each lie in one stream (n_steps and the first window a
+ * multiple of 64), without TRACE_TOKEN_ATTN, share byte groups between windows
+ * in a kernel whose sums are ordered differently: their results agree with the
+ * other launches' within rounding, not bit for bit. */
 int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams,
                        int64_t pos0, int32_t n_steps, float* d_bits, float* d_logits,
                        double* d_step_ce, uint32_t flags, void* stream);
@@ -168,6 +177,27 @@ typedef struct {
 } trace_controller;
 int trace_controller_init(trace_controller* c, int32_t t, double delta); /* 1 <= t <= 256 */
 int trace_controller_decide(trace_controller* c, double batch_ce_bits, int32_t* update);
+
+/* Alg. 1 with the controller of Alg. 2 on the model's estimated code lengths,
+ * for n_streams streams over steps s < n_steps (target position pos0 + s, as
+ * in trace_forward_bits): each step forms the estimates of the n_streams
+ * windows and the step cross-entropy e_s (mean bits, fp64); then, by mode,
+ * 0: no update, 1: the controller of Alg. 2 (t = ctl_t, delta = ctl_delta, as
+ * trace_controller_decide) decides, 2: always; an update runs the backward and
+ * Adam step of trace_adapt_step on that step's batch before step s + 1.
+ * Forwards run ahead over up to max_spec steps at unchanged weights; the
+ * controller walks their cross-entropies and the first step it flags is run
+ * again keeping activations and updated, the walk resuming after it.  Every
+ * forward uses TRACE_TOKEN_ATTN, so the cross-entropies, decisions and final
+ * state are bit for bit those of a loop of one-step forwards (max_spec = 1).
+ * Outputs (host, each may be NULL): step_ce[n_steps] (bits), decisions[n_steps]
+ * (0/1), *n_updates.  Requires n_streams <= max_keep when mode != 0.  The
+ * model's weights and Adam state advance with the updates.  Allocates its
+ * buffers for the call (device: n_streams*max_spec floats and n_steps doubles;
+ * pinned host: n_steps doubles) and synchronises the stream before returning. */
+int trace_gated_run(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams, int64_t pos0,
+                    int32_t n_steps, int32_t mode, int32_t ctl_t, double ctl_delta, int32_t max_spec,
+                    double* step_ce, int32_t* decisions, int64_t* n_updates, void* stream);
 
 /* Copies of the training state (host arrays of trace_param_count floats each;
  * any pointer may be NULL to skip it).  get synchronises the device; set also

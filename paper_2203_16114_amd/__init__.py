@@ -19,10 +19,11 @@ LIB_PATH = os.path.join(_HERE, "libtrace.so")
 
 TRACE_OK, TRACE_EINVAL, TRACE_ENOMEM, TRACE_EHIP, TRACE_ESTATE, TRACE_ENONFINITE, TRACE_EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
 TRACE_FP32, TRACE_BF16 = 0, 1
-TRACE_KEEP_ACTS = 1
+TRACE_KEEP_ACTS, TRACE_TOKEN_ATTN = 1, 2
 
 EXPORTS = ("trace_create", "trace_destroy", "trace_param_count", "trace_init_weights", "trace_init_flat_host",
            "trace_forward_bits", "trace_forward_bits_noalloc", "trace_adapt_step", "trace_controller_init", "trace_controller_decide",
+           "trace_gated_run",
            "trace_get_state", "trace_set_state", "trace_get_grads", "trace_quant_table", "trace_quantize",
            "trace_rc_encode", "trace_rc_decode", "trace_compress", "trace_decompress",
            "trace_debug_gemm", "trace_debug_gather",
@@ -78,6 +79,8 @@ def lib():
             "trace_adapt_step": (c_int32, [P, P]),
             "trace_controller_init": (c_int32, [POINTER(TraceControllerState), c_int32, c_double]),
             "trace_controller_decide": (c_int32, [POINTER(TraceControllerState), c_double, POINTER(c_int32)]),
+            "trace_gated_run": (c_int32, [P, P, c_int64, c_int32, c_int64, c_int32, c_int32, c_int32, c_double,
+                                          c_int32, P, P, POINTER(c_int64), P]),
             "trace_get_state": (c_int32, [P, P, P, P, POINTER(c_int64), c_int64]),
             "trace_set_state": (c_int32, [P, P, P, P, c_int64, c_int64]),
             "trace_get_grads": (c_int32, [P, P, c_int64]),
@@ -256,10 +259,10 @@ class TraceModel:
 
     def forward_bits(self, streams, pos0: int, n_steps: int, bits=None, logits=None, step_ce=None,
                      keep: bool = False, n_streams: int | None = None, stride: int | None = None, stream=None,
-                     noalloc: bool = False):
+                     token_attn: bool = False, noalloc: bool = False):
         """streams: uint8 CUDA tensor [B][L] (row stride = L) or flat with n_streams/stride given.
         bits/logits/step_ce: preallocated CUDA tensors, or True to allocate (logits, step_ce).
-        noalloc: through trace_forward_bits_noalloc."""
+        token_attn: TRACE_TOKEN_ATTN; noalloc: through trace_forward_bits_noalloc."""
         import torch
         if streams.dtype != torch.uint8 or not streams.is_cuda:
             raise TypeError("streams must be a uint8 CUDA tensor")
@@ -282,7 +285,7 @@ class TraceModel:
         check(fn(self._h, _dptr(streams), int(stride), int(n_streams), int(pos0), int(n_steps),
                  _dptr(bits), _dptr(logits) if logits is not None else None,
                  _dptr(step_ce) if step_ce is not None else None,
-                 TRACE_KEEP_ACTS if keep else 0, _stream_ptr(stream)))
+                 (TRACE_KEEP_ACTS if keep else 0) | (TRACE_TOKEN_ATTN if token_attn else 0), _stream_ptr(stream)))
         return {"bits": bits, "logits": logits, "step_ce": step_ce}
 
     def compress(self, streams, mode: int = MODE_NEVER, t: int = 16, delta: float = 0.05, length=None,
@@ -321,6 +324,23 @@ class TraceModel:
                                      int(t), float(delta), _dptr(out), out.shape[1], byref(nupd),
                                      _stream_ptr(stream)))
         return out[:, :length], nupd.value
+
+    def gated_run(self, streams, pos0: int, n_steps: int, mode: int = MODE_GATED, t: int = 16,
+                  delta: float = 0.05, max_spec: int = 64, stream=None):
+        """Alg. 1 with the controller of Alg. 2 (trace_gated_run) over a
+        contiguous uint8 CUDA tensor [B][L]: (step_ce [n_steps] float64,
+        decisions [n_steps] int32, number of updates)."""
+        import torch
+        if streams.dtype != torch.uint8 or not streams.is_cuda or streams.dim() != 2 or not streams.is_contiguous():
+            raise TypeError("streams must be a contiguous uint8 CUDA tensor [B][L]")
+        B, L = streams.shape
+        ce = np.empty(max(n_steps, 1), np.float64)
+        dec = np.empty(max(n_steps, 1), np.int32)
+        nupd = c_int64()
+        check(lib().trace_gated_run(self._h, _dptr(streams), L, B, int(pos0), int(n_steps), int(mode), int(t),
+                                    float(delta), int(max_spec), ce.ctypes.data, dec.ctypes.data, byref(nupd),
+                                    _stream_ptr(stream)))
+        return ce[:n_steps], dec[:n_steps], nupd.value
 
     def adapt_step(self, stream=None):
         check(lib().trace_adapt_step(self._h, _stream_ptr(stream)))

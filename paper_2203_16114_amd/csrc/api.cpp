@@ -366,7 +366,7 @@ int trace_forward_into(trace_model* m, const uint8_t* d_streams, int64_t stride,
                        void* stream, float* h0, int64_t chunk_cap, bool timed) {
   int rc = check_windows(m, d_streams, stride, n_streams, pos0, n_steps);
   if (rc) return rc;
-  if (flags & ~(uint32_t)TRACE_KEEP_ACTS) return fail(TRACE_EINVAL, "unknown flag");
+  if (flags & ~(uint32_t)(TRACE_KEEP_ACTS | TRACE_TOKEN_ATTN)) return fail(TRACE_EINVAL, "unknown flag");
   const bool keep = (flags & TRACE_KEEP_ACTS) != 0;
   const int64_t total = (int64_t)n_streams * n_steps;
   if (keep && (m->max_keep <= 0 || total > m->max_keep))
@@ -400,6 +400,7 @@ int trace_forward_into(trace_model* m, const uint8_t* d_streams, int64_t stride,
     a.Wv = m->Wv;
     a.Wo = m->Wo;
     a.h0 = h0;
+    a.token_only = (flags & TRACE_TOKEN_ATTN) != 0;
     a.scale = (float)(1.0 / std::sqrt((double)L.DH));
     FfnArgs f;
     std::memset(&f, 0, sizeof(f));
@@ -948,6 +949,102 @@ double coded_bits(const uint16_t* f, int x, uint32_t* cum_out, uint32_t* tot_out
   return std::log2((double)tot) - std::log2((double)f[x]);
 }
 }  // namespace
+
+extern "C" int trace_gated_run(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams,
+                               int64_t pos0, int32_t n_steps, int32_t mode, int32_t ctl_t, double ctl_delta,
+                               int32_t max_spec, double* step_ce, int32_t* decisions, int64_t* n_updates,
+                               void* stream) {
+  if (!m) return fail(TRACE_EINVAL, "model is NULL");
+  if (mode < 0 || mode > 2) return fail(TRACE_EINVAL, "mode must be 0 (never), 1 (gated) or 2 (always)");
+  if (max_spec < 1) return fail(TRACE_EINVAL, "max_spec must be at least 1");
+  if (n_streams < 1) return fail(TRACE_EINVAL, "n_streams must be at least 1");
+  int rc = check_windows(m, d_streams, stride, n_streams, pos0, n_steps);
+  if (rc) return rc;
+  if (mode != 0 && n_streams > m->max_keep) return fail(TRACE_EINVAL, "n_streams above max_keep with updates on");
+  trace_controller ctl;
+  if (mode == 1 && (rc = trace_controller_init(&ctl, ctl_t, ctl_delta))) return rc;
+  if (n_updates) *n_updates = 0;
+  if (n_steps == 0) return TRACE_OK;
+  const hipStream_t s = S(stream);
+  const int32_t spec_max = std::min(max_spec, n_steps);
+  float* d_bits = nullptr;
+  double *d_ce = nullptr, *h_ce = nullptr;
+  hipError_t e = hipMalloc(&d_bits, (size_t)n_streams * spec_max * 4);
+  if (e == hipSuccess) e = hipMalloc(&d_ce, (size_t)n_steps * 8);
+  if (e == hipSuccess) e = hipHostMalloc((void**)&h_ce, (size_t)n_steps * 8, hipHostMallocDefault);
+  rc = e == hipSuccess ? TRACE_OK : fail(TRACE_ENOMEM, "trace_gated_run: buffers");
+  const uint32_t tok = TRACE_TOKEN_ATTN;
+  int64_t updates = 0;
+  int32_t i = 0, spec = 1;
+  while (rc == TRACE_OK && i < n_steps) {
+    if (mode == 2) {  // always: every step keeps its activations and is updated
+      rc = trace_forward_bits(m, d_streams, stride, n_streams, pos0 + i, 1, d_bits, nullptr, d_ce + i,
+                              TRACE_KEEP_ACTS | tok, stream);
+      if (!rc) rc = trace_adapt_step(m, stream);
+      if (decisions) decisions[i] = 1;
+      ++updates;
+      ++i;
+      continue;
+    }
+    const int32_t S_ = mode == 0 ? std::min(spec_max, n_steps - i) : std::min(spec, n_steps - i);
+    rc = trace_forward_bits(m, d_streams, stride, n_streams, pos0 + i, S_, d_bits, nullptr, d_ce + i, tok, stream);
+    if (rc) break;
+    if (mode == 0) {
+      for (int32_t q = 0; q < S_ && decisions; ++q) decisions[i + q] = 0;
+      i += S_;
+      continue;
+    }
+    // the controller walks the speculated steps; the weights do not change
+    // before the first step it flags, so these are the values it would see
+    // one step at a time
+    e = hipMemcpyAsync(h_ce + i, d_ce + i, (size_t)S_ * 8, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+      rc = hip_fail(e, "trace_gated_run: step cross-entropies");
+      break;
+    }
+    int32_t used = S_, upd = 0;
+    for (int32_t q = 0; q < S_; ++q) {
+      rc = trace_controller_decide(&ctl, h_ce[i + q], &upd);
+      if (rc) break;
+      if (decisions) decisions[i + q] = upd;
+      if (upd) {
+        used = q + 1;
+        break;
+      }
+    }
+    if (rc) break;
+    if (upd) {  // Alg. 1 line 10 on the flagged step's batch
+      rc = trace_forward_bits(m, d_streams, stride, n_streams, pos0 + i + used - 1, 1, d_bits, nullptr, nullptr,
+                              TRACE_KEEP_ACTS | tok, stream);
+      if (!rc) rc = trace_adapt_step(m, stream);
+      ++updates;
+      spec = 1;
+    } else {
+      spec = std::min(spec_max, 2 * spec);
+    }
+    i += used;
+  }
+  if (rc == TRACE_OK && step_ce) {
+    e = hipMemcpyAsync(h_ce, d_ce, (size_t)n_steps * 8, hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e == hipSuccess)
+      std::memcpy(step_ce, h_ce, (size_t)n_steps * 8);
+    else
+      rc = hip_fail(e, "trace_gated_run: step cross-entropies");
+  }
+  if (rc == TRACE_OK) {
+    e = hipStreamSynchronize(s);
+    if (e != hipSuccess) rc = hip_fail(e, "trace_gated_run");
+  } else {
+    (void)hipStreamSynchronize(s);
+  }
+  (void)hipFree(d_bits);
+  (void)hipFree(d_ce);
+  if (h_ce) (void)hipHostFree(h_ce);
+  if (n_updates) *n_updates = updates;
+  return rc;
+}
 
 extern "C" int trace_compress(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams,
                               int64_t length, int32_t mode, int32_t ctl_t, double ctl_delta, uint8_t* out,

@@ -672,12 +672,13 @@ static bool launch_grp(const AttnArgs& a, hipStream_t s) {
 
 // bf16 launches whose 64-window tiles each lie in one stream (steps per stream
 // and the launch's first window multiples of 64) share the byte groups
-// (k_attn_grp); launches too small to give every CU a workgroup at the widest
+// (k_attn_grp) unless the caller asks for the per-token kernel, whose result
+// for a window does not depend on the launch; launches too small to give every CU a workgroup at the widest
 // token tile (one step of the update path) take one 16-row fragment per wave.
 template <bool BF, int T, int D, int DH>
 static void run_attn(const AttnArgs& a, hipStream_t s) {
   if constexpr (BF) {
-    if (!a.kK && a.w.n_steps % 64 == 0 && a.w.n0 % 64 == 0) {
+    if (!a.kK && !a.token_only && a.w.n_steps % 64 == 0 && a.w.n0 % 64 == 0) {
       if (a.g == 8 && launch_grp<T, 8, D, DH>(a, s)) return;
       if (a.g == 4 && launch_grp<T, 4, D, DH>(a, s)) return;
     }

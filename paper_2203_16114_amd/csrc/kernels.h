@@ -22,6 +22,7 @@ struct AttnArgs {
   const uint4 *Wq, *Wk, *Wv, *Wo;  // packed operand copies
   float* h0;                       // [N][D]: Attn + X, the residual stream entering the FFN
   float scale;                     // 1/sqrt(head width)
+  int32_t token_only;              // 1: the per-token kernel whatever the launch shape
   // kept activations for the backward (all NULL unless kept), indexed by local window
   uint8_t* kwin;  // [N][W]
   float* kq;      // [N][D]     query of the last token

@@ -44,7 +44,7 @@ def test_noalloc_forward_equals_forward_on_two_calls(shape, dtype):
     st2 = synth.random_streams(42, 7, W + 40)
     a2, b2 = _both(m, to_dev(st2), W + 3, 33)
     _equal(a2, b2)
-    a3, b3 = _both(m, to_dev(st2), W + 1, 5, keep=False)
+    a3, b3 = _both(m, to_dev(st2), W + 1, 5, token_attn=True)
     _equal(a3, b3)
 
 
