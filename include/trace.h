@@ -284,12 +284,15 @@ int trace_decompress(trace_model* m, const uint8_t* comp, int64_t comp_stride, c
 int trace_debug_gemm(int M, int N, int K, const void* d_A, int a_kc, int mode_a, const void* d_B, int b_kc,
                      int mode_b, void* d_C, int half_c, int kernel, float* d_ws, int64_t ws_floats, void* stream);
 
-/* Byte-group gather alone (Sec. 4.2): writes the tokens X = E[byte] + P[t],
- * d_X[((b*n_steps + s)*T + t)*d + c] (device, fp32: the sum of the operand
- * copies of E and P, not rounded), for the windows defined as in
- * trace_forward_bits. */
-int trace_debug_gather(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams, int64_t pos0,
-                       int32_t n_steps, float* d_X, void* stream);
+/* Byte-group gather of the update step (Sec. 4.2; test support): for the batch
+ * kept by the last KEEP_ACTS forward (window bytes as the attention kernel kept
+ * them), writes the byte-embedding part of every token with the kernel
+ * trace_adapt_step uses, d_X[(n*T + t)*d + j*e + c] = E[byte j of group t of
+ * window n][c] (device; fp32 for TRACE_FP32 models, the bf16 bit patterns of
+ * the operand copy for TRACE_BF16 models; n = b*n_steps + s of that forward).
+ * The positional table is not added (the update adds its part separately).
+ * ESTATE if no batch is kept; the kept batch stays kept. */
+int trace_debug_kept_tokens(trace_model* m, void* d_X, void* stream);
 
 /* Per-kernel timing with HIP events recorded on the caller's stream around each
  * launch (measurement support; off by default).  While enabled, every kernel

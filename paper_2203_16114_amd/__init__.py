@@ -26,7 +26,7 @@ EXPORTS = ("trace_create", "trace_destroy", "trace_param_count", "trace_init_wei
            "trace_gated_run",
            "trace_get_state", "trace_set_state", "trace_get_grads", "trace_quant_table", "trace_quantize",
            "trace_rc_encode", "trace_rc_decode", "trace_compress", "trace_decompress",
-           "trace_debug_gemm", "trace_debug_gather",
+           "trace_debug_gemm", "trace_debug_kept_tokens",
            "trace_set_timing",
            "trace_read_timing", "trace_strerror", "trace_last_error")
 KINDS = ("attn", "ffn_head", "step_ce", "backward", "adam", "refresh")
@@ -94,7 +94,7 @@ def lib():
                                            c_int64, POINTER(c_int64), P]),
             "trace_debug_gemm": (c_int32, [c_int32, c_int32, c_int32, P, c_int32, c_int32, P, c_int32, c_int32, P,
                                            c_int32, c_int32, P, c_int64, P]),
-            "trace_debug_gather": (c_int32, [P, P, c_int64, c_int32, c_int64, c_int32, P, P]),
+            "trace_debug_kept_tokens": (c_int32, [P, P, P]),
             "trace_set_timing": (c_int32, [P, c_int32]),
             "trace_read_timing": (c_int32, [P, P, P, POINTER(c_int64)]),
             "trace_strerror": (ctypes.c_char_p, [c_int32]),
@@ -378,10 +378,12 @@ class TraceModel:
         out["overflow"] = ov.value
         return out
 
-    def debug_gather(self, streams, pos0: int, n_steps: int, stream=None):
+    def debug_kept_tokens(self, n_windows: int, stream=None):
+        """Byte-embedding part of the kept batch's tokens, from the update's
+        gather (trace_debug_kept_tokens): CUDA tensor [n_windows][T][d], fp32
+        or int16 holding bf16 bits."""
         import torch
-        B, L = streams.shape
-        X = torch.empty(B * n_steps, self.T, self.d, dtype=torch.float32, device=streams.device)
-        check(lib().trace_debug_gather(self._h, _dptr(streams), L, B, int(pos0), int(n_steps), _dptr(X),
-                                       _stream_ptr(stream)))
+        dt = torch.int16 if self.dtype == "bf16" else torch.float32
+        X = torch.empty(n_windows, self.T, self.d, dtype=dt, device="cuda")
+        check(lib().trace_debug_kept_tokens(self._h, _dptr(X), _stream_ptr(stream)))
         return X

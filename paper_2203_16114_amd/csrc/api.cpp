@@ -644,22 +644,14 @@ extern "C" int trace_get_grads(trace_model* m, float* host_out, int64_t n) {
   return TRACE_OK;
 }
 
-extern "C" int trace_debug_gather(trace_model* m, const uint8_t* d_streams, int64_t stride, int32_t n_streams,
-                                  int64_t pos0, int32_t n_steps, float* d_X, void* stream) {
-  int rc = check_windows(m, d_streams, stride, n_streams, pos0, n_steps);
-  if (rc) return rc;
-  if (!d_X) return fail(TRACE_EINVAL, "X is NULL");
-  WinArgs w;
-  w.streams = d_streams;
-  w.stride = stride;
-  w.pos0 = pos0;
-  w.n_steps = n_steps;
-  w.n0 = 0;
-  w.N = (int64_t)n_streams * n_steps;
-  if (w.N == 0) return TRACE_OK;
-  launch_gather(m->bf, w, m->Ec, m->Pc, m->L.T, m->L.D, m->cfg.e, m->cfg.g, d_X, S(stream));
+extern "C" int trace_debug_kept_tokens(trace_model* m, void* d_X, void* stream) {
+  if (!m || !d_X) return fail(TRACE_EINVAL, "model or X is NULL");
+  if (!m->kept) return fail(TRACE_ESTATE, "no batch kept: run trace_forward_bits with TRACE_KEEP_ACTS first");
+  // the update's own gather (trace_adapt_step), on the window bytes the
+  // attention kernel kept
+  launch_gather_kept(m->bf, m->kwin, m->keepN, m->Ec, m->L.T, m->L.D, m->cfg.e, m->cfg.g, d_X, S(stream));
   const hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return hip_fail(e, "trace_debug_gather");
+  if (e != hipSuccess) return hip_fail(e, "trace_debug_kept_tokens");
   return TRACE_OK;
 }
 

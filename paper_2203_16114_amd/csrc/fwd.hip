@@ -181,37 +181,6 @@ void launch_zero(void* p, int64_t n32, hipStream_t s) {
   if (n32 > 0) hipLaunchKernelGGL(k_zero, dim3((unsigned)((n32 + 255) / 256)), dim3(256), 0, s, (uint32_t*)p, n32);
 }
 
-// ------------------------------------------------------------ gather (debug) ----
-// Token operand values X[n][t][c] of Sec. 4.2: byte j of group t (oldest first)
-// fills columns [j*e, (j+1)*e) with E[byte]; P[t] is added in fp32, then the sum
-// is rounded to the operand type.
-template <bool BF>
-__global__ void k_gather(WinArgs w, const typename Mma<BF>::T* __restrict__ E, const typename Mma<BF>::T* __restrict__ P,
-                         int T, int D, int e, int g, float* __restrict__ X) {
-  typedef Mma<BF> M;
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t total = w.N * T * D;
-  if (i >= total) return;
-  const int c = (int)(i % D);
-  const int64_t r = i / D;
-  const int t = (int)(r % T);
-  const int64_t n = r / T;
-  const int j = c / e, cc = c - j * e;
-  const int W = T * g;
-  const int byte = w.streams[target_offset(w, n) - W + t * g + j];
-  X[i] = M::val(E[byte * e + cc]) + M::val(P[t * D + c]);
-}
-void launch_gather(bool bf, const WinArgs& w, const void* E, const void* P, int T, int D, int e, int g, float* X,
-                   hipStream_t s) {
-  const int64_t total = w.N * T * D;
-  const dim3 grid((unsigned)((total + 255) / 256));
-  if (bf)
-    hipLaunchKernelGGL(k_gather<true>, grid, dim3(256), 0, s, w, (const uint16_t*)E, (const uint16_t*)P, T, D, e, g,
-                       X);
-  else
-    hipLaunchKernelGGL(k_gather<false>, grid, dim3(256), 0, s, w, (const float*)E, (const float*)P, T, D, e, g, X);
-}
-
 // ------------------------------------------------------------- step means ----
 // step_ce[s] = (1/B) sum_b bits[b][s] in double, in a fixed order.
 __global__ __launch_bounds__(256) void k_step_ce(const float* __restrict__ bits, int32_t n_streams, int32_t n_steps,

@@ -75,8 +75,6 @@ struct RefreshJob {
 constexpr int REFRESH_MAX_JOBS = 12;
 // Runs jobs[0..n) on stream s; false (nothing launched) for an unsupported job.
 bool launch_refresh(bool bf, const RefreshJob* jobs, int n, hipStream_t s);
-void launch_gather(bool bf, const WinArgs& w, const void* E, const void* P, int T, int D, int e, int g, float* X,
-                   hipStream_t s);
 
 // ---- backward building blocks (bwd.hip) ----
 struct GemmArgs {

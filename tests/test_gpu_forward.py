@@ -10,7 +10,7 @@ import torch
 
 import oracle as O
 import synth
-from gpu_helpers import check_parity, make_model, ocfg, oracle_mode, to_dev, workload_cfg
+from gpu_helpers import check_parity, make_model, ocfg, oracle_mode, structured_flat, to_dev, workload_cfg
 
 pytestmark = pytest.mark.gpu
 
@@ -21,24 +21,67 @@ def _oracle_at(shape, flat, streams, b, i, mode, use_pos=True):
     return O.forward(flat, cfg, w, y, mode=mode)
 
 
-@pytest.mark.parametrize("dtype", ["fp32", "bf16"])
-@pytest.mark.parametrize("shape", [dict(W=16, e=16, g=4, H=1, F=256, k=2), dict(W=64, e=64, g=8, H=8, F=256, k=1),
-                                   dict(W=32, e=32, g=4, H=4, F=256, k=1)])
-def test_byte_group_gather_is_bit_exact(dtype, shape):
-    if dtype == "fp32" and shape["e"] * shape["g"] == 512:
-        pytest.skip("no fp32 kernel at d=512")
-    m = make_model(shape, dtype, seed=5)
-    streams = synth.random_streams(11, 7, 300)
-    n_steps = 300 - shape["W"] - 5
-    X = m.debug_gather(to_dev(streams), shape["W"], n_steps).cpu().numpy()
+# ------------------------------------------- byte-group indexing, bit-exact
+_INDEX_CASES = [(1, "fp32"), (2, "fp32"), (3, "bf16"), (4, "bf16"), (5, "bf16"), (4, "fp32")]
+
+
+@pytest.mark.parametrize("wid,dtype", _INDEX_CASES)
+def test_byte_group_indexing_is_bit_exact_in_the_forward_kernels(wid, dtype):
+    """The gathers inside the path's kernels: the per-token attention kernel at
+    both tile sizes (launch sizes below and above the chip-filling bound) and,
+    in bf16, the shared-group kernel (64-window tiles in one stream, g = 4 and
+    8) and the kept-activation variant.  Logits equal the index formula and the
+    oracle's bit for bit, for every window."""
+    shape, _ = workload_cfg(wid)
     cfg = ocfg(**shape)
-    flat = O.init_flat(cfg, 5)
+    W, T, H = cfg.W, cfg.T, cfg.H
+    streams = synth.random_streams(90 + wid, 512, W + 300)
+    s = to_dev(streams)
+    for r in range(-(-T // H)):
+        sel = [(r * H + h) % T for h in range(H)]
+        flat, expected = structured_flat(cfg, sel)
+        m = make_model(shape, dtype, seed=0, flat=flat, max_windows=1 << 17, max_keep=512)
+        launches = [dict(B=3, pos0=W + 11, n=5, kw={}),                       # small tiles
+                    dict(B=256, pos0=W + 1, n=256, kw={"token_attn": True}),  # wide tiles
+                    dict(B=512, pos0=W + 7, n=1, kw={"keep": True})]          # kept activations
+        if dtype == "bf16":
+            launches.append(dict(B=256, pos0=W + 3, n=256, kw={}))            # shared byte groups
+        for L in launches:
+            st = s[:L["B"]].contiguous()
+            out = m.forward_bits(st, L["pos0"], L["n"], logits=True, **L["kw"])
+            z = out["logits"].cpu().numpy()
+            bb, ii = np.meshgrid(np.arange(L["B"]), L["pos0"] + np.arange(L["n"]), indexing="ij")
+            win, y = O.windows_at(streams, bb.ravel(), ii.ravel(), W)
+            want = expected(win)
+            assert np.array_equal(z.view(np.uint32), want.view(np.uint32)), (L, np.argwhere(z != want)[:5])
+            pick = np.random.default_rng(r).choice(len(win), size=min(64, len(win)), replace=False)
+            ref = O.forward(flat, cfg, win[pick], y[pick], mode=oracle_mode(dtype))
+            assert np.array_equal(np.asarray(ref["z"], np.float32).view(np.uint32), want[pick].view(np.uint32))
+
+
+@pytest.mark.parametrize("wid,dtype", [(1, "fp32"), (2, "fp32"), (3, "bf16"), (4, "bf16"), (5, "bf16")])
+def test_update_gather_is_bit_exact(wid, dtype):
+    """The update's own gather (the kernel trace_adapt_step runs on the window
+    bytes the attention kernel kept) against the oracle's grouping of the
+    rounded embedding, bit for bit, over a kept batch with a ragged end."""
+    shape, _ = workload_cfg(wid)
+    B = 777
+    m = make_model(shape, dtype, seed=5, max_keep=B)
+    streams = synth.random_streams(11, B, 300)
+    pos = shape["W"] + 100
+    m.forward_bits(to_dev(streams), pos, 1, keep=True)
+    X = m.debug_kept_tokens(B).cpu().numpy()
+    cfg = ocfg(**shape, use_pos=False)
+    flat = O.init_flat(ocfg(**shape), 5)
     mode = "fp32" if dtype == "fp32" else "bf16"
-    p = O.compute_params(flat, cfg, mode)
-    w, _ = O.all_windows(streams, cfg.W, shape["W"], n_steps)
-    mo = O.trace_oracle._Mode(mode)
-    Xref = O.embed_group(p, w, cfg, mo)  # the fp32 token, E + P of the rounded copies
-    assert np.array_equal(X.reshape(Xref.shape).view(np.uint32), Xref.astype(np.float32).view(np.uint32))
+    p = O.compute_params(flat, ocfg(**shape), mode)
+    w, _ = O.windows_at(streams, np.arange(B), np.full(B, pos), cfg.W)
+    Xref = O.embed_group(p, w, cfg, O.trace_oracle._Mode(mode)).astype(np.float32)
+    if dtype == "bf16":
+        got = (X.astype(np.uint16).astype(np.uint32) << 16).view(np.float32)
+    else:
+        got = X
+    assert np.array_equal(got.reshape(Xref.shape).view(np.uint32), Xref.view(np.uint32))
 
 
 def test_workload1_every_window():

@@ -390,3 +390,28 @@ def test_untied_ffn_with_equal_copies_is_the_shared_ffn():
     pu["W1"][1] *= 1.5
     r2 = O.forward(O.flatten(pu, unt, np.float64), unt, w, y)
     assert np.max(np.abs(r2["bits"] - ru["bits"])) > 1e-7
+
+
+# ------------------------------------------ structured weights (index test)
+@pytest.mark.parametrize("shape", [dict(W=16, e=16, g=4, H=1, F=256, k=2), dict(W=32, e=32, g=4, H=4, F=512, k=2),
+                                   dict(W=64, e=32, g=8, H=8, F=1024, k=3), dict(W=64, e=64, g=8, H=8, F=2048, k=3)])
+def test_structured_weights_show_every_slot_exactly(shape):
+    """The weights of the GPU index test make the oracle's logits (fp64 and
+    bf16 emulation) equal, exactly, the byte-embedding values the index map of
+    Sec. 4.2 puts in each slot of the selected tokens; a window with two slots
+    of one token exchanged gives different logits."""
+    from gpu_helpers import structured_flat
+    cfg = O.Config(**shape)
+    w, y = synth.random_windows(61, 40, cfg.W)
+    for r in range(-(-cfg.T // cfg.H)):
+        sel = [(r * cfg.H + h) % cfg.T for h in range(cfg.H)]
+        flat, expected = structured_flat(cfg, sel)
+        want = expected(w)
+        for mode in ("fp64", "bf16"):
+            z = np.asarray(O.forward(flat, cfg, w, y, mode)["z"], np.float32)
+            assert np.array_equal(z.view(np.uint32), want.view(np.uint32)), mode
+        t = sel[0]
+        sw = w.copy()
+        sw[:, [t * cfg.g, t * cfg.g + 1]] = sw[:, [t * cfg.g + 1, t * cfg.g]]
+        diff = np.any(expected(sw) != want, axis=1)
+        assert np.array_equal(diff, w[:, t * cfg.g] != w[:, t * cfg.g + 1])
