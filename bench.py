@@ -9,12 +9,16 @@ accumulation): `--steps-per-call` consecutive positions of every stream, i.e.
 predicted bytes (= windows) per second over the timed steps, with the streams
 already in device memory.
 
-Besides the headline line this run measures the controller-gated update loop
-against the always-update loop on the adaptation workload (the small model in
-bf16 with fp32 master weights, B = 4096 windows per step, sources switching
-every 2 KiB per stream) and on the large mixed workload (d = 512, B = 8192),
-and times the CPU oracle on a bounded sample of the main workload's windows on
-this machine's cores.
+Besides the headline line this run measures:
+  - the forward of the tiny and small fp32 workloads and of the large bf16
+    workload (bytes/s and the fraction of the MFMA peak of their dtype);
+  - the controller-gated loop of Alg. 1 / Alg. 2 (trace_gated_run) against the
+    always-update loop on the adaptation workload (its whole 32 KiB streams,
+    16 source regimes) and on the large mixed workload (4096 steps), with the
+    configured margin (0.05 bits) and with Eq. 7's margin 0;
+  - the compressor / decompressor round trip, the deep-FFN variant;
+  - the CPU oracle on a bounded sample of the main workload's windows, on all
+    host cores and on one.
 
 Prints ONE JSON line (rank 0).  Only one GPU is supported.
 """
@@ -56,92 +60,129 @@ def mfma_flops_per_window(w):
     return {"attn": 12 * d * d, "ffn_head": flops_per_window(w)["ffn_head"]}
 
 
-def gated_loop(model, sdev, B, pos0, n_steps, t, delta, always, max_spec=64):
-    """Alg. 1 with the controller of Alg. 2 over B streams.  Forward passes run
-    speculatively over up to max_spec steps at unchanged weights; the controller
-    walks their step cross-entropies and at the first step it flags, that step
-    is re-run keeping its activations and updated; the walk resumes after it."""
-    import torch
-    import paper_2203_16114_amd as P
-    ctl = P.Controller(t, delta)
-    dev = sdev.device
-    bits = torch.empty(B * max_spec, dtype=torch.float32, device=dev)
-    ce = torch.empty(max_spec, dtype=torch.float64, device=dev)
-    kb = torch.empty(B, dtype=torch.float32, device=dev)
-    kce = torch.empty(1, dtype=torch.float64, device=dev)
-    i, updates, spec, ce_sum = 0, 0, 1, 0.0
-    ce_dev = []
-    while i < n_steps:
-        if always:
-            model.forward_bits(sdev, pos0 + i, 1, bits=kb, step_ce=kce, keep=True)
-            model.adapt_step()
-            ce_dev.append(kce.clone())
-            i += 1
-            updates += 1
-            continue
-        S = min(spec, n_steps - i)
-        model.forward_bits(sdev, pos0 + i, S, bits=bits, step_ce=ce)
-        ces = ce[:S].cpu().numpy()
-        j = None
-        for s in range(S):
-            if ctl.decide(float(ces[s])):
-                j = s
-                break
-        used = S if j is None else j + 1
-        ce_sum += float(ces[:used].sum())
-        if j is not None:
-            model.forward_bits(sdev, pos0 + i + j, 1, bits=kb, keep=True)
-            model.adapt_step()
-            updates += 1
-            spec = 1
-        else:
-            spec = min(max_spec, spec * 2)
-        i += used
-    if ce_dev:
-        ce_sum = float(torch.cat(ce_dev).sum())
-    return updates, ce_sum / n_steps
-
-
-def measure_gated(wid, n):
-    """Gated (controller) vs always-update loop over n steps of workload wid."""
+def measure_gated(wid, n, variants):
+    """The gated loop of Alg. 1 with the controller of Alg. 2 (trace_gated_run:
+    speculative forwards over up to 64 steps, exact by construction) over n
+    steps of workload wid, for each (name, mode, delta) in variants, each from
+    the workload's initial weights.  Per variant: bytes/s, updates (overall and
+    after the warm-up), bits/byte (mean step cross-entropy), per-kind kernel
+    times, Adam's bytes per launch against HBM; for the adaptation workload the
+    update fraction and bits/byte in each 2 KiB source regime."""
+    import numpy as np
     import torch
     import paper_2203_16114_amd as P
     import synth
+    from synth.workloads import REGIME_BYTES_PER_STREAM
     w = synth.WORKLOADS[wid]
     B = w.B
-    L = min(w.L, w.W + 1 + 2 * n + 2 * 64 + 64)
+    n = min(n, w.L - w.W)            # targets at positions W .. W + n - 1
+    L = w.W + n
     t0 = time.time()
     streams, _ = synth.workload_streams(wid, L=L)
     log(f"[bench] {w.name} streams {streams.shape} in {time.time() - t0:.1f}s")
     sdev = torch.from_numpy(streams).cuda()
-    res = {}
-    for name, always in (("gated", False), ("always_update", True)):
-        m = P.TraceModel(w.W, w.e, w.g, w.H, w.F, w.k, dtype=w.dtype, max_windows=B * 64, max_keep=B)
-        m.init_weights(w.weight_seed)
-        gated_loop(m, sdev, B, w.W, 8, w.t, w.delta, always)      # warm-up, then a fresh start
+    mk = lambda: P.TraceModel(w.W, w.e, w.g, w.H, w.F, w.k, dtype=w.dtype, max_windows=B * 64, max_keep=B)
+    warm = mk()                                  # first launches of every kernel, untimed
+    warm.init_weights(w.weight_seed)
+    warm.gated_run(sdev, w.W, 80, P.MODE_GATED, w.t, 0.0)
+    warm.close()
+    res = {"workload": f"{w.name}: B={B} windows/step, W={w.W} e={w.e} g={w.g} d={w.d} H={w.H} F={w.F} "
+                       f"k={w.k}, controller t={w.t}; targets at positions {w.W}..{w.W + n - 1} of every stream",
+           "steps": n}
+    for name, mode, delta in variants:
+        m = mk()
         m.init_weights(w.weight_seed)
         torch.cuda.synchronize()
         m.set_timing(True)
         t0 = time.perf_counter()
-        upd, bpb = gated_loop(m, sdev, B, w.W + 8, n, w.t, w.delta, always)
+        ce, dec, upd = m.gated_run(sdev, w.W, n, mode, w.t, 0.0 if delta is None else delta)
         torch.cuda.synchronize()
         dt = time.perf_counter() - t0
         tm = m.read_timing()
         m.set_timing(False)
-        res[name] = {"bytes_per_s": B * n / dt, "steps": n, "updates": upd, "update_fraction": upd / n,
-                     "bits_per_byte": bpb,
-                     "kernel_ms": {k: round(v[0], 3) for k, v in tm.items() if k != "overflow" and v[1]},
-                     "kernel_launches": {k: v[1] for k, v in tm.items() if k != "overflow" and v[1]}}
+        r = {"mode": {P.MODE_GATED: "gated", P.MODE_ALWAYS: "always", P.MODE_NEVER: "never"}[mode],
+             "delta_bits": delta, "bytes_per_s": B * n / dt, "seconds": round(dt, 3), "updates": upd,
+             "update_fraction": round(upd / n, 5),
+             "updates_after_warmup": int(dec[w.t:].sum()),
+             "update_fraction_after_warmup": round(float(dec[w.t:].mean()), 5),
+             "bits_per_byte": float(ce.mean()),
+             "kernel_ms": {k: round(v[0], 3) for k, v in tm.items() if k != "overflow" and v[1]},
+             "kernel_launches": {k: v[1] for k, v in tm.items() if k != "overflow" and v[1]}}
+        if tm.get("backward", (0, 0))[1]:
+            r["backward_ms_per_update"] = round(tm["backward"][0] / tm["backward"][1], 4)
         if tm.get("adam", (0, 0))[1]:
             ms = tm["adam"][0] / tm["adam"][1]
             # Adam moves 28 bytes per parameter: reads theta, g, m, v; writes theta, m, v
-            res[name]["adam"] = {"avg_launch_ms": round(ms, 5), "bytes_per_launch": 28 * m.n_params,
-                                 "hbm_frac": round((28.0 * m.n_params / (ms * 1e-3)) / (HBM_GBS * 1e9), 4)}
-        log(f"[bench] {w.name} {name}: {res[name]['bytes_per_s']:.4g} B/s, updates {upd}/{n}")
+            r["adam"] = {"avg_launch_ms": round(ms, 5), "bytes_per_launch": 28 * m.n_params,
+                         "hbm_frac": round((28.0 * m.n_params / (ms * 1e-3)) / (HBM_GBS * 1e9), 4)}
+        if wid == 4:
+            pos = w.W + np.arange(n)
+            reg = pos // REGIME_BYTES_PER_STREAM
+            r["per_regime"] = [{"regime": int(q), "steps": int((reg == q).sum()),
+                                "update_fraction": round(float(dec[reg == q].mean()), 4),
+                                "bits_per_byte": round(float(ce[reg == q].mean()), 5)}
+                               for q in np.unique(reg)]
+        res[name] = r
+        log(f"[bench] {w.name} {name}: {r['bytes_per_s']:.4g} B/s, updates {upd}/{n}, "
+            f"bits/byte {r['bits_per_byte']:.5f}")
         m.close()
-    res["speedup_gated_vs_always"] = res["gated"]["bytes_per_s"] / res["always_update"]["bytes_per_s"]
-    res["workload"] = f"{w.name}: B={B} windows/step, W={w.W} e={w.e} g={w.g} d={w.d} H={w.H} F={w.F} k={w.k}, " \
-                      f"t={w.t} delta={w.delta}"
+    if "always_update" in res:
+        base = res["always_update"]
+        for name in res:
+            if isinstance(res[name], dict) and name != "always_update" and "bytes_per_s" in res[name]:
+                res[name]["speedup_vs_always"] = round(res[name]["bytes_per_s"] / base["bytes_per_s"], 4)
+                res[name]["bits_per_byte_cost_vs_always"] = round(
+                    (res[name]["bits_per_byte"] - base["bits_per_byte"]) / base["bits_per_byte"], 6)
+    return res
+
+
+def measure_forward(wid, steps_per_call, calls):
+    """Forward estimator + code lengths on workload wid: `calls` launches of
+    B x steps_per_call windows walking along the streams (one untimed first),
+    timed with HIP events on the launch stream; per-kernel launch times and
+    the fraction of the MFMA peak of the workload's dtype."""
+    import torch
+    import paper_2203_16114_amd as P
+    import synth
+    w = synth.WORKLOADS[wid]
+    B, S = w.B, steps_per_call
+    L = min(w.L, w.W + (calls + 1) * S + 1)
+    streams, _ = synth.workload_streams(wid, L=L)
+    sdev = torch.from_numpy(streams).cuda()
+    m = P.TraceModel(w.W, w.e, w.g, w.H, w.F, w.k, dtype=w.dtype, max_windows=B * S)
+    m.init_weights(w.weight_seed)
+    bits = torch.empty(B * S, dtype=torch.float32, device="cuda")
+    ce = torch.empty(calls, S, dtype=torch.float64, device="cuda")
+    pos = [w.W + ((i + 1) * S) % max(L - w.W - S, 1) for i in range(calls)]
+    m.forward_bits(sdev, w.W, S, bits=bits)
+    torch.cuda.synchronize()
+    m.set_timing(True)
+    m.read_timing()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for i in range(calls):
+        m.forward_bits(sdev, pos[i], S, bits=bits, step_ce=ce[i])
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1)
+    tm = m.read_timing()
+    m.set_timing(False)
+    fpw = flops_per_window(w)
+    wpl = B * S
+    per = {k: tm[k][0] / max(tm[k][1], 1) for k in ("attn", "ffn_head")}
+    peak = PEAK_TFLOPS[w.dtype]
+    value = wpl * calls / (ms * 1e-3)
+    path = (fpw["attn"] + fpw["ffn_head"]) * value / 1e12
+    m.close()
+    res = {"workload": f"{w.name}: B={B} streams x {S} positions per launch (first {L} bytes of each), "
+                       f"W={w.W} e={w.e} g={w.g} d={w.d} H={w.H} F={w.F} k={w.k}, {w.dtype}",
+           "bytes_per_s": value, "launches": calls, "windows_per_launch": wpl, "ms_per_launch": round(ms / calls, 4),
+           "bits_per_byte": float(ce.mean()), "dtype": w.dtype, "peak_tflops": peak,
+           "kernels": {k: {"avg_launch_ms": round(per[k], 4),
+                           "tflops": round(fpw[k] * wpl / (per[k] * 1e-3) / 1e12, 2),
+                           "frac": round(fpw[k] * wpl / (per[k] * 1e-3) / 1e12 / peak, 4)} for k in per},
+           "path_tflops": round(path, 2), "path_frac": round(path / peak, 4)}
+    log(f"[bench] forward {w.name}: {value:.4g} B/s, path {path:.1f} TFLOP/s ({path / peak:.3f} of {peak})")
     return res
 
 
@@ -163,27 +204,45 @@ def traffic_for(kernel, windows_per_launch):
         return None
 
 
-def cpu_baseline(streams, w, n_windows):
+def cpu_baseline(streams, w, n_windows, n_windows_one_core):
+    """The oracle, as it stands, on seeded windows of the main workload: on all
+    of this machine's cores, then pinned to one core with one BLAS thread."""
     import numpy as np
     import oracle as O
     import synth
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         threads = max([x.get("num_threads", 1) for x in threadpool_info()] or [1])
     except Exception:
-        threads = None
+        threadpool_limits, threads = None, None
     cores = len(os.sched_getaffinity(0))
     cfg = O.Config(W=w.W, e=w.e, g=w.g, H=w.H, F=w.F, k=w.k)
     flat = O.init_flat(cfg, w.weight_seed)
     b, i = synth.sample_positions(0xBA5E, streams.shape[0], streams.shape[1], w.W, n_windows)
     win, y = O.windows_at(streams, b, i, w.W)
     mode = "bf16" if w.dtype == "bf16" else "fp64"
+    O.forward(flat, cfg, win[:64], y[:64], mode=mode)       # first-call costs, untimed
     t0 = time.perf_counter()
     O.forward(flat, cfg, win, y, mode=mode)
     dt = time.perf_counter() - t0
-    return {"value": n_windows / dt, "unit": "bytes/s", "cores": threads or cores, "kind": "oracle",
-            "sample": f"{n_windows} seeded windows of the {w.name} streams, oracle forward + code length in "
-                      f"{mode} mode (numpy, {threads} BLAS threads on {cores} host cores), {dt:.1f} s"}
+    out = {"value": n_windows / dt, "unit": "bytes/s", "cores": threads or cores, "kind": "oracle",
+           "sample": f"{n_windows} seeded windows of the {w.name} streams, oracle forward + code length in "
+                     f"{mode} mode (numpy, {threads} BLAS threads on {cores} host cores), {dt:.1f} s"}
+    if n_windows_one_core > 0 and threadpool_limits is not None:
+        keep = os.sched_getaffinity(0)
+        try:
+            os.sched_setaffinity(0, {min(keep)})
+            with threadpool_limits(1):
+                nw = n_windows_one_core
+                t0 = time.perf_counter()
+                O.forward(flat, cfg, win[:nw], y[:nw], mode=mode)
+                dt1 = time.perf_counter() - t0
+        finally:
+            os.sched_setaffinity(0, keep)
+        out["one_core"] = {"value": nw / dt1, "unit": "bytes/s", "cores": 1,
+                           "sample": f"the first {nw} of those windows, pinned to one core, one BLAS thread, "
+                                     f"{dt1:.1f} s"}
+    return out
 
 
 def measure_codec(wid, n):
@@ -332,8 +391,13 @@ def main():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--steps-per-call", type=int, default=256, help="positions per stream in one step")
     ap.add_argument("--full", action="store_true", help="generate the full 256 KiB streams")
-    ap.add_argument("--gated-steps", type=int, default=256, help="steps of each gated-adaptation run (0: skip)")
+    ap.add_argument("--adapt-steps", type=int, default=32736,
+                    help="steps of each gated run on the adaptation workload (default: its whole streams; 0: skip)")
+    ap.add_argument("--large-steps", type=int, default=4096,
+                    help="steps of each gated run on the large mixed workload (0: skip)")
+    ap.add_argument("--fwd-legs", type=int, default=1, help="forward legs of workloads 1, 2 and 5 (0: skip)")
     ap.add_argument("--cpu-windows", type=int, default=16384, help="oracle sample (0: skip)")
+    ap.add_argument("--cpu-windows-one-core", type=int, default=1024, help="oracle sample on one core (0: skip)")
     ap.add_argument("--codec-steps", type=int, default=64, help="positions of the compress / decompress run (0: skip)")
     ap.add_argument("--sweep", action="store_true", help="only the LCR and batch-size sweeps (one JSON line)")
     ap.add_argument("--copy-probe-mib", type=int, default=0,
@@ -427,19 +491,28 @@ def main():
            "value": value, "unit": "bytes/s", "n_gpus": 1, "steps": K, "warmup": args.warmup,
            "ms_per_step": ms / K, "higher_is_better": True, "scaling": "weak", "vs_baseline": None,
            "dtype": "bf16", "data": "synthetic",
-           "config": {"workload": f"{w.name}: B={B} streams x {w.L} bytes (order-3 Markov Dirichlet(0.02) / "
-                                  f"Zipf(1.2) / uniform thirds), W={w.W} e={w.e} g={w.g} -> T={w.T} d={w.d}, "
-                                  f"H={w.H}, F={w.F} shared x{w.k}, bf16 operands fp32 accumulate",
+           "config": {"workload": f"{w.name}: B={B} streams (order-3 Markov Dirichlet(0.02) / Zipf(1.2) / "
+                                  f"uniform thirds), the first {L} bytes of each {w.L}-byte stream generated, "
+                                  f"{K} timed launches of {S} consecutive positions per stream; W={w.W} e={w.e} "
+                                  f"g={w.g} -> T={w.T} d={w.d}, H={w.H}, F={w.F} shared x{w.k}, bf16 operands "
+                                  f"fp32 accumulate",
                       "windows_per_step": B * S, "steps_per_call": S, "stream_prefix_bytes": L},
            "bits_per_byte": bpb, "mfma_util": roofline["path_mfma_frac"], "roofline": roofline}
-    if args.gated_steps > 0:
-        out["gated_adapt"] = {"adapt-bf16": measure_gated(4, args.gated_steps),
-                              "large-mixed-bf16": measure_gated(5, max(16, args.gated_steps // 2))}
+    if args.fwd_legs:
+        out["forward_legs"] = {"tiny-fp32": measure_forward(1, 4080, 5), "small-fp32": measure_forward(2, 256, 8),
+                               "large-mixed-bf16": measure_forward(5, 64, 8)}
+    variants = [("gated", P.MODE_GATED, 0.05), ("gated_eq7", P.MODE_GATED, 0.0),
+                ("always_update", P.MODE_ALWAYS, None)]
+    out["gated_adapt"] = {}
+    if args.adapt_steps > 0:
+        out["gated_adapt"]["adapt-bf16"] = measure_gated(4, args.adapt_steps, variants)
+    if args.large_steps > 0:
+        out["gated_adapt"]["large-mixed-bf16"] = measure_gated(5, args.large_steps, variants)
     if args.codec_steps > 0:
         out["codec"] = measure_codec(4, args.codec_steps)
         out["deep_ffn"] = measure_deep_ffn()
     if args.cpu_windows > 0:
-        out["cpu_baseline"] = cpu_baseline(streams, w, args.cpu_windows)
+        out["cpu_baseline"] = cpu_baseline(streams, w, args.cpu_windows, args.cpu_windows_one_core)
         log(f"[bench] cpu oracle: {out['cpu_baseline']['value']:.4g} bytes/s")
     print(json.dumps(out), flush=True)
 

@@ -301,8 +301,9 @@ int trace_debug_kept_tokens(trace_model* m, void* d_X, void* stream);
  * end, without the gap an event pair around one short launch adds; the other
  * kinds span all their kernels' launches); trace_read_timing waits
  * for them, returns per-kind totals (milliseconds) and launch counts in arrays
- * of TRACE_NKINDS entries, and starts a new measurement.  At most 65536 launches
- * are recorded between reads; later ones are counted in overflow. */
+ * of TRACE_NKINDS entries, and starts a new measurement.  Every 65536 regions
+ * the recorded ones are folded into the totals, which waits for the GPU (only
+ * while timing is on); overflow counts regions lost to a failed event read. */
 enum {
   TRACE_KIND_ATTN = 0,      /* fused gather + attention block                 */
   TRACE_KIND_FFN_HEAD = 1,  /* fused shared FFN x k + softmax head            */

@@ -57,6 +57,8 @@ struct trace_model {
   size_t ev_used;
   std::vector<int> ev_kind;  // kind of the launch bracketed by events 2i, 2i+1
   int64_t overflow;
+  double t_ms[TRACE_NKINDS];  // regions already folded in (see harvest)
+  int64_t t_n[TRACE_NKINDS];
 };
 
 namespace {
@@ -126,10 +128,34 @@ hipStream_t S(void* s) { return (hipStream_t)s; }
 
 constexpr size_t MAX_TIMED = 65536;
 
-// Reserves a timed region (two events); returns its index or -1.
+// Folds every recorded region into the per-kind totals (waiting for each
+// region's end) and frees the events for reuse; false if a HIP call failed.
+bool harvest(trace_model* m) {
+  bool ok = true;
+  for (size_t i = 0; i < m->ev_kind.size(); ++i) {
+    const int kind = m->ev_kind[i];
+    if (kind < 0) continue;
+    hipError_t e = hipEventSynchronize(m->events[2 * i + 1]);
+    float ms = 0.f;
+    if (e == hipSuccess) e = hipEventElapsedTime(&ms, m->events[2 * i], m->events[2 * i + 1]);
+    if (e != hipSuccess) {
+      ok = false;
+      continue;
+    }
+    m->t_ms[kind] += ms;
+    m->t_n[kind] += 1;
+  }
+  m->ev_kind.clear();
+  m->ev_used = 0;
+  return ok;
+}
+
+// Reserves a timed region (two events); returns its index or -1.  When all
+// MAX_TIMED regions are in use, the recorded ones are folded into the totals
+// first (a wait for the GPU; only while timing is on).
 long treserve(trace_model* m) {
   if (!m->timing) return -1;
-  if (m->ev_kind.size() >= MAX_TIMED) {
+  if (m->ev_kind.size() >= MAX_TIMED && !harvest(m)) {
     m->overflow += 1;
     return -1;
   }
@@ -688,23 +714,14 @@ extern "C" int trace_read_timing(trace_model* m, double* ms_total, int64_t* laun
     ms_total[k] = 0.0;
     launches[k] = 0;
   }
-  int rc = TRACE_OK;
-  for (size_t i = 0; i < m->ev_kind.size(); ++i) {
-    const int kind = m->ev_kind[i];
-    if (kind < 0) continue;
-    hipError_t e = hipEventSynchronize(m->events[2 * i + 1]);
-    float ms = 0.f;
-    if (e == hipSuccess) e = hipEventElapsedTime(&ms, m->events[2 * i], m->events[2 * i + 1]);
-    if (e != hipSuccess) {
-      rc = hip_fail(e, "trace_read_timing");
-      break;
-    }
-    ms_total[kind] += ms;
-    launches[kind] += 1;
+  const int rc = harvest(m) ? TRACE_OK : fail(TRACE_EHIP, "trace_read_timing: an event could not be read");
+  for (int k = 0; k < TRACE_NKINDS; ++k) {
+    ms_total[k] = m->t_ms[k];
+    launches[k] = m->t_n[k];
+    m->t_ms[k] = 0.0;
+    m->t_n[k] = 0;
   }
   if (overflow) *overflow = m->overflow;
-  m->ev_kind.clear();
-  m->ev_used = 0;
   m->overflow = 0;
   return rc;
 }
