@@ -285,48 +285,53 @@ def measure_codec(wid, n):
 def measure_sweep():
     """Synthetic analogues of the paper's Eq. 5 study (Fig. 3) and of its
     batch-size table: (1) for attention width d in {128, 256} and FFN width F in
-    {512, ..., 4096} (W=32, g=4, T=8, k=2, bf16), the model adapts on the small
-    workload's stream mix (order-2 Markov and Zipf bytes), 512 streams (the
-    paper's batch), with an update every step for 4096 steps; then its
-    compression ratio CR = 8 / (bits per byte of the next 64 positions, no
-    update) and its latency t (one forward step over the 512 windows) give
-    LCR = (t - t0) / (CR - CR0) against (d, F) = (128, 512); (2) forward
-    throughput and the model's device memory of the main workload's model at
-    128 to 8192 streams of 256 positions."""
+    {512, ..., 4096} (W=32, g=4, T=8, k=2, bf16), the model adapts, updating at
+    every step, on 512 streams (the paper's batch) drawn from ONE order-1 Markov
+    source with Dirichlet(0.1) rows (context every stream shares, which a shared
+    model can learn); after 1024 and after 4096 updates its compression ratio
+    CR = 8 / (bits per byte of the next 64 positions, no update) and its latency
+    t (one forward step over the 512 windows) give LCR = (t - t0) / (CR - CR0)
+    against (d, F) = (128, 512); (2) forward throughput and the model's device
+    memory of the main workload's model at 128 to 8192 streams of 256 positions."""
     import numpy as np
     import torch
     import paper_2203_16114_amd as P
     import synth
-    B, S_ad, S_ev = 512, 4096, 64
-    streams, _ = synth.workload_streams(2, L=32 + S_ad + S_ev + 1, B=B)
-    assert streams.shape[0] == B
+    B, S_ev = 512, 64
+    checkpoints = (1024, 4096)
+    S_ad = checkpoints[-1]
+    streams, codelen = synth.shared_markov_streams(B, 32 + S_ad + S_ev + 1, 1, 0.1, 0x7ACE5EED)
+    ideal = float(codelen.sum() / streams.size)
     sdev = torch.from_numpy(streams).cuda()
     rows = []
     for d in (128, 256):
         for F in (512, 1024, 2048, 4096):
             m = P.TraceModel(32, d // 4, 4, d // 32, F, 2, dtype="bf16", max_windows=B * S_ev, max_keep=B)
             m.init_weights(7)
-            for i in range(S_ad):
-                m.forward_bits(sdev, 32 + i, 1, keep=True)
-                m.adapt_step()
-            ce = torch.empty(S_ev, dtype=torch.float64, device="cuda")
-            bits = torch.empty(B * S_ev, dtype=torch.float32, device="cuda")
-            m.forward_bits(sdev, 32 + S_ad, S_ev, bits=bits, step_ce=ce)       # warm
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            m.forward_bits(sdev, 32 + S_ad, S_ev, bits=bits, step_ce=ce)
-            e1.record()
-            torch.cuda.synchronize()
-            bpb = float(ce.mean())
-            rows.append({"d": d, "F": F, "bits_per_byte": round(bpb, 4), "cr": round(8.0 / bpb, 4),
-                         "ms_per_step": round(e0.elapsed_time(e1) / S_ev, 4)})
+            done = 0
+            for cp in checkpoints:
+                m.gated_run(sdev, 32 + done, cp - done, P.MODE_ALWAYS)
+                done = cp
+                ce = torch.empty(S_ev, dtype=torch.float64, device="cuda")
+                bits = torch.empty(B * S_ev, dtype=torch.float32, device="cuda")
+                m.forward_bits(sdev, 32 + done, S_ev, bits=bits, step_ce=ce)       # warm
+                torch.cuda.synchronize()
+                e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                e0.record()
+                m.forward_bits(sdev, 32 + done, S_ev, bits=bits, step_ce=ce)
+                e1.record()
+                torch.cuda.synchronize()
+                bpb = float(ce.mean())
+                rows.append({"d": d, "F": F, "updates": cp, "bits_per_byte": round(bpb, 4),
+                             "cr": round(8.0 / bpb, 4), "ms_per_step": round(e0.elapsed_time(e1) / S_ev, 4)})
+                log(f"[bench] sweep {rows[-1]}")
             del m
-            log(f"[bench] sweep {rows[-1]}")
-    r0 = rows[0]
-    for r in rows[1:]:
-        dcr = r["cr"] - r0["cr"]
-        r["lcr_ms"] = round((r["ms_per_step"] - r0["ms_per_step"]) / dcr, 4) if abs(dcr) > 1e-6 else None
+    for cp in checkpoints:
+        sel = [r for r in rows if r["updates"] == cp]
+        r0 = sel[0]
+        for r in sel[1:]:
+            dcr = r["cr"] - r0["cr"]
+            r["lcr_ms"] = round((r["ms_per_step"] - r0["ms_per_step"]) / dcr, 4) if abs(dcr) > 1e-6 else None
     w = synth.WORKLOADS[3]
     st, _ = synth.workload_streams(3, L=w.W + 256 * 4 + 1)
     st = np.concatenate([st, st[::-1]])[:8192]       # the workload holds 4096 streams
@@ -350,7 +355,8 @@ def measure_sweep():
                       "device_mib": round(held / 2**20, 1)})
         del m, out, sd
         log(f"[bench] batch {batch[-1]}")
-    return {"lcr": rows, "batch": batch}
+    return {"lcr": rows, "lcr_source": "512 streams of one order-1 Markov source, Dirichlet(0.1) rows",
+            "lcr_source_bits_per_byte": round(ideal, 4), "batch": batch}
 
 
 def measure_deep_ffn(steps=3):

@@ -138,4 +138,31 @@ def sample_positions(seed: int, B: int, L: int, W: int, n: int):
     return r.integers(0, B, size=n), r.integers(W, L, size=n)
 
 
+def shared_markov_streams(B: int, L: int, order: int, alpha: float, seed: int):
+    """B streams drawn from ONE order-k Markov source with Dirichlet(alpha)
+    rows (a context every stream shares, so a shared model can learn it):
+    (uint8 [B][L], source code length [B] bits)."""
+    src = [(SRC_MARKOV, order, markov_table(order, alpha, splitmix64(seed ^ 0xABCDEF)))]
+    seeds = np.array([splitmix64(seed ^ (b + 1)) for b in range(B)], np.uint64)
+    return generate(src, np.zeros((B, 1), np.int32), L, L, seeds)
+
+
+def performer_features(seed: int, m: int, dh: int, orthogonal: bool = True) -> np.ndarray:
+    """The random projection of a Performer's positive random features: m
+    vectors omega_i in R^dh, i.i.d. N(0, I) or, when orthogonal, rows of
+    Gram-Schmidt-orthogonalised Gaussian blocks of dh rows rescaled by the
+    norms of independent N(0, I) vectors (orthogonal random features).
+    float32 [m][dh]; numpy PCG64 seeded with `seed`."""
+    r = np.random.default_rng(seed)
+    if not orthogonal:
+        return r.standard_normal((m, dh)).astype(np.float32)
+    blocks = []
+    for _ in range(-(-m // dh)):
+        q, _ = np.linalg.qr(r.standard_normal((dh, dh)))
+        blocks.append(q.T)
+    w = np.concatenate(blocks)[:m]
+    norms = np.linalg.norm(r.standard_normal((m, dh)), axis=1)
+    return (w * norms[:, None]).astype(np.float32)
+
+
 from .workloads import workload_streams  # noqa: E402,F401
