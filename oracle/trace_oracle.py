@@ -64,6 +64,11 @@ class Config:
     # False: the k repeats share W1, W2 (Sec. 4.3); True: one W1, W2 per repeat
     # (the deep-FFN variant of Sec. 6.3), stored as k consecutive blocks
     untied: bool = False
+    # "softmax": Eqs. 1-2; "performer": the FAVOR+ attention of the Performer
+    # the paper's experiments use as backbone (Sec. 6), with n_features random
+    # features (the projection matrix is an input of forward)
+    attention: str = "softmax"
+    n_features: int = 0
 
     @property
     def T(self) -> int:  # tokens per window (Sec. 4.2: c groups)
@@ -76,6 +81,10 @@ class Config:
     @property
     def dh(self) -> int:  # per-head width
         return self.d // self.H
+
+    @property
+    def m(self) -> int:  # Performer random features (reading: about dh ln dh, a multiple of 64)
+        return self.n_features or (128 if self.dh <= 32 else 256)
 
 
 def param_layout(cfg: Config):
@@ -269,12 +278,36 @@ def embed_group(p: dict, windows: np.ndarray, cfg: Config, m: _Mode):
     return X
 
 
+def performer_attention_weights(Qh, Kh, omega, dt):
+    """Causal FAVOR+ attention weights (Performer, Choromanski et al. 2021) for
+    one head: the softmax kernel exp(q.k / sqrt(dh)) of Eq. 1 is replaced by
+    phi(q')^T phi(k') with positive random features phi(x) = m^-1/2 exp(omega x
+    - |x|^2/2) of the scaled q' = q dh^-1/4, k' = k dh^-1/4 (so q'.k' =
+    q.k/sqrt(dh)), omega [m][dh].  Row t of A is phi(q'_t)^T phi(k'_u)
+    normalised over u <= t.  phi is taken relative to a constant per query
+    row (max over features) and per window for the keys (max over keys and
+    features), constants that cancel in the normalisation.
+    Qh, Kh [N][T][dh] -> A [N][T][T]."""
+    N, T, dh = Qh.shape
+    s4 = dt(dh ** -0.25)
+    qs, ks = Qh * s4, Kh * s4
+    pq = qs @ omega.T - dt(0.5) * np.sum(qs * qs, axis=-1, keepdims=True)      # [N][T][m]
+    pk = ks @ omega.T - dt(0.5) * np.sum(ks * ks, axis=-1, keepdims=True)
+    fq = np.exp(pq - np.max(pq, axis=-1, keepdims=True))
+    fk = np.exp(pk - np.max(pk, axis=(1, 2), keepdims=True))
+    kern = np.einsum("ntm,num->ntu", fq, fk)
+    kern = np.where(np.tril(np.ones((T, T), bool))[None], kern, dt(0))
+    return (kern / np.sum(kern, axis=-1, keepdims=True)).astype(dt)
+
+
 def forward(flat: np.ndarray, cfg: Config, windows: np.ndarray, targets: np.ndarray,
-            mode: str = "fp64", keep: bool = False):
+            mode: str = "fp64", keep: bool = False, features=None):
     """Model.forward of Alg. 1 line 8, the layer of Eqs. 1-4 with the shared FFN
     of Sec. 4.3, computed over ALL T rows with a causal mask (the head reads
     only the last).  Returns dict with logits z [N][256], bits [N]
-    (= -log2 p(target)), and, if keep, every intermediate."""
+    (= -log2 p(target)), and, if keep, every intermediate.  With
+    cfg.attention == "performer", `features` is the random projection omega
+    [m][dh] (one for all heads; rounded like a weight copy in bf16 mode)."""
     m = _Mode(mode)
     p = compute_params(flat, cfg, mode)
     windows = np.asarray(windows, np.uint8)
@@ -290,11 +323,20 @@ def forward(flat: np.ndarray, cfg: Config, windows: np.ndarray, targets: np.ndar
     causal = np.tril(np.ones((T, T), bool))
     A = np.zeros((N, H, T, T), m.dt)
     O = np.zeros((N, T, d), m.dt)
+    if cfg.attention == "performer":
+        if features is None or np.shape(features) != (cfg.m, dh):
+            raise ValueError("performer attention needs features of shape [m][dh]")
+        om = m.R(np.asarray(features, np.float32))
+    elif cfg.attention != "softmax":
+        raise ValueError(cfg.attention)
     for h in range(H):
         c = slice(h * dh, (h + 1) * dh)
-        S = np.einsum("ntc,nuc->ntu", Q[:, :, c], K[:, :, c]) * scale
-        S = np.where(causal[None], S, -np.inf)
-        Ah = softmax_lastaxis(S).astype(m.dt)
+        if cfg.attention == "performer":
+            Ah = performer_attention_weights(Q[:, :, c], K[:, :, c], om, m.dt)
+        else:
+            S = np.einsum("ntc,nuc->ntu", Q[:, :, c], K[:, :, c]) * scale
+            S = np.where(causal[None], S, -np.inf)
+            Ah = softmax_lastaxis(S).astype(m.dt)
         A[:, h] = Ah
         O[:, :, c] = np.einsum("ntu,nuc->ntc", Ah, V[:, :, c])
     Oo = m.R(O)
@@ -346,6 +388,8 @@ def backward(cache: dict, cfg: Config) -> dict:
     """Gradient of L = (1/N) sum_n CE_nats[n] w.r.t. every parameter (Alg. 1
     line 10), by the chain rule through the forward above.  All T rows are
     carried; only the last row of Y_k receives an upstream gradient."""
+    if cfg.attention != "softmax":
+        raise NotImplementedError("the backward covers softmax attention (Eqs. 1-2) only")
     m = _Mode(cache["mode"])
     p = cache["p"]
     N, T, d, H, dh = cache["X"].shape[0], cfg.T, cfg.d, cfg.H, cfg.dh
