@@ -359,6 +359,46 @@ def measure_sweep():
             "lcr_source_bits_per_byte": round(ideal, 4), "batch": batch}
 
 
+def measure_performer(steps=3):
+    """The Performer (FAVOR+) attention of the paper's experiments (Sec. 6)
+    against exact softmax attention (Eqs. 1-2), forward + code lengths on the
+    main workload's shape and streams, both models in the same process; the
+    feature projection is seeded orthogonal random features."""
+    import torch
+    import paper_2203_16114_amd as P
+    import synth
+    w = synth.WORKLOADS[3]
+    S = 256
+    st, _ = synth.workload_streams(3, L=w.W + S * (steps + 1) + 1)
+    sd = torch.from_numpy(st).cuda()
+    B = st.shape[0]
+    res = {"workload": w.name, "streams": B, "positions_per_step": S}
+    for name, att in (("softmax", "softmax"), ("performer", "performer")):
+        m = P.TraceModel(w.W, w.e, w.g, w.H, w.F, w.k, dtype=w.dtype, max_windows=B * S, attention=att)
+        m.init_weights(w.weight_seed)
+        if att == "performer":
+            nf = 128 if w.d // w.H <= 32 else 256
+            m.set_features(synth.performer_features(0x0FE43, nf, w.d // w.H))
+            res["n_features"] = nf
+        bits = torch.empty(B * S, dtype=torch.float32, device="cuda")
+        m.forward_bits(sd, w.W, S, bits=bits)
+        torch.cuda.synchronize()
+        m.set_timing(True)
+        m.read_timing()
+        t0 = time.time()
+        for i in range(steps):
+            m.forward_bits(sd, w.W + S * (i + 1), S, bits=bits)
+        torch.cuda.synchronize()
+        res[name + "_bytes_per_s"] = B * S * steps / (time.time() - t0)
+        tm = m.read_timing()
+        res[name + "_attn_ms"] = round(tm["attn"][0] / max(tm["attn"][1], 1), 4)
+        m.set_timing(False)
+        del m
+    res["performer_over_softmax"] = round(res["performer_bytes_per_s"] / res["softmax_bytes_per_s"], 4)
+    log(f"[bench] performer {res}")
+    return res
+
+
 def measure_deep_ffn(steps=3):
     """The deep-FFN variant of Sec. 6.3 (untied W1, W2 per repeat) against the
     shared FFN on the main workload's shape and streams: forward bytes/s of
@@ -517,6 +557,7 @@ def main():
     if args.codec_steps > 0:
         out["codec"] = measure_codec(4, args.codec_steps)
         out["deep_ffn"] = measure_deep_ffn()
+        out["performer"] = measure_performer()
     if args.cpu_windows > 0:
         out["cpu_baseline"] = cpu_baseline(streams, w, args.cpu_windows, args.cpu_windows_one_core)
         log(f"[bench] cpu oracle: {out['cpu_baseline']['value']:.4g} bytes/s")

@@ -85,8 +85,17 @@ typedef struct {
    * own (the deep-FFN variant of Sec. 6.3): W1 and W2 in the flat order become
    * k consecutive blocks, repeat r's at r * D * F. */
   int32_t untied_ffn;
+  /* TRACE_ATTN_SOFTMAX: Eqs. 1-2; TRACE_ATTN_PERFORMER: the FAVOR+ attention of
+   * the Performer the paper's experiments use as backbone (Sec. 6), forward
+   * only, with n_features positive random features (0: 128 for d/H = 32, 256
+   * for 64; a multiple of 16, at most 512) whose projection is set by
+   * trace_set_features before the first forward. */
+  int32_t attention;
+  int32_t n_features;
   int32_t reserved_; /* 0 */
 } trace_config;
+
+enum { TRACE_ATTN_SOFTMAX = 0, TRACE_ATTN_PERFORMER = 1 };
 
 typedef struct trace_model trace_model; /* opaque, library-owned */
 
@@ -111,6 +120,16 @@ int trace_param_count(const trace_config* cfg, int64_t* n);
  * copied instead.  Resets Adam (m = v = 0, step count 0) and drops any kept
  * batch.  Synchronises the device. */
 int trace_init_weights(trace_model* m, uint64_t seed, double std, const float* host_flat);
+
+/* The random projection of the Performer's positive random features (Sec. 6's
+ * backbone; FAVOR+): omega[i][c] (host, row-major [n_features][d/H] floats),
+ * one for all heads.  With q' = q (d/H)^-1/4 and k' = k (d/H)^-1/4 per head,
+ * the last query row's weight on key u is phi(q')^T phi(k'_u) normalised over
+ * u, phi(x) = exp(omega x - |x|^2/2) (the 1/sqrt(m) factor cancels); the
+ * projections are formed in fp32 (bf16 models: omega rounded to bf16, the
+ * projected vector split into two bf16 parts).  Copies omega (synchronises);
+ * EINVAL unless the model uses TRACE_ATTN_PERFORMER and n = n_features * d/H. */
+int trace_set_features(trace_model* m, const float* host_omega, int64_t n);
 
 /* The same generator into a host array of n = trace_param_count floats,
  * without a model or a GPU. */
@@ -141,7 +160,8 @@ int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int64_t stride,
                        double* d_step_ce, uint32_t flags, void* stream);
 
 /* Model.backward of Alg. 1 line 10 on the batch kept by the last
- * KEEP_ACTS forward: the gradient of the batch-mean cross-entropy (nats)
+ * KEEP_ACTS forward (softmax attention only: EUNSUPPORTED for a Performer
+ * model): the gradient of the batch-mean cross-entropy (nats)
  * followed by one Adam step (Kingma & Ba, Alg. 1; bias-corrected; the step
  * count advances once per call) on the fp32 master, then a refresh of the
  * operand copies.  The kept batch is consumed.  ESTATE if none is kept. */

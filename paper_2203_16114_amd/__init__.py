@@ -20,8 +20,9 @@ LIB_PATH = os.path.join(_HERE, "libtrace.so")
 TRACE_OK, TRACE_EINVAL, TRACE_ENOMEM, TRACE_EHIP, TRACE_ESTATE, TRACE_ENONFINITE, TRACE_EUNSUPPORTED = 0, -1, -2, -3, -4, -5, -6
 TRACE_FP32, TRACE_BF16 = 0, 1
 TRACE_KEEP_ACTS, TRACE_TOKEN_ATTN = 1, 2
+TRACE_ATTN_SOFTMAX, TRACE_ATTN_PERFORMER = 0, 1
 
-EXPORTS = ("trace_create", "trace_destroy", "trace_param_count", "trace_init_weights", "trace_init_flat_host",
+EXPORTS = ("trace_create", "trace_destroy", "trace_param_count", "trace_init_weights", "trace_init_flat_host", "trace_set_features",
            "trace_forward_bits", "trace_forward_bits_noalloc", "trace_adapt_step", "trace_controller_init", "trace_controller_decide",
            "trace_gated_run",
            "trace_get_state", "trace_set_state", "trace_get_grads", "trace_quant_table", "trace_quantize",
@@ -42,7 +43,7 @@ class TraceConfig(ctypes.Structure):
     _fields_ = [("W", c_int32), ("e", c_int32), ("g", c_int32), ("H", c_int32), ("F", c_int32), ("k", c_int32),
                 ("dtype", c_int32), ("use_pos", c_int32), ("max_windows", c_int64), ("max_keep", c_int64),
                 ("lr", c_double), ("beta1", c_double), ("beta2", c_double), ("eps", c_double),
-                ("untied_ffn", c_int32), ("reserved_", c_int32)]
+                ("untied_ffn", c_int32), ("attention", c_int32), ("n_features", c_int32), ("reserved_", c_int32)]
 
 
 class TraceControllerState(ctypes.Structure):
@@ -74,6 +75,7 @@ def lib():
             "trace_param_count": (c_int32, [POINTER(TraceConfig), POINTER(c_int64)]),
             "trace_init_weights": (c_int32, [P, c_uint64, c_double, P]),
             "trace_init_flat_host": (c_int32, [POINTER(TraceConfig), c_uint64, c_double, P, c_int64]),
+            "trace_set_features": (c_int32, [P, P, c_int64]),
             "trace_forward_bits": (c_int32, [P, P, c_int64, c_int32, c_int64, c_int32, P, P, P, c_uint32, P]),
             "trace_forward_bits_noalloc": (c_int32, [P, P, c_int64, c_int32, c_int64, c_int32, P, P, P, c_uint32, P]),
             "trace_adapt_step": (c_int32, [P, P]),
@@ -115,10 +117,13 @@ def check(rc: int):
 
 
 def make_config(W, e, g, H, F, k, dtype="fp32", use_pos=True, max_windows=1 << 16, max_keep=0,
-                lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, untied_ffn=False) -> TraceConfig:
+                lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, untied_ffn=False, attention="softmax",
+                n_features=0) -> TraceConfig:
     dt = {"fp32": TRACE_FP32, "bf16": TRACE_BF16}[dtype] if isinstance(dtype, str) else int(dtype)
+    att = {"softmax": TRACE_ATTN_SOFTMAX, "performer": TRACE_ATTN_PERFORMER}[attention]
     return TraceConfig(W, e, g, H, F, k, dt, int(bool(use_pos)), int(max_windows), int(max_keep),
-                       float(lr), float(beta1), float(beta2), float(eps), int(bool(untied_ffn)), 0)
+                       float(lr), float(beta1), float(beta2), float(eps), int(bool(untied_ffn)), att,
+                       int(n_features), 0)
 
 
 def param_count(cfg: TraceConfig) -> int:
@@ -227,9 +232,10 @@ class TraceModel:
     """One model on the current HIP device (see include/trace.h)."""
 
     def __init__(self, W, e, g, H, F, k, dtype="fp32", use_pos=True, max_windows=1 << 16, max_keep=0,
-                 lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, untied_ffn=False):
+                 lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, untied_ffn=False, attention="softmax", n_features=0):
         self.cfg = make_config(W, e, g, H, F, k, dtype, use_pos, max_windows, max_keep, lr, beta1, beta2, eps,
-                               untied_ffn)
+                               untied_ffn, attention, n_features)
+        self.attention = attention
         self.W, self.e, self.g, self.H, self.F, self.k = W, e, g, H, F, k
         self.T, self.d = W // g, g * e
         self.dtype = dtype
@@ -287,6 +293,11 @@ class TraceModel:
                  _dptr(step_ce) if step_ce is not None else None,
                  (TRACE_KEEP_ACTS if keep else 0) | (TRACE_TOKEN_ATTN if token_attn else 0), _stream_ptr(stream)))
         return {"bits": bits, "logits": logits, "step_ce": step_ce}
+
+    def set_features(self, omega: np.ndarray):
+        """The Performer's random projection omega [n_features][d/H] (trace_set_features)."""
+        om = np.ascontiguousarray(omega, np.float32)
+        check(lib().trace_set_features(self._h, om.ctypes.data, om.size))
 
     def compress(self, streams, mode: int = MODE_NEVER, t: int = 16, delta: float = 0.05, length=None,
                  stream=None):

@@ -28,6 +28,10 @@ struct trace_model {
   void *Ec, *Pc;
   float* PW;  // [3][T][D] positional parts of the q, k, v projections
   uint4 *Wq, *Wk, *Wv, *Wo, *W1, *W2, *Wout;
+  // Performer attention: packed random projection (device), features, set yet
+  uint4* Om;
+  int nfeat;
+  bool feats_set;
   // forward workspace
   float* h0;
   // kept batch
@@ -283,6 +287,8 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
   m->max_keep = cfg->max_keep;
   m->max_windows = std::max<int64_t>(std::max<int64_t>(cfg->max_windows, cfg->max_keep), 1);
   (void)hipGetDevice(&m->device);
+  if (cfg->attention == TRACE_ATTN_PERFORMER)
+    m->nfeat = cfg->n_features ? cfg->n_features : (L.DH <= 32 ? 128 : 256);
   const int64_t n = L.n, D = L.D, T = L.T, F = cfg->F, W = cfg->W;
   const int es = bf ? 2 : 4;
   bool ok = dalloc(m, &m->theta, n * 4) && dalloc(m, &m->am, n * 4) && dalloc(m, &m->av, n * 4) &&
@@ -291,7 +297,8 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
             dalloc(m, &m->Wq, D * D * es) && dalloc(m, &m->Wk, D * D * es) && dalloc(m, &m->Wv, D * D * es) &&
             dalloc(m, &m->Wo, D * D * es) && dalloc(m, &m->W1, D * F * es * (cfg->untied_ffn ? cfg->k : 1)) &&
             dalloc(m, &m->W2, F * D * es * (cfg->untied_ffn ? cfg->k : 1)) &&
-            dalloc(m, &m->Wout, D * 256 * es) && dalloc(m, &m->h0, m->max_windows * D * 4);
+            dalloc(m, &m->Wout, D * 256 * es) && dalloc(m, &m->h0, m->max_windows * D * 4) &&
+            (m->nfeat == 0 || dalloc(m, &m->Om, (int64_t)m->nfeat * L.DH * es));
   const int64_t K = cfg->max_keep;
   if (ok && K > 0) {
     ok = dalloc(m, &m->kwin, K * W) && dalloc(m, &m->ktgt, K * 4) && dalloc(m, &m->kq, K * D * 4) &&
@@ -384,6 +391,59 @@ static int check_windows(const trace_model* m, const uint8_t* d_streams, int64_t
   return TRACE_OK;
 }
 
+namespace {
+// fp32 -> bf16 bits, round to nearest even (finite inputs)
+uint16_t host_bf16(float f) {
+  uint32_t u;
+  std::memcpy(&u, &f, 4);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (uint16_t)((u >> 16) | 0x40u);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (uint16_t)(u >> 16);
+}
+}  // namespace
+
+extern "C" int trace_set_features(trace_model* m, const float* omega, int64_t n) {
+  if (!m || !omega) return fail(TRACE_EINVAL, "model or omega is NULL");
+  if (m->cfg.attention != TRACE_ATTN_PERFORMER) return fail(TRACE_EINVAL, "the model does not use Performer attention");
+  const int DH = m->L.DH, nf = m->nfeat;
+  if (n != (int64_t)nf * DH) return fail(TRACE_EINVAL, "n must be n_features * d/H");
+  for (int64_t i = 0; i < n; ++i)
+    if (!std::isfinite(omega[i])) return fail(TRACE_EINVAL, "omega must be finite");
+  // MFMA A fragments of omega, one per (16-feature block, k-step over the head
+  // width), 64 lanes each, lane l holding feature 16 b + l % 16.  fp32: the
+  // four k values 16 s + 4 (l/16) + t.  bf16: eight k values in the order in
+  // which a lane holds the projected vector (two accumulator quads of 4
+  // columns): j < 4 -> 32 s + 4 (l/16) + j, j >= 4 -> 32 s + 16 + 4 (l/16) + j - 4.
+  const int kst = m->bf ? DH / 32 : DH / 16;
+  std::vector<uint16_t> hb;
+  std::vector<float> hf;
+  if (m->bf)
+    hb.resize((size_t)n);
+  else
+    hf.resize((size_t)n);
+  for (int b = 0; b < nf / 16; ++b)
+    for (int st = 0; st < kst; ++st)
+      for (int l = 0; l < 64; ++l) {
+        const int i = 16 * b + l % 16, lg = l / 16;
+        const size_t base = ((size_t)(b * kst + st) * 64 + l);
+        if (m->bf) {
+          for (int j = 0; j < 8; ++j) {
+            const int c = 32 * st + (j < 4 ? 4 * lg + j : 16 + 4 * lg + (j - 4));
+            hb[base * 8 + j] = host_bf16(omega[(int64_t)i * DH + c]);
+          }
+        } else {
+          for (int t = 0; t < 4; ++t) hf[base * 4 + t] = omega[(int64_t)i * DH + 16 * st + 4 * lg + t];
+        }
+      }
+  hipError_t e = hipDeviceSynchronize();
+  if (e == hipSuccess)
+    e = hipMemcpy(m->Om, m->bf ? (const void*)hb.data() : (const void*)hf.data(), (size_t)n * (m->bf ? 2 : 4),
+                  hipMemcpyHostToDevice);
+  if (e != hipSuccess) return hip_fail(e, "trace_set_features");
+  m->feats_set = true;
+  return TRACE_OK;
+}
+
 int trace_model_dim(const trace_model* m) { return m->L.D; }
 int trace_model_device(const trace_model* m) { return m->device; }
 
@@ -400,6 +460,7 @@ int trace_forward_into(trace_model* m, const uint8_t* d_streams, int64_t stride,
   if (keep && total > chunk_cap) return fail(TRACE_EINVAL, "KEEP_ACTS batch larger than the workspace");
   if (total == 0) return TRACE_OK;  // nothing to write: output pointers may be NULL
   if (!d_bits) return fail(TRACE_EINVAL, "bits is NULL");
+  if (m->nfeat && !m->feats_set) return fail(TRACE_ESTATE, "Performer features not set (trace_set_features)");
   const hipStream_t s = S(stream);
   const Layout& L = m->L;
   const int64_t chunk = keep ? total : chunk_cap;
@@ -426,8 +487,11 @@ int trace_forward_into(trace_model* m, const uint8_t* d_streams, int64_t stride,
     a.Wv = m->Wv;
     a.Wo = m->Wo;
     a.h0 = h0;
-    a.token_only = (flags & TRACE_TOKEN_ATTN) != 0;
+    a.token_only = (flags & TRACE_TOKEN_ATTN) != 0 || m->nfeat != 0;
+    a.Om = m->nfeat ? m->Om : nullptr;
+    a.nfeat = m->nfeat;
     a.scale = (float)(1.0 / std::sqrt((double)L.DH));
+    a.scale4 = (float)std::pow((double)L.DH, -0.25);
     FfnArgs f;
     std::memset(&f, 0, sizeof(f));
     f.w = w;
@@ -486,6 +550,7 @@ extern "C" int trace_forward_bits(trace_model* m, const uint8_t* d_streams, int6
 
 extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   if (!m) return fail(TRACE_EINVAL, "model is NULL");
+  if (m->nfeat) return fail(TRACE_EUNSUPPORTED, "the update covers softmax attention only (Performer: forward only)");
   if (!m->kept) return fail(TRACE_ESTATE, "no batch kept: run trace_forward_bits with TRACE_KEEP_ACTS first");
   const hipStream_t s = S(stream);
   const Layout& L = m->L;

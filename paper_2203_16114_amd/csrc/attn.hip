@@ -48,6 +48,93 @@ __device__ __forceinline__ f32x4 rounded4(const f32x4& v, bool bf) {
   return f32x4{round_bf(v[0]), round_bf(v[1]), round_bf(v[2]), round_bf(v[3])};
 }
 
+// Performer (FAVOR+) weight of key row u of a window's last query, for one
+// head: phi(q')^T phi(k'_u) normalised over the window's T rows, with
+// phi(x) = exp(omega x - |x|^2/2), q' = q dh^-1/4, k' = k dh^-1/4 (the
+// 1/sqrt(m) factor cancels).  phi(q')^T phi(k'_u) = sum_i exp(omega_i w -
+// (|q'|^2 + |k'_u|^2)/2) with w = q' + k'_u.  The lane holds row u's key as an
+// accumulator quad per 16 columns (c = 16 f + 4 lg + r) and reads q from its
+// LDS row; w becomes the B operand of the projection in that same order (one
+// fp32 fragment per quad, or in bf16 a hi and a lo fragment per two quads,
+// matched by the packing of omega), so each 16-feature block is one MFMA chain
+// whose result gives the lane features 4 lg + r of row u.  The sum over
+// features runs with a running maximum (base 2); the maximum over the window
+// is subtracted before the rows are normalised (it cancels).
+template <bool BF, int T, int NFH>
+__device__ __forceinline__ float perf_weight(const f32x4 (&k)[NFH], const float* __restrict__ qrow, int lg,
+                                             const uint4* __restrict__ Om, int nfeat, float s4) {
+  typedef Mma<BF> M;
+  constexpr int KST = BF ? NFH / 2 : NFH;  // k-steps over the head width
+  float w[NFH][4];
+  float nrm = 0.f;
+#pragma unroll
+  for (int f = 0; f < NFH; ++f) {
+    const float4 q4 = *reinterpret_cast<const float4*>(qrow + f * 16 + 4 * lg);
+    const float qv[4] = {q4.x, q4.y, q4.z, q4.w};
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      nrm = fmaf(k[f][r], k[f][r], fmaf(qv[r], qv[r], nrm));
+      w[f][r] = s4 * (qv[r] + k[f][r]);
+    }
+  }
+  nrm += __shfl_xor(nrm, 16, 64);
+  nrm += __shfl_xor(nrm, 32, 64);
+  const float base = -0.5f * s4 * s4 * nrm * TRACE_LOG2E;  // -(|q'|^2 + |k'|^2)/2, base 2
+  uint4 bh[KST], bl[KST];
+#pragma unroll
+  for (int st = 0; st < KST; ++st) {
+    if constexpr (BF) {
+      float hv[8], lv[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const float x = j < 4 ? w[2 * st][j] : w[2 * st + 1][j - 4];
+        hv[j] = round_bf(x);
+        lv[j] = x - hv[j];
+      }
+      bh[st] = make_uint4(pack_bf16x2(hv[0], hv[1]), pack_bf16x2(hv[2], hv[3]), pack_bf16x2(hv[4], hv[5]),
+                          pack_bf16x2(hv[6], hv[7]));
+      bl[st] = make_uint4(pack_bf16x2(lv[0], lv[1]), pack_bf16x2(lv[2], lv[3]), pack_bf16x2(lv[4], lv[5]),
+                          pack_bf16x2(lv[6], lv[7]));
+    } else {
+      bh[st] = make_uint4(__float_as_uint(w[st][0]), __float_as_uint(w[st][1]), __float_as_uint(w[st][2]),
+                          __float_as_uint(w[st][3]));
+      bl[st] = bh[st];
+    }
+  }
+  const int lane = threadIdx.x & 63;
+  float mx = 0.f, sm = 0.f;
+  for (int b = 0; b < nfeat / 16; ++b) {
+    f32x4 z = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int st = 0; st < KST; ++st) {
+      const uint4 om = Om[(b * KST + st) * 64 + lane];
+      M::run(z, om, bh[st]);
+      if constexpr (BF) M::run(z, om, bl[st]);
+    }
+    float x[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) x[r] = fmaf(z[r], TRACE_LOG2E, base);
+    const float bm = fmaxf(fmaxf(x[0], x[1]), fmaxf(x[2], x[3]));
+    const float nm = b == 0 ? bm : fmaxf(mx, bm);
+    float acc = b == 0 ? 0.f : sm * __builtin_amdgcn_exp2f(mx - nm);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) acc += __builtin_amdgcn_exp2f(x[r] - nm);
+    sm = acc;
+    mx = nm;
+  }
+  // the row's four lane groups hold different features: combine them
+#pragma unroll
+  for (int off = 16; off <= 32; off <<= 1) {
+    const float om = __shfl_xor(mx, off, 64), os = __shfl_xor(sm, off, 64);
+    const float nm = fmaxf(mx, om);
+    sm = sm * __builtin_amdgcn_exp2f(mx - nm) + os * __builtin_amdgcn_exp2f(om - nm);
+    mx = nm;
+  }
+  const float wmax = group_max<T>(mx);
+  const float sc = sm * __builtin_amdgcn_exp2f(mx - wmax);
+  return sc * __builtin_amdgcn_rcpf(group_sum<T>(sc));
+}
+
 template <bool BF, int T, int D, int DH, bool SMALL = false>
 struct AttnShape {
   typedef typename Mma<BF>::T OT;
@@ -73,7 +160,7 @@ struct AttnShape {
 
 }  // namespace
 
-template <bool BF, int T, int D, int DH, bool KEEP, bool SMALL>
+template <bool BF, int T, int D, int DH, bool KEEP, bool SMALL, bool PERF>
 __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
   typedef Mma<BF> M;
   typedef typename M::T OT;
@@ -254,19 +341,23 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
           acc[rf][f][3] += p4.w;
         }
         if (pass == 0) {
-          float s = 0.f;
+          if constexpr (PERF) {
+            prob[rf] = perf_weight<BF, T, NFH>(acc[rf], Qs + m * D + h * DH, lg, a.Om, a.nfeat, a.scale4);
+          } else {
+            float s = 0.f;
 #pragma unroll
-          for (int f = 0; f < NFH; ++f) {
-            const float4 q4 = *reinterpret_cast<const float4*>(Qs + m * D + h * DH + f * 16 + 4 * lg);
-            s += q4.x * acc[rf][f][0] + q4.y * acc[rf][f][1] + q4.z * acc[rf][f][2] + q4.w * acc[rf][f][3];
+            for (int f = 0; f < NFH; ++f) {
+              const float4 q4 = *reinterpret_cast<const float4*>(Qs + m * D + h * DH + f * 16 + 4 * lg);
+              s += q4.x * acc[rf][f][0] + q4.y * acc[rf][f][1] + q4.z * acc[rf][f][2] + q4.w * acc[rf][f][3];
+            }
+            s += __shfl_xor(s, 16, 64);
+            s += __shfl_xor(s, 32, 64);
+            s *= scale;
+            const float mx = group_max<T>(s);
+            const float p = expf(s - mx);
+            const float sm = group_sum<T>(p);
+            prob[rf] = p * __builtin_amdgcn_rcpf(sm);
           }
-          s += __shfl_xor(s, 16, 64);
-          s += __shfl_xor(s, 32, 64);
-          s *= scale;
-          const float mx = group_max<T>(s);
-          const float p = expf(s - mx);
-          const float sm = group_sum<T>(p);
-          prob[rf] = p * __builtin_amdgcn_rcpf(sm);
           if (KEEP && live) {
             if (lg == 0) a.kA[(n * H + h) * T + t] = prob[rf];
 #pragma unroll
@@ -655,10 +746,16 @@ static void launch_attn(const AttnArgs& a, hipStream_t s) {
   typedef AttnShape<BF, T, D, DH, SMALL> S;
   static_assert(S::LDS <= 160 * 1024, "LDS");
   const dim3 grid((unsigned)((a.w.N + S::MA - 1) / S::MA));
-  if (a.kK)
-    hipLaunchKernelGGL((k_attn<BF, T, D, DH, true, SMALL>), grid, dim3(512), 0, s, a);
-  else
-    hipLaunchKernelGGL((k_attn<BF, T, D, DH, false, SMALL>), grid, dim3(512), 0, s, a);
+  if (a.Om) {
+    if (a.kK)
+      hipLaunchKernelGGL((k_attn<BF, T, D, DH, true, SMALL, true>), grid, dim3(512), 0, s, a);
+    else
+      hipLaunchKernelGGL((k_attn<BF, T, D, DH, false, SMALL, true>), grid, dim3(512), 0, s, a);
+  } else if (a.kK) {
+    hipLaunchKernelGGL((k_attn<BF, T, D, DH, true, SMALL, false>), grid, dim3(512), 0, s, a);
+  } else {
+    hipLaunchKernelGGL((k_attn<BF, T, D, DH, false, SMALL, false>), grid, dim3(512), 0, s, a);
+  }
 }
 
 template <int T, int G, int D, int DH>

@@ -67,6 +67,14 @@ int trace_check_config(const trace_config* c, Layout* L) {
     trace_set_error("untied_ffn must be 0 or 1");
     return TRACE_EINVAL;
   }
+  if (c->attention != TRACE_ATTN_SOFTMAX && c->attention != TRACE_ATTN_PERFORMER) {
+    trace_set_error("attention must be TRACE_ATTN_SOFTMAX or TRACE_ATTN_PERFORMER");
+    return TRACE_EINVAL;
+  }
+  if (c->n_features < 0 || c->n_features > 512 || c->n_features % 16 != 0) {
+    trace_set_error("n_features must be a multiple of 16 in [0, 512]");
+    return TRACE_EINVAL;
+  }
   if (!(c->lr >= 0.0) || !(c->beta1 >= 0.0 && c->beta1 < 1.0) || !(c->beta2 >= 0.0 && c->beta2 < 1.0) ||
       !(c->eps > 0.0)) {
     trace_set_error("Adam settings out of range (lr >= 0, 0 <= beta < 1, eps > 0)");

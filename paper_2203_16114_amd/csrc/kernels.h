@@ -22,7 +22,10 @@ struct AttnArgs {
   const uint4 *Wq, *Wk, *Wv, *Wo;  // packed operand copies
   float* h0;                       // [N][D]: Attn + X, the residual stream entering the FFN
   float scale;                     // 1/sqrt(head width)
+  float scale4;                    // (head width)^-1/4 (Performer)
   int32_t token_only;              // 1: the per-token kernel whatever the launch shape
+  const uint4* Om;                 // Performer: packed random projection (NULL: softmax attention)
+  int32_t nfeat;                   // Performer: features (a multiple of 16)
   // kept activations for the backward (all NULL unless kept), indexed by local window
   uint8_t* kwin;  // [N][W]
   float* kq;      // [N][D]     query of the last token
