@@ -79,12 +79,13 @@ def test_gradient_and_adam_step_match_oracle(name):
     # against the oracle's own step: the first step is -lr g/(|g| + eps), about
     # -lr sign(g); coordinates whose gradient is within the bf16 noise of zero
     # can take the other sign (2 lr each), so the relative error by norm is
-    # about 2 sqrt(fraction flipped): 0.2 allows 1 % of the coordinates
+    # about 2 sqrt(fraction flipped): 0.05 allows 0.06 % of the coordinates
+    # (measured: at most 1.6e-3 at the adaptation shape, 1.4e-2 at the large)
     dth = O.unflatten(th1.astype(np.float64) - flat.astype(np.float64), cfg)
     for n, sk in g["dtheta1"].items():
         total, _, _ = compare(sk, dth[n], seed)
         report["dtheta_" + n] = total
-        assert total <= 0.2, (n, total)
+        assert total <= 0.05, (n, total)
     print("relative errors:", {k: round(v, 6) for k, v in report.items()})
 
 
@@ -136,5 +137,6 @@ def test_teacher_forced_steps_match_oracle(name):
             pr = np.asarray(sk["proj"]) - r0 @ V
             rel = np.sqrt(np.sum((rg @ V - pr) ** 2) / np.sum(pr ** 2))
         report[n] = float(rel)
-        assert rel <= 0.2, (n, rel)
+        # the same sign-flip argument over the run's updates (measured: at most 6e-3)
+        assert rel <= 0.05, (n, rel)
     print("relative errors:", {k: round(v, 6) for k, v in report.items()})
