@@ -446,6 +446,10 @@ def main():
     ap.add_argument("--cpu-windows-one-core", type=int, default=1024, help="oracle sample on one core (0: skip)")
     ap.add_argument("--codec-steps", type=int, default=64, help="positions of the compress / decompress run (0: skip)")
     ap.add_argument("--sweep", action="store_true", help="only the LCR and batch-size sweeps (one JSON line)")
+    ap.add_argument("--update-profile", type=int, default=0,
+                    help="only run --update-steps always-update steps of this workload (4 or 5) "
+                         "and print one JSON line: the run that the update's kernel profiles come from")
+    ap.add_argument("--update-steps", type=int, default=30)
     ap.add_argument("--copy-probe-mib", type=int, default=0,
                     help="only run 5 device-to-device copies of this many MiB (calibrates the HBM "
                          "byte counters FETCH_SIZE / WRITE_SIZE against a copy of known size)")
@@ -462,6 +466,26 @@ def main():
 
     if args.sweep:
         print(json.dumps({"sweep": measure_sweep()}), flush=True)
+        return
+    if args.update_profile:
+        w = synth.WORKLOADS[args.update_profile]
+        n = args.update_steps
+        streams, _ = synth.workload_streams(args.update_profile, L=w.W + n + 9)
+        sd = torch.from_numpy(streams).cuda()
+        m = P.TraceModel(w.W, w.e, w.g, w.H, w.F, w.k, dtype=w.dtype, max_windows=w.B * 64, max_keep=w.B)
+        m.init_weights(w.weight_seed)
+        m.gated_run(sd, w.W, 8, P.MODE_ALWAYS)                      # first launches, untimed
+        torch.cuda.synchronize()
+        m.set_timing(True)
+        m.read_timing()
+        t0 = time.perf_counter()
+        m.gated_run(sd, w.W + 8, n, P.MODE_ALWAYS)
+        torch.cuda.synchronize()
+        dt = time.perf_counter() - t0
+        tm = m.read_timing()
+        print(json.dumps({"update_profile": w.name, "steps": n, "ms_per_step": dt / n * 1e3,
+                          "kernel_ms_per_launch": {k: round(v[0] / v[1], 4) for k, v in tm.items()
+                                                   if k != "overflow" and v[1]}}), flush=True)
         return
     if args.copy_probe_mib > 0:
         n = args.copy_probe_mib << 20

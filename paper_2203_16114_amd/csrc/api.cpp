@@ -46,7 +46,7 @@ struct trace_model {
   // activations (one buffer per repeat, read by the weight gradients later);
   // in bf16 models dU, Xk (the byte-embedding part of the kept tokens) and the
   // kept Y hold bf16 elements: all are only read as bf16 operands
-  float *dz, *dY, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *sP, *gws, *cws, *ews;
+  float *dz, *dY, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *sP, *gws, *cws, *ews, *apart;
   int64_t gws_cap;
   // second stream of the update step (the weight-gradient branch), its own
   // split-K and column-sum workspaces, and the events that order the two streams
@@ -311,10 +311,11 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
          (bf || dalloc(m, &m->G, K * F * 4)) &&
          dalloc(m, &m->dO, K * D * 4) && dalloc(m, &m->dQ, K * D * 4) && dalloc(m, &m->dK, K * T * D * 4) &&
          dalloc(m, &m->dV, K * T * D * 4) && dalloc(m, &m->dX, K * T * D * 4) && dalloc(m, &m->Xk, K * T * D * es) &&
-         dalloc(m, &m->sP, (T + 1) * D * 4) &&
+         dalloc(m, &m->sP, (2 * T + 2) * D * 4) &&
+         dalloc(m, &m->apart, attn_bwd_part_floats(K, T, D, cfg->H) * 4) &&
          dalloc(m, &m->gws, (m->gws_cap = adapt_gemm_ws(m, K)) * 4) &&
          dalloc(m, &m->ews, embed_bwd_ws_floats(K * W, cfg->e) * 4) &&
-         dalloc(m, &m->cws, colsum_ws_floats(std::max<int64_t>(T * D, 256)) * 4) &&
+         dalloc(m, &m->cws, colsum_ws_floats(std::max<int64_t>(2 * T * D, 256)) * 4) &&
          dalloc(m, &m->gws2, m->gws_cap * 4) && dalloc(m, &m->cws2, colsum_ws_floats(T * D) * 4);
     if (ok) ok = hipStreamCreateWithFlags(&m->side, hipStreamNonBlocking) == hipSuccess;
     for (int i = 0; ok && i < 16; ++i) {
@@ -572,7 +573,9 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // writer's stream, or, for the side stream's results, the final wait of s):
   //   s: dz -> s, side; dY_r, dU_r -> s, side (one buffer per repeat); dO, dX,
   //      grad P, grad E -> s; dQ, dK, dV -> s, side
-  //   side: Xk, sP, grad Wout, bout, W1, W2, Wo, Wq, Wk, Wv -> side only
+  //   s: sums over windows in sP (dK, dV, dQ before the mark that the side
+  //      stream waits on; dY_0 after it, read by s only)
+  //   side: Xk, grad Wout, bout, W1, W2, Wo, Wq, Wk, Wv -> side only
   //   kept activations (forward, on s) -> both; s waits for side before Adam,
   //   so the next forward cannot overwrite them while side still reads
   const hipStream_t w = m->side;
@@ -633,9 +636,16 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // attention output projection: dO = dY_0 . Wo^T, then the attention (last
   // query row) -> dQ, dK, dV
   launch_gemm(gemm(N, D, D, dYr(0), D, 1, rb, th + L.off[P_WO], 1, D, rb, m->dO, D, 0.f), ws, m->gws_cap, s);
+  // sP: [0, T D) sum over windows of dK, [T D, 2T D) of dV (from the attention
+  // backward), [2T D, (2T+1) D) of dQ, [(2T+1) D, (2T+2) D) of dY_0
+  float* sK = m->sP;
+  float* sV = m->sP + (int64_t)T * D;
+  float* sQ = m->sP + (int64_t)2 * T * D;
+  float* sY = m->sP + (int64_t)(2 * T + 1) * D;
   launch_attn_bwd(m->dO, m->kq, m->kK, m->kV, m->kA, N, T, D, H, (float)(1.0 / std::sqrt((double)L.DH)), rb, m->dQ,
-                  m->dK, m->dV, s);
-  order(m, s, w);  // dQ, dK, dV are complete
+                  m->dK, m->dV, m->apart, sK, m->cws, s);
+  if (m->cfg.use_pos) launch_colsum(m->dQ, N, D, D, sQ, 0.f, m->cws, s);
+  order(m, s, w);  // dQ, dK, dV and their sums over windows are complete
   // side: dWk = X^T dK, dWv = X^T dV (dK, dV stay fp32), with X = G + P[t]:
   // G^T dZ as GEMMs on the byte-embedding part G, then P^T (sum over windows of
   // dZ) for the positional part
@@ -645,10 +655,8 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   ok = launch_gemm(gk, ws2, m->gws_cap, w) && ok;
   ok = launch_gemm(gv, ws2, m->gws_cap, w) && ok;
   if (m->cfg.use_pos) {
-    launch_colsum(m->dK, N, (int64_t)T * D, (int64_t)T * D, m->sP, 0.f, m->cws2, w);
-    launch_pos_grad(m->bf, m->Pc, m->sP, 0, T, D, gr + L.off[P_WK], w);
-    launch_colsum(m->dV, N, (int64_t)T * D, (int64_t)T * D, m->sP, 0.f, m->cws2, w);
-    launch_pos_grad(m->bf, m->Pc, m->sP, 0, T, D, gr + L.off[P_WV], w);
+    launch_pos_grad(m->bf, m->Pc, sK, 0, T, D, gr + L.off[P_WK], w);
+    launch_pos_grad(m->bf, m->Pc, sV, 0, T, D, gr + L.off[P_WV], w);
   }
   // side: dWq = X_last^T dQ (+ its positional part); Xk was written on this
   // stream, dQ before the last mark
@@ -656,10 +664,7 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
                      gr + L.off[P_WQ], D, 0.f);
   gq.halfA = hf;
   ok = launch_gemm(gq, ws2, m->gws_cap, w) && ok;
-  if (m->cfg.use_pos) {
-    launch_colsum(m->dQ, N, D, D, m->sP + (int64_t)T * D, 0.f, m->cws2, w);
-    launch_pos_grad(m->bf, m->Pc, m->sP + (int64_t)T * D, T - 1, 1, D, gr + L.off[P_WQ], w);
-  }
+  if (m->cfg.use_pos) launch_pos_grad(m->bf, m->Pc, sQ, T - 1, 1, D, gr + L.off[P_WQ], w);
   // dX = dK Wk^T + dV Wv^T (+ dQ Wq^T + dY_0 on the last token)
   launch_gemm2(gemm(N * T, D, D, m->dK, D, 1, 0, th + L.off[P_WK], 1, D, rb, m->dX, D, 0.f),
                gemm(N * T, D, D, m->dV, D, 1, 0, th + L.off[P_WV], 1, D, rb, m->dX, D, 0.f), ws, m->gws_cap, s);
@@ -667,11 +672,15 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
                    1.f),
               ws, m->gws_cap, s);
   launch_add(m->dX + (int64_t)(T - 1) * D, dYr(0), N, D, (int64_t)T * D, D, s);
-  // positional table and byte embedding
-  if (m->cfg.use_pos)
-    launch_colsum(m->dX, N, (int64_t)T * D, (int64_t)T * D, gr + L.off[P_P], 0.f, m->cws, s);
-  else
+  // positional table: dP[t] = sum_n dX[n][t], from the sums over windows of
+  // dK, dV, dQ and dY_0 times the weights; then the byte embedding
+  if (m->cfg.use_pos) {
+    launch_colsum(dYr(0), N, D, D, sY, 0.f, m->cws, s);
+    launch_pos_table_grad(sK, sQ, sY, th + L.off[P_WQ], th + L.off[P_WK], th + L.off[P_WV], T, D, rb,
+                          gr + L.off[P_P], s);
+  } else {
     launch_zero(gr + L.off[P_P], L.size[P_P], s);
+  }
   launch_embed_bwd(m->kwin, m->dX, N, m->cfg.W, m->cfg.e, gr + L.off[P_E], m->ews, s);
   order(m, w, s);  // every gradient is complete
   if (!ok) {

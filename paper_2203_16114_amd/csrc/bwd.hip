@@ -562,63 +562,120 @@ void launch_add(float* y, const float* x, int64_t rows, int64_t cols, int64_t ld
 //   dq = scale sum_u dS_u K_u,  dK_u = scale dS_u q,  dV_u = a_u dO.
 // One thread per (window, head, column); the two reductions over the head's
 // columns go through LDS.
+// Attention backward of the last query row (Eqs. 1-2).  A block takes one
+// head of 4 (DH = 64) or 8 (DH = 32) consecutive windows, a wave (half a wave)
+// per window and a lane per column: dA_u = dO_h . V_h[u] by shuffle sums over
+// the head's lanes, dS = A (dA - sum_u A_u dA_u), dQ_h = scale sum_u dS_u
+// K_h[u], dK_h[u] = scale dS_u q_h, dV_h[u] = A_u dO_h.  The block also adds
+// its windows' dK and dV rows in a fixed order into part[chunk][0|1][u][col]:
+// the sums over windows that the positional gradients need come from a column
+// sum over the chunks (launch_colsum) instead of over every window's rows.
 template <int DH>
-__global__ __launch_bounds__(256) void k_attn_bwd(const float* __restrict__ dO, const float* __restrict__ q,
-                                                  const float* __restrict__ K, const float* __restrict__ V,
-                                                  const float* __restrict__ A, int64_t N, int T, int D, int H,
-                                                  float scale, int round_dO, float* __restrict__ dQ,
-                                                  float* __restrict__ dK, float* __restrict__ dV) {
-  constexpr int GROUPS = 256 / DH;  // (window, head) pairs per block
-  __shared__ float red[GROUPS][8][DH];
-  __shared__ float dS[GROUPS][8];
-  const int gi = threadIdx.x / DH, c = threadIdx.x % DH;
-  const int64_t pair = (int64_t)blockIdx.x * GROUPS + gi;
-  const bool live = pair < N * H;
-  const int64_t n = live ? pair / H : 0;
-  const int h = live ? (int)(pair % H) : 0;
+__global__ __launch_bounds__(256) void k_attn_bwd2(const float* __restrict__ dO, const float* __restrict__ q,
+                                                   const float* __restrict__ K, const float* __restrict__ V,
+                                                   const float* __restrict__ A, int64_t N, int T, int D, int H,
+                                                   float scale, int round_dO, float* __restrict__ dQ,
+                                                   float* __restrict__ dK, float* __restrict__ dV,
+                                                   float* __restrict__ part) {
+  constexpr int PW = 64 / DH;  // windows per wave
+  constexpr int CH = 4 * PW;   // windows per block
+  __shared__ float red[2][CH][8][DH];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int c = lane % DH, sub = lane / DH, slot = wave * PW + sub;
+  const int h = blockIdx.x % H;
+  const int64_t ch = blockIdx.x / H;
   const int col = h * DH + c;
-  float o = live ? dO[n * D + col] : 0.f;
+  const int64_t n = ch * CH + slot;
+  const bool live = n < N;
+  const int64_t nn = live ? n : ch * CH;  // dead slots redo the chunk's first window and store nothing
+  float o = dO[nn * D + col];
   if (round_dO) o = round_bf(o);
-  for (int u = 0; u < T; ++u) red[gi][u][c] = live ? o * V[(n * T + u) * D + col] : 0.f;
-  __syncthreads();
-  if (c < T) {
-    float s = 0.f;
-    for (int i = 0; i < DH; ++i) s += red[gi][c][i];
-    dS[gi][c] = s;  // dA_c for now
-  }
-  __syncthreads();
-  if (c == 0 && live) {
-    float a[8], dA[8], sum = 0.f;
-    for (int u = 0; u < T; ++u) {
-      a[u] = A[(n * H + h) * T + u];
-      dA[u] = dS[gi][u];
-      sum += a[u] * dA[u];
+  float a[8], dA[8];
+  float tot = 0.f;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    if (u < T) {
+      float x = o * V[(nn * T + u) * D + col];
+#pragma unroll
+      for (int off = 1; off < DH; off <<= 1) x += __shfl_xor(x, off, 64);
+      dA[u] = x;
+      a[u] = A[(nn * H + h) * T + u];
+      tot = fmaf(a[u], x, tot);
     }
-    for (int u = 0; u < T; ++u) dS[gi][u] = a[u] * (dA[u] - sum);
   }
-  __syncthreads();
-  if (!live) return;
-  const float qv = q[n * D + col];
+  const float qv = q[nn * D + col];
   float dq = 0.f;
-  for (int u = 0; u < T; ++u) {
-    const float ds = dS[gi][u];
-    dq += ds * K[(n * T + u) * D + col];
-    dK[(n * T + u) * D + col] = (ds * qv) * scale;
-    dV[(n * T + u) * D + col] = A[(n * H + h) * T + u] * o;
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    if (u < T) {
+      const float ds = a[u] * (dA[u] - tot);
+      dq = fmaf(ds, K[(nn * T + u) * D + col], dq);
+      const float dk = (ds * qv) * scale, dv = a[u] * o;
+      if (live) {
+        dK[(nn * T + u) * D + col] = dk;
+        dV[(nn * T + u) * D + col] = dv;
+      }
+      red[0][slot][u][c] = live ? dk : 0.f;
+      red[1][slot][u][c] = live ? dv : 0.f;
+    }
   }
-  dQ[n * D + col] = dq * scale;
+  if (live) dQ[nn * D + col] = dq * scale;
+  __syncthreads();
+  for (int i = threadIdx.x; i < 2 * T * DH; i += 256) {
+    const int which = i / (T * DH), u = (i / DH) % T, cc = i % DH;
+    float v = 0.f;
+#pragma unroll
+    for (int k = 0; k < CH; ++k) v += red[which][k][u][cc];
+    part[((ch * 2 + which) * T + u) * D + h * DH + cc] = v;
+  }
 }
+
+int64_t attn_bwd_chunks(int64_t N, int D, int H) { return (N + 4 * (64 / (D / H)) - 1) / (4 * (64 / (D / H))); }
+
+int64_t attn_bwd_part_floats(int64_t N, int T, int D, int H) { return attn_bwd_chunks(N, D, H) * 2 * T * D; }
+
 void launch_attn_bwd(const float* dO, const float* q, const float* K, const float* V, const float* A, int64_t N, int T,
-                     int D, int H, float scale, int round_dO, float* dQ, float* dK, float* dV, hipStream_t s) {
+                     int D, int H, float scale, int round_dO, float* dQ, float* dK, float* dV, float* part,
+                     float* colsums, float* cws, hipStream_t s) {
   const int DH = D / H;
-  const int64_t pairs = N * H;
-  if (DH == 32) {
-    hipLaunchKernelGGL(k_attn_bwd<32>, dim3((unsigned)((pairs + 7) / 8)), dim3(256), 0, s, dO, q, K, V, A, N, T, D,
-                       H, scale, round_dO, dQ, dK, dV);
-  } else {
-    hipLaunchKernelGGL(k_attn_bwd<64>, dim3((unsigned)((pairs + 3) / 4)), dim3(256), 0, s, dO, q, K, V, A, N, T, D,
-                       H, scale, round_dO, dQ, dK, dV);
+  const int64_t chunks = attn_bwd_chunks(N, D, H);
+  const dim3 grid((unsigned)(chunks * H));
+  if (DH == 32)
+    hipLaunchKernelGGL(k_attn_bwd2<32>, grid, dim3(256), 0, s, dO, q, K, V, A, N, T, D, H, scale, round_dO, dQ, dK,
+                       dV, part);
+  else
+    hipLaunchKernelGGL(k_attn_bwd2<64>, grid, dim3(256), 0, s, dO, q, K, V, A, N, T, D, H, scale, round_dO, dQ, dK,
+                       dV, part);
+  launch_colsum(part, chunks, (int64_t)2 * T * D, (int64_t)2 * T * D, colsums, 0.f, cws, s);
+}
+
+// dP[t][c] = sum_j sK[t][j] Wk[c][j] + sV[t][j] Wv[c][j], plus, for t = T-1,
+// sQ[j] Wq[c][j] + sY[c]: the positional table's gradient sum_n dX[n][t], with
+// the sums over windows taken before the products (weights as the operand
+// copies: rounded to bf16 in bf16 models).  One wave per output, the lanes
+// across j, the lane sums in a fixed tree.
+__global__ __launch_bounds__(256) void k_pos_table_grad(const float* __restrict__ sKV, const float* __restrict__ sQ,
+                                                        const float* __restrict__ sY, const float* __restrict__ Wq,
+                                                        const float* __restrict__ Wk, const float* __restrict__ Wv,
+                                                        int T, int D, int rb, float* __restrict__ dP) {
+  const int i = blockIdx.x * 4 + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  if (i >= T * D) return;
+  const int t = i / D, c = i % D;
+  auto w = [&](const float* W, int j) { return rb ? round_bf(W[(int64_t)c * D + j]) : W[(int64_t)c * D + j]; };
+  float acc = 0.f;
+  for (int j = lane; j < D; j += 64) {
+    acc = fmaf(sKV[t * D + j], w(Wk, j), acc);
+    acc = fmaf(sKV[(T + t) * D + j], w(Wv, j), acc);
+    if (t == T - 1) acc = fmaf(sQ[j], w(Wq, j), acc);
   }
+#pragma unroll
+  for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
+  if (lane == 0) dP[i] = t == T - 1 ? acc + sY[c] : acc;
+}
+void launch_pos_table_grad(const float* sKV, const float* sQ, const float* sY, const float* Wq, const float* Wk,
+                           const float* Wv, int T, int D, int rb, float* dP, hipStream_t s) {
+  hipLaunchKernelGGL(k_pos_table_grad, dim3((unsigned)((T * D + 3) / 4)), dim3(256), 0, s, sKV, sQ, sY, Wq, Wk, Wv,
+                     T, D, rb, dP);
 }
 
 // ------------------------------------------------------ embedding backward ----

@@ -123,7 +123,11 @@ void launch_ce_grad(const float* z, const int32_t* tgt, int64_t N, float* dz, hi
 void launch_gelu_fwd_round(const float* U, float* G, int64_t n, int round, hipStream_t s);
 void launch_gelu_bwd(const float* dG, const float* U, float* dU, int64_t n, hipStream_t s);
 void launch_attn_bwd(const float* dO, const float* q, const float* K, const float* V, const float* A, int64_t N, int T,
-                     int D, int H, float scale, int round_dO, float* dQ, float* dK, float* dV, hipStream_t s);
+                     int D, int H, float scale, int round_dO, float* dQ, float* dK, float* dV, float* part,
+                     float* colsums, float* cws, hipStream_t s);
+int64_t attn_bwd_part_floats(int64_t N, int T, int D, int H);
+void launch_pos_table_grad(const float* sKV, const float* sQ, const float* sY, const float* Wq, const float* Wk,
+                           const float* Wv, int T, int D, int rb, float* dP, hipStream_t s);
 void launch_add(float* y, const float* x, int64_t rows, int64_t cols, int64_t ldy, int64_t ldx, hipStream_t s);
 // dE[v][:] = sum of the e-vectors of dX (viewed as [N*W][e]) at the positions
 // whose window byte is v; N*W < 2^31; deterministic
