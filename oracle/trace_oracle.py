@@ -69,6 +69,9 @@ class Config:
     # features (the projection matrix is an input of forward)
     attention: str = "softmax"
     n_features: int = 0
+    # layers of Eq. 4 stacked (Sec. 6.3, Fig. 7); every layer has its own
+    # Wq, Wk, Wv, Wo, W1, W2, stored as `layers` consecutive blocks of each
+    layers: int = 1
 
     @property
     def T(self) -> int:  # tokens per window (Sec. 4.2: c groups)
@@ -90,18 +93,27 @@ class Config:
 def param_layout(cfg: Config):
     """Canonical flat parameter order, each matrix row-major [in][out]."""
     T, d, e, F = cfg.T, cfg.d, cfg.e, cfg.F
+    Ls = (cfg.layers,) if cfg.layers > 1 else ()
     return [
         ("E", (256, e)),
         ("P", (T, d)),
-        ("Wq", (d, d)),
-        ("Wk", (d, d)),
-        ("Wv", (d, d)),
-        ("Wo", (d, d)),
-        ("W1", (cfg.k, d, F) if cfg.untied else (d, F)),
-        ("W2", (cfg.k, F, d) if cfg.untied else (F, d)),
+        ("Wq", Ls + (d, d)),
+        ("Wk", Ls + (d, d)),
+        ("Wv", Ls + (d, d)),
+        ("Wo", Ls + (d, d)),
+        ("W1", Ls + ((cfg.k, d, F) if cfg.untied else (d, F))),
+        ("W2", Ls + ((cfg.k, F, d) if cfg.untied else (F, d))),
         ("Wout", (d, 256)),
         ("bout", (256,)),
     ]
+
+
+_LAYER_WEIGHTS = ("Wq", "Wk", "Wv", "Wo", "W1", "W2")
+
+
+def layer_params(p: dict, cfg: Config, l: int) -> dict:
+    """Layer l's Wq .. W2 (views into p, or p's own arrays when layers = 1)."""
+    return {n: (p[n][l] if cfg.layers > 1 else p[n]) for n in _LAYER_WEIGHTS}
 
 
 def param_count(cfg: Config) -> int:
@@ -300,35 +312,20 @@ def performer_attention_weights(Qh, Kh, omega, dt):
     return (kern / np.sum(kern, axis=-1, keepdims=True)).astype(dt)
 
 
-def forward(flat: np.ndarray, cfg: Config, windows: np.ndarray, targets: np.ndarray,
-            mode: str = "fp64", keep: bool = False, features=None):
-    """Model.forward of Alg. 1 line 8, the layer of Eqs. 1-4 with the shared FFN
-    of Sec. 4.3, computed over ALL T rows with a causal mask (the head reads
-    only the last).  Returns dict with logits z [N][256], bits [N]
-    (= -log2 p(target)), and, if keep, every intermediate.  With
-    cfg.attention == "performer", `features` is the random projection omega
-    [m][dh] (one for all heads; rounded like a weight copy in bf16 mode)."""
-    m = _Mode(mode)
-    p = compute_params(flat, cfg, mode)
-    windows = np.asarray(windows, np.uint8)
-    targets = np.asarray(targets, np.int64)
-    N, T, d, H, dh = windows.shape[0], cfg.T, cfg.d, cfg.H, cfg.dh
-
-    X = embed_group(p, windows, cfg, m)                 # residual copy
-    Xo = X                                              # GEMM operand (fp32, not rounded)
-    Q = Xo @ p["Wq"]
-    K = Xo @ p["Wk"]
-    V = Xo @ p["Wv"]
+def layer_forward(q: dict, X, Xo, cfg: Config, m, om=None) -> dict:
+    """One layer of Eq. 4 over all T rows (causal): attention of Eqs. 1-2 (or
+    the Performer's) on the GEMM operand Xo with the residual X, then the FFN
+    of Eq. 3 k times (Sec. 4.3; untied per repeat for Sec. 6.3).  q holds the
+    layer's (rounded) weights.  Returns every intermediate; Y[-1] is the
+    layer's output."""
+    N, T, d, H, dh = X.shape[0], cfg.T, cfg.d, cfg.H, cfg.dh
+    Q = Xo @ q["Wq"]
+    K = Xo @ q["Wk"]
+    V = Xo @ q["Wv"]
     scale = m.dt(1.0 / math.sqrt(dh))                   # Eq. 1, per head
     causal = np.tril(np.ones((T, T), bool))
     A = np.zeros((N, H, T, T), m.dt)
     O = np.zeros((N, T, d), m.dt)
-    if cfg.attention == "performer":
-        if features is None or np.shape(features) != (cfg.m, dh):
-            raise ValueError("performer attention needs features of shape [m][dh]")
-        om = m.R(np.asarray(features, np.float32))
-    elif cfg.attention != "softmax":
-        raise ValueError(cfg.attention)
     for h in range(H):
         c = slice(h * dh, (h + 1) * dh)
         if cfg.attention == "performer":
@@ -340,24 +337,59 @@ def forward(flat: np.ndarray, cfg: Config, windows: np.ndarray, targets: np.ndar
         A[:, h] = Ah
         O[:, :, c] = np.einsum("ntu,nuc->ntc", Ah, V[:, :, c])
     Oo = m.R(O)
-    Attn = Oo @ p["Wo"]                                 # Eq. 2 projection W
+    Attn = Oo @ q["Wo"]                                 # Eq. 2 projection W
     Y = [Attn + X]                                      # Eq. 4 inner residual
     U, Yop, Gop = [], [], []
     for r in range(cfg.k):                              # Sec. 4.3, shared W1, W2 (Sec. 6.3: untied)
-        W1r = p["W1"][r] if cfg.untied else p["W1"]
-        W2r = p["W2"][r] if cfg.untied else p["W2"]
+        W1r = q["W1"][r] if cfg.untied else q["W1"]
+        W2r = q["W2"][r] if cfg.untied else q["W2"]
         yo = m.R(Y[-1])
         u = yo @ W1r
         go = m.R(gelu(u))
         Y.append(Y[-1] + go @ W2r)
         U.append(u); Yop.append(yo); Gop.append(go)
-    hk = m.R(Y[-1][:, T - 1, :])
+    return dict(X=X, Xo=Xo, Q=Q, K=K, V=V, A=A, O=O, Oo=Oo, Y=Y, U=U, Yop=Yop, Gop=Gop)
+
+
+def forward(flat: np.ndarray, cfg: Config, windows: np.ndarray, targets: np.ndarray,
+            mode: str = "fp64", keep: bool = False, features=None):
+    """Model.forward of Alg. 1 line 8: byte grouping (Sec. 4.2), then
+    cfg.layers layers of Eqs. 1-4 with the shared FFN of Sec. 4.3, each over
+    ALL T rows with a causal mask, and the head on the last row.  Layer 0's
+    projections take the token X = E + P as it is; later layers take their
+    input (the residual stream) rounded like the FFN's input (a bf16 storage
+    point).  Returns dict with logits z [N][256], bits [N] (= -log2
+    p(target)), and, if keep, every intermediate (per layer in "layers"; with
+    one layer also at the top level).  With cfg.attention == "performer",
+    `features` is the random projection omega [m][dh] (one for all heads and
+    layers; rounded like a weight copy in bf16 mode)."""
+    m = _Mode(mode)
+    p = compute_params(flat, cfg, mode)
+    windows = np.asarray(windows, np.uint8)
+    targets = np.asarray(targets, np.int64)
+    T, dh = cfg.T, cfg.dh
+    om = None
+    if cfg.attention == "performer":
+        if features is None or np.shape(features) != (cfg.m, dh):
+            raise ValueError("performer attention needs features of shape [m][dh]")
+        om = m.R(np.asarray(features, np.float32))
+    elif cfg.attention != "softmax":
+        raise ValueError(cfg.attention)
+    X = embed_group(p, windows, cfg, m)                 # residual copy
+    layers = []
+    for l in range(cfg.layers):
+        Xo = X if l == 0 else m.R(X)                    # layer 0: fp32 token, not rounded
+        c = layer_forward(layer_params(p, cfg, l), X, Xo, cfg, m, om)
+        layers.append(c)
+        X = c["Y"][-1]
+    hk = m.R(X[:, T - 1, :])
     z = hk @ p["Wout"] + p["bout"]
     bits = code_length_bits(z, targets)
     out = {"z": z, "bits": bits}
     if keep:
-        out.update(dict(p=p, X=X, Xo=Xo, Q=Q, K=K, V=V, A=A, O=O, Oo=Oo, Y=Y, U=U,
-                        Yop=Yop, Gop=Gop, hk=hk, targets=targets, mode=mode))
+        out.update(dict(p=p, layers=layers, hk=hk, targets=targets, mode=mode))
+        if cfg.layers == 1:
+            out.update(layers[0])
     return out
 
 
@@ -384,15 +416,60 @@ def stream_bits_per_byte(bits_sum: float, B: int, L: int, W: int) -> float:
 
 
 # ----------------------------------------------------------------- backward ----
+def layer_backward(c: dict, q: dict, dY, cfg: Config, m) -> tuple:
+    """Gradients of one layer (the forward of layer_forward) given dY, the
+    gradient w.r.t. its output Y_k (all rows): returns (the layer's weight
+    gradients, the gradient w.r.t. its input X)."""
+    N, T, d, H, dh = c["X"].shape[0], cfg.T, cfg.d, cfg.H, cfg.dh
+    g = {"W1": np.zeros_like(q["W1"]), "W2": np.zeros_like(q["W2"])}
+    # shared FFN, repeats in reverse; W1, W2 gradients accumulate over repeats
+    for r in reversed(range(cfg.k)):
+        # untied: repeat r's own blocks (views, so += lands in g)
+        gW1, gW2 = (g["W1"][r], g["W2"][r]) if cfg.untied else (g["W1"], g["W2"])
+        W1r, W2r = (q["W1"][r], q["W2"][r]) if cfg.untied else (q["W1"], q["W2"])
+        dYo = m.R(dY)
+        gW2 += np.einsum("ntf,ntc->fc", c["Gop"][r], dYo)
+        dG = dYo @ W2r.T
+        dU = dG * gelu_grad(c["U"][r])
+        dUo = m.R(dU)
+        gW1 += np.einsum("ntc,ntf->cf", c["Yop"][r], dUo)
+        dY = dY + dUo @ W1r.T
+    dY0 = dY
+    dY0o = m.R(dY0)
+    g["Wo"] = np.einsum("ntc,nto->co", c["Oo"], dY0o)
+    dO = m.R(dY0o @ q["Wo"].T)
+    # attention (Eq. 1 per head)
+    scale = m.dt(1.0 / math.sqrt(dh))
+    dQ = np.zeros((N, T, d), m.dt)
+    dK = np.zeros((N, T, d), m.dt)
+    dV = np.zeros((N, T, d), m.dt)
+    for h in range(H):
+        cs = slice(h * dh, (h + 1) * dh)
+        Ah = c["A"][:, h]
+        dA = np.einsum("ntc,nuc->ntu", dO[:, :, cs], c["V"][:, :, cs])
+        dV[:, :, cs] = np.einsum("ntu,ntc->nuc", Ah, dO[:, :, cs])
+        dS = Ah * (dA - np.sum(dA * Ah, axis=-1, keepdims=True))
+        dQ[:, :, cs] = np.einsum("ntu,nuc->ntc", dS, c["K"][:, :, cs]) * scale
+        dK[:, :, cs] = np.einsum("ntu,ntc->nuc", dS, c["Q"][:, :, cs]) * scale
+    Xo = c["Xo"]
+    g["Wq"] = np.einsum("ntc,nto->co", Xo, dQ)
+    g["Wk"] = np.einsum("ntc,nto->co", Xo, dK)
+    g["Wv"] = np.einsum("ntc,nto->co", Xo, dV)
+    dX = dQ @ q["Wq"].T + dK @ q["Wk"].T + dV @ q["Wv"].T + dY0
+    return g, dX
+
+
 def backward(cache: dict, cfg: Config) -> dict:
     """Gradient of L = (1/N) sum_n CE_nats[n] w.r.t. every parameter (Alg. 1
-    line 10), by the chain rule through the forward above.  All T rows are
-    carried; only the last row of Y_k receives an upstream gradient."""
+    line 10), by the chain rule through the forward above, layer by layer from
+    the top.  All T rows are carried; only the last row of the top layer's
+    output receives an upstream gradient from the head."""
     if cfg.attention != "softmax":
         raise NotImplementedError("the backward covers softmax attention (Eqs. 1-2) only")
     m = _Mode(cache["mode"])
     p = cache["p"]
-    N, T, d, H, dh = cache["X"].shape[0], cfg.T, cfg.d, cfg.H, cfg.dh
+    layers = cache["layers"]
+    N, T, d = layers[0]["X"].shape[0], cfg.T, cfg.d
     y = cache["targets"]
     z = cache["z"]
     g = {}
@@ -404,44 +481,15 @@ def backward(cache: dict, cfg: Config) -> dict:
     dzo = m.R(dz)
     g["Wout"] = cache["hk"].T @ dzo
     g["bout"] = dz.sum(axis=0)
-    dY = np.zeros((N, T, d), m.dt)
-    dY[:, T - 1, :] = dzo @ p["Wout"].T
-    # shared FFN, repeats in reverse; W1, W2 gradients accumulate over repeats
-    g["W1"] = np.zeros_like(p["W1"])
-    g["W2"] = np.zeros_like(p["W2"])
-    for r in reversed(range(cfg.k)):
-        # untied: repeat r's own blocks (views, so += lands in g)
-        gW1, gW2 = (g["W1"][r], g["W2"][r]) if cfg.untied else (g["W1"], g["W2"])
-        W1r, W2r = (p["W1"][r], p["W2"][r]) if cfg.untied else (p["W1"], p["W2"])
-        dYo = m.R(dY)
-        gW2 += np.einsum("ntf,ntc->fc", cache["Gop"][r], dYo)
-        dG = dYo @ W2r.T
-        dU = dG * gelu_grad(cache["U"][r])
-        dUo = m.R(dU)
-        gW1 += np.einsum("ntc,ntf->cf", cache["Yop"][r], dUo)
-        dY = dY + dUo @ W1r.T
-    dY0 = dY
-    dY0o = m.R(dY0)
-    g["Wo"] = np.einsum("ntc,nto->co", cache["Oo"], dY0o)
-    dO = m.R(dY0o @ p["Wo"].T)
-    # attention (Eq. 1 per head)
-    scale = m.dt(1.0 / math.sqrt(dh))
-    dQ = np.zeros((N, T, d), m.dt)
-    dK = np.zeros((N, T, d), m.dt)
-    dV = np.zeros((N, T, d), m.dt)
-    for h in range(H):
-        c = slice(h * dh, (h + 1) * dh)
-        Ah = cache["A"][:, h]
-        dA = np.einsum("ntc,nuc->ntu", dO[:, :, c], cache["V"][:, :, c])
-        dV[:, :, c] = np.einsum("ntu,ntc->nuc", Ah, dO[:, :, c])
-        dS = Ah * (dA - np.sum(dA * Ah, axis=-1, keepdims=True))
-        dQ[:, :, c] = np.einsum("ntu,nuc->ntc", dS, cache["K"][:, :, c]) * scale
-        dK[:, :, c] = np.einsum("ntu,ntc->nuc", dS, cache["Q"][:, :, c]) * scale
-    Xo = cache["Xo"]
-    g["Wq"] = np.einsum("ntc,nto->co", Xo, dQ)
-    g["Wk"] = np.einsum("ntc,nto->co", Xo, dK)
-    g["Wv"] = np.einsum("ntc,nto->co", Xo, dV)
-    dX = dQ @ p["Wq"].T + dK @ p["Wk"].T + dV @ p["Wv"].T + dY0
+    dX = np.zeros((N, T, d), m.dt)
+    dX[:, T - 1, :] = dzo @ p["Wout"].T
+    for n in _LAYER_WEIGHTS:
+        g[n] = np.zeros_like(p[n])
+    for l in reversed(range(cfg.layers)):
+        gl, dX = layer_backward(layers[l], layer_params(p, cfg, l), dX, cfg, m)
+        dst = layer_params(g, cfg, l)
+        for n in _LAYER_WEIGHTS:
+            dst[n][...] = gl[n]
     g["P"] = dX.sum(axis=0) if cfg.use_pos else np.zeros_like(p["P"])
     # embedding: byte j of token t read E[w] into dims [j*e, (j+1)*e)
     gE = np.zeros_like(p["E"])

@@ -415,3 +415,73 @@ def test_structured_weights_show_every_slot_exactly(shape):
         sw[:, [t * cfg.g, t * cfg.g + 1]] = sw[:, [t * cfg.g + 1, t * cfg.g]]
         diff = np.any(expected(sw) != want, axis=1)
         assert np.array_equal(diff, w[:, t * cfg.g] != w[:, t * cfg.g + 1])
+
+
+# ---------------------------------------------------------------- layers > 1
+@pytest.mark.parametrize("cfg", [O.Config(W=8, e=4, g=2, H=2, F=12, k=2, layers=2),
+                                 O.Config(W=8, e=4, g=2, H=2, F=12, k=2, layers=3, use_pos=False),
+                                 O.Config(W=8, e=4, g=2, H=2, F=12, k=2, layers=2, untied=True)])
+def test_multilayer_gradients_match_central_finite_differences(cfg):
+    flat = _flat(cfg, 41, 0.4).astype(np.float64)
+    w, y = synth.random_windows(42, 5, cfg.W)
+    _, g = O.forward_backward(flat, cfg, w, y, "fp64")
+    gflat = O.flatten(g, cfg)
+    # central differences carry a round-off of about 1e-16 |loss| / h
+    floor = 2e-9 * max(1.0, O.loss_nats(flat, cfg, w, y))
+    r = np.random.default_rng(43)
+    off = 0
+    for name, shape in O.param_layout(cfg):
+        n = int(np.prod(shape))
+        if name == "E":
+            rows = np.unique(w)
+            idx = [int(rows[r.integers(len(rows))]) * cfg.e + int(r.integers(cfg.e)) for _ in range(6)]
+        else:
+            idx = r.choice(n, size=min(8, n), replace=False)
+        for i in idx:
+            j = off + int(i)
+            h = 1e-6 * max(1.0, abs(flat[j]))
+            fp = flat.copy(); fp[j] += h
+            fm = flat.copy(); fm[j] -= h
+            fd = (O.loss_nats(fp, cfg, w, y) - O.loss_nats(fm, cfg, w, y)) / (2 * h)
+            assert abs(fd - gflat[j]) <= 1e-6 * abs(gflat[j]) + floor, (name, i, fd, gflat[j])
+        off += n
+
+
+def test_pass_through_layer_and_layer_count():
+    """A layer with Wv = Wo = W2 = 0 adds exactly zero to its input (Eq. 4's
+    two residuals carry it through), so a 2-layer model whose first layer is
+    one computes the 1-layer model with the second layer's weights; the
+    parameter count grows by one set of Wq .. W2 per layer."""
+    one = O.Config(W=16, e=8, g=4, H=2, F=32, k=2)
+    two = O.Config(W=16, e=8, g=4, H=2, F=32, k=2, layers=2)
+    f1 = _flat(one, 44, 0.2).astype(np.float64)
+    p1 = O.unflatten(f1, one)
+    p2 = {n: np.array(v) for n, v in p1.items()}
+    rng = np.random.default_rng(45)
+    for n in ("Wq", "Wk", "Wv", "Wo", "W1", "W2"):
+        first = rng.standard_normal(p1[n].shape) * 0.2
+        if n in ("Wv", "Wo", "W2"):
+            first[:] = 0
+        p2[n] = np.stack([first, p1[n]])
+    f2 = O.flatten(p2, two, np.float64)
+    assert f2.size == O.param_count(one) + 4 * 32 * 32 + 2 * 32 * 32
+    w, y = synth.random_windows(46, 7, 16)
+    a = O.forward(f1, one, w, y, "fp64")
+    b = O.forward(f2, two, w, y, "fp64", keep=True)
+    np.testing.assert_allclose(b["z"], a["z"], rtol=1e-12, atol=1e-12)
+    np.testing.assert_array_equal(b["layers"][0]["Y"][-1], b["layers"][0]["X"])
+
+
+def test_multilayer_rows_are_causal():
+    """Row t of every layer's output depends only on tokens u <= t."""
+    cfg = O.Config(W=16, e=8, g=4, H=2, F=32, k=1, layers=3)
+    flat = _flat(cfg, 47, 0.3).astype(np.float64)
+    w, y = synth.random_windows(48, 4, 16)
+    a = O.forward(flat, cfg, w, y, "fp64", keep=True)
+    for t in range(cfg.T - 1):
+        w2 = w.copy()
+        w2[:, (t + 1) * cfg.g:] ^= 0x33               # every token after t changes
+        b = O.forward(flat, cfg, w2, y, "fp64", keep=True)
+        for l in range(cfg.layers):
+            np.testing.assert_array_equal(b["layers"][l]["Y"][-1][:, :t + 1], a["layers"][l]["Y"][-1][:, :t + 1])
+        assert not np.allclose(b["layers"][-1]["Y"][-1][:, t + 1:], a["layers"][-1]["Y"][-1][:, t + 1:])
