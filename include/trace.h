@@ -92,6 +92,13 @@ typedef struct {
    * trace_set_features before the first forward. */
   int32_t attention;
   int32_t n_features;
+  /* layers of Eq. 4 stacked (Sec. 6.3, Fig. 7; 0 or 1: one layer, the
+   * estimator of the workloads), at most 8; each has its own Wq, Wk, Wv, Wo,
+   * W1, W2, stored in the flat order as `layers` consecutive blocks of each
+   * (layer l's Wq at l * d * d within Wq's span).  Layer 0 reads the tokens
+   * X = E + P; later layers read the previous layer's output, rounded like an
+   * FFN input in bf16 models.  Softmax attention only. */
+  int32_t layers;
   int32_t reserved_; /* 0 */
 } trace_config;
 

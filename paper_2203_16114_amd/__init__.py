@@ -43,7 +43,8 @@ class TraceConfig(ctypes.Structure):
     _fields_ = [("W", c_int32), ("e", c_int32), ("g", c_int32), ("H", c_int32), ("F", c_int32), ("k", c_int32),
                 ("dtype", c_int32), ("use_pos", c_int32), ("max_windows", c_int64), ("max_keep", c_int64),
                 ("lr", c_double), ("beta1", c_double), ("beta2", c_double), ("eps", c_double),
-                ("untied_ffn", c_int32), ("attention", c_int32), ("n_features", c_int32), ("reserved_", c_int32)]
+                ("untied_ffn", c_int32), ("attention", c_int32), ("n_features", c_int32), ("layers", c_int32),
+                ("reserved_", c_int32)]
 
 
 class TraceControllerState(ctypes.Structure):
@@ -118,12 +119,12 @@ def check(rc: int):
 
 def make_config(W, e, g, H, F, k, dtype="fp32", use_pos=True, max_windows=1 << 16, max_keep=0,
                 lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, untied_ffn=False, attention="softmax",
-                n_features=0) -> TraceConfig:
+                n_features=0, layers=1) -> TraceConfig:
     dt = {"fp32": TRACE_FP32, "bf16": TRACE_BF16}[dtype] if isinstance(dtype, str) else int(dtype)
     att = {"softmax": TRACE_ATTN_SOFTMAX, "performer": TRACE_ATTN_PERFORMER}[attention]
     return TraceConfig(W, e, g, H, F, k, dt, int(bool(use_pos)), int(max_windows), int(max_keep),
                        float(lr), float(beta1), float(beta2), float(eps), int(bool(untied_ffn)), att,
-                       int(n_features), 0)
+                       int(n_features), int(layers), 0)
 
 
 def param_count(cfg: TraceConfig) -> int:
@@ -232,9 +233,11 @@ class TraceModel:
     """One model on the current HIP device (see include/trace.h)."""
 
     def __init__(self, W, e, g, H, F, k, dtype="fp32", use_pos=True, max_windows=1 << 16, max_keep=0,
-                 lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, untied_ffn=False, attention="softmax", n_features=0):
+                 lr=1e-3, beta1=0.9, beta2=0.999, eps=1e-8, untied_ffn=False, attention="softmax", n_features=0,
+                 layers=1):
         self.cfg = make_config(W, e, g, H, F, k, dtype, use_pos, max_windows, max_keep, lr, beta1, beta2, eps,
-                               untied_ffn, attention, n_features)
+                               untied_ffn, attention, n_features, layers)
+        self.layers = layers
         self.attention = attention
         self.W, self.e, self.g, self.H, self.F, self.k = W, e, g, H, F, k
         self.T, self.d = W // g, g * e

@@ -25,7 +25,7 @@ HIP_FLAGS = ["--offload-arch=" + ARCH, "-O3", "-fPIC", "-std=c++17",
              "-Wno-unused-result"]
 HOST_FLAGS = ["-O2", "-fPIC", "-std=c++17", "-ffp-contract=off", "-fno-fast-math"]
 
-HIP_SOURCES = ["fwd.hip", "attn.hip", "ffn.hip", "bwd.hip", "bgemm.hip", "codec.hip", "noalloc.hip", "api.cpp"]
+HIP_SOURCES = ["fwd.hip", "attn.hip", "ffn.hip", "bwd.hip", "bgemm.hip", "codec.hip", "noalloc.hip", "layers.hip", "api.cpp"]
 HOST_SOURCES = ["host.cpp"]
 
 

@@ -34,6 +34,14 @@ struct trace_model {
   bool feats_set;
   // forward workspace
   float* h0;
+  // stacked layers: the lower layers' forward buffers (per chunk of lcap
+  // windows) and split-K workspace; kept activations of every lower layer
+  // (klX: the input of every layer, the top's included) and their backward
+  // buffers
+  int64_t lcap, fws_cap;
+  float *lx[2], *lq, *lk, *lv, *lo, *ly[2], *lu, *lg, *fws;
+  float *klX, *klQ, *klK, *klV, *klA, *klO, *klY, *klU;
+  float *ldY, *ldU, *ldG, *ldO, *ldQ;
   // kept batch
   bool kept;
   int64_t keepN;
@@ -117,8 +125,16 @@ void order(trace_model* m, hipStream_t from, hipStream_t to) { after(to, mark(m,
 std::vector<std::array<int, 3>> adapt_gemm_shapes(const trace_model* m, int64_t N) {
   const int D = m->L.D, F = m->cfg.F, T = m->L.T;
   const int n = (int)N;
-  return {{D, 256, n}, {n, D, 256}, {F, D, n}, {n, F, D}, {D, F, n},
-          {n, D, F},   {D, D, n},   {n, D, D}, {D, D, n * T}, {n * T, D, D}, {n * T, D, 2 * D}};
+  std::vector<std::array<int, 3>> v = {{D, 256, n}, {n, D, 256}, {F, D, n},     {n, F, D},
+                                       {D, F, n},   {n, D, F},   {D, D, n},     {n, D, D},
+                                       {D, D, n * T}, {n * T, D, D}, {n * T, D, 2 * D}};
+  if (m->L.NL > 1) {  // the lower layers' products run over every token row
+    const int r = n * T;
+    for (std::array<int, 3> x : std::vector<std::array<int, 3>>{
+             {r, F, D}, {F, D, r}, {D, F, r}, {r, D, F}, {D, D, r}, {r, D, D}})
+      v.push_back(x);
+  }
+  return v;
 }
 // Largest split-K workspace (floats) over those GEMMs, for either GEMM path.
 int64_t adapt_gemm_ws(const trace_model* m, int64_t N) {
@@ -204,19 +220,25 @@ bool refresh_operands(trace_model* m, hipStream_t s) {
     j.scale = scale;
     return j;
   };
-  RefreshJob pt = job(RJ_PTAB, th + L.off[P_P], m->PW, L.T, D);
-  pt.src2 = th + L.off[P_WQ];  // W_q, W_k, W_v are consecutive D x D blocks of the master
-  pt.use_pos = pos;
+  // the fused kernels run the top layer (the only layer when NL = 1); with
+  // stacked layers its input carries no positional part, so P.W is zero
+  const int top = L.NL - 1;
+  RefreshJob pt = L.NL > 1 ? job(RJ_ZERO, nullptr, m->PW, 3 * (int64_t)L.T * D, 0)
+                           : job(RJ_PTAB, th + L.off[P_P], m->PW, L.T, D);
+  if (L.NL == 1) {
+    pt.src2 = th + L.off[P_WQ];  // W_q, W_k, W_v are consecutive D x D blocks of the master
+    pt.use_pos = pos;
+  }
   // the positional table's blocks run longest: they are dispatched first
   const RefreshJob jobs[] = {
       pt,
-      job(RJ_PACK, th + L.off[P_W1], m->W1, D, F),
+      job(RJ_PACK, th + L.at(P_W1, top), m->W1, D, F),
       // bf16: W2/2 (exact), since the bf16 FFN kernel forms 2 GELU(U) (exact in bf16 too)
-      job(RJ_PACK, th + L.off[P_W2], m->W2, F, D, m->bf ? 0.5f : 1.f),
-      job(RJ_PACK, th + L.off[P_WQ], m->Wq, D, D),
-      job(RJ_PACK, th + L.off[P_WK], m->Wk, D, D),
-      job(RJ_PACK, th + L.off[P_WV], m->Wv, D, D),
-      job(RJ_PACK, th + L.off[P_WO], m->Wo, D, D),
+      job(RJ_PACK, th + L.at(P_W2, top), m->W2, F, D, m->bf ? 0.5f : 1.f),
+      job(RJ_PACK, th + L.at(P_WQ, top), m->Wq, D, D),
+      job(RJ_PACK, th + L.at(P_WK, top), m->Wk, D, D),
+      job(RJ_PACK, th + L.at(P_WV, top), m->Wv, D, D),
+      job(RJ_PACK, th + L.at(P_WO, top), m->Wo, D, D),
       job(RJ_PACK, th + L.off[P_WOUT], m->Wout, D, 256),
       job(RJ_CVT, th + L.off[P_E], m->Ec, L.size[P_E], 0),
       pos ? job(RJ_CVT, th + L.off[P_P], m->Pc, L.size[P_P], 0)
@@ -227,8 +249,8 @@ bool refresh_operands(trace_model* m, hipStream_t s) {
   const int64_t es_ = m->bf ? 2 : 4;
   for (int r = 1; ok && m->cfg.untied_ffn && r < m->cfg.k; ++r) {
     const RefreshJob more[] = {
-        job(RJ_PACK, th + L.off[P_W1] + (int64_t)r * D * F, (char*)m->W1 + (int64_t)r * D * F * es_, D, F),
-        job(RJ_PACK, th + L.off[P_W2] + (int64_t)r * F * D, (char*)m->W2 + (int64_t)r * F * D * es_, F, D,
+        job(RJ_PACK, th + L.at(P_W1, top) + (int64_t)r * D * F, (char*)m->W1 + (int64_t)r * D * F * es_, D, F),
+        job(RJ_PACK, th + L.at(P_W2, top) + (int64_t)r * F * D, (char*)m->W2 + (int64_t)r * F * D * es_, F, D,
             m->bf ? 0.5f : 1.f)};
     ok = launch_refresh(m->bf, more, 2, s);
   }
@@ -256,6 +278,129 @@ GemmArgs gemm(int M, int N, int K, const float* A, int64_t sam, int64_t sak, int
   g.gelu_u = nullptr;
   g.halfA = g.halfB = g.halfC = 0;
   return g;
+}
+
+// Kept activations of lower layer l of a KEEP_ACTS forward (NULL: not kept).
+struct LowerKeep {
+  float *Q, *K, *V, *A, *O, *Y, *U;  // Y: inputs of the k FFN repeats; U: their pre-GELU values
+  int64_t ys, us;                    // floats between repeats in Y and in U
+};
+LowerKeep lower_keep(const trace_model* m, int l) {
+  LowerKeep k;
+  const int64_t R = m->max_keep * m->L.T, D = m->L.D, F = m->cfg.F, kk = m->cfg.k;
+  k.ys = R * D;
+  k.us = R * F;
+  k.Q = m->klQ + l * R * D;
+  k.K = m->klK + l * R * D;
+  k.V = m->klV + l * R * D;
+  k.A = m->klA + l * m->max_keep * m->cfg.H * m->L.T * m->L.T;
+  k.O = m->klO + l * R * D;
+  k.Y = m->klY + l * kk * R * D;
+  k.U = m->klU + l * kk * R * F;
+  return k;
+}
+
+// Lower layer l (every token row) of the forward over N windows: X -> Xn,
+// X and Xn [N][T][D] fp32.  The products are GEMMs on the update's kernels
+// (layer 0 reads the token X = E + P as it is: split into two bf16 parts in
+// bf16 models; later layers read their input rounded, a bf16 storage point).
+// With kp, every intermediate the backward needs is written there.
+bool lower_forward(trace_model* m, int l, const float* X, float* Xn, int64_t N, const LowerKeep* kp, hipStream_t s) {
+  const Layout& L = m->L;
+  const int T = L.T, D = L.D, F = m->cfg.F, H = m->cfg.H, k = m->cfg.k;
+  const int rb = m->bf ? 1 : 0, rX = (l == 0) ? 0 : rb;
+  const int R = (int)(N * T);
+  const float* th = m->theta;
+  float* ws = m->fws;
+  const int64_t cap = m->fws_cap;
+  float* Q = kp ? kp->Q : m->lq;
+  float* K = kp ? kp->K : m->lk;
+  float* V = kp ? kp->V : m->lv;
+  float* O = kp ? kp->O : m->lo;
+  bool ok = true;
+  ok = launch_gemm(gemm(R, D, D, X, D, 1, rX, th + L.at(P_WQ, l), D, 1, rb, Q, D, 0.f), ws, cap, s) && ok;
+  ok = launch_gemm(gemm(R, D, D, X, D, 1, rX, th + L.at(P_WK, l), D, 1, rb, K, D, 0.f), ws, cap, s) && ok;
+  ok = launch_gemm(gemm(R, D, D, X, D, 1, rX, th + L.at(P_WV, l), D, 1, rb, V, D, 0.f), ws, cap, s) && ok;
+  launch_attn_rows(Q, K, V, N, T, D, H, (float)(1.0 / std::sqrt((double)L.DH)), rb, O, kp ? kp->A : nullptr, s);
+  // Y_0 = O.Wo + X, then Y_r = Y_{r-1} + G(Y_{r-1} W1) W2 (each sum: copy, then
+  // a product accumulated onto it)
+  const float* Yin = kp ? kp->Y : m->ly[0];
+  (void)hipMemcpyAsync((void*)Yin, X, (size_t)R * D * 4, hipMemcpyDeviceToDevice, s);
+  ok = launch_gemm(gemm(R, D, D, O, D, 1, rb, th + L.at(P_WO, l), D, 1, rb, (float*)Yin, D, 1.f), ws, cap, s) && ok;
+  for (int r = 0; r < k; ++r) {
+    const int64_t wr = m->cfg.untied_ffn ? (int64_t)r * D * F : 0;
+    float* U = kp ? kp->U + r * kp->us : m->lu;
+    ok = launch_gemm(gemm(R, F, D, Yin, D, 1, rb, th + L.at(P_W1, l) + wr, F, 1, rb, U, F, 0.f), ws, cap, s) && ok;
+    launch_gelu_fwd_round(U, m->lg, (int64_t)R * F, rb, s);
+    float* Yout = r == k - 1 ? Xn : (kp ? kp->Y + (r + 1) * kp->ys : m->ly[(r + 1) & 1]);
+    (void)hipMemcpyAsync(Yout, Yin, (size_t)R * D * 4, hipMemcpyDeviceToDevice, s);
+    ok = launch_gemm(gemm(R, D, F, m->lg, F, 1, rb, th + L.at(P_W2, l) + wr, D, 1, rb, Yout, D, 1.f), ws, cap, s) &&
+         ok;
+    Yin = Yout;
+  }
+  return ok;
+}
+
+// Backward of lower layer l over every token row: on entry m->dX holds the
+// gradient w.r.t. the layer's output [N][T][D], on return w.r.t. its input.
+// The chain of layer_backward in the oracle, with the layer's weight
+// gradients written at layer l's blocks; layer 0's projection gradients take
+// the token X = E + P as G^T dZ (G = the byte-embedding part, bf16 exact in
+// Xk) plus P^T (sum over windows of dZ), later layers' their rounded input.
+bool lower_backward(trace_model* m, int l, int64_t N64, hipStream_t s) {
+  const Layout& L = m->L;
+  const int T = L.T, D = L.D, F = m->cfg.F, H = m->cfg.H, k = m->cfg.k, N = (int)N64;
+  const int rb = m->bf ? 1 : 0, hf = m->bf ? 1 : 0;
+  const int R = N * T;
+  const float* th = m->theta;
+  float* gr = m->grad;
+  float* ws = m->gws;
+  const int64_t cap = m->gws_cap;
+  const LowerKeep kp = lower_keep(m, l);
+  const float* X = m->klX + (int64_t)l * m->max_keep * T * D;
+  float* dY = m->ldY;
+  bool ok = true;
+  (void)hipMemcpyAsync(dY, m->dX, (size_t)R * D * 4, hipMemcpyDeviceToDevice, s);
+  for (int r = k - 1; r >= 0; --r) {
+    const int64_t wr = m->cfg.untied_ffn ? (int64_t)r * D * F : 0;
+    const float beta = (r == k - 1 || m->cfg.untied_ffn) ? 0.f : 1.f;
+    const float* U = kp.U + r * kp.us;
+    const float* Y = kp.Y + r * kp.ys;
+    GemmArgs gd = gemm(R, F, D, dY, D, 1, rb, th + L.at(P_W2, l) + wr, 1, D, rb, m->ldU, F, 0.f);
+    gd.gelu_u = U;
+    ok = launch_gemm(gd, ws, cap, s) && ok;
+    launch_gelu_fwd_round(U, m->ldG, (int64_t)R * F, rb, s);
+    ok = launch_gemm(gemm(F, D, R, m->ldG, 1, F, rb, dY, D, 1, rb, gr + L.at(P_W2, l) + wr, D, beta), ws, cap, s) &&
+         ok;
+    ok = launch_gemm(gemm(D, F, R, Y, 1, D, rb, m->ldU, F, 1, rb, gr + L.at(P_W1, l) + wr, F, beta), ws, cap, s) && ok;
+    ok = launch_gemm(gemm(R, D, F, m->ldU, F, 1, rb, th + L.at(P_W1, l) + wr, 1, F, rb, dY, D, 1.f), ws, cap, s) && ok;
+  }
+  // dY is now dY_0: dWo = O^T dY_0, dO = dY_0 Wo^T, attention over every row
+  ok = launch_gemm(gemm(D, D, R, kp.O, 1, D, rb, dY, D, 1, rb, gr + L.at(P_WO, l), D, 0.f), ws, cap, s) && ok;
+  ok = launch_gemm(gemm(R, D, D, dY, D, 1, rb, th + L.at(P_WO, l), 1, D, rb, m->ldO, D, 0.f), ws, cap, s) && ok;
+  launch_attn_bwd_rows(m->ldO, kp.Q, kp.K, kp.V, kp.A, N, T, D, H, (float)(1.0 / std::sqrt((double)L.DH)), rb,
+                       m->ldQ, m->dK, m->dV, s);
+  const float* dZ[3] = {m->ldQ, m->dK, m->dV};
+  const int pz[3] = {P_WQ, P_WK, P_WV};
+  for (int i = 0; i < 3; ++i) {
+    if (l == 0) {
+      GemmArgs g = gemm(D, D, R, m->Xk, 1, D, rb, dZ[i], D, 1, 0, gr + L.at(pz[i], l), D, 0.f);
+      g.halfA = hf;
+      ok = launch_gemm(g, ws, cap, s) && ok;
+      if (m->cfg.use_pos) {
+        launch_colsum(dZ[i], N, (int64_t)T * D, (int64_t)T * D, m->sP, 0.f, m->cws, s);
+        launch_pos_grad(m->bf, m->Pc, m->sP, 0, T, D, gr + L.at(pz[i], l), s);
+      }
+    } else {
+      ok = launch_gemm(gemm(D, D, R, X, 1, D, rb, dZ[i], D, 1, 0, gr + L.at(pz[i], l), D, 0.f), ws, cap, s) && ok;
+    }
+  }
+  // dX = dQ Wq^T + dK Wk^T + dV Wv^T + dY_0
+  launch_gemm2(gemm(R, D, D, m->dK, D, 1, 0, th + L.at(P_WK, l), 1, D, rb, m->dX, D, 0.f),
+               gemm(R, D, D, m->dV, D, 1, 0, th + L.at(P_WV, l), 1, D, rb, m->dX, D, 0.f), ws, cap, s);
+  ok = launch_gemm(gemm(R, D, D, m->ldQ, D, 1, 0, th + L.at(P_WQ, l), 1, D, rb, m->dX, D, 1.f), ws, cap, s) && ok;
+  launch_add(m->dX, dY, R, D, D, D, s);
+  return ok;
 }
 
 }  // namespace
@@ -299,7 +444,32 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
             dalloc(m, &m->W2, F * D * es * (cfg->untied_ffn ? cfg->k : 1)) &&
             dalloc(m, &m->Wout, D * 256 * es) && dalloc(m, &m->h0, m->max_windows * D * 4) &&
             (m->nfeat == 0 || dalloc(m, &m->Om, (int64_t)m->nfeat * L.DH * es));
+  const int NL = L.NL, H = cfg->H, kk = cfg->k;
+  if (ok && NL > 1) {
+    // windows per forward chunk: the lower layers hold about T (7 D + 2 F)
+    // floats per window
+    m->lcap = std::max<int64_t>(std::min<int64_t>(m->max_windows, 16384), cfg->max_keep);
+    const int64_t R = m->lcap * T;  // token rows
+    m->fws_cap = 0;
+    for (int64_t kd : {D, F})
+      for (int64_t nd : {D, F})
+        m->fws_cap = std::max(m->fws_cap, std::max(gemm_ws_floats((int)R, (int)nd, (int)kd),
+                                                   bgemm_ws_floats((int)R, (int)nd, (int)kd)));
+    ok = dalloc(m, &m->lx[0], R * D * 4) && dalloc(m, &m->lx[1], R * D * 4) && dalloc(m, &m->lq, R * D * 4) &&
+         dalloc(m, &m->lk, R * D * 4) && dalloc(m, &m->lv, R * D * 4) && dalloc(m, &m->lo, R * D * 4) &&
+         dalloc(m, &m->ly[0], R * D * 4) && dalloc(m, &m->ly[1], R * D * 4) && dalloc(m, &m->lu, R * F * 4) &&
+         dalloc(m, &m->lg, R * F * 4) && dalloc(m, &m->fws, m->fws_cap * 4);
+  }
   const int64_t K = cfg->max_keep;
+  if (ok && K > 0 && NL > 1) {
+    const int64_t R = K * T, nl = NL - 1;
+    ok = dalloc(m, &m->klX, NL * R * D * 4) && dalloc(m, &m->klQ, nl * R * D * 4) &&
+         dalloc(m, &m->klK, nl * R * D * 4) && dalloc(m, &m->klV, nl * R * D * 4) &&
+         dalloc(m, &m->klA, nl * K * H * T * T * 4) && dalloc(m, &m->klO, nl * R * D * 4) &&
+         dalloc(m, &m->klY, nl * kk * R * D * 4) && dalloc(m, &m->klU, nl * kk * R * F * 4) &&
+         dalloc(m, &m->ldY, R * D * 4) && dalloc(m, &m->ldU, R * F * 4) && dalloc(m, &m->ldG, R * F * 4) &&
+         dalloc(m, &m->ldO, R * D * 4) && dalloc(m, &m->ldQ, R * D * 4);
+  }
   if (ok && K > 0) {
     ok = dalloc(m, &m->kwin, K * W) && dalloc(m, &m->ktgt, K * 4) && dalloc(m, &m->kq, K * D * 4) &&
          dalloc(m, &m->kK, K * T * D * 4) && dalloc(m, &m->kV, K * T * D * 4) &&
@@ -464,9 +634,10 @@ int trace_forward_into(trace_model* m, const uint8_t* d_streams, int64_t stride,
   if (m->nfeat && !m->feats_set) return fail(TRACE_ESTATE, "Performer features not set (trace_set_features)");
   const hipStream_t s = S(stream);
   const Layout& L = m->L;
-  const int64_t chunk = keep ? total : chunk_cap;
+  const int64_t chunk = keep ? total : (L.NL > 1 ? std::min(chunk_cap, m->lcap) : chunk_cap);
   const bool was_timing = m->timing;
   if (!timed) m->timing = false;
+  bool lok = true;
   for (int64_t n0 = 0; n0 < total; n0 += chunk) {
     WinArgs w;
     w.streams = d_streams;
@@ -488,7 +659,21 @@ int trace_forward_into(trace_model* m, const uint8_t* d_streams, int64_t stride,
     a.Wv = m->Wv;
     a.Wo = m->Wo;
     a.h0 = h0;
-    a.token_only = (flags & TRACE_TOKEN_ATTN) != 0 || m->nfeat != 0;
+    a.token_only = (flags & TRACE_TOKEN_ATTN) != 0 || m->nfeat != 0 || L.NL > 1;
+    if (L.NL > 1) {  // the lower layers over every token row; the top reads their output
+      const int64_t R = w.N * L.T;
+      float* X = keep ? m->klX : m->lx[0];
+      launch_tokens(m->bf, w, m->Ec, m->Pc, L.T, L.D, m->cfg.e, m->cfg.g, X, s);
+      for (int l = 0; l + 1 < L.NL; ++l) {
+        LowerKeep kp;
+        if (keep) kp = lower_keep(m, l);
+        float* Xn = keep ? m->klX + (int64_t)(l + 1) * m->max_keep * L.T * L.D : m->lx[(l + 1) & 1];
+        lok = lower_forward(m, l, X, Xn, w.N, keep ? &kp : nullptr, s) && lok;
+        X = Xn;
+        (void)R;
+      }
+      a.Xin = X;
+    }
     a.Om = m->nfeat ? m->Om : nullptr;
     a.nfeat = m->nfeat;
     a.scale = (float)(1.0 / std::sqrt((double)L.DH));
@@ -532,6 +717,7 @@ int trace_forward_into(trace_model* m, const uint8_t* d_streams, int64_t stride,
     tend(m, tk, TRACE_KIND_STEP_CE, s);
   }
   m->timing = was_timing;
+  if (!lok) return fail(TRACE_EUNSUPPORTED, "a lower layer's product does not fit the GEMM kernels");
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "trace_forward_bits");
   if (keep) {
@@ -585,6 +771,11 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // bf16 element e of a buffer whose elements are bf16 (hf) or fp32
   auto at = [&](float* p, int64_t e) { return hf ? (float*)((uint16_t*)p + e) : p + e; };
   auto dUr = [&](int r) { return at(m->dU, (int64_t)r * N * F); };
+  // stacked layers: this sequence runs the top layer (its weights at layer
+  // NL - 1, its input the kept output of the layers below), then
+  // lower_backward runs each lower layer down to the tokens
+  const int NL = L.NL, top = NL - 1;
+  const float* Xtop = NL > 1 ? m->klX + (int64_t)top * m->max_keep * T * D : nullptr;
   // head: dz = (softmax(z) - onehot) / N
   launch_ce_grad(m->kZ, m->ktgt, N, m->dz, s);
   order(m, s, w);
@@ -606,7 +797,7 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   for (int r = k - 1; r >= 0; --r) {
     // untied FFN: repeat r's own W1, W2 and gradient blocks (each written once)
     const int64_t wr = m->cfg.untied_ffn ? (int64_t)r * D * F : 0;
-    GemmArgs gd = gemm(N, F, D, dYr(r + 1), D, 1, rb, th + L.off[P_W2] + wr, 1, D, rb, dUr(r), F, 0.f);
+    GemmArgs gd = gemm(N, F, D, dYr(r + 1), D, 1, rb, th + L.at(P_W2, top) + wr, 1, D, rb, dUr(r), F, 0.f);
     gd.gelu_u = m->kU + (int64_t)r * N * F;
     gd.halfC = hf;
     ok = launch_gemm(gd, ws, m->gws_cap, s) && ok;
@@ -615,27 +806,27 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
     GemmArgs g2w;
     if (m->kG) {
       g2w = gemm(F, D, N, (const float*)(m->kG + (int64_t)r * N * F), 1, F, rb, dYr(r + 1), D, 1, rb,
-                 gr + L.off[P_W2] + wr, D, beta);
+                 gr + L.at(P_W2, top) + wr, D, beta);
       g2w.halfA = 1;
     } else {
       launch_gelu_fwd_round(m->kU + (int64_t)r * N * F, m->G, (int64_t)N * F, rb, w);
-      g2w = gemm(F, D, N, m->G, 1, F, rb, dYr(r + 1), D, 1, rb, gr + L.off[P_W2] + wr, D, beta);
+      g2w = gemm(F, D, N, m->G, 1, F, rb, dYr(r + 1), D, 1, rb, gr + L.at(P_W2, top) + wr, D, beta);
     }
     ok = launch_gemm(g2w, ws2, m->gws_cap, w) && ok;
-    GemmArgs g1w = gemm(D, F, N, at(m->kY, (int64_t)r * N * D), 1, D, rb, dUr(r), F, 1, rb, gr + L.off[P_W1] + wr, F, beta);
+    GemmArgs g1w = gemm(D, F, N, at(m->kY, (int64_t)r * N * D), 1, D, rb, dUr(r), F, 1, rb, gr + L.at(P_W1, top) + wr, F, beta);
     g1w.halfA = g1w.halfB = hf;
     ok = launch_gemm(g1w, ws2, m->gws_cap, w) && ok;
     (void)hipMemcpyAsync(dYr(r), dYr(r + 1), (size_t)N * D * 4, hipMemcpyDeviceToDevice, s);
-    GemmArgs gy = gemm(N, D, F, dUr(r), F, 1, rb, th + L.off[P_W1] + wr, 1, F, rb, dYr(r), D, 1.f);
+    GemmArgs gy = gemm(N, D, F, dUr(r), F, 1, rb, th + L.at(P_W1, top) + wr, 1, F, rb, dYr(r), D, 1.f);
     gy.halfA = hf;
     ok = launch_gemm(gy, ws, m->gws_cap, s) && ok;
   }
   order(m, s, w);  // dY_0 is complete
   // side: dWo = O^T . dY_0
-  launch_gemm(gemm(D, D, N, m->kO, 1, D, rb, dYr(0), D, 1, rb, gr + L.off[P_WO], D, 0.f), ws2, m->gws_cap, w);
+  launch_gemm(gemm(D, D, N, m->kO, 1, D, rb, dYr(0), D, 1, rb, gr + L.at(P_WO, top), D, 0.f), ws2, m->gws_cap, w);
   // attention output projection: dO = dY_0 . Wo^T, then the attention (last
   // query row) -> dQ, dK, dV
-  launch_gemm(gemm(N, D, D, dYr(0), D, 1, rb, th + L.off[P_WO], 1, D, rb, m->dO, D, 0.f), ws, m->gws_cap, s);
+  launch_gemm(gemm(N, D, D, dYr(0), D, 1, rb, th + L.at(P_WO, top), 1, D, rb, m->dO, D, 0.f), ws, m->gws_cap, s);
   // sP: [0, T D) sum over windows of dK, [T D, 2T D) of dV (from the attention
   // backward), [2T D, (2T+1) D) of dQ, [(2T+1) D, (2T+2) D) of dY_0
   float* sK = m->sP;
@@ -649,34 +840,54 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // side: dWk = X^T dK, dWv = X^T dV (dK, dV stay fp32), with X = G + P[t]:
   // G^T dZ as GEMMs on the byte-embedding part G, then P^T (sum over windows of
   // dZ) for the positional part
-  GemmArgs gk = gemm(D, D, N * T, m->Xk, 1, D, rb, m->dK, D, 1, 0, gr + L.off[P_WK], D, 0.f);
-  GemmArgs gv = gemm(D, D, N * T, m->Xk, 1, D, rb, m->dV, D, 1, 0, gr + L.off[P_WV], D, 0.f);
-  gk.halfA = gv.halfA = hf;
-  ok = launch_gemm(gk, ws2, m->gws_cap, w) && ok;
-  ok = launch_gemm(gv, ws2, m->gws_cap, w) && ok;
-  if (m->cfg.use_pos) {
-    launch_pos_grad(m->bf, m->Pc, sK, 0, T, D, gr + L.off[P_WK], w);
-    launch_pos_grad(m->bf, m->Pc, sV, 0, T, D, gr + L.off[P_WV], w);
+  if (NL == 1) {
+    GemmArgs gk = gemm(D, D, N * T, m->Xk, 1, D, rb, m->dK, D, 1, 0, gr + L.at(P_WK, top), D, 0.f);
+    GemmArgs gv = gemm(D, D, N * T, m->Xk, 1, D, rb, m->dV, D, 1, 0, gr + L.at(P_WV, top), D, 0.f);
+    gk.halfA = gv.halfA = hf;
+    ok = launch_gemm(gk, ws2, m->gws_cap, w) && ok;
+    ok = launch_gemm(gv, ws2, m->gws_cap, w) && ok;
+    if (m->cfg.use_pos) {
+      launch_pos_grad(m->bf, m->Pc, sK, 0, T, D, gr + L.at(P_WK, top), w);
+      launch_pos_grad(m->bf, m->Pc, sV, 0, T, D, gr + L.at(P_WV, top), w);
+    }
+    // side: dWq = X_last^T dQ (+ its positional part); Xk was written on this
+    // stream, dQ before the last mark
+    GemmArgs gq = gemm(D, D, N, at(m->Xk, (int64_t)(T - 1) * D), 1, (int64_t)T * D, rb, m->dQ, D, 1, 0,
+                       gr + L.at(P_WQ, top), D, 0.f);
+    gq.halfA = hf;
+    ok = launch_gemm(gq, ws2, m->gws_cap, w) && ok;
+    if (m->cfg.use_pos) launch_pos_grad(m->bf, m->Pc, sQ, T - 1, 1, D, gr + L.at(P_WQ, top), w);
+  } else {
+    // the top layer's input: the layer below's output, rounded (bf16 storage point)
+    ok = launch_gemm(gemm(D, D, N * T, Xtop, 1, D, rb, m->dK, D, 1, 0, gr + L.at(P_WK, top), D, 0.f), ws2,
+                     m->gws_cap, w) && ok;
+    ok = launch_gemm(gemm(D, D, N * T, Xtop, 1, D, rb, m->dV, D, 1, 0, gr + L.at(P_WV, top), D, 0.f), ws2,
+                     m->gws_cap, w) && ok;
+    ok = launch_gemm(gemm(D, D, N, Xtop + (int64_t)(T - 1) * D, 1, (int64_t)T * D, rb, m->dQ, D, 1, 0,
+                          gr + L.at(P_WQ, top), D, 0.f),
+                     ws2, m->gws_cap, w) && ok;
   }
-  // side: dWq = X_last^T dQ (+ its positional part); Xk was written on this
-  // stream, dQ before the last mark
-  GemmArgs gq = gemm(D, D, N, at(m->Xk, (int64_t)(T - 1) * D), 1, (int64_t)T * D, rb, m->dQ, D, 1, 0,
-                     gr + L.off[P_WQ], D, 0.f);
-  gq.halfA = hf;
-  ok = launch_gemm(gq, ws2, m->gws_cap, w) && ok;
-  if (m->cfg.use_pos) launch_pos_grad(m->bf, m->Pc, sQ, T - 1, 1, D, gr + L.off[P_WQ], w);
   // dX = dK Wk^T + dV Wv^T (+ dQ Wq^T + dY_0 on the last token)
-  launch_gemm2(gemm(N * T, D, D, m->dK, D, 1, 0, th + L.off[P_WK], 1, D, rb, m->dX, D, 0.f),
-               gemm(N * T, D, D, m->dV, D, 1, 0, th + L.off[P_WV], 1, D, rb, m->dX, D, 0.f), ws, m->gws_cap, s);
-  launch_gemm(gemm(N, D, D, m->dQ, D, 1, 0, th + L.off[P_WQ], 1, D, rb, m->dX + (int64_t)(T - 1) * D, (int64_t)T * D,
+  launch_gemm2(gemm(N * T, D, D, m->dK, D, 1, 0, th + L.at(P_WK, top), 1, D, rb, m->dX, D, 0.f),
+               gemm(N * T, D, D, m->dV, D, 1, 0, th + L.at(P_WV, top), 1, D, rb, m->dX, D, 0.f), ws, m->gws_cap, s);
+  launch_gemm(gemm(N, D, D, m->dQ, D, 1, 0, th + L.at(P_WQ, top), 1, D, rb, m->dX + (int64_t)(T - 1) * D, (int64_t)T * D,
                    1.f),
               ws, m->gws_cap, s);
   launch_add(m->dX + (int64_t)(T - 1) * D, dYr(0), N, D, (int64_t)T * D, D, s);
-  // positional table: dP[t] = sum_n dX[n][t], from the sums over windows of
-  // dK, dV, dQ and dY_0 times the weights; then the byte embedding
-  if (m->cfg.use_pos) {
+  if (NL > 1) {
+    // dX is the gradient w.r.t. the top layer's input: down through the lower
+    // layers (on this stream, after the side stream's work: layer 0 reads Xk)
+    order(m, w, s);
+    for (int l = NL - 2; l >= 0; --l) ok = lower_backward(m, l, N, s) && ok;
+    if (m->cfg.use_pos)
+      launch_colsum(m->dX, N, (int64_t)T * D, (int64_t)T * D, gr + L.off[P_P], 0.f, m->cws, s);
+    else
+      launch_zero(gr + L.off[P_P], L.size[P_P], s);
+  } else if (m->cfg.use_pos) {
+    // positional table: dP[t] = sum_n dX[n][t], from the sums over windows of
+    // dK, dV, dQ and dY_0 times the weights; then the byte embedding
     launch_colsum(dYr(0), N, D, D, sY, 0.f, m->cws, s);
-    launch_pos_table_grad(sK, sQ, sY, th + L.off[P_WQ], th + L.off[P_WK], th + L.off[P_WV], T, D, rb,
+    launch_pos_table_grad(sK, sQ, sY, th + L.at(P_WQ, top), th + L.at(P_WK, top), th + L.at(P_WV, top), T, D, rb,
                           gr + L.off[P_P], s);
   } else {
     launch_zero(gr + L.off[P_P], L.size[P_P], s);

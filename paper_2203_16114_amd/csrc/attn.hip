@@ -37,6 +37,21 @@ __device__ __forceinline__ uint4 x_frag(const typename Mma<BF>::T* __restrict__ 
   return *reinterpret_cast<const uint4*>(E + byte * e + cc);
 }
 
+// A token fragment from an input row of a later layer: EPF consecutive fp32
+// values at X + i (i < 0: a dead window, zeros), as the operand type.
+template <bool BF>
+__device__ __forceinline__ uint4 x_row_frag(const float* __restrict__ X, int64_t i) {
+  if (i < 0) return make_uint4(0u, 0u, 0u, 0u);
+  const float4 lo = *reinterpret_cast<const float4*>(X + i);
+  if constexpr (BF) {
+    const float4 hi = *reinterpret_cast<const float4*>(X + i + 4);
+    return make_uint4(pack_bf16x2(lo.x, lo.y), pack_bf16x2(lo.z, lo.w), pack_bf16x2(hi.x, hi.y),
+                      pack_bf16x2(hi.z, hi.w));
+  } else {
+    return make_uint4(__float_as_uint(lo.x), __float_as_uint(lo.y), __float_as_uint(lo.z), __float_as_uint(lo.w));
+  }
+}
+
 __device__ __forceinline__ void put4o(uint16_t* p, const f32x4& v) {
   *reinterpret_cast<uint2*>(p) = make_uint2(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]));
 }
@@ -213,7 +228,10 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
 #pragma unroll
     for (int ks = 0; ks < KSTEPS; ++ks) {
       const int d = ks * M::KS + lg * M::EPF;
-      xb[rf][ks] = x_frag<BF>(E, Wb + m * 64, t, d, a.e, a.g, einv);
+      if (a.Xin)  // a later layer: its input rows, as operands (bf16: rounded)
+        xb[rf][ks] = x_row_frag<BF>(a.Xin, tile0 + m < N ? ((tile0 + m) * T + t) * D + d : -1);
+      else
+        xb[rf][ks] = x_frag<BF>(E, Wb + m * 64, t, d, a.e, a.g, einv);
       if (t == T - 1) *(uint4*)(Xl + m * XLSTR + ks * 64 + lg * 16) = xb[rf][ks];
     }
   }
@@ -414,13 +432,18 @@ __global__ __launch_bounds__(512) void k_attn(AttnArgs a) {
         const int64_t n = tile0 + m;
         if (n < N) {
           const int d = qf * 16 + 4 * lg;
-          const int j = (int)(((uint32_t)d * einv) >> 20), cc = d - j * a.e;
-          const int byte = Wb[m * 64 + (T - 1) * a.g + j];
           float4 r;
-          r.x = acc[nf][0] + (M::val(E[byte * a.e + cc]) + M::val(P[(T - 1) * D + d]));
-          r.y = acc[nf][1] + (M::val(E[byte * a.e + cc + 1]) + M::val(P[(T - 1) * D + d + 1]));
-          r.z = acc[nf][2] + (M::val(E[byte * a.e + cc + 2]) + M::val(P[(T - 1) * D + d + 2]));
-          r.w = acc[nf][3] + (M::val(E[byte * a.e + cc + 3]) + M::val(P[(T - 1) * D + d + 3]));
+          if (a.Xin) {  // the residual: the input row itself (fp32)
+            const float4 x = *reinterpret_cast<const float4*>(a.Xin + (n * T + T - 1) * D + d);
+            r = make_float4(acc[nf][0] + x.x, acc[nf][1] + x.y, acc[nf][2] + x.z, acc[nf][3] + x.w);
+          } else {
+            const int j = (int)(((uint32_t)d * einv) >> 20), cc = d - j * a.e;
+            const int byte = Wb[m * 64 + (T - 1) * a.g + j];
+            r.x = acc[nf][0] + (M::val(E[byte * a.e + cc]) + M::val(P[(T - 1) * D + d]));
+            r.y = acc[nf][1] + (M::val(E[byte * a.e + cc + 1]) + M::val(P[(T - 1) * D + d + 1]));
+            r.z = acc[nf][2] + (M::val(E[byte * a.e + cc + 2]) + M::val(P[(T - 1) * D + d + 2]));
+            r.w = acc[nf][3] + (M::val(E[byte * a.e + cc + 3]) + M::val(P[(T - 1) * D + d + 3]));
+          }
           *reinterpret_cast<float4*>(a.h0 + n * D + d) = r;
         }
       }

@@ -556,12 +556,6 @@ void launch_add(float* y, const float* x, int64_t rows, int64_t cols, int64_t ld
 }
 
 // ------------------------------------------------------- attention backward ----
-// Last query row only (the only row with an upstream gradient).  For window n
-// and head h with weights a_u over the T keys:
-//   dA_u = dO . V_u,  dS_u = a_u (dA_u - sum_u' a_u' dA_u'),
-//   dq = scale sum_u dS_u K_u,  dK_u = scale dS_u q,  dV_u = a_u dO.
-// One thread per (window, head, column); the two reductions over the head's
-// columns go through LDS.
 // Attention backward of the last query row (Eqs. 1-2).  A block takes one
 // head of 4 (DH = 64) or 8 (DH = 32) consecutive windows, a wave (half a wave)
 // per window and a lane per column: dA_u = dO_h . V_h[u] by shuffle sums over

@@ -71,6 +71,14 @@ int trace_check_config(const trace_config* c, Layout* L) {
     trace_set_error("attention must be TRACE_ATTN_SOFTMAX or TRACE_ATTN_PERFORMER");
     return TRACE_EINVAL;
   }
+  if (c->layers < 0 || c->layers > 8) {
+    trace_set_error("layers must be in [0, 8] (0: one layer)");
+    return TRACE_EINVAL;
+  }
+  if (c->layers > 1 && c->attention != TRACE_ATTN_SOFTMAX) {
+    trace_set_error("stacked layers use softmax attention");
+    return TRACE_EINVAL;
+  }
   if (c->n_features < 0 || c->n_features > 512 || c->n_features % 16 != 0) {
     trace_set_error("n_features must be a multiple of 16 in [0, 512]");
     return TRACE_EINVAL;
@@ -86,12 +94,16 @@ int trace_check_config(const trace_config* c, Layout* L) {
     L->DH = (int)(d / c->H);
     const int64_t T = L->T, D = d, e = c->e, F = c->F;
     const int64_t nr = c->untied_ffn ? c->k : 1;  // FFN weight blocks: one, or one per repeat
+    const int64_t NL = c->layers > 1 ? c->layers : 1;
+    L->NL = (int)NL;
     const int64_t sizes[NPARAM] = {256 * e, T * D, D * D, D * D, D * D, D * D, nr * D * F, nr * F * D, D * 256, 256};
     int64_t off = 0;
     for (int i = 0; i < NPARAM; ++i) {
+      const bool per_layer = i >= P_WQ && i <= P_W2;
       L->off[i] = off;
-      L->size[i] = sizes[i];
-      off += sizes[i];
+      L->lsize[i] = sizes[i];
+      L->size[i] = per_layer ? NL * sizes[i] : sizes[i];
+      off += L->size[i];
     }
     L->n = off;
   }

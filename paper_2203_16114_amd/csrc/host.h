@@ -10,7 +10,11 @@ enum { P_E = 0, P_P, P_WQ, P_WK, P_WV, P_WO, P_W1, P_W2, P_WOUT, P_BOUT, NPARAM 
 
 struct Layout {
   int T, D, DH;
+  int NL;                  // layers
   int64_t off[NPARAM], size[NPARAM], n;
+  int64_t lsize[NPARAM];   // one layer's block (Wq .. W2); the whole tensor otherwise
+  // offset of parameter i of layer l
+  int64_t at(int i, int l) const { return off[i] + (int64_t)l * lsize[i]; }
 };
 
 void trace_set_error(const std::string& msg);

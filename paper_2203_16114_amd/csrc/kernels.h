@@ -24,6 +24,7 @@ struct AttnArgs {
   float scale;                     // 1/sqrt(head width)
   float scale4;                    // (head width)^-1/4 (Performer)
   int32_t token_only;              // 1: the per-token kernel whatever the launch shape
+  const float* Xin;                // later layers: input rows [N][T][D] (fp32; NULL: byte-group tokens)
   const uint4* Om;                 // Performer: packed random projection (NULL: softmax attention)
   int32_t nfeat;                   // Performer: features (a multiple of 16)
   // kept activations for the backward (all NULL unless kept), indexed by local window
@@ -140,3 +141,11 @@ void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, i
 void launch_pos_grad(bool bf, const void* P, const float* S, int t0, int nt, int D, float* dW, hipStream_t s);
 void launch_adam(float* theta, const float* grad, float* m, float* v, int64_t n, float lr, float b1, float b2,
                  float eps, float bc1, float bc2, hipStream_t s, hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
+
+// ---- stacked layers (layers.hip) ----
+void launch_tokens(bool bf, const WinArgs& w, const void* E, const void* P, int T, int D, int e, int g, float* X,
+                   hipStream_t s);
+void launch_attn_rows(const float* Q, const float* K, const float* V, int64_t N, int T, int D, int H, float scale,
+                      int rb, float* O, float* Akeep, hipStream_t s);
+void launch_attn_bwd_rows(const float* dO, const float* Q, const float* K, const float* V, const float* A, int64_t N,
+                          int T, int D, int H, float scale, int rb, float* dQ, float* dK, float* dV, hipStream_t s);

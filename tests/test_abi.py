@@ -106,3 +106,14 @@ def test_untied_layout_and_initialiser_match_oracle(wid, seed):
     a = P.init_flat_host(cfg, seed, 0.02)
     b = O.init_flat(ocf, seed, 0.02)
     assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+@pytest.mark.parametrize("layers,untied", [(2, False), (3, True)])
+def test_multilayer_layout_and_init_match_oracle(layers, untied):
+    w = WORKLOADS[4]
+    cfg = P.make_config(w.W, w.e, w.g, w.H, w.F, w.k, w.dtype, untied_ffn=untied, layers=layers)
+    ocfg = O.Config(W=w.W, e=w.e, g=w.g, H=w.H, F=w.F, k=w.k, untied=untied, layers=layers)
+    assert P.param_count(cfg) == O.param_count(ocfg)
+    a = P.init_flat_host(cfg, 77)
+    b = O.init_flat(ocfg, 77)
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
