@@ -51,11 +51,11 @@ def flops_per_window(w):
 
 def mfma_flops_per_window(w):
     """Flops the matrix cores execute per window on the main workload's launches
-    (bf16, 64-window tiles within one stream): the attention block projects each
-    wave's 16 byte-group rows (15 distinct groups of its 8 windows) to K and V
-    once, 16 * 4d^2 / 8 = 8d^2 per window, plus q and Wo (2d^2 each); the
-    scores and weighted sums run on the vector ALUs.  The FFN executes its
-    algorithmic work."""
+    (bf16, 64-window tiles within one stream): the attention block projects the
+    tile's 128 byte-group rows (the 120 distinct groups of its 64 windows, in
+    16-row fragments) to K and V once, 128 * 4d^2 / 64 = 8d^2 per window, plus
+    q and Wo (2d^2 each); the scores and weighted sums run on the vector ALUs.
+    The FFN executes its algorithmic work."""
     d = w.d
     return {"attn": 12 * d * d, "ffn_head": flops_per_window(w)["ffn_head"]}
 
@@ -184,6 +184,19 @@ def measure_forward(wid, steps_per_call, calls):
            "path_tflops": round(path, 2), "path_frac": round(path / peak, 4)}
     log(f"[bench] forward {w.name}: {value:.4g} B/s, path {path:.1f} TFLOP/s ({path / peak:.3f} of {peak})")
     return res
+
+
+def attn_kernel(w, steps_per_call):
+    """The attention kernel of a forward launch: bf16 launches of whole
+    64-window tiles per stream share the byte groups between windows, one
+    head per wave at d = 256 with 8 heads and g = 8 (k_attn_wh), one window
+    class per wave otherwise (k_attn_grp); the per-token kernel (k_attn) for
+    the rest."""
+    if w.dtype != "bf16" or steps_per_call % 64:
+        return "k_attn"
+    if w.d == 256 and w.H == 8 and w.g == 8 and w.T in (4, 8):
+        return "k_attn_wh"
+    return "k_attn_grp"
 
 
 def traffic_for(kernel, windows_per_launch):
@@ -543,8 +556,7 @@ def main():
     peak = PEAK_TFLOPS[w.dtype]
     total_tflops = (fpw["attn"] + fpw["ffn_head"]) * value / 1e12
     # the FFN + head kernel is k_ffn_pipe in bf16, k_ffn_head in fp32
-    # bf16 launches of whole 64-window tiles per stream take the shared-group attention kernel
-    attn_k = "k_attn_grp" if (w.dtype == "bf16" and S % 64 == 0) else "k_attn"
+    attn_k = attn_kernel(w, S)
     kname = ("k_ffn_pipe" if w.dtype == "bf16" else "k_ffn_head") if dom == "ffn_head" else attn_k
     traffic = traffic_for(kname, wpl)
     roofline = {"bound": "mfma", "kernel": kname,

@@ -760,6 +760,374 @@ __global__ __launch_bounds__(512) void k_attn_grp(AttnArgs a) {
   }
 }
 
+// ------------------------------------------------------- one head per wave ----
+// k_attn_wh: the result of k_attn_grp for 64-window tiles of the shape with 8
+// heads of 32 features, g = 8 and T = 4 or 8, with the work cut by head
+// instead of by window.  Window i of the tile reads its token t from the group
+// that starts i + g t bytes into the tile's bytes, so the tile holds
+// MA + W - g distinct groups ("group rows" o); their E-parts go to LDS once
+// (16-byte unit u of row o at u ^ (o & 15), conflict-free fragment reads).
+// Wave h then forms everything of head h with no barrier until the output
+// projection:
+//   K_h^T = Wk_h^T . X_E^T over all group rows, q_h^T = Wq_h^T . E_last^T +
+//     (P.Wq)[T-1] (E_last of window i is group row i + g (T-1));
+//   a lane's accumulator quads hold group row 16 rf + lc (K) and window
+//     16 nf + lc (q), features 4 lg + r of each 16-feature block.  Key row
+//     i + g t of window 16 nf + lc is row lc of fragment nf + t/2 for even t;
+//     for odd t it is row lc ^ 8 of fragment nf + (t-1)/2 + (lc >= 8): each
+//     lane picks the fragment its partner needs and a DPP rotation by 8 lanes
+//     within the row of 16 brings it over (once per fragment, shift8);
+//   scores q . (K_E[row] + (P.Wk)[t]) as partial sums over the lane's 8
+//     features, summed over the 4 lane groups by a reduce-scatter (shuffles
+//     across 32 and 16 lanes) that leaves lane (lg, lc) with the T scores of
+//     window 16 lg + lc: softmax in the lane; the weights go through this
+//     wave's LDS rows to the lanes that hold each window;
+//   V_h^T = Wv_h^T . X_E^T and O_h = sum_t a_t (V_E[row] + (P.Wv)[t]) with the
+//     same row selection, rounded to bf16 into the O tile.
+// The output projection and residual follow as in k_attn_grp, the waves split
+// over output features.
+template <int T, int G, int D, int DH>
+struct WhShape {
+  static constexpr int NW = 8, MA = 64, W = T * G, H = D / DH;
+  static constexpr int NRF = (MA + W - G + 15) / 16;  // group-row fragments
+  static constexpr int NWF = MA / 16;                  // window fragments
+  static constexpr int KSTEPS = D / 32, NB = D / 16;
+  static constexpr int XSTR = D * 2, XM = (D / 8 >= 16 ? 16 : D / 8) - 1;
+  static constexpr int HSTR = D + 4;  // h0 rows staged for the write (floats, padded)
+  static constexpr int XG = NRF * 16 * XSTR > MA * HSTR * 4 ? NRF * 16 * XSTR : MA * HSTR * 4;
+  static constexpr int WB = MA + W + 64;
+  static constexpr int LDS = XG + MA * XSTR + 2 * T * D * 4 + NW * MA * T * 4 + WB;
+  static constexpr bool ok = H == NW && DH == 32 && G == 8 && (T == 4 || T == 8) && D == 256 &&
+                             (NRF * 16 * (D / 8)) % 512 == 0 && LDS <= 160 * 1024;
+};
+
+// x from lane lc ^ 8 of the same row of 16 lanes
+__device__ __forceinline__ float ror8(float x) {
+  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), 0x128, 0xF, 0xF, false));
+}
+
+// The group rows 8 below each fragment's: sh[j] lane lc holds row
+// 16 j + lc + 8, taken from fragment j (lc < 8) or j + 1 (lc >= 8) of the
+// partner lane lc ^ 8.  Row i + G t of window i = 16 nf + lc is then
+// acc[nf + t/2] for even t and sh[nf + (t-1)/2] for odd t.
+template <int NRF, int NSH>
+__device__ __forceinline__ void shift8(const f32x4 (&acc)[NRF][2], f32x4 (&sh)[NSH][2], bool hi) {
+  static_assert(NSH < NRF, "rows");
+#pragma unroll
+  for (int j = 0; j < NSH; ++j)
+#pragma unroll
+    for (int fr = 0; fr < 2; ++fr)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sh[j][fr][r] = ror8(hi ? acc[j][fr][r] : acc[j + 1][fr][r]);
+}
+template <int NRF, int NSH>
+__device__ __forceinline__ const f32x4& key_row(const f32x4 (&acc)[NRF][2], const f32x4 (&sh)[NSH][2], int nf, int t,
+                                                int fr) {
+  return (t & 1) == 0 ? acc[nf + t / 2][fr] : sh[nf + t / 2][fr];
+}
+
+template <int T, int G, int D, int DH>
+__global__ __launch_bounds__(512) void k_attn_wh(AttnArgs a) {
+  typedef Mma<true> M;
+  typedef WhShape<T, G, D, DH> S;
+  constexpr int NW = S::NW, MA = S::MA, W = S::W, NRF = S::NRF, NWF = S::NWF, KSTEPS = S::KSTEPS, NB = S::NB;
+  constexpr int XSTR = S::XSTR, XM = S::XM, HSTR = S::HSTR;
+  constexpr int EPB = D / G;            // features per byte embedding
+  constexpr int QOFF = (T - 1) * G;     // group row of window 0's last token
+  constexpr int NQF = D / 16, QFW = NQF / NW;
+  static_assert(S::ok, "shape");
+  __shared__ __align__(16) unsigned char Xg[S::XG];      // group rows (bf16), later the h0 rows (fp32)
+  __shared__ __align__(16) unsigned char Xo[MA * XSTR];  // O rows (bf16)
+  __shared__ __align__(16) float PKV[2][T * D];          // P.Wk, P.Wv
+  __shared__ __align__(16) float Aw[NW][MA * T];         // each wave's attention weights, one row per window
+  __shared__ uint8_t Wb[S::WB];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lg = lane >> 4, lc = lane & 15;
+  const int h = wave;
+  const int64_t tile0 = (int64_t)blockIdx.x * MA;
+  const int64_t N = a.w.N;
+  const uint16_t* __restrict__ E = (const uint16_t*)a.E;
+  const uint16_t* __restrict__ P = (const uint16_t*)a.P;
+
+  // the tile's bytes: Wb[k] = stream byte at (target of window 0) - W + k
+  {
+    const int64_t base = target_offset(a.w, tile0) - W;
+    for (int k = tid; k < S::WB; k += 512) Wb[k] = k < MA + W ? a.w.streams[base + k] : 0;
+    const float4* src = reinterpret_cast<const float4*>(a.PW + (int64_t)T * D);
+    for (int k = tid; k < 2 * T * D / 4; k += 512) reinterpret_cast<float4*>(&PKV[0][0])[k] = src[k];
+  }
+  __syncthreads();
+  // group rows o: unit u holds features 8u .. 8u + 7, from byte o + u / (EPB / 8)
+  {
+    constexpr int NU = NRF * 16 * (D / 8) / 512;
+    uint4 ev[NU];
+#pragma unroll
+    for (int r = 0; r < NU; ++r) {
+      const int q = tid + 512 * r, o = q / (D / 8), u = q % (D / 8);
+      const int byte = Wb[o + u / (EPB / 8)];
+      ev[r] = *reinterpret_cast<const uint4*>(E + byte * EPB + (u % (EPB / 8)) * 8);
+    }
+#pragma unroll
+    for (int r = 0; r < NU; ++r) {
+      const int q = tid + 512 * r, o = q / (D / 8), u = q % (D / 8);
+      *(uint4*)(Xg + o * XSTR + 16 * (u ^ (o & XM))) = ev[r];
+    }
+  }
+  __syncthreads();
+
+  // fragment reads of rows m (m & 15 = c) at units 4 ks + lg: byte 64 (ks & ~3) + off[ks & 3]
+  auto swz = [&](int c, int (&off)[4]) {
+    const int q = (c & XM) >> 2, p = lg ^ (c & 3);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) off[j] = 16 * (((j ^ q) << 2) | p);
+  };
+  int xo[4], qo[4];
+  swz(lc, xo);
+  swz((QOFF + lc) & 15, qo);
+  const bool hi = lc >= 8;
+
+  // K_h over all group rows and q_h over the windows' last tokens
+  f32x4 kacc[NRF][2], qacc[NWF][2];
+#pragma unroll
+  for (int rf = 0; rf < NRF; ++rf) kacc[rf][0] = kacc[rf][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int nf = 0; nf < NWF; ++nf) qacc[nf][0] = qacc[nf][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  {
+    const uint4* Wkh = a.Wk + (h * 2) * 64 + lane;
+    const uint4* Wqh = a.Wq + (h * 2) * 64 + lane;
+    uint4 wk[2][2], wq[2][2];
+#pragma unroll
+    for (int fr = 0; fr < 2; ++fr) {
+      wk[0][fr] = Wkh[fr * 64];
+      wq[0][fr] = Wqh[fr * 64];
+    }
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      if (ks + 1 < KSTEPS) {
+#pragma unroll
+        for (int fr = 0; fr < 2; ++fr) {
+          wk[(ks + 1) & 1][fr] = Wkh[((ks + 1) * NB + fr) * 64];
+          wq[(ks + 1) & 1][fr] = Wqh[((ks + 1) * NB + fr) * 64];
+        }
+      }
+      const int kb = (ks & ~3) * 64;
+      uint4 bg[NRF], bq[NWF];
+#pragma unroll
+      for (int rf = 0; rf < NRF; ++rf) bg[rf] = *(const uint4*)(Xg + (16 * rf + lc) * XSTR + kb + xo[ks & 3]);
+#pragma unroll
+      for (int nf = 0; nf < NWF; ++nf) bq[nf] = *(const uint4*)(Xg + (QOFF + 16 * nf + lc) * XSTR + kb + qo[ks & 3]);
+#pragma unroll
+      for (int rf = 0; rf < NRF; ++rf)
+#pragma unroll
+        for (int fr = 0; fr < 2; ++fr) M::run(kacc[rf][fr], wk[ks & 1][fr], bg[rf]);
+#pragma unroll
+      for (int nf = 0; nf < NWF; ++nf)
+#pragma unroll
+        for (int fr = 0; fr < 2; ++fr) M::run(qacc[nf][fr], wq[ks & 1][fr], bq[nf]);
+    }
+  }
+  {
+    const float* pq = a.PW + (T - 1) * D + h * DH + 4 * lg;
+#pragma unroll
+    for (int fr = 0; fr < 2; ++fr) {
+      const float4 p4 = *reinterpret_cast<const float4*>(pq + 16 * fr);
+#pragma unroll
+      for (int nf = 0; nf < NWF; ++nf) {
+        qacc[nf][fr][0] += p4.x;
+        qacc[nf][fr][1] += p4.y;
+        qacc[nf][fr][2] += p4.z;
+        qacc[nf][fr][3] += p4.w;
+      }
+    }
+  }
+
+  // scores: partial sums over the lane's 8 features
+  constexpr int NSH = NWF + (T - 1) / 2;
+  float sc[NWF][T];
+  {
+    f32x4 ksh[NSH][2];
+    shift8(kacc, ksh, hi);
+    const float* pk = &PKV[0][0] + h * DH + 4 * lg;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const float4 p0 = *reinterpret_cast<const float4*>(pk + t * D);
+      const float4 p1 = *reinterpret_cast<const float4*>(pk + t * D + 16);
+#pragma unroll
+      for (int nf = 0; nf < NWF; ++nf) {
+        const f32x4& k0 = key_row(kacc, ksh, nf, t, 0);
+        const f32x4& k1 = key_row(kacc, ksh, nf, t, 1);
+        const f32x4& q0 = qacc[nf][0];
+        const f32x4& q1 = qacc[nf][1];
+        float s = q0[0] * (k0[0] + p0.x) + q0[1] * (k0[1] + p0.y) + q0[2] * (k0[2] + p0.z) + q0[3] * (k0[3] + p0.w);
+        s += q1[0] * (k1[0] + p1.x) + q1[1] * (k1[1] + p1.y) + q1[2] * (k1[2] + p1.z) + q1[3] * (k1[3] + p1.w);
+        sc[nf][t] = s;
+      }
+    }
+  }
+  // reduce-scatter over the lane groups: lane (lg, lc) ends with window 16 lg + lc
+  float st[T];
+  {
+    const bool up = lg >= 2, od = (lg & 1) != 0;
+    float r1[2][T];
+#pragma unroll
+    for (int j = 0; j < 2; ++j)
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        const float keep = up ? sc[2 + j][t] : sc[j][t];
+        const float send = up ? sc[j][t] : sc[2 + j][t];
+        r1[j][t] = keep + __shfl_xor(send, 32, 64);
+      }
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const float keep = od ? r1[1][t] : r1[0][t];
+      const float send = od ? r1[0][t] : r1[1][t];
+      st[t] = keep + __shfl_xor(send, 16, 64);
+    }
+  }
+  {
+    const float scale = a.scale;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      st[t] *= scale;
+      mx = fmaxf(mx, st[t]);
+    }
+    float sm = 0.f;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      st[t] = expf(st[t] - mx);
+      sm += st[t];
+    }
+    const float rs = __builtin_amdgcn_rcpf(sm);
+    float* aw = Aw[wave] + (16 * lg + lc) * T;
+#pragma unroll
+    for (int t = 0; t < T; t += 4)
+      *reinterpret_cast<float4*>(aw + t) = make_float4(st[t] * rs, st[t + 1] * rs, st[t + 2] * rs, st[t + 3] * rs);
+  }
+
+  // V_h over all group rows
+  f32x4 vacc[NRF][2];
+#pragma unroll
+  for (int rf = 0; rf < NRF; ++rf) vacc[rf][0] = vacc[rf][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+  {
+    const uint4* Wvh = a.Wv + (h * 2) * 64 + lane;
+    uint4 wv[2][2];
+#pragma unroll
+    for (int fr = 0; fr < 2; ++fr) wv[0][fr] = Wvh[fr * 64];
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      if (ks + 1 < KSTEPS) {
+#pragma unroll
+        for (int fr = 0; fr < 2; ++fr) wv[(ks + 1) & 1][fr] = Wvh[((ks + 1) * NB + fr) * 64];
+      }
+      const int kb = (ks & ~3) * 64;
+      uint4 bg[NRF];
+#pragma unroll
+      for (int rf = 0; rf < NRF; ++rf) bg[rf] = *(const uint4*)(Xg + (16 * rf + lc) * XSTR + kb + xo[ks & 3]);
+#pragma unroll
+      for (int rf = 0; rf < NRF; ++rf)
+#pragma unroll
+        for (int fr = 0; fr < 2; ++fr) M::run(vacc[rf][fr], wv[ks & 1][fr], bg[rf]);
+    }
+  }
+  __builtin_amdgcn_wave_barrier();
+  // O_h[window 16 nf + lc][features 16 fr + 4 lg + r]
+  {
+    float aa[NWF][T];
+#pragma unroll
+    for (int nf = 0; nf < NWF; ++nf) {
+      const float* aw = Aw[wave] + (16 * nf + lc) * T;
+#pragma unroll
+      for (int t = 0; t < T; t += 4) {
+        const float4 v = *reinterpret_cast<const float4*>(aw + t);
+        aa[nf][t] = v.x;
+        aa[nf][t + 1] = v.y;
+        aa[nf][t + 2] = v.z;
+        aa[nf][t + 3] = v.w;
+      }
+    }
+    f32x4 vsh[NSH][2];
+    shift8(vacc, vsh, hi);
+    f32x4 o[NWF][2];
+#pragma unroll
+    for (int nf = 0; nf < NWF; ++nf) o[nf][0] = o[nf][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const float* pv = &PKV[1][0] + h * DH + 4 * lg;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const float4 p0 = *reinterpret_cast<const float4*>(pv + t * D);
+      const float4 p1 = *reinterpret_cast<const float4*>(pv + t * D + 16);
+#pragma unroll
+      for (int nf = 0; nf < NWF; ++nf) {
+        const f32x4& v0 = key_row(vacc, vsh, nf, t, 0);
+        const f32x4& v1 = key_row(vacc, vsh, nf, t, 1);
+        const float at = aa[nf][t];
+        o[nf][0][0] += at * (v0[0] + p0.x);
+        o[nf][0][1] += at * (v0[1] + p0.y);
+        o[nf][0][2] += at * (v0[2] + p0.z);
+        o[nf][0][3] += at * (v0[3] + p0.w);
+        o[nf][1][0] += at * (v1[0] + p1.x);
+        o[nf][1][1] += at * (v1[1] + p1.y);
+        o[nf][1][2] += at * (v1[2] + p1.z);
+        o[nf][1][3] += at * (v1[3] + p1.w);
+      }
+    }
+#pragma unroll
+    for (int nf = 0; nf < NWF; ++nf) {
+      const int m = 16 * nf + lc;
+#pragma unroll
+      for (int fr = 0; fr < 2; ++fr) {
+        const int oe = h * DH + 16 * fr + 4 * lg;
+        put4o((uint16_t*)(Xo + m * XSTR + 16 * ((oe >> 3) ^ (m & XM)) + 8 * ((oe >> 2) & 1)), o[nf][fr]);
+      }
+    }
+  }
+  __syncthreads();  // O complete; group rows no longer needed
+
+  // h0^T = Wo^T . O^T + X_last (fp32: E + P of the last token), rows staged
+  // over the group rows, then written out whole
+  float* Hs = reinterpret_cast<float*>(Xg);
+#pragma unroll
+  for (int qi = 0; qi < QFW; ++qi) {
+    const int qf = wave * QFW + qi;
+    f32x4 acc[NWF];
+#pragma unroll
+    for (int nf = 0; nf < NWF; ++nf) acc[nf] = f32x4{0.f, 0.f, 0.f, 0.f};
+    uint4 wo[2];
+    wo[0] = a.Wo[qf * 64 + lane];
+#pragma unroll
+    for (int ks = 0; ks < KSTEPS; ++ks) {
+      if (ks + 1 < KSTEPS) wo[(ks + 1) & 1] = a.Wo[((ks + 1) * NB + qf) * 64 + lane];
+#pragma unroll
+      for (int nf = 0; nf < NWF; ++nf) {
+        const uint4 bo = *(const uint4*)(Xo + (16 * nf + lc) * XSTR + (ks & ~3) * 64 + xo[ks & 3]);
+        M::run(acc[nf], wo[ks & 1], bo);
+      }
+    }
+#pragma unroll
+    for (int nf = 0; nf < NWF; ++nf) {
+      const int m = 16 * nf + lc;
+      const int d = qf * 16 + 4 * lg;
+      const int j = d / EPB, cc = d - j * EPB;
+      const int byte = Wb[m + QOFF + j];
+      float4 r;
+      r.x = acc[nf][0] + (M::val(E[byte * EPB + cc]) + M::val(P[(T - 1) * D + d]));
+      r.y = acc[nf][1] + (M::val(E[byte * EPB + cc + 1]) + M::val(P[(T - 1) * D + d + 1]));
+      r.z = acc[nf][2] + (M::val(E[byte * EPB + cc + 2]) + M::val(P[(T - 1) * D + d + 2]));
+      r.w = acc[nf][3] + (M::val(E[byte * EPB + cc + 3]) + M::val(P[(T - 1) * D + d + 3]));
+      *reinterpret_cast<float4*>(Hs + m * HSTR + d) = r;
+    }
+  }
+  __syncthreads();
+  for (int m = wave; m < MA; m += NW) {
+    const int64_t n = tile0 + m;
+    if (n < N) {
+#pragma unroll
+      for (int c = 4 * lane; c < D; c += 256)
+        *reinterpret_cast<float4*>(a.h0 + n * D + c) = *reinterpret_cast<const float4*>(Hs + m * HSTR + c);
+    }
+  }
+}
+
 // ------------------------------------------------------------ dispatch ----
 // Measured alternative, slower on the main workload (2^20 windows): two
 // accumulator sets so that the scores of head h run under the MFMAs of its V
@@ -783,7 +1151,10 @@ static void launch_attn(const AttnArgs& a, hipStream_t s) {
 
 template <int T, int G, int D, int DH>
 static bool launch_grp(const AttnArgs& a, hipStream_t s) {
-  if constexpr (GrpShape<T, G, D, DH>::ok) {
+  if constexpr (WhShape<T, G, D, DH>::ok) {
+    hipLaunchKernelGGL((k_attn_wh<T, G, D, DH>), dim3((unsigned)((a.w.N + 63) / 64)), dim3(512), 0, s, a);
+    return true;
+  } else if constexpr (GrpShape<T, G, D, DH>::ok) {
     hipLaunchKernelGGL((k_attn_grp<T, G, D, DH>), dim3((unsigned)((a.w.N + 63) / 64)), dim3(512), 0, s, a);
     return true;
   }

@@ -147,10 +147,11 @@ def test_ragged_tiles_and_chunking_are_bitwise_invariant(dtype):
     check_parity(dtype, a["logits"].cpu().numpy(), a["bits"].cpu().numpy(), ref)
 
 
-@pytest.mark.parametrize("shape", [dict(W=32, e=32, g=4, H=4, F=512, k=2), dict(W=64, e=32, g=8, H=8, F=256, k=1)])
+@pytest.mark.parametrize("shape", [dict(W=32, e=32, g=4, H=4, F=512, k=2), dict(W=64, e=32, g=8, H=8, F=256, k=1),
+                                   dict(W=32, e=32, g=8, H=8, F=256, k=1)])
 def test_shared_group_and_token_paths_agree(shape):
     """bf16 launches whose 64-window tiles lie in one stream share the byte groups
-    between windows (k_attn_grp).  A model whose chunks do not start on 64-window
+    between windows (k_attn_grp; k_attn_wh at d = 256 with 8 heads and g = 8).  A model whose chunks do not start on 64-window
     boundaries runs the token kernel (k_attn) on its later chunks; both match the
     oracle on every window and each other within the bf16 parity bar."""
     W = shape["W"]
