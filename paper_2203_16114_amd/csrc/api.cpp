@@ -28,6 +28,7 @@ struct trace_model {
   void *Ec, *Pc;
   float* PW;  // [3][T][D] positional parts of the q, k, v projections
   uint4 *Wq, *Wk, *Wv, *Wo, *W1, *W2, *Wout;
+  uint4 *WkT, *WvT;  // bf16 models that keep activations: packed Wk^T, Wv^T (input gradient of the tokens)
   // Performer attention: packed random projection (device), features, set yet
   uint4* Om;
   int nfeat;
@@ -55,6 +56,7 @@ struct trace_model {
   // in bf16 models dU, Xk (the byte-embedding part of the kept tokens) and the
   // kept Y hold bf16 elements: all are only read as bf16 operands
   float *dz, *dY, *dU, *G, *dO, *dQ, *dK, *dV, *dX, *Xk, *sP, *gws, *cws, *ews, *apart;
+  float* dSc;  // [N][H][T] gradients of the last row's attention scores
   int64_t gws_cap;
   // second stream of the update step (the weight-gradient branch), its own
   // split-K and column-sum workspaces, and the events that order the two streams
@@ -128,6 +130,10 @@ std::vector<std::array<int, 3>> adapt_gemm_shapes(const trace_model* m, int64_t 
   std::vector<std::array<int, 3>> v = {{D, 256, n}, {n, D, 256}, {F, D, n},     {n, F, D},
                                        {D, F, n},   {n, D, F},   {D, D, n},     {n, D, D},
                                        {D, D, n * T}, {n * T, D, D}, {n * T, D, 2 * D}};
+  if (m->cfg.k > 1) {  // the FFN weight gradients summed over the repeats in one product
+    v.push_back({F, D, m->cfg.k * n});
+    v.push_back({D, F, m->cfg.k * n});
+  }
   if (m->L.NL > 1) {  // the lower layers' products run over every token row
     const int r = n * T;
     for (std::array<int, 3> x : std::vector<std::array<int, 3>>{
@@ -243,8 +249,12 @@ bool refresh_operands(trace_model* m, hipStream_t s) {
       job(RJ_CVT, th + L.off[P_E], m->Ec, L.size[P_E], 0),
       pos ? job(RJ_CVT, th + L.off[P_P], m->Pc, L.size[P_P], 0)
           : job(RJ_ZERO, nullptr, m->Pc, (L.size[P_P] * (m->bf ? 2 : 4) + 3) / 4, 0),
+      // the update's input gradient of the tokens (bf16 models that keep activations)
+      job(RJ_PACKT, th + L.at(P_WK, top), m->WkT, D, D),
+      job(RJ_PACKT, th + L.at(P_WV, top), m->WvT, D, D),
   };
-  bool ok = launch_refresh(m->bf, jobs, (int)(sizeof(jobs) / sizeof(jobs[0])), s);
+  const int njobs = (int)(sizeof(jobs) / sizeof(jobs[0])) - (m->WkT ? 0 : 2);
+  bool ok = launch_refresh(m->bf, jobs, njobs, s);
   // untied FFN: the packed copies of repeats 1 .. k-1
   const int64_t es_ = m->bf ? 2 : 4;
   for (int r = 1; ok && m->cfg.untied_ffn && r < m->cfg.k; ++r) {
@@ -277,6 +287,7 @@ GemmArgs gemm(int M, int N, int K, const float* A, int64_t sam, int64_t sak, int
   g.beta = beta;
   g.gelu_u = nullptr;
   g.halfA = g.halfB = g.halfC = 0;
+  g.Cin = nullptr;
   return g;
 }
 
@@ -483,6 +494,8 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
          dalloc(m, &m->dV, K * T * D * 4) && dalloc(m, &m->dX, K * T * D * 4) && dalloc(m, &m->Xk, K * T * D * es) &&
          dalloc(m, &m->sP, (2 * T + 2) * D * 4) &&
          dalloc(m, &m->apart, attn_bwd_part_floats(K, T, D, cfg->H) * 4) &&
+         dalloc(m, &m->dSc, K * cfg->H * T * 4) &&
+         (!bf || (dalloc(m, &m->WkT, (int64_t)D * D * 2) && dalloc(m, &m->WvT, (int64_t)D * D * 2))) &&
          dalloc(m, &m->gws, (m->gws_cap = adapt_gemm_ws(m, K)) * 4) &&
          dalloc(m, &m->ews, embed_bwd_ws_floats(K * W, cfg->e) * 4) &&
          dalloc(m, &m->cws, colsum_ws_floats(std::max<int64_t>(2 * T * D, 256)) * 4) &&
@@ -793,7 +806,11 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // dY_r = dY_{r+1} + dU_r . W1^T; once dU_r exists the side stream forms
   // dW2 += G_r^T . dY_{r+1} and dW1 += Y_r^T . dU_r (accumulated over the repeats
   // in reverse; G = GELU(U) at its storage point: kept by the bf16 forward,
-  // formed here otherwise)
+  // formed here otherwise).  With shared weights and G kept, the sums over the
+  // repeats are single products over k N rows instead (the per-repeat buffers
+  // are consecutive: G_0..G_{k-1} with dY_1..dY_k, Y_0..Y_{k-1} with dU_0..dU_{k-1}),
+  // formed once the last repeat's dU_0 exists.
+  const bool merged = m->kG && !m->cfg.untied_ffn;
   for (int r = k - 1; r >= 0; --r) {
     // untied FFN: repeat r's own W1, W2 and gradient blocks (each written once)
     const int64_t wr = m->cfg.untied_ffn ? (int64_t)r * D * F : 0;
@@ -802,22 +819,33 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
     gd.halfC = hf;
     ok = launch_gemm(gd, ws, m->gws_cap, s) && ok;
     order(m, s, w);  // dY_{r+1} and dU_r are complete
-    const float beta = (r == k - 1 || m->cfg.untied_ffn) ? 0.f : 1.f;
-    GemmArgs g2w;
-    if (m->kG) {
-      g2w = gemm(F, D, N, (const float*)(m->kG + (int64_t)r * N * F), 1, F, rb, dYr(r + 1), D, 1, rb,
-                 gr + L.at(P_W2, top) + wr, D, beta);
+    if (!merged) {
+      const float beta = (r == k - 1 || m->cfg.untied_ffn) ? 0.f : 1.f;
+      GemmArgs g2w;
+      if (m->kG) {
+        g2w = gemm(F, D, N, (const float*)(m->kG + (int64_t)r * N * F), 1, F, rb, dYr(r + 1), D, 1, rb,
+                   gr + L.at(P_W2, top) + wr, D, beta);
+        g2w.halfA = 1;
+      } else {
+        launch_gelu_fwd_round(m->kU + (int64_t)r * N * F, m->G, (int64_t)N * F, rb, w);
+        g2w = gemm(F, D, N, m->G, 1, F, rb, dYr(r + 1), D, 1, rb, gr + L.at(P_W2, top) + wr, D, beta);
+      }
+      ok = launch_gemm(g2w, ws2, m->gws_cap, w) && ok;
+      GemmArgs g1w =
+          gemm(D, F, N, at(m->kY, (int64_t)r * N * D), 1, D, rb, dUr(r), F, 1, rb, gr + L.at(P_W1, top) + wr, F, beta);
+      g1w.halfA = g1w.halfB = hf;
+      ok = launch_gemm(g1w, ws2, m->gws_cap, w) && ok;
+    } else if (r == 0) {
+      GemmArgs g2w = gemm(F, D, k * N, (const float*)m->kG, 1, F, rb, dYr(1), D, 1, rb, gr + L.at(P_W2, top), D, 0.f);
       g2w.halfA = 1;
-    } else {
-      launch_gelu_fwd_round(m->kU + (int64_t)r * N * F, m->G, (int64_t)N * F, rb, w);
-      g2w = gemm(F, D, N, m->G, 1, F, rb, dYr(r + 1), D, 1, rb, gr + L.at(P_W2, top) + wr, D, beta);
+      ok = launch_gemm(g2w, ws2, m->gws_cap, w) && ok;
+      GemmArgs g1w = gemm(D, F, k * N, m->kY, 1, D, rb, m->dU, F, 1, rb, gr + L.at(P_W1, top), F, 0.f);
+      g1w.halfA = g1w.halfB = hf;
+      ok = launch_gemm(g1w, ws2, m->gws_cap, w) && ok;
     }
-    ok = launch_gemm(g2w, ws2, m->gws_cap, w) && ok;
-    GemmArgs g1w = gemm(D, F, N, at(m->kY, (int64_t)r * N * D), 1, D, rb, dUr(r), F, 1, rb, gr + L.at(P_W1, top) + wr, F, beta);
-    g1w.halfA = g1w.halfB = hf;
-    ok = launch_gemm(g1w, ws2, m->gws_cap, w) && ok;
-    (void)hipMemcpyAsync(dYr(r), dYr(r + 1), (size_t)N * D * 4, hipMemcpyDeviceToDevice, s);
+    // dY_r = dY_{r+1} + dU_r . W1^T (the addend read from dY_{r+1}'s own buffer)
     GemmArgs gy = gemm(N, D, F, dUr(r), F, 1, rb, th + L.at(P_W1, top) + wr, 1, F, rb, dYr(r), D, 1.f);
+    gy.Cin = dYr(r + 1);
     gy.halfA = hf;
     ok = launch_gemm(gy, ws, m->gws_cap, s) && ok;
   }
@@ -833,8 +861,9 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   float* sV = m->sP + (int64_t)T * D;
   float* sQ = m->sP + (int64_t)2 * T * D;
   float* sY = m->sP + (int64_t)(2 * T + 1) * D;
-  launch_attn_bwd(m->dO, m->kq, m->kK, m->kV, m->kA, N, T, D, H, (float)(1.0 / std::sqrt((double)L.DH)), rb, m->dQ,
-                  m->dK, m->dV, m->apart, sK, m->cws, s);
+  const float ascale = (float)(1.0 / std::sqrt((double)L.DH));
+  launch_attn_bwd(m->dO, m->kq, m->kK, m->kV, m->kA, N, T, D, H, ascale, rb, m->dQ, m->dK, m->dV, m->apart, sK, m->cws,
+                  s, m->bf ? m->dSc : nullptr);
   if (m->cfg.use_pos) launch_colsum(m->dQ, N, D, D, sQ, 0.f, m->cws, s);
   order(m, s, w);  // dQ, dK, dV and their sums over windows are complete
   // side: dWk = X^T dK, dWv = X^T dV (dK, dV stay fp32), with X = G + P[t]:
@@ -867,13 +896,19 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
                           gr + L.at(P_WQ, top), D, 0.f),
                      ws2, m->gws_cap, w) && ok;
   }
-  // dX = dK Wk^T + dV Wv^T (+ dQ Wq^T + dY_0 on the last token)
-  launch_gemm2(gemm(N * T, D, D, m->dK, D, 1, 0, th + L.at(P_WK, top), 1, D, rb, m->dX, D, 0.f),
-               gemm(N * T, D, D, m->dV, D, 1, 0, th + L.at(P_WV, top), 1, D, rb, m->dX, D, 0.f), ws, m->gws_cap, s);
+  // dX = dK Wk^T + dV Wv^T (+ dQ Wq^T + dY_0 on the last token).  bf16 models
+  // form the key and value part from the rank-one rows of dK and dV
+  // (launch_dx_rank1, which adds dY_0); otherwise two products over every token
+  // row, then dY_0
+  const bool rank1 = m->bf && m->WkT &&
+                     launch_dx_rank1(m->kq, m->dO, m->dSc, m->kA, m->WkT, m->WvT, dYr(0), N, T, D, H, ascale, m->dX, s);
+  if (!rank1)
+    launch_gemm2(gemm(N * T, D, D, m->dK, D, 1, 0, th + L.at(P_WK, top), 1, D, rb, m->dX, D, 0.f),
+                 gemm(N * T, D, D, m->dV, D, 1, 0, th + L.at(P_WV, top), 1, D, rb, m->dX, D, 0.f), ws, m->gws_cap, s);
   launch_gemm(gemm(N, D, D, m->dQ, D, 1, 0, th + L.at(P_WQ, top), 1, D, rb, m->dX + (int64_t)(T - 1) * D, (int64_t)T * D,
                    1.f),
               ws, m->gws_cap, s);
-  launch_add(m->dX + (int64_t)(T - 1) * D, dYr(0), N, D, (int64_t)T * D, D, s);
+  if (!rank1) launch_add(m->dX + (int64_t)(T - 1) * D, dYr(0), N, D, (int64_t)T * D, D, s);
   if (NL > 1) {
     // dX is the gradient w.r.t. the top layer's input: down through the lower
     // layers (on this stream, after the side stream's work: layer 0 reads Xk)
@@ -883,6 +918,9 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
       launch_colsum(m->dX, N, (int64_t)T * D, (int64_t)T * D, gr + L.off[P_P], 0.f, m->cws, s);
     else
       launch_zero(gr + L.off[P_P], L.size[P_P], s);
+  } else if (m->cfg.use_pos && rank1) {
+    // positional table: dP[t] = sum_n dX[n][t]
+    launch_colsum(m->dX, N, (int64_t)T * D, (int64_t)T * D, gr + L.off[P_P], 0.f, m->cws, s);
   } else if (m->cfg.use_pos) {
     // positional table: dP[t] = sum_n dX[n][t], from the sums over windows of
     // dK, dV, dQ and dY_0 times the weights; then the byte embedding

@@ -225,9 +225,9 @@ __device__ __forceinline__ void store_tile(const float4 (&vin)[8], uint32_t mask
 // that operand's contiguous dimension is k; SA / SB: that operand is split.
 // 1-D grid of tn * tm * splits blocks.
 template <bool AKC, bool BKC, bool SA, bool SB, bool HA, bool HB>
-__global__ __launch_bounds__(256) void k_bgemm(Src A, Src B, int Kp, int M, int N, float* __restrict__ C, int64_t ldc,
+__global__ __launch_bounds__(256) void k_bgemm(Src A, Src B, int Kp, int M, int N, float* C, int64_t ldc,
                                                float beta, float* __restrict__ part, int kchunk, int tn, int tm,
-                                               const float* __restrict__ gu, int hc) {
+                                               const float* __restrict__ gu, int hc, const float* cin) {
   static_assert(!(SA && SB), "at most one operand is split");
   constexpr int NT = 2 + (SA ? 1 : 0) + (SB ? 1 : 0);  // tiles per stage: A hi, B hi, [A lo | B lo]
   __shared__ uint4 lds[2][NT][UNITS];
@@ -318,7 +318,8 @@ __global__ __launch_bounds__(256) void k_bgemm(Src A, Src B, int Kp, int M, int 
         }
       }
   } else {
-    // with beta = 1, all the old values of C are read before any is written
+    // with beta = 1, all the values of Cin (which may be C) are read before any
+    // C is written
     if (beta != 0.f) {  // clamped addresses, as for gu below
 #pragma unroll
       for (int rf = 0; rf < 4; ++rf) {
@@ -327,7 +328,7 @@ __global__ __launch_bounds__(256) void k_bgemm(Src A, Src B, int Kp, int M, int 
         for (int r = 0; r < 4; ++r) {
           const int64_t mo = (int64_t)min(mb + rf * 16 + r, M - 1) * ldc;
 #pragma unroll
-          for (int nf = 0; nf < 4; ++nf) c[r][nf] = C[mo + min(nbase + nf * 16, N - 1)];
+          for (int nf = 0; nf < 4; ++nf) c[r][nf] = cin[mo + min(nbase + nf * 16, N - 1)];
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r)
@@ -532,9 +533,9 @@ __device__ __forceinline__ void store(const float4 (&v)[4], uint32_t mask, uint4
 }
 
 template <bool AKC, bool BKC, bool SA, bool SB, bool HA, bool HB>
-__global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, int N, float* __restrict__ C,
-                                                   int64_t ldc, float beta, float* __restrict__ part, int kchunk, int tn,
-                                                   int tm, const float* __restrict__ gu, int hc) {
+__global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, int N, float* C, int64_t ldc,
+                                                   float beta, float* __restrict__ part, int kchunk, int tn, int tm,
+                                                   const float* __restrict__ gu, int hc, const float* cin) {
   static_assert(!(SA && SB), "at most one operand is split");
   constexpr int NT = 2 + (SA ? 1 : 0) + (SB ? 1 : 0);
   constexpr int FM = SA ? 4 : 8, FN = SA ? 8 : 4;  // 16 x 16 fragments per wave along m, n
@@ -625,7 +626,7 @@ __global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, 
         for (int r = 0; r < 4; ++r) {
           const int64_t mo = (int64_t)min(mb + rf * 16 + r, M - 1) * ldc;
 #pragma unroll
-          for (int nf = 0; nf < FN; ++nf) c[r][nf] = C[mo + min(nbase + nf * 16, N - 1)];
+          for (int nf = 0; nf < FN; ++nf) c[r][nf] = cin[mo + min(nbase + nf * 16, N - 1)];
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r)
@@ -686,7 +687,7 @@ void launch_orient(bool sa, bool sb, bool ha, bool hb, dim3 grid, const Src& A, 
                    float* part, int kchunk, int tn, int tm, hipStream_t s) {
 #define TRACE_BGEMM(SA_, SB_, HA_, HB_)                                                                       \
   hipLaunchKernelGGL((k_bgemm_big<AKC, BKC, SA_, SB_, HA_, HB_>), grid, dim3(512), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc, \
-                     g.beta, part, kchunk, tn, tm, g.gelu_u, g.halfC)
+                     g.beta, part, kchunk, tn, tm, g.gelu_u, g.halfC, g.Cin ? g.Cin : g.C)
   if (sa) {
     if (hb)
       TRACE_BGEMM(true, false, false, true);
@@ -753,7 +754,7 @@ void launch_orient(bool sa, bool sb, bool ha, bool hb, dim3 grid, const Src& A, 
                    float* part, int kchunk, int tn, int tm, hipStream_t s) {
 #define TRACE_BGEMM(SA_, SB_, HA_, HB_)                                                                       \
   hipLaunchKernelGGL((k_bgemm<AKC, BKC, SA_, SB_, HA_, HB_>), grid, dim3(256), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc, \
-                     g.beta, part, kchunk, tn, tm, g.gelu_u, g.halfC)
+                     g.beta, part, kchunk, tn, tm, g.gelu_u, g.halfC, g.Cin ? g.Cin : g.C)
   if (sa) {
     if (hb)
       TRACE_BGEMM(true, false, false, true);
@@ -849,6 +850,6 @@ bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_c
     else
       launch_orient<false, false>(sa, sb, ha, hb, grid, A, B, Kp, g, part, kchunk, tn, tm, s);
   }
-  if (splits > 1) launch_splitk_reduce(ws, splits, g.M, g.N, g.C, g.ldc, g.beta, s);
+  if (splits > 1) launch_splitk_reduce(ws, splits, g.M, g.N, g.C, g.ldc, g.beta, g.Cin, s);
   return true;
 }

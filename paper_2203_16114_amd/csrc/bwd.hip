@@ -104,14 +104,14 @@ __global__ __launch_bounds__(256) void k_gemm(GemmArgs g, float* __restrict__ pa
 
 // C(m,n) = [C(m,n) +] sum_z part[z][m][n], z in increasing order.
 __global__ void k_splitk_reduce(const float* __restrict__ part, int splits, int M, int N, float* C, int64_t ldc,
-                                float beta) {
+                                float beta, const float* cin) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= (int64_t)M * N) return;
   const int m = (int)(i / N), n = (int)(i % N);
   float s = 0.f;
   for (int z = 0; z < splits; ++z) s += part[((int64_t)z * M + m) * N + n];
-  float* c = C + (int64_t)m * ldc + n;
-  *c = (beta != 0.f) ? (*c + s) : s;
+  const int64_t o = (int64_t)m * ldc + n;
+  C[o] = (beta != 0.f) ? (cin[o] + s) : s;
 }
 
 // 128x128-tile GEMM for the two operand layouts of the update: operands whose
@@ -323,15 +323,16 @@ static void launch128(const GemmArgs& g, float* part, int kchunk, dim3 grid, hip
     hipLaunchKernelGGL((k_gemm128<MODE, false, false>), grid, dim3(256), 0, s, g, part, kchunk);
 }
 
-// Four consecutive n per thread, eight partials in flight; the same sum order
-// (z increasing) as k_splitk_reduce.
+// Four consecutive n per thread (one float4 of C and of each partial), eight
+// partials in flight; the same sum order (z increasing, then the addend) as
+// k_splitk_reduce.  Needs N, ldc multiples of 4 and 16-byte aligned C, cin.
 __global__ __launch_bounds__(256) void k_splitk_reduce4(const float* __restrict__ part, int splits, int M, int N,
-                                                        float* C, int64_t ldc, float beta) {
-  const int64_t i = ((int64_t)blockIdx.x * 256 + threadIdx.x) * 4;
+                                                        float* C, int64_t ldc, float beta, const float* cin) {
+  const uint32_t q = blockIdx.x * 256u + threadIdx.x, n4 = (uint32_t)N >> 2;
+  if (q >= (uint32_t)M * n4) return;
+  const uint32_t m = q / n4, n = (q - m * n4) * 4;
   const int64_t MN = (int64_t)M * N;
-  if (i >= MN) return;
-  const int m = (int)(i / N), n = (int)(i % N);
-  const float* p = part + i;
+  const float* p = part + (int64_t)m * N + n;
   float4 s = make_float4(0.f, 0.f, 0.f, 0.f);
   auto add = [&](const float4& v) {
     s.x += v.x;
@@ -348,34 +349,35 @@ __global__ __launch_bounds__(256) void k_splitk_reduce4(const float* __restrict_
     for (int j = 0; j < 8; ++j) add(v[j]);
   }
   for (; z < splits; ++z) add(*reinterpret_cast<const float4*>(p + (int64_t)z * MN));
-  float* c = C + (int64_t)m * ldc + n;
-  if (beta != 0.f) {
-    s.x += c[0];
-    s.y += c[1];
-    s.z += c[2];
-    s.w += c[3];
-  }
-  c[0] = s.x;
-  c[1] = s.y;
-  c[2] = s.z;
-  c[3] = s.w;
+  const int64_t o = (int64_t)m * ldc + n;
+  if (beta != 0.f) add(*reinterpret_cast<const float4*>(cin + o));
+  *reinterpret_cast<float4*>(C + o) = s;
 }
 
-void launch_splitk_reduce(const float* ws, int splits, int M, int N, float* C, int64_t ldc, float beta, hipStream_t s) {
+void launch_splitk_reduce(const float* ws, int splits, int M, int N, float* C, int64_t ldc, float beta,
+                          const float* cin, hipStream_t s) {
+  if (!cin) cin = C;
   const int64_t tot = (int64_t)M * N;
-  if (N % 4 == 0 && ((uintptr_t)ws & 15) == 0)
+  if (N % 4 == 0 && ldc % 4 == 0 && ((uintptr_t)ws & 15) == 0 && ((uintptr_t)C & 15) == 0 &&
+      ((uintptr_t)cin & 15) == 0)
     hipLaunchKernelGGL(k_splitk_reduce4, dim3((unsigned)((tot / 4 + 255) / 256)), dim3(256), 0, s, ws, splits, M, N, C,
-                       ldc, beta);
+                       ldc, beta, cin);
   else
     hipLaunchKernelGGL(k_splitk_reduce, dim3((unsigned)((tot + 255) / 256)), dim3(256), 0, s, ws, splits, M, N, C, ldc,
-                       beta);
+                       beta, cin);
 }
 
-bool launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s) {
-  if (g.M <= 0 || g.N <= 0) return true;
+bool launch_gemm(const GemmArgs& g0, float* ws, int64_t ws_cap, hipStream_t s) {
+  if (g0.M <= 0 || g0.N <= 0) return true;
   // bf16 storage points on at least one side: register-staged bf16 GEMM
-  if (launch_bgemm(g, nullptr, ws, ws_cap, s)) return true;
-  if (g.halfA || g.halfB || g.halfC) return false;  // the kernels below use fp32 operands and results
+  if (launch_bgemm(g0, nullptr, ws, ws_cap, s)) return true;
+  if (g0.halfA || g0.halfB || g0.halfC) return false;  // the kernels below use fp32 operands and results
+  GemmArgs g = g0;
+  if (g.Cin && g.Cin != g.C && g.beta != 0.f) {  // the kernels below add C itself: the addend goes there first
+    (void)hipMemcpy2DAsync(g.C, (size_t)g.ldc * 4, g.Cin, (size_t)g.ldc * 4, (size_t)g.N * 4, (size_t)g.M,
+                           hipMemcpyDeviceToDevice, s);
+  }
+  g.Cin = nullptr;
   if (g.gelu_u) {  // the product, then the GELU derivative in place (C laid out densely, as gelu_u)
     GemmArgs h = g;
     h.gelu_u = nullptr;
@@ -408,7 +410,7 @@ bool launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s) {
     else
       hipLaunchKernelGGL(k_gemm<false>, grid, dim3(256), 0, s, g, part, kchunk);
   }
-  if (splits > 1) launch_splitk_reduce(ws, splits, g.M, g.N, g.C, g.ldc, g.beta, s);
+  if (splits > 1) launch_splitk_reduce(ws, splits, g.M, g.N, g.C, g.ldc, g.beta, nullptr, s);
   return true;
 }
 
@@ -454,14 +456,19 @@ __global__ __launch_bounds__(256) void k_colsum2(const float* __restrict__ ws, i
     out[c] = (beta != 0.f) ? out[c] + tot : tot;
   }
 }
-// four columns per thread, eight rows in flight; the same sum order as k_colsum1
-__global__ __launch_bounds__(64) void k_colsum1v(const float* __restrict__ in, int64_t rows, int64_t cols, int64_t ld,
-                                                 float* __restrict__ ws) {
-  const int64_t c = ((int64_t)blockIdx.x * 64 + threadIdx.x) * 4;
-  if (c >= cols) return;
+// four columns per thread, eight rows in flight; the four waves of a block
+// take consecutive quarters of the split's rows, and their sums are added in
+// wave order
+__global__ __launch_bounds__(256) void k_colsum1v(const float* __restrict__ in, int64_t rows, int64_t cols, int64_t ld,
+                                                  float* __restrict__ ws) {
+  __shared__ float4 red[4][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int64_t c = ((int64_t)blockIdx.x * 64 + lane) * 4;
   const int s = blockIdx.y;
   const int64_t chunk = (rows + COLSUM_SPLITS - 1) / COLSUM_SPLITS;
-  const int64_t r0 = s * chunk, r1 = min(rows, r0 + chunk);
+  const int64_t r0s = s * chunk, r1s = min(rows, r0s + chunk);
+  const int64_t sub = (chunk + 3) / 4;
+  const int64_t r0 = r0s + wave * sub, r1 = min(r1s, r0 + sub);
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   auto add = [&](const float4& v) {
     acc.x += v.x;
@@ -469,23 +476,38 @@ __global__ __launch_bounds__(64) void k_colsum1v(const float* __restrict__ in, i
     acc.z += v.z;
     acc.w += v.w;
   };
-  int64_t r = r0;
-  for (; r + 8 <= r1; r += 8) {
-    float4 v[8];
+  if (c < cols) {
+    int64_t r = r0;
+    for (; r + 8 <= r1; r += 8) {
+      float4 v[8];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = *reinterpret_cast<const float4*>(in + (r + j) * ld + c);
+      for (int j = 0; j < 8; ++j) v[j] = *reinterpret_cast<const float4*>(in + (r + j) * ld + c);
 #pragma unroll
-    for (int j = 0; j < 8; ++j) add(v[j]);
+      for (int j = 0; j < 8; ++j) add(v[j]);
+    }
+    for (; r < r1; ++r) add(*reinterpret_cast<const float4*>(in + r * ld + c));
   }
-  for (; r < r1; ++r) add(*reinterpret_cast<const float4*>(in + r * ld + c));
-  *reinterpret_cast<float4*>(ws + s * cols + c) = acc;
+  red[wave][lane] = acc;
+  __syncthreads();
+  if (wave == 0 && c < cols) {
+    float4 t = red[0][lane];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) {
+      const float4 v = red[w][lane];
+      t.x += v.x;
+      t.y += v.y;
+      t.z += v.z;
+      t.w += v.w;
+    }
+    *reinterpret_cast<float4*>(ws + s * cols + c) = t;
+  }
 }
 int64_t colsum_ws_floats(int64_t cols) { return COLSUM_SPLITS * cols; }
 void launch_colsum(const float* in, int64_t rows, int64_t cols, int64_t ld, float* out, float beta, float* ws,
                    hipStream_t s) {
   const unsigned gx = (unsigned)((cols + 255) / 256);
   if (cols % 4 == 0 && ld % 4 == 0 && ((uintptr_t)in & 15) == 0)
-    hipLaunchKernelGGL(k_colsum1v, dim3(gx, COLSUM_SPLITS), dim3(64), 0, s, in, rows, cols, ld, ws);
+    hipLaunchKernelGGL(k_colsum1v, dim3(gx, COLSUM_SPLITS), dim3(256), 0, s, in, rows, cols, ld, ws);
   else
     hipLaunchKernelGGL(k_colsum1, dim3(gx, COLSUM_SPLITS), dim3(256), 0, s, in, rows, cols, ld, ws);
   hipLaunchKernelGGL(k_colsum2, dim3((unsigned)((cols + 63) / 64)), dim3(256), 0, s, ws, cols, out, beta);
@@ -551,8 +573,26 @@ __global__ void k_add(float* __restrict__ y, const float* __restrict__ x, int64_
   const int64_t r = i / cols, c = i % cols;
   y[r * ldy + c] += x[r * ldx + c];
 }
+// the same, four columns per thread (cols, ldy, ldx multiples of 4, 16-byte aligned rows)
+__global__ __launch_bounds__(256) void k_add4(float* __restrict__ y, const float* __restrict__ x, uint32_t rows,
+                                              uint32_t cols4, int64_t ldy, int64_t ldx) {
+  const uint32_t q = blockIdx.x * 256u + threadIdx.x;
+  if (q >= rows * cols4) return;
+  const uint32_t r = q / cols4, c = (q - r * cols4) * 4;
+  float4* py = reinterpret_cast<float4*>(y + r * ldy + c);
+  const float4 a = *py, b = *reinterpret_cast<const float4*>(x + r * ldx + c);
+  *py = make_float4(a.x + b.x, a.y + b.y, a.z + b.z, a.w + b.w);
+}
 void launch_add(float* y, const float* x, int64_t rows, int64_t cols, int64_t ldy, int64_t ldx, hipStream_t s) {
-  hipLaunchKernelGGL(k_add, dim3((unsigned)((rows * cols + 255) / 256)), dim3(256), 0, s, y, x, rows, cols, ldy, ldx);
+  if (rows <= 0 || cols <= 0) return;
+  if (cols % 4 == 0 && ldy % 4 == 0 && ldx % 4 == 0 && ((uintptr_t)y & 15) == 0 && ((uintptr_t)x & 15) == 0 &&
+      rows * cols / 4 < ((int64_t)1 << 32)) {
+    const int64_t n4 = rows * cols / 4;
+    hipLaunchKernelGGL(k_add4, dim3((unsigned)((n4 + 255) / 256)), dim3(256), 0, s, y, x, (uint32_t)rows,
+                       (uint32_t)(cols / 4), ldy, ldx);
+  } else {
+    hipLaunchKernelGGL(k_add, dim3((unsigned)((rows * cols + 255) / 256)), dim3(256), 0, s, y, x, rows, cols, ldy, ldx);
+  }
 }
 
 // ------------------------------------------------------- attention backward ----
@@ -570,7 +610,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd2(const float* __restrict__ dO,
                                                    const float* __restrict__ A, int64_t N, int T, int D, int H,
                                                    float scale, int round_dO, float* __restrict__ dQ,
                                                    float* __restrict__ dK, float* __restrict__ dV,
-                                                   float* __restrict__ part) {
+                                                   float* __restrict__ part, float* __restrict__ dS) {
   constexpr int PW = 64 / DH;  // windows per wave
   constexpr int CH = 4 * PW;   // windows per block
   __shared__ float red[2][CH][8][DH];
@@ -603,6 +643,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd2(const float* __restrict__ dO,
   for (int u = 0; u < 8; ++u) {
     if (u < T) {
       const float ds = a[u] * (dA[u] - tot);
+      if (dS && live && c == 0) dS[(nn * H + h) * T + u] = ds;
       dq = fmaf(ds, K[(nn * T + u) * D + col], dq);
       const float dk = (ds * qv) * scale, dv = a[u] * o;
       if (live) {
@@ -630,17 +671,174 @@ int64_t attn_bwd_part_floats(int64_t N, int T, int D, int H) { return attn_bwd_c
 
 void launch_attn_bwd(const float* dO, const float* q, const float* K, const float* V, const float* A, int64_t N, int T,
                      int D, int H, float scale, int round_dO, float* dQ, float* dK, float* dV, float* part,
-                     float* colsums, float* cws, hipStream_t s) {
+                     float* colsums, float* cws, hipStream_t s, float* dS) {
   const int DH = D / H;
   const int64_t chunks = attn_bwd_chunks(N, D, H);
   const dim3 grid((unsigned)(chunks * H));
   if (DH == 32)
     hipLaunchKernelGGL(k_attn_bwd2<32>, grid, dim3(256), 0, s, dO, q, K, V, A, N, T, D, H, scale, round_dO, dQ, dK,
-                       dV, part);
+                       dV, part, dS);
   else
     hipLaunchKernelGGL(k_attn_bwd2<64>, grid, dim3(256), 0, s, dO, q, K, V, A, N, T, D, H, scale, round_dO, dQ, dK,
-                       dV, part);
+                       dV, part, dS);
   launch_colsum(part, chunks, (int64_t)2 * T * D, (int64_t)2 * T * D, colsums, 0.f, cws, s);
+}
+
+// Input gradient of the tokens through the keys and values, bf16 models:
+// dX[n][t] = sum_h dK_h[n][t] . Wk_h^T + dV_h[n][t] . Wv_h^T with the rank-one
+// rows dK_h[n][t] = dS[n][h][t] (scale q_h[n]) and dV_h[n][t] = A[n][h][t]
+// bf(dO_h[n]), so that
+//   dX[n][t] = sum_h dS[n][h][t] QK[n][h] + A[n][h][t] OV[n][h],
+//   QK[n][h] = Wk_h . (scale q_h[n]),  OV[n][h] = Wv_h . bf(dO_h[n]),
+// where Wk_h is the head's D x DH column block (weights rounded to bf16 as the
+// product's operands).  QK and OV are formed on the matrix cores (scale q in
+// hi + lo bf16 parts, dO exact in bf16), 2 D DH flops each per window and head
+// instead of 2 T D DH for the products over every token row; the T-fold
+// combination runs on the vector ALUs.  dY0 (the residual's gradient) is added
+// to the last token.
+// One block of 8 waves per 16 windows (the 16 columns of the B operand); wave
+// w owns features [w D/8, (w+1) D/8), its accumulators acc[t][f] holding
+// features w D/8 + 16 f + 4 lg + r of window n0 + lc.  The block first stages
+// its windows' B operands (scale q as hi and lo, dO, in bf16; unit u of row m
+// at u ^ (m & 15)) and their score gradients and weights in LDS with coalesced
+// loads; the weights come as fragment-packed copies of Wk^T and Wv^T, one
+// contiguous 16-byte load per lane and fragment.  dX is stored without keeping
+// it in the caches (later kernels read it once).
+template <int D, int DH, int T>
+__global__ __launch_bounds__(512) void k_dx_rank1(const float* __restrict__ q, const float* __restrict__ dO,
+                                                  const float* __restrict__ dS, const float* __restrict__ A,
+                                                  const uint4* __restrict__ WkT, const uint4* __restrict__ WvT,
+                                                  const float* __restrict__ dY0, int64_t N, float scale,
+                                                  float* __restrict__ dX) {
+  constexpr int H = D / DH, KS = DH / 32, NF = D / 128, NB = D / 16;
+  constexpr int RU = D / 8;          // 16-byte units per staged row
+  constexpr int SST = H * T + 4;     // floats per staged score row (padded: conflict-free lane reads)
+  static_assert(D % 128 == 0 && DH % 32 == 0 && T <= 8 && T % 4 == 0, "shape");
+  typedef Mma<true> M;
+  __shared__ uint4 Bq[3][16 * RU];   // scale q hi, scale q lo, dO
+  __shared__ __align__(16) float Sds[2][16 * SST];  // dS, A
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, lg = lane >> 4, lc = lane & 15;
+  const int64_t n0 = (int64_t)blockIdx.x * 16;
+  const int nwin = (int)min<int64_t>(16, N - n0);
+  // stage: rows n0 .. n0 + 15 of q and dO (four floats per thread and step),
+  // of dS and A (rows past N: zeros)
+  for (int i = tid; i < 16 * D / 4; i += 512) {
+    const int m = i / (D / 4), c4 = i - m * (D / 4);
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f), o = v;
+    if (m < nwin) {
+      v = *reinterpret_cast<const float4*>(q + (n0 + m) * D + 4 * c4);
+      o = *reinterpret_cast<const float4*>(dO + (n0 + m) * D + 4 * c4);
+    }
+    v.x *= scale;
+    v.y *= scale;
+    v.z *= scale;
+    v.w *= scale;
+    const uint32_t h0 = pack_bf16x2(v.x, v.y), h1 = pack_bf16x2(v.z, v.w);
+    const uint32_t l0 = pack_bf16x2(v.x - __uint_as_float(h0 << 16), v.y - __uint_as_float(h0 & 0xffff0000u));
+    const uint32_t l1 = pack_bf16x2(v.z - __uint_as_float(h1 << 16), v.w - __uint_as_float(h1 & 0xffff0000u));
+    const int off = (m * RU + ((c4 >> 1) ^ (m & 15))) * 16 + 8 * (c4 & 1);  // bytes
+    *reinterpret_cast<uint2*>(reinterpret_cast<unsigned char*>(Bq[0]) + off) = make_uint2(h0, h1);
+    *reinterpret_cast<uint2*>(reinterpret_cast<unsigned char*>(Bq[1]) + off) = make_uint2(l0, l1);
+    *reinterpret_cast<uint2*>(reinterpret_cast<unsigned char*>(Bq[2]) + off) =
+        make_uint2(pack_bf16x2(o.x, o.y), pack_bf16x2(o.z, o.w));
+  }
+  for (int i = tid; i < 2 * 16 * H * T; i += 512) {
+    const int which = i / (16 * H * T), j = i - which * (16 * H * T), m = j / (H * T), c = j - m * (H * T);
+    Sds[which][m * SST + c] = m < nwin ? (which ? A : dS)[(n0 + m) * H * T + c] : 0.f;
+  }
+  __syncthreads();
+
+  const int d0 = wave * (D / 8);
+  float acc[T][NF][4];
+#pragma unroll
+  for (int t = 0; t < T; ++t)
+#pragma unroll
+    for (int f = 0; f < NF; ++f)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) acc[t][f][r] = 0.f;
+  for (int h = 0; h < H; ++h) {
+    // A fragments (rows d0 + 16 f + lc, k = 32 (h KS + ks) + 8 lg + j): fragment
+    // (ks', nb) of the packed copy at ((ks' NB + nb) 64 + lane)
+    uint4 ak[NF][KS], av[NF][KS];
+#pragma unroll
+    for (int f = 0; f < NF; ++f)
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        const int64_t fi = ((int64_t)(h * KS + ks) * NB + d0 / 16 + f) * 64 + lane;
+        ak[f][ks] = WkT[fi];
+        av[f][ks] = WvT[fi];
+      }
+    uint4 bqh[KS], bql[KS], bo[KS];
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int u = ((h * KS + ks) * 4 + lg) ^ lc;
+      bqh[ks] = Bq[0][lc * RU + u];
+      bql[ks] = Bq[1][lc * RU + u];
+      bo[ks] = Bq[2][lc * RU + u];
+    }
+    float ds[T], aa[T];
+#pragma unroll
+    for (int t = 0; t < T; t += 4) {
+      const float4 x = *reinterpret_cast<const float4*>(&Sds[0][lc * SST + h * T + t]);
+      const float4 y = *reinterpret_cast<const float4*>(&Sds[1][lc * SST + h * T + t]);
+      ds[t] = x.x; ds[t + 1] = x.y; ds[t + 2] = x.z; ds[t + 3] = x.w;
+      aa[t] = y.x; aa[t + 1] = y.y; aa[t + 2] = y.z; aa[t + 3] = y.w;
+    }
+#pragma unroll
+    for (int f = 0; f < NF; ++f) {
+      f32x4 qk = f32x4{0.f, 0.f, 0.f, 0.f}, ov = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int ks = 0; ks < KS; ++ks) {
+        M::run(qk, ak[f][ks], bqh[ks]);
+        M::run(qk, ak[f][ks], bql[ks]);
+        M::run(ov, av[f][ks], bo[ks]);
+      }
+#pragma unroll
+      for (int t = 0; t < T; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) acc[t][f][r] = fmaf(aa[t], ov[r], fmaf(ds[t], qk[r], acc[t][f][r]));
+    }
+  }
+  if (lc >= nwin) return;
+  const int64_t n = n0 + lc;
+#pragma unroll
+  for (int f = 0; f < NF; ++f) {
+    const int d = d0 + 16 * f + 4 * lg;
+    const float4 y = *reinterpret_cast<const float4*>(dY0 + n * D + d);
+    acc[T - 1][f][0] += y.x;
+    acc[T - 1][f][1] += y.y;
+    acc[T - 1][f][2] += y.z;
+    acc[T - 1][f][3] += y.w;
+#pragma unroll
+    for (int t = 0; t < T; ++t) {
+      const f32x4 v = f32x4{acc[t][f][0], acc[t][f][1], acc[t][f][2], acc[t][f][3]};
+      __builtin_nontemporal_store(v, reinterpret_cast<f32x4*>(dX + (n * T + t) * D + d));
+    }
+  }
+}
+
+template <int D, int DH, int T>
+static void launch_dx_rank1_t(const float* q, const float* dO, const float* dS, const float* A, const uint4* WkT,
+                              const uint4* WvT, const float* dY0, int64_t N, float scale, float* dX, hipStream_t s) {
+  hipLaunchKernelGGL((k_dx_rank1<D, DH, T>), dim3((unsigned)((N + 15) / 16)), dim3(512), 0, s, q, dO, dS, A, WkT, WvT,
+                     dY0, N, scale, dX);
+}
+
+bool launch_dx_rank1(const float* q, const float* dO, const float* dS, const float* A, const uint4* WkT,
+                     const uint4* WvT, const float* dY0, int64_t N, int T, int D, int H, float scale, float* dX,
+                     hipStream_t s) {
+  if (N <= 0) return true;
+  const int DH = D / H;
+#define TRACE_DXR(D_, DH_, T_)                                                                      \
+  if (D == D_ && DH == DH_ && T == T_) {                                                           \
+    launch_dx_rank1_t<D_, DH_, T_>(q, dO, dS, A, WkT, WvT, dY0, N, scale, dX, s);                  \
+    return true;                                                                                   \
+  }
+  TRACE_DXR(128, 32, 4) TRACE_DXR(128, 32, 8) TRACE_DXR(128, 64, 4) TRACE_DXR(128, 64, 8)
+  TRACE_DXR(256, 32, 4) TRACE_DXR(256, 32, 8) TRACE_DXR(256, 64, 4) TRACE_DXR(256, 64, 8)
+  TRACE_DXR(512, 64, 4) TRACE_DXR(512, 64, 8)
+#undef TRACE_DXR
+  return false;
 }
 
 // dP[t][c] = sum_j sK[t][j] Wk[c][j] + sV[t][j] Wv[c][j], plus, for t = T-1,
@@ -860,7 +1058,7 @@ __global__ __launch_bounds__(1024) void k_emb_scatter(const uint8_t* __restrict_
 __global__ __launch_bounds__(64) void k_emb_piece(const float* __restrict__ dX, int e, const int* __restrict__ perm,
                                                   const int* __restrict__ piece, const int* __restrict__ pstart,
                                                   float* __restrict__ part) {
-  constexpr int B = 16;  // loads in flight per lane
+  constexpr int B = 32;  // loads in flight per lane
   const int p = blockIdx.x;
   if (p >= pstart[256]) return;
   const int st = piece[3 * p + 1], len = piece[3 * p + 2];
@@ -969,9 +1167,30 @@ __global__ __launch_bounds__(256) void k_gather_kept(const uint8_t* __restrict__
     *reinterpret_cast<float4*>((float*)X + row * D + c) =
         make_float4(M::val(src[0]), M::val(src[1]), M::val(src[2]), M::val(src[3]));
 }
+// bf16 with e a multiple of 8: eight consecutive columns per thread, one
+// 16-byte load of the embedding row and one 16-byte store
+__global__ __launch_bounds__(256) void k_gather_kept8(const uint8_t* __restrict__ win, int64_t rows,
+                                                      const uint16_t* __restrict__ E, int T, int D, int e, int g,
+                                                      uint16_t* __restrict__ X) {
+  const uint32_t q8 = (uint32_t)D / 8;
+  const uint32_t i = blockIdx.x * 256u + threadIdx.x;  // the grid has fewer than 2^32 threads
+  if ((int64_t)i >= rows * q8) return;
+  const uint32_t row32 = i / q8;
+  const int64_t row = row32;
+  const int c = (int)(i - row32 * q8) * 8;
+  const int j = c / e, cc = c - j * e;
+  const int byte = win[row * g + j];
+  *reinterpret_cast<uint4*>(X + row * D + c) = *reinterpret_cast<const uint4*>(E + byte * e + cc);
+}
 void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, int T, int D, int e, int g, void* X,
                         hipStream_t s) {
   const int64_t rows = N * T;
+  if (bf && e % 8 == 0 && ((uintptr_t)E & 15) == 0 && ((uintptr_t)X & 15) == 0) {
+    const dim3 grid8((unsigned)((rows * (D / 8) + 255) / 256));
+    hipLaunchKernelGGL(k_gather_kept8, grid8, dim3(256), 0, s, win, rows, (const uint16_t*)E, T, D, e, g,
+                       (uint16_t*)X);
+    return;
+  }
   const dim3 grid((unsigned)((rows * (D / 4) + 255) / 256));
   if (bf)
     hipLaunchKernelGGL(k_gather_kept<true>, grid, dim3(256), 0, s, win, rows, (const uint16_t*)E, T, D, e, g, X);

@@ -44,8 +44,13 @@ __device__ __forceinline__ void refresh_pack(const RefreshJob& jb, int64_t i) {
   const int n = nb * 16 + (lane & 15);
   const int kb = ks * M::KS + (lane >> 4) * M::EPF;
   float v[8];
+  if (jb.kind == RJ_PACKT) {  // src is [N][K]: element (k, n) of its transpose at src[n * K + k]
 #pragma unroll
-  for (int j = 0; j < M::EPF; ++j) v[j] = jb.src[(int64_t)(kb + j) * jb.N + n] * jb.scale;
+    for (int j = 0; j < M::EPF; ++j) v[j] = jb.src[(int64_t)n * jb.K + kb + j] * jb.scale;
+  } else {
+#pragma unroll
+    for (int j = 0; j < M::EPF; ++j) v[j] = jb.src[(int64_t)(kb + j) * jb.N + n] * jb.scale;
+  }
   union { uint4 u; typename M::T t[M::EPF]; } r;
 #pragma unroll
   for (int j = 0; j < M::EPF; ++j) r.t[j] = M::cvt(v[j]);
@@ -121,7 +126,7 @@ __global__ __launch_bounds__(256) void k_refresh(RefreshArgs a) {
   typedef Mma<BF> M;
   if (jb.kind == RJ_CVT) {
     if (i < jb.K) reinterpret_cast<typename M::T*>(jb.dst)[i] = M::cvt(jb.src[i]);
-  } else if (jb.kind == RJ_PACK) {
+  } else if (jb.kind == RJ_PACK || jb.kind == RJ_PACKT) {
     refresh_pack<BF>(jb, i);
   } else if (jb.kind == RJ_PTAB) {
     if (jb.K == 8)
@@ -142,7 +147,7 @@ bool launch_refresh(bool bf, const RefreshJob* jobs, int n, hipStream_t s) {
     int64_t nb = 0;
     if (jb.kind == RJ_CVT || jb.kind == RJ_ZERO) {
       nb = ((int64_t)jb.K + 255) / 256;
-    } else if (jb.kind == RJ_PACK) {
+    } else if (jb.kind == RJ_PACK || jb.kind == RJ_PACKT) {
       const int KS = bf ? 32 : 16;
       if (jb.K % KS != 0 || jb.N % 16 != 0) return false;
       nb = ((int64_t)(jb.K / KS) * (jb.N / 16) * 64 + 255) / 256;

@@ -68,7 +68,8 @@ void launch_step_ce(const float* bits, int32_t n_streams, int32_t n_steps, doubl
 //            of 64, at most 512), with the operand
 //            values of P (src; zero if use_pos is 0) and of W_q (src2, W_k and W_v following it in the master)
 //   RJ_ZERO  K 32-bit words of dst cleared
-enum { RJ_CVT = 0, RJ_PACK = 1, RJ_PTAB = 2, RJ_ZERO = 3 };
+//   RJ_PACKT as RJ_PACK for the transpose of src: the copy of [K][N] src^T, src being [N][K] row-major
+enum { RJ_CVT = 0, RJ_PACK = 1, RJ_PTAB = 2, RJ_ZERO = 3, RJ_PACKT = 4 };
 struct RefreshJob {
   const float* src;
   const float* src2;
@@ -90,7 +91,9 @@ struct GemmArgs {
   float* C;
   int64_t ldc;       // C(m,n) = C[m*ldc + n]
   int roundA, roundB;  // round that operand to bf16 (RNE) as it is read
-  float beta;          // C = beta*C + A.B  (beta 0 or 1)
+  float beta;          // C = beta*Cin + A.B  (beta 0 or 1)
+  // nullable: the addend of beta (laid out as C, ldc apart); NULL: C itself
+  const float* Cin;
   // nullable: C = (A.B) * GELU'(gelu_u) elementwise, gelu_u laid out as C
   // (the backward of the FFN activation fused into its product); needs beta 0
   const float* gelu_u;
@@ -110,7 +113,8 @@ bool launch_gemm(const GemmArgs& g, float* ws, int64_t ws_cap, hipStream_t s);
 // C = beta*C + A1.B1 + A2.B2: g and g2 share M, N, C, ldc, beta and rounding
 // flags; one launch when the bf16 kernel takes both, else two
 void launch_gemm2(const GemmArgs& g, const GemmArgs& g2, float* ws, int64_t ws_cap, hipStream_t s);
-void launch_splitk_reduce(const float* ws, int splits, int M, int N, float* C, int64_t ldc, float beta, hipStream_t s);
+void launch_splitk_reduce(const float* ws, int splits, int M, int N, float* C, int64_t ldc, float beta,
+                          const float* cin, hipStream_t s);
 // bgemm.hip: false (nothing launched) when the product is not one it takes;
 // g2 (nullable) is a second K segment summed into the same result
 // force: 0 the kernel the shape calls for, 1 the 128-tile kernel, 2 the 256-tile kernel
@@ -123,9 +127,16 @@ int64_t colsum_ws_floats(int64_t cols);
 void launch_ce_grad(const float* z, const int32_t* tgt, int64_t N, float* dz, hipStream_t s);
 void launch_gelu_fwd_round(const float* U, float* G, int64_t n, int round, hipStream_t s);
 void launch_gelu_bwd(const float* dG, const float* U, float* dU, int64_t n, hipStream_t s);
+// dS (nullable): [N][H][T] gradients of the attention scores of the last row
 void launch_attn_bwd(const float* dO, const float* q, const float* K, const float* V, const float* A, int64_t N, int T,
                      int D, int H, float scale, int round_dO, float* dQ, float* dK, float* dV, float* part,
-                     float* colsums, float* cws, hipStream_t s);
+                     float* colsums, float* cws, hipStream_t s, float* dS = nullptr);
+// bf16 models: dX[n][t] (all T tokens) from the rank-one key and value
+// gradients plus dY0 on the last token; false when no kernel is built for the shape
+// WkT, WvT: fragment-packed bf16 copies of Wk^T and Wv^T (RJ_PACKT of the [D][D] masters)
+bool launch_dx_rank1(const float* q, const float* dO, const float* dS, const float* A, const uint4* WkT,
+                     const uint4* WvT, const float* dY0, int64_t N, int T, int D, int H, float scale, float* dX,
+                     hipStream_t s);
 int64_t attn_bwd_part_floats(int64_t N, int T, int D, int H);
 void launch_pos_table_grad(const float* sKV, const float* sQ, const float* sY, const float* Wq, const float* Wk,
                            const float* Wv, int T, int D, int rb, float* dP, hipStream_t s);
