@@ -288,6 +288,9 @@ GemmArgs gemm(int M, int N, int K, const float* A, int64_t sam, int64_t sak, int
   g.gelu_u = nullptr;
   g.halfA = g.halfB = g.halfC = 0;
   g.Cin = nullptr;
+  g.r1c = nullptr;
+  g.r1tsh = g.r1dsh = g.r1H = g.r1round = 0;
+  g.r1scale = 1.f;
   return g;
 }
 
@@ -862,19 +865,42 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   float* sQ = m->sP + (int64_t)2 * T * D;
   float* sY = m->sP + (int64_t)(2 * T + 1) * D;
   const float ascale = (float)(1.0 / std::sqrt((double)L.DH));
-  launch_attn_bwd(m->dO, m->kq, m->kK, m->kV, m->kA, N, T, D, H, ascale, rb, m->dQ, m->dK, m->dV, m->apart, sK, m->cws,
-                  s, m->bf ? m->dSc : nullptr);
+  // bf16 models: the key and value gradients are used through their rank-one
+  // rows dK_h[n][t] = dS[n][h][t] scale q_h[n], dV_h[n][t] = A[n][h][t] bf(dO_h[n])
+  // (the weight gradients' B operands are formed from them as they are read,
+  // and the input gradient of the tokens by k_dx_rank1): dK, dV are not stored
+  const bool pow2 = (T & (T - 1)) == 0 && (L.DH & (L.DH - 1)) == 0;
+  const bool rank1 = m->bf && m->WkT && pow2 && dx_rank1_built(T, D, H);
+  launch_attn_bwd(m->dO, m->kq, m->kK, m->kV, m->kA, N, T, D, H, ascale, rb, m->dQ, rank1 ? nullptr : m->dK,
+                  rank1 ? nullptr : m->dV, m->apart, sK, m->cws, s, m->bf ? m->dSc : nullptr);
+  auto log2i = [](int x) {
+    int r = 0;
+    while ((1 << r) < x) ++r;
+    return r;
+  };
+  // B of X^T dK (rank1: from dS and q) and of X^T dV (rank1: from A and bf(dO))
+  auto kv_grad = [&](const float* Aop, int64_t sam, int64_t sak, bool halfA, bool value, float* C) {
+    GemmArgs g = rank1 ? gemm(D, D, N * T, Aop, sam, sak, rb, value ? m->dO : m->kq, D, 1, 0, C, D, 0.f)
+                       : gemm(D, D, N * T, Aop, sam, sak, rb, value ? m->dV : m->dK, D, 1, 0, C, D, 0.f);
+    g.halfA = halfA ? 1 : 0;
+    if (rank1) {
+      g.r1c = value ? m->kA : m->dSc;
+      g.r1tsh = log2i(T);
+      g.r1dsh = log2i(L.DH);
+      g.r1H = H;
+      g.r1round = value ? rb : 0;
+      g.r1scale = value ? 1.f : ascale;
+    }
+    return launch_gemm(g, ws2, m->gws_cap, w);
+  };
   if (m->cfg.use_pos) launch_colsum(m->dQ, N, D, D, sQ, 0.f, m->cws, s);
   order(m, s, w);  // dQ, dK, dV and their sums over windows are complete
   // side: dWk = X^T dK, dWv = X^T dV (dK, dV stay fp32), with X = G + P[t]:
   // G^T dZ as GEMMs on the byte-embedding part G, then P^T (sum over windows of
   // dZ) for the positional part
   if (NL == 1) {
-    GemmArgs gk = gemm(D, D, N * T, m->Xk, 1, D, rb, m->dK, D, 1, 0, gr + L.at(P_WK, top), D, 0.f);
-    GemmArgs gv = gemm(D, D, N * T, m->Xk, 1, D, rb, m->dV, D, 1, 0, gr + L.at(P_WV, top), D, 0.f);
-    gk.halfA = gv.halfA = hf;
-    ok = launch_gemm(gk, ws2, m->gws_cap, w) && ok;
-    ok = launch_gemm(gv, ws2, m->gws_cap, w) && ok;
+    ok = kv_grad(m->Xk, 1, D, hf, false, gr + L.at(P_WK, top)) && ok;
+    ok = kv_grad(m->Xk, 1, D, hf, true, gr + L.at(P_WV, top)) && ok;
     if (m->cfg.use_pos) {
       launch_pos_grad(m->bf, m->Pc, sK, 0, T, D, gr + L.at(P_WK, top), w);
       launch_pos_grad(m->bf, m->Pc, sV, 0, T, D, gr + L.at(P_WV, top), w);
@@ -888,10 +914,8 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
     if (m->cfg.use_pos) launch_pos_grad(m->bf, m->Pc, sQ, T - 1, 1, D, gr + L.at(P_WQ, top), w);
   } else {
     // the top layer's input: the layer below's output, rounded (bf16 storage point)
-    ok = launch_gemm(gemm(D, D, N * T, Xtop, 1, D, rb, m->dK, D, 1, 0, gr + L.at(P_WK, top), D, 0.f), ws2,
-                     m->gws_cap, w) && ok;
-    ok = launch_gemm(gemm(D, D, N * T, Xtop, 1, D, rb, m->dV, D, 1, 0, gr + L.at(P_WV, top), D, 0.f), ws2,
-                     m->gws_cap, w) && ok;
+    ok = kv_grad(Xtop, 1, D, false, false, gr + L.at(P_WK, top)) && ok;
+    ok = kv_grad(Xtop, 1, D, false, true, gr + L.at(P_WV, top)) && ok;
     ok = launch_gemm(gemm(D, D, N, Xtop + (int64_t)(T - 1) * D, 1, (int64_t)T * D, rb, m->dQ, D, 1, 0,
                           gr + L.at(P_WQ, top), D, 0.f),
                      ws2, m->gws_cap, w) && ok;
@@ -900,8 +924,7 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // form the key and value part from the rank-one rows of dK and dV
   // (launch_dx_rank1, which adds dY_0); otherwise two products over every token
   // row, then dY_0
-  const bool rank1 = m->bf && m->WkT &&
-                     launch_dx_rank1(m->kq, m->dO, m->dSc, m->kA, m->WkT, m->WvT, dYr(0), N, T, D, H, ascale, m->dX, s);
+  if (rank1) ok = launch_dx_rank1(m->kq, m->dO, m->dSc, m->kA, m->WkT, m->WvT, dYr(0), N, T, D, H, ascale, m->dX, s) && ok;
   if (!rank1)
     launch_gemm2(gemm(N * T, D, D, m->dK, D, 1, 0, th + L.at(P_WK, top), 1, D, rb, m->dX, D, 0.f),
                  gemm(N * T, D, D, m->dV, D, 1, 0, th + L.at(P_WV, top), 1, D, rb, m->dX, D, 0.f), ws, m->gws_cap, s);

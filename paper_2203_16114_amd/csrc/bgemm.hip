@@ -53,7 +53,32 @@ struct Src {
   int kext0, kext1;
   int k1p;
   int rows;
+  // rank-one rows (GemmArgs::r1c; one segment, rows contiguous, fp32):
+  // element (k, n) = (r1c[(w H + n >> dsh) << tsh | t] . V(w, n)) . r1scale, k = w << tsh | t
+  const float* r1c;
+  int r1tsh, r1dsh, r1H, r1round;
+  float r1scale;
 };
+
+// Element of a rank-one source at k (absolute within the segment) and
+// column n (its head n >> dsh): (c . V(w, n)) r1scale, V(w, n) = x.
+__device__ __forceinline__ float r1v(const Src& s, int k, int n, float x) {
+  const int w = k >> s.r1tsh, t = k & ((1 << s.r1tsh) - 1);
+  const float c = s.r1c[(((int64_t)w * s.r1H + (n >> s.r1dsh)) << s.r1tsh) + t];
+  if (s.r1round) x = __uint_as_float(pack_bf16x2(x, 0.f) << 16);
+  return (c * x) * s.r1scale;
+}
+// The eight coefficients c of k = k0 .. k0 + 7, k0 a multiple of 8, T = 8:
+// one window w = k0 / 8, t = 0 .. 7, head n >> dsh (two 16-byte loads).
+__device__ __forceinline__ void r1c8(const Src& s, int k0, int n, float (&c)[8]) {
+  const float* p = s.r1c + (((int64_t)(k0 >> 3) * s.r1H + (n >> s.r1dsh)) << 3);
+  const float4 a = *reinterpret_cast<const float4*>(p), b = *reinterpret_cast<const float4*>(p + 4);
+  c[0] = a.x; c[1] = a.y; c[2] = a.z; c[3] = a.w;
+  c[4] = b.x; c[5] = b.y; c[6] = b.z; c[7] = b.w;
+}
+__device__ __forceinline__ float r1round(const Src& s, float x) {
+  return s.r1round ? __uint_as_float(pack_bf16x2(x, 0.f) << 16) : x;
+}
 
 // LDS unit (16 bytes) of (row, k-chunk c) in a swizzled 128 x 64 tile: the
 // chunk XOR-ed with (row ^ row >> 2) & 7, measured free of bank conflicts both
@@ -138,6 +163,31 @@ __device__ __forceinline__ uint32_t load_tile(const Src& s, int row0, int k0, in
     const int rr = 4 * (tid & 31), kc = (tid >> 5) * 8;
     const bool rin = row0 + rr < s.rows;
     const int ro = min(rr, s.rows - 4 - row0);
+    if (s.r1c) {  // rows of V: window k >> tsh
+      const int n = row0 + ro;
+      if (s.r1tsh == 3 && kc + 8 <= kr) {  // the eight k of one window: V(w, n..n+3) once
+        const int k0 = kk0 + kc;
+        float4 x = *reinterpret_cast<const float4*>(p + (int64_t)(k0 >> 3) * ld + n);
+        x = make_float4(r1round(s, x.x), r1round(s, x.y), r1round(s, x.z), r1round(s, x.w));
+        float c[8];
+        r1c8(s, k0, n, c);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          v[j] = make_float4((c[j] * x.x) * s.r1scale, (c[j] * x.y) * s.r1scale, (c[j] * x.z) * s.r1scale,
+                             (c[j] * x.w) * s.r1scale);
+          mask |= (uint32_t)rin << j;
+        }
+        return mask;
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        const int k = kk0 + min(kc + j, kr - 1);
+        const float4 x = *reinterpret_cast<const float4*>(p + (int64_t)(k >> s.r1tsh) * ld + n);
+        v[j] = make_float4(r1v(s, k, n, x.x), r1v(s, k, n, x.y), r1v(s, k, n, x.z), r1v(s, k, n, x.w));
+        mask |= (uint32_t)(rin && kc + j < kr) << j;
+      }
+      return mask;
+    }
 #pragma unroll
     for (int j = 0; j < 8; ++j) {
       v[j] = ld4(base, min(kc + j, kr - 1) * ld + ro);
@@ -457,6 +507,34 @@ __device__ __forceinline__ uint32_t load(const Src& s, int row0, int k0, int tid
     const int rr = 2 * (tid & 127), kc = (tid >> 7) * 8;
     const bool rin = row0 + rr < s.rows;
     const int ro = min(rr, s.rows - 2 - row0);
+    if (s.r1c) {  // rows of V: window k >> tsh
+      const int n = row0 + ro;
+      if (s.r1tsh == 3 && kc + 8 <= kr) {  // the eight k of one window: V(w, n..n+1) once
+        const int k0 = kk0 + kc;
+        float2 x = *reinterpret_cast<const float2*>(p + (int64_t)(k0 >> 3) * ld + n);
+        x = make_float2(r1round(s, x.x), r1round(s, x.y));
+        float c[8];
+        r1c8(s, k0, n, c);
+#pragma unroll
+        for (int j = 0; j < 8; j += 2) {
+          v[j >> 1] = make_float4((c[j] * x.x) * s.r1scale, (c[j] * x.y) * s.r1scale, (c[j + 1] * x.x) * s.r1scale,
+                                  (c[j + 1] * x.y) * s.r1scale);
+          mask |= (uint32_t)rin << j;
+          mask |= (uint32_t)rin << (j + 1);
+        }
+        return mask;
+      }
+#pragma unroll
+      for (int j = 0; j < 8; j += 2) {
+        const int ka = kk0 + min(kc + j, kr - 1), kb = kk0 + min(kc + j + 1, kr - 1);
+        const float2 a = *reinterpret_cast<const float2*>(p + (int64_t)(ka >> s.r1tsh) * ld + n);
+        const float2 b = *reinterpret_cast<const float2*>(p + (int64_t)(kb >> s.r1tsh) * ld + n);
+        v[j >> 1] = make_float4(r1v(s, ka, n, a.x), r1v(s, ka, n, a.y), r1v(s, kb, n, b.x), r1v(s, kb, n, b.y));
+        mask |= (uint32_t)(rin && kc + j < kr) << j;
+        mask |= (uint32_t)(rin && kc + j + 1 < kr) << (j + 1);
+      }
+      return mask;
+    }
 #pragma unroll
     for (int j = 0; j < 8; j += 2) {
       const float2 a = *reinterpret_cast<const float2*>(at(base, min(kc + j, kr - 1) * ld + ro));
@@ -803,6 +881,15 @@ bool launch_bgemm(const GemmArgs& g, const GemmArgs* g2, float* ws, int64_t ws_c
     A.ld1 = A.ld0;
     B.p1 = B.p0;
     B.ld1 = B.ld0;
+  }
+  if (g.r1c) {  // rank-one rows: B fp32 with its rows contiguous, split, one segment
+    if (g2 || bkc || g.halfB || g.roundB || g.sbn != 1 || g.N % 4 != 0 || g.r1dsh < 2 || g.r1H <= 0) return false;
+    B.r1c = g.r1c;
+    B.r1tsh = g.r1tsh;
+    B.r1dsh = g.r1dsh;
+    B.r1H = g.r1H;
+    B.r1round = g.r1round;
+    B.r1scale = g.r1scale;
   }
   const int K0 = g.K, K1 = g2 ? g2->K : 0;
   if (K0 + K1 == 0) return false;

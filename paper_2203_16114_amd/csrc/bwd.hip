@@ -371,7 +371,8 @@ bool launch_gemm(const GemmArgs& g0, float* ws, int64_t ws_cap, hipStream_t s) {
   if (g0.M <= 0 || g0.N <= 0) return true;
   // bf16 storage points on at least one side: register-staged bf16 GEMM
   if (launch_bgemm(g0, nullptr, ws, ws_cap, s)) return true;
-  if (g0.halfA || g0.halfB || g0.halfC) return false;  // the kernels below use fp32 operands and results
+  // the kernels below use fp32 operands and results, and read B as stored
+  if (g0.halfA || g0.halfB || g0.halfC || g0.r1c) return false;
   GemmArgs g = g0;
   if (g.Cin && g.Cin != g.C && g.beta != 0.f) {  // the kernels below add C itself: the addend goes there first
     (void)hipMemcpy2DAsync(g.C, (size_t)g.ldc * 4, g.Cin, (size_t)g.ldc * 4, (size_t)g.N * 4, (size_t)g.M,
@@ -646,7 +647,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd2(const float* __restrict__ dO,
       if (dS && live && c == 0) dS[(nn * H + h) * T + u] = ds;
       dq = fmaf(ds, K[(nn * T + u) * D + col], dq);
       const float dk = (ds * qv) * scale, dv = a[u] * o;
-      if (live) {
+      if (live && dK) {
         dK[(nn * T + u) * D + col] = dk;
         dV[(nn * T + u) * D + col] = dv;
       }
@@ -822,6 +823,11 @@ static void launch_dx_rank1_t(const float* q, const float* dO, const float* dS, 
                               const uint4* WvT, const float* dY0, int64_t N, float scale, float* dX, hipStream_t s) {
   hipLaunchKernelGGL((k_dx_rank1<D, DH, T>), dim3((unsigned)((N + 15) / 16)), dim3(512), 0, s, q, dO, dS, A, WkT, WvT,
                      dY0, N, scale, dX);
+}
+
+bool dx_rank1_built(int T, int D, int H) {
+  const int DH = D / H;
+  return (D == 128 || D == 256 || (D == 512 && DH == 64)) && (DH == 32 || DH == 64) && (T == 4 || T == 8);
 }
 
 bool launch_dx_rank1(const float* q, const float* dO, const float* dS, const float* A, const uint4* WkT,

@@ -94,6 +94,13 @@ struct GemmArgs {
   float beta;          // C = beta*Cin + A.B  (beta 0 or 1)
   // nullable: the addend of beta (laid out as C, ldc apart); NULL: C itself
   const float* Cin;
+  // nullable: B formed from rank-one rows, B(k, n) = (r1c[(w H + n / dh) T + t] . V(w, n)) . r1scale
+  // for k = w T + t, with V(w, n) = B[w*sbk + n] (sbn = 1; rounded to bf16 first if r1round) and
+  // T = 2^r1tsh, dh = 2^r1dsh, H = r1H (the key and value gradients of the last query row);
+  // fp32 B split into hi and lo, bf16 kernels only
+  const float* r1c;
+  int r1tsh, r1dsh, r1H, r1round;
+  float r1scale;
   // nullable: C = (A.B) * GELU'(gelu_u) elementwise, gelu_u laid out as C
   // (the backward of the FFN activation fused into its product); needs beta 0
   const float* gelu_u;
@@ -128,12 +135,14 @@ void launch_ce_grad(const float* z, const int32_t* tgt, int64_t N, float* dz, hi
 void launch_gelu_fwd_round(const float* U, float* G, int64_t n, int round, hipStream_t s);
 void launch_gelu_bwd(const float* dG, const float* U, float* dU, int64_t n, hipStream_t s);
 // dS (nullable): [N][H][T] gradients of the attention scores of the last row
+// dK, dV may be NULL (not written; their sums over windows still are)
 void launch_attn_bwd(const float* dO, const float* q, const float* K, const float* V, const float* A, int64_t N, int T,
                      int D, int H, float scale, int round_dO, float* dQ, float* dK, float* dV, float* part,
                      float* colsums, float* cws, hipStream_t s, float* dS = nullptr);
 // bf16 models: dX[n][t] (all T tokens) from the rank-one key and value
 // gradients plus dY0 on the last token; false when no kernel is built for the shape
 // WkT, WvT: fragment-packed bf16 copies of Wk^T and Wv^T (RJ_PACKT of the [D][D] masters)
+bool dx_rank1_built(int T, int D, int H);
 bool launch_dx_rank1(const float* q, const float* dO, const float* dS, const float* A, const uint4* WkT,
                      const uint4* WvT, const float* dY0, int64_t N, int T, int D, int H, float scale, float* dX,
                      hipStream_t s);
