@@ -624,28 +624,35 @@ __global__ __launch_bounds__(256) void k_attn_bwd2(const float* __restrict__ dO,
   const bool live = n < N;
   const int64_t nn = live ? n : ch * CH;  // dead slots redo the chunk's first window and store nothing
   float o = dO[nn * D + col];
-  if (round_dO) o = round_bf(o);
-  float a[8], dA[8];
+  // (bf16 rounding by the hardware conversion: round to nearest even, no branch)
+  if (round_dO) o = __uint_as_float(pack_bf16x2(o, 0.f) << 16);
+  // every row of V and K first (all loads in flight together)
+  float vr[8], kr[8], a[8], dA[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) {
+    vr[u] = u < T ? V[(nn * T + u) * D + col] : 0.f;
+    kr[u] = u < T ? K[(nn * T + u) * D + col] : 0.f;
+    a[u] = u < T ? A[(nn * H + h) * T + u] : 0.f;
+  }
+  const float qv = q[nn * D + col];
   float tot = 0.f;
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
     if (u < T) {
-      float x = o * V[(nn * T + u) * D + col];
+      float x = o * vr[u];
 #pragma unroll
       for (int off = 1; off < DH; off <<= 1) x += __shfl_xor(x, off, 64);
       dA[u] = x;
-      a[u] = A[(nn * H + h) * T + u];
       tot = fmaf(a[u], x, tot);
     }
   }
-  const float qv = q[nn * D + col];
   float dq = 0.f;
 #pragma unroll
   for (int u = 0; u < 8; ++u) {
     if (u < T) {
       const float ds = a[u] * (dA[u] - tot);
       if (dS && live && c == 0) dS[(nn * H + h) * T + u] = ds;
-      dq = fmaf(ds, K[(nn * T + u) * D + col], dq);
+      dq = fmaf(ds, kr[u], dq);
       const float dk = (ds * qv) * scale, dv = a[u] * o;
       if (live && dK) {
         dK[(nn * T + u) * D + col] = dk;
@@ -1186,7 +1193,9 @@ __global__ __launch_bounds__(256) void k_gather_kept8(const uint8_t* __restrict_
   const int c = (int)(i - row32 * q8) * 8;
   const int j = c / e, cc = c - j * e;
   const int byte = win[row * g + j];
-  *reinterpret_cast<uint4*>(X + row * D + c) = *reinterpret_cast<const uint4*>(E + byte * e + cc);
+  const uint4 v = *reinterpret_cast<const uint4*>(E + byte * e + cc);
+  typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
+  __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, reinterpret_cast<u32x4*>(X + row * D + c));
 }
 void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, int T, int D, int e, int g, void* X,
                         hipStream_t s) {
