@@ -871,8 +871,13 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // and the input gradient of the tokens by k_dx_rank1): dK, dV are not stored
   const bool pow2 = (T & (T - 1)) == 0 && (L.DH & (L.DH - 1)) == 0;
   const bool rank1 = m->bf && m->WkT && pow2 && dx_rank1_built(T, D, H);
+  // rank1: the sums over windows of dK and dV (sK, sV; read by the positional
+  // gradients of a single layer only) from the rank-one rows
   launch_attn_bwd(m->dO, m->kq, m->kK, m->kV, m->kA, N, T, D, H, ascale, rb, m->dQ, rank1 ? nullptr : m->dK,
-                  rank1 ? nullptr : m->dV, m->apart, sK, m->cws, s, m->bf ? m->dSc : nullptr);
+                  rank1 ? nullptr : m->dV, rank1 ? nullptr : m->apart, sK, m->cws, s, m->bf ? m->dSc : nullptr);
+  if (rank1 && NL == 1 && m->cfg.use_pos &&
+      !launch_rank1_sums(m->dSc, m->kq, m->kA, m->dO, N, T, D, H, ascale, rb, m->apart, sK, m->cws, s))
+    ok = false;
   auto log2i = [](int x) {
     int r = 0;
     while ((1 << r) < x) ++r;
@@ -941,9 +946,6 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
       launch_colsum(m->dX, N, (int64_t)T * D, (int64_t)T * D, gr + L.off[P_P], 0.f, m->cws, s);
     else
       launch_zero(gr + L.off[P_P], L.size[P_P], s);
-  } else if (m->cfg.use_pos && rank1) {
-    // positional table: dP[t] = sum_n dX[n][t]
-    launch_colsum(m->dX, N, (int64_t)T * D, (int64_t)T * D, gr + L.off[P_P], 0.f, m->cws, s);
   } else if (m->cfg.use_pos) {
     // positional table: dP[t] = sum_n dX[n][t], from the sums over windows of
     // dK, dV, dQ and dY_0 times the weights; then the byte embedding

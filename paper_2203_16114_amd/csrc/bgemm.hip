@@ -17,6 +17,8 @@
 // Split-K partial sums go to a workspace and are added in a fixed order, so
 // results do not depend on scheduling.  Blocks are ordered so that the tiles
 // that share operand rows run on one XCD (one L2).
+#include <type_traits>
+
 #include "kcommon.h"
 #include "kernels.h"
 
@@ -610,11 +612,17 @@ __device__ __forceinline__ void store(const float4 (&v)[4], uint32_t mask, uint4
   }
 }
 
-template <bool AKC, bool BKC, bool SA, bool SB, bool HA, bool HB>
+// PD: stages whose loads are in flight while a stage is multiplied (1 or 2).
+// With 2, the loads of stage s + 2 are issued before the multiply of stage s,
+// and stage s + 1 (loaded during stage s - 1) goes to LDS after it: two stages
+// of matrix work cover each load's latency (two register sets: operands read
+// as bf16, or fp32 on one side only).
+template <bool AKC, bool BKC, bool SA, bool SB, bool HA, bool HB, int PD>
 __global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, int N, float* C, int64_t ldc,
                                                    float beta, float* __restrict__ part, int kchunk, int tn, int tm,
                                                    const float* __restrict__ gu, int hc, const float* cin) {
   static_assert(!(SA && SB), "at most one operand is split");
+  static_assert(PD == 1 || PD == 2, "prefetch depth");
   constexpr int NT = 2 + (SA ? 1 : 0) + (SB ? 1 : 0);
   constexpr int FM = SA ? 4 : 8, FN = SA ? 8 : 4;  // 16 x 16 fragments per wave along m, n
   constexpr int WN = TN / (16 * FN);                // waves along n
@@ -631,26 +639,17 @@ __global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, 
   for (int i = 0; i < FM; ++i)
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float4 va[4], vb[4];
-  uint32_t ma = 0, mbk = 0;
-  auto put = [&](int buf) {
-    store<AKC, SA, HA>(va, ma, lds[buf][0], lds[buf][SA ? 2 : 0], tid);
-    store<BKC, SB, HB>(vb, mbk, lds[buf][1], lds[buf][NT - 1], tid);
+  float4 va[PD][4], vb[PD][4];
+  uint32_t ma[PD] = {}, mbk[PD] = {};
+  auto ld = [&](int set, int k0) {
+    ma[set] = load<AKC, HA>(A, m0, k0, tid, va[set]);
+    mbk[set] = load<BKC, HB>(B, n0, k0, tid, vb[set]);
   };
-  if (kb < ke) {
-    ma = load<AKC, HA>(A, m0, kb, tid, va);
-    mbk = load<BKC, HB>(B, n0, kb, tid, vb);
-    put(0);
-  }
-  __syncthreads();
-  int buf = 0;
-  for (int k0 = kb; k0 < ke; k0 += TK, buf ^= 1) {
-    const bool more = k0 + TK < ke;
-    if (more) {
-      ma = load<AKC, HA>(A, m0, k0 + TK, tid, va);
-      mbk = load<BKC, HB>(B, n0, k0 + TK, tid, vb);
-    }
-    asm volatile("" ::: "memory");
+  auto put = [&](int set, int buf) {
+    store<AKC, SA, HA>(va[set], ma[set], lds[buf][0], lds[buf][SA ? 2 : 0], tid);
+    store<BKC, SB, HB>(vb[set], mbk[set], lds[buf][1], lds[buf][NT - 1], tid);
+  };
+  auto mult = [&](int buf) {
     uint4 af[FM], bf[FN];
 #pragma unroll
     for (int rf = 0; rf < FM; ++rf) af[rf] = lds[buf][0][unit_of(wm * 16 * FM + rf * 16 + lc, lg)];
@@ -676,9 +675,59 @@ __global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, 
 #pragma unroll
         for (int nf = 0; nf < FN; ++nf) Mma<true>::run(acc[rf][nf], af[rf], bf[nf]);
     }
-    asm volatile("" ::: "memory");
-    if (more) put(buf ^ 1);
+  };
+  if constexpr (PD == 1) {
+    if (kb < ke) {
+      ld(0, kb);
+      put(0, 0);
+    }
     __syncthreads();
+    int buf = 0;
+    for (int k0 = kb; k0 < ke; k0 += TK, buf ^= 1) {
+      const bool more = k0 + TK < ke;
+      if (more) ld(0, k0 + TK);  // next tile into registers while this one is multiplied
+      // keep the order loads / multiply / LDS writes: otherwise the writes to the
+      // other buffer are hoisted above the multiply and wait on the loads at once
+      asm volatile("" ::: "memory");
+      mult(buf);
+      asm volatile("" ::: "memory");
+      if (more) put(0, buf ^ 1);  // the other buffer was last read before the previous barrier
+      __syncthreads();
+    }
+  } else {
+    // stage s (k = kb + s TK) in LDS buffer s & 1 and register set s & 1
+    const int ns = (ke - kb + TK - 1) / TK;
+    if (ns > 0) {
+      ld(0, kb);
+      put(0, 0);
+    }
+    if (ns > 1) ld(1, kb + TK);
+    __syncthreads();
+    // one stage: loads of s + 2 into its set (free: stage s went to LDS), the
+    // multiply of s, and stage s + 1 (loaded a stage ago) from the other set to
+    // the other buffer (last read before the previous barrier), its conversion
+    // interleaved with the MFMAs.  The last stage writes that buffer too (a set
+    // already stored, or never loaded): nothing reads it afterwards.
+    constexpr int NMF = FM * FN * (1 + (SA ? 1 : 0) + (SB ? 1 : 0));
+    auto stage = [&](auto cc, int st) {
+      constexpr int c = decltype(cc)::value;
+      if (st + 2 < ns) ld(c, kb + (st + 2) * TK);
+      asm volatile("" ::: "memory");
+      mult(c);
+      put(c ^ 1, c ^ 1);
+      __builtin_amdgcn_sched_group_barrier(0x100, FM + FN, 0);  // the first fragments
+#pragma unroll
+      for (int i = 0; i < NMF; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+        if (i % 4 == 3) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
+      }
+      __syncthreads();
+    };
+    for (int st = 0; st < ns; st += 2) {
+      stage(std::integral_constant<int, 0>{}, st);
+      if (st + 1 < ns) stage(std::integral_constant<int, 1>{}, st + 1);
+    }
   }
   const int mb = m0 + wm * 16 * FM + 4 * lg, nbase = n0 + wn * 16 * FN + lc;
   if (part) {
@@ -760,30 +809,32 @@ int splits(int M, int N, int Kp) {
   return tiles * s >= 256 ? s : 0;
 }
 
+// PD = 2 where both register sets fit: an operand read as bf16 (its 16 values
+// of a stage in 8 registers) and at most one fp32 operand
 template <bool AKC, bool BKC>
 void launch_orient(bool sa, bool sb, bool ha, bool hb, dim3 grid, const Src& A, const Src& B, int Kp, const GemmArgs& g,
                    float* part, int kchunk, int tn, int tm, hipStream_t s) {
-#define TRACE_BGEMM(SA_, SB_, HA_, HB_)                                                                       \
-  hipLaunchKernelGGL((k_bgemm_big<AKC, BKC, SA_, SB_, HA_, HB_>), grid, dim3(512), 0, s, A, B, Kp, g.M, g.N, g.C, g.ldc, \
-                     g.beta, part, kchunk, tn, tm, g.gelu_u, g.halfC, g.Cin ? g.Cin : g.C)
+#define TRACE_BGEMM(SA_, SB_, HA_, HB_, PD_)                                                                 \
+  hipLaunchKernelGGL((k_bgemm_big<AKC, BKC, SA_, SB_, HA_, HB_, PD_>), grid, dim3(512), 0, s, A, B, Kp, g.M, g.N, g.C, \
+                     g.ldc, g.beta, part, kchunk, tn, tm, g.gelu_u, g.halfC, g.Cin ? g.Cin : g.C)
   if (sa) {
     if (hb)
-      TRACE_BGEMM(true, false, false, true);
+      TRACE_BGEMM(true, false, false, true, 2);
     else
-      TRACE_BGEMM(true, false, false, false);
+      TRACE_BGEMM(true, false, false, false, 1);
   } else if (sb) {
     if (ha)
-      TRACE_BGEMM(false, true, true, false);
+      TRACE_BGEMM(false, true, true, false, 2);
     else
-      TRACE_BGEMM(false, true, false, false);
+      TRACE_BGEMM(false, true, false, false, 1);
   } else if (ha && hb) {
-    TRACE_BGEMM(false, false, true, true);
+    TRACE_BGEMM(false, false, true, true, 2);
   } else if (ha) {
-    TRACE_BGEMM(false, false, true, false);
+    TRACE_BGEMM(false, false, true, false, 2);
   } else if (hb) {
-    TRACE_BGEMM(false, false, false, true);
+    TRACE_BGEMM(false, false, false, true, 2);
   } else {
-    TRACE_BGEMM(false, false, false, false);
+    TRACE_BGEMM(false, false, false, false, 1);
   }
 #undef TRACE_BGEMM
 }

@@ -605,6 +605,7 @@ void launch_add(float* y, const float* x, int64_t rows, int64_t cols, int64_t ld
 // its windows' dK and dV rows in a fixed order into part[chunk][0|1][u][col]:
 // the sums over windows that the positional gradients need come from a column
 // sum over the chunks (launch_colsum) instead of over every window's rows.
+// part NULL: no sums (they come from the rank-one rows, launch_rank1_sums).
 template <int DH>
 __global__ __launch_bounds__(256) void k_attn_bwd2(const float* __restrict__ dO, const float* __restrict__ q,
                                                    const float* __restrict__ K, const float* __restrict__ V,
@@ -658,11 +659,14 @@ __global__ __launch_bounds__(256) void k_attn_bwd2(const float* __restrict__ dO,
         dK[(nn * T + u) * D + col] = dk;
         dV[(nn * T + u) * D + col] = dv;
       }
-      red[0][slot][u][c] = live ? dk : 0.f;
-      red[1][slot][u][c] = live ? dv : 0.f;
+      if (part) {
+        red[0][slot][u][c] = live ? dk : 0.f;
+        red[1][slot][u][c] = live ? dv : 0.f;
+      }
     }
   }
   if (live) dQ[nn * D + col] = dq * scale;
+  if (!part) return;  // (uniform over the grid)
   __syncthreads();
   for (int i = threadIdx.x; i < 2 * T * DH; i += 256) {
     const int which = i / (T * DH), u = (i / DH) % T, cc = i % DH;
@@ -689,7 +693,94 @@ void launch_attn_bwd(const float* dO, const float* q, const float* K, const floa
   else
     hipLaunchKernelGGL(k_attn_bwd2<64>, grid, dim3(256), 0, s, dO, q, K, V, A, N, T, D, H, scale, round_dO, dQ, dK,
                        dV, part, dS);
+  if (part) launch_colsum(part, chunks, (int64_t)2 * T * D, (int64_t)2 * T * D, colsums, 0.f, cws, s);
+}
+
+// Sums over windows of the last query row's key and value gradients from their
+// rank-one rows, for the positional parts of the weight gradients and of the
+// positional table (the same values k_attn_bwd2 sums):
+//   sK[t][j] = sum_n (dS[n][h][t] q[n][j]) scale,  sV[t][j] = sum_n A[n][h][t] bf(dO[n][j]),
+// h = j / DH.  A block takes 64 columns of a chunk of RS_CW windows; its wave s
+// the windows s, s + 4, ... (four at a time, every load first), the four waves'
+// sums are added in wave order into part[chunk][0|1][t][j], and a column sum over
+// the chunks follows (launch_colsum).  36 bytes of dS, q, A, dO per window and
+// column pair instead of the 2 T D floats per window chunk of k_attn_bwd2's sums.
+constexpr int RS_CW = 64;
+template <int T>
+__global__ __launch_bounds__(256) void k_rank1_sums(const float* __restrict__ dS, const float* __restrict__ q,
+                                                    const float* __restrict__ A, const float* __restrict__ dO,
+                                                    int64_t N, int D, int H, int dsh, float scale, int round_dO,
+                                                    float* __restrict__ part) {
+  __shared__ float red[4][2][T][64];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int j = blockIdx.y * 64 + lane, h = j >> dsh;
+  const int64_t c = blockIdx.x, n0 = c * RS_CW;
+  const int nw = (int)min<int64_t>(RS_CW, N - n0);
+  float sk[T], sv[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) sk[t] = sv[t] = 0.f;
+#pragma unroll
+  for (int i0 = 0; i0 < RS_CW; i0 += 16) {
+    float qv[4], ov[4], ds[4][T], aa[4][T];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int64_t n = n0 + min(i0 + 4 * u + wave, nw - 1);  // clamped; the window is not added
+      qv[u] = q[n * D + j];
+      ov[u] = dO[n * D + j];
+#pragma unroll
+      for (int t = 0; t < T; t += 4) {
+        const float4 x = *reinterpret_cast<const float4*>(dS + (n * H + h) * T + t);
+        const float4 y = *reinterpret_cast<const float4*>(A + (n * H + h) * T + t);
+        ds[u][t] = x.x; ds[u][t + 1] = x.y; ds[u][t + 2] = x.z; ds[u][t + 3] = x.w;
+        aa[u][t] = y.x; aa[u][t + 1] = y.y; aa[u][t + 2] = y.z; aa[u][t + 3] = y.w;
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      if (i0 + 4 * u + wave < nw) {
+        float o = ov[u];
+        if (round_dO) o = __uint_as_float(pack_bf16x2(o, 0.f) << 16);
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          sk[t] += (ds[u][t] * qv[u]) * scale;
+          sv[t] += aa[u][t] * o;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+    red[wave][0][t][lane] = sk[t];
+    red[wave][1][t][lane] = sv[t];
+  }
+  __syncthreads();
+  for (int i = threadIdx.x; i < 2 * T * 64; i += 256) {
+    const int which = i / (T * 64), t = (i / 64) % T, jj = i % 64;
+    const float v = ((red[0][which][t][jj] + red[1][which][t][jj]) + red[2][which][t][jj]) + red[3][which][t][jj];
+    part[((c * 2 + which) * T + t) * D + blockIdx.y * 64 + jj] = v;
+  }
+}
+
+int64_t rank1_sums_part_floats(int64_t N, int T, int D) { return (N + RS_CW - 1) / RS_CW * 2 * T * D; }
+
+bool launch_rank1_sums(const float* dS, const float* q, const float* A, const float* dO, int64_t N, int T, int D,
+                       int H, float scale, int round_dO, float* part, float* colsums, float* cws, hipStream_t s) {
+  const int DH = D / H;
+  if (D % 64 != 0 || (DH & (DH - 1)) != 0 || (T != 4 && T != 8)) return false;
+  if (N <= 0) {
+    launch_zero(reinterpret_cast<uint32_t*>(colsums), (int64_t)2 * T * D, s);
+    return true;
+  }
+  int dsh = 0;
+  while ((1 << dsh) < DH) ++dsh;
+  const int64_t chunks = (N + RS_CW - 1) / RS_CW;
+  const dim3 grid((unsigned)chunks, (unsigned)(D / 64));
+  if (T == 8)
+    hipLaunchKernelGGL(k_rank1_sums<8>, grid, dim3(256), 0, s, dS, q, A, dO, N, D, H, dsh, scale, round_dO, part);
+  else
+    hipLaunchKernelGGL(k_rank1_sums<4>, grid, dim3(256), 0, s, dS, q, A, dO, N, D, H, dsh, scale, round_dO, part);
   launch_colsum(part, chunks, (int64_t)2 * T * D, (int64_t)2 * T * D, colsums, 0.f, cws, s);
+  return true;
 }
 
 // Input gradient of the tokens through the keys and values, bf16 models:
@@ -1180,28 +1271,47 @@ __global__ __launch_bounds__(256) void k_gather_kept(const uint8_t* __restrict__
     *reinterpret_cast<float4*>((float*)X + row * D + c) =
         make_float4(M::val(src[0]), M::val(src[1]), M::val(src[2]), M::val(src[3]));
 }
-// bf16 with e a multiple of 8: eight consecutive columns per thread, one
-// 16-byte load of the embedding row and one 16-byte store
+// bf16 with e a multiple of 8: units of eight consecutive columns, one 16-byte
+// load of the embedding row and one 16-byte store each.  A block takes
+// GK_U * 256 consecutive units, a thread GK_U of them 256 apart, all byte loads
+// first, then all row loads, then the stores.
+constexpr int GK_U = 8;
 __global__ __launch_bounds__(256) void k_gather_kept8(const uint8_t* __restrict__ win, int64_t rows,
                                                       const uint16_t* __restrict__ E, int T, int D, int e, int g,
                                                       uint16_t* __restrict__ X) {
   const uint32_t q8 = (uint32_t)D / 8;
-  const uint32_t i = blockIdx.x * 256u + threadIdx.x;  // the grid has fewer than 2^32 threads
-  if ((int64_t)i >= rows * q8) return;
-  const uint32_t row32 = i / q8;
-  const int64_t row = row32;
-  const int c = (int)(i - row32 * q8) * 8;
-  const int j = c / e, cc = c - j * e;
-  const int byte = win[row * g + j];
-  const uint4 v = *reinterpret_cast<const uint4*>(E + byte * e + cc);
+  const uint32_t nu = (uint32_t)rows * q8;  // the grid has fewer than 2^32 units
+  const uint32_t i0 = blockIdx.x * (256u * GK_U) + threadIdx.x;
+  int byte[GK_U], cc[GK_U];
+#pragma unroll
+  for (int u = 0; u < GK_U; ++u) {
+    const uint32_t i = min(i0 + 256u * u, nu - 1);  // clamped; stored only inside
+    const uint32_t row = i / q8;
+    const int c = (int)(i - row * q8) * 8;
+    const int j = c / e;
+    cc[u] = c - j * e;
+    byte[u] = win[(int64_t)row * g + j];
+  }
   typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
-  __builtin_nontemporal_store(u32x4{v.x, v.y, v.z, v.w}, reinterpret_cast<u32x4*>(X + row * D + c));
+  u32x4 v[GK_U];
+#pragma unroll
+  for (int u = 0; u < GK_U; ++u) {
+    const uint4 x = *reinterpret_cast<const uint4*>(E + byte[u] * e + cc[u]);
+    v[u] = u32x4{x.x, x.y, x.z, x.w};
+  }
+#pragma unroll
+  for (int u = 0; u < GK_U; ++u) {
+    const uint32_t i = i0 + 256u * u;
+    if (i < nu) __builtin_nontemporal_store(v[u], reinterpret_cast<u32x4*>(X + (int64_t)i * 8));
+  }
 }
 void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, int T, int D, int e, int g, void* X,
                         hipStream_t s) {
   const int64_t rows = N * T;
-  if (bf && e % 8 == 0 && ((uintptr_t)E & 15) == 0 && ((uintptr_t)X & 15) == 0) {
-    const dim3 grid8((unsigned)((rows * (D / 8) + 255) / 256));
+  if (rows <= 0) return;
+  if (bf && e % 8 == 0 && ((uintptr_t)E & 15) == 0 && ((uintptr_t)X & 15) == 0 &&
+      rows * (D / 8) < ((int64_t)1 << 31)) {
+    const dim3 grid8((unsigned)((rows * (D / 8) + 256 * GK_U - 1) / (256 * GK_U)));
     hipLaunchKernelGGL(k_gather_kept8, grid8, dim3(256), 0, s, win, rows, (const uint16_t*)E, T, D, e, g,
                        (uint16_t*)X);
     return;

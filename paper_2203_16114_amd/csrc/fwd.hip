@@ -45,8 +45,15 @@ __device__ __forceinline__ void refresh_pack(const RefreshJob& jb, int64_t i) {
   const int kb = ks * M::KS + (lane >> 4) * M::EPF;
   float v[8];
   if (jb.kind == RJ_PACKT) {  // src is [N][K]: element (k, n) of its transpose at src[n * K + k]
+    // (16-byte aligned: launch_refresh checks src and K)
 #pragma unroll
-    for (int j = 0; j < M::EPF; ++j) v[j] = jb.src[(int64_t)n * jb.K + kb + j] * jb.scale;
+    for (int j = 0; j < M::EPF; j += 4) {
+      const float4 x = *reinterpret_cast<const float4*>(jb.src + (int64_t)n * jb.K + kb + j);
+      v[j] = x.x * jb.scale;
+      v[j + 1] = x.y * jb.scale;
+      v[j + 2] = x.z * jb.scale;
+      v[j + 3] = x.w * jb.scale;
+    }
   } else {
 #pragma unroll
     for (int j = 0; j < M::EPF; ++j) v[j] = jb.src[(int64_t)(kb + j) * jb.N + n] * jb.scale;
@@ -62,34 +69,40 @@ __device__ __forceinline__ void refresh_pack(const RefreshJob& jb, int64_t i) {
 // a token's projection is an MFMA on the rounded byte embeddings plus PW[w][t]:
 // X.W = E.W + P.W.  A block takes 16 columns j of one W_w for every token t; its
 // 16 thread groups of 16 take consecutive sixteenths of i, read each weight value
-// once for all tokens, and their 16 partial sums are added in i order.
+// once for all tokens, and their 16 partial sums are added in i order.  A thread
+// issues all of its weight loads (at most 32) before it stages P, so that one
+// memory latency covers them.
 constexpr int PTAB_TMAX = 8, PTAB_DMAX = 512;
 template <bool BF, int T>
 __device__ __forceinline__ void refresh_ptab(const RefreshJob& jb, int lb, float* Pv, float* part) {
   typedef Mma<BF> M;
+  constexpr int KLMAX = PTAB_DMAX / 16;
   const int D = jb.N, nbw = D / 16;
   const int w = lb / nbw, j = (lb - w * nbw) * 16 + (threadIdx.x & 15), kg = threadIdx.x >> 4;
-  for (int i = threadIdx.x; i < T * D; i += 256) Pv[i] = jb.use_pos ? M::val(M::cvt(jb.src[i])) : 0.f;
-  __syncthreads();
   const float* Wm = jb.src2 + (int64_t)w * D * D + j;
   const int kl = D / 16, k0 = kg * kl;  // kl is a multiple of 4 (D a multiple of 64)
+  float wv[KLMAX];
+#pragma unroll
+  for (int u = 0; u < KLMAX; ++u) wv[u] = Wm[(int64_t)(k0 + min(u, kl - 1)) * D];  // (clamped: u < kl used)
+  for (int i = threadIdx.x; i < T * D; i += 256) Pv[i] = jb.use_pos ? M::val(M::cvt(jb.src[i])) : 0.f;
+  __syncthreads();
   float acc[T];
 #pragma unroll
   for (int t = 0; t < T; ++t) acc[t] = 0.f;
-#pragma unroll 4
-  for (int k = k0; k < k0 + kl; k += 4) {
-    float wv[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) wv[u] = Wm[(int64_t)(k + u) * D];
+  for (int u = 0; u < KLMAX; u += 4) {
+    if (u < kl) {
+      float x[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) wv[u] = M::val(M::cvt(wv[u]));
+      for (int e = 0; e < 4; ++e) x[e] = M::val(M::cvt(wv[u + e]));
 #pragma unroll
-    for (int t = 0; t < T; ++t) {
-      const float4 p = *reinterpret_cast<const float4*>(Pv + t * D + k);
-      acc[t] = fmaf(p.x, wv[0], acc[t]);
-      acc[t] = fmaf(p.y, wv[1], acc[t]);
-      acc[t] = fmaf(p.z, wv[2], acc[t]);
-      acc[t] = fmaf(p.w, wv[3], acc[t]);
+      for (int t = 0; t < T; ++t) {
+        const float4 p = *reinterpret_cast<const float4*>(Pv + t * D + k0 + u);
+        acc[t] = fmaf(p.x, x[0], acc[t]);
+        acc[t] = fmaf(p.y, x[1], acc[t]);
+        acc[t] = fmaf(p.z, x[2], acc[t]);
+        acc[t] = fmaf(p.w, x[3], acc[t]);
+      }
     }
   }
 #pragma unroll
@@ -150,6 +163,7 @@ bool launch_refresh(bool bf, const RefreshJob* jobs, int n, hipStream_t s) {
     } else if (jb.kind == RJ_PACK || jb.kind == RJ_PACKT) {
       const int KS = bf ? 32 : 16;
       if (jb.K % KS != 0 || jb.N % 16 != 0) return false;
+      if (jb.kind == RJ_PACKT && ((uintptr_t)jb.src & 15) != 0) return false;
       nb = ((int64_t)(jb.K / KS) * (jb.N / 16) * 64 + 255) / 256;
     } else if (jb.kind == RJ_PTAB) {
       if ((jb.K != 4 && jb.K != 8) || jb.N > PTAB_DMAX || jb.N % 64 != 0) return false;

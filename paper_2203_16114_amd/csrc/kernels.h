@@ -147,6 +147,12 @@ bool launch_dx_rank1(const float* q, const float* dO, const float* dS, const flo
                      const uint4* WvT, const float* dY0, int64_t N, int T, int D, int H, float scale, float* dX,
                      hipStream_t s);
 int64_t attn_bwd_part_floats(int64_t N, int T, int D, int H);
+// sums over windows of the rank-one key and value gradients of the last query
+// row into colsums [2][T][D] (sK, then sV); part: rank1_sums_part_floats floats
+// (at most attn_bwd_part_floats); false when the shape is not taken
+int64_t rank1_sums_part_floats(int64_t N, int T, int D);
+bool launch_rank1_sums(const float* dS, const float* q, const float* A, const float* dO, int64_t N, int T, int D,
+                       int H, float scale, int round_dO, float* part, float* colsums, float* cws, hipStream_t s);
 void launch_pos_table_grad(const float* sKV, const float* sQ, const float* sY, const float* Wq, const float* Wk,
                            const float* Wv, int T, int D, int rb, float* dP, hipStream_t s);
 void launch_add(float* y, const float* x, int64_t rows, int64_t cols, int64_t ldy, int64_t ldx, hipStream_t s);
