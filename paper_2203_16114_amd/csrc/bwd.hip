@@ -677,6 +677,90 @@ __global__ __launch_bounds__(256) void k_attn_bwd2(const float* __restrict__ dO,
   }
 }
 
+// The same backward for the rank-one path (no dK, dV rows, no window sums, so
+// no q): one wave per window, lane l holding columns CPL l .. CPL l + CPL - 1 (CPL = D / 64,
+// one head's DH / CPL lanes consecutive), so that every row of K and V comes in
+// CPL-float vector loads, all T rows of both first.  dA_u by a lane sum and a
+// shuffle tree over the head's lanes; dS and dQ as in k_attn_bwd2.
+template <int D, int DH, int T>
+__global__ __launch_bounds__(256) void k_attn_bwd_r1(const float* __restrict__ dO, const float* __restrict__ K,
+                                                     const float* __restrict__ V,
+                                                     const float* __restrict__ A, int64_t N, float scale,
+                                                     int round_dO, float* __restrict__ dQ, float* __restrict__ dS) {
+  constexpr int CPL = D / 64, LPH = DH / CPL, H = D / DH;
+  static_assert(CPL == 2 || CPL == 4 || CPL == 8, "columns per lane");
+  static_assert(LPH >= 1 && (LPH & (LPH - 1)) == 0 && LPH <= 64, "lanes per head");
+  typedef float __attribute__((ext_vector_type(CPL == 2 ? 2 : 4))) vec;
+  constexpr int NV = CPL == 8 ? 2 : 1;  // vector loads per row
+  constexpr int VW = CPL / NV;          // floats per vector load
+  const int lane = threadIdx.x & 63;
+  const int64_t n = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (n >= N) return;  // (whole waves)
+  const int c0 = lane * CPL, h = c0 / DH;
+  float kr[T][CPL], vr[T][CPL], o[CPL], a[T];
+#pragma unroll
+  for (int u = 0; u < T; ++u)
+#pragma unroll
+    for (int e = 0; e < NV; ++e) {
+      const vec x = *reinterpret_cast<const vec*>(V + (n * T + u) * D + c0 + e * VW);
+      const vec y = *reinterpret_cast<const vec*>(K + (n * T + u) * D + c0 + e * VW);
+#pragma unroll
+      for (int i = 0; i < VW; ++i) {
+        vr[u][e * VW + i] = x[i];
+        kr[u][e * VW + i] = y[i];
+      }
+    }
+#pragma unroll
+  for (int e = 0; e < NV; ++e) {
+    const vec x = *reinterpret_cast<const vec*>(dO + n * D + c0 + e * VW);
+#pragma unroll
+    for (int i = 0; i < VW; ++i) o[e * VW + i] = x[i];
+  }
+#pragma unroll
+  for (int u = 0; u < T; u += 4) {
+    const float4 x = *reinterpret_cast<const float4*>(A + (n * H + h) * T + u);
+    a[u] = x.x; a[u + 1] = x.y; a[u + 2] = x.z; a[u + 3] = x.w;
+  }
+  // (bf16 rounding by the hardware conversion: round to nearest even, no branch)
+  if (round_dO) {
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) o[i] = __uint_as_float(pack_bf16x2(o[i], 0.f) << 16);
+  }
+  float dA[T], tot = 0.f;
+#pragma unroll
+  for (int u = 0; u < T; ++u) {
+    float x = 0.f;
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) x = fmaf(o[i], vr[u][i], x);
+#pragma unroll
+    for (int off = 1; off < LPH; off <<= 1) x += __shfl_xor(x, off, 64);
+    dA[u] = x;
+    tot = fmaf(a[u], x, tot);
+  }
+  float dq[CPL];
+#pragma unroll
+  for (int i = 0; i < CPL; ++i) dq[i] = 0.f;
+  float ds[T];
+#pragma unroll
+  for (int u = 0; u < T; ++u) {
+    ds[u] = a[u] * (dA[u] - tot);
+#pragma unroll
+    for (int i = 0; i < CPL; ++i) dq[i] = fmaf(ds[u], kr[u][i], dq[i]);
+  }
+#pragma unroll
+  for (int e = 0; e < NV; ++e) {
+    vec x;
+#pragma unroll
+    for (int i = 0; i < VW; ++i) x[i] = dq[e * VW + i] * scale;
+    *reinterpret_cast<vec*>(dQ + n * D + c0 + e * VW) = x;
+  }
+  if ((lane & (LPH - 1)) == 0) {
+#pragma unroll
+    for (int u = 0; u < T; u += 4)
+      *reinterpret_cast<float4*>(dS + (n * H + h) * T + u) = make_float4(ds[u], ds[u + 1], ds[u + 2], ds[u + 3]);
+  }
+}
+
 int64_t attn_bwd_chunks(int64_t N, int D, int H) { return (N + 4 * (64 / (D / H)) - 1) / (4 * (64 / (D / H))); }
 
 int64_t attn_bwd_part_floats(int64_t N, int T, int D, int H) { return attn_bwd_chunks(N, D, H) * 2 * T * D; }
@@ -685,6 +769,19 @@ void launch_attn_bwd(const float* dO, const float* q, const float* K, const floa
                      int D, int H, float scale, int round_dO, float* dQ, float* dK, float* dV, float* part,
                      float* colsums, float* cws, hipStream_t s, float* dS) {
   const int DH = D / H;
+  if (!dK && !dV && !part && dS && N > 0 && (T == 4 || T == 8)) {
+    // the rank-one path: one wave per window
+    const dim3 g4((unsigned)((N + 3) / 4));
+#define TRACE_ABR1(D_, DH_, T_)                                                                                    \
+  if (D == D_ && DH == DH_ && T == T_) {                                                                           \
+    hipLaunchKernelGGL((k_attn_bwd_r1<D_, DH_, T_>), g4, dim3(256), 0, s, dO, K, V, A, N, scale, round_dO, dQ, dS);    \
+    return;                                                                                                        \
+  }
+    TRACE_ABR1(128, 32, 4) TRACE_ABR1(128, 32, 8) TRACE_ABR1(128, 64, 4) TRACE_ABR1(128, 64, 8)
+    TRACE_ABR1(256, 32, 4) TRACE_ABR1(256, 32, 8) TRACE_ABR1(256, 64, 4) TRACE_ABR1(256, 64, 8)
+    TRACE_ABR1(512, 64, 4) TRACE_ABR1(512, 64, 8)
+#undef TRACE_ABR1
+  }
   const int64_t chunks = attn_bwd_chunks(N, D, H);
   const dim3 grid((unsigned)(chunks * H));
   if (DH == 32)
@@ -701,17 +798,18 @@ void launch_attn_bwd(const float* dO, const float* q, const float* K, const floa
 // positional table (the same values k_attn_bwd2 sums):
 //   sK[t][j] = sum_n (dS[n][h][t] q[n][j]) scale,  sV[t][j] = sum_n A[n][h][t] bf(dO[n][j]),
 // h = j / DH.  A block takes 64 columns of a chunk of RS_CW windows; its wave s
-// the windows s, s + 4, ... (four at a time, every load first), the four waves'
+// the windows s, s + 8, ... (four at a time, every load first), the eight waves'
 // sums are added in wave order into part[chunk][0|1][t][j], and a column sum over
 // the chunks follows (launch_colsum).  36 bytes of dS, q, A, dO per window and
 // column pair instead of the 2 T D floats per window chunk of k_attn_bwd2's sums.
 constexpr int RS_CW = 64;
+constexpr int RS_W = 8;  // waves per block
 template <int T>
-__global__ __launch_bounds__(256) void k_rank1_sums(const float* __restrict__ dS, const float* __restrict__ q,
-                                                    const float* __restrict__ A, const float* __restrict__ dO,
-                                                    int64_t N, int D, int H, int dsh, float scale, int round_dO,
-                                                    float* __restrict__ part) {
-  __shared__ float red[4][2][T][64];
+__global__ __launch_bounds__(64 * RS_W) void k_rank1_sums(const float* __restrict__ dS, const float* __restrict__ q,
+                                                          const float* __restrict__ A, const float* __restrict__ dO,
+                                                          int64_t N, int D, int H, int dsh, float scale,
+                                                          int round_dO, float* __restrict__ part) {
+  __shared__ float red[RS_W][2][T][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int j = blockIdx.y * 64 + lane, h = j >> dsh;
   const int64_t c = blockIdx.x, n0 = c * RS_CW;
@@ -720,11 +818,11 @@ __global__ __launch_bounds__(256) void k_rank1_sums(const float* __restrict__ dS
 #pragma unroll
   for (int t = 0; t < T; ++t) sk[t] = sv[t] = 0.f;
 #pragma unroll
-  for (int i0 = 0; i0 < RS_CW; i0 += 16) {
+  for (int i0 = 0; i0 < RS_CW; i0 += 4 * RS_W) {
     float qv[4], ov[4], ds[4][T], aa[4][T];
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      const int64_t n = n0 + min(i0 + 4 * u + wave, nw - 1);  // clamped; the window is not added
+      const int64_t n = n0 + min(i0 + RS_W * u + wave, nw - 1);  // clamped; the window is not added
       qv[u] = q[n * D + j];
       ov[u] = dO[n * D + j];
 #pragma unroll
@@ -737,7 +835,7 @@ __global__ __launch_bounds__(256) void k_rank1_sums(const float* __restrict__ dS
     }
 #pragma unroll
     for (int u = 0; u < 4; ++u) {
-      if (i0 + 4 * u + wave < nw) {
+      if (i0 + RS_W * u + wave < nw) {
         float o = ov[u];
         if (round_dO) o = __uint_as_float(pack_bf16x2(o, 0.f) << 16);
 #pragma unroll
@@ -754,9 +852,11 @@ __global__ __launch_bounds__(256) void k_rank1_sums(const float* __restrict__ dS
     red[wave][1][t][lane] = sv[t];
   }
   __syncthreads();
-  for (int i = threadIdx.x; i < 2 * T * 64; i += 256) {
+  for (int i = threadIdx.x; i < 2 * T * 64; i += 64 * RS_W) {
     const int which = i / (T * 64), t = (i / 64) % T, jj = i % 64;
-    const float v = ((red[0][which][t][jj] + red[1][which][t][jj]) + red[2][which][t][jj]) + red[3][which][t][jj];
+    float v = red[0][which][t][jj];
+#pragma unroll
+    for (int w = 1; w < RS_W; ++w) v += red[w][which][t][jj];
     part[((c * 2 + which) * T + t) * D + blockIdx.y * 64 + jj] = v;
   }
 }
@@ -776,9 +876,11 @@ bool launch_rank1_sums(const float* dS, const float* q, const float* A, const fl
   const int64_t chunks = (N + RS_CW - 1) / RS_CW;
   const dim3 grid((unsigned)chunks, (unsigned)(D / 64));
   if (T == 8)
-    hipLaunchKernelGGL(k_rank1_sums<8>, grid, dim3(256), 0, s, dS, q, A, dO, N, D, H, dsh, scale, round_dO, part);
+    hipLaunchKernelGGL(k_rank1_sums<8>, grid, dim3(64 * RS_W), 0, s, dS, q, A, dO, N, D, H, dsh, scale, round_dO,
+                       part);
   else
-    hipLaunchKernelGGL(k_rank1_sums<4>, grid, dim3(256), 0, s, dS, q, A, dO, N, D, H, dsh, scale, round_dO, part);
+    hipLaunchKernelGGL(k_rank1_sums<4>, grid, dim3(64 * RS_W), 0, s, dS, q, A, dO, N, D, H, dsh, scale, round_dO,
+                       part);
   launch_colsum(part, chunks, (int64_t)2 * T * D, (int64_t)2 * T * D, colsums, 0.f, cws, s);
   return true;
 }
@@ -968,8 +1070,82 @@ __global__ __launch_bounds__(256) void k_pos_table_grad(const float* __restrict_
   for (int off = 32; off > 0; off >>= 1) acc += __shfl_xor(acc, off, 64);
   if (lane == 0) dP[i] = t == T - 1 ? acc + sY[c] : acc;
 }
+// The same sums with one wave per weight row c for all T tokens: the block
+// stages the window sums (2 T + 1 rows of D floats) in LDS, each wave reads its
+// row's weights once (all of a lane's loads first), and each output's terms are
+// added in the same order as above (bitwise the same results).
+constexpr int PTG_ROWS = 8;  // weight rows (waves) per block
+template <int T>
+__global__ __launch_bounds__(64 * PTG_ROWS) void k_pos_table_grad_rows(const float* __restrict__ sKV,
+                                                                       const float* __restrict__ sQ,
+                                                                       const float* __restrict__ sY,
+                                                                       const float* __restrict__ Wq,
+                                                                       const float* __restrict__ Wk,
+                                                                       const float* __restrict__ Wv, int D, int rb,
+                                                                       float* __restrict__ dP) {
+  constexpr int JMAX = 8;  // D <= 512
+  __shared__ float S[(2 * T + 1) * 64 * JMAX];
+  const int c = blockIdx.x * PTG_ROWS + (threadIdx.x >> 6), lane = threadIdx.x & 63;
+  const int nj = D / 64;  // D a multiple of 64
+  const int cc = min(c, D - 1);  // (rows past D: loads clamped, nothing stored)
+  float wk[JMAX], wv[JMAX], wq[JMAX];
+#pragma unroll
+  for (int i = 0; i < JMAX; ++i) {
+    const int j = lane + 64 * min(i, nj - 1);  // (clamped; i < nj used)
+    wk[i] = Wk[(int64_t)cc * D + j];
+    wv[i] = Wv[(int64_t)cc * D + j];
+    wq[i] = Wq[(int64_t)cc * D + j];
+  }
+  for (int i = threadIdx.x; i < 2 * T * D; i += 64 * PTG_ROWS) S[i] = sKV[i];
+  for (int i = threadIdx.x; i < D; i += 64 * PTG_ROWS) S[2 * T * D + i] = sQ[i];
+  __syncthreads();
+  if (c >= D) return;
+  if (rb) {
+#pragma unroll
+    for (int i = 0; i < JMAX; ++i) {
+      wk[i] = round_bf(wk[i]);
+      wv[i] = round_bf(wv[i]);
+      wq[i] = round_bf(wq[i]);
+    }
+  }
+  float acc[T];
+#pragma unroll
+  for (int t = 0; t < T; ++t) acc[t] = 0.f;
+#pragma unroll
+  for (int i = 0; i < JMAX; ++i) {
+    if (i < nj) {
+      const int j = lane + 64 * i;
+#pragma unroll
+      for (int t = 0; t < T; ++t) {
+        acc[t] = fmaf(S[t * D + j], wk[i], acc[t]);
+        acc[t] = fmaf(S[(T + t) * D + j], wv[i], acc[t]);
+        if (t == T - 1) acc[t] = fmaf(S[2 * T * D + j], wq[i], acc[t]);
+      }
+    }
+  }
+#pragma unroll
+  for (int t = 0; t < T; ++t) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) acc[t] += __shfl_xor(acc[t], off, 64);
+  }
+  if (lane == 0) {
+#pragma unroll
+    for (int t = 0; t < T; ++t) dP[t * D + c] = t == T - 1 ? acc[t] + sY[c] : acc[t];
+  }
+}
+
 void launch_pos_table_grad(const float* sKV, const float* sQ, const float* sY, const float* Wq, const float* Wk,
                            const float* Wv, int T, int D, int rb, float* dP, hipStream_t s) {
+  if (D % 64 == 0 && D <= 512 && (T == 4 || T == 8)) {
+    const dim3 grid((unsigned)((D + PTG_ROWS - 1) / PTG_ROWS));
+    if (T == 8)
+      hipLaunchKernelGGL(k_pos_table_grad_rows<8>, grid, dim3(64 * PTG_ROWS), 0, s, sKV, sQ, sY, Wq, Wk, Wv, D, rb,
+                         dP);
+    else
+      hipLaunchKernelGGL(k_pos_table_grad_rows<4>, grid, dim3(64 * PTG_ROWS), 0, s, sKV, sQ, sY, Wq, Wk, Wv, D, rb,
+                         dP);
+    return;
+  }
   hipLaunchKernelGGL(k_pos_table_grad, dim3((unsigned)((T * D + 3) / 4)), dim3(256), 0, s, sKV, sQ, sY, Wq, Wk, Wv,
                      T, D, rb, dP);
 }
@@ -1001,13 +1177,14 @@ static EmbWs emb_ws(float* ws, int64_t M, int e) {
   w.pstart = w.base + 256;
   w.piece = w.pstart + 260;
   w.perm = w.piece + 3 * pmax;
-  w.part = (float*)(w.perm + M);
+  // the piece sums start 16-byte aligned (if ws is)
+  w.part = ws + ((w.perm + M - (int*)ws + 3) & ~(int64_t)3);
   (void)e;
   return w;
 }
 int64_t embed_bwd_ws_floats(int64_t M, int e) {
   const int64_t nb = (M + EMB_CS - 1) / EMB_CS, pmax = (M + EMB_PIECE - 1) / EMB_PIECE + 256;
-  return 2 * nb * 256 + 512 + 260 + 3 * pmax + M + pmax * e;
+  return 2 * nb * 256 + 512 + 260 + 3 * pmax + M + 3 + pmax * e;
 }
 
 // cnt[b][v] = number of positions of block b (EMB_CS positions) holding byte v
@@ -1201,6 +1378,51 @@ __global__ __launch_bounds__(64) void k_emb_piece(const float* __restrict__ dX, 
   if (e > 64 && lane + 64 < e) part[(int64_t)p * e + lane + 64] = a1;
 }
 
+// The same piece sums with 16-byte loads, for e a multiple of 4 dividing 256:
+// LP = e / 4 lanes per position (four features each), 64 / LP positions per
+// load instruction, 16 loads in flight per lane; the lanes' position classes
+// are added in a fixed tree at the end.
+__global__ __launch_bounds__(64) void k_emb_piece4(const float* __restrict__ dX, int e, const int* __restrict__ perm,
+                                                   const int* __restrict__ piece, const int* __restrict__ pstart,
+                                                   float* __restrict__ part) {
+  constexpr int B = 16;
+  const int p = blockIdx.x;
+  if (p >= pstart[256]) return;
+  const int st = piece[3 * p + 1], len = piece[3 * p + 2];
+  const int lane = threadIdx.x;
+  const int LP = e >> 2, ipl = 64 / LP, sub = lane / LP, f = (lane - sub * LP) * 4;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int i0 = 0; i0 < len; i0 += 64) {
+    const int n = min(64, len - i0);
+    const int my = perm[st + i0 + min(lane, n - 1)];
+    for (int u0 = 0; u0 < n; u0 += B * ipl) {
+      float4 x[B];
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        const int j = u0 + u * ipl + sub;  // this lane's position (clamped; masked below)
+        const int q = __builtin_amdgcn_ds_bpermute(4 * min(j, n - 1), my);
+        x[u] = *reinterpret_cast<const float4*>(dX + (int64_t)q * e + f);
+      }
+#pragma unroll
+      for (int u = 0; u < B; ++u) {
+        if (u0 + u * ipl + sub < n) {
+          acc.x += x[u].x;
+          acc.y += x[u].y;
+          acc.z += x[u].z;
+          acc.w += x[u].w;
+        }
+      }
+    }
+  }
+  for (int d = 1; d < ipl; d <<= 1) {
+    acc.x += __shfl_down(acc.x, d * LP, 64);
+    acc.y += __shfl_down(acc.y, d * LP, 64);
+    acc.z += __shfl_down(acc.z, d * LP, 64);
+    acc.w += __shfl_down(acc.w, d * LP, 64);
+  }
+  if (lane < LP) *reinterpret_cast<float4*>(part + (int64_t)p * e + f) = acc;
+}
+
 // dE[v][c] = sum of byte v's pieces: row group rg of 256 / e takes every
 // (256 / e)-th piece in order, then the groups are added in order
 __global__ __launch_bounds__(256) void k_emb_sum(const float* __restrict__ part, const int* __restrict__ pstart, int e,
@@ -1238,8 +1460,12 @@ void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int
   hipLaunchKernelGGL(k_emb_pieces, dim3(1), dim3(1024), 0, s, (const int*)w.tot, w.base, w.pstart, w.piece);
   hipLaunchKernelGGL(k_emb_scatter, dim3(nb), dim3(1024), 0, s, win, (int)M, (const int*)w.off,
                      (const int*)w.base, w.perm);
-  hipLaunchKernelGGL(k_emb_piece, dim3(pmax), dim3(64), 0, s, dX, e, (const int*)w.perm, (const int*)w.piece,
-                     (const int*)w.pstart, w.part);
+  if (e % 4 == 0 && 256 % e == 0 && ((uintptr_t)dX & 15) == 0 && ((uintptr_t)w.part & 15) == 0)
+    hipLaunchKernelGGL(k_emb_piece4, dim3(pmax), dim3(64), 0, s, dX, e, (const int*)w.perm, (const int*)w.piece,
+                       (const int*)w.pstart, w.part);
+  else
+    hipLaunchKernelGGL(k_emb_piece, dim3(pmax), dim3(64), 0, s, dX, e, (const int*)w.perm, (const int*)w.piece,
+                       (const int*)w.pstart, w.part);
   hipLaunchKernelGGL(k_emb_sum, dim3(256), dim3(256), 0, s, (const float*)w.part, (const int*)w.pstart, e, dE);
 }
 
@@ -1275,7 +1501,7 @@ __global__ __launch_bounds__(256) void k_gather_kept(const uint8_t* __restrict__
 // load of the embedding row and one 16-byte store each.  A block takes
 // GK_U * 256 consecutive units, a thread GK_U of them 256 apart, all byte loads
 // first, then all row loads, then the stores.
-constexpr int GK_U = 8;
+constexpr int GK_U = 4;
 __global__ __launch_bounds__(256) void k_gather_kept8(const uint8_t* __restrict__ win, int64_t rows,
                                                       const uint16_t* __restrict__ E, int T, int D, int e, int g,
                                                       uint16_t* __restrict__ X) {

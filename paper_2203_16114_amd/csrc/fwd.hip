@@ -105,6 +105,7 @@ __device__ __forceinline__ void refresh_ptab(const RefreshJob& jb, int lb, float
       }
     }
   }
+  __syncthreads();  // (part overlays Pv)
 #pragma unroll
   for (int t = 0; t < T; ++t) part[(kg * T + t) * 16 + (threadIdx.x & 15)] = acc[t];
   __syncthreads();
@@ -117,10 +118,13 @@ __device__ __forceinline__ void refresh_ptab(const RefreshJob& jb, int lb, float
   }
 }
 
+// (16 KB of LDS per block, the partial sums over the staged P: every block of a
+// launch of about 2000 can be resident at once)
 template <bool BF>
 __global__ __launch_bounds__(256) void k_refresh(RefreshArgs a) {
+  static_assert(16 * PTAB_TMAX * 16 <= PTAB_TMAX * PTAB_DMAX, "part fits in Pv");
   __shared__ float Pv[PTAB_TMAX * PTAB_DMAX];
-  __shared__ float part[16 * PTAB_TMAX * 16];
+  float* const part = Pv;
   const int b = (int)blockIdx.x;
   int q = 0;
 #pragma unroll
