@@ -798,12 +798,13 @@ void launch_attn_bwd(const float* dO, const float* q, const float* K, const floa
 // positional table (the same values k_attn_bwd2 sums):
 //   sK[t][j] = sum_n (dS[n][h][t] q[n][j]) scale,  sV[t][j] = sum_n A[n][h][t] bf(dO[n][j]),
 // h = j / DH.  A block takes 64 columns of a chunk of RS_CW windows; its wave s
-// the windows s, s + 8, ... (four at a time, every load first), the eight waves'
+// the windows s, s + 8, ... (half of them at a time, every load first), the eight waves'
 // sums are added in wave order into part[chunk][0|1][t][j], and a column sum over
 // the chunks follows (launch_colsum).  36 bytes of dS, q, A, dO per window and
 // column pair instead of the 2 T D floats per window chunk of k_attn_bwd2's sums.
 constexpr int RS_CW = 64;
 constexpr int RS_W = 8;  // waves per block
+constexpr int RS_B = RS_CW / (2 * RS_W);  // windows per wave and batch (two batches: 164 registers for one)
 template <int T>
 __global__ __launch_bounds__(64 * RS_W) void k_rank1_sums(const float* __restrict__ dS, const float* __restrict__ q,
                                                           const float* __restrict__ A, const float* __restrict__ dO,
@@ -818,10 +819,10 @@ __global__ __launch_bounds__(64 * RS_W) void k_rank1_sums(const float* __restric
 #pragma unroll
   for (int t = 0; t < T; ++t) sk[t] = sv[t] = 0.f;
 #pragma unroll
-  for (int i0 = 0; i0 < RS_CW; i0 += 4 * RS_W) {
-    float qv[4], ov[4], ds[4][T], aa[4][T];
+  for (int i0 = 0; i0 < RS_CW; i0 += RS_B * RS_W) {
+    float qv[RS_B], ov[RS_B], ds[RS_B][T], aa[RS_B][T];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < RS_B; ++u) {
       const int64_t n = n0 + min(i0 + RS_W * u + wave, nw - 1);  // clamped; the window is not added
       qv[u] = q[n * D + j];
       ov[u] = dO[n * D + j];
@@ -834,7 +835,7 @@ __global__ __launch_bounds__(64 * RS_W) void k_rank1_sums(const float* __restric
       }
     }
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
+    for (int u = 0; u < RS_B; ++u) {
       if (i0 + RS_W * u + wave < nw) {
         float o = ov[u];
         if (round_dO) o = __uint_as_float(pack_bf16x2(o, 0.f) << 16);
@@ -1084,7 +1085,7 @@ __global__ __launch_bounds__(64 * PTG_ROWS) void k_pos_table_grad_rows(const flo
                                                                        const float* __restrict__ Wv, int D, int rb,
                                                                        float* __restrict__ dP) {
   constexpr int JMAX = 8;  // D <= 512
-  __shared__ float S[(2 * T + 1) * 64 * JMAX];
+  __shared__ __align__(16) float S[(2 * T + 1) * 64 * JMAX];
   const int c = blockIdx.x * PTG_ROWS + (threadIdx.x >> 6), lane = threadIdx.x & 63;
   const int nj = D / 64;  // D a multiple of 64
   const int cc = min(c, D - 1);  // (rows past D: loads clamped, nothing stored)
@@ -1096,8 +1097,22 @@ __global__ __launch_bounds__(64 * PTG_ROWS) void k_pos_table_grad_rows(const flo
     wv[i] = Wv[(int64_t)cc * D + j];
     wq[i] = Wq[(int64_t)cc * D + j];
   }
-  for (int i = threadIdx.x; i < 2 * T * D; i += 64 * PTG_ROWS) S[i] = sKV[i];
-  for (int i = threadIdx.x; i < D; i += 64 * PTG_ROWS) S[2 * T * D + i] = sQ[i];
+  {  // every load of the staging first (float4; 2 T D + D is a multiple of 4)
+    constexpr int NU = ((2 * T + 1) * 64 * JMAX / 4 + 64 * PTG_ROWS - 1) / (64 * PTG_ROWS);
+    const int n4 = (2 * T * D) / 4, q4 = D / 4;
+    float4 x[NU];
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      const int i = threadIdx.x + 64 * PTG_ROWS * u;
+      x[u] = i < n4 ? reinterpret_cast<const float4*>(sKV)[i]
+                    : (i < n4 + q4 ? reinterpret_cast<const float4*>(sQ)[i - n4] : make_float4(0.f, 0.f, 0.f, 0.f));
+    }
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      const int i = threadIdx.x + 64 * PTG_ROWS * u;
+      if (i < n4 + q4) reinterpret_cast<float4*>(S)[i] = x[u];
+    }
+  }
   __syncthreads();
   if (c >= D) return;
   if (rb) {
@@ -1136,7 +1151,7 @@ __global__ __launch_bounds__(64 * PTG_ROWS) void k_pos_table_grad_rows(const flo
 
 void launch_pos_table_grad(const float* sKV, const float* sQ, const float* sY, const float* Wq, const float* Wk,
                            const float* Wv, int T, int D, int rb, float* dP, hipStream_t s) {
-  if (D % 64 == 0 && D <= 512 && (T == 4 || T == 8)) {
+  if (D % 64 == 0 && D <= 512 && (T == 4 || T == 8) && ((uintptr_t)sKV & 15) == 0 && ((uintptr_t)sQ & 15) == 0) {
     const dim3 grid((unsigned)((D + PTG_ROWS - 1) / PTG_ROWS));
     if (T == 8)
       hipLaunchKernelGGL(k_pos_table_grad_rows<8>, grid, dim3(64 * PTG_ROWS), 0, s, sKV, sQ, sY, Wq, Wk, Wv, D, rb,

@@ -84,7 +84,23 @@ __device__ __forceinline__ void refresh_ptab(const RefreshJob& jb, int lb, float
   float wv[KLMAX];
 #pragma unroll
   for (int u = 0; u < KLMAX; ++u) wv[u] = Wm[(int64_t)(k0 + min(u, kl - 1)) * D];  // (clamped: u < kl used)
-  for (int i = threadIdx.x; i < T * D; i += 256) Pv[i] = jb.use_pos ? M::val(M::cvt(jb.src[i])) : 0.f;
+  {  // every load of P first (float4; T D is a multiple of 4, src 16-byte aligned)
+    constexpr int NU = PTAB_TMAX * PTAB_DMAX / 4 / 256;
+    const int n4 = T * D / 4;
+    float4 x[NU];
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      const int i = threadIdx.x + 256 * u;
+      x[u] = (jb.use_pos && i < n4) ? reinterpret_cast<const float4*>(jb.src)[i] : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+#pragma unroll
+    for (int u = 0; u < NU; ++u) {
+      const int i = threadIdx.x + 256 * u;
+      if (i < n4)
+        reinterpret_cast<float4*>(Pv)[i] = make_float4(M::val(M::cvt(x[u].x)), M::val(M::cvt(x[u].y)),
+                                                       M::val(M::cvt(x[u].z)), M::val(M::cvt(x[u].w)));
+    }
+  }
   __syncthreads();
   float acc[T];
 #pragma unroll
@@ -123,7 +139,7 @@ __device__ __forceinline__ void refresh_ptab(const RefreshJob& jb, int lb, float
 template <bool BF>
 __global__ __launch_bounds__(256) void k_refresh(RefreshArgs a) {
   static_assert(16 * PTAB_TMAX * 16 <= PTAB_TMAX * PTAB_DMAX, "part fits in Pv");
-  __shared__ float Pv[PTAB_TMAX * PTAB_DMAX];
+  __shared__ __align__(16) float Pv[PTAB_TMAX * PTAB_DMAX];
   float* const part = Pv;
   const int b = (int)blockIdx.x;
   int q = 0;
@@ -171,6 +187,7 @@ bool launch_refresh(bool bf, const RefreshJob* jobs, int n, hipStream_t s) {
       nb = ((int64_t)(jb.K / KS) * (jb.N / 16) * 64 + 255) / 256;
     } else if (jb.kind == RJ_PTAB) {
       if ((jb.K != 4 && jb.K != 8) || jb.N > PTAB_DMAX || jb.N % 64 != 0) return false;
+      if (jb.use_pos && ((uintptr_t)jb.src & 15) != 0) return false;
       nb = 3 * (int64_t)(jb.N / 16);
     } else {
       return false;
