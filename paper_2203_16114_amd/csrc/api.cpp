@@ -812,7 +812,7 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // formed here otherwise).  With shared weights and G kept, the sums over the
   // repeats are single products over k N rows instead (the per-repeat buffers
   // are consecutive: G_0..G_{k-1} with dY_1..dY_k, Y_0..Y_{k-1} with dU_0..dU_{k-1}),
-  // formed once the last repeat's dU_0 exists.
+  // formed on the side stream once dO is done (below).
   const bool merged = m->kG && !m->cfg.untied_ffn;
   for (int r = k - 1; r >= 0; --r) {
     // untied FFN: repeat r's own W1, W2 and gradient blocks (each written once)
@@ -821,8 +821,8 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
     gd.gelu_u = m->kU + (int64_t)r * N * F;
     gd.halfC = hf;
     ok = launch_gemm(gd, ws, m->gws_cap, s) && ok;
-    order(m, s, w);  // dY_{r+1} and dU_r are complete
     if (!merged) {
+      order(m, s, w);  // dY_{r+1} and dU_r are complete
       const float beta = (r == k - 1 || m->cfg.untied_ffn) ? 0.f : 1.f;
       GemmArgs g2w;
       if (m->kG) {
@@ -838,13 +838,6 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
           gemm(D, F, N, at(m->kY, (int64_t)r * N * D), 1, D, rb, dUr(r), F, 1, rb, gr + L.at(P_W1, top) + wr, F, beta);
       g1w.halfA = g1w.halfB = hf;
       ok = launch_gemm(g1w, ws2, m->gws_cap, w) && ok;
-    } else if (r == 0) {
-      GemmArgs g2w = gemm(F, D, k * N, (const float*)m->kG, 1, F, rb, dYr(1), D, 1, rb, gr + L.at(P_W2, top), D, 0.f);
-      g2w.halfA = 1;
-      ok = launch_gemm(g2w, ws2, m->gws_cap, w) && ok;
-      GemmArgs g1w = gemm(D, F, k * N, m->kY, 1, D, rb, m->dU, F, 1, rb, gr + L.at(P_W1, top), F, 0.f);
-      g1w.halfA = g1w.halfB = hf;
-      ok = launch_gemm(g1w, ws2, m->gws_cap, w) && ok;
     }
     // dY_r = dY_{r+1} + dU_r . W1^T (the addend read from dY_{r+1}'s own buffer)
     GemmArgs gy = gemm(N, D, F, dUr(r), F, 1, rb, th + L.at(P_W1, top) + wr, 1, F, rb, dYr(r), D, 1.f);
@@ -852,12 +845,24 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
     gy.halfA = hf;
     ok = launch_gemm(gy, ws, m->gws_cap, s) && ok;
   }
-  order(m, s, w);  // dY_0 is complete
-  // side: dWo = O^T . dY_0
-  launch_gemm(gemm(D, D, N, m->kO, 1, D, rb, dYr(0), D, 1, rb, gr + L.at(P_WO, top), D, 0.f), ws2, m->gws_cap, w);
   // attention output projection: dO = dY_0 . Wo^T, then the attention (last
   // query row) -> dQ, dK, dV
   launch_gemm(gemm(N, D, D, dYr(0), D, 1, rb, th + L.at(P_WO, top), 1, D, rb, m->dO, D, 0.f), ws, m->gws_cap, s);
+  // the side stream's large products start once dO is done (dY_0 complete), so
+  // that they share the CUs with the attention backward's memory-bound kernels
+  // rather than with the FFN chain's products
+  order(m, s, w);
+  if (merged) {
+    // dW2 = sum_r G_r^T dY_{r+1} and dW1 = sum_r Y_r^T dU_r over the k N rows
+    GemmArgs g2w = gemm(F, D, k * N, (const float*)m->kG, 1, F, rb, dYr(1), D, 1, rb, gr + L.at(P_W2, top), D, 0.f);
+    g2w.halfA = 1;
+    ok = launch_gemm(g2w, ws2, m->gws_cap, w) && ok;
+    GemmArgs g1w = gemm(D, F, k * N, m->kY, 1, D, rb, m->dU, F, 1, rb, gr + L.at(P_W1, top), F, 0.f);
+    g1w.halfA = g1w.halfB = hf;
+    ok = launch_gemm(g1w, ws2, m->gws_cap, w) && ok;
+  }
+  // side: dWo = O^T . dY_0
+  launch_gemm(gemm(D, D, N, m->kO, 1, D, rb, dYr(0), D, 1, rb, gr + L.at(P_WO, top), D, 0.f), ws2, m->gws_cap, w);
   // sP: [0, T D) sum over windows of dK, [T D, 2T D) of dV (from the attention
   // backward), [2T D, (2T+1) D) of dQ, [(2T+1) D, (2T+2) D) of dY_0
   float* sK = m->sP;

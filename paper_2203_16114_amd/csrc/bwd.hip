@@ -1393,51 +1393,6 @@ __global__ __launch_bounds__(64) void k_emb_piece(const float* __restrict__ dX, 
   if (e > 64 && lane + 64 < e) part[(int64_t)p * e + lane + 64] = a1;
 }
 
-// The same piece sums with 16-byte loads, for e a multiple of 4 dividing 256:
-// LP = e / 4 lanes per position (four features each), 64 / LP positions per
-// load instruction, 16 loads in flight per lane; the lanes' position classes
-// are added in a fixed tree at the end.
-__global__ __launch_bounds__(64) void k_emb_piece4(const float* __restrict__ dX, int e, const int* __restrict__ perm,
-                                                   const int* __restrict__ piece, const int* __restrict__ pstart,
-                                                   float* __restrict__ part) {
-  constexpr int B = 16;
-  const int p = blockIdx.x;
-  if (p >= pstart[256]) return;
-  const int st = piece[3 * p + 1], len = piece[3 * p + 2];
-  const int lane = threadIdx.x;
-  const int LP = e >> 2, ipl = 64 / LP, sub = lane / LP, f = (lane - sub * LP) * 4;
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int i0 = 0; i0 < len; i0 += 64) {
-    const int n = min(64, len - i0);
-    const int my = perm[st + i0 + min(lane, n - 1)];
-    for (int u0 = 0; u0 < n; u0 += B * ipl) {
-      float4 x[B];
-#pragma unroll
-      for (int u = 0; u < B; ++u) {
-        const int j = u0 + u * ipl + sub;  // this lane's position (clamped; masked below)
-        const int q = __builtin_amdgcn_ds_bpermute(4 * min(j, n - 1), my);
-        x[u] = *reinterpret_cast<const float4*>(dX + (int64_t)q * e + f);
-      }
-#pragma unroll
-      for (int u = 0; u < B; ++u) {
-        if (u0 + u * ipl + sub < n) {
-          acc.x += x[u].x;
-          acc.y += x[u].y;
-          acc.z += x[u].z;
-          acc.w += x[u].w;
-        }
-      }
-    }
-  }
-  for (int d = 1; d < ipl; d <<= 1) {
-    acc.x += __shfl_down(acc.x, d * LP, 64);
-    acc.y += __shfl_down(acc.y, d * LP, 64);
-    acc.z += __shfl_down(acc.z, d * LP, 64);
-    acc.w += __shfl_down(acc.w, d * LP, 64);
-  }
-  if (lane < LP) *reinterpret_cast<float4*>(part + (int64_t)p * e + f) = acc;
-}
-
 // dE[v][c] = sum of byte v's pieces: row group rg of 256 / e takes every
 // (256 / e)-th piece in order, then the groups are added in order
 __global__ __launch_bounds__(256) void k_emb_sum(const float* __restrict__ part, const int* __restrict__ pstart, int e,
@@ -1475,12 +1430,8 @@ void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int
   hipLaunchKernelGGL(k_emb_pieces, dim3(1), dim3(1024), 0, s, (const int*)w.tot, w.base, w.pstart, w.piece);
   hipLaunchKernelGGL(k_emb_scatter, dim3(nb), dim3(1024), 0, s, win, (int)M, (const int*)w.off,
                      (const int*)w.base, w.perm);
-  if (e % 4 == 0 && 256 % e == 0 && ((uintptr_t)dX & 15) == 0 && ((uintptr_t)w.part & 15) == 0)
-    hipLaunchKernelGGL(k_emb_piece4, dim3(pmax), dim3(64), 0, s, dX, e, (const int*)w.perm, (const int*)w.piece,
-                       (const int*)w.pstart, w.part);
-  else
-    hipLaunchKernelGGL(k_emb_piece, dim3(pmax), dim3(64), 0, s, dX, e, (const int*)w.perm, (const int*)w.piece,
-                       (const int*)w.pstart, w.part);
+  hipLaunchKernelGGL(k_emb_piece, dim3(pmax), dim3(64), 0, s, dX, e, (const int*)w.perm, (const int*)w.piece,
+                     (const int*)w.pstart, w.part);
   hipLaunchKernelGGL(k_emb_sum, dim3(256), dim3(256), 0, s, (const float*)w.part, (const int*)w.pstart, e, dE);
 }
 
