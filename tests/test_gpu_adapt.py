@@ -69,6 +69,31 @@ def test_bf16_gradient_matches_emulating_oracle(B):
         assert rel <= 1e-2, (name, rel)
 
 
+# d = 256 shapes of the rank-one key/value path (k_attn_bwd_r1 with four columns per
+# lane, k_dx_rank1, k_rank1_sums, the positional-table gradient from window sums):
+# the main workload's token shape (T = 8, dh = 32) and a T = 4 one (dh = 64)
+RANK1_SHAPES = {
+    "T8-dh32": dict(W=64, e=32, g=8, H=8, F=512, k=2),
+    "T4-dh64": dict(W=32, e=32, g=8, H=4, F=512, k=2),
+}
+
+
+@pytest.mark.parametrize("name", sorted(RANK1_SHAPES))
+def test_bf16_gradient_rank_one_shapes_match_emulating_oracle(name):
+    """B = 300 windows (partial tiles and a partial window group of 16)."""
+    shape = RANK1_SHAPES[name]
+    streams = synth.random_streams(0x77 + len(name), 300, shape["W"] + 40)
+    m, cfg, flat, g, _, w, y = _grad_run(shape, "bf16", 0x5150, streams, shape["W"] + 17)
+    _, ref = O.forward_backward(flat, cfg, w, y, mode="bf16")
+    gp = O.unflatten(g, cfg)
+    for pname, _ in O.param_layout(cfg):
+        a = gp[pname].astype(np.float64).ravel()
+        b = np.asarray(ref[pname], np.float64).ravel()
+        rel = np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30)
+        assert rel <= 1e-2, (name, pname, rel)
+        assert np.linalg.norm(b) > 0, (name, pname)
+
+
 @pytest.mark.parametrize("kind", ["skewed", "one_byte"])
 def test_fp32_embedding_gradient_over_many_sort_blocks(kind):
     """1100 kept windows of 32 bytes: 35200 positions, several blocks of the
