@@ -496,12 +496,12 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
          dalloc(m, &m->dO, K * D * 4) && dalloc(m, &m->dQ, K * D * 4) && dalloc(m, &m->dK, K * T * D * 4) &&
          dalloc(m, &m->dV, K * T * D * 4) && dalloc(m, &m->dX, K * T * D * 4) && dalloc(m, &m->Xk, K * T * D * es) &&
          dalloc(m, &m->sP, (2 * T + 2) * D * 4) &&
-         dalloc(m, &m->apart, attn_bwd_part_floats(K, T, D, cfg->H) * 4) &&
+         dalloc(m, &m->apart, std::max(attn_bwd_part_floats(K, T, D, cfg->H), rank1_sums_part_floats(K, T, D)) * 4) &&
          dalloc(m, &m->dSc, K * cfg->H * T * 4) &&
          (!bf || (dalloc(m, &m->WkT, (int64_t)D * D * 2) && dalloc(m, &m->WvT, (int64_t)D * D * 2))) &&
          dalloc(m, &m->gws, (m->gws_cap = adapt_gemm_ws(m, K)) * 4) &&
          dalloc(m, &m->ews, embed_bwd_ws_floats(K * W, cfg->e) * 4) &&
-         dalloc(m, &m->cws, colsum_ws_floats(std::max<int64_t>(2 * T * D, 256)) * 4) &&
+         dalloc(m, &m->cws, colsum_ws_floats(std::max<int64_t>((int64_t)(2 * T + 2) * D, 256)) * 4) &&
          dalloc(m, &m->gws2, m->gws_cap * 4) && dalloc(m, &m->cws2, colsum_ws_floats(T * D) * 4);
     if (ok) ok = hipStreamCreateWithFlags(&m->side, hipStreamNonBlocking) == hipSuccess;
     for (int i = 0; ok && i < 16; ++i) {
@@ -877,11 +877,13 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   const bool pow2 = (T & (T - 1)) == 0 && (L.DH & (L.DH - 1)) == 0;
   const bool rank1 = m->bf && m->WkT && pow2 && dx_rank1_built(T, D, H);
   // rank1: the sums over windows of dK and dV (sK, sV; read by the positional
-  // gradients of a single layer only) from the rank-one rows
+  // gradients of a single layer only) from the rank-one rows, with those of dQ
+  // and dY_0 (sQ, sY) in the same pass
+  const bool sums1 = rank1 && NL == 1 && m->cfg.use_pos;
   launch_attn_bwd(m->dO, m->kq, m->kK, m->kV, m->kA, N, T, D, H, ascale, rb, m->dQ, rank1 ? nullptr : m->dK,
                   rank1 ? nullptr : m->dV, rank1 ? nullptr : m->apart, sK, m->cws, s, m->bf ? m->dSc : nullptr);
-  if (rank1 && NL == 1 && m->cfg.use_pos &&
-      !launch_rank1_sums(m->dSc, m->kq, m->kA, m->dO, N, T, D, H, ascale, rb, m->apart, sK, m->cws, s))
+  if (sums1 &&
+      !launch_rank1_sums(m->dSc, m->kq, m->kA, m->dO, m->dQ, dYr(0), N, T, D, H, ascale, rb, m->apart, sK, m->cws, s))
     ok = false;
   auto log2i = [](int x) {
     int r = 0;
@@ -903,7 +905,7 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
     }
     return launch_gemm(g, ws2, m->gws_cap, w);
   };
-  if (m->cfg.use_pos) launch_colsum(m->dQ, N, D, D, sQ, 0.f, m->cws, s);
+  if (m->cfg.use_pos && !sums1) launch_colsum(m->dQ, N, D, D, sQ, 0.f, m->cws, s);
   order(m, s, w);  // dQ, dK, dV and their sums over windows are complete
   // side: dWk = X^T dK, dWv = X^T dV (dK, dV stay fp32), with X = G + P[t]:
   // G^T dZ as GEMMs on the byte-embedding part G, then P^T (sum over windows of
@@ -911,17 +913,18 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   if (NL == 1) {
     ok = kv_grad(m->Xk, 1, D, hf, false, gr + L.at(P_WK, top)) && ok;
     ok = kv_grad(m->Xk, 1, D, hf, true, gr + L.at(P_WV, top)) && ok;
-    if (m->cfg.use_pos) {
-      launch_pos_grad(m->bf, m->Pc, sK, 0, T, D, gr + L.at(P_WK, top), w);
-      launch_pos_grad(m->bf, m->Pc, sV, 0, T, D, gr + L.at(P_WV, top), w);
-    }
-    // side: dWq = X_last^T dQ (+ its positional part); Xk was written on this
-    // stream, dQ before the last mark
+    // side: dWq = X_last^T dQ; Xk was written on this stream, dQ before the last mark
     GemmArgs gq = gemm(D, D, N, at(m->Xk, (int64_t)(T - 1) * D), 1, (int64_t)T * D, rb, m->dQ, D, 1, 0,
                        gr + L.at(P_WQ, top), D, 0.f);
     gq.halfA = hf;
     ok = launch_gemm(gq, ws2, m->gws_cap, w) && ok;
-    if (m->cfg.use_pos) launch_pos_grad(m->bf, m->Pc, sQ, T - 1, 1, D, gr + L.at(P_WQ, top), w);
+    if (m->cfg.use_pos) {
+      // the positional parts of dWk, dWv, dWq in one launch
+      const float* S3[3] = {sK, sV, sQ};
+      const int t03[3] = {0, 0, T - 1}, nt3[3] = {T, T, 1};
+      float* dW3[3] = {gr + L.at(P_WK, top), gr + L.at(P_WV, top), gr + L.at(P_WQ, top)};
+      launch_pos_grad3(m->bf, m->Pc, S3, t03, nt3, dW3, 3, D, w);
+    }
   } else {
     // the top layer's input: the layer below's output, rounded (bf16 storage point)
     ok = kv_grad(Xtop, 1, D, false, false, gr + L.at(P_WK, top)) && ok;
@@ -954,7 +957,7 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   } else if (m->cfg.use_pos) {
     // positional table: dP[t] = sum_n dX[n][t], from the sums over windows of
     // dK, dV, dQ and dY_0 times the weights; then the byte embedding
-    launch_colsum(dYr(0), N, D, D, sY, 0.f, m->cws, s);
+    if (!sums1) launch_colsum(dYr(0), N, D, D, sY, 0.f, m->cws, s);
     launch_pos_table_grad(sK, sQ, sY, th + L.at(P_WQ, top), th + L.at(P_WK, top), th + L.at(P_WV, top), T, D, rb,
                           gr + L.off[P_P], s);
   } else {

@@ -795,37 +795,42 @@ void launch_attn_bwd(const float* dO, const float* q, const float* K, const floa
 
 // Sums over windows of the last query row's key and value gradients from their
 // rank-one rows, for the positional parts of the weight gradients and of the
-// positional table (the same values k_attn_bwd2 sums):
+// positional table (the same values k_attn_bwd2 sums), with the sums of dQ and
+// dY0 beside them:
 //   sK[t][j] = sum_n (dS[n][h][t] q[n][j]) scale,  sV[t][j] = sum_n A[n][h][t] bf(dO[n][j]),
-// h = j / DH.  A block takes 64 columns of a chunk of RS_CW windows; its wave s
-// the windows s, s + 8, ... (half of them at a time, every load first), the eight waves'
-// sums are added in wave order into part[chunk][0|1][t][j], and a column sum over
-// the chunks follows (launch_colsum).  36 bytes of dS, q, A, dO per window and
-// column pair instead of the 2 T D floats per window chunk of k_attn_bwd2's sums.
+//   sQ[j] = sum_n dQ[n][j],  sY[j] = sum_n dY0[n][j],  h = j / DH.
+// A block takes 64 columns of a chunk of RS_CW windows; its wave s the windows
+// s, s + 8, ... (half of them at a time, every load first), the eight waves'
+// sums are added in wave order into part[chunk][2 T + 2][D] (rows sK, sV, sQ,
+// sY), and a column sum over the chunks follows (launch_colsum).
 constexpr int RS_CW = 64;
 constexpr int RS_W = 8;  // waves per block
 constexpr int RS_B = RS_CW / (2 * RS_W);  // windows per wave and batch (two batches: 164 registers for one)
 template <int T>
 __global__ __launch_bounds__(64 * RS_W) void k_rank1_sums(const float* __restrict__ dS, const float* __restrict__ q,
                                                           const float* __restrict__ A, const float* __restrict__ dO,
+                                                          const float* __restrict__ dQ, const float* __restrict__ dY0,
                                                           int64_t N, int D, int H, int dsh, float scale,
                                                           int round_dO, float* __restrict__ part) {
-  __shared__ float red[RS_W][2][T][64];
+  constexpr int NR = 2 * T + 2;  // rows of sums
+  __shared__ float red[RS_W][NR][64];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int j = blockIdx.y * 64 + lane, h = j >> dsh;
   const int64_t c = blockIdx.x, n0 = c * RS_CW;
   const int nw = (int)min<int64_t>(RS_CW, N - n0);
-  float sk[T], sv[T];
+  float sk[T], sv[T], sq = 0.f, sy = 0.f;
 #pragma unroll
   for (int t = 0; t < T; ++t) sk[t] = sv[t] = 0.f;
 #pragma unroll
   for (int i0 = 0; i0 < RS_CW; i0 += RS_B * RS_W) {
-    float qv[RS_B], ov[RS_B], ds[RS_B][T], aa[RS_B][T];
+    float qv[RS_B], ov[RS_B], gq[RS_B], gy[RS_B], ds[RS_B][T], aa[RS_B][T];
 #pragma unroll
     for (int u = 0; u < RS_B; ++u) {
       const int64_t n = n0 + min(i0 + RS_W * u + wave, nw - 1);  // clamped; the window is not added
       qv[u] = q[n * D + j];
       ov[u] = dO[n * D + j];
+      gq[u] = dQ[n * D + j];
+      gy[u] = dY0[n * D + j];
 #pragma unroll
       for (int t = 0; t < T; t += 4) {
         const float4 x = *reinterpret_cast<const float4*>(dS + (n * H + h) * T + t);
@@ -844,32 +849,38 @@ __global__ __launch_bounds__(64 * RS_W) void k_rank1_sums(const float* __restric
           sk[t] += (ds[u][t] * qv[u]) * scale;
           sv[t] += aa[u][t] * o;
         }
+        sq += gq[u];
+        sy += gy[u];
       }
     }
   }
 #pragma unroll
   for (int t = 0; t < T; ++t) {
-    red[wave][0][t][lane] = sk[t];
-    red[wave][1][t][lane] = sv[t];
+    red[wave][t][lane] = sk[t];
+    red[wave][T + t][lane] = sv[t];
   }
+  red[wave][2 * T][lane] = sq;
+  red[wave][2 * T + 1][lane] = sy;
   __syncthreads();
-  for (int i = threadIdx.x; i < 2 * T * 64; i += 64 * RS_W) {
-    const int which = i / (T * 64), t = (i / 64) % T, jj = i % 64;
-    float v = red[0][which][t][jj];
+  for (int i = threadIdx.x; i < NR * 64; i += 64 * RS_W) {
+    const int r = i / 64, jj = i % 64;
+    float v = red[0][r][jj];
 #pragma unroll
-    for (int w = 1; w < RS_W; ++w) v += red[w][which][t][jj];
-    part[((c * 2 + which) * T + t) * D + blockIdx.y * 64 + jj] = v;
+    for (int w = 1; w < RS_W; ++w) v += red[w][r][jj];
+    part[(c * NR + r) * D + blockIdx.y * 64 + jj] = v;
   }
 }
 
-int64_t rank1_sums_part_floats(int64_t N, int T, int D) { return (N + RS_CW - 1) / RS_CW * 2 * T * D; }
+int64_t rank1_sums_part_floats(int64_t N, int T, int D) { return (N + RS_CW - 1) / RS_CW * (2 * T + 2) * D; }
 
-bool launch_rank1_sums(const float* dS, const float* q, const float* A, const float* dO, int64_t N, int T, int D,
-                       int H, float scale, int round_dO, float* part, float* colsums, float* cws, hipStream_t s) {
+bool launch_rank1_sums(const float* dS, const float* q, const float* A, const float* dO, const float* dQ,
+                       const float* dY0, int64_t N, int T, int D, int H, float scale, int round_dO, float* part,
+                       float* colsums, float* cws, hipStream_t s) {
   const int DH = D / H;
   if (D % 64 != 0 || (DH & (DH - 1)) != 0 || (T != 4 && T != 8)) return false;
+  const int64_t cols = (int64_t)(2 * T + 2) * D;
   if (N <= 0) {
-    launch_zero(reinterpret_cast<uint32_t*>(colsums), (int64_t)2 * T * D, s);
+    launch_zero(reinterpret_cast<uint32_t*>(colsums), cols, s);
     return true;
   }
   int dsh = 0;
@@ -877,12 +888,12 @@ bool launch_rank1_sums(const float* dS, const float* q, const float* A, const fl
   const int64_t chunks = (N + RS_CW - 1) / RS_CW;
   const dim3 grid((unsigned)chunks, (unsigned)(D / 64));
   if (T == 8)
-    hipLaunchKernelGGL(k_rank1_sums<8>, grid, dim3(64 * RS_W), 0, s, dS, q, A, dO, N, D, H, dsh, scale, round_dO,
-                       part);
+    hipLaunchKernelGGL(k_rank1_sums<8>, grid, dim3(64 * RS_W), 0, s, dS, q, A, dO, dQ, dY0, N, D, H, dsh, scale,
+                       round_dO, part);
   else
-    hipLaunchKernelGGL(k_rank1_sums<4>, grid, dim3(64 * RS_W), 0, s, dS, q, A, dO, N, D, H, dsh, scale, round_dO,
-                       part);
-  launch_colsum(part, chunks, (int64_t)2 * T * D, (int64_t)2 * T * D, colsums, 0.f, cws, s);
+    hipLaunchKernelGGL(k_rank1_sums<4>, grid, dim3(64 * RS_W), 0, s, dS, q, A, dO, dQ, dY0, N, D, H, dsh, scale,
+                       round_dO, part);
+  launch_colsum(part, chunks, cols, cols, colsums, 0.f, cws, s);
   return true;
 }
 
@@ -1536,6 +1547,46 @@ void launch_pos_grad(bool bf, const void* P, const float* S, int t0, int nt, int
     hipLaunchKernelGGL(k_pos_grad<true>, grid, dim3(256), 0, s, (const uint16_t*)P, S, t0, nt, D, dW);
   else
     hipLaunchKernelGGL(k_pos_grad<false>, grid, dim3(256), 0, s, (const float*)P, S, t0, nt, D, dW);
+}
+
+// Up to three positional parts in one launch (blockIdx.y = the job), each as
+// k_pos_grad computes it.
+struct PosGradJobs {
+  const float* S[3];
+  float* dW[3];
+  int t0[3], nt[3];
+};
+template <bool BF>
+__global__ void k_pos_grad3(const typename Mma<BF>::T* __restrict__ P, PosGradJobs jb, int D) {
+  typedef Mma<BF> M;
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= (int64_t)D * D) return;
+  const int y = blockIdx.y;
+  // the job's fields, selected with constant indexes (blockIdx.y is uniform)
+  const float* S = y == 0 ? jb.S[0] : (y == 1 ? jb.S[1] : jb.S[2]);
+  float* dW = y == 0 ? jb.dW[0] : (y == 1 ? jb.dW[1] : jb.dW[2]);
+  const int t0 = y == 0 ? jb.t0[0] : (y == 1 ? jb.t0[1] : jb.t0[2]);
+  const int nt = y == 0 ? jb.nt[0] : (y == 1 ? jb.nt[1] : jb.nt[2]);
+  const int r = (int)(i / D), c = (int)(i % D);
+  float acc = 0.f;
+  for (int u = 0; u < nt; ++u) acc += M::val(P[(t0 + u) * D + r]) * S[u * D + c];
+  dW[i] += acc;
+}
+void launch_pos_grad3(bool bf, const void* P, const float* const* S, const int* t0, const int* nt, float* const* dW,
+                      int njobs, int D, hipStream_t s) {
+  if (njobs < 1 || njobs > 3) return;
+  PosGradJobs jb{};
+  for (int j = 0; j < njobs; ++j) {
+    jb.S[j] = S[j];
+    jb.dW[j] = dW[j];
+    jb.t0[j] = t0[j];
+    jb.nt[j] = nt[j];
+  }
+  const dim3 grid((unsigned)(((int64_t)D * D + 255) / 256), (unsigned)njobs);
+  if (bf)
+    hipLaunchKernelGGL(k_pos_grad3<true>, grid, dim3(256), 0, s, (const uint16_t*)P, jb, D);
+  else
+    hipLaunchKernelGGL(k_pos_grad3<false>, grid, dim3(256), 0, s, (const float*)P, jb, D);
 }
 
 // -------------------------------------------------------------------- Adam ----

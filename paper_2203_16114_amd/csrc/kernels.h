@@ -148,11 +148,13 @@ bool launch_dx_rank1(const float* q, const float* dO, const float* dS, const flo
                      hipStream_t s);
 int64_t attn_bwd_part_floats(int64_t N, int T, int D, int H);
 // sums over windows of the rank-one key and value gradients of the last query
-// row into colsums [2][T][D] (sK, then sV); part: rank1_sums_part_floats floats
-// (at most attn_bwd_part_floats); false when the shape is not taken
+// row, of dQ and of dY0 into colsums [2 T + 2][D] (sK [T][D], sV [T][D], sQ, sY);
+// part: rank1_sums_part_floats floats (at most attn_bwd_part_floats); false when
+// the shape is not taken
 int64_t rank1_sums_part_floats(int64_t N, int T, int D);
-bool launch_rank1_sums(const float* dS, const float* q, const float* A, const float* dO, int64_t N, int T, int D,
-                       int H, float scale, int round_dO, float* part, float* colsums, float* cws, hipStream_t s);
+bool launch_rank1_sums(const float* dS, const float* q, const float* A, const float* dO, const float* dQ,
+                       const float* dY0, int64_t N, int T, int D, int H, float scale, int round_dO, float* part,
+                       float* colsums, float* cws, hipStream_t s);
 void launch_pos_table_grad(const float* sKV, const float* sQ, const float* sY, const float* Wq, const float* Wk,
                            const float* Wv, int T, int D, int rb, float* dP, hipStream_t s);
 void launch_add(float* y, const float* x, int64_t rows, int64_t cols, int64_t ldy, int64_t ldx, hipStream_t s);
@@ -165,6 +167,9 @@ void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, i
                         hipStream_t s);
 // dW[i][j] += sum_{u < nt} P[t0 + u][i] * S[u][j]  (P: operand copy [T][D])
 void launch_pos_grad(bool bf, const void* P, const float* S, int t0, int nt, int D, float* dW, hipStream_t s);
+// up to three positional parts (launch_pos_grad's (S, t0, nt, dW)) in one launch
+void launch_pos_grad3(bool bf, const void* P, const float* const* S, const int* t0, const int* nt, float* const* dW,
+                      int njobs, int D, hipStream_t s);
 void launch_adam(float* theta, const float* grad, float* m, float* v, int64_t n, float lr, float b1, float b2,
                  float eps, float bc1, float bc2, hipStream_t s, hipEvent_t t0 = nullptr, hipEvent_t t1 = nullptr);
 
