@@ -29,6 +29,9 @@ struct trace_model {
   float* PW;  // [3][T][D] positional parts of the q, k, v projections
   uint4 *Wq, *Wk, *Wv, *Wo, *W1, *W2, *Wout;
   uint4 *WkT, *WvT;  // bf16 models that keep activations: packed Wk^T, Wv^T (input gradient of the tokens)
+  // bf16 models that keep activations: the master's Wq .. Wout range as bf16
+  // operand values, same order (B operands of the update's products)
+  uint16_t* Wh;
   // Performer attention: packed random projection (device), features, set yet
   uint4* Om;
   int nfeat;
@@ -249,11 +252,13 @@ bool refresh_operands(trace_model* m, hipStream_t s) {
       job(RJ_CVT, th + L.off[P_E], m->Ec, L.size[P_E], 0),
       pos ? job(RJ_CVT, th + L.off[P_P], m->Pc, L.size[P_P], 0)
           : job(RJ_ZERO, nullptr, m->Pc, (L.size[P_P] * (m->bf ? 2 : 4) + 3) / 4, 0),
-      // the update's input gradient of the tokens (bf16 models that keep activations)
+      // the update's input gradient of the tokens and the B operands of its
+      // products (bf16 models that keep activations)
       job(RJ_PACKT, th + L.at(P_WK, top), m->WkT, D, D),
       job(RJ_PACKT, th + L.at(P_WV, top), m->WvT, D, D),
+      job(RJ_CVT8, th + L.off[P_WQ], m->Wh, L.off[P_BOUT] - L.off[P_WQ], 0),
   };
-  const int njobs = (int)(sizeof(jobs) / sizeof(jobs[0])) - (m->WkT ? 0 : 2);
+  const int njobs = (int)(sizeof(jobs) / sizeof(jobs[0])) - (m->WkT ? 0 : 3);
   bool ok = launch_refresh(m->bf, jobs, njobs, s);
   // untied FFN: the packed copies of repeats 1 .. k-1
   const int64_t es_ = m->bf ? 2 : 4;
@@ -498,7 +503,8 @@ extern "C" int trace_create(const trace_config* cfg, trace_model** out) {
          dalloc(m, &m->sP, (2 * T + 2) * D * 4) &&
          dalloc(m, &m->apart, std::max(attn_bwd_part_floats(K, T, D, cfg->H), rank1_sums_part_floats(K, T, D)) * 4) &&
          dalloc(m, &m->dSc, K * cfg->H * T * 4) &&
-         (!bf || (dalloc(m, &m->WkT, (int64_t)D * D * 2) && dalloc(m, &m->WvT, (int64_t)D * D * 2))) &&
+         (!bf || (dalloc(m, &m->WkT, (int64_t)D * D * 2) && dalloc(m, &m->WvT, (int64_t)D * D * 2) &&
+                  dalloc(m, &m->Wh, (m->L.off[P_BOUT] - m->L.off[P_WQ]) * 2))) &&
          dalloc(m, &m->gws, (m->gws_cap = adapt_gemm_ws(m, K)) * 4) &&
          dalloc(m, &m->ews, embed_bwd_ws_floats(K * W, cfg->e) * 4) &&
          dalloc(m, &m->cws, colsum_ws_floats(std::max<int64_t>((int64_t)(2 * T + 2) * D, 256)) * 4) &&
@@ -787,6 +793,12 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // bf16 element e of a buffer whose elements are bf16 (hf) or fp32
   auto at = [&](float* p, int64_t e) { return hf ? (float*)((uint16_t*)p + e) : p + e; };
   auto dUr = [&](int r) { return at(m->dU, (int64_t)r * N * F); };
+  // B operand from a weight of the master at offset o (Wq .. Wout): its bf16
+  // image when the model keeps one (the same rounded values, half the bytes)
+  const int hw = m->Wh ? 1 : 0;
+  auto wsrc = [&](int64_t o) {
+    return hw ? (const float*)(m->Wh + (o - L.off[P_WQ])) : (const float*)(th + o);
+  };
   // stacked layers: this sequence runs the top layer (its weights at layer
   // NL - 1, its input the kept output of the layers below), then
   // lower_backward runs each lower layer down to the tokens
@@ -804,7 +816,9 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   ok = launch_gemm(go, ws2, m->gws_cap, w) && ok;
   launch_colsum(m->dz, N, 256, 256, gr + L.off[P_BOUT], 0.f, m->cws2, w);
   // dY_k = dz . Wout^T
-  launch_gemm(gemm(N, D, 256, m->dz, 256, 1, rb, th + L.off[P_WOUT], 1, 256, rb, dYr(k), D, 0.f), ws, m->gws_cap, s);
+  GemmArgs gk = gemm(N, D, 256, m->dz, 256, 1, rb, wsrc(L.off[P_WOUT]), 1, 256, rb, dYr(k), D, 0.f);
+  gk.halfB = hw;
+  ok = launch_gemm(gk, ws, m->gws_cap, s) && ok;
   // shared FFN, repeats in reverse: dU_r = (dY_{r+1} . W2^T) * GELU'(U_r),
   // dY_r = dY_{r+1} + dU_r . W1^T; once dU_r exists the side stream forms
   // dW2 += G_r^T . dY_{r+1} and dW1 += Y_r^T . dU_r (accumulated over the repeats
@@ -817,9 +831,10 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   for (int r = k - 1; r >= 0; --r) {
     // untied FFN: repeat r's own W1, W2 and gradient blocks (each written once)
     const int64_t wr = m->cfg.untied_ffn ? (int64_t)r * D * F : 0;
-    GemmArgs gd = gemm(N, F, D, dYr(r + 1), D, 1, rb, th + L.at(P_W2, top) + wr, 1, D, rb, dUr(r), F, 0.f);
+    GemmArgs gd = gemm(N, F, D, dYr(r + 1), D, 1, rb, wsrc(L.at(P_W2, top) + wr), 1, D, rb, dUr(r), F, 0.f);
     gd.gelu_u = m->kU + (int64_t)r * N * F;
     gd.halfC = hf;
+    gd.halfB = hw;
     ok = launch_gemm(gd, ws, m->gws_cap, s) && ok;
     if (!merged) {
       order(m, s, w);  // dY_{r+1} and dU_r are complete
@@ -840,14 +855,17 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
       ok = launch_gemm(g1w, ws2, m->gws_cap, w) && ok;
     }
     // dY_r = dY_{r+1} + dU_r . W1^T (the addend read from dY_{r+1}'s own buffer)
-    GemmArgs gy = gemm(N, D, F, dUr(r), F, 1, rb, th + L.at(P_W1, top) + wr, 1, F, rb, dYr(r), D, 1.f);
+    GemmArgs gy = gemm(N, D, F, dUr(r), F, 1, rb, wsrc(L.at(P_W1, top) + wr), 1, F, rb, dYr(r), D, 1.f);
     gy.Cin = dYr(r + 1);
     gy.halfA = hf;
+    gy.halfB = hw;
     ok = launch_gemm(gy, ws, m->gws_cap, s) && ok;
   }
   // attention output projection: dO = dY_0 . Wo^T, then the attention (last
   // query row) -> dQ, dK, dV
-  launch_gemm(gemm(N, D, D, dYr(0), D, 1, rb, th + L.at(P_WO, top), 1, D, rb, m->dO, D, 0.f), ws, m->gws_cap, s);
+  GemmArgs go2 = gemm(N, D, D, dYr(0), D, 1, rb, wsrc(L.at(P_WO, top)), 1, D, rb, m->dO, D, 0.f);
+  go2.halfB = hw;
+  ok = launch_gemm(go2, ws, m->gws_cap, s) && ok;
   // the side stream's large products start once dO is done (dY_0 complete), so
   // that they share the CUs with the attention backward's memory-bound kernels
   // rather than with the FFN chain's products
@@ -938,12 +956,16 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // (launch_dx_rank1, which adds dY_0); otherwise two products over every token
   // row, then dY_0
   if (rank1) ok = launch_dx_rank1(m->kq, m->dO, m->dSc, m->kA, m->WkT, m->WvT, dYr(0), N, T, D, H, ascale, m->dX, s) && ok;
-  if (!rank1)
-    launch_gemm2(gemm(N * T, D, D, m->dK, D, 1, 0, th + L.at(P_WK, top), 1, D, rb, m->dX, D, 0.f),
-                 gemm(N * T, D, D, m->dV, D, 1, 0, th + L.at(P_WV, top), 1, D, rb, m->dX, D, 0.f), ws, m->gws_cap, s);
-  launch_gemm(gemm(N, D, D, m->dQ, D, 1, 0, th + L.at(P_WQ, top), 1, D, rb, m->dX + (int64_t)(T - 1) * D, (int64_t)T * D,
-                   1.f),
-              ws, m->gws_cap, s);
+  if (!rank1) {
+    GemmArgs gxk = gemm(N * T, D, D, m->dK, D, 1, 0, wsrc(L.at(P_WK, top)), 1, D, rb, m->dX, D, 0.f);
+    GemmArgs gxv = gemm(N * T, D, D, m->dV, D, 1, 0, wsrc(L.at(P_WV, top)), 1, D, rb, m->dX, D, 0.f);
+    gxk.halfB = gxv.halfB = hw;
+    launch_gemm2(gxk, gxv, ws, m->gws_cap, s);
+  }
+  GemmArgs gxq = gemm(N, D, D, m->dQ, D, 1, 0, wsrc(L.at(P_WQ, top)), 1, D, rb, m->dX + (int64_t)(T - 1) * D,
+                      (int64_t)T * D, 1.f);
+  gxq.halfB = hw;
+  ok = launch_gemm(gxq, ws, m->gws_cap, s) && ok;
   if (!rank1) launch_add(m->dX + (int64_t)(T - 1) * D, dYr(0), N, D, (int64_t)T * D, D, s);
   if (NL > 1) {
     // dX is the gradient w.r.t. the top layer's input: down through the lower

@@ -417,7 +417,7 @@ bool launch_gemm(const GemmArgs& g0, float* ws, int64_t ws_cap, hipStream_t s) {
 
 void launch_gemm2(const GemmArgs& g, const GemmArgs& g2, float* ws, int64_t ws_cap, hipStream_t s) {
   if (g.M <= 0 || g.N <= 0) return;
-  if (launch_bgemm(g, &g2, ws, ws_cap, s)) return;  // (no operand of these products is stored as bf16)
+  if (launch_bgemm(g, &g2, ws, ws_cap, s)) return;
   launch_gemm(g, ws, ws_cap, s);
   GemmArgs h = g2;
   h.C = g.C;

@@ -159,6 +159,22 @@ __global__ __launch_bounds__(256) void k_refresh(RefreshArgs a) {
   typedef Mma<BF> M;
   if (jb.kind == RJ_CVT) {
     if (i < jb.K) reinterpret_cast<typename M::T*>(jb.dst)[i] = M::cvt(jb.src[i]);
+  } else if (jb.kind == RJ_CVT8) {
+    if (i < jb.K / 8) {
+      const float4 x = reinterpret_cast<const float4*>(jb.src)[2 * i];
+      const float4 y = reinterpret_cast<const float4*>(jb.src)[2 * i + 1];
+      const float v[8] = {x.x, x.y, x.z, x.w, y.x, y.y, y.z, y.w};
+      union { uint4 u; typename M::T t[8]; } r;
+      static_assert(BF ? sizeof(r.t) == 16 : true, "eight bf16 values per 16 bytes");
+      if constexpr (BF) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) r.t[j] = M::cvt(v[j]);
+        reinterpret_cast<uint4*>(jb.dst)[i] = r.u;
+      } else {
+        reinterpret_cast<float4*>(jb.dst)[2 * i] = x;
+        reinterpret_cast<float4*>(jb.dst)[2 * i + 1] = y;
+      }
+    }
   } else if (jb.kind == RJ_PACK || jb.kind == RJ_PACKT) {
     refresh_pack<BF>(jb, i);
   } else if (jb.kind == RJ_PTAB) {
@@ -180,6 +196,9 @@ bool launch_refresh(bool bf, const RefreshJob* jobs, int n, hipStream_t s) {
     int64_t nb = 0;
     if (jb.kind == RJ_CVT || jb.kind == RJ_ZERO) {
       nb = ((int64_t)jb.K + 255) / 256;
+    } else if (jb.kind == RJ_CVT8) {
+      if (jb.K % 8 != 0 || ((uintptr_t)jb.src & 15) != 0 || ((uintptr_t)jb.dst & 15) != 0) return false;
+      nb = ((int64_t)jb.K / 8 + 255) / 256;
     } else if (jb.kind == RJ_PACK || jb.kind == RJ_PACKT) {
       const int KS = bf ? 32 : 16;
       if (jb.K % KS != 0 || jb.N % 16 != 0) return false;

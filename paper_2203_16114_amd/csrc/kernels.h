@@ -69,7 +69,8 @@ void launch_step_ce(const float* bits, int32_t n_streams, int32_t n_steps, doubl
 //            values of P (src; zero if use_pos is 0) and of W_q (src2, W_k and W_v following it in the master)
 //   RJ_ZERO  K 32-bit words of dst cleared
 //   RJ_PACKT as RJ_PACK for the transpose of src: the copy of [K][N] src^T, src being [N][K] row-major
-enum { RJ_CVT = 0, RJ_PACK = 1, RJ_PTAB = 2, RJ_ZERO = 3, RJ_PACKT = 4 };
+//   RJ_CVT8  as RJ_CVT, eight values per thread (K a multiple of 8, src and dst 16-byte aligned)
+enum { RJ_CVT = 0, RJ_PACK = 1, RJ_PTAB = 2, RJ_ZERO = 3, RJ_PACKT = 4, RJ_CVT8 = 5 };
 struct RefreshJob {
   const float* src;
   const float* src2;
@@ -77,7 +78,7 @@ struct RefreshJob {
   int kind, K, N, use_pos;
   float scale;
 };
-constexpr int REFRESH_MAX_JOBS = 12;
+constexpr int REFRESH_MAX_JOBS = 13;
 // Runs jobs[0..n) on stream s; false (nothing launched) for an unsupported job.
 bool launch_refresh(bool bf, const RefreshJob* jobs, int n, hipStream_t s);
 
