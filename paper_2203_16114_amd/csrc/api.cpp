@@ -150,6 +150,7 @@ int64_t adapt_gemm_ws(const trace_model* m, int64_t N) {
   int64_t w = 0;
   for (auto& s : adapt_gemm_shapes(m, N))
     w = std::max(w, std::max(gemm_ws_floats(s[0], s[1], s[2]), bgemm_ws_floats(s[0], s[1], s[2])));
+  if (m->bf) w = std::max(w, kv_wgrad_ws_floats(N, m->L.D));
   return w;
 }
 
@@ -929,8 +930,12 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // G^T dZ as GEMMs on the byte-embedding part G, then P^T (sum over windows of
   // dZ) for the positional part
   if (NL == 1) {
-    ok = kv_grad(m->Xk, 1, D, hf, false, gr + L.at(P_WK, top)) && ok;
-    ok = kv_grad(m->Xk, 1, D, hf, true, gr + L.at(P_WV, top)) && ok;
+    // rank1: both from the per-window sums over the tokens (one launch)
+    if (!(rank1 && launch_kv_wgrad((const uint16_t*)m->Xk, m->dSc, m->kA, m->kq, m->dO, N, T, D, H, ascale, ws2,
+                                   m->gws_cap, gr + L.at(P_WK, top), gr + L.at(P_WV, top), w))) {
+      ok = kv_grad(m->Xk, 1, D, hf, false, gr + L.at(P_WK, top)) && ok;
+      ok = kv_grad(m->Xk, 1, D, hf, true, gr + L.at(P_WV, top)) && ok;
+    }
     // side: dWq = X_last^T dQ; Xk was written on this stream, dQ before the last mark
     GemmArgs gq = gemm(D, D, N, at(m->Xk, (int64_t)(T - 1) * D), 1, (int64_t)T * D, rb, m->dQ, D, 1, 0,
                        gr + L.at(P_WQ, top), D, 0.f);

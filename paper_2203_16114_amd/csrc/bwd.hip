@@ -1059,6 +1059,278 @@ bool launch_dx_rank1(const float* q, const float* dO, const float* dS, const flo
   return false;
 }
 
+// Weight gradients of the key and value projections (bf16 models, the rank-one
+// rows of the last query row): with the token rows X[n][t] (byte-embedding part)
+// and, per window n and head h,
+//   ZK_h[n] = sum_t dS[n][h][t] X[n][t],   ZV_h[n] = sum_t A[n][h][t] X[n][t],
+// the head-h columns of the gradients are
+//   dWk[:, h] = sum_n ZK_h[n]^T (scale q_h[n]),   dWv[:, h] = sum_n ZV_h[n]^T bf(dO_h[n]),
+// the same sums as X^T dK and X^T dV over every token row with T times fewer
+// products.  Block: 32 rows d of the key or the value gradient for every head
+// (wave h: head h) over one range of windows, in tiles of 32 windows (one
+// k-step of v_mfma_f32_16x16x32_bf16).  X (as fp32) and the coefficients of
+// the next tile are staged in LDS while the current one is used; each wave
+// forms its head's Z on the vector ALUs and splits it into bf16 hi + lo; the B
+// operand is q as hi + lo (three products per fragment pair; the scale applied
+// to the sums) or bf(dO), exact (two).  Fragment row m of d-fragment f is
+// d = d0 + 2 m + f, column c of j-fragment jf is j = h DH + NJF c + jf, so a
+// lane's pair of X values and its NJF values of q or dO are contiguous.  Partial sums of the window range z go
+// to part[kv][z][d][j] (kv 0: key, 1: value), summed by the split-K reduce.
+constexpr int KVW_DC = 32, KVW_NT = 32;
+
+template <int T, int H>
+struct KvwLds {
+  static constexpr int XBUF = (KVW_NT * T + 4) * KVW_DC;  // token rows + one row of padding per 8 windows
+  static constexpr int CW = KVW_NT * H * T;               // coefficients of one tile
+  float xs[2][XBUF];
+  float cs[2][CW];
+};
+
+template <int T, int DH, int H, bool VAL>
+__device__ __forceinline__ void kv_wgrad_body(KvwLds<T, H>& sm, const uint16_t* __restrict__ X,
+                                              const float* __restrict__ C, const float* __restrict__ V, int N,
+                                              int nps, float bscale, float* __restrict__ part, int d0, int z,
+                                              int S) {
+  constexpr int D = H * DH, NJF = DH / 16, NTH = 64 * H;
+  constexpr int XROW = KVW_DC;  // floats of one staged token row
+  constexpr int CW = KvwLds<T, H>::CW;
+  auto& xs = sm.xs;
+  auto& cs = sm.cs;
+  constexpr int XU = KVW_NT * T * (KVW_DC / 8);  // 16-byte units of X per tile
+  constexpr int XPT = XU / NTH, CPT = (CW / 4 + NTH - 1) / NTH;  // (T = 4: half the threads)
+  static_assert(XU % NTH == 0 && ((CW / 4) % NTH == 0 || CW / 4 < NTH), "staging split");
+  static_assert(NJF == 2 || NJF == 4, "head width");
+  const int h = threadIdx.x >> 6, l = threadIdx.x & 63, g = l >> 4, m = l & 15;
+  const int nb = z * nps, ne = min(N, nb + nps);
+  const int ntiles = (ne - nb + KVW_NT - 1) / KVW_NT;
+
+  uint4 xr[XPT];
+  float4 cr[CPT];
+  // loads of tile k: X units (row r = n T + t, 8 values p) from clamped rows,
+  // coefficients of windows past the range as zero (32-bit element offsets:
+  // N T D < 2^30)
+  auto load = [&](int k) {
+    const int n0 = nb + k * KVW_NT;
+#pragma unroll
+    for (int i = 0; i < XPT; ++i) {
+      const int u = threadIdx.x + i * NTH, r = u >> 2, p = u & 3;
+      const int n = min(n0 + r / T, N - 1), t = r % T;
+      xr[i] = *reinterpret_cast<const uint4*>(X + ((uint32_t)(n * T + t) * D + d0 + 8 * p));
+    }
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int e = 4 * min((int)threadIdx.x + i * NTH, CW / 4 - 1), n = n0 + e / (H * T);
+      const float4 v = *reinterpret_cast<const float4*>(C + ((uint32_t)min(n, N - 1) * (H * T) + e % (H * T)));
+      cr[i] = n < ne ? v : make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+  };
+  auto put = [&](int b) {
+#pragma unroll
+    for (int i = 0; i < XPT; ++i) {
+      const int u = threadIdx.x + i * NTH, r = u >> 2, p = u & 3;
+      float* dst = &xs[b][(r + (r / T >> 3)) * XROW + 8 * p];
+      const uint32_t w[4] = {xr[i].x, xr[i].y, xr[i].z, xr[i].w};
+      *reinterpret_cast<float4*>(dst) = make_float4(__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xffff0000u),
+                                                    __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xffff0000u));
+      *reinterpret_cast<float4*>(dst + 4) = make_float4(__uint_as_float(w[2] << 16), __uint_as_float(w[2] & 0xffff0000u),
+                                                        __uint_as_float(w[3] << 16), __uint_as_float(w[3] & 0xffff0000u));
+    }
+#pragma unroll
+    for (int i = 0; i < CPT; ++i)
+      if (threadIdx.x + i * NTH < CW / 4) *reinterpret_cast<float4*>(&cs[b][4 * (threadIdx.x + i * NTH)]) = cr[i];
+  };
+
+  // this lane's B values of tile k: windows nb + 32 k + 8 g + i, columns
+  // h DH + NJF m + jf, from clamped rows (32-bit element offsets: N D < 2^29).
+  // Windows past the range need no mask: their coefficients, so their Z, are 0.
+  auto loadB = [&](float (&bv)[8][NJF], int k) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const uint32_t o = (uint32_t)min(nb + k * KVW_NT + 8 * g + i, N - 1) * D + h * DH + NJF * m;
+      if constexpr (NJF == 4) {
+        const float4 a = *reinterpret_cast<const float4*>(V + o);
+        bv[i][0] = a.x; bv[i][1] = a.y; bv[i][2] = a.z; bv[i][3] = a.w;
+      } else {
+        const float2 a = *reinterpret_cast<const float2*>(V + o);
+        bv[i][0] = a.x; bv[i][1] = a.y;
+      }
+    }
+  };
+
+  f32x4 acc[2][NJF];
+#pragma unroll
+  for (int f = 0; f < 2; ++f)
+#pragma unroll
+    for (int jf = 0; jf < NJF; ++jf) acc[f][jf] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  float bv[8][NJF];
+  if (ntiles > 0) {
+    load(0);
+    loadB(bv, 0);
+    put(0);
+  }
+  __syncthreads();
+#pragma unroll 1
+  for (int k = 0; k < ntiles; ++k) {
+    const int b = k & 1;
+    if (k + 1 < ntiles) load(k + 1);
+    // the next tile's B values, one tile ahead (clamped rows past the last)
+    float bn[8][NJF];
+    loadB(bn, k + 1);
+    // Z of this head for rows d0 + 2 m + f, windows 8 g + i, packed by pairs of
+    // windows (word ip: windows 2 ip, 2 ip + 1)
+    // (window 8 g + i: X rows (8 g + i) T + t plus g rows of padding,
+    // coefficients at ((8 g + i) H + h) T; one base address each, the rest
+    // constant offsets)
+    const float* xb = &xs[b][(8 * g * T + g) * XROW + 2 * m];
+    const float* cb = &cs[b][(8 * g * H + h) * T];
+    // LDS values of pair ip: X (two values per token) and coefficients; the
+    // next pair's reads are issued before this pair's sums (two pairs in
+    // flight at most: issued all at once, they spill)
+    float2 xv[2][2][T];
+    float cv[2][2][T];
+    auto rd = [&](int ip, int sl) {
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        const int i = 2 * ip + e;
+        const float* cn = cb + i * H * T;
+#pragma unroll
+        for (int t = 0; t < T; t += 4) {
+          const float4 a = *reinterpret_cast<const float4*>(cn + t);
+          cv[sl][e][t] = a.x; cv[sl][e][t + 1] = a.y; cv[sl][e][t + 2] = a.z; cv[sl][e][t + 3] = a.w;
+        }
+#pragma unroll
+        for (int t = 0; t < T; ++t) xv[sl][e][t] = *reinterpret_cast<const float2*>(xb + (i * T + t) * XROW);
+      }
+    };
+    uint32_t zh[2][4], zl[2][4];
+    rd(0, 0);
+#pragma unroll
+    for (int ip = 0; ip < 4; ++ip) {
+      __builtin_amdgcn_sched_barrier(0);
+      if (ip + 1 < 4) rd(ip + 1, (ip + 1) & 1);
+      const int sl = ip & 1;
+      float zz[2][2];
+#pragma unroll
+      for (int e = 0; e < 2; ++e) {
+        float a0 = 0.f, a1 = 0.f;
+#pragma unroll
+        for (int t = 0; t < T; ++t) {
+          a0 = fmaf(cv[sl][e][t], xv[sl][e][t].x, a0);
+          a1 = fmaf(cv[sl][e][t], xv[sl][e][t].y, a1);
+        }
+        zz[0][e] = a0; zz[1][e] = a1;
+      }
+#pragma unroll
+      for (int f = 0; f < 2; ++f) {
+        const uint32_t hw = pack_bf16x2(zz[f][0], zz[f][1]);
+        zh[f][ip] = hw;
+        zl[f][ip] = pack_bf16x2(zz[f][0] - __uint_as_float(hw << 16), zz[f][1] - __uint_as_float(hw & 0xffff0000u));
+      }
+    }
+    auto u4 = [](const uint32_t (&w)[4]) { return make_uint4(w[0], w[1], w[2], w[3]); };
+#pragma unroll
+    for (int jf = 0; jf < NJF; ++jf) {
+      // B fragment: V as bf16 hi + lo (hi alone is bf(dO) for the value)
+      uint32_t bh[4], bl[4];
+#pragma unroll
+      for (int ip = 0; ip < 4; ++ip) {
+        const float a = bv[2 * ip][jf], c = bv[2 * ip + 1][jf];
+        bh[ip] = pack_bf16x2(a, c);
+        if constexpr (!VAL)
+          bl[ip] = pack_bf16x2(a - __uint_as_float(bh[ip] << 16), c - __uint_as_float(bh[ip] & 0xffff0000u));
+      }
+#pragma unroll
+      for (int f = 0; f < 2; ++f) {
+        Mma<true>::run(acc[f][jf], u4(zh[f]), u4(bh));
+        Mma<true>::run(acc[f][jf], u4(zl[f]), u4(bh));
+        if constexpr (!VAL) Mma<true>::run(acc[f][jf], u4(zh[f]), u4(bl));
+      }
+    }
+    if (k + 1 < ntiles) put(b ^ 1);
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+#pragma unroll
+      for (int jf = 0; jf < NJF; ++jf) bv[i][jf] = bn[i][jf];
+    __syncthreads();
+  }
+  // lane holds rows 4 g + r of column m: d = d0 + 2 (4 g + r) + f, j = h DH + NJF m + jf
+  const int64_t DD = (int64_t)D * D;
+  float* p = part + ((int64_t)(VAL ? 1 : 0) * S + z) * DD;
+#pragma unroll
+  for (int f = 0; f < 2; ++f)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t o = (int64_t)(d0 + 2 * (4 * g + r) + f) * D + h * DH + NJF * m;
+      if constexpr (NJF == 4)
+        *reinterpret_cast<float4*>(p + o) = make_float4(acc[f][0][r] * bscale, acc[f][1][r] * bscale,
+                                                        acc[f][2][r] * bscale, acc[f][3][r] * bscale);
+      else
+        *reinterpret_cast<float2*>(p + o) = make_float2(acc[f][0][r] * bscale, acc[f][1][r] * bscale);
+    }
+}
+
+template <int T, int DH, int H>
+__global__ __launch_bounds__(64 * H) void k_kv_wgrad(const uint16_t* __restrict__ X, const float* __restrict__ dS,
+                                                     const float* __restrict__ Ac, const float* __restrict__ q,
+                                                     const float* __restrict__ dO, int N, int nps, float scale,
+                                                     float* __restrict__ part) {
+  __shared__ __align__(16) KvwLds<T, H> sm;
+  // blocks are dealt to the 8 XCDs in turn (block L on XCD L % 8): logical
+  // block lam = (L % 8) per + L / 8 gives each XCD a contiguous run of them,
+  // i.e. whole window ranges (their D / 32 row groups, key then value), so
+  // the ranges' rows of q, dO and X are fetched into that XCD's L2 once
+  constexpr int ND = H * DH / KVW_DC;
+  const int tot = (int)gridDim.x, per = tot / 8, L = (int)blockIdx.x;
+  const int lam = L < 8 * per ? (L % 8) * per + L / 8 : L;
+  const int x = lam % ND, kv = (lam / ND) & 1, z = lam / (2 * ND), S = tot / (2 * ND);
+  if (kv == 0)
+    kv_wgrad_body<T, DH, H, false>(sm, X, dS, q, N, nps, scale, part, x * KVW_DC, z, S);
+  else
+    kv_wgrad_body<T, DH, H, true>(sm, X, Ac, dO, N, nps, 1.f, part, x * KVW_DC, z, S);
+}
+
+// windows per range (a multiple of the tile) and number of ranges: about 256
+// blocks of D / 32 row groups
+static void kv_wgrad_split(int64_t N, int D, int& nps, int& S) {
+  const int64_t tiles = (N + KVW_NT - 1) / KVW_NT;
+  const int64_t want = std::max<int64_t>(1, std::min<int64_t>(tiles, (256 + D / KVW_DC - 1) / (D / KVW_DC)));
+  nps = (int)((tiles + want - 1) / want) * KVW_NT;
+  S = (int)((N + nps - 1) / nps);
+}
+
+int64_t kv_wgrad_ws_floats(int64_t N, int D) {
+  if (N <= 0) return 0;
+  int nps, S;
+  kv_wgrad_split(N, D, nps, S);
+  return (int64_t)2 * S * D * D;
+}
+
+bool kv_wgrad_built(int T, int D, int H) { return dx_rank1_built(T, D, H) && H <= 8; }
+
+bool launch_kv_wgrad(const uint16_t* X, const float* dS, const float* A, const float* q, const float* dO, int64_t N,
+                     int T, int D, int H, float scale, float* ws, int64_t ws_cap, float* dWk, float* dWv,
+                     hipStream_t s) {
+  // 32-bit element offsets in the kernel
+  if (N <= 0 || N * D >= ((int64_t)1 << 29) || N * T * D >= ((int64_t)1 << 30) || !kv_wgrad_built(T, D, H)) return false;
+  if (kv_wgrad_ws_floats(N, D) > ws_cap) return false;
+  if (((uintptr_t)X | (uintptr_t)dS | (uintptr_t)A | (uintptr_t)q | (uintptr_t)dO | (uintptr_t)ws) & 15) return false;
+  int nps, S;
+  kv_wgrad_split(N, D, nps, S);
+  const int DH = D / H;
+  const dim3 grid((unsigned)(2 * S * (D / KVW_DC)));
+#define TRACE_KVW(T_, DH_, H_)                                                                              \
+  if (T == T_ && DH == DH_ && H == H_)                                                                      \
+    hipLaunchKernelGGL((k_kv_wgrad<T_, DH_, H_>), grid, dim3(64 * H_), 0, s, X, dS, A, q, dO, (int)N, nps, scale, ws);
+  TRACE_KVW(4, 32, 4) TRACE_KVW(8, 32, 4) TRACE_KVW(4, 64, 2) TRACE_KVW(8, 64, 2)
+  TRACE_KVW(4, 32, 8) TRACE_KVW(8, 32, 8) TRACE_KVW(4, 64, 4) TRACE_KVW(8, 64, 4)
+  TRACE_KVW(4, 64, 8) TRACE_KVW(8, 64, 8)
+#undef TRACE_KVW
+  launch_splitk_reduce(ws, S, D, D, dWk, D, 0.f, nullptr, s);
+  launch_splitk_reduce(ws + (int64_t)S * D * D, S, D, D, dWv, D, 0.f, nullptr, s);
+  return true;
+}
+
 // dP[t][c] = sum_j sK[t][j] Wk[c][j] + sV[t][j] Wv[c][j], plus, for t = T-1,
 // sQ[j] Wq[c][j] + sY[c]: the positional table's gradient sum_n dX[n][t], with
 // the sums over windows taken before the products (weights as the operand
