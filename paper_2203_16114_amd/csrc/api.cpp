@@ -150,7 +150,7 @@ int64_t adapt_gemm_ws(const trace_model* m, int64_t N) {
   int64_t w = 0;
   for (auto& s : adapt_gemm_shapes(m, N))
     w = std::max(w, std::max(gemm_ws_floats(s[0], s[1], s[2]), bgemm_ws_floats(s[0], s[1], s[2])));
-  if (m->bf) w = std::max(w, kv_wgrad_ws_floats(N, m->L.D));
+  if (m->bf) w = std::max(w, kv_wgrad_ws_floats(N, m->L.T, m->L.D, m->cfg.H));
   return w;
 }
 

@@ -1066,95 +1066,111 @@ bool launch_dx_rank1(const float* q, const float* dO, const float* dS, const flo
 // the head-h columns of the gradients are
 //   dWk[:, h] = sum_n ZK_h[n]^T (scale q_h[n]),   dWv[:, h] = sum_n ZV_h[n]^T bf(dO_h[n]),
 // the same sums as X^T dK and X^T dV over every token row with T times fewer
-// products.  Block: 32 rows d of the key or the value gradient for every head
-// (wave h: head h) over one range of windows, in tiles of 32 windows (one
-// k-step of v_mfma_f32_16x16x32_bf16).  X (as fp32) and the coefficients of
-// the next tile are staged in LDS while the current one is used; each wave
-// forms its head's Z on the vector ALUs and splits it into bf16 hi + lo; the B
-// operand is q as hi + lo (three products per fragment pair; the scale applied
-// to the sums) or bf(dO), exact (two).  Fragment row m of d-fragment f is
-// d = d0 + 2 m + f, column c of j-fragment jf is j = h DH + NJF c + jf, so a
-// lane's pair of X values and its NJF values of q or dO are contiguous.  Partial sums of the window range z go
-// to part[kv][z][d][j] (kv 0: key, 1: value), summed by the split-K reduce.
+// products.  Block: 32 rows d of the key or the value gradient over one range
+// of windows, in tiles of 32 windows; H waves.  Per tile, both products run on
+// v_mfma_f32_16x16x32_bf16:
+//  1. Z^T = X^T Cbd: rows d, k = (window w, token t) over 32 / T windows per
+//     k-step, columns (w', h) of 16 / H windows; Cbd(w t, w' h) = C[w][h][t]
+//     where w = w', 0 elsewhere (block diagonal, C = dS or A as bf16 hi + lo,
+//     packed as fragments by k_kv_pack).
+//     X is staged in LDS transposed (rows d, k contiguous), so that a lane's
+//     A fragment is one 16-byte read; the k-steps are dealt to the waves.  Z
+//     goes to LDS as fp32, rows (h, d) of the tile's 32 windows.
+//  2. wave h: dW[d][h DH + j] += sum_w Z_h[w][d] B[w][j], Z as bf16 hi + lo,
+//     B = q as hi + lo (three products; the scale applied to the sums) or
+//     bf(dO), exact (two), packed as fragments by k_kv_pack.  Fragment row m of d-fragment f is d = 16 f + m,
+//     column c of j-fragment jf is j = h DH + NJF c + jf, so a lane's NJF
+//     values of q or dO are contiguous.
+// Windows past the range have zero coefficients, so zero Z (their rows are read
+// clamped).  Partial sums of the window range z go to part[kv][z][d][j]
+// (kv 0: key, 1: value), summed by the split-K reduce.
 constexpr int KVW_DC = 32, KVW_NT = 32;
 
 template <int T, int H>
 struct KvwLds {
-  static constexpr int XBUF = (KVW_NT * T + 4) * KVW_DC;  // token rows + one row of padding per 8 windows
-  static constexpr int CW = KVW_NT * H * T;               // coefficients of one tile
-  float xs[2][XBUF];
-  float cs[2][CW];
+  static constexpr int XR = KVW_NT * T + 8;   // bf16 per staged row d (k = w T + t) + 16 bytes of padding
+  static constexpr int ZR = KVW_NT + 4;       // floats per Z row (h, d) + padding
+  static constexpr int ZH = KVW_DC * ZR + 4;  // floats per head + padding
+  uint16_t xt[2][KVW_DC * XR];
+  float zs[H * ZH];
 };
+
+// bf16 hi + lo of eight values
+__device__ __forceinline__ void kvw_split8(const float (&v)[8], uint4& hi, uint4& lo) {
+  uint32_t a[4], b[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    a[i] = pack_bf16x2(v[2 * i], v[2 * i + 1]);
+    b[i] = pack_bf16x2(v[2 * i] - __uint_as_float(a[i] << 16), v[2 * i + 1] - __uint_as_float(a[i] & 0xffff0000u));
+  }
+  hi = make_uint4(a[0], a[1], a[2], a[3]);
+  lo = make_uint4(b[0], b[1], b[2], b[3]);
+}
 
 template <int T, int DH, int H, bool VAL>
 __device__ __forceinline__ void kv_wgrad_body(KvwLds<T, H>& sm, const uint16_t* __restrict__ X,
-                                              const float* __restrict__ C, const float* __restrict__ V, int N,
+                                              const uint4* __restrict__ Cp, const uint4* __restrict__ Bp, int N,
                                               int nps, float bscale, float* __restrict__ part, int d0, int z,
                                               int S) {
   constexpr int D = H * DH, NJF = DH / 16, NTH = 64 * H;
-  constexpr int XROW = KVW_DC;  // floats of one staged token row
-  constexpr int CW = KvwLds<T, H>::CW;
-  auto& xs = sm.xs;
-  auto& cs = sm.cs;
-  constexpr int XU = KVW_NT * T * (KVW_DC / 8);  // 16-byte units of X per tile
-  constexpr int XPT = XU / NTH, CPT = (CW / 4 + NTH - 1) / NTH;  // (T = 4: half the threads)
-  static_assert(XU % NTH == 0 && ((CW / 4) % NTH == 0 || CW / 4 < NTH), "staging split");
+  constexpr int XR = KvwLds<T, H>::XR, ZR = KvwLds<T, H>::ZR, ZH = KvwLds<T, H>::ZH;
+  constexpr int NKS = KVW_NT * T / 32;  // k-steps of the first product per tile
+  constexpr int WPC = 16 / H;           // windows per column block of Z^T
+  constexpr int NCB = 32 / T / WPC;     // column blocks per k-step
+  constexpr int NSU = KVW_NT * T / 8 * (KVW_DC / 8);  // staging units (8 k x 8 d)
   static_assert(NJF == 2 || NJF == 4, "head width");
+  static_assert(NCB >= 1 && NSU <= NTH, "tile shape");
   const int h = threadIdx.x >> 6, l = threadIdx.x & 63, g = l >> 4, m = l & 15;
   const int nb = z * nps, ne = min(N, nb + nps);
   const int ntiles = (ne - nb + KVW_NT - 1) / KVW_NT;
+  const bool stager = threadIdx.x < NSU;
+  const int so = threadIdx.x >> 2, sp = threadIdx.x & 3;  // staging unit: k-octet so, d-octet sp
 
-  uint4 xr[XPT];
-  float4 cr[CPT];
-  // loads of tile k: X units (row r = n T + t, 8 values p) from clamped rows,
-  // coefficients of windows past the range as zero (32-bit element offsets:
-  // N T D < 2^30)
+  // X of tile k, unit (so, sp): rows k = 8 so + i of d0 + 8 sp .. + 7, clamped
+  // (32-bit element offsets: N T D < 2^30)
+  uint4 xr[8];
   auto load = [&](int k) {
+    if (!stager) return;
     const int n0 = nb + k * KVW_NT;
 #pragma unroll
-    for (int i = 0; i < XPT; ++i) {
-      const int u = threadIdx.x + i * NTH, r = u >> 2, p = u & 3;
-      const int n = min(n0 + r / T, N - 1), t = r % T;
-      xr[i] = *reinterpret_cast<const uint4*>(X + ((uint32_t)(n * T + t) * D + d0 + 8 * p));
-    }
-#pragma unroll
-    for (int i = 0; i < CPT; ++i) {
-      const int e = 4 * min((int)threadIdx.x + i * NTH, CW / 4 - 1), n = n0 + e / (H * T);
-      const float4 v = *reinterpret_cast<const float4*>(C + ((uint32_t)min(n, N - 1) * (H * T) + e % (H * T)));
-      cr[i] = n < ne ? v : make_float4(0.f, 0.f, 0.f, 0.f);
-    }
-  };
-  auto put = [&](int b) {
-#pragma unroll
-    for (int i = 0; i < XPT; ++i) {
-      const int u = threadIdx.x + i * NTH, r = u >> 2, p = u & 3;
-      float* dst = &xs[b][(r + (r / T >> 3)) * XROW + 8 * p];
-      const uint32_t w[4] = {xr[i].x, xr[i].y, xr[i].z, xr[i].w};
-      *reinterpret_cast<float4*>(dst) = make_float4(__uint_as_float(w[0] << 16), __uint_as_float(w[0] & 0xffff0000u),
-                                                    __uint_as_float(w[1] << 16), __uint_as_float(w[1] & 0xffff0000u));
-      *reinterpret_cast<float4*>(dst + 4) = make_float4(__uint_as_float(w[2] << 16), __uint_as_float(w[2] & 0xffff0000u),
-                                                        __uint_as_float(w[3] << 16), __uint_as_float(w[3] & 0xffff0000u));
-    }
-#pragma unroll
-    for (int i = 0; i < CPT; ++i)
-      if (threadIdx.x + i * NTH < CW / 4) *reinterpret_cast<float4*>(&cs[b][4 * (threadIdx.x + i * NTH)]) = cr[i];
-  };
-
-  // this lane's B values of tile k: windows nb + 32 k + 8 g + i, columns
-  // h DH + NJF m + jf, from clamped rows (32-bit element offsets: N D < 2^29).
-  // Windows past the range need no mask: their coefficients, so their Z, are 0.
-  auto loadB = [&](float (&bv)[8][NJF], int k) {
-#pragma unroll
     for (int i = 0; i < 8; ++i) {
-      const uint32_t o = (uint32_t)min(nb + k * KVW_NT + 8 * g + i, N - 1) * D + h * DH + NJF * m;
-      if constexpr (NJF == 4) {
-        const float4 a = *reinterpret_cast<const float4*>(V + o);
-        bv[i][0] = a.x; bv[i][1] = a.y; bv[i][2] = a.z; bv[i][3] = a.w;
-      } else {
-        const float2 a = *reinterpret_cast<const float2*>(V + o);
-        bv[i][0] = a.x; bv[i][1] = a.y;
-      }
+      const int kk = 8 * so + i, n = min(n0 + kk / T, N - 1), t = kk % T;
+      xr[i] = *reinterpret_cast<const uint4*>(X + ((uint32_t)(n * T + t) * D + d0 + 8 * sp));
     }
+  };
+  // transposed: row d = 8 sp + e holds k = 8 so .. + 7 (one 16-byte write)
+  auto put = [&](int b) {
+    if (!stager) return;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      uint32_t w[4];
+#pragma unroll
+      for (int a = 0; a < 4; ++a) {
+        const uint32_t lo = (&xr[2 * a].x)[e >> 1], hi = (&xr[2 * a + 1].x)[e >> 1];
+        w[a] = (e & 1) ? ((lo >> 16) | (hi & 0xffff0000u)) : ((lo & 0xffffu) | (hi << 16));
+      }
+      *reinterpret_cast<uint4*>(&sm.xt[b][(8 * sp + e) * XR + 8 * so]) = make_uint4(w[0], w[1], w[2], w[3]);
+    }
+  };
+  // packed fragments of tile k (k_kv_pack): the first product's B (Cbd, hi and
+  // lo) for this wave's k-steps, the second product's B (V: hi and lo for the
+  // key, hi for the value)
+  constexpr int NSI = (NKS + H - 1) / H, NBS = VAL ? 1 : 2;
+  const int tile0 = nb / KVW_NT;
+  auto loadF = [&](uint4 (&cf)[NSI][NCB][2], uint4 (&bf)[NJF][NBS], int k) {
+    const int64_t tl = tile0 + k;
+#pragma unroll
+    for (int si = 0; si < NSI; ++si) {
+      const int ks = min(h + si * H, NKS - 1);
+#pragma unroll
+      for (int cb = 0; cb < NCB; ++cb)
+#pragma unroll
+        for (int e = 0; e < 2; ++e) cf[si][cb][e] = Cp[(((tl * NKS + ks) * NCB + cb) * 2 + e) * 64 + l];
+    }
+#pragma unroll
+    for (int jf = 0; jf < NJF; ++jf)
+#pragma unroll
+      for (int e = 0; e < NBS; ++e) bf[jf][e] = Bp[(((tl * H + h) * NJF + jf) * NBS + e) * 64 + l];
   };
 
   f32x4 acc[2][NJF];
@@ -1163,105 +1179,82 @@ __device__ __forceinline__ void kv_wgrad_body(KvwLds<T, H>& sm, const uint16_t* 
 #pragma unroll
     for (int jf = 0; jf < NJF; ++jf) acc[f][jf] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  float bv[8][NJF];
+  uint4 cf[NSI][NCB][2], bf[NJF][NBS];
   if (ntiles > 0) {
     load(0);
-    loadB(bv, 0);
+    loadF(cf, bf, 0);
     put(0);
   }
   __syncthreads();
 #pragma unroll 1
   for (int k = 0; k < ntiles; ++k) {
     const int b = k & 1;
+    // the next tile's fragments (clamped past the last tile: the pack has
+    // every tile of the product)
     if (k + 1 < ntiles) load(k + 1);
-    // the next tile's B values, one tile ahead (clamped rows past the last)
-    float bn[8][NJF];
-    loadB(bn, k + 1);
-    // Z of this head for rows d0 + 2 m + f, windows 8 g + i, packed by pairs of
-    // windows (word ip: windows 2 ip, 2 ip + 1)
-    // (window 8 g + i: X rows (8 g + i) T + t plus g rows of padding,
-    // coefficients at ((8 g + i) H + h) T; one base address each, the rest
-    // constant offsets)
-    const float* xb = &xs[b][(8 * g * T + g) * XROW + 2 * m];
-    const float* cb = &cs[b][(8 * g * H + h) * T];
-    // LDS values of pair ip: X (two values per token) and coefficients; the
-    // next pair's reads are issued before this pair's sums (two pairs in
-    // flight at most: issued all at once, they spill)
-    float2 xv[2][2][T];
-    float cv[2][2][T];
-    auto rd = [&](int ip, int sl) {
+    uint4 cn[NSI][NCB][2], bn[NJF][NBS];
+    loadF(cn, bn, min(k + 1, ntiles - 1));
+    // first product, k-steps ks = wave, wave + H, ..
 #pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const int i = 2 * ip + e;
-        const float* cn = cb + i * H * T;
+    for (int si = 0; si < NSI; ++si) {
+      const int ks = h + si * H;
+      if (ks < NKS) {
 #pragma unroll
-        for (int t = 0; t < T; t += 4) {
-          const float4 a = *reinterpret_cast<const float4*>(cn + t);
-          cv[sl][e][t] = a.x; cv[sl][e][t + 1] = a.y; cv[sl][e][t + 2] = a.z; cv[sl][e][t + 3] = a.w;
+        for (int f = 0; f < 2; ++f) {
+          const uint4 xa = *reinterpret_cast<const uint4*>(&sm.xt[b][(16 * f + m) * XR + 32 * ks + 8 * g]);
+#pragma unroll
+          for (int cb = 0; cb < NCB; ++cb) {
+            f32x4 o = f32x4{0.f, 0.f, 0.f, 0.f};
+            Mma<true>::run(o, xa, cf[si][cb][0]);
+            Mma<true>::run(o, xa, cf[si][cb][1]);
+            // o[r]: Z[w][hh][d = 16 f + 4 g + r], w = 32 ks / T + cb WPC + m / H (in the tile)
+            const int w = 32 * ks / T + cb * WPC + m / H, hh = m % H;
+#pragma unroll
+            for (int r = 0; r < 4; ++r) sm.zs[hh * ZH + (16 * f + 4 * g + r) * ZR + w] = o[r];
+          }
         }
-#pragma unroll
-        for (int t = 0; t < T; ++t) xv[sl][e][t] = *reinterpret_cast<const float2*>(xb + (i * T + t) * XROW);
-      }
-    };
-    uint32_t zh[2][4], zl[2][4];
-    rd(0, 0);
-#pragma unroll
-    for (int ip = 0; ip < 4; ++ip) {
-      __builtin_amdgcn_sched_barrier(0);
-      if (ip + 1 < 4) rd(ip + 1, (ip + 1) & 1);
-      const int sl = ip & 1;
-      float zz[2][2];
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        float a0 = 0.f, a1 = 0.f;
-#pragma unroll
-        for (int t = 0; t < T; ++t) {
-          a0 = fmaf(cv[sl][e][t], xv[sl][e][t].x, a0);
-          a1 = fmaf(cv[sl][e][t], xv[sl][e][t].y, a1);
-        }
-        zz[0][e] = a0; zz[1][e] = a1;
-      }
-#pragma unroll
-      for (int f = 0; f < 2; ++f) {
-        const uint32_t hw = pack_bf16x2(zz[f][0], zz[f][1]);
-        zh[f][ip] = hw;
-        zl[f][ip] = pack_bf16x2(zz[f][0] - __uint_as_float(hw << 16), zz[f][1] - __uint_as_float(hw & 0xffff0000u));
       }
     }
-    auto u4 = [](const uint32_t (&w)[4]) { return make_uint4(w[0], w[1], w[2], w[3]); };
+    __syncthreads();
+    // second product, wave h: Z_h rows 16 f + m, windows 8 g + j
+    uint4 zh[2], zl[2];
 #pragma unroll
-    for (int jf = 0; jf < NJF; ++jf) {
-      // B fragment: V as bf16 hi + lo (hi alone is bf(dO) for the value)
-      uint32_t bh[4], bl[4];
+    for (int f = 0; f < 2; ++f) {
+      const float* zp = &sm.zs[h * ZH + (16 * f + m) * ZR + 8 * g];
+      const float4 a = *reinterpret_cast<const float4*>(zp), c = *reinterpret_cast<const float4*>(zp + 4);
+      const float v[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
+      kvw_split8(v, zh[f], zl[f]);
+    }
 #pragma unroll
-      for (int ip = 0; ip < 4; ++ip) {
-        const float a = bv[2 * ip][jf], c = bv[2 * ip + 1][jf];
-        bh[ip] = pack_bf16x2(a, c);
-        if constexpr (!VAL)
-          bl[ip] = pack_bf16x2(a - __uint_as_float(bh[ip] << 16), c - __uint_as_float(bh[ip] & 0xffff0000u));
-      }
+    for (int jf = 0; jf < NJF; ++jf)
 #pragma unroll
       for (int f = 0; f < 2; ++f) {
-        Mma<true>::run(acc[f][jf], u4(zh[f]), u4(bh));
-        Mma<true>::run(acc[f][jf], u4(zl[f]), u4(bh));
-        if constexpr (!VAL) Mma<true>::run(acc[f][jf], u4(zh[f]), u4(bl));
+        Mma<true>::run(acc[f][jf], zh[f], bf[jf][0]);
+        Mma<true>::run(acc[f][jf], zl[f], bf[jf][0]);
+        if constexpr (!VAL) Mma<true>::run(acc[f][jf], zh[f], bf[jf][NBS - 1]);
       }
-    }
     if (k + 1 < ntiles) put(b ^ 1);
 #pragma unroll
-    for (int i = 0; i < 8; ++i)
+    for (int si = 0; si < NSI; ++si)
 #pragma unroll
-      for (int jf = 0; jf < NJF; ++jf) bv[i][jf] = bn[i][jf];
+      for (int cb = 0; cb < NCB; ++cb) {
+        cf[si][cb][0] = cn[si][cb][0];
+        cf[si][cb][1] = cn[si][cb][1];
+      }
+#pragma unroll
+    for (int jf = 0; jf < NJF; ++jf)
+#pragma unroll
+      for (int e = 0; e < NBS; ++e) bf[jf][e] = bn[jf][e];
     __syncthreads();
   }
-  // lane holds rows 4 g + r of column m: d = d0 + 2 (4 g + r) + f, j = h DH + NJF m + jf
+  // lane holds rows 4 g + r of column m: d = d0 + 16 f + 4 g + r, j = h DH + NJF m + jf
   const int64_t DD = (int64_t)D * D;
   float* p = part + ((int64_t)(VAL ? 1 : 0) * S + z) * DD;
 #pragma unroll
   for (int f = 0; f < 2; ++f)
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      const int64_t o = (int64_t)(d0 + 2 * (4 * g + r) + f) * D + h * DH + NJF * m;
+      const int64_t o = (int64_t)(d0 + 16 * f + 4 * g + r) * D + h * DH + NJF * m;
       if constexpr (NJF == 4)
         *reinterpret_cast<float4*>(p + o) = make_float4(acc[f][0][r] * bscale, acc[f][1][r] * bscale,
                                                         acc[f][2][r] * bscale, acc[f][3][r] * bscale);
@@ -1270,24 +1263,95 @@ __device__ __forceinline__ void kv_wgrad_body(KvwLds<T, H>& sm, const uint16_t* 
     }
 }
 
+// The B operands of both products as fragments, once per tile of 32 windows
+// (every row group of the gradients reads the same ones): block (tile, kv),
+// wave h.  Cp[tile][ks][cb][hi | lo][lane]: the first product's Cbd for k-step
+// ks and column block cb (C = dS for the key, A for the value; lane (g, m):
+// k = 32 ks + 8 g + j, column m); Bp[tile][h][jf][hi, lo | hi][lane]: scale-free
+// q as hi + lo, or bf(dO), at windows 8 g + j, column h DH + NJF m + jf.  Rows
+// past N are read clamped (their coefficients are zero).
 template <int T, int DH, int H>
-__global__ __launch_bounds__(64 * H) void k_kv_wgrad(const uint16_t* __restrict__ X, const float* __restrict__ dS,
-                                                     const float* __restrict__ Ac, const float* __restrict__ q,
-                                                     const float* __restrict__ dO, int N, int nps, float scale,
+__global__ __launch_bounds__(64 * H) void k_kv_pack(const float* __restrict__ dS, const float* __restrict__ Ac,
+                                                    const float* __restrict__ q, const float* __restrict__ dO, int N,
+                                                    uint4* __restrict__ Ck, uint4* __restrict__ Cv,
+                                                    uint4* __restrict__ Bq, uint4* __restrict__ Bd) {
+  constexpr int D = H * DH, NJF = DH / 16;
+  constexpr int NKS = KVW_NT * T / 32, WPC = 16 / H, NCB = 32 / T / WPC;
+  const int h = threadIdx.x >> 6, l = threadIdx.x & 63, g = l >> 4, m = l & 15;
+  const int64_t tl = blockIdx.x;
+  const int n0 = (int)tl * KVW_NT;
+  const bool val = blockIdx.y != 0;
+  const float* __restrict__ C = val ? Ac : dS;
+  uint4* __restrict__ Cp = val ? Cv : Ck;
+  for (int ks = h; ks < NKS; ks += H)
+#pragma unroll
+    for (int cb = 0; cb < NCB; ++cb) {
+      // lane's k = 32 ks + 8 g + j (window k / T, token k % T); column m:
+      // window 32 ks / T + cb WPC + m / H, head m % H
+      const int wcol = 32 * ks / T + cb * WPC + m / H, hh = m % H;
+      float v[8];
+#pragma unroll
+      for (int jq = 0; jq < 2; ++jq) {
+        const int k4 = 32 * ks + 8 * g + 4 * jq, w = k4 / T, t0 = k4 % T;
+        const float4 c = *reinterpret_cast<const float4*>(C + ((uint32_t)min(n0 + w, N - 1) * H + hh) * T + t0);
+        const bool on = w == wcol && n0 + w < N;
+        v[4 * jq] = on ? c.x : 0.f;
+        v[4 * jq + 1] = on ? c.y : 0.f;
+        v[4 * jq + 2] = on ? c.z : 0.f;
+        v[4 * jq + 3] = on ? c.w : 0.f;
+      }
+      uint4 hi, lo;
+      kvw_split8(v, hi, lo);
+      Cp[(((tl * NKS + ks) * NCB + cb) * 2) * 64 + l] = hi;
+      Cp[(((tl * NKS + ks) * NCB + cb) * 2 + 1) * 64 + l] = lo;
+    }
+  float bv[8][NJF];
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const uint32_t o = (uint32_t)min(n0 + 8 * g + j, N - 1) * D + h * DH + NJF * m;
+    const float* V = val ? dO : q;
+    if constexpr (NJF == 4) {
+      const float4 a = *reinterpret_cast<const float4*>(V + o);
+      bv[j][0] = a.x; bv[j][1] = a.y; bv[j][2] = a.z; bv[j][3] = a.w;
+    } else {
+      const float2 a = *reinterpret_cast<const float2*>(V + o);
+      bv[j][0] = a.x; bv[j][1] = a.y;
+    }
+  }
+#pragma unroll
+  for (int jf = 0; jf < NJF; ++jf) {
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = bv[j][jf];
+    uint4 hi, lo;
+    kvw_split8(v, hi, lo);
+    if (val) {
+      Bd[((tl * H + h) * NJF + jf) * 64 + l] = hi;
+    } else {
+      Bq[(((tl * H + h) * NJF + jf) * 2) * 64 + l] = hi;
+      Bq[(((tl * H + h) * NJF + jf) * 2 + 1) * 64 + l] = lo;
+    }
+  }
+}
+
+template <int T, int DH, int H>
+__global__ __launch_bounds__(64 * H) void k_kv_wgrad(const uint16_t* __restrict__ X, const uint4* __restrict__ Ck,
+                                                     const uint4* __restrict__ Cv, const uint4* __restrict__ Bq,
+                                                     const uint4* __restrict__ Bd, int N, int nps, float scale,
                                                      float* __restrict__ part) {
   __shared__ __align__(16) KvwLds<T, H> sm;
   // blocks are dealt to the 8 XCDs in turn (block L on XCD L % 8): logical
   // block lam = (L % 8) per + L / 8 gives each XCD a contiguous run of them,
   // i.e. whole window ranges (their D / 32 row groups, key then value), so
-  // the ranges' rows of q, dO and X are fetched into that XCD's L2 once
+  // the ranges' rows of X and their fragments are fetched into that XCD's L2 once
   constexpr int ND = H * DH / KVW_DC;
   const int tot = (int)gridDim.x, per = tot / 8, L = (int)blockIdx.x;
   const int lam = L < 8 * per ? (L % 8) * per + L / 8 : L;
   const int x = lam % ND, kv = (lam / ND) & 1, z = lam / (2 * ND), S = tot / (2 * ND);
   if (kv == 0)
-    kv_wgrad_body<T, DH, H, false>(sm, X, dS, q, N, nps, scale, part, x * KVW_DC, z, S);
+    kv_wgrad_body<T, DH, H, false>(sm, X, Ck, Bq, N, nps, scale, part, x * KVW_DC, z, S);
   else
-    kv_wgrad_body<T, DH, H, true>(sm, X, Ac, dO, N, nps, 1.f, part, x * KVW_DC, z, S);
+    kv_wgrad_body<T, DH, H, true>(sm, X, Cv, Bd, N, nps, 1.f, part, x * KVW_DC, z, S);
 }
 
 // windows per range (a multiple of the tile) and number of ranges: about 256
@@ -1299,30 +1363,45 @@ static void kv_wgrad_split(int64_t N, int D, int& nps, int& S) {
   S = (int)((N + nps - 1) / nps);
 }
 
-int64_t kv_wgrad_ws_floats(int64_t N, int D) {
+// workspace: partial sums [2][S][D][D], then (16-byte units) Ck, Cv
+// [tiles][T][2 H / T][2][64], Bq [tiles][D / 16][2][64], Bd [tiles][D / 16][64]
+int64_t kv_wgrad_ws_floats(int64_t N, int T, int D, int H) {
   if (N <= 0) return 0;
   int nps, S;
   kv_wgrad_split(N, D, nps, S);
-  return (int64_t)2 * S * D * D;
+  const int64_t tiles = (N + KVW_NT - 1) / KVW_NT;
+  return (int64_t)2 * S * D * D + 4 * tiles * 64 * (2 * (int64_t)2 * H * 2 + (int64_t)D / 16 * 3);
 }
 
-bool kv_wgrad_built(int T, int D, int H) { return dx_rank1_built(T, D, H) && H <= 8; }
+// (the first product's column blocks need 32 / T windows per k-step to cover
+// at least 16 / H windows: 2 H >= T)
+bool kv_wgrad_built(int T, int D, int H) { return dx_rank1_built(T, D, H) && H <= 8 && 2 * H >= T; }
 
 bool launch_kv_wgrad(const uint16_t* X, const float* dS, const float* A, const float* q, const float* dO, int64_t N,
                      int T, int D, int H, float scale, float* ws, int64_t ws_cap, float* dWk, float* dWv,
                      hipStream_t s) {
-  // 32-bit element offsets in the kernel
-  if (N <= 0 || N * D >= ((int64_t)1 << 29) || N * T * D >= ((int64_t)1 << 30) || !kv_wgrad_built(T, D, H)) return false;
-  if (kv_wgrad_ws_floats(N, D) > ws_cap) return false;
+  // 32-bit element offsets in the kernels
+  if (N <= 0 || N * D >= ((int64_t)1 << 29) || N * T * D >= ((int64_t)1 << 30) || !kv_wgrad_built(T, D, H))
+    return false;
+  if (kv_wgrad_ws_floats(N, T, D, H) > ws_cap) return false;
   if (((uintptr_t)X | (uintptr_t)dS | (uintptr_t)A | (uintptr_t)q | (uintptr_t)dO | (uintptr_t)ws) & 15) return false;
   int nps, S;
   kv_wgrad_split(N, D, nps, S);
   const int DH = D / H;
+  const int64_t tiles = (N + KVW_NT - 1) / KVW_NT;
+  uint4* Ck = reinterpret_cast<uint4*>(ws + (int64_t)2 * S * D * D);
+  uint4* Cv = Ck + tiles * 2 * H * 2 * 64;
+  uint4* Bq = Cv + tiles * 2 * H * 2 * 64;
+  uint4* Bd = Bq + tiles * (D / 16) * 2 * 64;
   const dim3 grid((unsigned)(2 * S * (D / KVW_DC)));
-#define TRACE_KVW(T_, DH_, H_)                                                                              \
-  if (T == T_ && DH == DH_ && H == H_)                                                                      \
-    hipLaunchKernelGGL((k_kv_wgrad<T_, DH_, H_>), grid, dim3(64 * H_), 0, s, X, dS, A, q, dO, (int)N, nps, scale, ws);
-  TRACE_KVW(4, 32, 4) TRACE_KVW(8, 32, 4) TRACE_KVW(4, 64, 2) TRACE_KVW(8, 64, 2)
+#define TRACE_KVW(T_, DH_, H_)                                                                                  \
+  if (T == T_ && DH == DH_ && H == H_) {                                                                        \
+    hipLaunchKernelGGL((k_kv_pack<T_, DH_, H_>), dim3((unsigned)tiles, 2), dim3(64 * H_), 0, s, dS, A, q, dO,   \
+                       (int)N, Ck, Cv, Bq, Bd);                                                                 \
+    hipLaunchKernelGGL((k_kv_wgrad<T_, DH_, H_>), grid, dim3(64 * H_), 0, s, X, Ck, Cv, Bq, Bd, (int)N, nps,    \
+                       scale, ws);                                                                              \
+  }
+  TRACE_KVW(4, 32, 4) TRACE_KVW(8, 32, 4) TRACE_KVW(4, 64, 2)
   TRACE_KVW(4, 32, 8) TRACE_KVW(8, 32, 8) TRACE_KVW(4, 64, 4) TRACE_KVW(8, 64, 4)
   TRACE_KVW(4, 64, 8) TRACE_KVW(8, 64, 8)
 #undef TRACE_KVW

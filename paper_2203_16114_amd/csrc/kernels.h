@@ -150,10 +150,10 @@ bool launch_dx_rank1(const float* q, const float* dO, const float* dS, const flo
 int64_t attn_bwd_part_floats(int64_t N, int T, int D, int H);
 // bf16 models: dWk, dWv (written, [D][D]) from the rank-one key and value
 // gradients of the last query row and the token rows X (bf16, [N][T][D]);
-// ws: kv_wgrad_ws_floats(N, D) floats; false (nothing launched) when the shape
+// ws: kv_wgrad_ws_floats(N, T, D, H) floats; false (nothing launched) when the shape
 // is not built, the workspace is short or a pointer is not 16-byte aligned
 bool kv_wgrad_built(int T, int D, int H);
-int64_t kv_wgrad_ws_floats(int64_t N, int D);
+int64_t kv_wgrad_ws_floats(int64_t N, int T, int D, int H);
 bool launch_kv_wgrad(const uint16_t* X, const float* dS, const float* A, const float* q, const float* dO, int64_t N,
                      int T, int D, int H, float scale, float* ws, int64_t ws_cap, float* dWk, float* dWv,
                      hipStream_t s);
