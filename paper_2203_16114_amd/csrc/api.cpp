@@ -808,9 +808,20 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // head: dz = (softmax(z) - onehot) / N
   launch_ce_grad(m->kZ, m->ktgt, N, m->dz, s);
   order(m, s, w);
+  // bf16 models: the key and value gradients are used through their rank-one
+  // rows dK_h[n][t] = dS[n][h][t] scale q_h[n], dV_h[n][t] = A[n][h][t] bf(dO_h[n])
+  // (the weight gradients from sums over each window's tokens, the input
+  // gradient of the tokens by k_dx_rank1): dK, dV are not stored
+  const bool pow2 = (T & (T - 1)) == 0 && (L.DH & (L.DH - 1)) == 0;
+  const bool rank1 = m->bf && m->WkT && pow2 && dx_rank1_built(T, D, H);
+  // one layer with those weight gradients: they gather their token rows
+  // themselves, and only the last token's rows are gathered (dWq's operand)
+  const bool kvfold = rank1 && NL == 1 && kv_wgrad_ready(N, T, D, H, m->cfg.e, m->gws_cap);
   // side: the byte-embedding part of the tokens (read by the projection
   // gradients), dWout = h_k^T . dz and dbout = sum_n dz
-  launch_gather_kept(m->bf, m->kwin, N, m->Ec, T, D, m->cfg.e, m->cfg.g, m->Xk, w);
+  const bool xlast = kvfold && launch_gather_last(m->kwin, N, (const uint16_t*)m->Ec, T, D, m->cfg.e, m->cfg.g,
+                                                 (uint16_t*)m->Xk, w);
+  if (!xlast) launch_gather_kept(m->bf, m->kwin, N, m->Ec, T, D, m->cfg.e, m->cfg.g, m->Xk, w);
   GemmArgs go =
       gemm(D, 256, N, at(m->kY, (int64_t)k * N * D), 1, D, rb, m->dz, 256, 1, rb, gr + L.off[P_WOUT], 256, 0.f);
   go.halfA = hf;
@@ -889,12 +900,6 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   float* sQ = m->sP + (int64_t)2 * T * D;
   float* sY = m->sP + (int64_t)(2 * T + 1) * D;
   const float ascale = (float)(1.0 / std::sqrt((double)L.DH));
-  // bf16 models: the key and value gradients are used through their rank-one
-  // rows dK_h[n][t] = dS[n][h][t] scale q_h[n], dV_h[n][t] = A[n][h][t] bf(dO_h[n])
-  // (the weight gradients' B operands are formed from them as they are read,
-  // and the input gradient of the tokens by k_dx_rank1): dK, dV are not stored
-  const bool pow2 = (T & (T - 1)) == 0 && (L.DH & (L.DH - 1)) == 0;
-  const bool rank1 = m->bf && m->WkT && pow2 && dx_rank1_built(T, D, H);
   // rank1: the sums over windows of dK and dV (sK, sV; read by the positional
   // gradients of a single layer only) from the rank-one rows, with those of dQ
   // and dY_0 (sQ, sY) in the same pass
@@ -930,15 +935,22 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   // G^T dZ as GEMMs on the byte-embedding part G, then P^T (sum over windows of
   // dZ) for the positional part
   if (NL == 1) {
-    // rank1: both from the per-window sums over the tokens (one launch)
-    if (!(rank1 && launch_kv_wgrad((const uint16_t*)m->Xk, m->dSc, m->kA, m->kq, m->dO, N, T, D, H, ascale, ws2,
-                                   m->gws_cap, gr + L.at(P_WK, top), gr + L.at(P_WV, top), w))) {
+    // rank1: both from the per-window sums over the tokens (one launch; xlast:
+    // their rows gathered in it, Xk holding the last tokens only)
+    if (xlast) {
+      ok = launch_kv_wgrad(nullptr, m->kwin, (const uint16_t*)m->Ec, m->cfg.e, m->cfg.g, m->dSc, m->kA, m->kq, m->dO,
+                           N, T, D, H, ascale, ws2, m->gws_cap, gr + L.at(P_WK, top), gr + L.at(P_WV, top), w) &&
+           ok;
+    } else if (!(rank1 && launch_kv_wgrad((const uint16_t*)m->Xk, nullptr, nullptr, 8, 1, m->dSc, m->kA, m->kq,
+                                          m->dO, N, T, D, H, ascale, ws2, m->gws_cap, gr + L.at(P_WK, top),
+                                          gr + L.at(P_WV, top), w))) {
       ok = kv_grad(m->Xk, 1, D, hf, false, gr + L.at(P_WK, top)) && ok;
       ok = kv_grad(m->Xk, 1, D, hf, true, gr + L.at(P_WV, top)) && ok;
     }
     // side: dWq = X_last^T dQ; Xk was written on this stream, dQ before the last mark
-    GemmArgs gq = gemm(D, D, N, at(m->Xk, (int64_t)(T - 1) * D), 1, (int64_t)T * D, rb, m->dQ, D, 1, 0,
-                       gr + L.at(P_WQ, top), D, 0.f);
+    GemmArgs gq = xlast ? gemm(D, D, N, m->Xk, 1, D, rb, m->dQ, D, 1, 0, gr + L.at(P_WQ, top), D, 0.f)
+                        : gemm(D, D, N, at(m->Xk, (int64_t)(T - 1) * D), 1, (int64_t)T * D, rb, m->dQ, D, 1, 0,
+                               gr + L.at(P_WQ, top), D, 0.f);
     gq.halfA = hf;
     ok = launch_gemm(gq, ws2, m->gws_cap, w) && ok;
     if (m->cfg.use_pos) {

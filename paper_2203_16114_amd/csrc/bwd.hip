@@ -1114,9 +1114,10 @@ __device__ __forceinline__ void kvw_split8(const float (&v)[8], uint4& hi, uint4
 
 template <int T, int DH, int H, bool VAL>
 __device__ __forceinline__ void kv_wgrad_body(KvwLds<T, H>& sm, const uint16_t* __restrict__ X,
-                                              const uint4* __restrict__ Cp, const uint4* __restrict__ Bp, int N,
-                                              int nps, float bscale, float* __restrict__ part, int d0, int z,
-                                              int S) {
+                                              const uint8_t* __restrict__ win, const uint16_t* __restrict__ E,
+                                              int e, int gw, const uint4* __restrict__ Cp,
+                                              const uint4* __restrict__ Bp, int N, int nps, float bscale,
+                                              float* __restrict__ part, int d0, int z, int S) {
   constexpr int D = H * DH, NJF = DH / 16, NTH = 64 * H;
   constexpr int XR = KvwLds<T, H>::XR, ZR = KvwLds<T, H>::ZR, ZH = KvwLds<T, H>::ZH;
   constexpr int NKS = KVW_NT * T / 32;  // k-steps of the first product per tile
@@ -1132,15 +1133,29 @@ __device__ __forceinline__ void kv_wgrad_body(KvwLds<T, H>& sm, const uint16_t* 
   const int so = threadIdx.x >> 2, sp = threadIdx.x & 3;  // staging unit: k-octet so, d-octet sp
 
   // X of tile k, unit (so, sp): rows k = 8 so + i of d0 + 8 sp .. + 7, clamped
-  // (32-bit element offsets: N T D < 2^30)
+  // (32-bit element offsets: N T D < 2^30).  With win: gathered here, token
+  // (n, t) columns c .. c + 7 being E[win[(n T + t) gw + c / e]][c % e ..] (gw
+  // bytes per token, e a multiple of 8), all byte loads first
   uint4 xr[8];
+  const int xc = d0 + 8 * sp, xj = win ? xc / e : 0, xcc = win ? xc - xj * e : 0;
   auto load = [&](int k) {
     if (!stager) return;
     const int n0 = nb + k * KVW_NT;
+    if (win) {
+      int by[8];
 #pragma unroll
-    for (int i = 0; i < 8; ++i) {
-      const int kk = 8 * so + i, n = min(n0 + kk / T, N - 1), t = kk % T;
-      xr[i] = *reinterpret_cast<const uint4*>(X + ((uint32_t)(n * T + t) * D + d0 + 8 * sp));
+      for (int i = 0; i < 8; ++i) {
+        const int kk = 8 * so + i, n = min(n0 + kk / T, N - 1), t = kk % T;
+        by[i] = win[(uint32_t)(n * T + t) * gw + xj];
+      }
+#pragma unroll
+      for (int i = 0; i < 8; ++i) xr[i] = *reinterpret_cast<const uint4*>(E + by[i] * e + xcc);
+    } else {
+#pragma unroll
+      for (int i = 0; i < 8; ++i) {
+        const int kk = 8 * so + i, n = min(n0 + kk / T, N - 1), t = kk % T;
+        xr[i] = *reinterpret_cast<const uint4*>(X + ((uint32_t)(n * T + t) * D + xc));
+      }
     }
   };
   // transposed: row d = 8 sp + e holds k = 8 so .. + 7 (one 16-byte write)
@@ -1340,10 +1355,11 @@ __global__ __launch_bounds__(64 * H) void k_kv_pack(const float* __restrict__ dS
 }
 
 template <int T, int DH, int H>
-__global__ __launch_bounds__(64 * H) void k_kv_wgrad(const uint16_t* __restrict__ X, const uint4* __restrict__ Ck,
-                                                     const uint4* __restrict__ Cv, const uint4* __restrict__ Bq,
-                                                     const uint4* __restrict__ Bd, int N, int nps, float scale,
-                                                     float* __restrict__ part) {
+__global__ __launch_bounds__(64 * H) void k_kv_wgrad(const uint16_t* __restrict__ X, const uint8_t* __restrict__ win,
+                                                     const uint16_t* __restrict__ E, int e, int g,
+                                                     const uint4* __restrict__ Ck, const uint4* __restrict__ Cv,
+                                                     const uint4* __restrict__ Bq, const uint4* __restrict__ Bd, int N,
+                                                     int nps, float scale, float* __restrict__ part) {
   __shared__ __align__(16) KvwLds<T, H> sm;
   // blocks are dealt to the 8 XCDs in turn (block L on XCD L % 8): logical
   // block lam = (L % 8) per + L / 8 gives each XCD a contiguous run of them,
@@ -1354,9 +1370,9 @@ __global__ __launch_bounds__(64 * H) void k_kv_wgrad(const uint16_t* __restrict_
   const int lam = L < 8 * per ? (L % 8) * per + L / 8 : L;
   const int x = lam % ND, kv = (lam / ND) & 1, z = lam / (2 * ND), S = tot / (2 * ND);
   if (kv == 0)
-    kv_wgrad_body<T, DH, H, false>(sm, X, Ck, Bq, N, nps, scale, part, x * KVW_DC, z, S);
+    kv_wgrad_body<T, DH, H, false>(sm, X, win, E, e, g, Ck, Bq, N, nps, scale, part, x * KVW_DC, z, S);
   else
-    kv_wgrad_body<T, DH, H, true>(sm, X, Cv, Bd, N, nps, 1.f, part, x * KVW_DC, z, S);
+    kv_wgrad_body<T, DH, H, true>(sm, X, win, E, e, g, Cv, Bd, N, nps, 1.f, part, x * KVW_DC, z, S);
 }
 
 // windows per range (a multiple of the tile) and number of ranges: about 256
@@ -1382,14 +1398,18 @@ int64_t kv_wgrad_ws_floats(int64_t N, int T, int D, int H) {
 // at least 16 / H windows: 2 H >= T)
 bool kv_wgrad_built(int T, int D, int H) { return dx_rank1_built(T, D, H) && H <= 8 && 2 * H >= T; }
 
-bool launch_kv_wgrad(const uint16_t* X, const float* dS, const float* A, const float* q, const float* dO, int64_t N,
-                     int T, int D, int H, float scale, float* ws, int64_t ws_cap, float* dWk, float* dWv,
-                     hipStream_t s) {
-  // 32-bit element offsets in the kernels
-  if (N <= 0 || N * D >= ((int64_t)1 << 29) || N * T * D >= ((int64_t)1 << 30) || !kv_wgrad_built(T, D, H))
+bool kv_wgrad_ready(int64_t N, int T, int D, int H, int e, int64_t ws_cap) {
+  // 32-bit element offsets in the kernels; the gathered form needs e a multiple of 8
+  return N > 0 && N * D < ((int64_t)1 << 29) && N * T * D < ((int64_t)1 << 30) && kv_wgrad_built(T, D, H) &&
+         kv_wgrad_ws_floats(N, T, D, H) <= ws_cap && e % 8 == 0;
+}
+
+bool launch_kv_wgrad(const uint16_t* X, const uint8_t* win, const uint16_t* E, int e, int g, const float* dS,
+                     const float* A, const float* q, const float* dO, int64_t N, int T, int D, int H, float scale,
+                     float* ws, int64_t ws_cap, float* dWk, float* dWv, hipStream_t s) {
+  if (!kv_wgrad_ready(N, T, D, H, win ? e : 8, ws_cap) || (!win && !X)) return false;
+  if (((uintptr_t)X | (uintptr_t)E | (uintptr_t)dS | (uintptr_t)A | (uintptr_t)q | (uintptr_t)dO | (uintptr_t)ws) & 15)
     return false;
-  if (kv_wgrad_ws_floats(N, T, D, H) > ws_cap) return false;
-  if (((uintptr_t)X | (uintptr_t)dS | (uintptr_t)A | (uintptr_t)q | (uintptr_t)dO | (uintptr_t)ws) & 15) return false;
   int nps, S;
   kv_wgrad_split(N, D, nps, S);
   const int DH = D / H;
@@ -1403,8 +1423,8 @@ bool launch_kv_wgrad(const uint16_t* X, const float* dS, const float* A, const f
   if (T == T_ && DH == DH_ && H == H_) {                                                                        \
     hipLaunchKernelGGL((k_kv_pack<T_, DH_, H_>), dim3((unsigned)tiles, 2), dim3(64 * H_), 0, s, dS, A, q, dO,   \
                        (int)N, Ck, Cv, Bq, Bd);                                                                 \
-    hipLaunchKernelGGL((k_kv_wgrad<T_, DH_, H_>), grid, dim3(64 * H_), 0, s, X, Ck, Cv, Bq, Bd, (int)N, nps,    \
-                       scale, ws);                                                                              \
+    hipLaunchKernelGGL((k_kv_wgrad<T_, DH_, H_>), grid, dim3(64 * H_), 0, s, X, win, E, e, g, Ck, Cv, Bq, Bd,   \
+                       (int)N, nps, scale, ws);                                                                 \
   }
   TRACE_KVW(4, 32, 4) TRACE_KVW(8, 32, 4) TRACE_KVW(4, 64, 2)
   TRACE_KVW(4, 32, 8) TRACE_KVW(8, 32, 8) TRACE_KVW(4, 64, 4) TRACE_KVW(8, 64, 4)
@@ -1835,8 +1855,8 @@ __global__ __launch_bounds__(256) void k_gather_kept(const uint8_t* __restrict__
 // GK_U * 256 consecutive units, a thread GK_U of them 256 apart, all byte loads
 // first, then all row loads, then the stores.
 constexpr int GK_U = 4;
-__global__ __launch_bounds__(256) void k_gather_kept8(const uint8_t* __restrict__ win, int64_t rows,
-                                                      const uint16_t* __restrict__ E, int T, int D, int e, int g,
+__global__ __launch_bounds__(256) void k_gather_kept8(const uint8_t* __restrict__ win, int64_t rows, int wstride,
+                                                      const uint16_t* __restrict__ E, int D, int e,
                                                       uint16_t* __restrict__ X) {
   const uint32_t q8 = (uint32_t)D / 8;
   const uint32_t nu = (uint32_t)rows * q8;  // the grid has fewer than 2^32 units
@@ -1849,7 +1869,7 @@ __global__ __launch_bounds__(256) void k_gather_kept8(const uint8_t* __restrict_
     const int c = (int)(i - row * q8) * 8;
     const int j = c / e;
     cc[u] = c - j * e;
-    byte[u] = win[(int64_t)row * g + j];
+    byte[u] = win[(int64_t)row * wstride + j];
   }
   typedef __attribute__((ext_vector_type(4))) uint32_t u32x4;
   u32x4 v[GK_U];
@@ -1871,7 +1891,7 @@ void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, i
   if (bf && e % 8 == 0 && ((uintptr_t)E & 15) == 0 && ((uintptr_t)X & 15) == 0 &&
       rows * (D / 8) < ((int64_t)1 << 31)) {
     const dim3 grid8((unsigned)((rows * (D / 8) + 256 * GK_U - 1) / (256 * GK_U)));
-    hipLaunchKernelGGL(k_gather_kept8, grid8, dim3(256), 0, s, win, rows, (const uint16_t*)E, T, D, e, g,
+    hipLaunchKernelGGL(k_gather_kept8, grid8, dim3(256), 0, s, win, rows, g, (const uint16_t*)E, D, e,
                        (uint16_t*)X);
     return;
   }
@@ -1880,6 +1900,17 @@ void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, i
     hipLaunchKernelGGL(k_gather_kept<true>, grid, dim3(256), 0, s, win, rows, (const uint16_t*)E, T, D, e, g, X);
   else
     hipLaunchKernelGGL(k_gather_kept<false>, grid, dim3(256), 0, s, win, rows, (const float*)E, T, D, e, g, X);
+}
+
+bool launch_gather_last(const uint8_t* win, int64_t N, const uint16_t* E, int T, int D, int e, int g, uint16_t* X,
+                        hipStream_t s) {
+  if (N <= 0) return true;
+  if (e % 8 != 0 || ((uintptr_t)E & 15) != 0 || ((uintptr_t)X & 15) != 0 || N * (D / 8) >= ((int64_t)1 << 31))
+    return false;
+  // the last token's group of window n starts (T - 1) g bytes into its W = T g bytes
+  const dim3 grid8((unsigned)((N * (D / 8) + 256 * GK_U - 1) / (256 * GK_U)));
+  hipLaunchKernelGGL(k_gather_kept8, grid8, dim3(256), 0, s, win + (int64_t)(T - 1) * g, N, T * g, E, D, e, X);
+  return true;
 }
 
 // Positional part of a projection's weight gradient:

@@ -154,9 +154,14 @@ int64_t attn_bwd_part_floats(int64_t N, int T, int D, int H);
 // is not built, the workspace is short or a pointer is not 16-byte aligned
 bool kv_wgrad_built(int T, int D, int H);
 int64_t kv_wgrad_ws_floats(int64_t N, int T, int D, int H);
-bool launch_kv_wgrad(const uint16_t* X, const float* dS, const float* A, const float* q, const float* dO, int64_t N,
-                     int T, int D, int H, float scale, float* ws, int64_t ws_cap, float* dWk, float* dWv,
-                     hipStream_t s);
+// X: the token rows' byte-embedding part (bf16, [N][T][D]), or NULL with win (the
+// window bytes, [N][T g]) and E (the bf16 embedding copy, [256][e]): the rows are
+// gathered in the kernel.  kv_wgrad_ready: whether launch_kv_wgrad takes the shape
+// with its rows gathered (pointers from the device allocator)
+bool kv_wgrad_ready(int64_t N, int T, int D, int H, int e, int64_t ws_cap);
+bool launch_kv_wgrad(const uint16_t* X, const uint8_t* win, const uint16_t* E, int e, int g, const float* dS,
+                     const float* A, const float* q, const float* dO, int64_t N, int T, int D, int H, float scale,
+                     float* ws, int64_t ws_cap, float* dWk, float* dWv, hipStream_t s);
 // sums over windows of the rank-one key and value gradients of the last query
 // row, of dQ and of dY0 into colsums [2 T + 2][D] (sK [T][D], sV [T][D], sQ, sY);
 // part: rank1_sums_part_floats floats (at most attn_bwd_part_floats); false when
@@ -174,6 +179,10 @@ int64_t embed_bwd_ws_floats(int64_t M, int e);  // M = N * W positions
 void launch_embed_bwd(const uint8_t* win, const float* dX, int64_t N, int W, int e, float* dE, float* ws,
                       hipStream_t s);
 void launch_gather_kept(bool bf, const uint8_t* win, int64_t N, const void* E, int T, int D, int e, int g, void* X,
+                        hipStream_t s);
+// bf16, the last token of each window only: X [N][D]; false (nothing launched)
+// unless e is a multiple of 8 and E, X are 16-byte aligned
+bool launch_gather_last(const uint8_t* win, int64_t N, const uint16_t* E, int T, int D, int e, int g, uint16_t* X,
                         hipStream_t s);
 // dW[i][j] += sum_{u < nt} P[t0 + u][i] * S[u][j]  (P: operand copy [T][D])
 void launch_pos_grad(bool bf, const void* P, const float* S, int t0, int nt, int D, float* dW, hipStream_t s);
