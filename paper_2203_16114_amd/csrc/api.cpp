@@ -816,7 +816,8 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   const bool rank1 = m->bf && m->WkT && pow2 && dx_rank1_built(T, D, H);
   // one layer with those weight gradients: they gather their token rows
   // themselves, and only the last token's rows are gathered (dWq's operand)
-  const bool kvfold = rank1 && NL == 1 && kv_wgrad_ready(N, T, D, H, m->cfg.e, m->gws_cap);
+  const bool kvfold = rank1 && NL == 1 && kv_wgrad_ready(N, T, D, H, m->cfg.e, m->gws_cap) &&
+                      L.at(P_WV, top) == L.at(P_WK, top) + (int64_t)D * D;
   // side: the byte-embedding part of the tokens (read by the projection
   // gradients), dWout = h_k^T . dz and dbout = sum_n dz
   const bool xlast = kvfold && launch_gather_last(m->kwin, N, (const uint16_t*)m->Ec, T, D, m->cfg.e, m->cfg.g,

@@ -1087,7 +1087,7 @@ bool launch_dx_rank1(const float* q, const float* dO, const float* dS, const flo
 //     column c of j-fragment jf is j = h DH + NJF c + jf, so a lane's NJF
 //     values of q or dO are contiguous.
 // Windows past the range have zero coefficients, so zero Z (their rows are read
-// clamped).  Partial sums of the window range z go to part[kv][z][d][j]
+// clamped).  Partial sums of the window range z go to part[z][kv][d][j]
 // (kv 0: key, 1: value), summed by the split-K reduce.
 constexpr int KVW_DC = 32, KVW_NT = 32;
 
@@ -1269,7 +1269,7 @@ __device__ __forceinline__ void kv_wgrad_body(KvwLds<T, H>& sm, const uint16_t* 
   }
   // lane holds rows 4 g + r of column m: d = d0 + 16 f + 4 g + r, j = h DH + NJF m + jf
   const int64_t DD = (int64_t)D * D;
-  float* p = part + ((int64_t)(VAL ? 1 : 0) * S + z) * DD;
+  float* p = part + ((int64_t)z * 2 + (VAL ? 1 : 0)) * DD;
 #pragma unroll
   for (int f = 0; f < 2; ++f)
 #pragma unroll
@@ -1384,7 +1384,7 @@ static void kv_wgrad_split(int64_t N, int D, int& nps, int& S) {
   S = (int)((N + nps - 1) / nps);
 }
 
-// workspace: partial sums [2][S][D][D], then (16-byte units) Ck, Cv
+// workspace: partial sums [S][2][D][D], then (16-byte units) Ck, Cv
 // [tiles][T][2 H / T][2][64], Bq [tiles][D / 16][2][64], Bd [tiles][D / 16][64]
 int64_t kv_wgrad_ws_floats(int64_t N, int T, int D, int H) {
   if (N <= 0) return 0;
@@ -1408,6 +1408,7 @@ bool launch_kv_wgrad(const uint16_t* X, const uint8_t* win, const uint16_t* E, i
                      const float* A, const float* q, const float* dO, int64_t N, int T, int D, int H, float scale,
                      float* ws, int64_t ws_cap, float* dWk, float* dWv, hipStream_t s) {
   if (!kv_wgrad_ready(N, T, D, H, win ? e : 8, ws_cap) || (!win && !X)) return false;
+  if (dWv != dWk + (int64_t)D * D) return false;  // one split-K pass for both
   if (((uintptr_t)X | (uintptr_t)E | (uintptr_t)dS | (uintptr_t)A | (uintptr_t)q | (uintptr_t)dO | (uintptr_t)ws) & 15)
     return false;
   int nps, S;
@@ -1430,8 +1431,8 @@ bool launch_kv_wgrad(const uint16_t* X, const uint8_t* win, const uint16_t* E, i
   TRACE_KVW(4, 32, 8) TRACE_KVW(8, 32, 8) TRACE_KVW(4, 64, 4) TRACE_KVW(8, 64, 4)
   TRACE_KVW(4, 64, 8) TRACE_KVW(8, 64, 8)
 #undef TRACE_KVW
-  launch_splitk_reduce(ws, S, D, D, dWk, D, 0.f, nullptr, s);
-  launch_splitk_reduce(ws + (int64_t)S * D * D, S, D, D, dWv, D, 0.f, nullptr, s);
+  // the two gradients as one [2 D][D] product
+  launch_splitk_reduce(ws, S, 2 * D, D, dWk, D, 0.f, nullptr, s);
   return true;
 }
 

@@ -157,7 +157,8 @@ int64_t kv_wgrad_ws_floats(int64_t N, int T, int D, int H);
 // X: the token rows' byte-embedding part (bf16, [N][T][D]), or NULL with win (the
 // window bytes, [N][T g]) and E (the bf16 embedding copy, [256][e]): the rows are
 // gathered in the kernel.  kv_wgrad_ready: whether launch_kv_wgrad takes the shape
-// with its rows gathered (pointers from the device allocator)
+// with its rows gathered (pointers from the device allocator; dWv must follow
+// dWk, dWv = dWk + D D)
 bool kv_wgrad_ready(int64_t N, int T, int D, int H, int e, int64_t ws_cap);
 bool launch_kv_wgrad(const uint16_t* X, const uint8_t* win, const uint16_t* E, int e, int g, const float* dS,
                      const float* A, const float* q, const float* dO, int64_t N, int T, int D, int H, float scale,
