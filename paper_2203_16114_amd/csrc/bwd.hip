@@ -460,13 +460,15 @@ __global__ __launch_bounds__(256) void k_colsum2(const float* __restrict__ ws, i
 // four columns per thread, eight rows in flight; the four waves of a block
 // take consecutive quarters of the split's rows, and their sums are added in
 // wave order
+// (gridDim.y splits of the rows; with one, the sums go straight to out, added
+// to it when beta is not 0)
 __global__ __launch_bounds__(256) void k_colsum1v(const float* __restrict__ in, int64_t rows, int64_t cols, int64_t ld,
-                                                  float* __restrict__ ws) {
+                                                  float* __restrict__ ws, float* __restrict__ out, float beta) {
   __shared__ float4 red[4][64];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int64_t c = ((int64_t)blockIdx.x * 64 + lane) * 4;
   const int s = blockIdx.y;
-  const int64_t chunk = (rows + COLSUM_SPLITS - 1) / COLSUM_SPLITS;
+  const int64_t chunk = (rows + gridDim.y - 1) / gridDim.y;
   const int64_t r0s = s * chunk, r1s = min(rows, r0s + chunk);
   const int64_t sub = (chunk + 3) / 4;
   const int64_t r0 = r0s + wave * sub, r1 = min(r1s, r0 + sub);
@@ -500,15 +502,31 @@ __global__ __launch_bounds__(256) void k_colsum1v(const float* __restrict__ in, 
       t.z += v.z;
       t.w += v.w;
     }
-    *reinterpret_cast<float4*>(ws + s * cols + c) = t;
+    if (gridDim.y > 1) {
+      *reinterpret_cast<float4*>(ws + s * cols + c) = t;
+    } else {
+      float4* o = reinterpret_cast<float4*>(out + c);
+      if (beta != 0.f) {
+        const float4 u = *o;
+        t = make_float4(u.x + t.x, u.y + t.y, u.z + t.z, u.w + t.w);
+      }
+      *o = t;
+    }
   }
 }
 int64_t colsum_ws_floats(int64_t cols) { return COLSUM_SPLITS * cols; }
 void launch_colsum(const float* in, int64_t rows, int64_t cols, int64_t ld, float* out, float beta, float* ws,
                    hipStream_t s) {
   const unsigned gx = (unsigned)((cols + 255) / 256);
-  if (cols % 4 == 0 && ld % 4 == 0 && ((uintptr_t)in & 15) == 0)
-    hipLaunchKernelGGL(k_colsum1v, dim3(gx, COLSUM_SPLITS), dim3(256), 0, s, in, rows, cols, ld, ws);
+  const bool vec = cols % 4 == 0 && ld % 4 == 0 && ((uintptr_t)in & 15) == 0;
+  // few rows (sums over chunks of windows): one pass, each block over all rows
+  if (vec && rows <= 512 && ((uintptr_t)out & 15) == 0) {
+    hipLaunchKernelGGL(k_colsum1v, dim3((unsigned)((cols / 4 + 63) / 64), 1), dim3(256), 0, s, in, rows, cols, ld, ws,
+                       out, beta);
+    return;
+  }
+  if (vec)
+    hipLaunchKernelGGL(k_colsum1v, dim3(gx, COLSUM_SPLITS), dim3(256), 0, s, in, rows, cols, ld, ws, out, beta);
   else
     hipLaunchKernelGGL(k_colsum1, dim3(gx, COLSUM_SPLITS), dim3(256), 0, s, in, rows, cols, ld, ws);
   hipLaunchKernelGGL(k_colsum2, dim3((unsigned)((cols + 63) / 64)), dim3(256), 0, s, ws, cols, out, beta);
