@@ -1095,15 +1095,17 @@ bool launch_dx_rank1(const float* q, const float* dO, const float* dS, const flo
 //  1. Z^T = X^T Cbd: rows d, k = (window w, token t) over 32 / T windows per
 //     k-step, columns (w', h) of 16 / H windows; Cbd(w t, w' h) = C[w][h][t]
 //     where w = w', 0 elsewhere (block diagonal, C = dS or A as bf16 hi + lo,
-//     packed as fragments by k_kv_pack).
-//     X is staged in LDS transposed (rows d, k contiguous), so that a lane's
-//     A fragment is one 16-byte read; the k-steps are dealt to the waves.  Z
+//     packed as fragments by k_kv_pack).  X (the tokens' rows, or gathered
+//     here from the window bytes and the embedding copy) is staged in LDS
+//     transposed (rows d, k contiguous), double-buffered, so that a lane's A
+//     fragment is one 16-byte read; the k-steps are dealt to the waves.  Z
 //     goes to LDS as fp32, rows (h, d) of the tile's 32 windows.
 //  2. wave h: dW[d][h DH + j] += sum_w Z_h[w][d] B[w][j], Z as bf16 hi + lo,
 //     B = q as hi + lo (three products; the scale applied to the sums) or
-//     bf(dO), exact (two), packed as fragments by k_kv_pack.  Fragment row m of d-fragment f is d = 16 f + m,
-//     column c of j-fragment jf is j = h DH + NJF c + jf, so a lane's NJF
-//     values of q or dO are contiguous.
+//     bf(dO), exact (two), packed as fragments by k_kv_pack.  Fragment row m of
+//     d-fragment f is d = 16 f + m, column c of j-fragment jf is
+//     j = h DH + NJF c + jf.
+// The next tile's fragments are loaded while the current one is used.
 // Windows past the range have zero coefficients, so zero Z (their rows are read
 // clamped).  Partial sums of the window range z go to part[z][kv][d][j]
 // (kv 0: key, 1: value), summed by the split-K reduce.
