@@ -94,6 +94,23 @@ def test_bf16_gradient_rank_one_shapes_match_emulating_oracle(name):
         assert np.linalg.norm(b) > 0, (name, pname)
 
 
+@pytest.mark.parametrize("name", sorted(RANK1_SHAPES))
+def test_bf16_gradient_rank_one_tiny_batch_matches_emulating_oracle(name):
+    """B = 5 windows: fewer than one 32-window tile of the key/value weight
+    gradients (the rest of the tile has zero coefficients, its rows read clamped)."""
+    shape = RANK1_SHAPES[name]
+    streams = synth.random_streams(0x99 + len(name), 5, shape["W"] + 40)
+    m, cfg, flat, g, _, w, y = _grad_run(shape, "bf16", 0x5151, streams, shape["W"] + 9)
+    _, ref = O.forward_backward(flat, cfg, w, y, mode="bf16")
+    gp = O.unflatten(g, cfg)
+    for pname, _ in O.param_layout(cfg):
+        a = gp[pname].astype(np.float64).ravel()
+        b = np.asarray(ref[pname], np.float64).ravel()
+        rel = np.linalg.norm(a - b) / max(np.linalg.norm(b), 1e-30)
+        assert rel <= 1e-2, (name, pname, rel)
+        assert np.linalg.norm(b) > 0, (name, pname)
+
+
 @pytest.mark.parametrize("kind", ["skewed", "one_byte"])
 def test_fp32_embedding_gradient_over_many_sort_blocks(kind):
     """1100 kept windows of 32 bytes: 35200 positions, several blocks of the
