@@ -321,6 +321,19 @@ int trace_debug_gemm(int M, int N, int K, const void* d_A, int a_kc, int mode_a,
  * ESTATE if no batch is kept; the kept batch stays kept. */
 int trace_debug_kept_tokens(trace_model* m, void* d_X, void* stream);
 
+/* Test support for the key and value weight gradients of bf16 models (the
+ * rank-one rows of the last query row, Eq. 2's attention; Alg. 1 line 10):
+ * recomputes dWk and dWv from the buffers the last trace_adapt_step left (its
+ * score gradients, attention weights, q and dO; the window bytes of its batch;
+ * the current embedding copy) twice, into d_rows from the token rows written
+ * by the update's gather (trace_debug_kept_tokens' kernel), into d_gathered
+ * with the rows gathered inside the weight-gradient kernel.  Each output is
+ * [2][d][d] fp32 (dWk, then dWv), device memory owned by the caller; the model's
+ * gradient is not touched.  The two are meant to be bitwise equal.  ESTATE
+ * before the first update; EUNSUPPORTED for fp32 models and shapes the kernel
+ * does not take (the path that uses it then is the GEMM over every token row). */
+int trace_debug_kv_wgrad(trace_model* m, float* d_gathered, float* d_rows, void* stream);
+
 /* Per-kernel timing with HIP events recorded on the caller's stream around each
  * launch (measurement support; off by default).  While enabled, every kernel
  * launch of the calls above is bracketed by two events (the Adam kernel's

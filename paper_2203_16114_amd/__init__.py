@@ -27,7 +27,7 @@ EXPORTS = ("trace_create", "trace_destroy", "trace_param_count", "trace_init_wei
            "trace_gated_run",
            "trace_get_state", "trace_set_state", "trace_get_grads", "trace_quant_table", "trace_quantize",
            "trace_rc_encode", "trace_rc_decode", "trace_compress", "trace_decompress",
-           "trace_debug_gemm", "trace_debug_kept_tokens",
+           "trace_debug_gemm", "trace_debug_kept_tokens", "trace_debug_kv_wgrad",
            "trace_set_timing",
            "trace_read_timing", "trace_strerror", "trace_last_error")
 KINDS = ("attn", "ffn_head", "step_ce", "backward", "adam", "refresh")
@@ -98,6 +98,7 @@ def lib():
             "trace_debug_gemm": (c_int32, [c_int32, c_int32, c_int32, P, c_int32, c_int32, P, c_int32, c_int32, P,
                                            c_int32, c_int32, P, c_int64, P]),
             "trace_debug_kept_tokens": (c_int32, [P, P, P]),
+            "trace_debug_kv_wgrad": (c_int32, [P, P, P, P]),
             "trace_set_timing": (c_int32, [P, c_int32]),
             "trace_read_timing": (c_int32, [P, P, P, POINTER(c_int64)]),
             "trace_strerror": (ctypes.c_char_p, [c_int32]),
@@ -391,6 +392,17 @@ class TraceModel:
         out = {k: (float(ms[i]), int(n[i])) for i, k in enumerate(KINDS)}
         out["overflow"] = ov.value
         return out
+
+    def debug_kv_wgrad(self, stream=None):
+        """dWk and dWv of the last update recomputed twice by the rank-one
+        weight-gradient kernel (trace_debug_kv_wgrad): from the gathered token
+        rows and with the rows gathered in the kernel.  Two CUDA tensors
+        [2][d][d] fp32 (gathered in the kernel, from the rows)."""
+        import torch
+        a = torch.empty(2, self.d, self.d, dtype=torch.float32, device="cuda")
+        b = torch.empty_like(a)
+        check(lib().trace_debug_kv_wgrad(self._h, _dptr(a), _dptr(b), _stream_ptr(stream)))
+        return a, b
 
     def debug_kept_tokens(self, n_windows: int, stream=None):
         """Byte-embedding part of the kept batch's tokens, from the update's

@@ -24,6 +24,7 @@ struct trace_model {
   // fp32 master, Adam moments, gradient (canonical flat order)
   float *theta, *am, *av, *grad;
   int64_t step;
+  bool upd_run;  // trace_adapt_step has run in this process (its backward buffers hold values)
   // operand copies
   void *Ec, *Pc;
   float* PW;  // [3][T][D] positional parts of the q, k, v projections
@@ -1012,6 +1013,7 @@ extern "C" int trace_adapt_step(trace_model* m, void* stream) {
   tend(m, tk, TRACE_KIND_BACKWARD, s);
   // Adam on the flat master, then new operand copies
   m->step += 1;
+  m->upd_run = true;
   const float bc1 = (float)(1.0 - std::pow(m->cfg.beta1, (double)m->step));
   const float bc2 = (float)(1.0 - std::pow(m->cfg.beta2, (double)m->step));
   // one kernel: its dispatch records the two events itself, so the region is the kernel's own duration
@@ -1074,6 +1076,30 @@ extern "C" int trace_debug_kept_tokens(trace_model* m, void* d_X, void* stream) 
   launch_gather_kept(m->bf, m->kwin, m->keepN, m->Ec, m->L.T, m->L.D, m->cfg.e, m->cfg.g, d_X, S(stream));
   const hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_fail(e, "trace_debug_kept_tokens");
+  return TRACE_OK;
+}
+
+extern "C" int trace_debug_kv_wgrad(trace_model* m, float* d_gathered, float* d_rows, void* stream) {
+  if (!m || !d_gathered || !d_rows) return fail(TRACE_EINVAL, "model or output is NULL");
+  if (!m->upd_run) return fail(TRACE_ESTATE, "no update yet: run trace_adapt_step first");
+  const Layout& L = m->L;
+  const int64_t N = m->keepN;
+  const int T = L.T, D = L.D, H = m->cfg.H;
+  const bool pow2 = (T & (T - 1)) == 0 && (L.DH & (L.DH - 1)) == 0;
+  if (!m->bf || !m->WkT || !pow2 || !dx_rank1_built(T, D, H) || L.NL != 1 ||
+      !kv_wgrad_ready(N, T, D, H, m->cfg.e, m->gws_cap))
+    return fail(TRACE_EUNSUPPORTED, "trace_debug_kv_wgrad: not a shape of the rank-one weight-gradient kernel");
+  const hipStream_t s = S(stream);
+  const float ascale = (float)(1.0 / std::sqrt((double)L.DH));
+  const int64_t DD = (int64_t)D * D;
+  launch_gather_kept(true, m->kwin, N, m->Ec, T, D, m->cfg.e, m->cfg.g, m->Xk, s);
+  bool ok = launch_kv_wgrad((const uint16_t*)m->Xk, nullptr, nullptr, 8, 1, m->dSc, m->kA, m->kq, m->dO, N, T, D, H,
+                            ascale, m->gws2, m->gws_cap, d_rows, d_rows + DD, s);
+  ok = ok && launch_kv_wgrad(nullptr, m->kwin, (const uint16_t*)m->Ec, m->cfg.e, m->cfg.g, m->dSc, m->kA, m->kq, m->dO,
+                             N, T, D, H, ascale, m->gws2, m->gws_cap, d_gathered, d_gathered + DD, s);
+  if (!ok) return fail(TRACE_EUNSUPPORTED, "trace_debug_kv_wgrad: the kernel did not take the operands");
+  const hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_fail(e, "trace_debug_kv_wgrad");
   return TRACE_OK;
 }
 

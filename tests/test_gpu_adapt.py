@@ -94,6 +94,31 @@ def test_bf16_gradient_rank_one_shapes_match_emulating_oracle(name):
         assert np.linalg.norm(b) > 0, (name, pname)
 
 
+# the key/value weight-gradient kernel at the shapes above and at d = 512 (the
+# large workload's token shape, T = 8, dh = 64)
+KV_SHAPES = dict(RANK1_SHAPES, **{"T8-d512": dict(W=64, e=64, g=8, H=8, F=512, k=1)})
+
+
+@pytest.mark.parametrize("name", sorted(KV_SHAPES))
+def test_kv_weight_gradient_in_kernel_gather_is_bitwise_the_update_gather(name):
+    """dWk, dWv of the last update recomputed by the kernel from token rows
+    written by the update's gather (bit-exact vs the oracle's embed_group in
+    test_gpu_forward.py) and with the rows gathered inside the kernel: the same
+    bits, so the in-kernel byte-group indexing is the tested one (Sec. 4.2)."""
+    shape = KV_SHAPES[name]
+    B = 300
+    streams = synth.random_streams(0x5A + len(name), B, shape["W"] + 40)
+    m = make_model(shape, "bf16", 0x77, max_keep=B)
+    m.forward_bits(to_dev(streams), shape["W"] + 11, 1, keep=True)
+    m.adapt_step()
+    a, b = m.debug_kv_wgrad()
+    torch.cuda.synchronize()
+    a = a.cpu().numpy()
+    b = b.cpu().numpy()
+    assert np.isfinite(a).all() and np.abs(a).max() > 0
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
 @pytest.mark.parametrize("name", sorted(RANK1_SHAPES))
 def test_bf16_gradient_rank_one_tiny_batch_matches_emulating_oracle(name):
     """B = 5 windows: fewer than one 32-window tile of the key/value weight
