@@ -700,7 +700,7 @@ __global__ __launch_bounds__(256) void k_attn_bwd2(const float* __restrict__ dO,
 // one head's DH / CPL lanes consecutive), so that every row of K and V comes in
 // CPL-float vector loads, all T rows of both first.  dA_u by a lane sum and a
 // shuffle tree over the head's lanes; dS and dQ as in k_attn_bwd2.
-template <int D, int DH, int T>
+template <int D, int DH, int T, bool NTL>
 __global__ __launch_bounds__(256) void k_attn_bwd_r1(const float* __restrict__ dO, const float* __restrict__ K,
                                                      const float* __restrict__ V,
                                                      const float* __restrict__ A, int64_t N, float scale,
@@ -716,16 +716,26 @@ __global__ __launch_bounds__(256) void k_attn_bwd_r1(const float* __restrict__ d
   if (n >= N) return;  // (whole waves)
   const int c0 = lane * CPL, h = c0 / DH;
   float kr[T][CPL], vr[T][CPL], o[CPL], a[T];
+  // NTL: K and V larger than the last-level cache, streamed past it (they are
+  // read once), the V rows first (dA needs them alone), then K's, so that the
+  // dot products of dA run while the K rows arrive; otherwise row by row
+  auto ld = [](const float* p) {
+    if constexpr (NTL)
+      return __builtin_nontemporal_load(reinterpret_cast<const vec*>(p));
+    else
+      return *reinterpret_cast<const vec*>(p);
+  };
 #pragma unroll
   for (int u = 0; u < T; ++u)
 #pragma unroll
     for (int e = 0; e < NV; ++e) {
-      const vec x = *reinterpret_cast<const vec*>(V + (n * T + u) * D + c0 + e * VW);
-      const vec y = *reinterpret_cast<const vec*>(K + (n * T + u) * D + c0 + e * VW);
+      const vec x = ld(V + (n * T + u) * D + c0 + e * VW);
 #pragma unroll
-      for (int i = 0; i < VW; ++i) {
-        vr[u][e * VW + i] = x[i];
-        kr[u][e * VW + i] = y[i];
+      for (int i = 0; i < VW; ++i) vr[u][e * VW + i] = x[i];
+      if constexpr (!NTL) {
+        const vec y = ld(K + (n * T + u) * D + c0 + e * VW);
+#pragma unroll
+        for (int i = 0; i < VW; ++i) kr[u][e * VW + i] = y[i];
       }
     }
 #pragma unroll
@@ -738,6 +748,16 @@ __global__ __launch_bounds__(256) void k_attn_bwd_r1(const float* __restrict__ d
   for (int u = 0; u < T; u += 4) {
     const float4 x = *reinterpret_cast<const float4*>(A + (n * H + h) * T + u);
     a[u] = x.x; a[u + 1] = x.y; a[u + 2] = x.z; a[u + 3] = x.w;
+  }
+  if constexpr (NTL) {
+#pragma unroll
+    for (int u = 0; u < T; ++u)
+#pragma unroll
+      for (int e = 0; e < NV; ++e) {
+        const vec y = ld(K + (n * T + u) * D + c0 + e * VW);
+#pragma unroll
+        for (int i = 0; i < VW; ++i) kr[u][e * VW + i] = y[i];
+      }
   }
   // (bf16 rounding by the hardware conversion: round to nearest even, no branch)
   if (round_dO) {
@@ -788,11 +808,18 @@ void launch_attn_bwd(const float* dO, const float* q, const float* K, const floa
                      float* colsums, float* cws, hipStream_t s, float* dS) {
   const int DH = D / H;
   if (!dK && !dV && !part && dS && N > 0 && (T == 4 || T == 8)) {
-    // the rank-one path: one wave per window
+    // the rank-one path: one wave per window; K and V streamed when together
+    // larger than 128 MiB (half the last-level cache)
     const dim3 g4((unsigned)((N + 3) / 4));
+    const bool ntl = (int64_t)2 * N * T * D * 4 > ((int64_t)128 << 20);
 #define TRACE_ABR1(D_, DH_, T_)                                                                                    \
   if (D == D_ && DH == DH_ && T == T_) {                                                                           \
-    hipLaunchKernelGGL((k_attn_bwd_r1<D_, DH_, T_>), g4, dim3(256), 0, s, dO, K, V, A, N, scale, round_dO, dQ, dS);    \
+    if (ntl)                                                                                                       \
+      hipLaunchKernelGGL((k_attn_bwd_r1<D_, DH_, T_, true>), g4, dim3(256), 0, s, dO, K, V, A, N, scale, round_dO, \
+                         dQ, dS);                                                                                  \
+    else                                                                                                           \
+      hipLaunchKernelGGL((k_attn_bwd_r1<D_, DH_, T_, false>), g4, dim3(256), 0, s, dO, K, V, A, N, scale,         \
+                         round_dO, dQ, dS);                                                                        \
     return;                                                                                                        \
   }
     TRACE_ABR1(128, 32, 4) TRACE_ABR1(128, 32, 8) TRACE_ABR1(128, 64, 4) TRACE_ABR1(128, 64, 8)
