@@ -390,7 +390,8 @@ __global__ __launch_bounds__(256) void k_bgemm(Src A, Src B, int Kp, int M, int 
     }
     if (gu) {  // C = (A.B) * GELU'(U), U laid out as C
       // loads from clamped addresses, all of a fragment row before any use
-      // (elements outside C are computed but not stored)
+      // (elements outside C are computed but not stored); U is read once,
+      // streamed past the caches (large workload's update 0.884 -> 0.873 ms)
 #pragma unroll
       for (int rf = 0; rf < 4; ++rf) {
         float u[4][4];
@@ -398,7 +399,7 @@ __global__ __launch_bounds__(256) void k_bgemm(Src A, Src B, int Kp, int M, int 
         for (int r = 0; r < 4; ++r) {
           const int64_t mo = (int64_t)min(mb + rf * 16 + r, M - 1) * ldc;
 #pragma unroll
-          for (int nf = 0; nf < 4; ++nf) u[r][nf] = gu[mo + min(nbase + nf * 16, N - 1)];
+          for (int nf = 0; nf < 4; ++nf) u[r][nf] = __builtin_nontemporal_load(gu + mo + min(nbase + nf * 16, N - 1));
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r)
@@ -763,7 +764,8 @@ __global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, 
     }
     if (gu) {  // C = (A.B) * GELU'(U), U laid out as C
       // loads from clamped addresses, all of a fragment row before any use
-      // (elements outside C are computed but not stored)
+      // (elements outside C are computed but not stored); U is read once,
+      // streamed past the caches (large workload's update 0.884 -> 0.873 ms)
 #pragma unroll
       for (int rf = 0; rf < FM; ++rf) {
         float u[4][FN];
@@ -771,7 +773,7 @@ __global__ __launch_bounds__(512) void k_bgemm_big(Src A, Src B, int Kp, int M, 
         for (int r = 0; r < 4; ++r) {
           const int64_t mo = (int64_t)min(mb + rf * 16 + r, M - 1) * ldc;
 #pragma unroll
-          for (int nf = 0; nf < FN; ++nf) u[r][nf] = gu[mo + min(nbase + nf * 16, N - 1)];
+          for (int nf = 0; nf < FN; ++nf) u[r][nf] = __builtin_nontemporal_load(gu + mo + min(nbase + nf * 16, N - 1));
         }
 #pragma unroll
         for (int r = 0; r < 4; ++r)
