@@ -1433,12 +1433,14 @@ static void kv_wgrad_split(int64_t N, int D, int& nps, int& S) {
 
 // workspace: partial sums [S][2][D][D], then (16-byte units) Ck, Cv
 // [tiles][T][2 H / T][2][64], Bq [tiles][D / 16][2][64], Bd [tiles][D / 16][64]
+// (sized with the bound of the number of ranges, min(tiles, 256 / (D / 32)),
+// which grows with N, so that a workspace sized for N windows serves every
+// smaller batch; the number itself does not always grow with N)
 int64_t kv_wgrad_ws_floats(int64_t N, int T, int D, int H) {
   if (N <= 0) return 0;
-  int nps, S;
-  kv_wgrad_split(N, D, nps, S);
   const int64_t tiles = (N + KVW_NT - 1) / KVW_NT;
-  return (int64_t)2 * S * D * D + 4 * tiles * 64 * (2 * (int64_t)2 * H * 2 + (int64_t)D / 16 * 3);
+  const int64_t smax = std::max<int64_t>(1, std::min<int64_t>(tiles, (256 + D / KVW_DC - 1) / (D / KVW_DC)));
+  return (int64_t)2 * smax * D * D + 4 * tiles * 64 * (2 * (int64_t)2 * H * 2 + (int64_t)D / 16 * 3);
 }
 
 // (the first product's column blocks need 32 / T windows per k-step to cover
